@@ -1,0 +1,434 @@
+"""CPU oracle for one 3DGS training view -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg
+of ``bench.py`` may import this package.  It shares no code with the HIP path
+(``paper_2607_19893_amd``): the renderer, its derivative and the projection are
+in ``gs_oracle.c`` (plain C, fp64 except the fp32 geometry that decides
+integers, see that file's header); the L1 loss, Adam and the pending-update
+pack/apply are plain numpy below.
+
+What each stage follows:
+  * a training view renders one camera, computes an image loss and updates
+    only the participating primitives (paper Section 2.1); the renderer is
+    the cited 3D Gaussian Splatting method;
+  * the loss is L1 over all 3*H*W pixel channels;
+  * the update is Adam (Kingma & Ba) with torch.optim.Adam's bias-corrected
+    form, applied to the rows of the visible set only;
+  * pending updates are staged rows of primitive state that a later consumer
+    commits (Section 4.3, Shadow Graph steps 3-5): pack gathers the rows of
+    an ascending index list into one message, apply adds or copies them into
+    a replica and stamps the message version per primitive.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+import subprocess
+import time
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gs_oracle.c")
+_LIB = os.path.join(_HERE, "liborc.so")
+TILE = 16
+
+
+def build(force: bool = True) -> str:
+    """Compile the C part (plain gcc, no FMA contraction, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
+               "-std=gnu11", _SRC, "-o", tmp, "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Cam(ctypes.Structure):
+    _fields_ = [("width", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("fx", ctypes.c_float), ("fy", ctypes.c_float), ("cx", ctypes.c_float), ("cy", ctypes.c_float),
+                ("tan_fovx", ctypes.c_float), ("tan_fovy", ctypes.c_float), ("near_z", ctypes.c_float),
+                ("R", ctypes.c_float * 9), ("t", ctypes.c_float * 3), ("campos", ctypes.c_float * 3)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+        L.orc_project.argtypes = [i32, i32, P, P, P, P, P, ctypes.POINTER(_Cam), i32] + [P] * 13
+        L.orc_project.restype = None
+        L.orc_visible.argtypes = [i32, P, i32, P]
+        L.orc_visible.restype = i64
+        L.orc_sorted_pairs.argtypes = [i64, P, P, P, i32, i32, P, P, P]
+        L.orc_sorted_pairs.restype = i64
+        L.orc_render.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, P, P, P, P, P, P]
+        L.orc_render.restype = None
+        L.orc_render_backward.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, i32, P, P, f64, f64, f64, P, f64]
+        L.orc_render_backward.restype = None
+        L.orc_project_backward.argtypes = [i32, i32, P, P, P, P, P, ctypes.POINTER(_Cam), i64, P, P, P,
+                                           P, P, P, P, P, P]
+        L.orc_project_backward.restype = None
+        L.orc_sh_basis.argtypes = [i32, P, i32, P]
+        L.orc_sh_basis_grad.argtypes = [i32, P, i32, P]
+        L.orc_set_mutation.argtypes = [i32]
+        L.orc_num_threads.restype = i32
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"], "oracle arrays must be C-contiguous"
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _cam(c) -> _Cam:
+    cc = _Cam()
+    cc.width, cc.height = int(c.width), int(c.height)
+    for k in ("fx", "fy", "cx", "cy", "tan_fovx", "tan_fovy", "near_z"):
+        setattr(cc, k, float(getattr(c, k)))
+    R = np.asarray(c.R, np.float32).reshape(9)
+    for i in range(9):
+        cc.R[i] = float(R[i])
+    for i in range(3):
+        cc.t[i] = float(np.float32(c.t[i]))
+        cc.campos[i] = float(np.float32(c.campos[i]))
+    return cc
+
+
+def set_mutation(k: int) -> None:
+    """Switch on deliberate mistake k in the oracle (0 = off); tests only."""
+    lib().orc_set_mutation(int(k))
+    global _MUT
+    _MUT = int(k)
+
+
+_MUT = 0
+
+
+def num_threads() -> int:
+    return int(lib().orc_num_threads())
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+# ---------------------------------------------------------------------------
+# stages
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class Projection:
+    radius: np.ndarray
+    tiles: np.ndarray
+    rect: np.ndarray
+    depth: np.ndarray
+    mean2d: np.ndarray       # fp64 (widened fp32 in mode 0)
+    conic: np.ndarray
+    mean2d_f32: np.ndarray
+    conic_f32: np.ndarray
+    opacity: np.ndarray      # fp64
+    rgb: np.ndarray          # fp64
+    clamp: np.ndarray
+    clamp_margin: np.ndarray
+    jclamp_margin: np.ndarray
+
+
+def project(scene, cam, mode: int = 0) -> Projection:
+    """EWA projection + SH colour of every primitive (mode 0: fp32 geometry, 1: fp64)."""
+    n, deg = scene.n, scene.sh_degree
+    mean, ls, q, lo, sh = (_f32(scene.mean), _f32(scene.log_scale), _f32(scene.quat),
+                           _f32(scene.opacity), _f32(scene.sh))
+    out = Projection(radius=np.zeros(n, np.int32), tiles=np.zeros(n, np.uint32), rect=np.zeros((n, 4), np.int32),
+                     depth=np.zeros(n, np.float32), mean2d=np.zeros((n, 2)), conic=np.zeros((n, 3)),
+                     mean2d_f32=np.zeros((n, 2), np.float32), conic_f32=np.zeros((n, 3), np.float32),
+                     opacity=np.zeros(n), rgb=np.zeros((n, 3)), clamp=np.zeros(n, np.uint8),
+                     clamp_margin=np.full(n, np.inf), jclamp_margin=np.full(n, np.inf))
+    cc = _cam(cam)
+    lib().orc_project(n, deg, _p(mean), _p(ls), _p(q), _p(lo), _p(sh), ctypes.byref(cc), int(mode),
+                      _p(out.radius), _p(out.tiles), _p(out.rect), _p(out.depth), _p(out.mean2d), _p(out.conic),
+                      _p(out.mean2d_f32), _p(out.conic_f32), _p(out.opacity), _p(out.rgb), _p(out.clamp),
+                      _p(out.clamp_margin), _p(out.jclamp_margin))
+    return out
+
+
+def visible(src: np.ndarray) -> np.ndarray:
+    """Ascending ids whose predicate value is non-zero (u8 or u32 input)."""
+    src = np.ascontiguousarray(src)
+    eb = src.dtype.itemsize
+    assert eb in (1, 4)
+    idx = np.zeros(max(1, src.size), np.uint32)
+    c = lib().orc_visible(int(src.size), _p(src), eb, _p(idx))
+    return idx[:c].copy()
+
+
+def sorted_pairs(vis: np.ndarray, proj: Projection, cam):
+    """All (tile<<32 | depth bits, id) pairs sorted; per-tile [start, end)."""
+    vis = np.ascontiguousarray(vis, np.uint32)
+    m = int(proj.tiles[vis].astype(np.int64).sum())
+    keys = np.zeros(max(1, m), np.uint64)
+    vals = np.zeros(max(1, m), np.uint32)
+    T = cam.tiles_x * cam.tiles_y
+    ranges = np.zeros((T, 2), np.uint32)
+    got = lib().orc_sorted_pairs(vis.size, _p(vis), _p(proj.rect), _p(proj.depth), cam.tiles_x, cam.tiles_y,
+                                 _p(keys), _p(vals), _p(ranges))
+    assert got == m
+    return keys[:m].copy(), vals[:m].copy(), ranges
+
+
+@dataclasses.dataclass
+class Render:
+    img: np.ndarray          # [3,H,W] fp64
+    T_final: np.ndarray
+    n_contrib: np.ndarray
+    active: np.ndarray
+    margin_alpha: np.ndarray
+    margin_T: np.ndarray
+    n_hits: np.ndarray
+
+
+def render(vis, proj: Projection, cam, bg=(0.0, 0.0, 0.0)) -> Render:
+    W, H = cam.width, cam.height
+    n = proj.radius.size
+    vis = np.ascontiguousarray(vis, np.uint32)
+    bg = np.ascontiguousarray(bg, np.float64)
+    r = Render(img=np.zeros((3, H, W)), T_final=np.zeros((H, W)), n_contrib=np.zeros((H, W), np.uint32),
+               active=np.zeros(n, np.uint8), margin_alpha=np.zeros((H, W)), margin_T=np.zeros((H, W)),
+               n_hits=np.zeros((H, W), np.uint32))
+    lib().orc_render(vis.size, _p(vis), _p(proj.rect), _p(proj.depth), _p(proj.mean2d), _p(proj.conic),
+                     _p(proj.opacity), _p(proj.rgb), W, H, _p(bg), _p(r.img), _p(r.T_final), _p(r.n_contrib),
+                     _p(r.active), _p(r.margin_alpha), _p(r.margin_T), _p(r.n_hits))
+    return r
+
+
+# Bands inside which a threshold decision of the fp32 kernel may go either way
+# relative to this fp64 oracle (derivation in the design notes): relative
+# distance of o*exp(-sigma) from 1/255, of T*(1-alpha) from 1e-4, of
+# o*exp(-sigma) from the 0.99 cap, and absolute distance |img - target|.
+AMB_ALPHA = 4e-6
+AMB_T = 5e-5
+AMB_CAP = 4e-6
+AMB_LOSS = 4e-6
+
+
+def render_backward(vis, proj: Projection, cam, dL_dimg, bg=(0.0, 0.0, 0.0), loss_margin=None,
+                    amb_alpha=AMB_ALPHA, amb_T=AMB_T, amb_cap=AMB_CAP, amb_loss=AMB_LOSS):
+    """d loss / d(u, v, A, B, C, opacity, rgb) per visible primitive, plus ambiguity flags."""
+    W, H = cam.width, cam.height
+    n = proj.radius.size
+    vis = np.ascontiguousarray(vis, np.uint32)
+    bg = np.ascontiguousarray(bg, np.float64)
+    g = np.ascontiguousarray(dL_dimg, np.float64).reshape(3, H, W)
+    grad2d = np.zeros((n, 9))
+    flag = np.zeros(n, np.uint8)
+    lm = None if loss_margin is None else np.ascontiguousarray(loss_margin, np.float64).reshape(3, H, W)
+    lib().orc_render_backward(vis.size, _p(vis), _p(proj.rect), _p(proj.depth), _p(proj.mean2d), _p(proj.conic),
+                              _p(proj.opacity), _p(proj.rgb), W, H, _p(bg), _p(g), n, _p(grad2d), _p(flag),
+                              float(amb_alpha), float(amb_T), float(amb_cap),
+                              None if lm is None else _p(lm), float(amb_loss))
+    return grad2d, flag
+
+
+@dataclasses.dataclass
+class Grads:
+    mean: np.ndarray
+    log_scale: np.ndarray
+    quat: np.ndarray
+    opacity: np.ndarray
+    sh: np.ndarray
+    grad_norm: np.ndarray
+
+    def groups(self):
+        n = self.mean.shape[0]
+        return [self.mean.reshape(n, 3), self.log_scale.reshape(n, 3), self.quat.reshape(n, 4),
+                self.opacity.reshape(n, 1), self.sh.reshape(n, -1)]
+
+
+def project_backward(scene, cam, vis, grad2d, proj: Projection) -> Grads:
+    n, deg = scene.n, scene.sh_degree
+    K = (deg + 1) ** 2
+    vis = np.ascontiguousarray(vis, np.uint32)
+    g = Grads(mean=np.zeros((n, 3)), log_scale=np.zeros((n, 3)), quat=np.zeros((n, 4)), opacity=np.zeros(n),
+              sh=np.zeros((n, K, 3)), grad_norm=np.zeros(n))
+    cc = _cam(cam)
+    lib().orc_project_backward(n, deg, _p(_f32(scene.mean)), _p(_f32(scene.log_scale)), _p(_f32(scene.quat)),
+                               _p(_f32(scene.opacity)), _p(_f32(scene.sh)), ctypes.byref(cc), vis.size, _p(vis),
+                               _p(np.ascontiguousarray(grad2d, np.float64)), _p(proj.clamp),
+                               _p(g.mean), _p(g.log_scale), _p(g.quat), _p(g.opacity), _p(g.sh), _p(g.grad_norm))
+    return g
+
+
+def loss_l1(img, target):
+    """L = mean |img - target| over all 3*H*W entries; dL/dimg = sign(img - target) / (3HW).
+
+    img and target are the fp32 images both sides see; the sign is taken on
+    their exact difference; the scale 1/(3HW) is the fp32-rounded constant.
+    """
+    img64 = np.asarray(img, np.float64)
+    t64 = np.asarray(target, np.float64)
+    d = img64 - t64
+    inv = np.float32(1.0 / d.size)
+    return float(np.abs(d).mean()), (np.sign(d) * np.float64(inv)), d
+
+
+def adam(p, g, m, v, rows, step, lr, beta1=0.9, beta2=0.999, eps=1e-15):
+    """torch.optim.Adam update of rows `rows` of one parameter group (fp64).
+
+    m <- b1 m + (1-b1) g ; v <- b2 v + (1-b2) g^2
+    delta = -(lr / (1 - b1^t)) * m / (sqrt(v) / sqrt(1 - b2^t) + eps) ; p <- p + delta
+    Rows outside `rows` are returned unchanged.  Returns (p, m, v, delta[rows]).
+    """
+    p = np.array(p, np.float64, copy=True)
+    m = np.array(m, np.float64, copy=True)
+    v = np.array(v, np.float64, copy=True)
+    rows = np.asarray(rows, np.int64)
+    gr = np.asarray(g, np.float64)[rows]
+    m[rows] = beta1 * m[rows] + (1.0 - beta1) * gr
+    v[rows] = beta2 * v[rows] + (1.0 - beta2) * gr * gr
+    bc1 = 1.0 - beta1 ** step
+    bc2 = 1.0 - beta2 ** step
+    if _MUT == 7:
+        bc1 = bc2 = 1.0
+    delta = -(lr / bc1) * m[rows] / (np.sqrt(v[rows]) / np.sqrt(bc2) + eps)
+    p[rows] = p[rows] + delta
+    return p, m, v, delta
+
+
+MSG_MAGIC = 0x47534D31  # "GSM1"
+
+
+def delta_pack(idx, groups, version):
+    """Message = header (magic, count, version, row_len, n_groups, cols...) + idx[K] + rows[K][row_len].
+
+    The header is 8 u32 words (cols of up to 3 groups inline is not enough in
+    general, so the per-group widths follow the header as n_groups u32 words,
+    padded to a multiple of 4 words).  Rows are the concatenation of every
+    group's row, in group order, as fp32 bit patterns.
+    """
+    idx = np.asarray(idx, np.uint32)
+    cols = [int(a.shape[1]) for a in groups]
+    row_len = sum(cols)
+    hdr = np.zeros(8, np.uint32)
+    hdr[0], hdr[1], hdr[2], hdr[3], hdr[4] = MSG_MAGIC, idx.size, version, row_len, len(groups)
+    colw = np.zeros(((len(groups) + 3) // 4) * 4, np.uint32)
+    colw[:len(groups)] = cols
+    rows = np.concatenate([np.asarray(a, np.float32)[idx.astype(np.int64)] for a in groups], axis=1) \
+        if idx.size else np.zeros((0, row_len), np.float32)
+    return np.concatenate([hdr, colw, idx, rows.reshape(-1).view(np.uint32)])
+
+
+def delta_apply(msg, groups, mode, version_arr=None):
+    """ADD (fp32 p += row) or OVERWRITE (copy) every message row into `groups`; stamp versions."""
+    msg = np.asarray(msg, np.uint32)
+    assert msg[0] == MSG_MAGIC
+    K, version, row_len, ng = int(msg[1]), int(msg[2]), int(msg[3]), int(msg[4])
+    ncw = ((ng + 3) // 4) * 4
+    cols = [int(c) for c in msg[8:8 + ng]]
+    off = 8 + ncw
+    idx = msg[off:off + K].astype(np.int64)
+    rows = msg[off + K:off + K + K * row_len].view(np.float32).reshape(K, row_len)
+    out = []
+    c0 = 0
+    for a, c in zip(groups, cols):
+        a = np.array(a, np.float32, copy=True)
+        r = rows[:, c0:c0 + c]
+        if mode == "add":
+            a[idx] = (a[idx].astype(np.float64) + r.astype(np.float64)).astype(np.float32)
+        else:
+            a[idx] = r
+        out.append(a)
+        c0 += c
+    if version_arr is not None:
+        version_arr = np.array(version_arr, np.uint32, copy=True)
+        version_arr[idx] = version
+    return out, version_arr
+
+
+# ---------------------------------------------------------------------------
+# one whole view
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class ViewResult:
+    proj: Projection
+    vis: np.ndarray
+    keys: Optional[np.ndarray]
+    vals: Optional[np.ndarray]
+    ranges: Optional[np.ndarray]
+    render: Render
+    loss: float
+    dL_dimg: np.ndarray
+    loss_margin: np.ndarray
+    grad2d: np.ndarray
+    flag: np.ndarray
+    grads: Grads
+    new_params: list
+    new_m: list
+    new_v: list
+    deltas: list
+    msg: Optional[np.ndarray]
+    times: dict
+
+
+def train_view(scene, cam, target, m_groups, v_groups, step, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-15,
+               with_pairs=True, with_msg=True, version=1, dL_dimg=None):
+    """Projection -> visible set -> pairs -> render -> L1 -> backward -> Adam -> pack (one view).
+
+    The loss sign is taken on the fp32-rounded rendered image (the precision
+    the kernel decides it in); pass dL_dimg to bypass the loss.
+    """
+    tm = {}
+    t0 = time.perf_counter()
+    proj = project(scene, cam, 0)
+    tm["project"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    vis = visible(proj.tiles)
+    tm["visible"] = time.perf_counter() - t0
+    keys = vals = ranges = None
+    if with_pairs:
+        t0 = time.perf_counter()
+        keys, vals, ranges = sorted_pairs(vis, proj, cam)
+        tm["pairs"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    rnd = render(vis, proj, cam)
+    tm["render"] = time.perf_counter() - t0
+    if dL_dimg is None:
+        loss, dL, diff = loss_l1(rnd.img.astype(np.float32), target)
+        lm = diff
+    else:
+        loss, dL, lm = float("nan"), np.asarray(dL_dimg, np.float64), None
+    t0 = time.perf_counter()
+    grad2d, flag = render_backward(vis, proj, cam, dL, loss_margin=lm)
+    tm["render_backward"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    grads = project_backward(scene, cam, vis, grad2d, proj)
+    tm["project_backward"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    params = [a for _, a in scene.groups()]
+    newp, newm, newv, deltas = [], [], [], []
+    for p, g, m, v in zip(params, grads.groups(), m_groups, v_groups):
+        pn, mn, vn, d = adam(p, g, m, v, vis, step, lr, beta1, beta2, eps)
+        newp.append(pn); newm.append(mn); newv.append(vn); deltas.append(d)
+    tm["adam"] = time.perf_counter() - t0
+    msg = None
+    if with_msg:
+        t0 = time.perf_counter()
+        dfull = []
+        for p, d in zip(params, deltas):
+            a = np.zeros(p.shape, np.float32)
+            a[vis.astype(np.int64)] = d.astype(np.float32)
+            dfull.append(a)
+        msg = delta_pack(vis, dfull, version)
+        tm["pack"] = time.perf_counter() - t0
+    return ViewResult(proj, vis, keys, vals, ranges, rnd, loss, dL, lm, grad2d, flag, grads, newp, newm, newv,
+                      deltas, msg, tm)
