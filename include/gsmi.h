@@ -1,0 +1,309 @@
+/*
+ * gsmi.h -- C ABI of the MI355X (gfx950) 3D Gaussian Splatting training-view
+ * hot path: one view of point-based neural rendering training on one GPU's
+ * share of the primitive pool, plus the primitive-indexed publication steps
+ * that a primitive-level synchronization runtime drives.
+ *
+ * The paper frames a training view as: render one camera, compute an image
+ * loss, back-propagate, and update only the primitives that participate; the
+ * pool is a set of aligned per-primitive tensors whose dependency unit is the
+ * primitive index (Introduction; Section 2.1).  The renderer is the cited
+ * 3D Gaussian Splatting method.  Each call below is one phase of that view
+ * (Section 4.1.2 lists the phases: scope extraction, preprocessing,
+ * rendering, backward, communication, optimizer update) or one of the
+ * runtime's publication steps (Section 4.3, Shadow Graph; Section 5 hooks).
+ *
+ * Conventions for every call:
+ *  - All array pointers are DEVICE pointers owned by the caller; the library
+ *    never allocates, frees, or keeps them.  Host-side structs (gs_scene,
+ *    gs_camera, gs_proj, gs_group, gs_adam_group) are read during the call
+ *    only.
+ *  - Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *    NULL = the default stream) and never synchronizes the host.
+ *  - Argument problems are reported synchronously as a gs_status and nothing
+ *    is enqueued.  Data-dependent conditions found on the device (a pair list
+ *    or message larger than its buffer, a message that does not match its
+ *    destination) are reported through a gs_device_status in device memory;
+ *    the outputs of that call are then undefined and the caller retries with
+ *    larger buffers after its next synchronization.
+ *  - Counts produced on the device (visible-set size, pair count) stay on the
+ *    device; later calls read them from there.
+ *  - Row-major layouts: a "[n,c]" array holds row i at elements [i*c, i*c+c).
+ *  - Thread safety: calls on different streams may run concurrently if they
+ *    do not share output buffers.
+ */
+#ifndef GSMI_H
+#define GSMI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GSMI_ABI_VERSION 1
+#define GS_TILE 16            /* pixels per tile side */
+#define GS_MAX_SH_DEGREE 3
+#define GS_MAX_GROUPS 8
+#define GS_MAX_IMAGE_SIDE 32768
+
+typedef enum {
+    GS_OK = 0,
+    GS_ERR_INVALID_ARG = 1,   /* null pointer, negative size, bad enum, ... */
+    GS_ERR_UNSUPPORTED = 2,   /* size beyond a documented limit */
+    GS_ERR_WORKSPACE = 3,     /* workspace smaller than gs_workspace_bytes() */
+    GS_ERR_HIP = 4            /* the HIP runtime refused a launch */
+} gs_status;
+
+/* Device-side error channel (16 bytes of device memory, caller-zeroed). */
+typedef struct {
+    uint32_t flags;           /* OR of GS_DEV_* */
+    uint32_t required;        /* elements (pairs) or bytes (messages) needed */
+    uint32_t reserved[2];
+} gs_device_status;
+
+#define GS_DEV_PAIR_OVERFLOW 1u     /* gs_bin_sort: pairs > capacity */
+#define GS_DEV_MSG_OVERFLOW 2u      /* gs_delta_pack: message > msg_capacity */
+#define GS_DEV_MSG_MISMATCH 4u      /* gs_delta_apply: bad magic / widths / ids */
+
+/*
+ * Primitive pool Theta (Section 2.1): five aligned fp32 tensors, one row per
+ * primitive.  The same struct describes gradients and optimizer moments.
+ *   mean      [n,3] world position
+ *   log_scale [n,3] log standard deviation per axis
+ *   quat      [n,4] rotation quaternion (w,x,y,z), any non-zero length
+ *   opacity   [n]   opacity logit
+ *   sh        [n,(sh_degree+1)^2,3] colour coefficients, coefficient
+ *             k = l*l + l + m (m = -l..l), channel fastest
+ */
+typedef struct {
+    int32_t n;
+    int32_t sh_degree;        /* 0..3 */
+    float* mean;
+    float* log_scale;
+    float* quat;
+    float* opacity;
+    float* sh;
+} gs_scene;
+
+/*
+ * Pinhole camera (host struct, by pointer): world-to-camera rotation R
+ * (row-major; rows = right, down, forward), translation t, centre campos,
+ * focal lengths, principal point, tangents of the half fields of view and
+ * the near plane.  Pixel (i,k) is centred at (i+0.5, k+0.5).
+ */
+typedef struct {
+    int32_t width, height;
+    float fx, fy, cx, cy;
+    float tan_fovx, tan_fovy;
+    float near_z;
+    float R[9];
+    float t[3];
+    float campos[3];
+} gs_camera;
+
+/*
+ * Per-primitive projection results ([n] rows; device).  Culled primitives
+ * have radius = 0 and tiles = 0; their other rows are not written.
+ *   radius        [n]   int32   3-sigma pixel radius
+ *   tiles         [n]   uint32  number of 16x16 tiles the radius touches
+ *   rect          [n,4] uint16  tile rectangle x0,y0,x1,y1 (half-open)
+ *   depth         [n]   fp32    camera-space z
+ *   mean2d        [n,2] fp32    pixel-space mean
+ *   conic_opacity [n,4] fp32    inverse 2D covariance (A,B,C) and opacity
+ *   rgb           [n,3] fp32    view-dependent colour
+ *   clamp         [n]   uint8   bit c set: colour channel c was clamped at 0
+ */
+typedef struct {
+    int32_t* radius;
+    uint32_t* tiles;
+    uint16_t* rect;
+    float* depth;
+    float* mean2d;
+    float* conic_opacity;
+    float* rgb;
+    uint8_t* clamp;
+} gs_proj;
+
+/* ---------------------------------------------------------------------- */
+
+int32_t gs_abi_version(void);
+const char* gs_status_string(int32_t status);
+/* Message of the last synchronous error on this thread ("" if none). */
+const char* gs_last_error(void);
+
+enum {
+    GS_WS_VISIBLE_SET = 1,
+    GS_WS_BIN_SORT = 2,
+    GS_WS_RASTER_BWD = 3,
+    GS_WS_LOSS = 4
+};
+/*
+ * Workspace bytes a call needs, for a pool of n primitives, a pair capacity
+ * (gs_bin_sort, gs_raster_bwd) and an image size.  Workspaces are caller-
+ * owned device memory, 256-byte aligned, with no state kept between calls.
+ */
+size_t gs_workspace_bytes(int32_t which, int32_t n, uint32_t capacity, int32_t width, int32_t height);
+
+/*
+ * Phase "preprocessing" (Section 4.1.2; P in Figure 6): EWA projection of
+ * every primitive of `scene` into `cam`, with spherical-harmonic colour
+ * evaluated along the viewing direction.  The geometry that decides radius,
+ * tile rectangle and depth is computed in fp32 in a fixed operation order
+ * (no fused multiply-add) so that it is reproducible bit for bit:
+ *   p = R mu + t (cull if p_z <= near_z); s = exp(log_scale); Sigma = (Rq S)(Rq S)^T
+ *   J from p with x/z, y/z clamped to +-1.3 tan_fov; Sigma2D = J R Sigma R^T J^T + 0.3 I
+ *   conic = Sigma2D^-1 (cull if det <= 0); r = ceil(3 sqrt(mid + sqrt(max(0.1, mid^2 - det))))
+ *   u = fx p_x/p_z + cx, v = fy p_y/p_z + cy; rectangle from (u +- r)/16 (cull if empty)
+ * opacity = sigmoid(logit); rgb = max(0, SH(d) + 0.5), d = (mu - campos)/|mu - campos|.
+ * Errors: GS_ERR_INVALID_ARG on null pointers, n < 0, degree outside 0..3;
+ * GS_ERR_UNSUPPORTED if width/height exceed GS_MAX_IMAGE_SIDE.
+ */
+gs_status gs_project(const gs_scene* scene, const gs_camera* cam, const gs_proj* out, void* stream);
+
+/*
+ * Scope extraction (Section 4.1.2) and the pre-observation / post-backward
+ * scope hooks (Section 5): ordered stream compaction of a per-primitive
+ * predicate into ascending primitive ids.  With `tiles` from gs_project the
+ * result is the projection-visible set (a superset of the realized active
+ * set C_i of Section 2.1); with the active flags of gs_raster_fwd it is C_i
+ * itself; any caller mask works the same way.
+ *   kind: GS_PRED_U32_NONZERO (src is uint32[n]) or GS_PRED_U8_NONZERO (uint8[n])
+ *   out_idx [n] uint32 (the first *out_count entries are written)
+ *   out_count: one uint32 on the device
+ *   ws: gs_workspace_bytes(GS_WS_VISIBLE_SET, n, 0, 0, 0) bytes
+ */
+enum { GS_PRED_U32_NONZERO = 0, GS_PRED_U8_NONZERO = 1 };
+gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Phase "rendering", part 1 (Section 4.1.2): duplicate every visible
+ * primitive once per touched tile and order the (tile, primitive) pairs by
+ * (tile, depth, primitive id).  Equal depths keep ascending ids.
+ *   vis_idx/vis_count: ascending visible ids (gs_visible_set on `tiles`)
+ *   capacity: length of vals (and keys); more pairs set GS_DEV_PAIR_OVERFLOW
+ *   vals   [capacity] uint32  primitive id of every sorted pair
+ *   ranges [T,2] uint32       [start, end) of each tile's pairs, T = tiles in the image
+ *   pair_offset [n] uint32    per visible primitive: first of its pairs in
+ *                             emission order (rectangle row-major); read by gs_raster_bwd
+ *   keys   [capacity] uint64 or NULL: (tile << 32) | bits(depth) per sorted pair
+ *   num_pairs: one uint32 on the device (the pair count, also on overflow)
+ *   ws: gs_workspace_bytes(GS_WS_BIN_SORT, n, capacity, width, height) bytes
+ */
+gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
+                      int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
+                      uint32_t* pair_offset, uint64_t* keys, uint32_t* num_pairs, gs_device_status* status,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Phase "rendering", part 2 (R in Figure 6): front-to-back alpha blending of
+ * each pixel over its tile's sorted pairs.  Per pair: sigma = A dx^2/2 +
+ * B dx dy + C dy^2/2 (dx = u - px, pixel centres at +0.5), skipped if
+ * sigma < 0; alpha = min(0.99, o e^-sigma), skipped if alpha < 1/255; the pixel
+ * stops before a pair that would take T(1-alpha) below 1e-4.
+ *   img [3,H,W] fp32 planar = sum alpha T rgb + T_final bg
+ *   final_T [H,W] fp32; n_contrib [H,W] uint32 = 1 + position (within the tile's
+ *   range) of the last included pair, 0 if none
+ *   active [n] uint8 or NULL: set to 1 for every primitive included in at least
+ *   one pixel (never cleared: zero it before the call)
+ *   bg: 3 floats on the HOST
+ */
+gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,
+                        int32_t width, int32_t height, const float* bg, float* img, float* final_T,
+                        uint32_t* n_contrib, uint8_t* active, void* stream);
+
+/*
+ * Image loss (Section 2.1): L = mean over all 3*H*W entries of |img - target|;
+ * dL_dimg = sign(img - target) / (3HW) with sign(0) = 0.
+ *   loss: one float on the device; ws: gs_workspace_bytes(GS_WS_LOSS, 0, 0, W, H)
+ */
+gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32_t height, float* loss,
+                     float* dL_dimg, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Phase "backward" (B in Figure 6; Shadow Graph step 2 of Section 4.3): the
+ * analytic derivative of the rendered view, first w.r.t. each pair's 2D
+ * quantities (replayed back to front per pixel from final_T and n_contrib),
+ * summed per primitive in a fixed order (no floating-point atomics), then
+ * chained through projection and colour to the parameters.  grad_norm is the
+ * per-primitive gradient evidence g(p) of Section 2.1 that the post-backward
+ * hook of Section 5 reports: |dL/d(u,v)| of this view.
+ *   grads: same layout as the scene; only rows in vis_idx are written
+ *   grad2d [n,9] fp32 or NULL: (du, dv, dA, dB, dC, dopacity, dr, dg, db) per visible row
+ *   grad_norm [n] fp32 or NULL (visible rows)
+ *   ws: gs_workspace_bytes(GS_WS_RASTER_BWD, n, capacity, W, H); capacity as in gs_bin_sort
+ */
+gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
+                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* vis_idx,
+                        const uint32_t* vis_count, uint32_t capacity, const float* final_T,
+                        const uint32_t* n_contrib, const float* dL_dimg, const float* bg, const gs_scene* grads,
+                        float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Optimizer update (U in Figure 6; Shadow Graph step 5): Adam on the rows in
+ * idx only ("updating only visible primitives", Introduction), torch.optim.Adam
+ * form with one global step t >= 1:
+ *   m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2
+ *   delta = -(lr/(1-b1^t)) m / (sqrt(v)/sqrt(1-b2^t) + eps);  p += delta
+ * Rows not in idx are not touched.  delta (if not NULL) receives the step of
+ * every updated row ([n,cols] layout) -- the pending update that
+ * gs_delta_pack publishes.
+ */
+typedef struct {
+    float* p;
+    const float* g;
+    float* m;
+    float* v;
+    float* delta;             /* may be NULL */
+    int32_t cols;
+    float lr;
+} gs_adam_group;
+
+gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
+                         const uint32_t* count, int32_t max_rows, int32_t step, float beta1, float beta2,
+                         float eps, void* stream);
+
+/*
+ * Staged publication (Shadow Graph steps 3-4 of Section 4.3; publication
+ * callback of Section 5): pack gathers the rows of an ascending primitive id
+ * list (e.g. the updated set, or the part of it a later task may observe)
+ * from n_groups row-major tensors into one contiguous message; apply commits
+ * a message into a replica and stamps the per-primitive publication version
+ * (the publication metadata of Section 4.3's throughput-first path).
+ *
+ * Message layout (uint32 words, little endian):
+ *   [0] magic 0x47534D31  [1] count K  [2] version  [3] row_len (sum of cols)
+ *   [4] n_groups  [5..7] 0
+ *   [8 .. 8+G) cols of each group, G = n_groups rounded up to a multiple of 4
+ *   then K ids, then zero padding to a 16-byte boundary, then K rows of
+ *   row_len fp32 values (each row = the groups' rows concatenated).
+ *   gs_delta_msg_bytes(K, row_len, n_groups) gives the size.
+ */
+typedef struct {
+    float* ptr;               /* [rows, cols] */
+    int32_t cols;
+} gs_group;
+
+#define GS_MSG_MAGIC 0x47534D31u
+size_t gs_delta_msg_bytes(uint32_t count, int32_t row_len, int32_t n_groups);
+
+gs_status gs_delta_pack(const uint32_t* idx, const uint32_t* count, int32_t max_rows, const gs_group* src,
+                        int32_t n_groups, uint32_t version, void* msg, size_t msg_capacity,
+                        gs_device_status* status, void* stream);
+
+/* mode: GS_APPLY_ADD (one fp32 add per element) or GS_APPLY_OVERWRITE (copy).
+ * msg_capacity: bytes readable at msg.  prim_version [n_rows] uint32 or NULL.
+ * A bad magic, group widths that differ from dst, a count above max_rows, a
+ * message longer than msg_capacity or an id >= n_rows set GS_DEV_MSG_MISMATCH
+ * and nothing is written.  max_rows also sizes the launch. */
+enum { GS_APPLY_ADD = 0, GS_APPLY_OVERWRITE = 1 };
+gs_status gs_delta_apply(const void* msg, size_t msg_capacity, const gs_group* dst, int32_t n_groups, int32_t n_rows,
+                         int32_t max_rows, int32_t mode, uint32_t* prim_version, gs_device_status* status,
+                         void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GSMI_H */

@@ -308,12 +308,10 @@ MSG_MAGIC = 0x47534D31  # "GSM1"
 
 
 def delta_pack(idx, groups, version):
-    """Message = header (magic, count, version, row_len, n_groups, cols...) + idx[K] + rows[K][row_len].
-
-    The header is 8 u32 words (cols of up to 3 groups inline is not enough in
-    general, so the per-group widths follow the header as n_groups u32 words,
-    padded to a multiple of 4 words).  Rows are the concatenation of every
-    group's row, in group order, as fp32 bit patterns.
+    """Message = 8 header words (magic, count, version, row_len, n_groups, 0, 0, 0),
+    the group widths (padded with zeros to a multiple of 4 words), the K ids,
+    zero padding to a 16-byte boundary, then K rows of row_len fp32 values
+    (each row = the groups' rows concatenated in group order).
     """
     idx = np.asarray(idx, np.uint32)
     cols = [int(a.shape[1]) for a in groups]
@@ -324,7 +322,9 @@ def delta_pack(idx, groups, version):
     colw[:len(groups)] = cols
     rows = np.concatenate([np.asarray(a, np.float32)[idx.astype(np.int64)] for a in groups], axis=1) \
         if idx.size else np.zeros((0, row_len), np.float32)
-    return np.concatenate([hdr, colw, idx, rows.reshape(-1).view(np.uint32)])
+    head = 8 + colw.size + idx.size
+    pad = np.zeros((-head) % 4, np.uint32)
+    return np.concatenate([hdr, colw, idx, pad, rows.reshape(-1).view(np.uint32)])
 
 
 def delta_apply(msg, groups, mode, version_arr=None):
@@ -336,7 +336,8 @@ def delta_apply(msg, groups, mode, version_arr=None):
     cols = [int(c) for c in msg[8:8 + ng]]
     off = 8 + ncw
     idx = msg[off:off + K].astype(np.int64)
-    rows = msg[off + K:off + K + K * row_len].view(np.float32).reshape(K, row_len)
+    r0 = (off + K + 3) // 4 * 4
+    rows = msg[r0:r0 + K * row_len].view(np.float32).reshape(K, row_len)
     out = []
     c0 = 0
     for a, c in zip(groups, cols):

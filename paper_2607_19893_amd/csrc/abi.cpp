@@ -1,0 +1,251 @@
+// C-ABI entry points: synchronous argument validation, then the launches.
+// No entry point allocates, frees or synchronizes.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "internal.h"
+
+namespace {
+
+thread_local char g_err[256] = "";
+
+gs_status fail(gs_status s, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+gs_status ok() {
+    g_err[0] = 0;
+    return GS_OK;
+}
+
+gs_status hip_status(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(GS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+#define GS_REQUIRE(cond, ...)                                   \
+    do {                                                        \
+        if (!(cond)) return fail(GS_ERR_INVALID_ARG, __VA_ARGS__); \
+    } while (0)
+
+gs_status check_scene(const gs_scene* s, const char* what) {
+    GS_REQUIRE(s != nullptr, "%s: null scene", what);
+    GS_REQUIRE(s->n >= 0, "%s: n < 0", what);
+    GS_REQUIRE(s->sh_degree >= 0 && s->sh_degree <= GS_MAX_SH_DEGREE, "%s: sh_degree %d outside 0..3", what,
+               s->sh_degree);
+    if (s->n > 0) {
+        GS_REQUIRE(s->mean && s->log_scale && s->quat && s->opacity && s->sh, "%s: null parameter pointer", what);
+        GS_REQUIRE(aligned(s->quat, 16), "%s: quat must be 16-byte aligned", what);
+    }
+    return GS_OK;
+}
+
+gs_status check_camera(const gs_camera* c, const char* what) {
+    if (c == nullptr) return fail(GS_ERR_INVALID_ARG, "%s: null camera", what);
+    if (c->width < 0 || c->height < 0) return fail(GS_ERR_INVALID_ARG, "%s: negative image size", what);
+    if (c->width > GS_MAX_IMAGE_SIDE || c->height > GS_MAX_IMAGE_SIDE)
+        return fail(GS_ERR_UNSUPPORTED, "%s: image side above %d", what, GS_MAX_IMAGE_SIDE);
+    return GS_OK;
+}
+
+gs_status check_proj(const gs_proj* p, bool need_all, const char* what) {
+    GS_REQUIRE(p != nullptr, "%s: null proj", what);
+    GS_REQUIRE(p->tiles && p->rect && p->depth && p->mean2d && p->conic_opacity && p->rgb, "%s: null proj array",
+               what);
+    if (need_all) GS_REQUIRE(p->radius && p->clamp, "%s: null proj array", what);
+    GS_REQUIRE(aligned(p->rect, 8) && aligned(p->mean2d, 8) && aligned(p->conic_opacity, 16),
+               "%s: proj arrays misaligned (rect 8, mean2d 8, conic_opacity 16 bytes)", what);
+    return GS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t gs_abi_version(void) { return GSMI_ABI_VERSION; }
+
+const char* gs_status_string(int32_t s) {
+    switch (s) {
+        case GS_OK: return "ok";
+        case GS_ERR_INVALID_ARG: return "invalid argument";
+        case GS_ERR_UNSUPPORTED: return "unsupported size";
+        case GS_ERR_WORKSPACE: return "workspace too small";
+        case GS_ERR_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+const char* gs_last_error(void) { return g_err; }
+
+size_t gs_workspace_bytes(int32_t which, int32_t n, uint32_t capacity, int32_t width, int32_t height) {
+    if (n < 0 || width < 0 || height < 0) return 0;
+    switch (which) {
+        case GS_WS_VISIBLE_SET: return gsmi::visible_ws_bytes(n);
+        case GS_WS_BIN_SORT: return gsmi::binsort_ws_bytes(n, capacity, width, height);
+        case GS_WS_RASTER_BWD: return gsmi::raster_bwd_ws_bytes(n, capacity);
+        case GS_WS_LOSS: return gsmi::loss_ws_bytes(width, height);
+        default: return 0;
+    }
+}
+
+size_t gs_delta_msg_bytes(uint32_t count, int32_t row_len, int32_t n_groups) {
+    if (row_len < 0 || n_groups < 0) return 0;
+    return gsmi::delta_msg_bytes(count, row_len, n_groups);
+}
+
+gs_status gs_project(const gs_scene* scene, const gs_camera* cam, const gs_proj* out, void* stream) {
+    gs_status s;
+    if ((s = check_scene(scene, "gs_project")) != GS_OK) return s;
+    if ((s = check_camera(cam, "gs_project")) != GS_OK) return s;
+    if ((s = check_proj(out, true, "gs_project")) != GS_OK) return s;
+    const gsmi::CamArgs c = gsmi::make_cam_args(cam);
+    return hip_status(gsmi::launch_project(*scene, c, *out, static_cast<hipStream_t>(stream)), "gs_project");
+}
+
+gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count, void* ws,
+                         size_t ws_bytes, void* stream) {
+    GS_REQUIRE(kind == GS_PRED_U32_NONZERO || kind == GS_PRED_U8_NONZERO, "gs_visible_set: bad kind %d", kind);
+    GS_REQUIRE(n >= 0, "gs_visible_set: n < 0");
+    GS_REQUIRE(out_count != nullptr, "gs_visible_set: null out_count");
+    if (n > 0) {
+        GS_REQUIRE(src && out_idx && ws, "gs_visible_set: null pointer");
+        GS_REQUIRE(aligned(src, kind == GS_PRED_U32_NONZERO ? 16 : 8), "gs_visible_set: src misaligned");
+    }
+    if (ws_bytes < gsmi::visible_ws_bytes(n)) return fail(GS_ERR_WORKSPACE, "gs_visible_set: workspace too small");
+    return hip_status(gsmi::launch_visible(kind, src, n, out_idx, out_count, ws, static_cast<hipStream_t>(stream)),
+                      "gs_visible_set");
+}
+
+gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
+                      int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
+                      uint32_t* pair_offset, uint64_t* keys, uint32_t* num_pairs, gs_device_status* status,
+                      void* ws, size_t ws_bytes, void* stream) {
+    gs_status s;
+    if ((s = check_proj(proj, false, "gs_bin_sort")) != GS_OK) return s;
+    GS_REQUIRE(n >= 0 && width >= 0 && height >= 0, "gs_bin_sort: negative size");
+    if (width > GS_MAX_IMAGE_SIDE || height > GS_MAX_IMAGE_SIDE)
+        return fail(GS_ERR_UNSUPPORTED, "gs_bin_sort: image side above %d", GS_MAX_IMAGE_SIDE);
+    GS_REQUIRE(vis_idx && vis_count && ranges && pair_offset && num_pairs && status && ws,
+               "gs_bin_sort: null pointer");
+    GS_REQUIRE(capacity == 0 || vals, "gs_bin_sort: null vals");
+    if (ws_bytes < gsmi::binsort_ws_bytes(n, capacity, width, height))
+        return fail(GS_ERR_WORKSPACE, "gs_bin_sort: workspace too small");
+    return hip_status(gsmi::launch_binsort(*proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges,
+                                           pair_offset, keys, num_pairs, status, ws, static_cast<hipStream_t>(stream)),
+                      "gs_bin_sort");
+}
+
+gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges, int32_t width,
+                        int32_t height, const float* bg, float* img, float* final_T, uint32_t* n_contrib,
+                        uint8_t* active, void* stream) {
+    gs_status s;
+    if ((s = check_proj(proj, false, "gs_raster_fwd")) != GS_OK) return s;
+    GS_REQUIRE(n >= 0 && width >= 0 && height >= 0, "gs_raster_fwd: negative size");
+    if (width > GS_MAX_IMAGE_SIDE || height > GS_MAX_IMAGE_SIDE)
+        return fail(GS_ERR_UNSUPPORTED, "gs_raster_fwd: image side above %d", GS_MAX_IMAGE_SIDE);
+    GS_REQUIRE(vals && ranges && bg && img && final_T && n_contrib, "gs_raster_fwd: null pointer");
+    return hip_status(gsmi::launch_raster_fwd(*proj, vals, ranges, width, height, bg, img, final_T, n_contrib, active,
+                                              static_cast<hipStream_t>(stream)),
+                      "gs_raster_fwd");
+}
+
+gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32_t height, float* loss,
+                     float* dL_dimg, void* ws, size_t ws_bytes, void* stream) {
+    GS_REQUIRE(width >= 0 && height >= 0, "gs_loss_l1: negative size");
+    GS_REQUIRE(img && target && loss && dL_dimg && ws, "gs_loss_l1: null pointer");
+    if (ws_bytes < gsmi::loss_ws_bytes(width, height)) return fail(GS_ERR_WORKSPACE, "gs_loss_l1: workspace too small");
+    return hip_status(gsmi::launch_loss_l1(img, target, width, height, loss, dL_dimg, ws,
+                                           static_cast<hipStream_t>(stream)),
+                      "gs_loss_l1");
+}
+
+gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
+                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* vis_idx,
+                        const uint32_t* vis_count, uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
+                        const float* dL_dimg, const float* bg, const gs_scene* grads, float* grad2d, float* grad_norm,
+                        void* ws, size_t ws_bytes, void* stream) {
+    gs_status s;
+    if ((s = check_scene(scene, "gs_raster_bwd")) != GS_OK) return s;
+    if ((s = check_scene(grads, "gs_raster_bwd(grads)")) != GS_OK) return s;
+    GS_REQUIRE(grads->n == scene->n && grads->sh_degree == scene->sh_degree, "gs_raster_bwd: grads shape differs");
+    if ((s = check_camera(cam, "gs_raster_bwd")) != GS_OK) return s;
+    if ((s = check_proj(proj, true, "gs_raster_bwd")) != GS_OK) return s;
+    GS_REQUIRE(vals && ranges && pair_offset && vis_idx && vis_count && final_T && n_contrib && dL_dimg && bg && ws,
+               "gs_raster_bwd: null pointer");
+    if (ws_bytes < gsmi::raster_bwd_ws_bytes(scene->n, capacity))
+        return fail(GS_ERR_WORKSPACE, "gs_raster_bwd: workspace too small");
+    const gsmi::CamArgs c = gsmi::make_cam_args(cam);
+    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, vals, ranges, pair_offset, vis_idx, vis_count, capacity,
+                                              final_T, n_contrib, dL_dimg, bg, *grads, grad2d, grad_norm, ws,
+                                              static_cast<hipStream_t>(stream)),
+                      "gs_raster_bwd");
+}
+
+gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx, const uint32_t* count,
+                         int32_t max_rows, int32_t step, float beta1, float beta2, float eps, void* stream) {
+    GS_REQUIRE(groups && n_groups > 0 && n_groups <= GS_MAX_GROUPS, "gs_sparse_adam: 1..%d groups", GS_MAX_GROUPS);
+    GS_REQUIRE(idx && count, "gs_sparse_adam: null index list");
+    GS_REQUIRE(max_rows >= 0, "gs_sparse_adam: max_rows < 0");
+    GS_REQUIRE(step >= 1, "gs_sparse_adam: step must be >= 1");
+    GS_REQUIRE(beta1 >= 0.0f && beta1 < 1.0f && beta2 >= 0.0f && beta2 < 1.0f, "gs_sparse_adam: betas outside [0,1)");
+    int32_t row_len = 0;
+    for (int i = 0; i < n_groups; ++i) {
+        GS_REQUIRE(groups[i].p && groups[i].g && groups[i].m && groups[i].v, "gs_sparse_adam: group %d null", i);
+        GS_REQUIRE(groups[i].cols > 0, "gs_sparse_adam: group %d cols <= 0", i);
+        row_len += groups[i].cols;
+    }
+    if (row_len > 64) return fail(GS_ERR_UNSUPPORTED, "gs_sparse_adam: row length %d above 64", row_len);
+    return hip_status(gsmi::launch_sparse_adam(groups, n_groups, idx, count, max_rows, step, beta1, beta2, eps,
+                                               static_cast<hipStream_t>(stream)),
+                      "gs_sparse_adam");
+}
+
+static gs_status check_groups(const gs_group* g, int32_t n, const char* what) {
+    GS_REQUIRE(g && n > 0 && n <= GS_MAX_GROUPS, "%s: 1..%d groups", what, GS_MAX_GROUPS);
+    int32_t rl = 0;
+    for (int i = 0; i < n; ++i) {
+        GS_REQUIRE(g[i].ptr && g[i].cols > 0, "%s: group %d invalid", what, i);
+        rl += g[i].cols;
+    }
+    if (rl > 64) return fail(GS_ERR_UNSUPPORTED, "%s: row length %d above 64", what, rl);
+    return GS_OK;
+}
+
+gs_status gs_delta_pack(const uint32_t* idx, const uint32_t* count, int32_t max_rows, const gs_group* src,
+                        int32_t n_groups, uint32_t version, void* msg, size_t msg_capacity, gs_device_status* status,
+                        void* stream) {
+    gs_status s;
+    if ((s = check_groups(src, n_groups, "gs_delta_pack")) != GS_OK) return s;
+    GS_REQUIRE(idx && count && msg && status, "gs_delta_pack: null pointer");
+    GS_REQUIRE(max_rows >= 0, "gs_delta_pack: max_rows < 0");
+    GS_REQUIRE(aligned(msg, 16), "gs_delta_pack: msg must be 16-byte aligned");
+    return hip_status(gsmi::launch_delta_pack(idx, count, max_rows, src, n_groups, version, msg, msg_capacity, status,
+                                              static_cast<hipStream_t>(stream)),
+                      "gs_delta_pack");
+}
+
+gs_status gs_delta_apply(const void* msg, size_t msg_capacity, const gs_group* dst, int32_t n_groups, int32_t n_rows,
+                         int32_t max_rows, int32_t mode, uint32_t* prim_version, gs_device_status* status,
+                         void* stream) {
+    gs_status s;
+    if ((s = check_groups(dst, n_groups, "gs_delta_apply")) != GS_OK) return s;
+    GS_REQUIRE(msg && status, "gs_delta_apply: null pointer");
+    GS_REQUIRE(msg_capacity >= gsmi::delta_msg_bytes(0, 0, n_groups), "gs_delta_apply: message buffer below header size");
+    GS_REQUIRE(mode == GS_APPLY_ADD || mode == GS_APPLY_OVERWRITE, "gs_delta_apply: bad mode %d", mode);
+    GS_REQUIRE(n_rows >= 0 && max_rows >= 0, "gs_delta_apply: negative size");
+    GS_REQUIRE(aligned(msg, 16), "gs_delta_apply: msg must be 16-byte aligned");
+    return hip_status(gsmi::launch_delta_apply(msg, msg_capacity, dst, n_groups, n_rows, max_rows, mode, prim_version, status,
+                                               static_cast<hipStream_t>(stream)),
+                      "gs_delta_apply");
+}
+
+}  // extern "C"

@@ -1,0 +1,331 @@
+// Rendering phase, part 1: duplicate visible primitives per touched tile and
+// order the pairs by (tile, depth, primitive id).
+//
+// Instead of one wide radix sort over 64-bit (tile, depth) keys, the order is
+// built in two narrow steps:
+//   1. sort the V visible primitives by the bits of their fp32 depth (31
+//      significant bits, 4 LSD passes over V keys, stable, so equal depths
+//      keep ascending ids because the visible list is ascending);
+//   2. emit every primitive's tile pairs in that depth order and stable-sort
+//      the M pairs by tile id only (ceil(log2 T) bits: 1-2 passes).
+// Stability of step 2 keeps the depth order inside each tile, so the result
+// is exactly the (tile, depth bits, id) order, with M-sized passes cut from
+// 4-6 to 1-2.
+//
+// Each LSD pass is three launches: per-block digit histograms (digit-major
+// matrix), a per-digit scan across blocks, and a scatter whose in-block rank
+// comes from a 64-lane match built from ballots (stable: round, wave, lane).
+#include "common.h"
+#include "internal.h"
+
+namespace gsmi {
+
+namespace {
+
+constexpr int kRadixBits = 8;
+constexpr int kRadix = 1 << kRadixBits;
+
+__global__ void __launch_bounds__(GS_BLOCK) k_radix_hist(const uint32_t* __restrict__ keys,
+                                                         const uint32_t* __restrict__ count_ptr, int shift,
+                                                         uint32_t mask, uint32_t* __restrict__ hist,
+                                                         uint32_t nblocks) {
+    __shared__ uint32_t h[kRadix];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const uint32_t cnt = *count_ptr;
+    const uint32_t base = blockIdx.x * GS_TILE_ITEMS;
+    if (base < cnt) {
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) {
+            const uint32_t i = base + k * GS_BLOCK + threadIdx.x;
+            if (i < cnt) atomicAdd(&h[(keys[i] >> shift) & mask], 1u);
+        }
+    }
+    __syncthreads();
+    hist[threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
+}
+
+// One workgroup per digit row: exclusive scan across blocks, row total -> totals[d].
+__global__ void __launch_bounds__(GS_BLOCK) k_radix_scan(uint32_t* __restrict__ hist, uint32_t nblocks,
+                                                         uint32_t* __restrict__ totals) {
+    __shared__ uint32_t scratch[4];
+    uint32_t* row = hist + (size_t)blockIdx.x * nblocks;
+    uint32_t carry = 0;
+    for (uint32_t chunk = 0; chunk < nblocks; chunk += GS_TILE_ITEMS) {
+        const uint32_t base = chunk + threadIdx.x * GS_ITEMS;
+        uint32_t v[GS_ITEMS];
+        uint32_t s = 0;
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) {
+            v[k] = (base + k < nblocks) ? row[base + k] : 0u;
+            s += v[k];
+        }
+        uint32_t tot;
+        uint32_t run = block_excl_scan(s, scratch, &tot) + carry;
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) {
+            if (base + k < nblocks) row[base + k] = run;
+            run += v[k];
+        }
+        carry += tot;
+    }
+    if (threadIdx.x == 0) totals[blockIdx.x] = carry;
+}
+
+__global__ void __launch_bounds__(GS_BLOCK) k_radix_scatter(
+    const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, uint32_t* __restrict__ keys_out,
+    uint32_t* __restrict__ vals_out, const uint32_t* __restrict__ count_ptr, int shift, uint32_t mask,
+    int nbits, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals, uint32_t nblocks) {
+    __shared__ uint32_t s_base[kRadix];
+    __shared__ uint32_t s_run[kRadix];
+    __shared__ uint32_t s_wc[4][kRadix];
+    __shared__ uint32_t scratch[4];
+    const uint32_t cnt = *count_ptr;
+    const uint32_t base = blockIdx.x * GS_TILE_ITEMS;
+    if (base >= cnt) return;
+    const int tid = threadIdx.x;
+    const int w = tid / GS_WAVE;
+    uint32_t tot;
+    const uint32_t dex = block_excl_scan(totals[tid], scratch, &tot);
+    s_base[tid] = dex + hist[tid * nblocks + blockIdx.x];
+    s_run[tid] = 0;
+    s_wc[0][tid] = 0; s_wc[1][tid] = 0; s_wc[2][tid] = 0; s_wc[3][tid] = 0;
+    uint32_t key[GS_ITEMS], val[GS_ITEMS];
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        const uint32_t i = base + k * GS_BLOCK + tid;
+        key[k] = (i < cnt) ? keys_in[i] : 0u;
+        val[k] = (i < cnt) ? vals_in[i] : 0u;
+    }
+    __syncthreads();
+    const uint64_t lt = lanemask_lt();
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        const uint32_t i = base + k * GS_BLOCK + tid;
+        const bool valid = i < cnt;
+        const uint32_t d = (key[k] >> shift) & mask;
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < nbits; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t bb = __ballot(bit);
+            peers &= bit ? bb : ~bb;
+        }
+        const uint32_t rank = (uint32_t)popc64(peers & lt);
+        if (valid && rank == 0) s_wc[w][d] = (uint32_t)popc64(peers);
+        __syncthreads();
+        uint32_t pos = 0;
+        if (valid) {
+            pos = s_base[d] + s_run[d] + rank;
+            if (w > 0) pos += s_wc[0][d];
+            if (w > 1) pos += s_wc[1][d];
+            if (w > 2) pos += s_wc[2][d];
+        }
+        __syncthreads();
+        s_run[tid] += s_wc[0][tid] + s_wc[1][tid] + s_wc[2][tid] + s_wc[3][tid];
+        s_wc[0][tid] = 0; s_wc[1][tid] = 0; s_wc[2][tid] = 0; s_wc[3][tid] = 0;
+        __syncthreads();
+        if (valid) {
+            keys_out[pos] = key[k];
+            vals_out[pos] = val[k];
+        }
+    }
+}
+
+// depth keys of the visible primitives (key = fp32 bits, value = id)
+__global__ void __launch_bounds__(GS_BLOCK) k_depth_keys(const uint32_t* __restrict__ vis_idx,
+                                                         const uint32_t* __restrict__ vis_count,
+                                                         const float* __restrict__ depth,
+                                                         uint32_t* __restrict__ keys, uint32_t* __restrict__ vals) {
+    const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
+    if (r >= *vis_count) return;
+    const uint32_t g = vis_idx[r];
+    keys[r] = __float_as_uint(depth[g]);
+    vals[r] = g;
+}
+
+// per-block sums of tiles[] in depth order
+__global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restrict__ order,
+                                                        const uint32_t* __restrict__ vis_count,
+                                                        const uint32_t* __restrict__ tiles,
+                                                        uint32_t* __restrict__ bsum) {
+    __shared__ uint32_t scratch[4];
+    const uint32_t V = *vis_count;
+    const uint32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x * GS_ITEMS;
+    uint32_t s = 0;
+    if (blockIdx.x * GS_TILE_ITEMS < V) {
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k)
+            if (base + k < V) s += tiles[order[base + k]];
+    }
+    const uint32_t t = block_sum_u32(s, scratch);
+    if (threadIdx.x == 0) bsum[blockIdx.x] = t;
+}
+
+// Exclusive offsets in depth order, pair_offset[id], and the pair emission
+// (tile id, primitive id) in rectangle row-major order.
+__global__ void __launch_bounds__(GS_BLOCK) k_emit(
+    const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
+    const ushort4* __restrict__ rect, const uint32_t* __restrict__ bsum, const uint32_t* __restrict__ total,
+    uint32_t capacity, int32_t tiles_x, uint32_t* __restrict__ pair_offset, uint32_t* __restrict__ pkeys,
+    uint32_t* __restrict__ pvals, uint32_t* __restrict__ sort_count, uint32_t* __restrict__ num_pairs,
+    gs_device_status* __restrict__ status) {
+    __shared__ uint32_t scratch[4];
+    const uint32_t V = *vis_count;
+    const uint32_t M = *total;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        *num_pairs = M;
+        *sort_count = M <= capacity ? M : 0u;
+        if (M > capacity && status) {
+            atomicOr(&status->flags, GS_DEV_PAIR_OVERFLOW);
+            atomicMax(&status->required, M);
+        }
+    }
+    if (blockIdx.x * GS_TILE_ITEMS >= V) return;
+    const uint32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x * GS_ITEMS;
+    uint32_t t[GS_ITEMS], g[GS_ITEMS];
+    uint32_t s = 0;
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        g[k] = (base + k < V) ? order[base + k] : 0u;
+        t[k] = (base + k < V) ? tiles[g[k]] : 0u;
+        s += t[k];
+    }
+    uint32_t tot;
+    uint32_t off = block_excl_scan(s, scratch, &tot) + bsum[blockIdx.x];
+    const bool fits = M <= capacity;
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        if (base + k >= V) break;
+        pair_offset[g[k]] = off;
+        if (fits) {
+            const ushort4 rc = rect[g[k]];
+            uint32_t o = off;
+            for (int ty = rc.y; ty < rc.w; ++ty)
+                for (int tx = rc.x; tx < rc.z; ++tx) {
+                    pkeys[o] = (uint32_t)(ty * tiles_x + tx);
+                    pvals[o] = g[k];
+                    ++o;
+                }
+        }
+        off += t[k];
+    }
+}
+
+__global__ void __launch_bounds__(GS_BLOCK) k_finalize(const uint32_t* __restrict__ skeys,
+                                                       const uint32_t* __restrict__ svals,
+                                                       const uint32_t* __restrict__ sort_count,
+                                                       const float* __restrict__ depth,
+                                                       uint32_t* __restrict__ ranges, uint64_t* __restrict__ keys64) {
+    const uint32_t M = *sort_count;
+    const uint32_t i = blockIdx.x * GS_BLOCK + threadIdx.x;
+    if (i >= M) return;
+    const uint32_t t = skeys[i];
+    if (i == 0 || skeys[i - 1] != t) ranges[2 * t] = i;
+    if (i == M - 1 || skeys[i + 1] != t) ranges[2 * t + 1] = i + 1;
+    if (keys64) keys64[i] = ((uint64_t)t << 32) | (uint64_t)__float_as_uint(depth[svals[i]]);
+}
+
+struct BinsortLayout {
+    size_t dk[3], dv[3];      // depth sort: in, tmp, out
+    size_t pk[3], pv[2];      // pair sort: in, tmp, out (values out = caller's vals)
+    size_t hist, totals, bsum, counters;
+    size_t bytes;
+    uint32_t nblocks_hist;
+};
+
+BinsortLayout binsort_layout(int32_t n, uint32_t capacity) {
+    BinsortLayout L;
+    size_t o = 0;
+    const size_t nn = (size_t)(n > 0 ? n : 1), cc = (size_t)(capacity > 0 ? capacity : 1);
+    for (int i = 0; i < 3; ++i) { L.dk[i] = o; o += align256(4 * nn); }
+    for (int i = 0; i < 3; ++i) { L.dv[i] = o; o += align256(4 * nn); }
+    for (int i = 0; i < 3; ++i) { L.pk[i] = o; o += align256(4 * cc); }
+    for (int i = 0; i < 2; ++i) { L.pv[i] = o; o += align256(4 * cc); }
+    L.nblocks_hist = div_up(nn > cc ? nn : cc, GS_TILE_ITEMS);
+    L.hist = o; o += align256(4 * (size_t)kRadix * L.nblocks_hist);
+    L.totals = o; o += align256(4 * kRadix);
+    L.bsum = o; o += align256(4 * ((size_t)div_up(nn, GS_TILE_ITEMS) + 1));
+    L.counters = o; o += 256;
+    L.bytes = o;
+    return L;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(ws) + off); }
+
+// LSD passes over bits [0, total_bits) of `count` keys.  Buffers: in, tmp, out.
+hipError_t radix_sort(uint32_t* kin, uint32_t* vin, uint32_t* ktmp, uint32_t* vtmp, uint32_t* kout, uint32_t* vout,
+                      const uint32_t* count, uint32_t max_count, int total_bits, uint32_t* hist,
+                      uint32_t* totals, hipStream_t st) {
+    const uint32_t nblocks = div_up(max_count > 0 ? max_count : 1, GS_TILE_ITEMS);
+    const int passes = (total_bits + kRadixBits - 1) / kRadixBits;
+    uint32_t* kb[2] = {ktmp, kin};
+    uint32_t* vb[2] = {vtmp, vin};
+    for (int p = 0; p < passes; ++p) {
+        const int shift = p * kRadixBits;
+        const int nbits = (total_bits - shift) < kRadixBits ? (total_bits - shift) : kRadixBits;
+        const uint32_t mask = (1u << nbits) - 1u;
+        const uint32_t* ks = (p == 0) ? kin : kb[(p - 1) & 1];
+        const uint32_t* vs = (p == 0) ? vin : vb[(p - 1) & 1];
+        uint32_t* kd = (p == passes - 1) ? kout : kb[p & 1];
+        uint32_t* vd = (p == passes - 1) ? vout : vb[p & 1];
+        hipLaunchKernelGGL(k_radix_hist, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, count, shift, mask, hist, nblocks);
+        hipLaunchKernelGGL(k_radix_scan, dim3(kRadix), dim3(GS_BLOCK), 0, st, hist, nblocks, totals);
+        hipLaunchKernelGGL(k_radix_scatter, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, vs, kd, vd, count, shift, mask,
+                           nbits, hist, totals, nblocks);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t binsort_ws_bytes(int32_t n, uint32_t capacity, int32_t, int32_t) { return binsort_layout(n, capacity).bytes; }
+
+hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
+                          int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
+                          uint32_t* pair_offset, uint64_t* keys, uint32_t* num_pairs, gs_device_status* status,
+                          void* ws, hipStream_t st) {
+    const BinsortLayout L = binsort_layout(n, capacity);
+    const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
+    const uint32_t T = (uint32_t)TX * (uint32_t)TY;
+    uint32_t* hist = at<uint32_t>(ws, L.hist);
+    uint32_t* totals = at<uint32_t>(ws, L.totals);
+    uint32_t* bsum = at<uint32_t>(ws, L.bsum);
+    uint32_t* ctr = at<uint32_t>(ws, L.counters);   // [0] M, [1] sort count
+    hipError_t e = launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
+    if (e != hipSuccess) return e;
+    if (n == 0) {
+        e = launch_fill_u32(num_pairs, 0u, 1, st);
+        return e;
+    }
+    // 1. depth order of the visible set
+    hipLaunchKernelGGL(k_depth_keys, dim3(div_up(n, GS_BLOCK)), dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.depth,
+                       at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]));
+    e = radix_sort(at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]), at<uint32_t>(ws, L.dk[1]),
+                   at<uint32_t>(ws, L.dv[1]), at<uint32_t>(ws, L.dk[2]), at<uint32_t>(ws, L.dv[2]), vis_count,
+                   (uint32_t)n, 31, hist, totals, st);
+    if (e != hipSuccess) return e;
+    const uint32_t* order = at<uint32_t>(ws, L.dv[2]);
+    // 2. offsets in depth order + emission
+    const uint32_t nb = div_up(n, GS_TILE_ITEMS);
+    hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles, bsum);
+    e = launch_scan_blocks(bsum, nb, ctr + 0, nullptr, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_emit, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles,
+                       reinterpret_cast<const ushort4*>(proj.rect), bsum, ctr + 0, capacity, TX, pair_offset,
+                       at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), ctr + 1, num_pairs, status);
+    // 3. stable sort of the pairs by tile id
+    int tbits = 1;
+    while (tbits < 32 && (1u << tbits) < T) ++tbits;
+    e = radix_sort(at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), at<uint32_t>(ws, L.pk[1]),
+                   at<uint32_t>(ws, L.pv[1]), at<uint32_t>(ws, L.pk[2]), vals, ctr + 1, capacity, tbits, hist,
+                   totals, st);
+    if (e != hipSuccess) return e;
+    // 4. tile ranges (+ optional 64-bit keys)
+    if (capacity > 0)
+        hipLaunchKernelGGL(k_finalize, dim3(div_up(capacity, GS_BLOCK)), dim3(GS_BLOCK), 0, st,
+                           at<uint32_t>(ws, L.pk[2]), vals, ctr + 1, proj.depth, ranges, keys);
+    return hipGetLastError();
+}
+
+}  // namespace gsmi

@@ -1,0 +1,94 @@
+// Internal helpers shared by the gfx950 kernels of libgsmi (wave64 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/gsmi.h"
+
+#define GS_WAVE 64
+#define GS_BLOCK 256              // 4 waves
+#define GS_ITEMS 8                // items per thread in scans / sorts
+#define GS_TILE_ITEMS (GS_BLOCK * GS_ITEMS)
+
+namespace gsmi {
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+    const int l = lane_id();
+    return (l == 0) ? 0ull : (~0ull >> (64 - l));
+}
+
+__device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+    const int l = lane_id();
+#pragma unroll
+    for (int d = 1; d < GS_WAVE; d <<= 1) {
+        uint32_t o = __shfl_up(v, d, GS_WAVE);
+        if (l >= d) v += o;
+    }
+    return v;
+}
+
+// Sum over a wave; every lane gets the result.  DPP row reductions followed
+// by a combination of the four 16-lane rows through readlane.
+__device__ __forceinline__ float dpp_row_sum(float v) {
+    // quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, false));
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+    v = dpp_row_sum(v);
+    float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return (r0 + r1) + (r2 + r3);
+}
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, GS_WAVE);
+    return v;
+}
+
+// Exclusive scan over a 256-thread block.  `scratch` holds >= 4 uint32.
+// Returns the exclusive prefix of v; *total receives the block sum.
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratch, uint32_t* total) {
+    const int w = threadIdx.x / GS_WAVE;
+    const int l = lane_id();
+    uint32_t inc = wave_incl_scan(v);
+    if (l == GS_WAVE - 1) scratch[w] = inc;
+    __syncthreads();
+    uint32_t s0 = scratch[0], s1 = scratch[1], s2 = scratch[2], s3 = scratch[3];
+    uint32_t before = (w > 0 ? s0 : 0) + (w > 1 ? s1 : 0) + (w > 2 ? s2 : 0);
+    *total = s0 + s1 + s2 + s3;
+    __syncthreads();
+    return before + inc - v;
+}
+
+__device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* scratch) {
+    uint32_t t;
+    block_excl_scan(v, scratch, &t);
+    return t;
+}
+
+}  // namespace gsmi
+
+// ---------------------------------------------------------------------------
+// Host-side helpers shared by the launch wrappers.
+// ---------------------------------------------------------------------------
+
+namespace gsmi {
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline uint32_t div_up(uint64_t a, uint64_t b) { return (uint32_t)((a + b - 1) / b); }
+
+}  // namespace gsmi

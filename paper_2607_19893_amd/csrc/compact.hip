@@ -1,0 +1,149 @@
+// Scope extraction: ordered (ascending) stream compaction of a per-primitive
+// predicate, plus the small device-wide scan used by several passes.
+//
+// Three launches: per-block counts (blocked arrangement, 2048 items per
+// block), one single-workgroup exclusive scan of the block counts, and the
+// scatter that recomputes each item's rank within its block.
+#include "common.h"
+#include "internal.h"
+
+namespace gsmi {
+
+namespace {
+
+template <int KIND>
+__device__ __forceinline__ void load_pred(const void* src, int32_t n, int32_t base, uint32_t (&on)[GS_ITEMS]) {
+    if (KIND == GS_PRED_U32_NONZERO) {
+        const uint32_t* s = static_cast<const uint32_t*>(src);
+        if (base + GS_ITEMS <= n) {
+            const uint4 a = *reinterpret_cast<const uint4*>(s + base);
+            const uint4 b = *reinterpret_cast<const uint4*>(s + base + 4);
+            on[0] = a.x != 0; on[1] = a.y != 0; on[2] = a.z != 0; on[3] = a.w != 0;
+            on[4] = b.x != 0; on[5] = b.y != 0; on[6] = b.z != 0; on[7] = b.w != 0;
+        } else {
+#pragma unroll
+            for (int k = 0; k < GS_ITEMS; ++k) on[k] = (base + k < n) ? (s[base + k] != 0) : 0;
+        }
+    } else {
+        const uint8_t* s = static_cast<const uint8_t*>(src);
+        if (base + GS_ITEMS <= n) {
+            const uint2 a = *reinterpret_cast<const uint2*>(s + base);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) on[k] = ((a.x >> (8 * k)) & 0xFF) != 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) on[4 + k] = ((a.y >> (8 * k)) & 0xFF) != 0;
+        } else {
+#pragma unroll
+            for (int k = 0; k < GS_ITEMS; ++k) on[k] = (base + k < n) ? (s[base + k] != 0) : 0;
+        }
+    }
+}
+
+template <int KIND>
+__global__ void __launch_bounds__(GS_BLOCK) k_vis_count(const void* __restrict__ src, int32_t n,
+                                                        uint32_t* __restrict__ counts) {
+    __shared__ uint32_t scratch[4];
+    const int32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x * GS_ITEMS;
+    uint32_t on[GS_ITEMS];
+    load_pred<KIND>(src, n, base, on);
+    uint32_t c = 0;
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) c += on[k];
+    const uint32_t tot = block_sum_u32(c, scratch);
+    if (threadIdx.x == 0) counts[blockIdx.x] = tot;
+}
+
+template <int KIND>
+__global__ void __launch_bounds__(GS_BLOCK) k_vis_scatter(const void* __restrict__ src, int32_t n,
+                                                          const uint32_t* __restrict__ offsets,
+                                                          uint32_t* __restrict__ out_idx) {
+    __shared__ uint32_t scratch[4];
+    const int32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x * GS_ITEMS;
+    uint32_t on[GS_ITEMS];
+    load_pred<KIND>(src, n, base, on);
+    uint32_t c = 0;
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) c += on[k];
+    uint32_t tot;
+    uint32_t pos = block_excl_scan(c, scratch, &tot) + offsets[blockIdx.x];
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k)
+        if (on[k]) out_idx[pos++] = (uint32_t)(base + k);
+}
+
+// Exclusive scan of data[0..n) in place by one workgroup; total -> *total_out.
+__global__ void __launch_bounds__(GS_BLOCK) k_scan_single(uint32_t* __restrict__ data, uint32_t n,
+                                                          uint32_t* __restrict__ total_out) {
+    __shared__ uint32_t scratch[4];
+    uint32_t carry = 0;
+    for (uint32_t chunk = 0; chunk < n; chunk += GS_TILE_ITEMS) {
+        const uint32_t base = chunk + threadIdx.x * GS_ITEMS;
+        uint32_t v[GS_ITEMS];
+        uint32_t s = 0;
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) {
+            v[k] = (base + k < n) ? data[base + k] : 0u;
+            s += v[k];
+        }
+        uint32_t tot;
+        uint32_t run = block_excl_scan(s, scratch, &tot) + carry;
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) {
+            if (base + k < n) data[base + k] = run;
+            run += v[k];
+        }
+        carry += tot;
+    }
+    if (threadIdx.x == 0 && total_out) *total_out = carry;
+}
+
+__global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t value, size_t n) {
+    const size_t i = (size_t)blockIdx.x * GS_BLOCK + threadIdx.x;
+    const size_t stride = (size_t)gridDim.x * GS_BLOCK;
+    for (size_t j = i; j < n; j += stride) p[j] = value;
+}
+
+}  // namespace
+
+size_t scan_blocks_aux_words(uint32_t) { return 0; }
+
+hipError_t launch_scan_blocks(uint32_t* data, uint32_t n, uint32_t* total_out, uint32_t*, hipStream_t s) {
+    hipLaunchKernelGGL(k_scan_single, dim3(1), dim3(GS_BLOCK), 0, s, data, n, total_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t value, size_t n, hipStream_t st) {
+    if (n == 0) return hipSuccess;
+    uint32_t blocks = div_up(n, GS_BLOCK);
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(k_fill_u32, dim3(blocks), dim3(GS_BLOCK), 0, st, p, value, n);
+    return hipGetLastError();
+}
+
+size_t visible_ws_bytes(int32_t n) {
+    return align256(sizeof(uint32_t) * (size_t)(div_up((uint64_t)(n > 0 ? n : 0), GS_TILE_ITEMS) + 1));
+}
+
+hipError_t launch_visible(int kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count, void* ws,
+                          hipStream_t st) {
+    uint32_t* counts = static_cast<uint32_t*>(ws);
+    const uint32_t nb = div_up((uint64_t)n, GS_TILE_ITEMS);
+    if (nb == 0) return launch_fill_u32(out_count, 0u, 1, st);
+    if (kind == GS_PRED_U32_NONZERO)
+        hipLaunchKernelGGL(k_vis_count<GS_PRED_U32_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
+    else
+        hipLaunchKernelGGL(k_vis_count<GS_PRED_U8_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_scan_blocks(counts, nb, out_count, nullptr, st);
+    if (e != hipSuccess) return e;
+    if (kind == GS_PRED_U32_NONZERO)
+        hipLaunchKernelGGL(k_vis_scatter<GS_PRED_U32_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,
+                           out_idx);
+    else
+        hipLaunchKernelGGL(k_vis_scatter<GS_PRED_U8_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,
+                           out_idx);
+    return hipGetLastError();
+}
+
+}  // namespace gsmi

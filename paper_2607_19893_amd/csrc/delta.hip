@@ -1,0 +1,185 @@
+// Staged publication of pending updates: pack the rows of an ascending id
+// list into one message, and commit a message into a replica (add or copy),
+// stamping the per-primitive publication version.
+//
+// Same lane layout as the optimizer: one row per floor(64/row_len) lanes,
+// lane -> (group, column) fixed once, grid-strided rows.  Message writes are
+// contiguous; source/destination rows are gathered/scattered by id.
+#include "common.h"
+#include "internal.h"
+
+namespace gsmi {
+
+namespace {
+
+struct GroupArgs {
+    float* ptr[GS_MAX_GROUPS];
+    int32_t cols[GS_MAX_GROUPS];
+    int32_t n_groups;
+    int32_t row_len;
+    int32_t rows_per_wave;
+};
+
+__host__ __device__ inline uint64_t msg_words_before_rows(uint64_t count, int32_t n_groups) {
+    const uint64_t gw = (uint64_t)((n_groups + 3) / 4) * 4;
+    return ((8 + gw + count) + 3) / 4 * 4;
+}
+
+__host__ __device__ inline uint64_t msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups) {
+    return 4 * (msg_words_before_rows(count, n_groups) + count * (uint64_t)row_len);
+}
+
+__device__ __forceinline__ void lane_group(const GroupArgs& a, int lane, int& sub, int& grp, int& c) {
+    sub = lane / a.row_len;
+    c = lane - sub * a.row_len;
+    grp = 0;
+    while (grp + 1 < a.n_groups && c >= a.cols[grp]) {
+        c -= a.cols[grp];
+        ++grp;
+    }
+}
+
+__global__ void __launch_bounds__(GS_BLOCK) k_pack(GroupArgs a, const uint32_t* __restrict__ idx,
+                                                   const uint32_t* __restrict__ count, uint32_t version,
+                                                   uint32_t* __restrict__ msg, uint64_t capacity,
+                                                   gs_device_status* __restrict__ status) {
+    const uint32_t K = *count;
+    const uint64_t need = msg_bytes(K, a.row_len, a.n_groups);
+    if (need > capacity) {
+        if (blockIdx.x == 0 && threadIdx.x == 0 && status) {
+            atomicOr(&status->flags, GS_DEV_MSG_OVERFLOW);
+            atomicMax(&status->required, (uint32_t)(need > 0xFFFFFFFFull ? 0xFFFFFFFFull : need));
+        }
+        return;
+    }
+    const uint64_t gw = (uint64_t)((a.n_groups + 3) / 4) * 4;
+    if (blockIdx.x == 0 && threadIdx.x < 8 + gw) {
+        const uint32_t t = threadIdx.x;
+        uint32_t v = 0;
+        if (t == 0) v = GS_MSG_MAGIC;
+        else if (t == 1) v = K;
+        else if (t == 2) v = version;
+        else if (t == 3) v = (uint32_t)a.row_len;
+        else if (t == 4) v = (uint32_t)a.n_groups;
+        else if (t >= 8 && t - 8 < (uint32_t)a.n_groups) v = (uint32_t)a.cols[t - 8];
+        msg[t] = v;
+    }
+    uint32_t* __restrict__ ids = msg + 8 + gw;
+    const uint64_t row0 = msg_words_before_rows(K, a.n_groups);
+    // zero padding between the ids and the rows
+    if (blockIdx.x == 0 && threadIdx.x < 4) {
+        const uint64_t pw = 8 + gw + K + threadIdx.x;
+        if (pw < row0) msg[pw] = 0;
+    }
+    float* __restrict__ rows = reinterpret_cast<float*>(msg + row0);
+    const int lane = lane_id();
+    int sub, grp, c;
+    lane_group(a, lane, sub, grp, c);
+    if (sub >= a.rows_per_wave) return;
+    const float* __restrict__ src = a.ptr[grp];
+    const int cols = a.cols[grp];
+    const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
+    const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
+    for (uint32_t r = wave * a.rows_per_wave + sub; r < K; r += waves * a.rows_per_wave) {
+        const uint32_t id = idx[r];
+        if (lane - sub * a.row_len == 0) ids[r] = id;
+        rows[(size_t)r * a.row_len + (lane - sub * a.row_len)] = src[(size_t)id * cols + c];
+    }
+}
+
+// Header and id check; sets GS_DEV_MSG_MISMATCH when the message cannot be applied.
+__global__ void __launch_bounds__(GS_BLOCK) k_apply_check(GroupArgs a, const uint32_t* __restrict__ msg,
+                                                          uint64_t msg_capacity, int32_t n_rows, int32_t max_rows,
+                                                          gs_device_status* __restrict__ status) {
+    bool bad = false;
+    const uint32_t K = msg[1];
+    if (msg[0] != GS_MSG_MAGIC || msg[3] != (uint32_t)a.row_len || msg[4] != (uint32_t)a.n_groups ||
+        K > (uint32_t)max_rows || msg_bytes(K, a.row_len, a.n_groups) > msg_capacity)
+        bad = true;
+    if (!bad && blockIdx.x == 0 && threadIdx.x < (uint32_t)a.n_groups)
+        if (msg[8 + threadIdx.x] != (uint32_t)a.cols[threadIdx.x]) bad = true;
+    if (!bad) {
+        const uint64_t gw = (uint64_t)((a.n_groups + 3) / 4) * 4;
+        const uint32_t* ids = msg + 8 + gw;
+        for (uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x; r < K; r += gridDim.x * GS_BLOCK)
+            if (ids[r] >= (uint32_t)n_rows) bad = true;
+    }
+    if (bad) atomicOr(&status->flags, GS_DEV_MSG_MISMATCH);
+}
+
+__global__ void __launch_bounds__(GS_BLOCK) k_apply(GroupArgs a, const uint32_t* __restrict__ msg, int32_t mode,
+                                                    uint32_t* __restrict__ prim_version,
+                                                    const gs_device_status* __restrict__ status) {
+    if (status->flags & GS_DEV_MSG_MISMATCH) return;
+    const uint32_t K = msg[1];
+    const uint32_t version = msg[2];
+    const uint64_t gw = (uint64_t)((a.n_groups + 3) / 4) * 4;
+    const uint32_t* __restrict__ ids = msg + 8 + gw;
+    const float* __restrict__ rows = reinterpret_cast<const float*>(msg + msg_words_before_rows(K, a.n_groups));
+    const int lane = lane_id();
+    int sub, grp, c;
+    lane_group(a, lane, sub, grp, c);
+    if (sub >= a.rows_per_wave) return;
+    float* __restrict__ dst = a.ptr[grp];
+    const int cols = a.cols[grp];
+    const int col = lane - sub * a.row_len;
+    const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
+    const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
+    for (uint32_t r = wave * a.rows_per_wave + sub; r < K; r += waves * a.rows_per_wave) {
+        const uint32_t id = ids[r];
+        const float val = rows[(size_t)r * a.row_len + col];
+        float* q = dst + (size_t)id * cols + c;
+        *q = (mode == GS_APPLY_ADD) ? (*q + val) : val;
+        if (col == 0 && prim_version) prim_version[id] = version;
+    }
+}
+
+GroupArgs make_group_args(const gs_group* g, int32_t n) {
+    GroupArgs a = {};
+    int32_t rl = 0;
+    for (int i = 0; i < n; ++i) {
+        a.ptr[i] = g[i].ptr;
+        a.cols[i] = g[i].cols;
+        rl += g[i].cols;
+    }
+    a.n_groups = n;
+    a.row_len = rl;
+    a.rows_per_wave = rl > 0 ? GS_WAVE / rl : 0;
+    return a;
+}
+
+uint32_t row_blocks(int32_t max_rows, int32_t rpw) {
+    if (max_rows <= 0 || rpw <= 0) return 1;
+    uint32_t b = div_up(div_up((uint64_t)max_rows, (uint64_t)rpw), GS_BLOCK / GS_WAVE);
+    return b > 8192 ? 8192 : (b == 0 ? 1 : b);
+}
+
+}  // namespace
+
+size_t delta_msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups) {
+    return (size_t)msg_bytes(count, row_len, n_groups);
+}
+
+hipError_t launch_delta_pack(const uint32_t* idx, const uint32_t* count, int32_t max_rows, const gs_group* src,
+                             int32_t n_groups, uint32_t version, void* msg, size_t msg_capacity,
+                             gs_device_status* status, hipStream_t st) {
+    const GroupArgs a = make_group_args(src, n_groups);
+    hipLaunchKernelGGL(k_pack, dim3(row_blocks(max_rows, a.rows_per_wave)), dim3(GS_BLOCK), 0, st, a, idx, count,
+                       version, static_cast<uint32_t*>(msg), (uint64_t)msg_capacity, status);
+    return hipGetLastError();
+}
+
+hipError_t launch_delta_apply(const void* msg, size_t msg_capacity, const gs_group* dst, int32_t n_groups,
+                              int32_t n_rows, int32_t max_rows, int32_t mode, uint32_t* prim_version,
+                              gs_device_status* status, hipStream_t st) {
+    const GroupArgs a = make_group_args(dst, n_groups);
+    uint32_t cb = div_up((uint64_t)(max_rows > 0 ? max_rows : 1), GS_BLOCK);
+    if (cb > 4096) cb = 4096;
+    hipLaunchKernelGGL(k_apply_check, dim3(cb), dim3(GS_BLOCK), 0, st, a, static_cast<const uint32_t*>(msg),
+                       (uint64_t)msg_capacity, n_rows, max_rows, status);
+    hipLaunchKernelGGL(k_apply, dim3(row_blocks(max_rows, a.rows_per_wave)), dim3(GS_BLOCK), 0, st, a,
+                       static_cast<const uint32_t*>(msg), mode, prim_version, status);
+    return hipGetLastError();
+}
+
+}  // namespace gsmi

@@ -1,0 +1,68 @@
+// Launch wrappers shared between the kernel files and the C-ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/gsmi.h"
+
+namespace gsmi {
+
+struct CamArgs {
+    int32_t width, height, tiles_x, tiles_y;
+    float fx, fy, cx, cy, tan_fovx, tan_fovy, near_z;
+    float R[9];
+    float t[3];
+    float campos[3];
+};
+
+CamArgs make_cam_args(const gs_camera* c);
+
+// project.hip
+hipError_t launch_project(const gs_scene& s, const CamArgs& cam, const gs_proj& out, hipStream_t st);
+
+// compact.hip
+size_t visible_ws_bytes(int32_t n);
+hipError_t launch_visible(int kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count, void* ws,
+                          hipStream_t st);
+hipError_t launch_scan_blocks(uint32_t* data, uint32_t n, uint32_t* total_out, uint32_t* aux, hipStream_t s);
+size_t scan_blocks_aux_words(uint32_t n);
+hipError_t launch_fill_u32(uint32_t* p, uint32_t value, size_t n, hipStream_t st);
+
+// binsort.hip
+size_t binsort_ws_bytes(int32_t n, uint32_t capacity, int32_t width, int32_t height);
+hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
+                          int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
+                          uint32_t* pair_offset, uint64_t* keys, uint32_t* num_pairs, gs_device_status* status,
+                          void* ws, hipStream_t st);
+
+// raster.hip
+hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
+                             int32_t height, const float bg[3], float* img, float* final_T, uint32_t* n_contrib,
+                             uint8_t* active, hipStream_t st);
+size_t loss_ws_bytes(int32_t width, int32_t height);
+hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, int32_t height, float* loss,
+                          float* dL, void* ws, hipStream_t st);
+size_t raster_bwd_ws_bytes(int32_t n, uint32_t capacity);
+hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
+                             const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* vis_idx,
+                             const uint32_t* vis_count, uint32_t capacity, const float* final_T,
+                             const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
+                             const gs_scene& grads, float* grad2d, float* grad_norm, void* ws, hipStream_t st);
+
+// adam.hip
+hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
+                              const uint32_t* count, int32_t max_rows, int32_t step, float beta1, float beta2,
+                              float eps, hipStream_t st);
+
+// delta.hip
+size_t delta_msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups);
+hipError_t launch_delta_pack(const uint32_t* idx, const uint32_t* count, int32_t max_rows, const gs_group* src,
+                             int32_t n_groups, uint32_t version, void* msg, size_t msg_capacity,
+                             gs_device_status* status, hipStream_t st);
+hipError_t launch_delta_apply(const void* msg, size_t msg_capacity, const gs_group* dst, int32_t n_groups,
+                              int32_t n_rows, int32_t max_rows, int32_t mode, uint32_t* prim_version,
+                              gs_device_status* status, hipStream_t st);
+
+}  // namespace gsmi

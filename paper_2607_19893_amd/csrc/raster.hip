@@ -1,0 +1,563 @@
+// Rendering phase part 2 (forward alpha blending), the L1 image loss, and the
+// backward phase (pixel replay + per-primitive chain rule).
+//
+// Forward: one 256-thread workgroup per 16x16 tile, one pixel per thread.
+// The tile's sorted pairs are staged through LDS in batches of 256
+// (id, mean2d, conic+opacity, rgb); a workgroup-wide count of finished
+// pixels ends the batch loop early.
+//
+// Backward: same tile/pixel mapping, walking each tile's pairs back to front.
+// Each pixel recovers the transmittance in front of a pair by dividing by
+// (1 - alpha) and keeps the suffix colour sum; per pair, the 9 partial
+// derivatives are summed across each wave with DPP row reductions and across
+// the 4 waves through LDS, then written to the pair's own slot (the pair's
+// position in emission order).  A second kernel, one thread per visible
+// primitive, sums its slots in a fixed order -- the result is deterministic,
+// no floating-point atomics -- and applies the projection and colour chain
+// rule in fp32.
+#include "common.h"
+#include "internal.h"
+
+namespace gsmi {
+
+namespace {
+
+constexpr float kAlphaMin = 1.0f / 255.0f;
+constexpr float kAlphaMax = 0.99f;
+constexpr float kTMin = 1e-4f;
+
+// alpha of one (pixel, primitive) pair.  The forward and backward kernels both
+// call this, built without contraction, so they take identical decisions.
+#pragma clang fp contract(off)
+struct PairEval {
+    float dx, dy, sigma, e, g, alpha;
+};
+
+__device__ __forceinline__ PairEval eval_pair(float2 m, float4 co, float px, float py) {
+    PairEval r;
+    r.dx = m.x - px;
+    r.dy = m.y - py;
+    r.sigma = fmaf(r.dx, fmaf(0.5f * co.x, r.dx, co.y * r.dy), (0.5f * co.z * r.dy) * r.dy);
+    r.e = __expf(-r.sigma);
+    r.g = co.w * r.e;
+    r.alpha = fminf(kAlphaMax, r.g);
+    return r;
+}
+#pragma clang fp contract(on)
+
+__global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
+    const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
+    const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
+    float bg1, float bg2, float* __restrict__ img, float* __restrict__ final_T, uint32_t* __restrict__ n_contrib,
+    uint8_t* __restrict__ active) {
+    __shared__ float2 s_xy[GS_BLOCK];
+    __shared__ float4 s_co[GS_BLOCK];
+    __shared__ float s_rgb[3 * GS_BLOCK];
+    __shared__ uint32_t s_id[GS_BLOCK];
+    __shared__ uint32_t s_hit[GS_BLOCK];
+    const int tile = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int px = (tile % TX) * GS_TILE + (tid % GS_TILE);
+    const int py = (tile / TX) * GS_TILE + (tid / GS_TILE);
+    const bool inside = px < W && py < H;
+    const float fx = px + 0.5f, fy = py + 0.5f;
+    const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
+    float T = 1.0f, c0 = 0.0f, c1 = 0.0f, c2 = 0.0f;
+    uint32_t last = 0;
+    bool done = !inside;
+    for (uint32_t bs = start; bs < end; bs += GS_BLOCK) {
+        if (__syncthreads_count(done) == GS_BLOCK) break;
+        const uint32_t j = bs + tid;
+        if (j < end) {
+            const uint32_t g = vals[j];
+            s_id[tid] = g;
+            s_xy[tid] = mean2d[g];
+            s_co[tid] = conic_op[g];
+            s_rgb[3 * tid + 0] = rgb[3 * g + 0];
+            s_rgb[3 * tid + 1] = rgb[3 * g + 1];
+            s_rgb[3 * tid + 2] = rgb[3 * g + 2];
+        }
+        s_hit[tid] = 0;
+        __syncthreads();
+        const int nb = (int)min((uint32_t)GS_BLOCK, end - bs);
+        for (int k = 0; k < nb && !done; ++k) {
+            const PairEval p = eval_pair(s_xy[k], s_co[k], fx, fy);
+            if (p.sigma < 0.0f || p.alpha < kAlphaMin) continue;
+            const float Tn = T * (1.0f - p.alpha);
+            if (Tn < kTMin) {
+                done = true;
+                break;
+            }
+            const float wgt = p.alpha * T;
+            c0 = fmaf(wgt, s_rgb[3 * k + 0], c0);
+            c1 = fmaf(wgt, s_rgb[3 * k + 1], c1);
+            c2 = fmaf(wgt, s_rgb[3 * k + 2], c2);
+            T = Tn;
+            last = bs - start + k + 1;
+            s_hit[k] = 1u;
+        }
+        __syncthreads();
+        if (active && j < end && s_hit[tid]) active[s_id[tid]] = 1;
+    }
+    if (inside) {
+        const size_t HW = (size_t)W * H, p = (size_t)py * W + px;
+        img[p] = fmaf(T, bg0, c0);
+        img[HW + p] = fmaf(T, bg1, c1);
+        img[2 * HW + p] = fmaf(T, bg2, c2);
+        final_T[p] = T;
+        n_contrib[p] = last;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// L1 loss
+// ---------------------------------------------------------------------------
+
+__global__ void __launch_bounds__(GS_BLOCK) k_loss_l1(const float* __restrict__ img, const float* __restrict__ tgt,
+                                                      uint32_t total, float inv, float* __restrict__ dL,
+                                                      float* __restrict__ partial) {
+    __shared__ float s_red[4];
+    const uint32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x;
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        const uint32_t i = base + k * GS_BLOCK;
+        if (i < total) {
+            const float d = img[i] - tgt[i];
+            dL[i] = d > 0.0f ? inv : (d < 0.0f ? -inv : 0.0f);
+            acc += fabsf(d);
+        }
+    }
+    acc = wave_sum(acc);
+    if (lane_id() == 0) s_red[threadIdx.x / GS_WAVE] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) partial[blockIdx.x] = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
+}
+
+__global__ void __launch_bounds__(GS_BLOCK) k_loss_final(const float* __restrict__ partial, uint32_t nb,
+                                                         double inv_total, float* __restrict__ loss) {
+    __shared__ double s[GS_BLOCK];
+    double acc = 0.0;
+    for (uint32_t i = threadIdx.x; i < nb; i += GS_BLOCK) acc += (double)partial[i];
+    s[threadIdx.x] = acc;
+    __syncthreads();
+    for (int w = GS_BLOCK / 2; w > 0; w >>= 1) {
+        if (threadIdx.x < w) s[threadIdx.x] += s[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *loss = (float)(s[0] * inv_total);
+}
+
+// ---------------------------------------------------------------------------
+// backward, part 1: per pixel, back to front
+// ---------------------------------------------------------------------------
+
+constexpr int kG = 9;   // du dv dA dB dC dopacity dr dg db
+
+__global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
+    const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
+    const float4* __restrict__ conic_op, const float* __restrict__ rgb, const ushort4* __restrict__ rect,
+    const uint32_t* __restrict__ pair_offset, int32_t W, int32_t H, int32_t TX, float bg0, float bg1, float bg2,
+    const float* __restrict__ final_T, const uint32_t* __restrict__ n_contrib, const float* __restrict__ dL_dimg,
+    float* __restrict__ slots) {
+    __shared__ float2 s_xy[GS_BLOCK];
+    __shared__ float4 s_co[GS_BLOCK];
+    __shared__ float s_rgb[3 * GS_BLOCK];
+    __shared__ uint32_t s_id[GS_BLOCK];
+    __shared__ float s_part[4][kG][GS_BLOCK];
+    __shared__ uint32_t s_max;
+    const int tile = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int w = tid / GS_WAVE;
+    const int tx = tile % TX, ty = tile / TX;
+    const int px = tx * GS_TILE + (tid % GS_TILE);
+    const int py = ty * GS_TILE + (tid / GS_TILE);
+    const bool inside = px < W && py < H;
+    const float fx = px + 0.5f, fy = py + 0.5f;
+    const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
+    const size_t HW = (size_t)W * H, pix = (size_t)py * W + px;
+    float T = inside ? final_T[pix] : 1.0f;
+    const uint32_t last = inside ? n_contrib[pix] : 0u;
+    const float gC0 = inside ? dL_dimg[pix] : 0.0f;
+    const float gC1 = inside ? dL_dimg[HW + pix] : 0.0f;
+    const float gC2 = inside ? dL_dimg[2 * HW + pix] : 0.0f;
+    float S0 = T * bg0, S1 = T * bg1, S2 = T * bg2;
+    if (tid == 0) s_max = 0;
+    __syncthreads();
+    if (last > 0) atomicMax(&s_max, last);
+    __syncthreads();
+    const uint32_t maxlast = s_max;
+    const uint32_t n = end - start;
+    for (int64_t be = n; be > 0; be -= GS_BLOCK) {
+        const uint32_t bs = (uint32_t)(be > GS_BLOCK ? be - GS_BLOCK : 0);
+        const uint32_t cnt = (uint32_t)be - bs;
+        const uint32_t j = start + bs + tid;
+        uint32_t g = 0;
+        if ((uint32_t)tid < cnt) {
+            g = vals[j];
+            s_id[tid] = g;
+            s_xy[tid] = mean2d[g];
+            s_co[tid] = conic_op[g];
+            s_rgb[3 * tid + 0] = rgb[3 * g + 0];
+            s_rgb[3 * tid + 1] = rgb[3 * g + 1];
+            s_rgb[3 * tid + 2] = rgb[3 * g + 2];
+        }
+        __syncthreads();
+        if (bs < maxlast) {
+            for (int k = (int)cnt - 1; k >= 0; --k) {
+                float gr[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+                bool contrib = false;
+                if (bs + (uint32_t)k < last) {
+                    const float4 co = s_co[k];
+                    const PairEval p = eval_pair(s_xy[k], co, fx, fy);
+                    if (!(p.sigma < 0.0f) && !(p.alpha < kAlphaMin)) {
+                        contrib = true;
+                        const float om = 1.0f - p.alpha;
+                        T = T / om;
+                        const float inv_om = 1.0f / om;
+                        const float wgt = p.alpha * T;
+                        const float r0 = s_rgb[3 * k + 0], r1 = s_rgb[3 * k + 1], r2 = s_rgb[3 * k + 2];
+                        const float dalpha = gC0 * (T * r0 - S0 * inv_om) + gC1 * (T * r1 - S1 * inv_om) +
+                                             gC2 * (T * r2 - S2 * inv_om);
+                        S0 = fmaf(wgt, r0, S0);
+                        S1 = fmaf(wgt, r1, S1);
+                        S2 = fmaf(wgt, r2, S2);
+                        gr[6] = gC0 * wgt;
+                        gr[7] = gC1 * wgt;
+                        gr[8] = gC2 * wgt;
+                        if (p.g < kAlphaMax) {
+                            gr[5] = dalpha * p.e;
+                            const float ds = -dalpha * p.alpha;
+                            gr[0] = ds * (co.x * p.dx + co.y * p.dy);
+                            gr[1] = ds * (co.y * p.dx + co.z * p.dy);
+                            gr[2] = ds * 0.5f * p.dx * p.dx;
+                            gr[3] = ds * p.dx * p.dy;
+                            gr[4] = ds * 0.5f * p.dy * p.dy;
+                        }
+                    }
+                }
+                if (__ballot(contrib) != 0ull) {
+#pragma unroll
+                    for (int c = 0; c < kG; ++c) {
+                        const float v = wave_sum(gr[c]);
+                        if (lane_id() == 0) s_part[w][c][k] = v;
+                    }
+                } else if (lane_id() == 0) {
+#pragma unroll
+                    for (int c = 0; c < kG; ++c) s_part[w][c][k] = 0.0f;
+                }
+            }
+        }
+        __syncthreads();
+        if ((uint32_t)tid < cnt) {
+            const ushort4 rc = rect[g];
+            const uint32_t slot = pair_offset[g] + (uint32_t)(ty - rc.y) * (uint32_t)(rc.z - rc.x) + (uint32_t)(tx - rc.x);
+            float* dst = slots + (size_t)slot * kG;
+            if (bs < maxlast) {
+#pragma unroll
+                for (int c = 0; c < kG; ++c)
+                    dst[c] = (s_part[0][c][tid] + s_part[1][c][tid]) + (s_part[2][c][tid] + s_part[3][c][tid]);
+            } else {
+#pragma unroll
+                for (int c = 0; c < kG; ++c) dst[c] = 0.0f;
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// backward, part 2: per visible primitive
+// ---------------------------------------------------------------------------
+
+constexpr float kY1 = 0.48860251190291992f;
+constexpr float kY2a = 1.0925484305920792f;
+constexpr float kY2b = 0.31539156525252005f;
+constexpr float kY2c = 0.54627421529603959f;
+constexpr float kY3a = 0.59004358992664352f;
+constexpr float kY3b = 2.8906114426405538f;
+constexpr float kY3c = 0.45704579946446572f;
+constexpr float kY3d = 0.37317633259011546f;
+constexpr float kY3e = 1.4453057213202769f;
+
+// SH basis values and gradients of their polynomial form at d.
+template <int DEG>
+__device__ __forceinline__ void sh_basis_grad(float x, float y, float z, float* Y, float (*G)[3]) {
+    Y[0] = 0.28209479177387814f;
+    G[0][0] = G[0][1] = G[0][2] = 0.0f;
+    if (DEG < 1) return;
+    Y[1] = -kY1 * y; G[1][0] = 0.0f; G[1][1] = -kY1; G[1][2] = 0.0f;
+    Y[2] = kY1 * z;  G[2][0] = 0.0f; G[2][1] = 0.0f; G[2][2] = kY1;
+    Y[3] = -kY1 * x; G[3][0] = -kY1; G[3][1] = 0.0f; G[3][2] = 0.0f;
+    if (DEG < 2) return;
+    const float xx = x * x, yy = y * y, zz = z * z;
+    Y[4] = kY2a * x * y;  G[4][0] = kY2a * y; G[4][1] = kY2a * x; G[4][2] = 0.0f;
+    Y[5] = -kY2a * y * z; G[5][0] = 0.0f; G[5][1] = -kY2a * z; G[5][2] = -kY2a * y;
+    Y[6] = kY2b * (2.0f * zz - xx - yy);
+    G[6][0] = -2.0f * kY2b * x; G[6][1] = -2.0f * kY2b * y; G[6][2] = 4.0f * kY2b * z;
+    Y[7] = -kY2a * x * z; G[7][0] = -kY2a * z; G[7][1] = 0.0f; G[7][2] = -kY2a * x;
+    Y[8] = kY2c * (xx - yy); G[8][0] = 2.0f * kY2c * x; G[8][1] = -2.0f * kY2c * y; G[8][2] = 0.0f;
+    if (DEG < 3) return;
+    Y[9] = -kY3a * y * (3.0f * xx - yy);
+    G[9][0] = -6.0f * kY3a * x * y; G[9][1] = -3.0f * kY3a * (xx - yy); G[9][2] = 0.0f;
+    Y[10] = kY3b * x * y * z;
+    G[10][0] = kY3b * y * z; G[10][1] = kY3b * x * z; G[10][2] = kY3b * x * y;
+    Y[11] = -kY3c * y * (4.0f * zz - xx - yy);
+    G[11][0] = 2.0f * kY3c * x * y; G[11][1] = -kY3c * (4.0f * zz - xx - 3.0f * yy); G[11][2] = -8.0f * kY3c * y * z;
+    Y[12] = kY3d * z * (2.0f * zz - 3.0f * xx - 3.0f * yy);
+    G[12][0] = -6.0f * kY3d * x * z; G[12][1] = -6.0f * kY3d * y * z; G[12][2] = kY3d * (6.0f * zz - 3.0f * xx - 3.0f * yy);
+    Y[13] = -kY3c * x * (4.0f * zz - xx - yy);
+    G[13][0] = -kY3c * (4.0f * zz - 3.0f * xx - yy); G[13][1] = 2.0f * kY3c * x * y; G[13][2] = -8.0f * kY3c * x * z;
+    Y[14] = kY3e * z * (xx - yy);
+    G[14][0] = 2.0f * kY3e * x * z; G[14][1] = -2.0f * kY3e * y * z; G[14][2] = kY3e * (xx - yy);
+    Y[15] = -kY3a * x * (xx - 3.0f * yy);
+    G[15][0] = -3.0f * kY3a * (xx - yy); G[15][1] = 6.0f * kY3a * x * y; G[15][2] = 0.0f;
+}
+
+__device__ __forceinline__ float dot3(const float* a, const float* b) { return a[0] * b[0] + a[1] * b[1] + a[2] * b[2]; }
+
+template <int DEG>
+__global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
+    const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
+    const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, const uint8_t* __restrict__ clampm,
+    const float* __restrict__ mean, const float* __restrict__ log_scale, const float* __restrict__ quat,
+    const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c, uint32_t capacity,
+    float* __restrict__ g_mean,
+    float* __restrict__ g_ls, float* __restrict__ g_quat, float* __restrict__ g_op, float* __restrict__ g_sh,
+    float* __restrict__ grad2d, float* __restrict__ grad_norm) {
+    const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
+    if (r >= *vis_count) return;
+    const uint32_t id = vis_idx[r];
+    // 1. this primitive's 2D gradient: its pair slots in order (none if the
+    //    pair list overflowed its capacity)
+    float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+    {
+        const uint64_t first = pair_offset[id];
+        const uint32_t nt = tiles[id];
+        const float* sl = slots + first * kG;
+        if (first + nt <= capacity)
+            for (uint32_t k = 0; k < nt; ++k)
+#pragma unroll
+            for (int q = 0; q < kG; ++q) g2[q] += sl[k * kG + q];
+    }
+    if (grad2d) {
+#pragma unroll
+        for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
+    }
+    if (grad_norm) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
+
+    const float mu[3] = {mean[3 * id], mean[3 * id + 1], mean[3 * id + 2]};
+    // 2. opacity
+    const float o = 1.0f / (1.0f + expf(-opacity[id]));
+    g_op[id] = g2[5] * o * (1.0f - o);
+
+    // 3. colour: dL/dsh and the view-direction path into the mean
+    float gmu[3];
+    {
+        float v[3] = {mu[0] - c.campos[0], mu[1] - c.campos[1], mu[2] - c.campos[2]};
+        const float len = sqrtf(dot3(v, v));
+        const float il = 1.0f / len;
+        const float d[3] = {v[0] * il, v[1] * il, v[2] * il};
+        constexpr int K = (DEG + 1) * (DEG + 1);
+        float Y[16], G[16][3];
+        sh_basis_grad<DEG>(d[0], d[1], d[2], Y, G);
+        const uint8_t cm = clampm[id];
+        const float gc[3] = {(cm & 1) ? 0.0f : g2[6], (cm & 2) ? 0.0f : g2[7], (cm & 4) ? 0.0f : g2[8]};
+        const float* co = sh + (size_t)id * K * 3;
+        float* gco = g_sh + (size_t)id * K * 3;
+        float gd[3] = {0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const float a = gc[0] * co[3 * k] + gc[1] * co[3 * k + 1] + gc[2] * co[3 * k + 2];
+            gd[0] += a * G[k][0];
+            gd[1] += a * G[k][1];
+            gd[2] += a * G[k][2];
+            gco[3 * k + 0] = gc[0] * Y[k];
+            gco[3 * k + 1] = gc[1] * Y[k];
+            gco[3 * k + 2] = gc[2] * Y[k];
+        }
+        const float rad = dot3(gd, d);
+        gmu[0] = (gd[0] - d[0] * rad) * il;
+        gmu[1] = (gd[1] - d[1] * rad) * il;
+        gmu[2] = (gd[2] - d[2] * rad) * il;
+    }
+
+    // 4. geometry
+    const float* R = c.R;
+    float p[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) p[k] = R[3 * k] * mu[0] + R[3 * k + 1] * mu[1] + R[3 * k + 2] * mu[2] + c.t[k];
+    const float s[3] = {expf(log_scale[3 * id]), expf(log_scale[3 * id + 1]), expf(log_scale[3 * id + 2])};
+    const float4 qr = reinterpret_cast<const float4*>(quat)[id];
+    const float qn = sqrtf(qr.x * qr.x + qr.y * qr.y + qr.z * qr.z + qr.w * qr.w);
+    const float iq = 1.0f / qn;
+    const float w = qr.x * iq, x = qr.y * iq, y = qr.z * iq, z = qr.w * iq;
+    const float Rq[3][3] = {{1.0f - 2.0f * (y * y + z * z), 2.0f * (x * y - w * z), 2.0f * (x * z + w * y)},
+                            {2.0f * (x * y + w * z), 1.0f - 2.0f * (x * x + z * z), 2.0f * (y * z - w * x)},
+                            {2.0f * (x * z - w * y), 2.0f * (y * z + w * x), 1.0f - 2.0f * (x * x + y * y)}};
+    float M[3][3], Sg[3][3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 3; ++b) M[a][b] = Rq[a][b] * s[b];
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 3; ++b) Sg[a][b] = M[a][0] * M[b][0] + M[a][1] * M[b][1] + M[a][2] * M[b][2];
+    const float tz = p[2], itz = 1.0f / tz;
+    const float lx = 1.3f * c.tan_fovx, ly = 1.3f * c.tan_fovy;
+    const float rx = p[0] * itz, ry = p[1] * itz;
+    const bool clx = rx < -lx || rx > lx, cly = ry < -ly || ry > ly;
+    const float xr = fminf(lx, fmaxf(-lx, rx)), yr = fminf(ly, fmaxf(-ly, ry));
+    const float j00 = c.fx * itz, j11 = c.fy * itz;
+    const float j02 = -c.fx * xr * itz, j12 = -c.fy * yr * itz;
+    float T0[3], T1[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        T0[k] = j00 * R[k] + j02 * R[6 + k];
+        T1[k] = j11 * R[3 + k] + j12 * R[6 + k];
+    }
+    float ST0[3], ST1[3];   // Sigma T0, Sigma T1
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+        ST0[a] = Sg[a][0] * T0[0] + Sg[a][1] * T0[1] + Sg[a][2] * T0[2];
+        ST1[a] = Sg[a][0] * T1[0] + Sg[a][1] * T1[1] + Sg[a][2] * T1[2];
+    }
+    const float ca = dot3(T0, ST0) + 0.3f, cb = dot3(T0, ST1), cc = dot3(T1, ST1) + 0.3f;
+    const float det = ca * cc - cb * cb;
+    const float id2 = 1.0f / (det * det);
+    // conic (A,B,C) = (c, -b, a)/det  ->  gradient w.r.t. (a, b, c)
+    const float gA = g2[2], gB = g2[3], gC = g2[4];
+    const float ga = (-gA * cc * cc + gB * cb * cc - gC * cb * cb) * id2;
+    const float gb = (2.0f * gA * cb * cc - gB * (ca * cc + cb * cb) + 2.0f * gC * ca * cb) * id2;
+    const float gcv = (-gA * cb * cb + gB * ca * cb - gC * ca * ca) * id2;
+    // a = T0.S.T0, b = T0.S.T1, c = T1.S.T1
+    float gT0[3], gT1[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+        gT0[a] = 2.0f * ga * ST0[a] + gb * ST1[a];
+        gT1[a] = gb * ST0[a] + 2.0f * gcv * ST1[a];
+    }
+    const float gj00 = gT0[0] * R[0] + gT0[1] * R[1] + gT0[2] * R[2];
+    const float gj02 = gT0[0] * R[6] + gT0[1] * R[7] + gT0[2] * R[8];
+    const float gj11 = gT1[0] * R[3] + gT1[1] * R[4] + gT1[2] * R[5];
+    const float gj12 = gT1[0] * R[6] + gT1[1] * R[7] + gT1[2] * R[8];
+    const float itz2 = itz * itz;
+    float gp[3] = {0.0f, 0.0f, 0.0f};
+    gp[2] -= (gj00 * c.fx + gj11 * c.fy) * itz2;
+    if (clx) {
+        gp[2] += gj02 * c.fx * xr * itz2;
+    } else {
+        gp[0] -= gj02 * c.fx * itz2;
+        gp[2] += 2.0f * gj02 * c.fx * p[0] * itz2 * itz;
+    }
+    if (cly) {
+        gp[2] += gj12 * c.fy * yr * itz2;
+    } else {
+        gp[1] -= gj12 * c.fy * itz2;
+        gp[2] += 2.0f * gj12 * c.fy * p[1] * itz2 * itz;
+    }
+    gp[0] += g2[0] * c.fx * itz;
+    gp[1] += g2[1] * c.fy * itz;
+    gp[2] -= (g2[0] * c.fx * p[0] + g2[1] * c.fy * p[1]) * itz2;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) gmu[k] += R[k] * gp[0] + R[3 + k] * gp[1] + R[6 + k] * gp[2];
+    g_mean[3 * id + 0] = gmu[0];
+    g_mean[3 * id + 1] = gmu[1];
+    g_mean[3 * id + 2] = gmu[2];
+    // Sigma = M M^T with symmetric gradient Gs = ga T0T0^T + gb (T0T1^T + T1T0^T)/2 + gc T1T1^T
+    float Gs[3][3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 3; ++b)
+            Gs[a][b] = ga * T0[a] * T0[b] + 0.5f * gb * (T0[a] * T1[b] + T1[a] * T0[b]) + gcv * T1[a] * T1[b];
+    float gR[3][3];
+#pragma unroll
+    for (int b = 0; b < 3; ++b) {
+        float gsb = 0.0f;
+#pragma unroll
+        for (int a = 0; a < 3; ++a) {
+            const float gM = 2.0f * (Gs[a][0] * M[0][b] + Gs[a][1] * M[1][b] + Gs[a][2] * M[2][b]);
+            gR[a][b] = gM * s[b];
+            gsb += gM * Rq[a][b];
+        }
+        g_ls[3 * id + b] = gsb * s[b];
+    }
+    float gw = 2.0f * (x * (gR[2][1] - gR[1][2]) + y * (gR[0][2] - gR[2][0]) + z * (gR[1][0] - gR[0][1]));
+    float gx = 2.0f * (w * (gR[2][1] - gR[1][2]) - 2.0f * x * (gR[1][1] + gR[2][2]) + y * (gR[0][1] + gR[1][0]) +
+                       z * (gR[0][2] + gR[2][0]));
+    float gy = 2.0f * (w * (gR[0][2] - gR[2][0]) + x * (gR[0][1] + gR[1][0]) - 2.0f * y * (gR[0][0] + gR[2][2]) +
+                       z * (gR[1][2] + gR[2][1]));
+    float gz = 2.0f * (w * (gR[1][0] - gR[0][1]) + x * (gR[0][2] + gR[2][0]) + y * (gR[1][2] + gR[2][1]) -
+                       2.0f * z * (gR[0][0] + gR[1][1]));
+    const float along = w * gw + x * gx + y * gy + z * gz;
+    reinterpret_cast<float4*>(g_quat)[id] =
+        make_float4((gw - w * along) * iq, (gx - x * along) * iq, (gy - y * along) * iq, (gz - z * along) * iq);
+}
+
+}  // namespace
+
+hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
+                             int32_t height, const float bg[3], float* img, float* final_T, uint32_t* n_contrib,
+                             uint8_t* active, hipStream_t st) {
+    const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
+    if (TX * TY == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_raster_fwd, dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
+                       reinterpret_cast<const float2*>(proj.mean2d), reinterpret_cast<const float4*>(proj.conic_opacity),
+                       proj.rgb, width, height, TX, bg[0], bg[1], bg[2], img, final_T, n_contrib, active);
+    return hipGetLastError();
+}
+
+size_t loss_ws_bytes(int32_t width, int32_t height) {
+    return align256(sizeof(float) * (div_up(3ull * (uint64_t)width * (uint64_t)height, GS_TILE_ITEMS) + 1));
+}
+
+hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, int32_t height, float* loss,
+                          float* dL, void* ws, hipStream_t st) {
+    const uint64_t total = 3ull * (uint64_t)width * (uint64_t)height;
+    const uint32_t nb = div_up(total, GS_TILE_ITEMS);
+    float* partial = static_cast<float*>(ws);
+    const float inv = (float)(1.0 / (double)total);
+    if (nb > 0)
+        hipLaunchKernelGGL(k_loss_l1, dim3(nb), dim3(GS_BLOCK), 0, st, img, target, (uint32_t)total, inv, dL, partial);
+    hipLaunchKernelGGL(k_loss_final, dim3(1), dim3(GS_BLOCK), 0, st, partial, nb,
+                       total ? 1.0 / (double)total : 0.0, loss);
+    return hipGetLastError();
+}
+
+size_t raster_bwd_ws_bytes(int32_t, uint32_t capacity) {
+    return align256(sizeof(float) * kG * (size_t)(capacity > 0 ? capacity : 1));
+}
+
+hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
+                             const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* vis_idx,
+                             const uint32_t* vis_count, uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
+                             const float* dL_dimg, const float bg[3], const gs_scene& grads, float* grad2d,
+                             float* grad_norm, void* ws, hipStream_t st) {
+    float* slots = static_cast<float*>(ws);
+    const int32_t T = cam.tiles_x * cam.tiles_y;
+    if (T > 0)
+        hipLaunchKernelGGL(k_raster_bwd, dim3(T), dim3(GS_BLOCK), 0, st, ranges, vals,
+                           reinterpret_cast<const float2*>(proj.mean2d),
+                           reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb,
+                           reinterpret_cast<const ushort4*>(proj.rect), pair_offset, cam.width, cam.height,
+                           cam.tiles_x, bg[0], bg[1], bg[2], final_T, n_contrib, dL_dimg, slots);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || scene.n == 0) return e;
+    const dim3 grid(div_up(scene.n, GS_BLOCK));
+#define GS_LAUNCH_PBWD(D)                                                                                        \
+    hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset, \
+                       slots, proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam,     \
+                       capacity, grads.mean, grads.log_scale, grads.quat, grads.opacity, grads.sh, grad2d, grad_norm)
+    switch (scene.sh_degree) {
+        case 0: GS_LAUNCH_PBWD(0); break;
+        case 1: GS_LAUNCH_PBWD(1); break;
+        case 2: GS_LAUNCH_PBWD(2); break;
+        default: GS_LAUNCH_PBWD(3); break;
+    }
+#undef GS_LAUNCH_PBWD
+    return hipGetLastError();
+}
+
+}  // namespace gsmi

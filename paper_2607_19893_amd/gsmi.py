@@ -1,0 +1,243 @@
+"""Thin ctypes binding of libgsmi (include/gsmi.h): same names, argument
+marshalling only.  Tensors are torch tensors on the GPU; their data pointers
+and the current HIP stream are handed to the C ABI unchanged.
+
+Importing this module loads the in-tree libgsmi.so and fails loudly if it is
+missing; there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libgsmi.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libgsmi.so is not built (run __graft_entry__.build() or "
+                      "python -m paper_2607_19893_amd.build); there is no fallback path")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+P = ctypes.c_void_p
+i32, u32, i64, f32, sz = ctypes.c_int32, ctypes.c_uint32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+
+GS_OK, GS_ERR_INVALID_ARG, GS_ERR_UNSUPPORTED, GS_ERR_WORKSPACE, GS_ERR_HIP = range(5)
+GS_WS_VISIBLE_SET, GS_WS_BIN_SORT, GS_WS_RASTER_BWD, GS_WS_LOSS = 1, 2, 3, 4
+GS_PRED_U32_NONZERO, GS_PRED_U8_NONZERO = 0, 1
+GS_APPLY_ADD, GS_APPLY_OVERWRITE = 0, 1
+GS_DEV_PAIR_OVERFLOW, GS_DEV_MSG_OVERFLOW, GS_DEV_MSG_MISMATCH = 1, 2, 4
+GS_MSG_MAGIC = 0x47534D31
+GS_MAX_GROUPS = 8
+
+
+class gs_scene(ctypes.Structure):
+    _fields_ = [("n", i32), ("sh_degree", i32), ("mean", P), ("log_scale", P), ("quat", P), ("opacity", P),
+                ("sh", P)]
+
+
+class gs_camera(ctypes.Structure):
+    _fields_ = [("width", i32), ("height", i32), ("fx", f32), ("fy", f32), ("cx", f32), ("cy", f32),
+                ("tan_fovx", f32), ("tan_fovy", f32), ("near_z", f32), ("R", f32 * 9), ("t", f32 * 3),
+                ("campos", f32 * 3)]
+
+
+class gs_proj(ctypes.Structure):
+    _fields_ = [("radius", P), ("tiles", P), ("rect", P), ("depth", P), ("mean2d", P), ("conic_opacity", P),
+                ("rgb", P), ("clamp", P)]
+
+
+class gs_adam_group(ctypes.Structure):
+    _fields_ = [("p", P), ("g", P), ("m", P), ("v", P), ("delta", P), ("cols", i32), ("lr", f32)]
+
+
+class gs_group(ctypes.Structure):
+    _fields_ = [("ptr", P), ("cols", i32)]
+
+
+_lib.gs_abi_version.restype = i32
+_lib.gs_status_string.restype = ctypes.c_char_p
+_lib.gs_status_string.argtypes = [i32]
+_lib.gs_last_error.restype = ctypes.c_char_p
+_lib.gs_workspace_bytes.restype = sz
+_lib.gs_workspace_bytes.argtypes = [i32, i32, u32, i32, i32]
+_lib.gs_delta_msg_bytes.restype = sz
+_lib.gs_delta_msg_bytes.argtypes = [u32, i32, i32]
+_lib.gs_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P]
+_lib.gs_visible_set.argtypes = [i32, P, i32, P, P, P, sz, P]
+_lib.gs_bin_sort.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, u32, P, P, P, P, P, P, P, sz, P]
+_lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, P, P, P, P, P]
+_lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
+_lib.gs_raster_bwd.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P, P, P,
+                               P, P, u32, P, P, P, P, ctypes.POINTER(gs_scene), P, P, P, sz, P]
+_lib.gs_sparse_adam.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, i32, f32, f32, f32, P]
+_lib.gs_delta_pack.argtypes = [P, P, i32, ctypes.POINTER(gs_group), i32, u32, P, sz, P, P]
+_lib.gs_delta_apply.argtypes = [P, sz, ctypes.POINTER(gs_group), i32, i32, i32, i32, P, P, P]
+for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
+              "gs_sparse_adam", "gs_delta_pack", "gs_delta_apply"):
+    getattr(_lib, _name).restype = i32
+
+EXPORTS = ["gs_abi_version", "gs_status_string", "gs_last_error", "gs_workspace_bytes", "gs_delta_msg_bytes",
+           "gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
+           "gs_sparse_adam", "gs_delta_pack", "gs_delta_apply"]
+
+
+class GsmiError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        msg = _lib.gs_last_error().decode()
+        super().__init__("%s -> %s: %s" % (fn, _lib.gs_status_string(status).decode(), msg))
+
+
+def _check(fn, st):
+    if st != GS_OK:
+        raise GsmiError(fn, st)
+    return st
+
+
+def ptr(t):
+    """Device pointer of a tensor (or None)."""
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def current_stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def make_camera(cam) -> gs_camera:
+    c = gs_camera()
+    c.width, c.height = int(cam.width), int(cam.height)
+    for k in ("fx", "fy", "cx", "cy", "tan_fovx", "tan_fovy", "near_z"):
+        setattr(c, k, float(getattr(cam, k)))
+    R = [float(x) for x in cam.R.reshape(9)]
+    for i in range(9):
+        c.R[i] = R[i]
+    for i in range(3):
+        c.t[i] = float(cam.t[i])
+        c.campos[i] = float(cam.campos[i])
+    return c
+
+
+def make_scene(n, sh_degree, mean, log_scale, quat, opacity, sh) -> gs_scene:
+    return gs_scene(int(n), int(sh_degree), ptr(mean), ptr(log_scale), ptr(quat), ptr(opacity), ptr(sh))
+
+
+def make_proj(radius, tiles, rect, depth, mean2d, conic_opacity, rgb, clamp) -> gs_proj:
+    return gs_proj(ptr(radius), ptr(tiles), ptr(rect), ptr(depth), ptr(mean2d), ptr(conic_opacity), ptr(rgb),
+                   ptr(clamp))
+
+
+# ---- the entry points -------------------------------------------------------
+
+def gs_abi_version() -> int:
+    return int(_lib.gs_abi_version())
+
+
+def gs_status_string(s: int) -> str:
+    return _lib.gs_status_string(int(s)).decode()
+
+
+def gs_last_error() -> str:
+    return _lib.gs_last_error().decode()
+
+
+def gs_workspace_bytes(which, n, capacity=0, width=0, height=0) -> int:
+    return int(_lib.gs_workspace_bytes(int(which), int(n), int(capacity), int(width), int(height)))
+
+
+def gs_delta_msg_bytes(count, row_len, n_groups) -> int:
+    return int(_lib.gs_delta_msg_bytes(int(count), int(row_len), int(n_groups)))
+
+
+def gs_project(scene: gs_scene, cam: gs_camera, proj: gs_proj, stream=None):
+    return _check("gs_project", _lib.gs_project(ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj),
+                                                stream if stream is not None else current_stream()))
+
+
+def gs_visible_set(kind, src, n, out_idx, out_count, ws, stream=None):
+    return _check("gs_visible_set", _lib.gs_visible_set(int(kind), ptr(src), int(n), ptr(out_idx), ptr(out_count),
+                                                        ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
+                                                        stream if stream is not None else current_stream()))
+
+
+def gs_bin_sort(proj: gs_proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges, pair_offset, keys,
+                num_pairs, status, ws, stream=None):
+    return _check("gs_bin_sort", _lib.gs_bin_sort(ctypes.byref(proj), int(n), ptr(vis_idx), ptr(vis_count),
+                                                  int(width), int(height), int(capacity), ptr(vals), ptr(ranges),
+                                                  ptr(pair_offset), ptr(keys), ptr(num_pairs), ptr(status), ptr(ws),
+                                                  ws.numel() * ws.element_size(),
+                                                  stream if stream is not None else current_stream()))
+
+
+def _bg(bg):
+    arr = (ctypes.c_float * 3)(*[float(x) for x in bg])
+    return arr
+
+
+def gs_raster_fwd(proj: gs_proj, n, vals, ranges, width, height, bg, img, final_T, n_contrib, active=None,
+                  stream=None):
+    b = _bg(bg)
+    return _check("gs_raster_fwd", _lib.gs_raster_fwd(ctypes.byref(proj), int(n), ptr(vals), ptr(ranges), int(width),
+                                                      int(height), ctypes.cast(b, P), ptr(img), ptr(final_T),
+                                                      ptr(n_contrib), ptr(active),
+                                                      stream if stream is not None else current_stream()))
+
+
+def gs_loss_l1(img, target, width, height, loss, dL_dimg, ws, stream=None):
+    return _check("gs_loss_l1", _lib.gs_loss_l1(ptr(img), ptr(target), int(width), int(height), ptr(loss),
+                                                ptr(dL_dimg), ptr(ws), ws.numel() * ws.element_size(),
+                                                stream if stream is not None else current_stream()))
+
+
+def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, pair_offset, vis_idx, vis_count,
+                  capacity, final_T, n_contrib, dL_dimg, bg, grads: gs_scene, grad2d, grad_norm, ws, stream=None):
+    b = _bg(bg)
+    return _check("gs_raster_bwd", _lib.gs_raster_bwd(ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj),
+                                                      ptr(vals), ptr(ranges), ptr(pair_offset), ptr(vis_idx),
+                                                      ptr(vis_count), int(capacity), ptr(final_T), ptr(n_contrib),
+                                                      ptr(dL_dimg), ctypes.cast(b, P), ctypes.byref(grads),
+                                                      ptr(grad2d), ptr(grad_norm), ptr(ws),
+                                                      ws.numel() * ws.element_size(),
+                                                      stream if stream is not None else current_stream()))
+
+
+def make_adam_groups(groups):
+    """groups: list of (p, g, m, v, delta_or_None, lr) tensors [n, cols]."""
+    arr = (gs_adam_group * len(groups))()
+    for i, (p, g, m, v, d, lr) in enumerate(groups):
+        arr[i] = gs_adam_group(ptr(p), ptr(g), ptr(m), ptr(v), ptr(d), int(p.shape[1]), float(lr))
+    return arr
+
+
+def gs_sparse_adam(groups_arr, n_groups, idx, count, max_rows, step, beta1, beta2, eps, stream=None):
+    return _check("gs_sparse_adam", _lib.gs_sparse_adam(groups_arr, int(n_groups), ptr(idx), ptr(count),
+                                                        int(max_rows), int(step), float(beta1), float(beta2),
+                                                        float(eps), stream if stream is not None else current_stream()))
+
+
+def make_groups(tensors):
+    arr = (gs_group * len(tensors))()
+    for i, t in enumerate(tensors):
+        arr[i] = gs_group(ptr(t), int(t.shape[1]))
+    return arr
+
+
+def gs_delta_pack(idx, count, max_rows, groups_arr, n_groups, version, msg, status, stream=None):
+    return _check("gs_delta_pack", _lib.gs_delta_pack(ptr(idx), ptr(count), int(max_rows), groups_arr, int(n_groups),
+                                                      int(version), ptr(msg), msg.numel() * msg.element_size(),
+                                                      ptr(status), stream if stream is not None else current_stream()))
+
+
+def gs_delta_apply(msg, groups_arr, n_groups, n_rows, max_rows, mode, prim_version, status, stream=None):
+    return _check("gs_delta_apply", _lib.gs_delta_apply(ptr(msg), msg.numel() * msg.element_size(), groups_arr,
+                                                        int(n_groups), int(n_rows),
+                                                        int(max_rows), int(mode), ptr(prim_version), ptr(status),
+                                                        stream if stream is not None else current_stream()))
+
+
+def raw():
+    """The loaded ctypes library (for tests of argument validation)."""
+    return _lib

@@ -1,0 +1,211 @@
+"""One training view on the GPU, driven through the C ABI.
+
+`ViewTrainer` owns the device buffers of one primitive pool (parameters,
+gradients, Adam moments, projection outputs, pair lists, images, workspaces,
+a replica and the publication message) and calls the gs_* entry points in
+phase order.  torch is used for allocation, host<->device copies and the
+stream only; every step of the path runs in libgsmi's kernels.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import gsmi
+
+GROUPS = ("mean", "log_scale", "quat", "opacity", "sh")
+
+
+def _u32(n, device):
+    return torch.zeros(max(1, int(n)), dtype=torch.int32, device=device)
+
+
+def to_u32(t) -> np.ndarray:
+    return t.detach().cpu().numpy().view(np.uint32)
+
+
+class ViewTrainer:
+    def __init__(self, scene, capacity: int = 0, max_width: int = 0, max_height: int = 0, device="cuda",
+                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-15, with_replica=True, with_keys=False):
+        self.dev = torch.device(device)
+        self.n = int(scene.n)
+        self.deg = int(scene.sh_degree)
+        self.K = (self.deg + 1) ** 2
+        self.cols = [3, 3, 4, 1, 3 * self.K]
+        self.row_len = sum(self.cols)
+        self.lr, self.beta1, self.beta2, self.eps = lr, beta1, beta2, eps
+        n = self.n
+        host = [scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh]
+        self.params = [torch.from_numpy(np.ascontiguousarray(a, np.float32).reshape(n, c)).to(self.dev)
+                       for a, c in zip(host, self.cols)]
+        self.grads = [torch.zeros(n, c, device=self.dev) for c in self.cols]
+        self.m = [torch.zeros(n, c, device=self.dev) for c in self.cols]
+        self.v = [torch.zeros(n, c, device=self.dev) for c in self.cols]
+        self.delta = [torch.zeros(n, c, device=self.dev) for c in self.cols]
+        self.replica = [p.clone() for p in self.params] if with_replica else None
+        self.version = _u32(n, self.dev)
+        # projection
+        self.radius = _u32(n, self.dev)
+        self.tiles = _u32(n, self.dev)
+        self.rect = torch.zeros(max(1, n), 4, dtype=torch.int16, device=self.dev)
+        self.depth = torch.zeros(max(1, n), device=self.dev)
+        self.mean2d = torch.zeros(max(1, n), 2, device=self.dev)
+        self.conic = torch.zeros(max(1, n), 4, device=self.dev)
+        self.rgb = torch.zeros(max(1, n), 3, device=self.dev)
+        self.clamp = torch.zeros(max(1, n), dtype=torch.uint8, device=self.dev)
+        self.active = torch.zeros(max(1, n), dtype=torch.uint8, device=self.dev)
+        self.vis_idx = _u32(n, self.dev)
+        self.act_idx = _u32(n, self.dev)
+        self.counts = _u32(8, self.dev)          # [0] V, [1] M, [2] active count
+        self.status = _u32(4, self.dev)
+        self.pair_offset = _u32(n, self.dev)
+        self.grad2d = torch.zeros(max(1, n), 9, device=self.dev)
+        self.grad_norm = torch.zeros(max(1, n), device=self.dev)
+        self.loss = torch.zeros(1, device=self.dev)
+        self.with_keys = with_keys
+        self.ws_vis = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_VISIBLE_SET, n), dtype=torch.uint8,
+                                  device=self.dev)
+        self.capacity = 0
+        self.width = self.height = 0
+        self._set_image(max(1, max_width), max(1, max_height))
+        self._set_capacity(max(1, capacity))
+        self.scene_s = gsmi.make_scene(n, self.deg, *self.params)
+        self.grads_s = gsmi.make_scene(n, self.deg, *self.grads)
+        self.proj_s = gsmi.make_proj(self.radius, self.tiles, self.rect, self.depth, self.mean2d, self.conic,
+                                     self.rgb, self.clamp)
+        self.adam_arr = gsmi.make_adam_groups([(p, g, m, v, d, lr) for p, g, m, v, d in
+                                               zip(self.params, self.grads, self.m, self.v, self.delta)])
+        self.delta_arr = gsmi.make_groups(self.delta)
+        self.replica_arr = gsmi.make_groups(self.replica) if with_replica else None
+        self.msg = torch.zeros((gsmi.gs_delta_msg_bytes(n, self.row_len, 5) + 15) // 16 * 4, dtype=torch.int32,
+                               device=self.dev)
+
+    # -- buffers -------------------------------------------------------------
+    def _set_image(self, w, h):
+        if w <= self.width and h <= self.height:
+            return
+        self.width, self.height = max(w, self.width), max(h, self.height)
+        w, h = self.width, self.height
+        T = ((w + 15) // 16) * ((h + 15) // 16)
+        self.img = torch.zeros(3, h, w, device=self.dev)
+        self.final_T = torch.zeros(h, w, device=self.dev)
+        self.n_contrib = torch.zeros(h * w, dtype=torch.int32, device=self.dev)
+        self.dL = torch.zeros(3, h, w, device=self.dev)
+        self.target = torch.zeros(3, h, w, device=self.dev)
+        self.ranges = _u32(2 * T, self.dev)
+        self.ws_loss = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_LOSS, 0, 0, w, h), dtype=torch.uint8,
+                                   device=self.dev)
+        if self.capacity:
+            self._set_capacity(self.capacity, force=True)
+
+    def _set_capacity(self, cap, force=False):
+        if cap <= self.capacity and not force:
+            return
+        self.capacity = int(cap)
+        self.vals = _u32(cap, self.dev)
+        self.keys = torch.zeros(max(1, cap), dtype=torch.int64, device=self.dev) if self.with_keys else None
+        self.ws_sort = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_BIN_SORT, self.n, cap, self.width,
+                                                           self.height), dtype=torch.uint8, device=self.dev)
+        self.ws_bwd = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_RASTER_BWD, self.n, cap), dtype=torch.uint8,
+                                  device=self.dev)
+
+    def _view(self, cam):
+        """Image tensors cropped to this camera (views of the max-size buffers)."""
+        w, h = cam.width, cam.height
+        self._set_image(w, h)
+        return w, h
+
+    # -- phases --------------------------------------------------------------
+    def project(self, cam):
+        self._view(cam)
+        self.cam_c = gsmi.make_camera(cam)
+        self.cam = cam
+        gsmi.gs_project(self.scene_s, self.cam_c, self.proj_s)
+
+    def visible(self):
+        gsmi.gs_visible_set(gsmi.GS_PRED_U32_NONZERO, self.tiles, self.n, self.vis_idx, self.counts[0:1], self.ws_vis)
+
+    def bin_sort(self):
+        w, h = self.cam.width, self.cam.height
+        gsmi.gs_bin_sort(self.proj_s, self.n, self.vis_idx, self.counts[0:1], w, h, self.capacity, self.vals,
+                         self.ranges, self.pair_offset, self.keys, self.counts[1:2], self.status, self.ws_sort)
+
+    def _img_views(self):
+        w, h = self.cam.width, self.cam.height
+        hw = w * h
+        img = self.img.view(-1)[:3 * hw]
+        fT = self.final_T.view(-1)[:hw]
+        nc = self.n_contrib[:hw]
+        dL = self.dL.view(-1)[:3 * hw]
+        tgt = self.target.view(-1)[:3 * hw]
+        return img, fT, nc, dL, tgt
+
+    def raster_fwd(self, bg=(0.0, 0.0, 0.0), active=True):
+        img, fT, nc, _, _ = self._img_views()
+        if active:
+            self.active.zero_()
+        gsmi.gs_raster_fwd(self.proj_s, self.n, self.vals, self.ranges, self.cam.width, self.cam.height, bg, img, fT,
+                           nc, self.active if active else None)
+
+    def set_target(self, target_np):
+        _, _, _, _, tgt = self._img_views()
+        tgt.copy_(torch.from_numpy(np.ascontiguousarray(target_np, np.float32).reshape(-1)))
+
+    def loss_l1(self):
+        img, _, _, dL, tgt = self._img_views()
+        gsmi.gs_loss_l1(img, tgt, self.cam.width, self.cam.height, self.loss, dL, self.ws_loss)
+
+    def set_dL(self, dL_np):
+        _, _, _, dL, _ = self._img_views()
+        dL.copy_(torch.from_numpy(np.ascontiguousarray(dL_np, np.float32).reshape(-1)))
+
+    def raster_bwd(self, bg=(0.0, 0.0, 0.0), grad2d=True):
+        _, fT, nc, dL, _ = self._img_views()
+        gsmi.gs_raster_bwd(self.scene_s, self.cam_c, self.proj_s, self.vals, self.ranges, self.pair_offset,
+                           self.vis_idx, self.counts[0:1], self.capacity, fT, nc, dL, bg, self.grads_s,
+                           self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
+
+    def active_set(self):
+        gsmi.gs_visible_set(gsmi.GS_PRED_U8_NONZERO, self.active, self.n, self.act_idx, self.counts[2:3], self.ws_vis)
+
+    def adam(self, step):
+        gsmi.gs_sparse_adam(self.adam_arr, 5, self.vis_idx, self.counts[0:1], self.n, step, self.beta1, self.beta2,
+                            self.eps)
+
+    def pack(self, version):
+        gsmi.gs_delta_pack(self.vis_idx, self.counts[0:1], self.n, self.delta_arr, 5, version, self.msg, self.status)
+
+    def apply(self, mode=gsmi.GS_APPLY_ADD):
+        gsmi.gs_delta_apply(self.msg, self.replica_arr, 5, self.n, self.n, mode, self.version, self.status)
+
+    # -- whole view ----------------------------------------------------------
+    def step(self, cam, step, version=1, publish=True, active=False):
+        """Project, visible set, bin+sort, forward, L1, backward, Adam, pack + apply.
+        The target must already be in place (set_target)."""
+        self.project(cam)
+        self.visible()
+        self.bin_sort()
+        self.raster_fwd(active=active)
+        self.loss_l1()
+        self.raster_bwd(grad2d=False)
+        self.adam(step)
+        if publish:
+            self.pack(version)
+            self.apply()
+
+    def ensure_capacity(self, cams, margin=1.25):
+        """Size the pair buffers for the given cameras (synchronizes)."""
+        need = 0
+        for cam in cams:
+            self.project(cam)
+            self.visible()
+            self.status.zero_()
+            self.bin_sort()
+            torch.cuda.synchronize()
+            need = max(need, int(to_u32(self.counts[1:2])[0]))
+        if need > self.capacity:
+            self._set_capacity(int(need * margin) + 1024)
+        return need
+
+    def host_status(self):
+        return to_u32(self.status)

@@ -141,19 +141,34 @@ def _camera_from_pose(R, eye, width, height, fov_x_deg) -> Camera:
                   R=R.astype(np.float32), t=t.astype(np.float32), campos=eye.astype(np.float32))
 
 
+def normals(rng, shape, dtype=np.float32) -> np.ndarray:
+    """Seeded standard normal samples of the given shape and dtype."""
+    if dtype == np.float32:
+        return rng.standard_normal(shape, dtype=np.float32)
+    return rng.standard_normal(shape)
+
+
 def random_quats(rng, n) -> np.ndarray:
-    q = rng.standard_normal((n, 4))
+    q = normals(rng, (n, 4), np.float64)
     q /= np.sqrt((q * q).sum(axis=1, keepdims=True))
     return q.astype(np.float32)
 
 
 def _finish(rng, mean, ls_mu, ls_sd, logit_sd, logit_mu, degree, dc_kind) -> Scene:
     n = mean.shape[0]
-    log_scale = rng.standard_normal((n, 3), dtype=np.float32) * np.float32(ls_sd) + np.float32(ls_mu)
+    log_scale = normals(rng, (n, 3))
+    log_scale *= np.float32(ls_sd)
+    log_scale += np.float32(ls_mu)
     quat = random_quats(rng, n)
-    opacity = rng.standard_normal(n, dtype=np.float32) * np.float32(logit_sd) + np.float32(logit_mu)
+    opacity = normals(rng, (n,))
+    opacity *= np.float32(logit_sd)
+    opacity += np.float32(logit_mu)
     k = (degree + 1) ** 2
+    # draw every coefficient N(0, 0.05) in place, then overwrite the DC term
     sh = np.empty((n, k, 3), np.float32)
+    if k > 1:
+        rng.standard_normal(dtype=np.float32, out=sh.reshape(-1))
+        sh *= np.float32(0.05)
     if dc_kind == "rgb":
         # The colour itself is drawn U(0,1); the degree-0 coefficient that
         # yields it is (rgb - 0.5) / Y00 with the constant basis value
@@ -162,9 +177,7 @@ def _finish(rng, mean, ls_mu, ls_sd, logit_sd, logit_mu, degree, dc_kind) -> Sce
         sh[:, 0, :] = ((rgb - 0.5) * (2.0 * math.sqrt(math.pi))).astype(np.float32)
     else:
         sh[:, 0, :] = rng.random((n, 3), dtype=np.float32)
-    if k > 1:
-        sh[:, 1:, :] = rng.standard_normal((n, k - 1, 3), dtype=np.float32) * np.float32(0.05)
-    return Scene(mean=mean.astype(np.float32), log_scale=log_scale, quat=quat,
+    return Scene(mean=np.ascontiguousarray(mean, dtype=np.float32), log_scale=log_scale, quat=quat,
                  opacity=opacity, sh=sh, sh_degree=degree)
 
 
@@ -217,7 +230,7 @@ def ring(seed: int = 1, n: int = 200_000, width: int = 1280, height: int = 720) 
     rng = np.random.default_rng(seed)
     centres = rng.uniform(-3.0, 3.0, (20, 3))
     which = rng.integers(0, 20, n)
-    mean = centres[which] + rng.normal(0.0, 0.3, (n, 3))
+    mean = centres[which] + 0.3 * normals(rng, (n, 3), np.float64)
     scene = _finish(rng, mean, -4.5, 0.7, 1.5, 0.0, 3, "coef")
     cams = []
     for i in range(8):
@@ -235,7 +248,7 @@ def room(seed: int = 2, n: int = 1_000_000, width: int = 1920, height: int = 108
     uni = rng.uniform(lo, hi, (n_uni, 3))
     centres = rng.uniform(lo, hi, (50, 3))
     which = rng.integers(0, 50, n - n_uni)
-    clu = centres[which] + rng.normal(0.0, 0.25, (n - n_uni, 3))
+    clu = centres[which] + 0.25 * normals(rng, (n - n_uni, 3), np.float64)
     mean = np.concatenate([uni, clu], axis=0)
     scene = _finish(rng, mean, -5.0, 0.8, 1.5, 0.0, 3, "coef")
     cams = []
@@ -253,7 +266,7 @@ def spiral(seed: int = 3, n: int = 3_000_000, width: int = 1600, height: int = 1
     rots = np.stack([_rand_rot(rng) for _ in range(k)])
     lam = rng.uniform(0.05, 2.0, (k, 3))
     which = rng.integers(0, k, n)
-    z = rng.standard_normal((n, 3)) * np.sqrt(lam[which])
+    z = normals(rng, (n, 3), np.float64) * np.sqrt(lam[which])
     mean = centres[which] + np.einsum("nij,nj->ni", rots[which], z)
     scene = _finish(rng, mean, -5.5, 1.0, 2.0, -0.5, 3, "coef")
     cams = []
@@ -272,10 +285,10 @@ def spiral(seed: int = 3, n: int = 3_000_000, width: int = 1600, height: int = 1
 def aerial(seed: int = 4, n: int = 10_000_000, width: int = 1920, height: int = 1080) -> Workload:
     """One GPU's shard of an aerial city scene: 10M Gaussians, lawn-mower path of 128 cameras."""
     rng = np.random.default_rng(seed)
-    mean = np.empty((n, 3))
-    mean[:, 0] = rng.uniform(-500.0, 500.0, n)
-    mean[:, 1] = rng.uniform(-500.0, 500.0, n)
-    mean[:, 2] = np.abs(rng.normal(0.0, 20.0, n))
+    mean = np.empty((n, 3), np.float32)
+    mean[:, 0] = rng.random(n, dtype=np.float32) * np.float32(1000.0) - np.float32(500.0)
+    mean[:, 1] = rng.random(n, dtype=np.float32) * np.float32(1000.0) - np.float32(500.0)
+    mean[:, 2] = np.abs(normals(rng, (n,)) * np.float32(20.0))
     scene = _finish(rng, mean, -3.0, 1.2, 2.0, 0.0, 3, "coef")
     cams = []
     c45 = math.cos(math.radians(45.0))

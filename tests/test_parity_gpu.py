@@ -1,0 +1,313 @@
+"""GPU parity: every C-ABI entry point against the CPU oracle on the same
+seeded inputs (run on an MI355X; `-m gpu`).
+
+Small cases span several tiles and ragged tails (image sides that are not
+multiples of 16); the full-size cases are the five workloads in the exact
+launch configuration the benchmark times.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from parity_util import assert_grads, assert_pixels
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU parity tests need an MI355X"
+    return torch
+
+
+def small_cases():
+    from paper_2607_19893_amd import scenes
+    return {
+        "tiny-10k-256": lambda: scenes.tiny(),
+        "ring-20k-328x184": lambda: scenes.ring(n=20000, width=328, height=184),
+        "room-60k-392x216": lambda: scenes.room(n=60000, width=392, height=216),
+    }
+
+
+CASES = list(small_cases().keys())
+_CACHE = {}
+
+
+def get_case(name):
+    if name not in _CACHE:
+        _CACHE[name] = small_cases()[name]()
+    return _CACHE[name]
+
+
+def trainer_for(w, torch_gpu, capacity=None):
+    from paper_2607_19893_amd.pipeline import ViewTrainer
+    cam = w.cameras[0]
+    tr = ViewTrainer(w.scene, capacity=capacity or 1, max_width=max(c.width for c in w.cameras),
+                     max_height=max(c.height for c in w.cameras), with_keys=True)
+    if capacity is None:
+        tr.ensure_capacity(w.cameras[:2])
+    return tr
+
+
+def u32(t):
+    from paper_2607_19893_amd.pipeline import to_u32
+    return to_u32(t)
+
+
+# ---------------------------------------------------------------------------
+# stage by stage
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case", CASES)
+def test_project_visible_sort(case, torch_gpu, orc):
+    w = get_case(case)
+    _say("case", case, "n", w.scene.n)
+    tr = trainer_for(w, torch_gpu)
+    for vi, cam in enumerate(w.cameras[:2]):
+        tr.status.zero_()
+        tr.project(cam)
+        tr.visible()
+        tr.bin_sort()
+        torch_gpu.cuda.synchronize()
+        assert u32(tr.status)[0] == 0
+        ref = orc.project(w.scene, cam, 0)
+        n = w.scene.n
+        rad = tr.radius.cpu().numpy()[:n]
+        tiles = u32(tr.tiles)[:n]
+        np.testing.assert_array_equal(rad, ref.radius)
+        np.testing.assert_array_equal(tiles, ref.tiles)
+        vis_ref = orc.visible(ref.tiles)
+        V = int(u32(tr.counts[0:1])[0])
+        vis = u32(tr.vis_idx)[:V]
+        np.testing.assert_array_equal(vis, vis_ref)
+        rect = tr.rect.cpu().numpy().view(np.uint16)[:n]
+        np.testing.assert_array_equal(rect[vis].astype(np.int32), ref.rect[vis])
+        np.testing.assert_array_equal(tr.depth.cpu().numpy()[vis].view(np.uint32), ref.depth[vis].view(np.uint32))
+        np.testing.assert_array_equal(tr.mean2d.cpu().numpy()[vis].view(np.uint32), ref.mean2d_f32[vis].view(np.uint32))
+        co = tr.conic.cpu().numpy()[vis]
+        np.testing.assert_array_equal(co[:, :3].view(np.uint32), ref.conic_f32[vis].view(np.uint32))
+        np.testing.assert_allclose(co[:, 3], ref.opacity[vis], rtol=2e-6, atol=1e-7)
+        rgb = tr.rgb.cpu().numpy()[vis]
+        np.testing.assert_allclose(rgb, ref.rgb[vis], rtol=1e-5, atol=2e-6)
+        cl = tr.clamp.cpu().numpy()[vis]
+        sure = ref.clamp_margin[vis] > 1e-5
+        np.testing.assert_array_equal(cl[sure], ref.clamp[vis][sure])
+        # sorted pairs
+        keys_ref, vals_ref, ranges_ref = orc.sorted_pairs(vis_ref, ref, cam)
+        M = int(u32(tr.counts[1:2])[0])
+        assert M == keys_ref.size
+        np.testing.assert_array_equal(u32(tr.vals)[:M], vals_ref)
+        np.testing.assert_array_equal(tr.keys.cpu().numpy()[:M].view(np.uint64), keys_ref)
+        T = cam.num_tiles
+        np.testing.assert_array_equal(u32(tr.ranges)[:2 * T].reshape(T, 2), ranges_ref)
+        # emission offsets: exclusive sums of tiles in (depth bits, id) order
+        order = vis_ref[np.lexsort((vis_ref, ref.depth[vis_ref].view(np.uint32)))]
+        offs = np.concatenate([[0], np.cumsum(ref.tiles[order].astype(np.int64))[:-1]])
+        np.testing.assert_array_equal(u32(tr.pair_offset)[order], offs)
+        _say(case, "view", vi, "V", V, "M", M, "ok")
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_raster_forward(case, torch_gpu, orc):
+    w = get_case(case)
+    tr = trainer_for(w, torch_gpu)
+    cam = w.cameras[0]
+    tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd(active=True)
+    torch_gpu.cuda.synchronize()
+    ref = orc.project(w.scene, cam, 0)
+    vis = orc.visible(ref.tiles)
+    rn = orc.render(vis, ref, cam)
+    H, W = cam.height, cam.width
+    img = tr.img.view(-1)[:3 * H * W].cpu().numpy().reshape(3, H, W)
+    amb = (rn.margin_alpha < orc.AMB_ALPHA) | (rn.margin_T < orc.AMB_T)
+    ok = ~amb
+    frac = amb.mean()
+    _say(case, "ambiguous pixels", int(amb.sum()), "of", amb.size)
+    assert frac < 2e-3
+    assert_pixels(img, rn.img, np.broadcast_to(ok, img.shape), "img")
+    fT = tr.final_T.view(-1)[:H * W].cpu().numpy().reshape(H, W)
+    assert_pixels(fT, rn.T_final, ok, "final_T")
+    nc = u32(tr.n_contrib)[:H * W].reshape(H, W)
+    np.testing.assert_array_equal(nc[ok], rn.n_contrib[ok])
+    act = tr.active.cpu().numpy()[:w.scene.n]
+    diff = np.flatnonzero(act != rn.active)
+    assert diff.size <= max(2, int(amb.sum())), diff[:10]
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_loss_l1(case, torch_gpu, orc):
+    w = get_case(case)
+    tr = trainer_for(w, torch_gpu)
+    cam = w.cameras[0]
+    tgt = w.target(0)
+    tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd()
+    tr.set_target(tgt)
+    tr.loss_l1()
+    torch_gpu.cuda.synchronize()
+    H, W = cam.height, cam.width
+    img = tr.img.view(-1)[:3 * H * W].cpu().numpy().reshape(3, H, W)
+    loss, g, _ = orc.loss_l1(img, tgt)
+    dL = tr.dL.view(-1)[:3 * H * W].cpu().numpy().reshape(3, H, W)
+    np.testing.assert_array_equal(dL, g.astype(np.float32))
+    assert abs(tr.loss.item() - loss) <= 1e-5 * abs(loss)
+
+
+def _bwd_compare(w, tr, cam, orc, dL, case, check_flags=True):
+    ref = orc.project(w.scene, cam, 0)
+    vis = orc.visible(ref.tiles)
+    g2, flag = orc.render_backward(vis, ref, cam, dL)
+    gr = orc.project_backward(w.scene, cam, vis, g2, ref)
+    ok = np.zeros(w.scene.n, bool)
+    ok[vis] = True
+    ok &= flag == 0
+    ok &= ref.clamp_margin > 1e-5
+    ok &= ref.jclamp_margin > 1e-5
+    nflag = int((flag[vis] != 0).sum())
+    _say(case, "flagged primitives", nflag, "of", vis.size)
+    if check_flags:
+        assert nflag <= 0.2 * vis.size
+    g2_gpu = tr.grad2d.cpu().numpy()[:w.scene.n]
+    stats = {}
+    names = ["du", "dv", "dA", "dB", "dC", "dop", "dr", "dg", "db"]
+    for c, nm in enumerate(names):
+        stats[nm] = assert_grads(g2_gpu[:, c], g2[:, c], ok, "grad2d." + nm)
+    for name, gp, go in zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.grads, gr.groups()):
+        stats[name] = assert_grads(gp.cpu().numpy(), go, ok, "grad." + name)
+    gn = tr.grad_norm.cpu().numpy()[:w.scene.n]
+    stats["grad_norm"] = assert_grads(gn, gr.grad_norm, ok, "grad_norm")
+    _say(case, {k: (round(v.get("max_rel", 0), 6), round(v.get("norm_rel", 0), 8)) for k, v in stats.items()})
+    return vis, ok, gr
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_raster_backward(case, torch_gpu, orc):
+    from paper_2607_19893_amd import scenes
+    w = get_case(case)
+    tr = trainer_for(w, torch_gpu)
+    cam = w.cameras[0]
+    dL = scenes.make_upstream_grad(cam.width, cam.height, 17)
+    tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd()
+    tr.set_dL(dL)
+    tr.raster_bwd(grad2d=True)
+    torch_gpu.cuda.synchronize()
+    _bwd_compare(w, tr, cam, orc, dL.astype(np.float64), case)
+
+
+def test_sparse_adam(torch_gpu, orc):
+    import torch
+    from paper_2607_19893_amd import gsmi, scenes
+    rng = np.random.default_rng(3)
+    n = 5000
+    cols = [3, 3, 4, 1, 48]
+    p = [rng.standard_normal((n, c)).astype(np.float32) for c in cols]
+    g = [(rng.standard_normal((n, c)) * 1e-3).astype(np.float32) for c in cols]
+    mv = [scenes.adam_state(5, n, c) for c in cols]
+    idx = np.sort(rng.choice(n, 1234, replace=False)).astype(np.uint32)
+    dev = torch.device("cuda")
+    P = [torch.from_numpy(a).to(dev) for a in p]
+    G = [torch.from_numpy(a).to(dev) for a in g]
+    M = [torch.from_numpy(a[0]).to(dev) for a in mv]
+    Vv = [torch.from_numpy(a[1]).to(dev) for a in mv]
+    D = [torch.zeros(n, c, device=dev) for c in cols]
+    lrs = [1e-3, 2e-3, 1e-3, 5e-2, 2.5e-3]
+    arr = gsmi.make_adam_groups([(a, b, c, d, e, lr) for a, b, c, d, e, lr in zip(P, G, M, Vv, D, lrs)])
+    I = torch.from_numpy(idx.view(np.int32)).to(dev)
+    cnt = torch.tensor([idx.size], dtype=torch.int32, device=dev)
+    for step in (1, 7):
+        gsmi.gs_sparse_adam(arr, 5, I, cnt, n, step, 0.9, 0.999, 1e-15)
+        torch.cuda.synchronize()
+        for k in range(5):
+            pr, mr, vr, dr = orc.adam(p[k], g[k], mv[k][0], mv[k][1], idx, step, lrs[k], 0.9, 0.999, 1e-15)
+            rows = np.zeros(n, bool); rows[idx] = True
+            gp = P[k].cpu().numpy()
+            np.testing.assert_array_equal(gp[~rows], p[k][~rows])        # untouched rows
+            assert_grads(M[k].cpu().numpy(), mr, rows, "m%d" % k, rtol=1e-5)
+            assert_grads(Vv[k].cpu().numpy(), vr, rows, "v%d" % k, rtol=1e-5)
+            assert_grads(D[k].cpu().numpy()[idx], dr, np.ones(idx.size, bool), "delta%d" % k, rtol=2e-5)
+            assert_grads(gp, pr, rows, "p%d" % k, rtol=1e-6)
+            p[k], mv[k] = pr.astype(np.float32), (mr.astype(np.float32), vr.astype(np.float32))
+            P[k].copy_(torch.from_numpy(p[k])); M[k].copy_(torch.from_numpy(mv[k][0]))
+            Vv[k].copy_(torch.from_numpy(mv[k][1]))
+
+
+def test_delta_pack_apply(torch_gpu, orc):
+    import torch
+    from paper_2607_19893_amd import gsmi
+    rng = np.random.default_rng(4)
+    dev = torch.device("cuda")
+    for n, K, cols in ((1000, 333, [3, 3, 4, 1, 48]), (64, 0, [3, 3, 4, 1, 3]), (70000, 70000, [3, 3, 4, 1, 48])):
+        src = [rng.standard_normal((n, c)).astype(np.float32) for c in cols]
+        dst0 = [rng.standard_normal((n, c)).astype(np.float32) for c in cols]
+        idx = np.sort(rng.choice(n, K, replace=False)).astype(np.uint32)
+        S = [torch.from_numpy(a).to(dev) for a in src]
+        I = torch.from_numpy(idx.view(np.int32).copy() if K else np.zeros(1, np.int32)).to(dev)
+        cnt = torch.tensor([K], dtype=torch.int32, device=dev)
+        nbytes = gsmi.gs_delta_msg_bytes(K, sum(cols), len(cols))
+        msg = torch.zeros((nbytes + 15) // 4, dtype=torch.int32, device=dev)
+        st = torch.zeros(4, dtype=torch.int32, device=dev)
+        gsmi.gs_delta_pack(I, cnt, n, gsmi.make_groups(S), len(cols), 5, msg, st)
+        torch.cuda.synchronize()
+        assert st.cpu().numpy()[0] == 0
+        ref = orc.delta_pack(idx, src, 5)
+        got = msg.cpu().numpy().view(np.uint32)[:ref.size]
+        np.testing.assert_array_equal(got, ref)
+        for mode, name in ((gsmi.GS_APPLY_ADD, "add"), (gsmi.GS_APPLY_OVERWRITE, "overwrite")):
+            Dd = [torch.from_numpy(a.copy()).to(dev) for a in dst0]
+            ver = torch.zeros(n, dtype=torch.int32, device=dev)
+            gsmi.gs_delta_apply(msg, gsmi.make_groups(Dd), len(cols), n, n, mode, ver, st)
+            torch.cuda.synchronize()
+            out, vref = orc.delta_apply(ref, dst0, name, np.zeros(n, np.uint32))
+            for a, b in zip(Dd, out):
+                np.testing.assert_array_equal(a.cpu().numpy().view(np.uint32), b.view(np.uint32))
+            np.testing.assert_array_equal(ver.cpu().numpy().view(np.uint32), vref)
+    # overflow: capacity too small -> flag + required bytes, no header written
+    msg = torch.zeros(16, dtype=torch.int32, device=dev)
+    st = torch.zeros(4, dtype=torch.int32, device=dev)
+    gsmi.gs_delta_pack(I, cnt, n, gsmi.make_groups(S), len(cols), 5, msg, st)
+    torch.cuda.synchronize()
+    s = st.cpu().numpy().view(np.uint32)
+    assert s[0] & gsmi.GS_DEV_MSG_OVERFLOW and s[1] == gsmi.gs_delta_msg_bytes(K, sum(cols), len(cols))
+    # mismatch: a destination with different widths is refused and left untouched
+    good = torch.zeros((gsmi.gs_delta_msg_bytes(K, sum(cols), len(cols)) + 15) // 4, dtype=torch.int32, device=dev)
+    st.zero_()
+    gsmi.gs_delta_pack(I, cnt, n, gsmi.make_groups(S), len(cols), 5, good, st)
+    wrong = [torch.zeros(n, c, device=dev) for c in (3, 3, 4, 1, 45)]
+    gsmi.gs_delta_apply(good, gsmi.make_groups(wrong), 5, n, n, gsmi.GS_APPLY_ADD, None, st)
+    torch.cuda.synchronize()
+    assert st.cpu().numpy()[0] & gsmi.GS_DEV_MSG_MISMATCH
+    assert all(float(t.abs().sum()) == 0.0 for t in wrong)
+
+
+def test_pair_overflow_flag(torch_gpu, orc):
+    """Capacity below the pair count: the flag and the required count are set."""
+    w = get_case("tiny-10k-256")
+    tr = trainer_for(w, torch_gpu, capacity=1000)
+    tr.status.zero_()
+    tr.project(w.cameras[0]); tr.visible(); tr.bin_sort()
+    torch_gpu.cuda.synchronize()
+    s = u32(tr.status)
+    M = int(u32(tr.counts[1:2])[0])
+    assert s[0] & 1 and s[1] == M and M > 1000
+    assert np.all(u32(tr.ranges) == 0)
+
+
+def test_empty_and_degenerate(torch_gpu, orc):
+    """All primitives behind the camera: empty visible set, empty image."""
+    from paper_2607_19893_amd import scenes
+    w = scenes.tiny(n=500)
+    w.scene.mean[:, 2] = -10.0
+    tr = trainer_for(w, torch_gpu, capacity=1024)
+    tr.set_target(w.target(0))
+    tr.step(w.cameras[0], step=1)
+    torch_gpu.cuda.synchronize()
+    assert int(u32(tr.counts[0:1])[0]) == 0 and int(u32(tr.counts[1:2])[0]) == 0
+    hw = w.cameras[0].width * w.cameras[0].height
+    assert float(tr.img.view(-1)[:3 * hw].abs().max()) == 0.0
+    assert float(tr.final_T.view(-1)[:hw].min()) == 1.0
