@@ -1,0 +1,207 @@
+"""Throughput of the one-GPU 3DGS training-view hot path.
+
+A step is one training view through every phase: projection, visible-set
+extraction, tile binning + sort, forward raster, L1 loss, backward, sparse
+Adam over the visible rows, and pack + apply of the Adam deltas into a
+replica (the pending-update publication).  The workload is the 1M-Gaussian
+SH-degree-3 room scene with 32 forward-facing 1920x1080 cameras; steps cycle
+through the cameras.  Inputs (scene, Adam state, all 32 targets) are resident
+in HBM before the timed region.
+
+Prints one JSON line (the driver's contract) with a roofline entry for the
+dominant kernel (timed with HIP events on the stream it runs on) and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+FP32_PEAK_TFLOPS = 157.3       # MI355X vector FP32 (packed), TFLOP/s
+
+# Algorithmic work per unit (see the design notes for the derivation).
+FWD_FLOP_EVAL = 13.0           # per evaluated (pixel, pair): offsets, quadratic form, exp, alpha
+FWD_FLOP_INC = 9.0             # per included pair: transmittance update + colour accumulation
+BWD_FLOP_EVAL = 13.0           # per replayed (pixel, pair): alpha recomputation
+BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/dalpha, 9 partials + their sum
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="room")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-views", type=int, default=2, help="views of the CPU oracle sample")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (collectives and sharding are "
+              "out of scope); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_19893_amd import scenes
+    from paper_2607_19893_amd.pipeline import ViewTrainer, to_u32
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    w = scenes.workload(args.workload)
+    cams = w.cameras
+    log("workload %s: n=%d, %d views, %dx%d (generated in %.1fs)" % (w.name, w.scene.n, len(cams), cams[0].width,
+                                                                     cams[0].height, time.time() - t0))
+    tr = ViewTrainer(w.scene, capacity=1, max_width=max(c.width for c in cams),
+                     max_height=max(c.height for c in cams), lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps)
+    need = tr.ensure_capacity(cams)
+    log("pair capacity %d (max pairs over the views %d)" % (tr.capacity, need))
+    t0 = time.time()
+    targets = []
+    for i, c in enumerate(cams):
+        tg = torch.from_numpy(w.target(i).reshape(-1)).to(tr.dev)
+        targets.append(tg)
+    log("targets resident (%.1fs)" % (time.time() - t0))
+
+    # pair statistics per view (untimed): evaluated / included (pixel, pair) counts
+    ev_pairs, inc_pairs, vis_counts, pair_counts = [], [], [], []
+    for i, c in enumerate(cams):
+        tr.project(c); tr.visible(); tr.bin_sort()
+        tr.pair_stats.zero_()
+        tr.raster_fwd(active=False, stats=True)
+        torch.cuda.synchronize()
+        st = tr.pair_stats.cpu().numpy()
+        ev_pairs.append(int(st[0])); inc_pairs.append(int(st[1]))
+        vis_counts.append(int(to_u32(tr.counts[0:1])[0])); pair_counts.append(int(to_u32(tr.counts[1:2])[0]))
+
+    step = 0
+    nviews = len(cams)
+    for k in range(args.warmup):
+        step += 1
+        tr.step(cams[k % nviews], step, version=step, target=targets[k % nviews])
+    torch.cuda.synchronize()
+    assert to_u32(tr.status)[0] == 0, "device status flags set during warm-up"
+
+    nph = len(ViewTrainer.PHASES)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)] for _ in range(args.steps)]
+    views = []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        step += 1
+        v = (args.warmup + k) % nviews
+        views.append(v)
+        tr.step(cams[v], step, version=step, target=targets[v], events=evs[k])
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    wall = t_end - t_start
+    assert to_u32(tr.status)[0] == 0, "device status flags set during the timed steps"
+
+    phase_ms = np.zeros(nph)
+    for k in range(args.steps):
+        for p in range(nph):
+            phase_ms[p] += evs[k][p].elapsed_time(evs[k][p + 1])
+    phase_ms /= args.steps
+    log("per-phase ms: " + ", ".join("%s %.3f" % (n, t) for n, t in zip(ViewTrainer.PHASES, phase_ms)))
+
+    ms_per_step = 1e3 * wall / args.steps
+    value = args.steps / wall
+    ev_mean = float(np.mean([ev_pairs[v] for v in views]))
+    inc_mean = float(np.mean([inc_pairs[v] for v in views]))
+    V_mean = float(np.mean([vis_counts[v] for v in views]))
+    M_mean = float(np.mean([pair_counts[v] for v in views]))
+    row_bytes = 4 * tr.row_len
+
+    # roofline of each timed phase; the dominant one is reported
+    names = list(ViewTrainer.PHASES)
+    fwd_flops = FWD_FLOP_EVAL * ev_mean + FWD_FLOP_INC * inc_mean
+    bwd_flops = BWD_FLOP_EVAL * ev_mean + BWD_FLOP_INC * inc_mean
+    adam_bytes = V_mean * row_bytes * 7 + 4 * V_mean            # p g m v read; p m v write; ids
+    adam_bytes_delta = adam_bytes + V_mean * row_bytes           # + delta write
+    pack_bytes = 2 * V_mean * (4 + row_bytes) + 4 * V_mean
+    apply_bytes = V_mean * (4 + row_bytes) + 2 * V_mean * row_bytes + 4 * V_mean
+    roofs = {
+        "raster_fwd": ("alu", fwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
+        "raster_bwd": ("alu", bwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
+        "adam": ("hbm", adam_bytes_delta / 1e9, HBM_PEAK_GBS, "GB/s"),
+        "pack": ("hbm", pack_bytes / 1e9, HBM_PEAK_GBS, "GB/s"),
+        "apply": ("hbm", apply_bytes / 1e9, HBM_PEAK_GBS, "GB/s"),
+    }
+    per_phase = {}
+    for name, t in zip(names, phase_ms):
+        if name in roofs:
+            bound, work, peak, unit = roofs[name]
+            ach = work / (t * 1e-3)
+            per_phase[name] = {"ms": round(float(t), 4), "bound": bound, "achieved": round(ach, 2), "peak": peak,
+                               "unit": unit, "frac": round(ach / peak, 4)}
+        else:
+            per_phase[name] = {"ms": round(float(t), 4)}
+    dom = max(roofs, key=lambda n: phase_ms[names.index(n)])
+    bound, work, peak, unit = roofs[dom]
+    ach = work / (phase_ms[names.index(dom)] * 1e-3)
+    roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
+                "frac": round(ach / peak, 5), "traffic": None}
+    log("phase rooflines: " + json.dumps(per_phase))
+    log("mean per view: V=%.0f M=%.0f evaluated=%.3g included=%.3g" % (V_mean, M_mean, ev_mean, inc_mean))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, args.cpu_views)
+
+    out = {
+        "metric": "train views/sec (fwd+bwd+sparse Adam), 1M Gaussians 1080p",
+        "value": round(value, 3),
+        "unit": "views/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "gaussians": w.scene.n, "sh_degree": w.scene.sh_degree,
+                   "width": cams[0].width, "height": cams[0].height, "views": nviews,
+                   "mean_visible": round(V_mean), "mean_pairs": round(M_mean),
+                   "step": "project+visible+bin_sort+fwd+L1+bwd+sparse_adam+delta_pack+delta_apply"},
+        "roofline": roofline,
+        "phases_ms": {k: v["ms"] for k, v in per_phase.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, nviews):
+    """The CPU oracle, as it stands, on `nviews` full views of the same workload."""
+    import oracle
+    t0 = time.perf_counter()
+    done = 0
+    m = [np.zeros_like(a) for _, a in w.scene.groups()]
+    v = [np.zeros_like(a) for _, a in w.scene.groups()]
+    for i in range(nviews):
+        cam = w.cameras[i % len(w.cameras)]
+        oracle.train_view(w.scene, cam, w.target(i), m, v, i + 1, lr=w.lr, with_pairs=False)
+        done += 1
+    dt = time.perf_counter() - t0
+    return {"value": round(done / dt, 4), "unit": "views/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "%d full views (%s, %dx%d) through the oracle's projection, per-pixel render, L1, exact "
+                      "backward, Adam and pack; %.1f s" % (done, w.name, w.cameras[0].width,
+                                                            w.cameras[0].height, dt)}
+
+
+if __name__ == "__main__":
+    main()

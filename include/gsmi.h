@@ -208,11 +208,13 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
  *   range) of the last included pair, 0 if none
  *   active [n] uint8 or NULL: set to 1 for every primitive included in at least
  *   one pixel (never cleared: zero it before the call)
+ *   pair_stats [2] uint64 or NULL: += number of (pixel, pair) evaluations and
+ *   of included pairs (accumulated: zero it before the call)
  *   bg: 3 floats on the HOST
  */
 gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,
                         int32_t width, int32_t height, const float* bg, float* img, float* final_T,
-                        uint32_t* n_contrib, uint8_t* active, void* stream);
+                        uint32_t* n_contrib, uint8_t* active, uint64_t* pair_stats, void* stream);
 
 /*
  * Image loss (Section 2.1): L = mean over all 3*H*W entries of |img - target|;

@@ -241,6 +241,8 @@ def render_backward(vis, proj: Projection, cam, dL_dimg, bg=(0.0, 0.0, 0.0), los
 
 @dataclasses.dataclass
 class Grads:
+    """Parameter gradients of the visible rows only: row a belongs to primitive vis[a]."""
+    vis: np.ndarray
     mean: np.ndarray
     log_scale: np.ndarray
     quat: np.ndarray
@@ -249,17 +251,27 @@ class Grads:
     grad_norm: np.ndarray
 
     def groups(self):
-        n = self.mean.shape[0]
-        return [self.mean.reshape(n, 3), self.log_scale.reshape(n, 3), self.quat.reshape(n, 4),
-                self.opacity.reshape(n, 1), self.sh.reshape(n, -1)]
+        v = self.vis.size
+        return [self.mean.reshape(v, 3), self.log_scale.reshape(v, 3), self.quat.reshape(v, 4),
+                self.opacity.reshape(v, 1), self.sh.reshape(v, -1)]
+
+    def full(self, n):
+        """Scatter into [n, cols] arrays (zeros elsewhere)."""
+        out = []
+        for g in self.groups():
+            a = np.zeros((n, g.shape[1]))
+            a[self.vis.astype(np.int64)] = g
+            out.append(a)
+        return out
 
 
 def project_backward(scene, cam, vis, grad2d, proj: Projection) -> Grads:
     n, deg = scene.n, scene.sh_degree
     K = (deg + 1) ** 2
     vis = np.ascontiguousarray(vis, np.uint32)
-    g = Grads(mean=np.zeros((n, 3)), log_scale=np.zeros((n, 3)), quat=np.zeros((n, 4)), opacity=np.zeros(n),
-              sh=np.zeros((n, K, 3)), grad_norm=np.zeros(n))
+    v = vis.size
+    g = Grads(vis=vis, mean=np.zeros((v, 3)), log_scale=np.zeros((v, 3)), quat=np.zeros((v, 4)), opacity=np.zeros(v),
+              sh=np.zeros((v, K, 3)), grad_norm=np.zeros(v))
     cc = _cam(cam)
     lib().orc_project_backward(n, deg, _p(_f32(scene.mean)), _p(_f32(scene.log_scale)), _p(_f32(scene.quat)),
                                _p(_f32(scene.opacity)), _p(_f32(scene.sh)), ctypes.byref(cc), vis.size, _p(vis),
@@ -281,6 +293,23 @@ def loss_l1(img, target):
     return float(np.abs(d).mean()), (np.sign(d) * np.float64(inv)), d
 
 
+def adam_rows(p, g, m, v, step, lr, beta1=0.9, beta2=0.999, eps=1e-15):
+    """torch.optim.Adam update of the given rows (all fp64): returns (p, m, v, delta).
+
+    m <- b1 m + (1-b1) g ; v <- b2 v + (1-b2) g^2
+    delta = -(lr / (1 - b1^t)) * m / (sqrt(v) / sqrt(1 - b2^t) + eps) ; p <- p + delta
+    """
+    p, g, m, v = (np.asarray(a, np.float64) for a in (p, g, m, v))
+    m = beta1 * m + (1.0 - beta1) * g
+    v = beta2 * v + (1.0 - beta2) * g * g
+    bc1 = 1.0 - beta1 ** step
+    bc2 = 1.0 - beta2 ** step
+    if _MUT == 7:
+        bc1 = bc2 = 1.0
+    delta = -(lr / bc1) * m / (np.sqrt(v) / np.sqrt(bc2) + eps)
+    return p + delta, m, v, delta
+
+
 def adam(p, g, m, v, rows, step, lr, beta1=0.9, beta2=0.999, eps=1e-15):
     """torch.optim.Adam update of rows `rows` of one parameter group (fp64).
 
@@ -292,39 +321,40 @@ def adam(p, g, m, v, rows, step, lr, beta1=0.9, beta2=0.999, eps=1e-15):
     m = np.array(m, np.float64, copy=True)
     v = np.array(v, np.float64, copy=True)
     rows = np.asarray(rows, np.int64)
-    gr = np.asarray(g, np.float64)[rows]
-    m[rows] = beta1 * m[rows] + (1.0 - beta1) * gr
-    v[rows] = beta2 * v[rows] + (1.0 - beta2) * gr * gr
-    bc1 = 1.0 - beta1 ** step
-    bc2 = 1.0 - beta2 ** step
-    if _MUT == 7:
-        bc1 = bc2 = 1.0
-    delta = -(lr / bc1) * m[rows] / (np.sqrt(v[rows]) / np.sqrt(bc2) + eps)
-    p[rows] = p[rows] + delta
+    p[rows], m[rows], v[rows], delta = adam_rows(p[rows], np.asarray(g, np.float64)[rows], m[rows], v[rows], step,
+                                                 lr, beta1, beta2, eps)
     return p, m, v, delta
 
 
 MSG_MAGIC = 0x47534D31  # "GSM1"
 
 
-def delta_pack(idx, groups, version):
-    """Message = 8 header words (magic, count, version, row_len, n_groups, 0, 0, 0),
+def delta_message(idx, row_groups, version):
+    """Message for ids `idx` whose rows are given (row a of each group belongs to idx[a]).
+
+    Layout: 8 header words (magic, count, version, row_len, n_groups, 0, 0, 0),
     the group widths (padded with zeros to a multiple of 4 words), the K ids,
     zero padding to a 16-byte boundary, then K rows of row_len fp32 values
     (each row = the groups' rows concatenated in group order).
     """
     idx = np.asarray(idx, np.uint32)
-    cols = [int(a.shape[1]) for a in groups]
+    cols = [int(a.shape[1]) for a in row_groups]
     row_len = sum(cols)
     hdr = np.zeros(8, np.uint32)
-    hdr[0], hdr[1], hdr[2], hdr[3], hdr[4] = MSG_MAGIC, idx.size, version, row_len, len(groups)
-    colw = np.zeros(((len(groups) + 3) // 4) * 4, np.uint32)
-    colw[:len(groups)] = cols
-    rows = np.concatenate([np.asarray(a, np.float32)[idx.astype(np.int64)] for a in groups], axis=1) \
+    hdr[0], hdr[1], hdr[2], hdr[3], hdr[4] = MSG_MAGIC, idx.size, version, row_len, len(row_groups)
+    colw = np.zeros(((len(row_groups) + 3) // 4) * 4, np.uint32)
+    colw[:len(row_groups)] = cols
+    rows = np.concatenate([np.asarray(a, np.float32) for a in row_groups], axis=1) \
         if idx.size else np.zeros((0, row_len), np.float32)
     head = 8 + colw.size + idx.size
     pad = np.zeros((-head) % 4, np.uint32)
-    return np.concatenate([hdr, colw, idx, pad, rows.reshape(-1).view(np.uint32)])
+    return np.concatenate([hdr, colw, idx, pad, np.ascontiguousarray(rows).reshape(-1).view(np.uint32)])
+
+
+def delta_pack(idx, groups, version):
+    """Gather rows `idx` of full [n, cols] groups into one message (see delta_message)."""
+    idx = np.asarray(idx, np.uint32)
+    return delta_message(idx, [np.asarray(a, np.float32)[idx.astype(np.int64)] for a in groups], version)
 
 
 def delta_apply(msg, groups, mode, version_arr=None):
@@ -373,7 +403,7 @@ class ViewResult:
     grad2d: np.ndarray
     flag: np.ndarray
     grads: Grads
-    new_params: list
+    new_params: list      # visible rows only (row a = primitive vis[a]), fp64
     new_m: list
     new_v: list
     deltas: list
@@ -416,20 +446,16 @@ def train_view(scene, cam, target, m_groups, v_groups, step, lr=1e-3, beta1=0.9,
     tm["project_backward"] = time.perf_counter() - t0
     t0 = time.perf_counter()
     params = [a for _, a in scene.groups()]
+    rows = vis.astype(np.int64)
     newp, newm, newv, deltas = [], [], [], []
     for p, g, m, v in zip(params, grads.groups(), m_groups, v_groups):
-        pn, mn, vn, d = adam(p, g, m, v, vis, step, lr, beta1, beta2, eps)
+        pn, mn, vn, d = adam_rows(p[rows], g, m[rows], v[rows], step, lr, beta1, beta2, eps)
         newp.append(pn); newm.append(mn); newv.append(vn); deltas.append(d)
     tm["adam"] = time.perf_counter() - t0
     msg = None
     if with_msg:
         t0 = time.perf_counter()
-        dfull = []
-        for p, d in zip(params, deltas):
-            a = np.zeros(p.shape, np.float32)
-            a[vis.astype(np.int64)] = d.astype(np.float32)
-            dfull.append(a)
-        msg = delta_pack(vis, dfull, version)
+        msg = delta_message(vis, [d.astype(np.float32) for d in deltas], version)
         tm["pack"] = time.perf_counter() - t0
     return ViewResult(proj, vis, keys, vals, ranges, rnd, loss, dL, lm, grad2d, flag, grads, newp, newm, newv,
                       deltas, msg, tm)

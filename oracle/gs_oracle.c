@@ -771,8 +771,10 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
 /* ------------------------------------------------------------------------ */
 
 /*
- * For each visible j: from grad2d[9*j] = (du, dv, dA, dB, dC, do, dr, dg, db)
- * to the parameter gradients.  The geometry is re-evaluated in fp64.
+ * For each visible j = vis[row]: from grad2d[9*j] = (du, dv, dA, dB, dC, do,
+ * dr, dg, db) to the parameter gradients, written to `row` of the compact
+ * outputs (dmean [nvis,3], dls [nvis,3], dquat [nvis,4], dlogit [nvis],
+ * dsh [nvis,K,3], grad_norm [nvis]).  The geometry is re-evaluated in fp64.
  *   opacity:  dlogit = do * o (1 - o)
  *   colour:   channels with the clamp bit carry no gradient; dsh[k][ch] = dc_ch Y_k(d);
  *             d(view dir) -> d(mean) through d = (mu - campos)/|mu - campos|
@@ -794,8 +796,8 @@ void orc_project_backward(int n, int deg, const float* mean, const float* ls, co
     const int K = (deg + 1) * (deg + 1);
     (void)n;
 #pragma omp parallel for schedule(static)
-    for (int64_t a = 0; a < nvis; ++a) {
-        const size_t j = vis[a];
+    for (int64_t row = 0; row < nvis; ++row) {
+        const size_t j = vis[row];
         const double* g2 = grad2d + 9 * j;
         double R[9];
         for (int i = 0; i < 9; ++i) R[i] = cam->R[i];
@@ -883,7 +885,7 @@ void orc_project_backward(int n, int deg, const float* mean, const float* ls, co
         for (int i = 0; i < 3; ++i) for (int k = 0; k < 3; ++k) gRq[i][k] = gM[i][k] * s[k];
         for (int k = 0; k < 3; ++k) {
             double gs = gM[0][k] * Rq[0][k] + gM[1][k] * Rq[1][k] + gM[2][k] * Rq[2][k];
-            dls[3 * j + k] = gs * s[k];
+            dls[3 * row + k] = gs * s[k];
         }
         double w = q[0], x = q[1], y = q[2], z = q[3];
         double gq[4];
@@ -895,10 +897,10 @@ void orc_project_backward(int n, int deg, const float* mean, const float* ls, co
         gq[3] = 2.0 * (-2.0 * z * gRq[0][0] - w * gRq[0][1] + x * gRq[0][2] + w * gRq[1][0] - 2.0 * z * gRq[1][1]
                        + y * gRq[1][2] + x * gRq[2][0] + y * gRq[2][1]);
         double qd = q[0] * gq[0] + q[1] * gq[1] + q[2] * gq[2] + q[3] * gq[3];
-        for (int k = 0; k < 4; ++k) dquat[4 * j + k] = (gq[k] - q[k] * qd) / nq;
+        for (int k = 0; k < 4; ++k) dquat[4 * row + k] = (gq[k] - q[k] * qd) / nq;
         /* opacity */
         double o = 1.0 / (1.0 + exp(-(double)logit[j]));
-        dlogit[j] = g2[5] * o * (1.0 - o);
+        dlogit[row] = g2[5] * o * (1.0 - o);
         /* colour */
         double dv[3], nrm = 0.0;
         for (int k = 0; k < 3; ++k) { dv[k] = mu[k] - (double)cam->campos[k]; nrm += dv[k] * dv[k]; }
@@ -910,7 +912,7 @@ void orc_project_backward(int n, int deg, const float* mean, const float* ls, co
         for (int ch = 0; ch < 3; ++ch) {
             double gc = (clamp[j] >> ch & 1) ? 0.0 : g2[6 + ch];
             for (int k = 0; k < K; ++k) {
-                dsh[(j * K + k) * 3 + ch] = gc * Y[k];
+                dsh[((size_t)row * K + k) * 3 + ch] = gc * Y[k];
                 double cf = sh[(j * K + k) * 3 + ch];
                 gd[0] += gc * cf * dY[k][0];
                 gd[1] += gc * cf * dY[k][1];
@@ -919,7 +921,7 @@ void orc_project_backward(int n, int deg, const float* mean, const float* ls, co
         }
         double dd = gd[0] * d[0] + gd[1] * d[1] + gd[2] * d[2];
         for (int k = 0; k < 3; ++k) gmu[k] += (gd[k] - d[k] * dd) / nrm;
-        for (int k = 0; k < 3; ++k) dmean[3 * j + k] = gmu[k];
-        grad_norm[j] = sqrt(g2[0] * g2[0] + g2[1] * g2[1]);
+        for (int k = 0; k < 3; ++k) dmean[3 * row + k] = gmu[k];
+        grad_norm[row] = sqrt(g2[0] * g2[0] + g2[1] * g2[1]);
     }
 }

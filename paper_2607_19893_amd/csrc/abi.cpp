@@ -146,15 +146,16 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
 
 gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges, int32_t width,
                         int32_t height, const float* bg, float* img, float* final_T, uint32_t* n_contrib,
-                        uint8_t* active, void* stream) {
+                        uint8_t* active, uint64_t* pair_stats, void* stream) {
     gs_status s;
     if ((s = check_proj(proj, false, "gs_raster_fwd")) != GS_OK) return s;
     GS_REQUIRE(n >= 0 && width >= 0 && height >= 0, "gs_raster_fwd: negative size");
     if (width > GS_MAX_IMAGE_SIDE || height > GS_MAX_IMAGE_SIDE)
         return fail(GS_ERR_UNSUPPORTED, "gs_raster_fwd: image side above %d", GS_MAX_IMAGE_SIDE);
     GS_REQUIRE(vals && ranges && bg && img && final_T && n_contrib, "gs_raster_fwd: null pointer");
+    GS_REQUIRE(pair_stats == nullptr || aligned(pair_stats, 8), "gs_raster_fwd: pair_stats misaligned");
     return hip_status(gsmi::launch_raster_fwd(*proj, vals, ranges, width, height, bg, img, final_T, n_contrib, active,
-                                              static_cast<hipStream_t>(stream)),
+                                              pair_stats, static_cast<hipStream_t>(stream)),
                       "gs_raster_fwd");
 }
 

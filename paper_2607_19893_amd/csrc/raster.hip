@@ -49,8 +49,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, float* __restrict__ img, float* __restrict__ final_T, uint32_t* __restrict__ n_contrib,
-    uint8_t* __restrict__ active) {
+    uint8_t* __restrict__ active, unsigned long long* __restrict__ pair_stats) {
     __shared__ float2 s_xy[GS_BLOCK];
+    __shared__ uint32_t s_stat[2][4];
     __shared__ float4 s_co[GS_BLOCK];
     __shared__ float s_rgb[3 * GS_BLOCK];
     __shared__ uint32_t s_id[GS_BLOCK];
@@ -63,7 +64,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const float fx = px + 0.5f, fy = py + 0.5f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
     float T = 1.0f, c0 = 0.0f, c1 = 0.0f, c2 = 0.0f;
-    uint32_t last = 0;
+    uint32_t last = 0, n_eval = 0, n_inc = 0;
     bool done = !inside;
     for (uint32_t bs = start; bs < end; bs += GS_BLOCK) {
         if (__syncthreads_count(done) == GS_BLOCK) break;
@@ -82,12 +83,14 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
         const int nb = (int)min((uint32_t)GS_BLOCK, end - bs);
         for (int k = 0; k < nb && !done; ++k) {
             const PairEval p = eval_pair(s_xy[k], s_co[k], fx, fy);
+            ++n_eval;
             if (p.sigma < 0.0f || p.alpha < kAlphaMin) continue;
             const float Tn = T * (1.0f - p.alpha);
             if (Tn < kTMin) {
                 done = true;
                 break;
             }
+            ++n_inc;
             const float wgt = p.alpha * T;
             c0 = fmaf(wgt, s_rgb[3 * k + 0], c0);
             c1 = fmaf(wgt, s_rgb[3 * k + 1], c1);
@@ -98,6 +101,18 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
         }
         __syncthreads();
         if (active && j < end && s_hit[tid]) active[s_id[tid]] = 1;
+    }
+    if (pair_stats) {
+        const uint32_t e = wave_sum_u32(n_eval), i = wave_sum_u32(n_inc);
+        if (lane_id() == 0) {
+            s_stat[0][tid / GS_WAVE] = e;
+            s_stat[1][tid / GS_WAVE] = i;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            atomicAdd(&pair_stats[0], (unsigned long long)s_stat[0][0] + s_stat[0][1] + s_stat[0][2] + s_stat[0][3]);
+            atomicAdd(&pair_stats[1], (unsigned long long)s_stat[1][0] + s_stat[1][1] + s_stat[1][2] + s_stat[1][3]);
+        }
     }
     if (inside) {
         const size_t HW = (size_t)W * H, p = (size_t)py * W + px;
@@ -500,12 +515,13 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
 
 hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
                              int32_t height, const float bg[3], float* img, float* final_T, uint32_t* n_contrib,
-                             uint8_t* active, hipStream_t st) {
+                             uint8_t* active, uint64_t* pair_stats, hipStream_t st) {
     const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
     if (TX * TY == 0) return hipSuccess;
     hipLaunchKernelGGL(k_raster_fwd, dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
                        reinterpret_cast<const float2*>(proj.mean2d), reinterpret_cast<const float4*>(proj.conic_opacity),
-                       proj.rgb, width, height, TX, bg[0], bg[1], bg[2], img, final_T, n_contrib, active);
+                       proj.rgb, width, height, TX, bg[0], bg[1], bg[2], img, final_T, n_contrib, active,
+                       reinterpret_cast<unsigned long long*>(pair_stats));
     return hipGetLastError();
 }
 

@@ -66,7 +66,7 @@ _lib.gs_delta_msg_bytes.argtypes = [u32, i32, i32]
 _lib.gs_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P]
 _lib.gs_visible_set.argtypes = [i32, P, i32, P, P, P, sz, P]
 _lib.gs_bin_sort.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, u32, P, P, P, P, P, P, P, sz, P]
-_lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, P, P, P, P, P]
+_lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, P, P, P, P, P, P]
 _lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
 _lib.gs_raster_bwd.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P, P, P,
                                P, P, u32, P, P, P, P, ctypes.POINTER(gs_scene), P, P, P, sz, P]
@@ -178,11 +178,11 @@ def _bg(bg):
 
 
 def gs_raster_fwd(proj: gs_proj, n, vals, ranges, width, height, bg, img, final_T, n_contrib, active=None,
-                  stream=None):
+                  pair_stats=None, stream=None):
     b = _bg(bg)
     return _check("gs_raster_fwd", _lib.gs_raster_fwd(ctypes.byref(proj), int(n), ptr(vals), ptr(ranges), int(width),
                                                       int(height), ctypes.cast(b, P), ptr(img), ptr(final_T),
-                                                      ptr(n_contrib), ptr(active),
+                                                      ptr(n_contrib), ptr(active), ptr(pair_stats),
                                                       stream if stream is not None else current_stream()))
 
 

@@ -62,6 +62,7 @@ class ViewTrainer:
         self.grad2d = torch.zeros(max(1, n), 9, device=self.dev)
         self.grad_norm = torch.zeros(max(1, n), device=self.dev)
         self.loss = torch.zeros(1, device=self.dev)
+        self.pair_stats = torch.zeros(2, dtype=torch.int64, device=self.dev)
         self.with_keys = with_keys
         self.ws_vis = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_VISIBLE_SET, n), dtype=torch.uint8,
                                   device=self.dev)
@@ -140,20 +141,22 @@ class ViewTrainer:
         tgt = self.target.view(-1)[:3 * hw]
         return img, fT, nc, dL, tgt
 
-    def raster_fwd(self, bg=(0.0, 0.0, 0.0), active=True):
+    def raster_fwd(self, bg=(0.0, 0.0, 0.0), active=True, stats=False):
         img, fT, nc, _, _ = self._img_views()
         if active:
             self.active.zero_()
         gsmi.gs_raster_fwd(self.proj_s, self.n, self.vals, self.ranges, self.cam.width, self.cam.height, bg, img, fT,
-                           nc, self.active if active else None)
+                           nc, self.active if active else None, self.pair_stats if stats else None)
 
     def set_target(self, target_np):
         _, _, _, _, tgt = self._img_views()
         tgt.copy_(torch.from_numpy(np.ascontiguousarray(target_np, np.float32).reshape(-1)))
 
-    def loss_l1(self):
+    def loss_l1(self, target=None):
+        """target: a device tensor holding 3*H*W floats, or None for the set_target buffer."""
         img, _, _, dL, tgt = self._img_views()
-        gsmi.gs_loss_l1(img, tgt, self.cam.width, self.cam.height, self.loss, dL, self.ws_loss)
+        gsmi.gs_loss_l1(img, tgt if target is None else target, self.cam.width, self.cam.height, self.loss, dL,
+                        self.ws_loss)
 
     def set_dL(self, dL_np):
         _, _, _, dL, _ = self._img_views()
@@ -179,19 +182,33 @@ class ViewTrainer:
         gsmi.gs_delta_apply(self.msg, self.replica_arr, 5, self.n, self.n, mode, self.version, self.status)
 
     # -- whole view ----------------------------------------------------------
-    def step(self, cam, step, version=1, publish=True, active=False):
+    PHASES = ("project", "visible", "bin_sort", "raster_fwd", "loss_l1", "raster_bwd", "adam", "pack", "apply")
+
+    def step(self, cam, step, version=1, publish=True, active=False, target=None, events=None):
         """Project, visible set, bin+sort, forward, L1, backward, Adam, pack + apply.
-        The target must already be in place (set_target)."""
+        target: device tensor (3*H*W) or None for the set_target buffer.
+        events: optional list of len(PHASES)+1 torch.cuda.Event recorded around the phases."""
+        ev = events
+        if ev: ev[0].record()
         self.project(cam)
+        if ev: ev[1].record()
         self.visible()
+        if ev: ev[2].record()
         self.bin_sort()
+        if ev: ev[3].record()
         self.raster_fwd(active=active)
-        self.loss_l1()
+        if ev: ev[4].record()
+        self.loss_l1(target)
+        if ev: ev[5].record()
         self.raster_bwd(grad2d=False)
+        if ev: ev[6].record()
         self.adam(step)
+        if ev: ev[7].record()
         if publish:
             self.pack(version)
+            if ev: ev[8].record()
             self.apply()
+        if ev: ev[9].record()
 
     def ensure_capacity(self, cams, margin=1.25):
         """Size the pair buffers for the given cameras (synchronizes)."""

@@ -185,23 +185,30 @@ def make_target(width: int, height: int, seed: int, view: int, kind: str) -> np.
     """Target image [3,H,W] in [0,1].
 
     "uniform": i.i.d. U(0,1) per pixel.  "smooth": a seeded low-frequency
-    colour field (a few random plane waves per channel) plus 5% noise; it
-    stands in for a photograph of the scene.
+    colour field (four random plane waves per channel, built separably) plus
+    +-5% uniform noise; it stands in for a photograph of the scene.
     """
     rng = np.random.default_rng([seed, 7919, view])
     if kind == "uniform":
-        return rng.uniform(0.0, 1.0, (3, height, width)).astype(np.float32)
-    ys = (np.arange(height, dtype=np.float64) + 0.5) / height
-    xs = (np.arange(width, dtype=np.float64) + 0.5) / width
+        return rng.random((3, height, width), dtype=np.float32)
+    ys = ((np.arange(height, dtype=np.float64) + 0.5) / height)[:, None]
+    xs = ((np.arange(width, dtype=np.float64) + 0.5) / width)[None, :]
     img = np.empty((3, height, width), np.float32)
     for ch in range(3):
-        acc = np.zeros((height, width))
+        acc = np.zeros((height, width), np.float32)
         for _ in range(4):
             fx_, fy_ = rng.uniform(-3.0, 3.0, 2)
             ph = rng.uniform(0, 2 * math.pi)
-            acc += np.cos(2 * math.pi * (fx_ * xs[None, :] + fy_ * ys[:, None]) + ph)
-        acc = 0.5 + 0.1 * acc + 0.05 * rng.standard_normal((height, width))
-        img[ch] = np.clip(acc, 0.0, 1.0)
+            ax = 2 * math.pi * fx_ * xs + ph
+            by = 2 * math.pi * fy_ * ys
+            # cos(a + b) = cos a cos b - sin a sin b, as two outer products
+            acc += (np.cos(by) * np.cos(ax) - np.sin(by) * np.sin(ax)).astype(np.float32)
+        noise = rng.random((height, width), dtype=np.float32)
+        acc *= np.float32(0.1)
+        acc += np.float32(0.45)
+        acc += np.float32(0.1) * noise
+        np.clip(acc, 0.0, 1.0, out=acc)
+        img[ch] = acc
     return img
 
 

@@ -28,6 +28,7 @@ def compute():
     m = [np.zeros_like(a) for _, a in sc.groups()]
     v = [np.zeros_like(a) for _, a in sc.groups()]
     r = oracle.train_view(sc, cam, tgt, m, v, 1)
+    g = r.grads.full(sc.n)
     return {
         "radius": r.proj.radius.tolist(),
         "rect": r.proj.rect.tolist(),
@@ -39,11 +40,11 @@ def compute():
         "img_row16": r.render.img[:, 16, :].reshape(-1).tolist(),
         "n_contrib_row16": r.render.n_contrib[16].tolist(),
         "loss": r.loss,
-        "grad_mean": r.grads.mean.reshape(-1).tolist(),
-        "grad_log_scale": r.grads.log_scale.reshape(-1).tolist(),
-        "grad_quat": r.grads.quat.reshape(-1).tolist(),
-        "grad_opacity": r.grads.opacity.reshape(-1).tolist(),
-        "grad_sh": r.grads.sh.reshape(-1).tolist(),
+        "grad_mean": g[0].reshape(-1).tolist(),
+        "grad_log_scale": g[1].reshape(-1).tolist(),
+        "grad_quat": g[2].reshape(-1).tolist(),
+        "grad_opacity": g[3].reshape(-1).tolist(),
+        "grad_sh": g[4].reshape(-1).tolist(),
     }
 
 

@@ -46,13 +46,18 @@ def assert_grads(gpu, ref, rows_ok, name, rtol=GRAD_RTOL, floor=None):
     g, r = gpu[rows_ok], ref[rows_ok]
     if r.size == 0:
         return {}
-    fl = grad_floor(r) if floor is None else floor
+    if floor is None:
+        fl = grad_floor(r)
+    elif np.ndim(floor) == 0:
+        fl = floor
+    else:
+        fl = np.asarray(floor, np.float64)[rows_ok]
     err = np.abs(g - r)
     tol = rtol * np.maximum(np.abs(r), fl)
     bad = err > tol
     nrm = float(np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-300))
     stats = {"max_rel": float((err / np.maximum(np.abs(r), fl)).max()), "norm_rel": nrm, "bad": int(bad.sum())}
     assert bad.sum() == 0, "%s: %d elements beyond %.0e relative (floor %.3g): worst err %.3g ref %.3g" % (
-        name, int(bad.sum()), rtol, fl, err[bad].max(), r[bad][np.argmax(err[bad])])
+        name, int(bad.sum()), rtol, float(np.max(fl)), err[bad].max(), r[bad][np.argmax(err[bad])])
     assert nrm <= rtol, "%s: normwise error %.3g" % (name, nrm)
     return stats

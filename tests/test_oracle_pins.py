@@ -388,7 +388,7 @@ def check_fd_gradients(orc, seed=0, n=6, deg=3, W=40, H=32, tol=1e-5):
     g2, _ = orc.render_backward(vis, pr, cam, wimg)
     gr = orc.project_backward(sc, cam, vis, g2, pr)
     names = ["mean", "log_scale", "quat", "opacity", "sh"]
-    an_groups = dict(zip(names, gr.groups()))
+    an_groups = dict(zip(names, gr.full(n)))
     base_loss, base_sig = _forward_loss(orc, sc, cam, wimg)
     checked = skipped = 0
     for name in names:

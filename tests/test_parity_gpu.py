@@ -178,10 +178,12 @@ def _bwd_compare(w, tr, cam, orc, dL, case, check_flags=True):
     names = ["du", "dv", "dA", "dB", "dC", "dop", "dr", "dg", "db"]
     for c, nm in enumerate(names):
         stats[nm] = assert_grads(g2_gpu[:, c], g2[:, c], ok, "grad2d." + nm)
-    for name, gp, go in zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.grads, gr.groups()):
+    for name, gp, go in zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.grads, gr.full(w.scene.n)):
         stats[name] = assert_grads(gp.cpu().numpy(), go, ok, "grad." + name)
     gn = tr.grad_norm.cpu().numpy()[:w.scene.n]
-    stats["grad_norm"] = assert_grads(gn, gr.grad_norm, ok, "grad_norm")
+    gn_ref = np.zeros(w.scene.n)
+    gn_ref[vis.astype(np.int64)] = gr.grad_norm
+    stats["grad_norm"] = assert_grads(gn, gn_ref, ok, "grad_norm")
     _say(case, {k: (round(v.get("max_rel", 0), 6), round(v.get("norm_rel", 0), 8)) for k, v in stats.items()})
     return vis, ok, gr
 
@@ -228,8 +230,12 @@ def test_sparse_adam(torch_gpu, orc):
             rows = np.zeros(n, bool); rows[idx] = True
             gp = P[k].cpu().numpy()
             np.testing.assert_array_equal(gp[~rows], p[k][~rows])        # untouched rows
-            assert_grads(M[k].cpu().numpy(), mr, rows, "m%d" % k, rtol=1e-5)
-            assert_grads(Vv[k].cpu().numpy(), vr, rows, "v%d" % k, rtol=1e-5)
+            # fp32 rounding of b*m + (1-b)*g is relative to the operands' magnitudes
+            g64 = g[k].astype(np.float64)
+            fm = 0.9 * np.abs(mv[k][0]) + 0.1 * np.abs(g64)
+            fv = 0.999 * np.abs(mv[k][1]) + 0.001 * g64 * g64
+            assert_grads(M[k].cpu().numpy(), mr, rows, "m%d" % k, rtol=1e-5, floor=fm)
+            assert_grads(Vv[k].cpu().numpy(), vr, rows, "v%d" % k, rtol=1e-5, floor=fv)
             assert_grads(D[k].cpu().numpy()[idx], dr, np.ones(idx.size, bool), "delta%d" % k, rtol=2e-5)
             assert_grads(gp, pr, rows, "p%d" % k, rtol=1e-6)
             p[k], mv[k] = pr.astype(np.float32), (mr.astype(np.float32), vr.astype(np.float32))
