@@ -249,6 +249,9 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
  * form with one global step t >= 1:
  *   m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2
  *   delta = -(lr/(1-b1^t)) m / (sqrt(v)/sqrt(1-b2^t) + eps);  p += delta
+ * The hyper-parameters are taken in fp64; b, 1-b, the bias corrections and
+ * lr/(1-b1^t) are formed in fp64 and rounded to fp32 once (the arithmetic per
+ * element is fp32).  max_rows bounds *count (launch size).
  * Rows not in idx are not touched.  delta (if not NULL) receives the step of
  * every updated row ([n,cols] layout) -- the pending update that
  * gs_delta_pack publishes.
@@ -264,8 +267,8 @@ typedef struct {
 } gs_adam_group;
 
 gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
-                         const uint32_t* count, int32_t max_rows, int32_t step, float beta1, float beta2,
-                         float eps, void* stream);
+                         const uint32_t* count, int32_t max_rows, int32_t step, double beta1, double beta2,
+                         double eps, void* stream);
 
 /*
  * Staged publication (Shadow Graph steps 3-4 of Section 4.3; publication

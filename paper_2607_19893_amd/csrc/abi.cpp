@@ -192,12 +192,13 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
 }
 
 gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx, const uint32_t* count,
-                         int32_t max_rows, int32_t step, float beta1, float beta2, float eps, void* stream) {
+                         int32_t max_rows, int32_t step, double beta1, double beta2, double eps, void* stream) {
     GS_REQUIRE(groups && n_groups > 0 && n_groups <= GS_MAX_GROUPS, "gs_sparse_adam: 1..%d groups", GS_MAX_GROUPS);
     GS_REQUIRE(idx && count, "gs_sparse_adam: null index list");
     GS_REQUIRE(max_rows >= 0, "gs_sparse_adam: max_rows < 0");
     GS_REQUIRE(step >= 1, "gs_sparse_adam: step must be >= 1");
-    GS_REQUIRE(beta1 >= 0.0f && beta1 < 1.0f && beta2 >= 0.0f && beta2 < 1.0f, "gs_sparse_adam: betas outside [0,1)");
+    GS_REQUIRE(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0, "gs_sparse_adam: betas outside [0,1)");
+    GS_REQUIRE(eps >= 0.0, "gs_sparse_adam: eps < 0");
     int32_t row_len = 0;
     for (int i = 0; i < n_groups; ++i) {
         GS_REQUIRE(groups[i].p && groups[i].g && groups[i].m && groups[i].v, "gs_sparse_adam: group %d null", i);

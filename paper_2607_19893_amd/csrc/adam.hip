@@ -65,12 +65,12 @@ __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint
 }  // namespace
 
 hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
-                              const uint32_t* count, int32_t max_rows, int32_t step, float beta1, float beta2,
-                              float eps, hipStream_t st) {
+                              const uint32_t* count, int32_t max_rows, int32_t step, double beta1, double beta2,
+                              double eps, hipStream_t st) {
     AdamArgs a = {};
     int32_t row_len = 0;
-    const double bc1 = 1.0 - pow((double)beta1, (double)step);
-    const double bc2 = 1.0 - pow((double)beta2, (double)step);
+    const double bc1 = 1.0 - pow(beta1, (double)step);
+    const double bc2 = 1.0 - pow(beta2, (double)step);
     for (int i = 0; i < n_groups; ++i) {
         a.p[i] = groups[i].p;
         a.g[i] = groups[i].g;
@@ -84,12 +84,12 @@ hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, con
     a.n_groups = n_groups;
     a.row_len = row_len;
     a.rows_per_wave = GS_WAVE / row_len;
-    a.beta1 = beta1;
-    a.beta2 = beta2;
-    a.one_m_b1 = 1.0f - beta1;
-    a.one_m_b2 = 1.0f - beta2;
+    a.beta1 = (float)beta1;
+    a.beta2 = (float)beta2;
+    a.one_m_b1 = (float)(1.0 - beta1);
+    a.one_m_b2 = (float)(1.0 - beta2);
     a.sqrt_bc2 = (float)sqrt(bc2);
-    a.eps = eps;
+    a.eps = (float)eps;
     if (max_rows <= 0) return hipSuccess;
     const uint64_t waves_needed = div_up((uint64_t)max_rows, (uint64_t)a.rows_per_wave);
     uint32_t blocks = div_up(waves_needed, GS_BLOCK / GS_WAVE);

@@ -53,8 +53,8 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
 
 // adam.hip
 hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
-                              const uint32_t* count, int32_t max_rows, int32_t step, float beta1, float beta2,
-                              float eps, hipStream_t st);
+                              const uint32_t* count, int32_t max_rows, int32_t step, double beta1, double beta2,
+                              double eps, hipStream_t st);
 
 // delta.hip
 size_t delta_msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups);

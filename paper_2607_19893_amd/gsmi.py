@@ -70,7 +70,8 @@ _lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, 
 _lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
 _lib.gs_raster_bwd.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P, P, P,
                                P, P, u32, P, P, P, P, ctypes.POINTER(gs_scene), P, P, P, sz, P]
-_lib.gs_sparse_adam.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, i32, f32, f32, f32, P]
+_lib.gs_sparse_adam.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, i32, ctypes.c_double,
+                                ctypes.c_double, ctypes.c_double, P]
 _lib.gs_delta_pack.argtypes = [P, P, i32, ctypes.POINTER(gs_group), i32, u32, P, sz, P, P]
 _lib.gs_delta_apply.argtypes = [P, sz, ctypes.POINTER(gs_group), i32, i32, i32, i32, P, P, P]
 for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
