@@ -149,8 +149,10 @@ class ViewTrainer:
                            nc, self.active if active else None, self.pair_stats if stats else None)
 
     def set_target(self, target_np):
-        _, _, _, _, tgt = self._img_views()
-        tgt.copy_(torch.from_numpy(np.ascontiguousarray(target_np, np.float32).reshape(-1)))
+        """Copy a [3,H,W] target into the target buffer (planar, first 3*H*W floats)."""
+        a = np.ascontiguousarray(target_np, np.float32)
+        self._set_image(a.shape[2], a.shape[1])
+        self.target.view(-1)[:a.size].copy_(torch.from_numpy(a.reshape(-1)))
 
     def loss_l1(self, target=None):
         """target: a device tensor holding 3*H*W floats, or None for the set_target buffer."""
@@ -159,8 +161,10 @@ class ViewTrainer:
                         self.ws_loss)
 
     def set_dL(self, dL_np):
-        _, _, _, dL, _ = self._img_views()
-        dL.copy_(torch.from_numpy(np.ascontiguousarray(dL_np, np.float32).reshape(-1)))
+        """Copy a [3,H,W] upstream image gradient into the dL buffer."""
+        a = np.ascontiguousarray(dL_np, np.float32)
+        self._set_image(a.shape[2], a.shape[1])
+        self.dL.view(-1)[:a.size].copy_(torch.from_numpy(a.reshape(-1)))
 
     def raster_bwd(self, bg=(0.0, 0.0, 0.0), grad2d=True):
         _, fT, nc, dL, _ = self._img_views()
