@@ -226,6 +226,7 @@ class ViewTrainer:
             need = max(need, int(to_u32(self.counts[1:2])[0]))
         if need > self.capacity:
             self._set_capacity(int(need * margin) + 1024)
+        self.status.zero_()
         return need
 
     def host_status(self):
