@@ -47,7 +47,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="room")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-views", type=int, default=2, help="views of the CPU oracle sample")
+    ap.add_argument("--cpu-views", type=int, default=8, help="views of the CPU oracle sample")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (collectives and sharding are "
