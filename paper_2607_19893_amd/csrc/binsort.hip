@@ -161,20 +161,21 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restri
     if (threadIdx.x == 0) bsum[blockIdx.x] = t;
 }
 
-// Exclusive offsets in depth order, pair_offset[id], and the pair emission
-// (tile id, primitive id) in rectangle row-major order.
-__global__ void __launch_bounds__(GS_BLOCK) k_emit(
+// Exclusive offsets in depth order: pair_offset[id] and offs_r[rank], with
+// offs_r[V] = M as a sentinel.  Also publishes the pair count and the
+// overflow flag.
+__global__ void __launch_bounds__(GS_BLOCK) k_offsets(
     const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
-    const ushort4* __restrict__ rect, const uint32_t* __restrict__ bsum, const uint32_t* __restrict__ total,
-    uint32_t capacity, int32_t tiles_x, uint32_t* __restrict__ pair_offset, uint32_t* __restrict__ pkeys,
-    uint32_t* __restrict__ pvals, uint32_t* __restrict__ sort_count, uint32_t* __restrict__ num_pairs,
-    gs_device_status* __restrict__ status) {
+    const uint32_t* __restrict__ bsum, const uint32_t* __restrict__ total, uint32_t capacity,
+    uint32_t* __restrict__ pair_offset, uint32_t* __restrict__ offs_r, uint32_t* __restrict__ sort_count,
+    uint32_t* __restrict__ num_pairs, gs_device_status* __restrict__ status) {
     __shared__ uint32_t scratch[4];
     const uint32_t V = *vis_count;
     const uint32_t M = *total;
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         *num_pairs = M;
         *sort_count = M <= capacity ? M : 0u;
+        offs_r[V] = M;
         if (M > capacity && status) {
             atomicOr(&status->flags, GS_DEV_PAIR_OVERFLOW);
             atomicMax(&status->required, M);
@@ -192,22 +193,68 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit(
     }
     uint32_t tot;
     uint32_t off = block_excl_scan(s, scratch, &tot) + bsum[blockIdx.x];
-    const bool fits = M <= capacity;
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) {
         if (base + k >= V) break;
         pair_offset[g[k]] = off;
-        if (fits) {
-            const ushort4 rc = rect[g[k]];
-            uint32_t o = off;
-            for (int ty = rc.y; ty < rc.w; ++ty)
-                for (int tx = rc.x; tx < rc.z; ++tx) {
-                    pkeys[o] = (uint32_t)(ty * tiles_x + tx);
-                    pvals[o] = g[k];
-                    ++o;
-                }
-        }
+        offs_r[base + k] = off;
         off += t[k];
+    }
+}
+
+// One thread per pair: pair i belongs to the rank r with offs_r[r] <= i <
+// offs_r[r+1] and covers tile number i - offs_r[r] of that primitive's
+// rectangle (row-major).  Each block locates its rank range once, stages the
+// offsets, ids and rectangles of those ranks in LDS and binary-searches
+// there; key (tile id) and value (primitive id) stores are contiguous.
+__global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
+    const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ offs_r,
+    const ushort4* __restrict__ rect, const uint32_t* __restrict__ sort_count, int32_t tiles_x,
+    uint32_t* __restrict__ pkeys, uint32_t* __restrict__ pvals) {
+    __shared__ uint32_t s_off[GS_TILE_ITEMS + 1];
+    __shared__ uint32_t s_gid[GS_TILE_ITEMS + 1];
+    __shared__ ushort4 s_rect[GS_TILE_ITEMS + 1];
+    __shared__ uint32_t s_range[2];
+    const uint32_t M = *sort_count;
+    const uint32_t base = blockIdx.x * GS_TILE_ITEMS;
+    if (base >= M) return;
+    const uint32_t hi = min(base + (uint32_t)GS_TILE_ITEMS, M);
+    if (threadIdx.x < 2) {
+        // largest r in [0, V) with offs_r[r] <= key
+        const uint32_t key = threadIdx.x == 0 ? base : hi - 1;
+        uint32_t lo = 0, up = *vis_count;   // invariant: offs_r[lo] <= key < offs_r[up]
+        while (up - lo > 1) {
+            const uint32_t mid = (lo + up) >> 1;
+            if (offs_r[mid] <= key) lo = mid; else up = mid;
+        }
+        s_range[threadIdx.x] = lo;
+    }
+    __syncthreads();
+    const uint32_t r0 = s_range[0];
+    const uint32_t nr = s_range[1] - r0 + 1;     // <= GS_TILE_ITEMS: every rank holds >= 1 pair
+    for (uint32_t j = threadIdx.x; j < nr; j += GS_BLOCK) {
+        const uint32_t g = order[r0 + j];
+        s_off[j] = offs_r[r0 + j];
+        s_gid[j] = g;
+        s_rect[j] = rect[g];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        const uint32_t i = base + k * GS_BLOCK + threadIdx.x;
+        if (i >= hi) break;
+        uint32_t lo = 0, up = nr;   // s_off[lo] <= i < s_off[up] (s_off[nr] taken as +inf)
+        while (up - lo > 1) {
+            const uint32_t mid = (lo + up) >> 1;
+            if (s_off[mid] <= i) lo = mid; else up = mid;
+        }
+        const ushort4 rc = s_rect[lo];
+        const uint32_t local = i - s_off[lo];
+        const uint32_t w = (uint32_t)(rc.z - rc.x);
+        const uint32_t ty = rc.y + local / w;
+        const uint32_t tx = rc.x + local % w;
+        pkeys[i] = ty * (uint32_t)tiles_x + tx;
+        pvals[i] = s_gid[lo];
     }
 }
 
@@ -228,7 +275,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_finalize(const uint32_t* __restric
 struct BinsortLayout {
     size_t dk[3], dv[3];      // depth sort: in, tmp, out
     size_t pk[3], pv[2];      // pair sort: in, tmp, out (values out = caller's vals)
-    size_t hist, totals, bsum, counters;
+    size_t hist, totals, bsum, offs, counters;
     size_t bytes;
     uint32_t nblocks_hist;
 };
@@ -245,6 +292,7 @@ BinsortLayout binsort_layout(int32_t n, uint32_t capacity) {
     L.hist = o; o += align256(4 * (size_t)kRadix * L.nblocks_hist);
     L.totals = o; o += align256(4 * kRadix);
     L.bsum = o; o += align256(4 * ((size_t)div_up(nn, GS_TILE_ITEMS) + 1));
+    L.offs = o; o += align256(4 * (nn + 1));
     L.counters = o; o += 256;
     L.bytes = o;
     return L;
@@ -311,9 +359,13 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles, bsum);
     e = launch_scan_blocks(bsum, nb, ctr + 0, nullptr, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_emit, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles,
-                       reinterpret_cast<const ushort4*>(proj.rect), bsum, ctr + 0, capacity, TX, pair_offset,
-                       at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), ctr + 1, num_pairs, status);
+    uint32_t* offs_r = at<uint32_t>(ws, L.offs);
+    hipLaunchKernelGGL(k_offsets, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles, bsum, ctr + 0,
+                       capacity, pair_offset, offs_r, ctr + 1, num_pairs, status);
+    if (capacity > 0)
+        hipLaunchKernelGGL(k_emit_pairs, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, order,
+                           vis_count, offs_r, reinterpret_cast<const ushort4*>(proj.rect), ctr + 1, TX,
+                           at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]));
     // 3. stable sort of the pairs by tile id
     int tbits = 1;
     while (tbits < 32 && (1u << tbits) < T) ++tbits;

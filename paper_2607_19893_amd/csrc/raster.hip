@@ -331,184 +331,237 @@ __device__ __forceinline__ void sh_basis_grad(float x, float y, float z, float* 
 
 __device__ __forceinline__ float dot3(const float* a, const float* b) { return a[0] * b[0] + a[1] * b[1] + a[2] * b[2]; }
 
+// Per-primitive row I/O goes through LDS: a block stages the parameter rows of
+// its 256 primitives with row-contiguous loads (lanes walk along a row, so a
+// 192-byte SH row is read by consecutive lanes), each thread works on its own
+// row in LDS (odd row stride: conflict-free), and the gradient rows leave the
+// same way.
+template <int DEG>
+struct RowLayout {
+    static constexpr int K = (DEG + 1) * (DEG + 1);
+    static constexpr int SH = 3 * K;
+    static constexpr int ROW = 11 + SH;                        // mean 3, log_scale 3, quat 4, opacity 1, sh
+    static constexpr int STRIDE = (ROW % 2 == 0) ? ROW + 1 : ROW;
+};
+
+template <int COLS, int OFF, int STRIDE>
+__device__ __forceinline__ void rows_to_lds(const float* __restrict__ src, const uint32_t* s_id, uint32_t nrows,
+                                            float* s_row) {
+    for (uint32_t e = threadIdx.x; e < nrows * COLS; e += GS_BLOCK) {
+        const uint32_t r = e / COLS, c = e - r * COLS;
+        s_row[r * STRIDE + OFF + c] = src[(size_t)s_id[r] * COLS + c];
+    }
+}
+
+template <int COLS, int OFF, int STRIDE>
+__device__ __forceinline__ void lds_to_rows(float* __restrict__ dst, const uint32_t* s_id, uint32_t nrows,
+                                            const float* s_row) {
+    for (uint32_t e = threadIdx.x; e < nrows * COLS; e += GS_BLOCK) {
+        const uint32_t r = e / COLS, c = e - r * COLS;
+        dst[(size_t)s_id[r] * COLS + c] = s_row[r * STRIDE + OFF + c];
+    }
+}
+
 template <int DEG>
 __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
     const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
     const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, const uint8_t* __restrict__ clampm,
     const float* __restrict__ mean, const float* __restrict__ log_scale, const float* __restrict__ quat,
     const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c, uint32_t capacity,
-    float* __restrict__ g_mean,
-    float* __restrict__ g_ls, float* __restrict__ g_quat, float* __restrict__ g_op, float* __restrict__ g_sh,
-    float* __restrict__ grad2d, float* __restrict__ grad_norm) {
-    const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
-    if (r >= *vis_count) return;
-    const uint32_t id = vis_idx[r];
-    // 1. this primitive's 2D gradient: its pair slots in order (none if the
-    //    pair list overflowed its capacity)
-    float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-    {
-        const uint64_t first = pair_offset[id];
-        const uint32_t nt = tiles[id];
-        const float* sl = slots + first * kG;
-        if (first + nt <= capacity)
-            for (uint32_t k = 0; k < nt; ++k)
+    float* __restrict__ g_mean, float* __restrict__ g_ls, float* __restrict__ g_quat, float* __restrict__ g_op,
+    float* __restrict__ g_sh, float* __restrict__ grad2d, float* __restrict__ grad_norm) {
+    using L = RowLayout<DEG>;
+    constexpr int K = L::K, ST = L::STRIDE;
+    __shared__ float s_row[GS_BLOCK * ST];
+    __shared__ uint32_t s_id[GS_BLOCK];
+    const uint32_t V = *vis_count;
+    const uint32_t r0 = blockIdx.x * GS_BLOCK;
+    if (r0 >= V) return;
+    const uint32_t nrows = min((uint32_t)GS_BLOCK, V - r0);
+    const int tid = threadIdx.x;
+    const bool valid = (uint32_t)tid < nrows;
+    const uint32_t id = valid ? vis_idx[r0 + tid] : 0u;
+    s_id[tid] = id;
+    __syncthreads();
+    rows_to_lds<3, 0, ST>(mean, s_id, nrows, s_row);
+    rows_to_lds<3, 3, ST>(log_scale, s_id, nrows, s_row);
+    rows_to_lds<4, 6, ST>(quat, s_id, nrows, s_row);
+    rows_to_lds<1, 10, ST>(opacity, s_id, nrows, s_row);
+    rows_to_lds<L::SH, 11, ST>(sh, s_id, nrows, s_row);
+    __syncthreads();
+    if (valid) {
+        float* row = s_row + tid * ST;
+        // 1. this primitive's 2D gradient: its pair slots in order (none if the
+        //    pair list overflowed its capacity)
+        float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+        {
+            const uint64_t first = pair_offset[id];
+            const uint32_t nt = tiles[id];
+            const float* sl = slots + first * kG;
+            if (first + nt <= capacity)
+                for (uint32_t k = 0; k < nt; ++k)
 #pragma unroll
-            for (int q = 0; q < kG; ++q) g2[q] += sl[k * kG + q];
-    }
-    if (grad2d) {
-#pragma unroll
-        for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
-    }
-    if (grad_norm) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
-
-    const float mu[3] = {mean[3 * id], mean[3 * id + 1], mean[3 * id + 2]};
-    // 2. opacity
-    const float o = 1.0f / (1.0f + expf(-opacity[id]));
-    g_op[id] = g2[5] * o * (1.0f - o);
-
-    // 3. colour: dL/dsh and the view-direction path into the mean
-    float gmu[3];
-    {
-        float v[3] = {mu[0] - c.campos[0], mu[1] - c.campos[1], mu[2] - c.campos[2]};
-        const float len = sqrtf(dot3(v, v));
-        const float il = 1.0f / len;
-        const float d[3] = {v[0] * il, v[1] * il, v[2] * il};
-        constexpr int K = (DEG + 1) * (DEG + 1);
-        float Y[16], G[16][3];
-        sh_basis_grad<DEG>(d[0], d[1], d[2], Y, G);
-        const uint8_t cm = clampm[id];
-        const float gc[3] = {(cm & 1) ? 0.0f : g2[6], (cm & 2) ? 0.0f : g2[7], (cm & 4) ? 0.0f : g2[8]};
-        const float* co = sh + (size_t)id * K * 3;
-        float* gco = g_sh + (size_t)id * K * 3;
-        float gd[3] = {0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const float a = gc[0] * co[3 * k] + gc[1] * co[3 * k + 1] + gc[2] * co[3 * k + 2];
-            gd[0] += a * G[k][0];
-            gd[1] += a * G[k][1];
-            gd[2] += a * G[k][2];
-            gco[3 * k + 0] = gc[0] * Y[k];
-            gco[3 * k + 1] = gc[1] * Y[k];
-            gco[3 * k + 2] = gc[2] * Y[k];
+                    for (int q = 0; q < kG; ++q) g2[q] += sl[k * kG + q];
         }
-        const float rad = dot3(gd, d);
-        gmu[0] = (gd[0] - d[0] * rad) * il;
-        gmu[1] = (gd[1] - d[1] * rad) * il;
-        gmu[2] = (gd[2] - d[2] * rad) * il;
-    }
+        if (grad2d) {
+#pragma unroll
+            for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
+        }
+        if (grad_norm) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
 
-    // 4. geometry
-    const float* R = c.R;
-    float p[3];
+        const float mu[3] = {row[0], row[1], row[2]};
+        const float ls[3] = {row[3], row[4], row[5]};
+        const float qr[4] = {row[6], row[7], row[8], row[9]};
+        // 2. opacity
+        const float o = 1.0f / (1.0f + expf(-row[10]));
+        row[10] = g2[5] * o * (1.0f - o);
+
+        // 3. colour: dL/dsh (written over the coefficients) and the view-direction path
+        float gmu[3];
+        {
+            float v[3] = {mu[0] - c.campos[0], mu[1] - c.campos[1], mu[2] - c.campos[2]};
+            const float len = sqrtf(dot3(v, v));
+            const float il = 1.0f / len;
+            const float d[3] = {v[0] * il, v[1] * il, v[2] * il};
+            float Y[16], G[16][3];
+            sh_basis_grad<DEG>(d[0], d[1], d[2], Y, G);
+            const uint8_t cm = clampm[id];
+            const float gc[3] = {(cm & 1) ? 0.0f : g2[6], (cm & 2) ? 0.0f : g2[7], (cm & 4) ? 0.0f : g2[8]};
+            float* co = row + 11;
+            float gd[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int k = 0; k < 3; ++k) p[k] = R[3 * k] * mu[0] + R[3 * k + 1] * mu[1] + R[3 * k + 2] * mu[2] + c.t[k];
-    const float s[3] = {expf(log_scale[3 * id]), expf(log_scale[3 * id + 1]), expf(log_scale[3 * id + 2])};
-    const float4 qr = reinterpret_cast<const float4*>(quat)[id];
-    const float qn = sqrtf(qr.x * qr.x + qr.y * qr.y + qr.z * qr.z + qr.w * qr.w);
-    const float iq = 1.0f / qn;
-    const float w = qr.x * iq, x = qr.y * iq, y = qr.z * iq, z = qr.w * iq;
-    const float Rq[3][3] = {{1.0f - 2.0f * (y * y + z * z), 2.0f * (x * y - w * z), 2.0f * (x * z + w * y)},
-                            {2.0f * (x * y + w * z), 1.0f - 2.0f * (x * x + z * z), 2.0f * (y * z - w * x)},
-                            {2.0f * (x * z - w * y), 2.0f * (y * z + w * x), 1.0f - 2.0f * (x * x + y * y)}};
-    float M[3][3], Sg[3][3];
+            for (int k = 0; k < K; ++k) {
+                const float a = gc[0] * co[3 * k] + gc[1] * co[3 * k + 1] + gc[2] * co[3 * k + 2];
+                gd[0] += a * G[k][0];
+                gd[1] += a * G[k][1];
+                gd[2] += a * G[k][2];
+                co[3 * k + 0] = gc[0] * Y[k];
+                co[3 * k + 1] = gc[1] * Y[k];
+                co[3 * k + 2] = gc[2] * Y[k];
+            }
+            const float rad = dot3(gd, d);
+            gmu[0] = (gd[0] - d[0] * rad) * il;
+            gmu[1] = (gd[1] - d[1] * rad) * il;
+            gmu[2] = (gd[2] - d[2] * rad) * il;
+        }
+
+        // 4. geometry
+        const float* R = c.R;
+        float p[3];
 #pragma unroll
-    for (int a = 0; a < 3; ++a)
+        for (int k = 0; k < 3; ++k) p[k] = R[3 * k] * mu[0] + R[3 * k + 1] * mu[1] + R[3 * k + 2] * mu[2] + c.t[k];
+        const float s[3] = {expf(ls[0]), expf(ls[1]), expf(ls[2])};
+        const float qn = sqrtf(qr[0] * qr[0] + qr[1] * qr[1] + qr[2] * qr[2] + qr[3] * qr[3]);
+        const float iq = 1.0f / qn;
+        const float w = qr[0] * iq, x = qr[1] * iq, y = qr[2] * iq, z = qr[3] * iq;
+        const float Rq[3][3] = {{1.0f - 2.0f * (y * y + z * z), 2.0f * (x * y - w * z), 2.0f * (x * z + w * y)},
+                                {2.0f * (x * y + w * z), 1.0f - 2.0f * (x * x + z * z), 2.0f * (y * z - w * x)},
+                                {2.0f * (x * z - w * y), 2.0f * (y * z + w * x), 1.0f - 2.0f * (x * x + y * y)}};
+        float M[3][3], Sg[3][3];
 #pragma unroll
-        for (int b = 0; b < 3; ++b) M[a][b] = Rq[a][b] * s[b];
+        for (int a = 0; a < 3; ++a)
 #pragma unroll
-    for (int a = 0; a < 3; ++a)
+            for (int b = 0; b < 3; ++b) M[a][b] = Rq[a][b] * s[b];
 #pragma unroll
-        for (int b = 0; b < 3; ++b) Sg[a][b] = M[a][0] * M[b][0] + M[a][1] * M[b][1] + M[a][2] * M[b][2];
-    const float tz = p[2], itz = 1.0f / tz;
-    const float lx = 1.3f * c.tan_fovx, ly = 1.3f * c.tan_fovy;
-    const float rx = p[0] * itz, ry = p[1] * itz;
-    const bool clx = rx < -lx || rx > lx, cly = ry < -ly || ry > ly;
-    const float xr = fminf(lx, fmaxf(-lx, rx)), yr = fminf(ly, fmaxf(-ly, ry));
-    const float j00 = c.fx * itz, j11 = c.fy * itz;
-    const float j02 = -c.fx * xr * itz, j12 = -c.fy * yr * itz;
-    float T0[3], T1[3];
+        for (int a = 0; a < 3; ++a)
 #pragma unroll
-    for (int k = 0; k < 3; ++k) {
-        T0[k] = j00 * R[k] + j02 * R[6 + k];
-        T1[k] = j11 * R[3 + k] + j12 * R[6 + k];
-    }
-    float ST0[3], ST1[3];   // Sigma T0, Sigma T1
+            for (int b = 0; b < 3; ++b) Sg[a][b] = M[a][0] * M[b][0] + M[a][1] * M[b][1] + M[a][2] * M[b][2];
+        const float tz = p[2], itz = 1.0f / tz;
+        const float lx = 1.3f * c.tan_fovx, ly = 1.3f * c.tan_fovy;
+        const float rx = p[0] * itz, ry = p[1] * itz;
+        const bool clx = rx < -lx || rx > lx, cly = ry < -ly || ry > ly;
+        const float xr = fminf(lx, fmaxf(-lx, rx)), yr = fminf(ly, fmaxf(-ly, ry));
+        const float j00 = c.fx * itz, j11 = c.fy * itz;
+        const float j02 = -c.fx * xr * itz, j12 = -c.fy * yr * itz;
+        float T0[3], T1[3];
 #pragma unroll
-    for (int a = 0; a < 3; ++a) {
-        ST0[a] = Sg[a][0] * T0[0] + Sg[a][1] * T0[1] + Sg[a][2] * T0[2];
-        ST1[a] = Sg[a][0] * T1[0] + Sg[a][1] * T1[1] + Sg[a][2] * T1[2];
-    }
-    const float ca = dot3(T0, ST0) + 0.3f, cb = dot3(T0, ST1), cc = dot3(T1, ST1) + 0.3f;
-    const float det = ca * cc - cb * cb;
-    const float id2 = 1.0f / (det * det);
-    // conic (A,B,C) = (c, -b, a)/det  ->  gradient w.r.t. (a, b, c)
-    const float gA = g2[2], gB = g2[3], gC = g2[4];
-    const float ga = (-gA * cc * cc + gB * cb * cc - gC * cb * cb) * id2;
-    const float gb = (2.0f * gA * cb * cc - gB * (ca * cc + cb * cb) + 2.0f * gC * ca * cb) * id2;
-    const float gcv = (-gA * cb * cb + gB * ca * cb - gC * ca * ca) * id2;
-    // a = T0.S.T0, b = T0.S.T1, c = T1.S.T1
-    float gT0[3], gT1[3];
-#pragma unroll
-    for (int a = 0; a < 3; ++a) {
-        gT0[a] = 2.0f * ga * ST0[a] + gb * ST1[a];
-        gT1[a] = gb * ST0[a] + 2.0f * gcv * ST1[a];
-    }
-    const float gj00 = gT0[0] * R[0] + gT0[1] * R[1] + gT0[2] * R[2];
-    const float gj02 = gT0[0] * R[6] + gT0[1] * R[7] + gT0[2] * R[8];
-    const float gj11 = gT1[0] * R[3] + gT1[1] * R[4] + gT1[2] * R[5];
-    const float gj12 = gT1[0] * R[6] + gT1[1] * R[7] + gT1[2] * R[8];
-    const float itz2 = itz * itz;
-    float gp[3] = {0.0f, 0.0f, 0.0f};
-    gp[2] -= (gj00 * c.fx + gj11 * c.fy) * itz2;
-    if (clx) {
-        gp[2] += gj02 * c.fx * xr * itz2;
-    } else {
-        gp[0] -= gj02 * c.fx * itz2;
-        gp[2] += 2.0f * gj02 * c.fx * p[0] * itz2 * itz;
-    }
-    if (cly) {
-        gp[2] += gj12 * c.fy * yr * itz2;
-    } else {
-        gp[1] -= gj12 * c.fy * itz2;
-        gp[2] += 2.0f * gj12 * c.fy * p[1] * itz2 * itz;
-    }
-    gp[0] += g2[0] * c.fx * itz;
-    gp[1] += g2[1] * c.fy * itz;
-    gp[2] -= (g2[0] * c.fx * p[0] + g2[1] * c.fy * p[1]) * itz2;
-#pragma unroll
-    for (int k = 0; k < 3; ++k) gmu[k] += R[k] * gp[0] + R[3 + k] * gp[1] + R[6 + k] * gp[2];
-    g_mean[3 * id + 0] = gmu[0];
-    g_mean[3 * id + 1] = gmu[1];
-    g_mean[3 * id + 2] = gmu[2];
-    // Sigma = M M^T with symmetric gradient Gs = ga T0T0^T + gb (T0T1^T + T1T0^T)/2 + gc T1T1^T
-    float Gs[3][3];
-#pragma unroll
-    for (int a = 0; a < 3; ++a)
-#pragma unroll
-        for (int b = 0; b < 3; ++b)
-            Gs[a][b] = ga * T0[a] * T0[b] + 0.5f * gb * (T0[a] * T1[b] + T1[a] * T0[b]) + gcv * T1[a] * T1[b];
-    float gR[3][3];
-#pragma unroll
-    for (int b = 0; b < 3; ++b) {
-        float gsb = 0.0f;
+        for (int k = 0; k < 3; ++k) {
+            T0[k] = j00 * R[k] + j02 * R[6 + k];
+            T1[k] = j11 * R[3 + k] + j12 * R[6 + k];
+        }
+        float ST0[3], ST1[3];   // Sigma T0, Sigma T1
 #pragma unroll
         for (int a = 0; a < 3; ++a) {
-            const float gM = 2.0f * (Gs[a][0] * M[0][b] + Gs[a][1] * M[1][b] + Gs[a][2] * M[2][b]);
-            gR[a][b] = gM * s[b];
-            gsb += gM * Rq[a][b];
+            ST0[a] = Sg[a][0] * T0[0] + Sg[a][1] * T0[1] + Sg[a][2] * T0[2];
+            ST1[a] = Sg[a][0] * T1[0] + Sg[a][1] * T1[1] + Sg[a][2] * T1[2];
         }
-        g_ls[3 * id + b] = gsb * s[b];
+        const float ca = dot3(T0, ST0) + 0.3f, cb = dot3(T0, ST1), cc = dot3(T1, ST1) + 0.3f;
+        const float det = ca * cc - cb * cb;
+        const float id2 = 1.0f / (det * det);
+        // conic (A,B,C) = (c, -b, a)/det  ->  gradient w.r.t. (a, b, c)
+        const float gA = g2[2], gB = g2[3], gC = g2[4];
+        const float ga = (-gA * cc * cc + gB * cb * cc - gC * cb * cb) * id2;
+        const float gb = (2.0f * gA * cb * cc - gB * (ca * cc + cb * cb) + 2.0f * gC * ca * cb) * id2;
+        const float gcv = (-gA * cb * cb + gB * ca * cb - gC * ca * ca) * id2;
+        // a = T0.S.T0, b = T0.S.T1, c = T1.S.T1
+        float gT0[3], gT1[3];
+#pragma unroll
+        for (int a = 0; a < 3; ++a) {
+            gT0[a] = 2.0f * ga * ST0[a] + gb * ST1[a];
+            gT1[a] = gb * ST0[a] + 2.0f * gcv * ST1[a];
+        }
+        const float gj00 = gT0[0] * R[0] + gT0[1] * R[1] + gT0[2] * R[2];
+        const float gj02 = gT0[0] * R[6] + gT0[1] * R[7] + gT0[2] * R[8];
+        const float gj11 = gT1[0] * R[3] + gT1[1] * R[4] + gT1[2] * R[5];
+        const float gj12 = gT1[0] * R[6] + gT1[1] * R[7] + gT1[2] * R[8];
+        const float itz2 = itz * itz;
+        float gp[3] = {0.0f, 0.0f, 0.0f};
+        gp[2] -= (gj00 * c.fx + gj11 * c.fy) * itz2;
+        if (clx) {
+            gp[2] += gj02 * c.fx * xr * itz2;
+        } else {
+            gp[0] -= gj02 * c.fx * itz2;
+            gp[2] += 2.0f * gj02 * c.fx * p[0] * itz2 * itz;
+        }
+        if (cly) {
+            gp[2] += gj12 * c.fy * yr * itz2;
+        } else {
+            gp[1] -= gj12 * c.fy * itz2;
+            gp[2] += 2.0f * gj12 * c.fy * p[1] * itz2 * itz;
+        }
+        gp[0] += g2[0] * c.fx * itz;
+        gp[1] += g2[1] * c.fy * itz;
+        gp[2] -= (g2[0] * c.fx * p[0] + g2[1] * c.fy * p[1]) * itz2;
+#pragma unroll
+        for (int k = 0; k < 3; ++k) row[k] = gmu[k] + R[k] * gp[0] + R[3 + k] * gp[1] + R[6 + k] * gp[2];
+        // Sigma = M M^T with symmetric gradient Gs = ga T0T0^T + gb (T0T1^T + T1T0^T)/2 + gc T1T1^T
+        float Gs[3][3];
+#pragma unroll
+        for (int a = 0; a < 3; ++a)
+#pragma unroll
+            for (int b = 0; b < 3; ++b)
+                Gs[a][b] = ga * T0[a] * T0[b] + 0.5f * gb * (T0[a] * T1[b] + T1[a] * T0[b]) + gcv * T1[a] * T1[b];
+        float gR[3][3];
+#pragma unroll
+        for (int b = 0; b < 3; ++b) {
+            float gsb = 0.0f;
+#pragma unroll
+            for (int a = 0; a < 3; ++a) {
+                const float gM = 2.0f * (Gs[a][0] * M[0][b] + Gs[a][1] * M[1][b] + Gs[a][2] * M[2][b]);
+                gR[a][b] = gM * s[b];
+                gsb += gM * Rq[a][b];
+            }
+            row[3 + b] = gsb * s[b];
+        }
+        const float gw = 2.0f * (x * (gR[2][1] - gR[1][2]) + y * (gR[0][2] - gR[2][0]) + z * (gR[1][0] - gR[0][1]));
+        const float gx = 2.0f * (w * (gR[2][1] - gR[1][2]) - 2.0f * x * (gR[1][1] + gR[2][2]) +
+                                 y * (gR[0][1] + gR[1][0]) + z * (gR[0][2] + gR[2][0]));
+        const float gy = 2.0f * (w * (gR[0][2] - gR[2][0]) + x * (gR[0][1] + gR[1][0]) -
+                                 2.0f * y * (gR[0][0] + gR[2][2]) + z * (gR[1][2] + gR[2][1]));
+        const float gz = 2.0f * (w * (gR[1][0] - gR[0][1]) + x * (gR[0][2] + gR[2][0]) + y * (gR[1][2] + gR[2][1]) -
+                                 2.0f * z * (gR[0][0] + gR[1][1]));
+        const float along = w * gw + x * gx + y * gy + z * gz;
+        row[6] = (gw - w * along) * iq;
+        row[7] = (gx - x * along) * iq;
+        row[8] = (gy - y * along) * iq;
+        row[9] = (gz - z * along) * iq;
     }
-    float gw = 2.0f * (x * (gR[2][1] - gR[1][2]) + y * (gR[0][2] - gR[2][0]) + z * (gR[1][0] - gR[0][1]));
-    float gx = 2.0f * (w * (gR[2][1] - gR[1][2]) - 2.0f * x * (gR[1][1] + gR[2][2]) + y * (gR[0][1] + gR[1][0]) +
-                       z * (gR[0][2] + gR[2][0]));
-    float gy = 2.0f * (w * (gR[0][2] - gR[2][0]) + x * (gR[0][1] + gR[1][0]) - 2.0f * y * (gR[0][0] + gR[2][2]) +
-                       z * (gR[1][2] + gR[2][1]));
-    float gz = 2.0f * (w * (gR[1][0] - gR[0][1]) + x * (gR[0][2] + gR[2][0]) + y * (gR[1][2] + gR[2][1]) -
-                       2.0f * z * (gR[0][0] + gR[1][1]));
-    const float along = w * gw + x * gx + y * gy + z * gz;
-    reinterpret_cast<float4*>(g_quat)[id] =
-        make_float4((gw - w * along) * iq, (gx - x * along) * iq, (gy - y * along) * iq, (gz - z * along) * iq);
+    __syncthreads();
+    lds_to_rows<3, 0, ST>(g_mean, s_id, nrows, s_row);
+    lds_to_rows<3, 3, ST>(g_ls, s_id, nrows, s_row);
+    lds_to_rows<4, 6, ST>(g_quat, s_id, nrows, s_row);
+    lds_to_rows<1, 10, ST>(g_op, s_id, nrows, s_row);
+    lds_to_rows<L::SH, 11, ST>(g_sh, s_id, nrows, s_row);
 }
 
 }  // namespace
