@@ -25,43 +25,77 @@ namespace {
 constexpr float kAlphaMin = 1.0f / 255.0f;
 constexpr float kAlphaMax = 0.99f;
 constexpr float kTMin = 1e-4f;
+constexpr float kCutMargin = 1e-3f;   // extra sigma beyond the 1/255 cut-off when bounding a footprint
 
-// alpha of one (pixel, primitive) pair.  The forward and backward kernels both
-// call this, built without contraction, so they take identical decisions.
-#pragma clang fp contract(off)
-struct PairEval {
-    float dx, dy, sigma, e, g, alpha;
+// One pair's primitive as staged in LDS (48 bytes, all lanes read the same
+// record): (u, v, A/2, B), (C/2, opacity, r, g), (b, hx, hy, -).  hx, hy bound
+// the pixel offsets at which o*exp(-sigma) can reach 1/255: for
+// sigma = d^T Q d / 2 <= s the offsets obey |dx| <= sqrt(2 s C / det Q) and
+// |dy| <= sqrt(2 s A / det Q); s = ln(255 o) + kCutMargin keeps every skipped
+// pair at least 0.1% below the threshold, far outside fp32 rounding.
+struct Splat {
+    float4 a, b, c;
 };
 
-__device__ __forceinline__ PairEval eval_pair(float2 m, float4 co, float px, float py) {
-    PairEval r;
-    r.dx = m.x - px;
-    r.dy = m.y - py;
-    r.sigma = fmaf(r.dx, fmaf(0.5f * co.x, r.dx, co.y * r.dy), (0.5f * co.z * r.dy) * r.dy);
-    r.e = __expf(-r.sigma);
-    r.g = co.w * r.e;
-    r.alpha = fminf(kAlphaMax, r.g);
-    return r;
+__device__ __forceinline__ Splat make_splat(float2 m, float4 co, const float* __restrict__ rgb3) {
+    Splat s;
+    s.a = make_float4(m.x, m.y, 0.5f * co.x, co.y);
+    const float cut = logf(255.0f * co.w) + kCutMargin;
+    const float det = co.x * co.z - co.y * co.y;
+    float hx, hy;
+    if (!(cut > 0.0f)) {
+        hx = hy = -1e30f;                 // opacity below 1/255: no pixel can take it
+    } else if (!(det > 0.0f)) {
+        hx = hy = 1e30f;                  // degenerate conic in fp32: never skip
+    } else {
+        hx = sqrtf(2.0f * cut * co.z / det);
+        hy = sqrtf(2.0f * cut * co.x / det);
+    }
+    s.b = make_float4(0.5f * co.z, co.w, rgb3[0], rgb3[1]);
+    s.c = make_float4(rgb3[2], hx, hy, 0.0f);
+    return s;
+}
+
+// Can any pixel centre of the wave's strip [x0,x1] x [y0,y1] reach the cut-off?
+__device__ __forceinline__ bool splat_touches(float4 a, float4 c, float x0, float x1, float y0, float y1) {
+    return (a.x + c.y >= x0) && (a.x - c.y <= x1) && (a.y + c.z >= y0) && (a.y - c.z <= y1);
+}
+
+// sigma of one (pixel, primitive) pair.  Forward and backward both call this
+// on the same staged record, built without contraction, so they take
+// identical decisions.
+#pragma clang fp contract(off)
+__device__ __forceinline__ float splat_sigma(float4 a, float4 b, float px, float py, float& dx, float& dy) {
+    dx = a.x - px;
+    dy = a.y - py;
+    return fmaf(dx, fmaf(a.z, dx, a.w * dy), (b.x * dy) * dy);
 }
 #pragma clang fp contract(on)
 
+__device__ __forceinline__ bool wave_any(bool p) { return __ballot(p) != 0ull; }
+__device__ __forceinline__ bool uniform(bool p) { return __builtin_amdgcn_readfirstlane((int)p) != 0; }
+
+template <bool STATS>
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, float* __restrict__ img, float* __restrict__ final_T, uint32_t* __restrict__ n_contrib,
     uint8_t* __restrict__ active, unsigned long long* __restrict__ pair_stats) {
-    __shared__ float2 s_xy[GS_BLOCK];
-    __shared__ uint32_t s_stat[2][4];
-    __shared__ float4 s_co[GS_BLOCK];
-    __shared__ float s_rgb[3 * GS_BLOCK];
+    __shared__ float4 s_a[GS_BLOCK], s_b[GS_BLOCK], s_c[GS_BLOCK];
     __shared__ uint32_t s_id[GS_BLOCK];
     __shared__ uint32_t s_hit[GS_BLOCK];
+    __shared__ uint32_t s_stat[2][4];
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
-    const int px = (tile % TX) * GS_TILE + (tid % GS_TILE);
-    const int py = (tile / TX) * GS_TILE + (tid / GS_TILE);
+    const int w = tid / GS_WAVE;
+    const int tx = tile % TX, ty = tile / TX;
+    const int px = tx * GS_TILE + (tid % GS_TILE);
+    const int py = ty * GS_TILE + (tid / GS_TILE);
     const bool inside = px < W && py < H;
     const float fx = px + 0.5f, fy = py + 0.5f;
+    // pixel-centre bounds of this wave's 16x4 strip
+    const float wx0 = tx * GS_TILE + 0.5f, wx1 = wx0 + 15.0f;
+    const float wy0 = ty * GS_TILE + 4 * w + 0.5f, wy1 = wy0 + 3.0f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
     float T = 1.0f, c0 = 0.0f, c1 = 0.0f, c2 = 0.0f;
     uint32_t last = 0, n_eval = 0, n_inc = 0;
@@ -71,42 +105,46 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
         const uint32_t j = bs + tid;
         if (j < end) {
             const uint32_t g = vals[j];
+            const Splat sp = make_splat(mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
             s_id[tid] = g;
-            s_xy[tid] = mean2d[g];
-            s_co[tid] = conic_op[g];
-            s_rgb[3 * tid + 0] = rgb[3 * g + 0];
-            s_rgb[3 * tid + 1] = rgb[3 * g + 1];
-            s_rgb[3 * tid + 2] = rgb[3 * g + 2];
+            s_a[tid] = sp.a;
+            s_b[tid] = sp.b;
+            s_c[tid] = sp.c;
         }
         s_hit[tid] = 0;
         __syncthreads();
         const int nb = (int)min((uint32_t)GS_BLOCK, end - bs);
-        for (int k = 0; k < nb && !done; ++k) {
-            const PairEval p = eval_pair(s_xy[k], s_co[k], fx, fy);
-            ++n_eval;
-            if (p.sigma < 0.0f || p.alpha < kAlphaMin) continue;
-            const float Tn = T * (1.0f - p.alpha);
-            if (Tn < kTMin) {
-                done = true;
-                break;
-            }
-            ++n_inc;
-            const float wgt = p.alpha * T;
-            c0 = fmaf(wgt, s_rgb[3 * k + 0], c0);
-            c1 = fmaf(wgt, s_rgb[3 * k + 1], c1);
-            c2 = fmaf(wgt, s_rgb[3 * k + 2], c2);
-            T = Tn;
-            last = bs - start + k + 1;
-            s_hit[k] = 1u;
+        for (int k = 0; k < nb; ++k) {
+            if (STATS) n_eval += done ? 0u : 1u;
+            const float4 a = s_a[k], c = s_c[k];
+            if (!uniform(splat_touches(a, c, wx0, wx1, wy0, wy1))) continue;
+            if (!wave_any(!done)) break;
+            const float4 b = s_b[k];
+            float dx, dy;
+            const float sigma = splat_sigma(a, b, fx, fy, dx, dy);
+            const float alpha = fminf(kAlphaMax, b.y * __expf(-sigma));
+            bool ok = !done && !(sigma < 0.0f) && !(alpha < kAlphaMin);
+            const float Tn = T * (1.0f - alpha);
+            const bool term = ok && (Tn < kTMin);
+            done = done || term;
+            ok = ok && !term;
+            const float wgt = ok ? alpha * T : 0.0f;
+            c0 = fmaf(wgt, b.z, c0);
+            c1 = fmaf(wgt, b.w, c1);
+            c2 = fmaf(wgt, c.x, c2);
+            T = ok ? Tn : T;
+            last = ok ? bs - start + (uint32_t)k + 1u : last;
+            if (STATS) n_inc += ok ? 1u : 0u;
+            if (active != nullptr && wave_any(ok) && lane_id() == 0) s_hit[k] = 1u;
         }
         __syncthreads();
         if (active && j < end && s_hit[tid]) active[s_id[tid]] = 1;
     }
-    if (pair_stats) {
+    if (STATS) {
         const uint32_t e = wave_sum_u32(n_eval), i = wave_sum_u32(n_inc);
         if (lane_id() == 0) {
-            s_stat[0][tid / GS_WAVE] = e;
-            s_stat[1][tid / GS_WAVE] = i;
+            s_stat[0][w] = e;
+            s_stat[1][w] = i;
         }
         __syncthreads();
         if (tid == 0) {
@@ -168,6 +206,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_loss_final(const float* __restrict
 // ---------------------------------------------------------------------------
 
 constexpr int kG = 9;   // du dv dA dB dC dopacity dr dg db
+constexpr int kAtomicLanes = 32;   // up to this many contributing lanes: LDS atomics, else DPP sums
 
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
@@ -175,11 +214,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const uint32_t* __restrict__ pair_offset, int32_t W, int32_t H, int32_t TX, float bg0, float bg1, float bg2,
     const float* __restrict__ final_T, const uint32_t* __restrict__ n_contrib, const float* __restrict__ dL_dimg,
     float* __restrict__ slots) {
-    __shared__ float2 s_xy[GS_BLOCK];
-    __shared__ float4 s_co[GS_BLOCK];
-    __shared__ float s_rgb[3 * GS_BLOCK];
+    __shared__ float4 s_a[GS_BLOCK], s_b[GS_BLOCK], s_c[GS_BLOCK];
     __shared__ uint32_t s_id[GS_BLOCK];
-    __shared__ float s_part[4][kG][GS_BLOCK];
+    __shared__ float s_acc[4][kG][GS_BLOCK];
     __shared__ uint32_t s_max;
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
@@ -189,6 +226,8 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const int py = ty * GS_TILE + (tid / GS_TILE);
     const bool inside = px < W && py < H;
     const float fx = px + 0.5f, fy = py + 0.5f;
+    const float wx0 = tx * GS_TILE + 0.5f, wx1 = wx0 + 15.0f;
+    const float wy0 = ty * GS_TILE + 4 * w + 0.5f, wy1 = wy0 + 3.0f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
     const size_t HW = (size_t)W * H, pix = (size_t)py * W + px;
     float T = inside ? final_T[pix] : 1.0f;
@@ -206,60 +245,73 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     for (int64_t be = n; be > 0; be -= GS_BLOCK) {
         const uint32_t bs = (uint32_t)(be > GS_BLOCK ? be - GS_BLOCK : 0);
         const uint32_t cnt = (uint32_t)be - bs;
-        const uint32_t j = start + bs + tid;
+        const bool work = bs < maxlast;
         uint32_t g = 0;
         if ((uint32_t)tid < cnt) {
-            g = vals[j];
-            s_id[tid] = g;
-            s_xy[tid] = mean2d[g];
-            s_co[tid] = conic_op[g];
-            s_rgb[3 * tid + 0] = rgb[3 * g + 0];
-            s_rgb[3 * tid + 1] = rgb[3 * g + 1];
-            s_rgb[3 * tid + 2] = rgb[3 * g + 2];
+            g = vals[start + bs + tid];
+            if (work) {
+                const Splat sp = make_splat(mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
+                s_a[tid] = sp.a;
+                s_b[tid] = sp.b;
+                s_c[tid] = sp.c;
+            }
+        }
+        if (work) {
+#pragma unroll
+            for (int ww = 0; ww < 4; ++ww)
+#pragma unroll
+                for (int q = 0; q < kG; ++q) s_acc[ww][q][tid] = 0.0f;
         }
         __syncthreads();
-        if (bs < maxlast) {
+        if (work) {
             for (int k = (int)cnt - 1; k >= 0; --k) {
-                float gr[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-                bool contrib = false;
-                if (bs + (uint32_t)k < last) {
-                    const float4 co = s_co[k];
-                    const PairEval p = eval_pair(s_xy[k], co, fx, fy);
-                    if (!(p.sigma < 0.0f) && !(p.alpha < kAlphaMin)) {
-                        contrib = true;
-                        const float om = 1.0f - p.alpha;
-                        T = T / om;
-                        const float inv_om = 1.0f / om;
-                        const float wgt = p.alpha * T;
-                        const float r0 = s_rgb[3 * k + 0], r1 = s_rgb[3 * k + 1], r2 = s_rgb[3 * k + 2];
-                        const float dalpha = gC0 * (T * r0 - S0 * inv_om) + gC1 * (T * r1 - S1 * inv_om) +
-                                             gC2 * (T * r2 - S2 * inv_om);
-                        S0 = fmaf(wgt, r0, S0);
-                        S1 = fmaf(wgt, r1, S1);
-                        S2 = fmaf(wgt, r2, S2);
-                        gr[6] = gC0 * wgt;
-                        gr[7] = gC1 * wgt;
-                        gr[8] = gC2 * wgt;
-                        if (p.g < kAlphaMax) {
-                            gr[5] = dalpha * p.e;
-                            const float ds = -dalpha * p.alpha;
-                            gr[0] = ds * (co.x * p.dx + co.y * p.dy);
-                            gr[1] = ds * (co.y * p.dx + co.z * p.dy);
-                            gr[2] = ds * 0.5f * p.dx * p.dx;
-                            gr[3] = ds * p.dx * p.dy;
-                            gr[4] = ds * 0.5f * p.dy * p.dy;
-                        }
-                    }
+                const float4 a = s_a[k], c = s_c[k];
+                if (!uniform(splat_touches(a, c, wx0, wx1, wy0, wy1))) continue;
+                const bool in_range = bs + (uint32_t)k < last;
+                if (!wave_any(in_range)) continue;
+                const float4 b = s_b[k];
+                float dx, dy;
+                const float sigma = splat_sigma(a, b, fx, fy, dx, dy);
+                const float e = __expf(-sigma);
+                const float gv = b.y * e;
+                const float alpha = fminf(kAlphaMax, gv);
+                const bool ok = in_range && !(sigma < 0.0f) && !(alpha < kAlphaMin);
+                const uint64_t mask = __ballot(ok);
+                if (mask == 0ull) continue;
+                const float inv_om = __builtin_amdgcn_rcpf(1.0f - alpha);
+                const float Tk = ok ? T * inv_om : T;
+                const float wgt = alpha * Tk;
+                const float dalpha = gC0 * (Tk * b.z - S0 * inv_om) + gC1 * (Tk * b.w - S1 * inv_om) +
+                                     gC2 * (Tk * c.x - S2 * inv_om);
+                if (ok) {
+                    S0 = fmaf(wgt, b.z, S0);
+                    S1 = fmaf(wgt, b.w, S1);
+                    S2 = fmaf(wgt, c.x, S2);
+                    T = Tk;
                 }
-                if (__ballot(contrib) != 0ull) {
+                const bool geo = ok && gv < kAlphaMax;      // the 0.99 cap stops d/d(opacity, sigma)
+                const float ds = geo ? -dalpha * alpha : 0.0f;
+                float gr[kG];
+                gr[0] = ds * (2.0f * a.z * dx + a.w * dy);
+                gr[1] = ds * (a.w * dx + 2.0f * b.x * dy);
+                gr[2] = ds * 0.5f * dx * dx;
+                gr[3] = ds * dx * dy;
+                gr[4] = ds * 0.5f * dy * dy;
+                gr[5] = geo ? dalpha * e : 0.0f;
+                gr[6] = ok ? gC0 * wgt : 0.0f;
+                gr[7] = ok ? gC1 * wgt : 0.0f;
+                gr[8] = ok ? gC2 * wgt : 0.0f;
+                if (popc64(mask) <= kAtomicLanes) {
+                    if (ok) {
 #pragma unroll
-                    for (int c = 0; c < kG; ++c) {
-                        const float v = wave_sum(gr[c]);
-                        if (lane_id() == 0) s_part[w][c][k] = v;
+                        for (int q = 0; q < kG; ++q) atomicAdd(&s_acc[w][q][k], gr[q]);
                     }
-                } else if (lane_id() == 0) {
+                } else {
 #pragma unroll
-                    for (int c = 0; c < kG; ++c) s_part[w][c][k] = 0.0f;
+                    for (int q = 0; q < kG; ++q) {
+                        const float v = wave_sum(gr[q]);
+                        if (lane_id() == 0) s_acc[w][q][k] = v;
+                    }
                 }
             }
         }
@@ -268,13 +320,13 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             const ushort4 rc = rect[g];
             const uint32_t slot = pair_offset[g] + (uint32_t)(ty - rc.y) * (uint32_t)(rc.z - rc.x) + (uint32_t)(tx - rc.x);
             float* dst = slots + (size_t)slot * kG;
-            if (bs < maxlast) {
+            if (work) {
 #pragma unroll
-                for (int c = 0; c < kG; ++c)
-                    dst[c] = (s_part[0][c][tid] + s_part[1][c][tid]) + (s_part[2][c][tid] + s_part[3][c][tid]);
+                for (int q = 0; q < kG; ++q)
+                    dst[q] = (s_acc[0][q][tid] + s_acc[1][q][tid]) + (s_acc[2][q][tid] + s_acc[3][q][tid]);
             } else {
 #pragma unroll
-                for (int c = 0; c < kG; ++c) dst[c] = 0.0f;
+                for (int q = 0; q < kG; ++q) dst[q] = 0.0f;
             }
         }
         __syncthreads();
@@ -336,6 +388,8 @@ __device__ __forceinline__ float dot3(const float* a, const float* b) { return a
 // 192-byte SH row is read by consecutive lanes), each thread works on its own
 // row in LDS (odd row stride: conflict-free), and the gradient rows leave the
 // same way.
+constexpr uint32_t kSerialSlots = 32;
+
 template <int DEG>
 struct RowLayout {
     static constexpr int K = (DEG + 1) * (DEG + 1);
@@ -388,21 +442,41 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
     rows_to_lds<4, 6, ST>(quat, s_id, nrows, s_row);
     rows_to_lds<1, 10, ST>(opacity, s_id, nrows, s_row);
     rows_to_lds<L::SH, 11, ST>(sh, s_id, nrows, s_row);
+    // 1. this primitive's 2D gradient: the sum of its pair slots (none if the
+    //    pair list overflowed its capacity).  Short lists are summed by their
+    //    own lane; long ones (a primitive spanning many tiles) by the whole
+    //    wave, 64 slots at a time, so no lane walks thousands of slots alone.
+    float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+    {
+        const uint32_t first = valid ? pair_offset[id] : 0u;
+        const uint32_t nt = valid ? tiles[id] : 0u;
+        const bool fits = (uint64_t)first + nt <= capacity;
+        if (fits && nt <= kSerialSlots) {
+            const float* sl = slots + (size_t)first * kG;
+            for (uint32_t k = 0; k < nt; ++k)
+#pragma unroll
+                for (int q = 0; q < kG; ++q) g2[q] += sl[k * kG + q];
+        }
+        uint64_t big = __ballot(fits && nt > kSerialSlots);
+        while (big) {
+            const int owner = __ffsll((unsigned long long)big) - 1;
+            big &= big - 1;
+            const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)first, owner);
+            const uint32_t nb = (uint32_t)__builtin_amdgcn_readlane((int)nt, owner);
+            float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+            for (uint32_t k = lane_id(); k < nb; k += GS_WAVE)
+#pragma unroll
+                for (int q = 0; q < kG; ++q) acc[q] += slots[((size_t)f + k) * kG + q];
+#pragma unroll
+            for (int q = 0; q < kG; ++q) {
+                const float v = wave_sum(acc[q]);
+                if (lane_id() == owner) g2[q] = v;
+            }
+        }
+    }
     __syncthreads();
     if (valid) {
         float* row = s_row + tid * ST;
-        // 1. this primitive's 2D gradient: its pair slots in order (none if the
-        //    pair list overflowed its capacity)
-        float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-        {
-            const uint64_t first = pair_offset[id];
-            const uint32_t nt = tiles[id];
-            const float* sl = slots + first * kG;
-            if (first + nt <= capacity)
-                for (uint32_t k = 0; k < nt; ++k)
-#pragma unroll
-                    for (int q = 0; q < kG; ++q) g2[q] += sl[k * kG + q];
-        }
         if (grad2d) {
 #pragma unroll
             for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
@@ -571,10 +645,17 @@ hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const ui
                              uint8_t* active, uint64_t* pair_stats, hipStream_t st) {
     const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
     if (TX * TY == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_raster_fwd, dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
-                       reinterpret_cast<const float2*>(proj.mean2d), reinterpret_cast<const float4*>(proj.conic_opacity),
-                       proj.rgb, width, height, TX, bg[0], bg[1], bg[2], img, final_T, n_contrib, active,
-                       reinterpret_cast<unsigned long long*>(pair_stats));
+    if (pair_stats)
+        hipLaunchKernelGGL(k_raster_fwd<true>, dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
+                           reinterpret_cast<const float2*>(proj.mean2d),
+                           reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, width, height, TX, bg[0],
+                           bg[1], bg[2], img, final_T, n_contrib, active,
+                           reinterpret_cast<unsigned long long*>(pair_stats));
+    else
+        hipLaunchKernelGGL(k_raster_fwd<false>, dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
+                           reinterpret_cast<const float2*>(proj.mean2d),
+                           reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, width, height, TX, bg[0],
+                           bg[1], bg[2], img, final_T, n_contrib, active, nullptr);
     return hipGetLastError();
 }
 
