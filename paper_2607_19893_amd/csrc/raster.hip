@@ -75,6 +75,30 @@ __device__ __forceinline__ float splat_sigma(float4 a, float4 b, float px, float
 __device__ __forceinline__ bool wave_any(bool p) { return __ballot(p) != 0ull; }
 __device__ __forceinline__ bool uniform(bool p) { return __builtin_amdgcn_readfirstlane((int)p) != 0; }
 
+// Per batch, each wave first compacts the batch entries whose footprint can
+// reach its 16x4 strip into a wave-private LDS list (ascending, via ballots),
+// then walks only that list.  Only the wave itself reads its list, so a
+// wave-level barrier orders the writes before the reads.
+__device__ __forceinline__ uint32_t compact_touching(const float4* s_a, const float4* s_c, int nb, float x0,
+                                                     float x1, float y0, float y1, uint32_t limit,
+                                                     uint8_t* list) {
+    const int lane = lane_id();
+    const uint64_t lt = lanemask_lt();
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int r = 0; r < GS_BLOCK / GS_WAVE; ++r) {
+        const int k = r * GS_WAVE + lane;
+        const bool t = k < nb && (uint32_t)k < limit && splat_touches(s_a[k], s_c[k], x0, x1, y0, y1);
+        const uint64_t m = __ballot(t);
+        if (t) list[cnt + popc64(m & lt)] = (uint8_t)k;
+        cnt += popc64(m);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    return cnt;
+}
+
 template <bool STATS>
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
@@ -84,6 +108,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     __shared__ float4 s_a[GS_BLOCK], s_b[GS_BLOCK], s_c[GS_BLOCK];
     __shared__ uint32_t s_id[GS_BLOCK];
     __shared__ uint32_t s_hit[GS_BLOCK];
+    __shared__ uint8_t s_list[4][GS_BLOCK];
     __shared__ uint32_t s_stat[2][4];
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
@@ -98,8 +123,8 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const float wy0 = ty * GS_TILE + 4 * w + 0.5f, wy1 = wy0 + 3.0f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
     float T = 1.0f, c0 = 0.0f, c1 = 0.0f, c2 = 0.0f;
-    uint32_t last = 0, n_eval = 0, n_inc = 0;
-    bool done = !inside;
+    uint32_t last = 0, n_inc = 0, term_at = 0;
+    bool done = !inside, terminated = false;
     for (uint32_t bs = start; bs < end; bs += GS_BLOCK) {
         if (__syncthreads_count(done) == GS_BLOCK) break;
         const uint32_t j = bs + tid;
@@ -114,18 +139,21 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
         s_hit[tid] = 0;
         __syncthreads();
         const int nb = (int)min((uint32_t)GS_BLOCK, end - bs);
-        for (int k = 0; k < nb; ++k) {
-            if (STATS) n_eval += done ? 0u : 1u;
-            const float4 a = s_a[k], c = s_c[k];
-            if (!uniform(splat_touches(a, c, wx0, wx1, wy0, wy1))) continue;
+        const uint32_t cnt = wave_any(!done) ? compact_touching(s_a, s_c, nb, wx0, wx1, wy0, wy1, GS_BLOCK, s_list[w])
+                                              : 0u;
+        for (uint32_t i = 0; i < cnt; ++i) {
             if (!wave_any(!done)) break;
-            const float4 b = s_b[k];
+            const int k = s_list[w][i];
+            const float4 a = s_a[k], b = s_b[k], c = s_c[k];
             float dx, dy;
             const float sigma = splat_sigma(a, b, fx, fy, dx, dy);
             const float alpha = fminf(kAlphaMax, b.y * __expf(-sigma));
             bool ok = !done && !(sigma < 0.0f) && !(alpha < kAlphaMin);
             const float Tn = T * (1.0f - alpha);
             const bool term = ok && (Tn < kTMin);
+            const uint32_t pos = bs - start + (uint32_t)k;
+            if (STATS && term) term_at = pos;
+            terminated = terminated || term;
             done = done || term;
             ok = ok && !term;
             const float wgt = ok ? alpha * T : 0.0f;
@@ -133,7 +161,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
             c1 = fmaf(wgt, b.w, c1);
             c2 = fmaf(wgt, c.x, c2);
             T = ok ? Tn : T;
-            last = ok ? bs - start + (uint32_t)k + 1u : last;
+            last = ok ? pos + 1u : last;
             if (STATS) n_inc += ok ? 1u : 0u;
             if (active != nullptr && wave_any(ok) && lane_id() == 0) s_hit[k] = 1u;
         }
@@ -141,6 +169,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
         if (active && j < end && s_hit[tid]) active[s_id[tid]] = 1;
     }
     if (STATS) {
+        // entries the per-pixel definition examines: up to and including the
+        // terminating one, else the whole list
+        const uint32_t n_eval = !inside ? 0u : (terminated ? term_at + 1u : end - start);
         const uint32_t e = wave_sum_u32(n_eval), i = wave_sum_u32(n_inc);
         if (lane_id() == 0) {
             s_stat[0][w] = e;
@@ -217,6 +248,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     __shared__ float4 s_a[GS_BLOCK], s_b[GS_BLOCK], s_c[GS_BLOCK];
     __shared__ uint32_t s_id[GS_BLOCK];
     __shared__ float s_acc[4][kG][GS_BLOCK];
+    __shared__ uint8_t s_list[4][GS_BLOCK];
     __shared__ uint32_t s_max;
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
@@ -241,6 +273,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     if (last > 0) atomicMax(&s_max, last);
     __syncthreads();
     const uint32_t maxlast = s_max;
+    uint32_t wave_last = last;     // largest n_contrib among this wave's pixels
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) wave_last = max(wave_last, (uint32_t)__shfl_xor((int)wave_last, d, GS_WAVE));
     const uint32_t n = end - start;
     for (int64_t be = n; be > 0; be -= GS_BLOCK) {
         const uint32_t bs = (uint32_t)(be > GS_BLOCK ? be - GS_BLOCK : 0);
@@ -264,12 +299,12 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
         }
         __syncthreads();
         if (work) {
-            for (int k = (int)cnt - 1; k >= 0; --k) {
-                const float4 a = s_a[k], c = s_c[k];
-                if (!uniform(splat_touches(a, c, wx0, wx1, wy0, wy1))) continue;
+            const uint32_t limit = wave_last > bs ? wave_last - bs : 0u;
+            const uint32_t nl = limit ? compact_touching(s_a, s_c, (int)cnt, wx0, wx1, wy0, wy1, limit, s_list[w]) : 0u;
+            for (int i = (int)nl - 1; i >= 0; --i) {
+                const int k = s_list[w][i];
+                const float4 a = s_a[k], b = s_b[k], c = s_c[k];
                 const bool in_range = bs + (uint32_t)k < last;
-                if (!wave_any(in_range)) continue;
-                const float4 b = s_b[k];
                 float dx, dy;
                 const float sigma = splat_sigma(a, b, fx, fy, dx, dy);
                 const float e = __expf(-sigma);
