@@ -188,14 +188,16 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
  *   ranges [T,2] uint32       [start, end) of each tile's pairs, T = tiles in the image
  *   pair_offset [n] uint32    per visible primitive: first of its pairs in
  *                             emission order (rectangle row-major); read by gs_raster_bwd
+ *   pair_perm [capacity] uint32  sorted position of every pair, indexed by
+ *                             emission order (pair_offset[id] + tile number in the rectangle)
  *   keys   [capacity] uint64 or NULL: (tile << 32) | bits(depth) per sorted pair
  *   num_pairs: one uint32 on the device (the pair count, also on overflow)
  *   ws: gs_workspace_bytes(GS_WS_BIN_SORT, n, capacity, width, height) bytes
  */
 gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                       int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                      uint32_t* pair_offset, uint64_t* keys, uint32_t* num_pairs, gs_device_status* status,
-                      void* ws, size_t ws_bytes, void* stream);
+                      uint32_t* pair_offset, uint32_t* pair_perm, uint64_t* keys, uint32_t* num_pairs,
+                      gs_device_status* status, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Phase "rendering", part 2 (R in Figure 6): front-to-back alpha blending of
@@ -228,7 +230,7 @@ gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32
  * Phase "backward" (B in Figure 6; Shadow Graph step 2 of Section 4.3): the
  * analytic derivative of the rendered view, first w.r.t. each pair's 2D
  * quantities (replayed back to front per pixel from final_T and n_contrib),
- * summed per primitive in a fixed order (no floating-point atomics), then
+ * summed per primitive in a fixed order, then
  * chained through projection and colour to the parameters.  grad_norm is the
  * per-primitive gradient evidence g(p) of Section 2.1 that the post-backward
  * hook of Section 5 reports: |dL/d(u,v)| of this view.
@@ -238,7 +240,8 @@ gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32
  *   ws: gs_workspace_bytes(GS_WS_RASTER_BWD, n, capacity, W, H); capacity as in gs_bin_sort
  */
 gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
-                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* vis_idx,
+                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
+                        const uint32_t* vis_idx,
                         const uint32_t* vis_count, uint32_t capacity, const float* final_T,
                         const uint32_t* n_contrib, const float* dL_dimg, const float* bg, const gs_scene* grads,
                         float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream);

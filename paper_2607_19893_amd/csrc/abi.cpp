@@ -127,8 +127,8 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
 
 gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                       int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                      uint32_t* pair_offset, uint64_t* keys, uint32_t* num_pairs, gs_device_status* status,
-                      void* ws, size_t ws_bytes, void* stream) {
+                      uint32_t* pair_offset, uint32_t* pair_perm, uint64_t* keys, uint32_t* num_pairs,
+                      gs_device_status* status, void* ws, size_t ws_bytes, void* stream) {
     gs_status s;
     if ((s = check_proj(proj, false, "gs_bin_sort")) != GS_OK) return s;
     GS_REQUIRE(n >= 0 && width >= 0 && height >= 0, "gs_bin_sort: negative size");
@@ -136,11 +136,12 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
         return fail(GS_ERR_UNSUPPORTED, "gs_bin_sort: image side above %d", GS_MAX_IMAGE_SIDE);
     GS_REQUIRE(vis_idx && vis_count && ranges && pair_offset && num_pairs && status && ws,
                "gs_bin_sort: null pointer");
-    GS_REQUIRE(capacity == 0 || vals, "gs_bin_sort: null vals");
+    GS_REQUIRE(capacity == 0 || (vals && pair_perm), "gs_bin_sort: null vals / pair_perm");
     if (ws_bytes < gsmi::binsort_ws_bytes(n, capacity, width, height))
         return fail(GS_ERR_WORKSPACE, "gs_bin_sort: workspace too small");
     return hip_status(gsmi::launch_binsort(*proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges,
-                                           pair_offset, keys, num_pairs, status, ws, static_cast<hipStream_t>(stream)),
+                                           pair_offset, pair_perm, keys, num_pairs, status, ws,
+                                           static_cast<hipStream_t>(stream)),
                       "gs_bin_sort");
 }
 
@@ -170,7 +171,8 @@ gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32
 }
 
 gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
-                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* vis_idx,
+                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
+                        const uint32_t* vis_idx,
                         const uint32_t* vis_count, uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
                         const float* dL_dimg, const float* bg, const gs_scene* grads, float* grad2d, float* grad_norm,
                         void* ws, size_t ws_bytes, void* stream) {
@@ -180,12 +182,14 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
     GS_REQUIRE(grads->n == scene->n && grads->sh_degree == scene->sh_degree, "gs_raster_bwd: grads shape differs");
     if ((s = check_camera(cam, "gs_raster_bwd")) != GS_OK) return s;
     if ((s = check_proj(proj, true, "gs_raster_bwd")) != GS_OK) return s;
-    GS_REQUIRE(vals && ranges && pair_offset && vis_idx && vis_count && final_T && n_contrib && dL_dimg && bg && ws,
+    GS_REQUIRE(vals && ranges && pair_offset && pair_perm && vis_idx && vis_count && final_T && n_contrib && dL_dimg &&
+                   bg && ws,
                "gs_raster_bwd: null pointer");
     if (ws_bytes < gsmi::raster_bwd_ws_bytes(scene->n, capacity))
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
-    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, vals, ranges, pair_offset, vis_idx, vis_count, capacity,
+    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, vals, ranges, pair_offset, pair_perm, vis_idx,
+                                              vis_count, capacity,
                                               final_T, n_contrib, dL_dimg, bg, *grads, grad2d, grad_norm, ws,
                                               static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd");

@@ -258,18 +258,27 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
     }
 }
 
+// Tile ranges, optional 64-bit keys, and the emission->sorted permutation
+// (pair_perm[pair_offset[id] + local tile number] = sorted position).
 __global__ void __launch_bounds__(GS_BLOCK) k_finalize(const uint32_t* __restrict__ skeys,
                                                        const uint32_t* __restrict__ svals,
                                                        const uint32_t* __restrict__ sort_count,
                                                        const float* __restrict__ depth,
-                                                       uint32_t* __restrict__ ranges, uint64_t* __restrict__ keys64) {
+                                                       const ushort4* __restrict__ rect,
+                                                       const uint32_t* __restrict__ pair_offset, int32_t tiles_x,
+                                                       uint32_t* __restrict__ ranges, uint64_t* __restrict__ keys64,
+                                                       uint32_t* __restrict__ pair_perm) {
     const uint32_t M = *sort_count;
     const uint32_t i = blockIdx.x * GS_BLOCK + threadIdx.x;
     if (i >= M) return;
     const uint32_t t = skeys[i];
+    const uint32_t g = svals[i];
     if (i == 0 || skeys[i - 1] != t) ranges[2 * t] = i;
     if (i == M - 1 || skeys[i + 1] != t) ranges[2 * t + 1] = i + 1;
-    if (keys64) keys64[i] = ((uint64_t)t << 32) | (uint64_t)__float_as_uint(depth[svals[i]]);
+    if (keys64) keys64[i] = ((uint64_t)t << 32) | (uint64_t)__float_as_uint(depth[g]);
+    const ushort4 rc = rect[g];
+    const uint32_t ty = t / (uint32_t)tiles_x, tx = t - ty * (uint32_t)tiles_x;
+    pair_perm[pair_offset[g] + (ty - rc.y) * (uint32_t)(rc.z - rc.x) + (tx - rc.x)] = i;
 }
 
 struct BinsortLayout {
@@ -331,8 +340,8 @@ size_t binsort_ws_bytes(int32_t n, uint32_t capacity, int32_t, int32_t) { return
 
 hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                           int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                          uint32_t* pair_offset, uint64_t* keys, uint32_t* num_pairs, gs_device_status* status,
-                          void* ws, hipStream_t st) {
+                          uint32_t* pair_offset, uint32_t* pair_perm, uint64_t* keys, uint32_t* num_pairs,
+                          gs_device_status* status, void* ws, hipStream_t st) {
     const BinsortLayout L = binsort_layout(n, capacity);
     const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
     const uint32_t T = (uint32_t)TX * (uint32_t)TY;
@@ -376,7 +385,8 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     // 4. tile ranges (+ optional 64-bit keys)
     if (capacity > 0)
         hipLaunchKernelGGL(k_finalize, dim3(div_up(capacity, GS_BLOCK)), dim3(GS_BLOCK), 0, st,
-                           at<uint32_t>(ws, L.pk[2]), vals, ctr + 1, proj.depth, ranges, keys);
+                           at<uint32_t>(ws, L.pk[2]), vals, ctr + 1, proj.depth,
+                           reinterpret_cast<const ushort4*>(proj.rect), pair_offset, TX, ranges, keys, pair_perm);
     return hipGetLastError();
 }
 

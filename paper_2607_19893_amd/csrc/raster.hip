@@ -237,14 +237,14 @@ __global__ void __launch_bounds__(GS_BLOCK) k_loss_final(const float* __restrict
 // ---------------------------------------------------------------------------
 
 constexpr int kG = 9;   // du dv dA dB dC dopacity dr dg db
-constexpr int kAtomicLanes = 32;   // up to this many contributing lanes: LDS atomics, else DPP sums
+constexpr int kAtomicLanes = 4;    // up to this many contributing lanes: LDS atomics, else row sums first
+constexpr int kSlot = 12;          // floats per pair slot (9 used, padded for 16-byte stores)
 
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
-    const float4* __restrict__ conic_op, const float* __restrict__ rgb, const ushort4* __restrict__ rect,
-    const uint32_t* __restrict__ pair_offset, int32_t W, int32_t H, int32_t TX, float bg0, float bg1, float bg2,
-    const float* __restrict__ final_T, const uint32_t* __restrict__ n_contrib, const float* __restrict__ dL_dimg,
-    float* __restrict__ slots) {
+    const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
+    float bg1, float bg2, const float* __restrict__ final_T, const uint32_t* __restrict__ n_contrib,
+    const float* __restrict__ dL_dimg, float* __restrict__ slots) {
     __shared__ float4 s_a[GS_BLOCK], s_b[GS_BLOCK], s_c[GS_BLOCK];
     __shared__ uint32_t s_id[GS_BLOCK];
     __shared__ float s_acc[4][kG][GS_BLOCK];
@@ -281,9 +281,8 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
         const uint32_t bs = (uint32_t)(be > GS_BLOCK ? be - GS_BLOCK : 0);
         const uint32_t cnt = (uint32_t)be - bs;
         const bool work = bs < maxlast;
-        uint32_t g = 0;
         if ((uint32_t)tid < cnt) {
-            g = vals[start + bs + tid];
+            const uint32_t g = vals[start + bs + tid];
             if (work) {
                 const Splat sp = make_splat(mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
                 s_a[tid] = sp.a;
@@ -337,32 +336,37 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
                 gr[7] = ok ? gC1 * wgt : 0.0f;
                 gr[8] = ok ? gC2 * wgt : 0.0f;
                 if (popc64(mask) <= kAtomicLanes) {
+                    // few contributing lanes: add them straight into the wave's accumulator
                     if (ok) {
 #pragma unroll
                         for (int q = 0; q < kG; ++q) atomicAdd(&s_acc[w][q][k], gr[q]);
                     }
                 } else {
+                    // sum each 16-lane row (one pixel row of the strip) with DPP, then
+                    // one lane per contributing row adds the row sum
 #pragma unroll
-                    for (int q = 0; q < kG; ++q) {
-                        const float v = wave_sum(gr[q]);
-                        if (lane_id() == 0) s_acc[w][q][k] = v;
+                    for (int q = 0; q < kG; ++q) gr[q] = dpp_row_sum(gr[q]);
+                    const int lane = lane_id();
+                    if ((lane & 15) == 0 && ((mask >> lane) & 0xFFFFull) != 0ull) {
+#pragma unroll
+                        for (int q = 0; q < kG; ++q) atomicAdd(&s_acc[w][q][k], gr[q]);
                     }
                 }
             }
         }
         __syncthreads();
         if ((uint32_t)tid < cnt) {
-            const ushort4 rc = rect[g];
-            const uint32_t slot = pair_offset[g] + (uint32_t)(ty - rc.y) * (uint32_t)(rc.z - rc.x) + (uint32_t)(tx - rc.x);
-            float* dst = slots + (size_t)slot * kG;
+            // the pair's slot is its sorted position: consecutive threads write consecutive slots
+            float v[kSlot] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
             if (work) {
 #pragma unroll
                 for (int q = 0; q < kG; ++q)
-                    dst[q] = (s_acc[0][q][tid] + s_acc[1][q][tid]) + (s_acc[2][q][tid] + s_acc[3][q][tid]);
-            } else {
-#pragma unroll
-                for (int q = 0; q < kG; ++q) dst[q] = 0.0f;
+                    v[q] = (s_acc[0][q][tid] + s_acc[1][q][tid]) + (s_acc[2][q][tid] + s_acc[3][q][tid]);
             }
+            float4* dst = reinterpret_cast<float4*>(slots + (size_t)(start + bs + tid) * kSlot);
+            dst[0] = make_float4(v[0], v[1], v[2], v[3]);
+            dst[1] = make_float4(v[4], v[5], v[6], v[7]);
+            dst[2] = make_float4(v[8], v[9], v[10], v[11]);
         }
         __syncthreads();
     }
@@ -454,7 +458,8 @@ __device__ __forceinline__ void lds_to_rows(float* __restrict__ dst, const uint3
 template <int DEG>
 __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
     const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
-    const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, const uint8_t* __restrict__ clampm,
+    const uint32_t* __restrict__ pair_offset, const uint32_t* __restrict__ pair_perm, const float* __restrict__ slots,
+    const uint8_t* __restrict__ clampm,
     const float* __restrict__ mean, const float* __restrict__ log_scale, const float* __restrict__ quat,
     const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c, uint32_t capacity,
     float* __restrict__ g_mean, float* __restrict__ g_ls, float* __restrict__ g_quat, float* __restrict__ g_op,
@@ -487,10 +492,12 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
         const uint32_t nt = valid ? tiles[id] : 0u;
         const bool fits = (uint64_t)first + nt <= capacity;
         if (fits && nt <= kSerialSlots) {
-            const float* sl = slots + (size_t)first * kG;
-            for (uint32_t k = 0; k < nt; ++k)
-#pragma unroll
-                for (int q = 0; q < kG; ++q) g2[q] += sl[k * kG + q];
+            for (uint32_t k = 0; k < nt; ++k) {
+                const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)pair_perm[first + k] * kSlot);
+                const float4 v0 = sl[0], v1 = sl[1], v2 = sl[2];
+                g2[0] += v0.x; g2[1] += v0.y; g2[2] += v0.z; g2[3] += v0.w;
+                g2[4] += v1.x; g2[5] += v1.y; g2[6] += v1.z; g2[7] += v1.w; g2[8] += v2.x;
+            }
         }
         uint64_t big = __ballot(fits && nt > kSerialSlots);
         while (big) {
@@ -499,9 +506,12 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
             const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)first, owner);
             const uint32_t nb = (uint32_t)__builtin_amdgcn_readlane((int)nt, owner);
             float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-            for (uint32_t k = lane_id(); k < nb; k += GS_WAVE)
-#pragma unroll
-                for (int q = 0; q < kG; ++q) acc[q] += slots[((size_t)f + k) * kG + q];
+            for (uint32_t k = lane_id(); k < nb; k += GS_WAVE) {
+                const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)pair_perm[f + k] * kSlot);
+                const float4 v0 = sl[0], v1 = sl[1], v2 = sl[2];
+                acc[0] += v0.x; acc[1] += v0.y; acc[2] += v0.z; acc[3] += v0.w;
+                acc[4] += v1.x; acc[5] += v1.y; acc[6] += v1.z; acc[7] += v1.w; acc[8] += v2.x;
+            }
 #pragma unroll
             for (int q = 0; q < kG; ++q) {
                 const float v = wave_sum(acc[q]);
@@ -712,11 +722,12 @@ hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, 
 }
 
 size_t raster_bwd_ws_bytes(int32_t, uint32_t capacity) {
-    return align256(sizeof(float) * kG * (size_t)(capacity > 0 ? capacity : 1));
+    return align256(sizeof(float) * kSlot * (size_t)(capacity > 0 ? capacity : 1));
 }
 
 hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
-                             const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* vis_idx,
+                             const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
+                             const uint32_t* vis_idx,
                              const uint32_t* vis_count, uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
                              const float* dL_dimg, const float bg[3], const gs_scene& grads, float* grad2d,
                              float* grad_norm, void* ws, hipStream_t st) {
@@ -725,15 +736,14 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
     if (T > 0)
         hipLaunchKernelGGL(k_raster_bwd, dim3(T), dim3(GS_BLOCK), 0, st, ranges, vals,
                            reinterpret_cast<const float2*>(proj.mean2d),
-                           reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb,
-                           reinterpret_cast<const ushort4*>(proj.rect), pair_offset, cam.width, cam.height,
+                           reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, cam.width, cam.height,
                            cam.tiles_x, bg[0], bg[1], bg[2], final_T, n_contrib, dL_dimg, slots);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || scene.n == 0) return e;
     const dim3 grid(div_up(scene.n, GS_BLOCK));
 #define GS_LAUNCH_PBWD(D)                                                                                        \
     hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset, \
-                       slots, proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam,     \
+                       pair_perm, slots, proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam,     \
                        capacity, grads.mean, grads.log_scale, grads.quat, grads.opacity, grads.sh, grad2d, grad_norm)
     switch (scene.sh_degree) {
         case 0: GS_LAUNCH_PBWD(0); break;

@@ -65,11 +65,11 @@ _lib.gs_delta_msg_bytes.restype = sz
 _lib.gs_delta_msg_bytes.argtypes = [u32, i32, i32]
 _lib.gs_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P]
 _lib.gs_visible_set.argtypes = [i32, P, i32, P, P, P, sz, P]
-_lib.gs_bin_sort.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, u32, P, P, P, P, P, P, P, sz, P]
+_lib.gs_bin_sort.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, u32, P, P, P, P, P, P, P, P, sz, P]
 _lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, P, P, P, P, P, P]
 _lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
 _lib.gs_raster_bwd.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P, P, P,
-                               P, P, u32, P, P, P, P, ctypes.POINTER(gs_scene), P, P, P, sz, P]
+                               P, P, P, u32, P, P, P, P, ctypes.POINTER(gs_scene), P, P, P, sz, P]
 _lib.gs_sparse_adam.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, i32, ctypes.c_double,
                                 ctypes.c_double, ctypes.c_double, P]
 _lib.gs_delta_pack.argtypes = [P, P, i32, ctypes.POINTER(gs_group), i32, u32, P, sz, P, P]
@@ -164,11 +164,12 @@ def gs_visible_set(kind, src, n, out_idx, out_count, ws, stream=None):
                                                         stream if stream is not None else current_stream()))
 
 
-def gs_bin_sort(proj: gs_proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges, pair_offset, keys,
-                num_pairs, status, ws, stream=None):
+def gs_bin_sort(proj: gs_proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges, pair_offset,
+                pair_perm, keys, num_pairs, status, ws, stream=None):
     return _check("gs_bin_sort", _lib.gs_bin_sort(ctypes.byref(proj), int(n), ptr(vis_idx), ptr(vis_count),
                                                   int(width), int(height), int(capacity), ptr(vals), ptr(ranges),
-                                                  ptr(pair_offset), ptr(keys), ptr(num_pairs), ptr(status), ptr(ws),
+                                                  ptr(pair_offset), ptr(pair_perm), ptr(keys), ptr(num_pairs),
+                                                  ptr(status), ptr(ws),
                                                   ws.numel() * ws.element_size(),
                                                   stream if stream is not None else current_stream()))
 
@@ -193,11 +194,13 @@ def gs_loss_l1(img, target, width, height, loss, dL_dimg, ws, stream=None):
                                                 stream if stream is not None else current_stream()))
 
 
-def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, pair_offset, vis_idx, vis_count,
-                  capacity, final_T, n_contrib, dL_dimg, bg, grads: gs_scene, grad2d, grad_norm, ws, stream=None):
+def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, pair_offset, pair_perm, vis_idx,
+                  vis_count, capacity, final_T, n_contrib, dL_dimg, bg, grads: gs_scene, grad2d, grad_norm, ws,
+                  stream=None):
     b = _bg(bg)
     return _check("gs_raster_bwd", _lib.gs_raster_bwd(ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj),
-                                                      ptr(vals), ptr(ranges), ptr(pair_offset), ptr(vis_idx),
+                                                      ptr(vals), ptr(ranges), ptr(pair_offset), ptr(pair_perm),
+                                                      ptr(vis_idx),
                                                       ptr(vis_count), int(capacity), ptr(final_T), ptr(n_contrib),
                                                       ptr(dL_dimg), ctypes.cast(b, P), ctypes.byref(grads),
                                                       ptr(grad2d), ptr(grad_norm), ptr(ws),
