@@ -221,9 +221,22 @@ AMB_CAP = 4e-6
 AMB_LOSS = 4e-6
 
 
+FLAG_AMB_PIXEL = 1   # examined by a pixel whose decisions or loss sign are within the bands
+FLAG_NEAR_CAP = 2    # has an included pair within AMB_CAP of the 0.99 alpha cap
+
+
+def ambiguous_pixels(rnd: "Render", loss_margin=None, amb_alpha=AMB_ALPHA, amb_T=AMB_T, amb_loss=AMB_LOSS):
+    """[H,W] mask of pixels whose result (or loss sign) the fp32 kernel may decide differently."""
+    amb = (rnd.margin_alpha < amb_alpha) | (rnd.margin_T < amb_T)
+    if loss_margin is not None:
+        amb |= (np.abs(np.asarray(loss_margin)) < amb_loss).any(axis=0)
+    return amb
+
+
 def render_backward(vis, proj: Projection, cam, dL_dimg, bg=(0.0, 0.0, 0.0), loss_margin=None,
                     amb_alpha=AMB_ALPHA, amb_T=AMB_T, amb_cap=AMB_CAP, amb_loss=AMB_LOSS):
-    """d loss / d(u, v, A, B, C, opacity, rgb) per visible primitive, plus ambiguity flags."""
+    """d loss / d(u, v, A, B, C, opacity, rgb) per visible primitive, plus flags
+    (FLAG_AMB_PIXEL | FLAG_NEAR_CAP bits per primitive)."""
     W, H = cam.width, cam.height
     n = proj.radius.size
     vis = np.ascontiguousarray(vis, np.uint32)

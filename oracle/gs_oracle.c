@@ -667,10 +667,11 @@ void orc_render(int64_t nvis, const uint32_t* vis, const int32_t* rect, const fl
  *
  * grad2d[9*j] = (du, dv, dA, dB, dC, dopacity, dr, dg, db), summed over the
  * pixels in a fixed tile order (deterministic).  Rows of invisible primitives
- * are zeroed.  flag[j] (if not NULL) is set when j was examined by a pixel
- * whose margins fall below (amb_alpha, amb_T), or whose loss sign is close
- * (|loss_margin| < amb_loss, if loss_margin != NULL), or when one of its
- * included pairs sits within amb_cap of the 0.99 cap.
+ * are zeroed.  flag[j] (if not NULL) gets bit 0 when j was examined by a
+ * pixel whose margins fall below (amb_alpha, amb_T), or whose loss sign is
+ * close (|loss_margin| < amb_loss, if loss_margin != NULL), and bit 1 when one
+ * of its included pairs sits within amb_cap of the 0.99 cap (where the
+ * derivative w.r.t. opacity and sigma jumps).
  */
 void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect, const float* depth,
                          const double* mean2d, const double* conic, const double* opacity, const double* rgb,
@@ -720,7 +721,7 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
                         for (int ch = 0; ch < 3; ++ch) if (fabs(loss_margin[ch * HW + p]) < amb_loss) amb = 1;
                     if (amb) {
                         int upto = (r.margin_T < amb_T) ? nl : r.n_seen;
-                        for (int k = 0; k < upto; ++k) tf[k] = 1;
+                        for (int k = 0; k < upto; ++k) tf[k] |= 1;
                     }
                     /* suffix sum S, walking back to front */
                     double S[3] = {r.T * bg[0], r.T * bg[1], r.T * bg[2]};
@@ -735,7 +736,7 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
                             dalpha += gC[ch] * (e->T * c[ch] - sk);
                             g[6 + ch] += gC[ch] * e->alpha * e->T;
                         }
-                        if (e->capped || fabs(e->g - ORC_ALPHA_MAX) / ORC_ALPHA_MAX < amb_cap) tf[e->pos] = 1;
+                        if (fabs(e->g - ORC_ALPHA_MAX) / ORC_ALPHA_MAX < amb_cap) tf[e->pos] |= 2;
                         if (!e->capped) {
                             double A = conic[3 * j], B = conic[3 * j + 1], Cc = conic[3 * j + 2];
                             g[5] += dalpha * e->e;
@@ -760,7 +761,7 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
     for (int64_t i = 0; i < toff[T]; ++i) {
         uint32_t j = accj[i];
         for (int c = 0; c < 9; ++c) grad2d[9 * (size_t)j + c] += acc[9 * (size_t)i + c];
-        if (flag && accf[i]) flag[j] = 1;
+        if (flag) flag[j] |= accf[i];
     }
     (void)n;
     free(acc); free(accj); free(accf); free(toff);

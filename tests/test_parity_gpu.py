@@ -170,20 +170,29 @@ def test_loss_l1(case, torch_gpu, orc):
     assert abs(tr.loss.item() - loss) <= 1e-5 * abs(loss)
 
 
-def _bwd_compare(w, tr, cam, orc, dL, case, check_flags=True):
+def masked_upstream(orc, w, cam, dL, loss_margin=None):
+    """dL with the ambiguous pixels zeroed: a pixel's decisions reach the
+    gradients only through its own upstream gradient, so with dL = 0 there the
+    fp32 and fp64 sides must agree on every primitive."""
     ref = orc.project(w.scene, cam, 0)
     vis = orc.visible(ref.tiles)
-    g2, flag = orc.render_backward(vis, ref, cam, dL)
+    rn = orc.render(vis, ref, cam)
+    amb = orc.ambiguous_pixels(rn, loss_margin)
+    return np.where(amb[None, :, :], 0.0, np.asarray(dL, np.float64)), amb, ref, vis
+
+
+def bwd_compare(w, tr, orc, ref, vis, dL_masked, case):
+    cam = tr.cam
+    g2, flag = orc.render_backward(vis, ref, cam, dL_masked)
     gr = orc.project_backward(w.scene, cam, vis, g2, ref)
     ok = np.zeros(w.scene.n, bool)
     ok[vis] = True
-    ok &= flag == 0
+    ok &= (flag & orc.FLAG_NEAR_CAP) == 0
     ok &= ref.clamp_margin > 1e-5
     ok &= ref.jclamp_margin > 1e-5
-    nflag = int((flag[vis] != 0).sum())
-    _say(case, "flagged primitives", nflag, "of", vis.size)
-    if check_flags:
-        assert nflag <= 0.2 * vis.size
+    nskip = int(vis.size - ok.sum())
+    _say(case, "primitives outside the element-wise check (cap / clamp margins):", nskip, "of", vis.size)
+    assert nskip <= max(5, 1e-3 * vis.size)
     g2_gpu = tr.grad2d.cpu().numpy()[:w.scene.n]
     stats = {}
     names = ["du", "dv", "dA", "dB", "dC", "dop", "dr", "dg", "db"]
@@ -196,7 +205,7 @@ def _bwd_compare(w, tr, cam, orc, dL, case, check_flags=True):
     gn_ref[vis.astype(np.int64)] = gr.grad_norm
     stats["grad_norm"] = assert_grads(gn, gn_ref, ok, "grad_norm")
     _say(case, {k: (round(v.get("max_rel", 0), 6), round(v.get("norm_rel", 0), 8)) for k, v in stats.items()})
-    return vis, ok, gr
+    return gr
 
 
 @pytest.mark.parametrize("case", CASES)
@@ -206,11 +215,13 @@ def test_raster_backward(case, torch_gpu, orc):
     tr = trainer_for(w, torch_gpu)
     cam = w.cameras[0]
     dL = scenes.make_upstream_grad(cam.width, cam.height, 17)
+    dLm, amb, ref, vis = masked_upstream(orc, w, cam, dL)
+    _say(case, "ambiguous pixels zeroed in dL:", int(amb.sum()))
     tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd()
-    tr.set_dL(dL)
+    tr.set_dL(dLm.astype(np.float32))
     tr.raster_bwd(grad2d=True)
     torch_gpu.cuda.synchronize()
-    _bwd_compare(w, tr, cam, orc, dL.astype(np.float64), case)
+    bwd_compare(w, tr, orc, ref, vis, dLm.astype(np.float32).astype(np.float64), case)
 
 
 def test_sparse_adam(torch_gpu, orc):
