@@ -3,9 +3,12 @@
 Bars (derivations in the design notes):
   * integers, ids, keys, ranges, messages: bit-exact;
   * rendered pixels: |gpu - oracle| <= 1e-4 * max(|oracle|, PIX_FLOOR);
-  * gradients and updated parameters: |gpu - oracle| <= 2e-3 * max(|oracle|, floor_g)
-    with floor_g = GRAD_FLOOR_FRAC * (99th percentile of |oracle| over the group),
-    plus a normwise check ||gpu - oracle|| / ||oracle|| <= 2e-3.
+  * gradients and updated parameters: |gpu - oracle| <= 2e-3 * max(|oracle|, floor)
+    with floor = max(GRAD_FLOOR_FRAC * (99th percentile of |oracle| over the
+    group), GRAD_ROW_FRAC * |oracle row|) -- the row term covers components
+    that nearly cancel inside one primitive's gradient row, whose fp32 error
+    is relative to the row's magnitude -- plus a normwise check
+    ||gpu - oracle|| / ||oracle|| <= 2e-3.
 Pixels / primitives whose result depends on a threshold decision that the
 fp32 kernel may take differently from the fp64 oracle are excluded from the
 element-wise check and reported; their share is bounded.
@@ -16,6 +19,7 @@ PIX_RTOL = 1e-4
 PIX_FLOOR = 0.05
 GRAD_RTOL = 2e-3
 GRAD_FLOOR_FRAC = 1e-2
+GRAD_ROW_FRAC = 1e-1
 
 
 def assert_pixels(gpu, ref, mask=None, name="img"):
@@ -48,6 +52,8 @@ def assert_grads(gpu, ref, rows_ok, name, rtol=GRAD_RTOL, floor=None):
         return {}
     if floor is None:
         fl = grad_floor(r)
+        if r.ndim == 2 and r.shape[1] > 1:
+            fl = np.maximum(fl, GRAD_ROW_FRAC * np.linalg.norm(r, axis=1, keepdims=True))
     elif np.ndim(floor) == 0:
         fl = floor
     else:
