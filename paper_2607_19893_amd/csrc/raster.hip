@@ -455,6 +455,132 @@ __device__ __forceinline__ void lds_to_rows(float* __restrict__ dst, const uint3
     }
 }
 
+// Chain rule from one primitive's 2D gradient (du, dv, dA, dB, dC in g2) back
+// to mean, log-scale and quaternion, evaluated in scalar type Rl.  gmu holds
+// the colour path's contribution to dL/dmean; out receives mean (0..2),
+// log_scale (3..5) and quat (6..9) gradients.
+template <typename Rl>
+__device__ __forceinline__ void geometry_bwd(const float* mu_f, const float* ls_f, const float* qr_f,
+                                             const float* g2, const CamArgs& c, const float* gmu, float* out) {
+    Rl R[9];
+#pragma unroll
+    for (int k = 0; k < 9; ++k) R[k] = (Rl)c.R[k];
+    const Rl mu[3] = {(Rl)mu_f[0], (Rl)mu_f[1], (Rl)mu_f[2]};
+    const Rl fx = (Rl)c.fx, fy = (Rl)c.fy;
+    Rl p[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) p[k] = R[3 * k] * mu[0] + R[3 * k + 1] * mu[1] + R[3 * k + 2] * mu[2] + (Rl)c.t[k];
+    const Rl s[3] = {exp((Rl)ls_f[0]), exp((Rl)ls_f[1]), exp((Rl)ls_f[2])};
+    const Rl q0 = (Rl)qr_f[0], q1 = (Rl)qr_f[1], q2 = (Rl)qr_f[2], q3 = (Rl)qr_f[3];
+    const Rl iq = (Rl)1 / sqrt(q0 * q0 + q1 * q1 + q2 * q2 + q3 * q3);
+    const Rl w = q0 * iq, x = q1 * iq, y = q2 * iq, z = q3 * iq;
+    const Rl Rq[3][3] = {{1 - 2 * (y * y + z * z), 2 * (x * y - w * z), 2 * (x * z + w * y)},
+                         {2 * (x * y + w * z), 1 - 2 * (x * x + z * z), 2 * (y * z - w * x)},
+                         {2 * (x * z - w * y), 2 * (y * z + w * x), 1 - 2 * (x * x + y * y)}};
+    Rl M[3][3], Sg[3][3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 3; ++b) M[a][b] = Rq[a][b] * s[b];
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 3; ++b) Sg[a][b] = M[a][0] * M[b][0] + M[a][1] * M[b][1] + M[a][2] * M[b][2];
+    const Rl tz = p[2], itz = (Rl)1 / tz;
+    const Rl lx = (Rl)(1.3f * c.tan_fovx), ly = (Rl)(1.3f * c.tan_fovy);
+    const Rl rx = p[0] * itz, ry = p[1] * itz;
+    const bool clx = rx < -lx || rx > lx, cly = ry < -ly || ry > ly;
+    const Rl xr = rx < -lx ? -lx : (rx > lx ? lx : rx);
+    const Rl yr = ry < -ly ? -ly : (ry > ly ? ly : ry);
+    const Rl j00 = fx * itz, j11 = fy * itz;
+    const Rl j02 = -fx * xr * itz, j12 = -fy * yr * itz;
+    Rl T0[3], T1[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        T0[k] = j00 * R[k] + j02 * R[6 + k];
+        T1[k] = j11 * R[3 + k] + j12 * R[6 + k];
+    }
+    Rl ST0[3], ST1[3];   // Sigma T0, Sigma T1
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+        ST0[a] = Sg[a][0] * T0[0] + Sg[a][1] * T0[1] + Sg[a][2] * T0[2];
+        ST1[a] = Sg[a][0] * T1[0] + Sg[a][1] * T1[1] + Sg[a][2] * T1[2];
+    }
+    const Rl ca = T0[0] * ST0[0] + T0[1] * ST0[1] + T0[2] * ST0[2] + (Rl)0.3f;
+    const Rl cb = T0[0] * ST1[0] + T0[1] * ST1[1] + T0[2] * ST1[2];
+    const Rl cc = T1[0] * ST1[0] + T1[1] * ST1[1] + T1[2] * ST1[2] + (Rl)0.3f;
+    const Rl det = ca * cc - cb * cb;
+    const Rl id2 = (Rl)1 / (det * det);
+    // conic (A,B,C) = (c, -b, a)/det  ->  gradient w.r.t. (a, b, c)
+    const Rl gA = g2[2], gB = g2[3], gC = g2[4];
+    const Rl ga = (-gA * cc * cc + gB * cb * cc - gC * cb * cb) * id2;
+    const Rl gb = (2 * gA * cb * cc - gB * (ca * cc + cb * cb) + 2 * gC * ca * cb) * id2;
+    const Rl gcv = (-gA * cb * cb + gB * ca * cb - gC * ca * ca) * id2;
+    // a = T0.S.T0, b = T0.S.T1, c = T1.S.T1
+    Rl gT0[3], gT1[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+        gT0[a] = 2 * ga * ST0[a] + gb * ST1[a];
+        gT1[a] = gb * ST0[a] + 2 * gcv * ST1[a];
+    }
+    const Rl gj00 = gT0[0] * R[0] + gT0[1] * R[1] + gT0[2] * R[2];
+    const Rl gj02 = gT0[0] * R[6] + gT0[1] * R[7] + gT0[2] * R[8];
+    const Rl gj11 = gT1[0] * R[3] + gT1[1] * R[4] + gT1[2] * R[5];
+    const Rl gj12 = gT1[0] * R[6] + gT1[1] * R[7] + gT1[2] * R[8];
+    const Rl itz2 = itz * itz;
+    Rl gp[3] = {0, 0, 0};
+    gp[2] -= (gj00 * fx + gj11 * fy) * itz2;
+    if (clx) {
+        gp[2] += gj02 * fx * xr * itz2;
+    } else {
+        gp[0] -= gj02 * fx * itz2;
+        gp[2] += 2 * gj02 * fx * p[0] * itz2 * itz;
+    }
+    if (cly) {
+        gp[2] += gj12 * fy * yr * itz2;
+    } else {
+        gp[1] -= gj12 * fy * itz2;
+        gp[2] += 2 * gj12 * fy * p[1] * itz2 * itz;
+    }
+    const Rl gu = g2[0], gv = g2[1];
+    gp[0] += gu * fx * itz;
+    gp[1] += gv * fy * itz;
+    gp[2] -= (gu * fx * p[0] + gv * fy * p[1]) * itz2;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) out[k] = (float)((Rl)gmu[k] + R[k] * gp[0] + R[3 + k] * gp[1] + R[6 + k] * gp[2]);
+    // Sigma = M M^T with symmetric gradient Gs = ga T0T0^T + gb (T0T1^T + T1T0^T)/2 + gc T1T1^T
+    Rl Gs[3][3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 3; ++b)
+            Gs[a][b] = ga * T0[a] * T0[b] + (Rl)0.5 * gb * (T0[a] * T1[b] + T1[a] * T0[b]) + gcv * T1[a] * T1[b];
+    Rl gR[3][3];
+#pragma unroll
+    for (int b = 0; b < 3; ++b) {
+        Rl gsb = 0;
+#pragma unroll
+        for (int a = 0; a < 3; ++a) {
+            const Rl gM = 2 * (Gs[a][0] * M[0][b] + Gs[a][1] * M[1][b] + Gs[a][2] * M[2][b]);
+            gR[a][b] = gM * s[b];
+            gsb += gM * Rq[a][b];
+        }
+        out[3 + b] = (float)(gsb * s[b]);
+    }
+    const Rl gw = 2 * (x * (gR[2][1] - gR[1][2]) + y * (gR[0][2] - gR[2][0]) + z * (gR[1][0] - gR[0][1]));
+    const Rl gx = 2 * (w * (gR[2][1] - gR[1][2]) - 2 * x * (gR[1][1] + gR[2][2]) + y * (gR[0][1] + gR[1][0]) +
+                       z * (gR[0][2] + gR[2][0]));
+    const Rl gy = 2 * (w * (gR[0][2] - gR[2][0]) + x * (gR[0][1] + gR[1][0]) - 2 * y * (gR[0][0] + gR[2][2]) +
+                       z * (gR[1][2] + gR[2][1]));
+    const Rl gz = 2 * (w * (gR[1][0] - gR[0][1]) + x * (gR[0][2] + gR[2][0]) + y * (gR[1][2] + gR[2][1]) -
+                       2 * z * (gR[0][0] + gR[1][1]));
+    const Rl along = w * gw + x * gx + y * gy + z * gz;
+    out[6] = (float)((gw - w * along) * iq);
+    out[7] = (float)((gx - x * along) * iq);
+    out[8] = (float)((gy - y * along) * iq);
+    out[9] = (float)((gz - z * along) * iq);
+}
+
 template <int DEG>
 __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
     const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
@@ -564,116 +690,10 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
             gmu[2] = (gd[2] - d[2] * rad) * il;
         }
 
-        // 4. geometry
-        const float* R = c.R;
-        float p[3];
-#pragma unroll
-        for (int k = 0; k < 3; ++k) p[k] = R[3 * k] * mu[0] + R[3 * k + 1] * mu[1] + R[3 * k + 2] * mu[2] + c.t[k];
-        const float s[3] = {expf(ls[0]), expf(ls[1]), expf(ls[2])};
-        const float qn = sqrtf(qr[0] * qr[0] + qr[1] * qr[1] + qr[2] * qr[2] + qr[3] * qr[3]);
-        const float iq = 1.0f / qn;
-        const float w = qr[0] * iq, x = qr[1] * iq, y = qr[2] * iq, z = qr[3] * iq;
-        const float Rq[3][3] = {{1.0f - 2.0f * (y * y + z * z), 2.0f * (x * y - w * z), 2.0f * (x * z + w * y)},
-                                {2.0f * (x * y + w * z), 1.0f - 2.0f * (x * x + z * z), 2.0f * (y * z - w * x)},
-                                {2.0f * (x * z - w * y), 2.0f * (y * z + w * x), 1.0f - 2.0f * (x * x + y * y)}};
-        float M[3][3], Sg[3][3];
-#pragma unroll
-        for (int a = 0; a < 3; ++a)
-#pragma unroll
-            for (int b = 0; b < 3; ++b) M[a][b] = Rq[a][b] * s[b];
-#pragma unroll
-        for (int a = 0; a < 3; ++a)
-#pragma unroll
-            for (int b = 0; b < 3; ++b) Sg[a][b] = M[a][0] * M[b][0] + M[a][1] * M[b][1] + M[a][2] * M[b][2];
-        const float tz = p[2], itz = 1.0f / tz;
-        const float lx = 1.3f * c.tan_fovx, ly = 1.3f * c.tan_fovy;
-        const float rx = p[0] * itz, ry = p[1] * itz;
-        const bool clx = rx < -lx || rx > lx, cly = ry < -ly || ry > ly;
-        const float xr = fminf(lx, fmaxf(-lx, rx)), yr = fminf(ly, fmaxf(-ly, ry));
-        const float j00 = c.fx * itz, j11 = c.fy * itz;
-        const float j02 = -c.fx * xr * itz, j12 = -c.fy * yr * itz;
-        float T0[3], T1[3];
-#pragma unroll
-        for (int k = 0; k < 3; ++k) {
-            T0[k] = j00 * R[k] + j02 * R[6 + k];
-            T1[k] = j11 * R[3 + k] + j12 * R[6 + k];
-        }
-        float ST0[3], ST1[3];   // Sigma T0, Sigma T1
-#pragma unroll
-        for (int a = 0; a < 3; ++a) {
-            ST0[a] = Sg[a][0] * T0[0] + Sg[a][1] * T0[1] + Sg[a][2] * T0[2];
-            ST1[a] = Sg[a][0] * T1[0] + Sg[a][1] * T1[1] + Sg[a][2] * T1[2];
-        }
-        const float ca = dot3(T0, ST0) + 0.3f, cb = dot3(T0, ST1), cc = dot3(T1, ST1) + 0.3f;
-        const float det = ca * cc - cb * cb;
-        const float id2 = 1.0f / (det * det);
-        // conic (A,B,C) = (c, -b, a)/det  ->  gradient w.r.t. (a, b, c)
-        const float gA = g2[2], gB = g2[3], gC = g2[4];
-        const float ga = (-gA * cc * cc + gB * cb * cc - gC * cb * cb) * id2;
-        const float gb = (2.0f * gA * cb * cc - gB * (ca * cc + cb * cb) + 2.0f * gC * ca * cb) * id2;
-        const float gcv = (-gA * cb * cb + gB * ca * cb - gC * ca * ca) * id2;
-        // a = T0.S.T0, b = T0.S.T1, c = T1.S.T1
-        float gT0[3], gT1[3];
-#pragma unroll
-        for (int a = 0; a < 3; ++a) {
-            gT0[a] = 2.0f * ga * ST0[a] + gb * ST1[a];
-            gT1[a] = gb * ST0[a] + 2.0f * gcv * ST1[a];
-        }
-        const float gj00 = gT0[0] * R[0] + gT0[1] * R[1] + gT0[2] * R[2];
-        const float gj02 = gT0[0] * R[6] + gT0[1] * R[7] + gT0[2] * R[8];
-        const float gj11 = gT1[0] * R[3] + gT1[1] * R[4] + gT1[2] * R[5];
-        const float gj12 = gT1[0] * R[6] + gT1[1] * R[7] + gT1[2] * R[8];
-        const float itz2 = itz * itz;
-        float gp[3] = {0.0f, 0.0f, 0.0f};
-        gp[2] -= (gj00 * c.fx + gj11 * c.fy) * itz2;
-        if (clx) {
-            gp[2] += gj02 * c.fx * xr * itz2;
-        } else {
-            gp[0] -= gj02 * c.fx * itz2;
-            gp[2] += 2.0f * gj02 * c.fx * p[0] * itz2 * itz;
-        }
-        if (cly) {
-            gp[2] += gj12 * c.fy * yr * itz2;
-        } else {
-            gp[1] -= gj12 * c.fy * itz2;
-            gp[2] += 2.0f * gj12 * c.fy * p[1] * itz2 * itz;
-        }
-        gp[0] += g2[0] * c.fx * itz;
-        gp[1] += g2[1] * c.fy * itz;
-        gp[2] -= (g2[0] * c.fx * p[0] + g2[1] * c.fy * p[1]) * itz2;
-#pragma unroll
-        for (int k = 0; k < 3; ++k) row[k] = gmu[k] + R[k] * gp[0] + R[3 + k] * gp[1] + R[6 + k] * gp[2];
-        // Sigma = M M^T with symmetric gradient Gs = ga T0T0^T + gb (T0T1^T + T1T0^T)/2 + gc T1T1^T
-        float Gs[3][3];
-#pragma unroll
-        for (int a = 0; a < 3; ++a)
-#pragma unroll
-            for (int b = 0; b < 3; ++b)
-                Gs[a][b] = ga * T0[a] * T0[b] + 0.5f * gb * (T0[a] * T1[b] + T1[a] * T0[b]) + gcv * T1[a] * T1[b];
-        float gR[3][3];
-#pragma unroll
-        for (int b = 0; b < 3; ++b) {
-            float gsb = 0.0f;
-#pragma unroll
-            for (int a = 0; a < 3; ++a) {
-                const float gM = 2.0f * (Gs[a][0] * M[0][b] + Gs[a][1] * M[1][b] + Gs[a][2] * M[2][b]);
-                gR[a][b] = gM * s[b];
-                gsb += gM * Rq[a][b];
-            }
-            row[3 + b] = gsb * s[b];
-        }
-        const float gw = 2.0f * (x * (gR[2][1] - gR[1][2]) + y * (gR[0][2] - gR[2][0]) + z * (gR[1][0] - gR[0][1]));
-        const float gx = 2.0f * (w * (gR[2][1] - gR[1][2]) - 2.0f * x * (gR[1][1] + gR[2][2]) +
-                                 y * (gR[0][1] + gR[1][0]) + z * (gR[0][2] + gR[2][0]));
-        const float gy = 2.0f * (w * (gR[0][2] - gR[2][0]) + x * (gR[0][1] + gR[1][0]) -
-                                 2.0f * y * (gR[0][0] + gR[2][2]) + z * (gR[1][2] + gR[2][1]));
-        const float gz = 2.0f * (w * (gR[1][0] - gR[0][1]) + x * (gR[0][2] + gR[2][0]) + y * (gR[1][2] + gR[2][1]) -
-                                 2.0f * z * (gR[0][0] + gR[1][1]));
-        const float along = w * gw + x * gx + y * gy + z * gz;
-        row[6] = (gw - w * along) * iq;
-        row[7] = (gx - x * along) * iq;
-        row[8] = (gy - y * along) * iq;
-        row[9] = (gz - z * along) * iq;
+        // 4. geometry, in fp64: for wide footprints the conic gradient is large
+        //    while the scale / rotation gradients it produces are tiny, and the
+        //    chain cancels too much for fp32
+        geometry_bwd<double>(mu, ls, qr, g2, c, gmu, row);
     }
     __syncthreads();
     lds_to_rows<3, 0, ST>(g_mean, s_id, nrows, s_row);
