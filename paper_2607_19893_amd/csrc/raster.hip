@@ -147,7 +147,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
             const float4 a = s_a[k], b = s_b[k], c = s_c[k];
             float dx, dy;
             const float sigma = splat_sigma(a, b, fx, fy, dx, dy);
-            const float alpha = fminf(kAlphaMax, b.y * __expf(-sigma));
+            const float alpha = fminf(kAlphaMax, b.y * expf(-sigma));
             bool ok = !done && !(sigma < 0.0f) && !(alpha < kAlphaMin);
             const float Tn = T * (1.0f - alpha);
             const bool term = ok && (Tn < kTMin);
@@ -306,7 +306,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
                 const bool in_range = bs + (uint32_t)k < last;
                 float dx, dy;
                 const float sigma = splat_sigma(a, b, fx, fy, dx, dy);
-                const float e = __expf(-sigma);
+                const float e = expf(-sigma);
                 const float gv = b.y * e;
                 const float alpha = fminf(kAlphaMax, gv);
                 const bool ok = in_range && !(sigma < 0.0f) && !(alpha < kAlphaMin);
