@@ -212,11 +212,13 @@ def render(vis, proj: Projection, cam, bg=(0.0, 0.0, 0.0)) -> Render:
 
 
 # Bands inside which a threshold decision of the fp32 kernel may go either way
-# relative to this fp64 oracle (derivation in the design notes): relative
-# distance of o*exp(-sigma) from 1/255, of T*(1-alpha) from 1e-4, of
-# o*exp(-sigma) from the 0.99 cap, and absolute distance |img - target|.
+# relative to this fp64 oracle: relative distance of o*exp(-sigma) from 1/255
+# (fp32 sigma and exp: a few 1e-7), of T*(1-alpha) from 1e-4 (fp32
+# transmittance after N included pairs carries up to ~N * 1.2e-7 relative
+# error; 5e-4 covers N ~ 4000), of o*exp(-sigma) from the 0.99 cap, and the
+# absolute distance |img - target| of the loss sign.
 AMB_ALPHA = 4e-6
-AMB_T = 5e-5
+AMB_T = 5e-4
 AMB_CAP = 4e-6
 AMB_LOSS = 4e-6
 
