@@ -61,14 +61,20 @@ __device__ __forceinline__ bool splat_touches(float4 a, float4 c, float x0, floa
     return (a.x + c.y >= x0) && (a.x - c.y <= x1) && (a.y + c.z >= y0) && (a.y - c.z <= y1);
 }
 
-// sigma of one (pixel, primitive) pair.  Forward and backward both call this
-// on the same staged record, built without contraction, so they take
-// identical decisions.
+// sigma of one (pixel, primitive) pair.  The quadratic form is evaluated in
+// fp64: for elongated footprints far from their centre its three terms are
+// large and cancel, and fp32 loses up to ~1e-3 of sigma there (the error grows
+// with the conic's condition number).  Forward and backward both call this on
+// the same staged record, built without contraction, so they take identical
+// decisions.  px, py are the pixel centre in fp64.
 #pragma clang fp contract(off)
-__device__ __forceinline__ float splat_sigma(float4 a, float4 b, float px, float py, float& dx, float& dy) {
-    dx = a.x - px;
-    dy = a.y - py;
-    return fmaf(dx, fmaf(a.z, dx, a.w * dy), (b.x * dy) * dy);
+__device__ __forceinline__ float splat_sigma(float4 a, float4 b, double px, double py, float& dx, float& dy) {
+    const double ddx = (double)a.x - px;
+    const double ddy = (double)a.y - py;
+    const double s = fma(ddx, fma((double)a.z, ddx, (double)a.w * ddy), ((double)b.x * ddy) * ddy);
+    dx = (float)ddx;
+    dy = (float)ddy;
+    return (float)s;
 }
 #pragma clang fp contract(on)
 
@@ -117,7 +123,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const int px = tx * GS_TILE + (tid % GS_TILE);
     const int py = ty * GS_TILE + (tid / GS_TILE);
     const bool inside = px < W && py < H;
-    const float fx = px + 0.5f, fy = py + 0.5f;
+    const double fx = px + 0.5, fy = py + 0.5;
     // pixel-centre bounds of this wave's 16x4 strip
     const float wx0 = tx * GS_TILE + 0.5f, wx1 = wx0 + 15.0f;
     const float wy0 = ty * GS_TILE + 4 * w + 0.5f, wy1 = wy0 + 3.0f;
@@ -257,7 +263,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const int px = tx * GS_TILE + (tid % GS_TILE);
     const int py = ty * GS_TILE + (tid / GS_TILE);
     const bool inside = px < W && py < H;
-    const float fx = px + 0.5f, fy = py + 0.5f;
+    const double fx = px + 0.5, fy = py + 0.5;
     const float wx0 = tx * GS_TILE + 0.5f, wx1 = wx0 + 15.0f;
     const float wy0 = ty * GS_TILE + 4 * w + 0.5f, wy1 = wy0 + 3.0f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
