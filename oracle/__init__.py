@@ -73,7 +73,8 @@ def lib():
         L.orc_sorted_pairs.restype = i64
         L.orc_render.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, P, P, P, P, P, P]
         L.orc_render.restype = None
-        L.orc_render_backward.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, i32, P, P, f64, f64, f64, P, f64]
+        L.orc_render_backward.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, i32, P, P, f64, f64, f64, P, f64,
+                                          P]
         L.orc_render_backward.restype = None
         L.orc_project_backward.argtypes = [i32, i32, P, P, P, P, P, ctypes.POINTER(_Cam), i64, P, P, P,
                                            P, P, P, P, P, P]
@@ -236,7 +237,7 @@ def ambiguous_pixels(rnd: "Render", loss_margin=None, amb_alpha=AMB_ALPHA, amb_T
 
 
 def render_backward(vis, proj: Projection, cam, dL_dimg, bg=(0.0, 0.0, 0.0), loss_margin=None,
-                    amb_alpha=AMB_ALPHA, amb_T=AMB_T, amb_cap=AMB_CAP, amb_loss=AMB_LOSS):
+                    amb_alpha=AMB_ALPHA, amb_T=AMB_T, amb_cap=AMB_CAP, amb_loss=AMB_LOSS, want_abs=False):
     """d loss / d(u, v, A, B, C, opacity, rgb) per visible primitive, plus flags
     (FLAG_AMB_PIXEL | FLAG_NEAR_CAP bits per primitive)."""
     W, H = cam.width, cam.height
@@ -246,11 +247,14 @@ def render_backward(vis, proj: Projection, cam, dL_dimg, bg=(0.0, 0.0, 0.0), los
     g = np.ascontiguousarray(dL_dimg, np.float64).reshape(3, H, W)
     grad2d = np.zeros((n, 9))
     flag = np.zeros(n, np.uint8)
+    gabs = np.zeros((n, 9)) if want_abs else None
     lm = None if loss_margin is None else np.ascontiguousarray(loss_margin, np.float64).reshape(3, H, W)
     lib().orc_render_backward(vis.size, _p(vis), _p(proj.rect), _p(proj.depth), _p(proj.mean2d), _p(proj.conic),
                               _p(proj.opacity), _p(proj.rgb), W, H, _p(bg), _p(g), n, _p(grad2d), _p(flag),
                               float(amb_alpha), float(amb_T), float(amb_cap),
-                              None if lm is None else _p(lm), float(amb_loss))
+                              None if lm is None else _p(lm), float(amb_loss), None if gabs is None else _p(gabs))
+    if want_abs:
+        return grad2d, flag, gabs
     return grad2d, flag
 
 
@@ -293,6 +297,28 @@ def project_backward(scene, cam, vis, grad2d, proj: Projection) -> Grads:
                                _p(np.ascontiguousarray(grad2d, np.float64)), _p(proj.clamp),
                                _p(g.mean), _p(g.log_scale), _p(g.quat), _p(g.opacity), _p(g.sh), _p(g.grad_norm))
     return g
+
+
+def gradient_magnitudes(scene, cam, vis, grad2d_abs, proj: Projection):
+    """Per element of the parameter gradients: sum_c |d g_k / d g2d_c| * S_c, with
+    S_c = grad2d_abs[:, c] the sum of |per-pixel terms| of 2D component c.
+
+    The chain from the 2D gradient to the parameters is linear per primitive,
+    so its Jacobian columns are the chain applied to unit vectors.  An error
+    that is relative to S_c in each 2D component reaches the parameters scaled
+    by these magnitudes.  Returns compact rows (one per visible primitive) per
+    group, plus the grad_norm entry |S_u| + |S_v|.
+    """
+    vis = np.ascontiguousarray(vis, np.uint32)
+    rows = vis.astype(np.int64)
+    acc = None
+    for c in range(9):
+        g2 = np.zeros_like(grad2d_abs)
+        g2[rows, c] = grad2d_abs[rows, c]
+        gr = project_backward(scene, cam, vis, g2, proj)
+        parts = [np.abs(a) for a in gr.groups()]
+        acc = parts if acc is None else [x + y for x, y in zip(acc, parts)]
+    return acc, grad2d_abs[rows, 0] + grad2d_abs[rows, 1]
 
 
 def loss_l1(img, target):

@@ -671,13 +671,15 @@ void orc_render(int64_t nvis, const uint32_t* vis, const int32_t* rect, const fl
  * pixel whose margins fall below (amb_alpha, amb_T), or whose loss sign is
  * close (|loss_margin| < amb_loss, if loss_margin != NULL), and bit 1 when one
  * of its included pairs sits within amb_cap of the 0.99 cap (where the
- * derivative w.r.t. opacity and sigma jumps).
+ * derivative w.r.t. opacity and sigma jumps).  grad2d_abs (if not NULL)
+ * receives the per-component sums of |per-pixel term| (the magnitude an
+ * fp32 summation's rounding error is proportional to).
  */
 void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect, const float* depth,
                          const double* mean2d, const double* conic, const double* opacity, const double* rgb,
                          int W, int H, const double* bg, const double* dL_dimg, int n,
                          double* grad2d, uint8_t* flag, double amb_alpha, double amb_T, double amb_cap,
-                         const double* loss_margin, double amb_loss)
+                         const double* loss_margin, double amb_loss, double* grad2d_abs)
 {
     orc_scene2d s = {nvis, vis, rect, depth, mean2d, conic, opacity, rgb, W, H,
                      (W + ORC_TILE - 1) / ORC_TILE, (H + ORC_TILE - 1) / ORC_TILE, {bg[0], bg[1], bg[2]}};
@@ -697,6 +699,7 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
         free(cnt);
     }
     double* acc = (double*)calloc((size_t)toff[T] * 9 + 1, sizeof(double));
+    double* aab = grad2d_abs ? (double*)calloc((size_t)toff[T] * 9 + 1, sizeof(double)) : NULL;
     uint32_t* accj = (uint32_t*)malloc(sizeof(uint32_t) * (size_t)(toff[T] + 1));
     uint8_t* accf = (uint8_t*)calloc((size_t)toff[T] + 1, 1);
     const size_t HW = (size_t)W * H;
@@ -709,6 +712,7 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
             int tx = t % s.TX, ty = t / s.TX;
             int nl = tile_candidates(&s, tx, ty, L);
             double* ta = acc + (size_t)toff[t] * 9;
+            double* tb = aab ? aab + (size_t)toff[t] * 9 : NULL;
             uint8_t* tf = accf + toff[t];
             for (int k = 0; k < nl; ++k) accj[toff[t] + k] = L[k].j;
             for (int py = ty * ORC_TILE; py < (ty + 1) * ORC_TILE && py < H; ++py)
@@ -730,23 +734,27 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
                         uint32_t j = L[e->pos].j;
                         double* g = ta + (size_t)e->pos * 9;
                         const double* c = rgb + 3 * (size_t)j;
+                        double term[9] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
                         double dalpha = 0.0;
                         for (int ch = 0; ch < 3; ++ch) {
                             double sk = (g_mutation == 5) ? S[ch] : S[ch] / (1.0 - e->alpha);
                             dalpha += gC[ch] * (e->T * c[ch] - sk);
-                            g[6 + ch] += gC[ch] * e->alpha * e->T;
+                            term[6 + ch] = gC[ch] * e->alpha * e->T;
                         }
                         if (fabs(e->g - ORC_ALPHA_MAX) / ORC_ALPHA_MAX < amb_cap) tf[e->pos] |= 2;
                         if (!e->capped) {
                             double A = conic[3 * j], B = conic[3 * j + 1], Cc = conic[3 * j + 2];
-                            g[5] += dalpha * e->e;
+                            term[5] = dalpha * e->e;
                             double dsig = -dalpha * e->alpha;
-                            g[0] += dsig * (A * e->dx + B * e->dy);
-                            g[1] += dsig * (B * e->dx + Cc * e->dy);
-                            g[2] += dsig * 0.5 * e->dx * e->dx;
-                            g[3] += dsig * e->dx * e->dy;
-                            g[4] += dsig * 0.5 * e->dy * e->dy;
+                            term[0] = dsig * (A * e->dx + B * e->dy);
+                            term[1] = dsig * (B * e->dx + Cc * e->dy);
+                            term[2] = dsig * 0.5 * e->dx * e->dx;
+                            term[3] = dsig * e->dx * e->dy;
+                            term[4] = dsig * 0.5 * e->dy * e->dy;
                         }
+                        for (int q = 0; q < 9; ++q) g[q] += term[q];
+                        if (tb)
+                            for (int q = 0; q < 9; ++q) tb[(size_t)e->pos * 9 + q] += fabs(term[q]);
                         for (int ch = 0; ch < 3; ++ch) S[ch] += e->alpha * e->T * c[ch];
                     }
                 }
@@ -756,15 +764,18 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
     }
     for (int64_t a = 0; a < nvis; ++a) {
         memset(grad2d + 9 * (size_t)vis[a], 0, 9 * sizeof(double));
+        if (grad2d_abs) memset(grad2d_abs + 9 * (size_t)vis[a], 0, 9 * sizeof(double));
         if (flag) flag[vis[a]] = 0;
     }
     for (int64_t i = 0; i < toff[T]; ++i) {
         uint32_t j = accj[i];
         for (int c = 0; c < 9; ++c) grad2d[9 * (size_t)j + c] += acc[9 * (size_t)i + c];
+        if (aab)
+            for (int c = 0; c < 9; ++c) grad2d_abs[9 * (size_t)j + c] += aab[9 * (size_t)i + c];
         if (flag) flag[j] |= accf[i];
     }
     (void)n;
-    free(acc); free(accj); free(accf); free(toff);
+    free(acc); free(aab); free(accj); free(accf); free(toff);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -85,15 +85,17 @@ def test_full_view(name, orc):
     tr.set_dL(dLm)
     tr.raster_bwd(grad2d=True)
     torch.cuda.synchronize()
-    g2m, flagm = orc.render_backward(ref.vis, ref.proj, cam, dLm.astype(np.float64))
+    g2m, flagm, gabs = orc.render_backward(ref.vis, ref.proj, cam, dLm.astype(np.float64), want_abs=True)
     grm = orc.project_backward(w.scene, cam, ref.vis, g2m, ref.proj)
+    mags, _ = orc.gradient_magnitudes(w.scene, cam, ref.vis, gabs, ref.proj)
     ok_rows = ((flagm[vis] & orc.FLAG_NEAR_CAP) == 0) & (ref.proj.clamp_margin[vis] > 1e-5) & \
         (ref.proj.jclamp_margin[vis] > 1e-5)
     _say(name, "dL zeroed at %d pixels; gradient rows checked %d of %d" % (int(amb_all.sum()), int(ok_rows.sum()), V))
     assert ok_rows.mean() > 0.999
     rows = vis.astype(np.int64)
-    for gi, (gname, gp, go) in enumerate(zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.grads, grm.groups())):
-        st = assert_grads(gp.cpu().numpy()[rows], go, ok_rows, "grad." + gname)
+    for gi, (gname, gp, go, mg) in enumerate(zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.grads,
+                                                 grm.groups(), mags)):
+        st = assert_grads(gp.cpu().numpy()[rows], go, ok_rows, "grad." + gname, mag=mg)
         _say(name, gname, st)
     # the chain itself: recompute the loss gradient on the GPU and run backward,
     # Adam, pack and apply exactly as the benchmark does

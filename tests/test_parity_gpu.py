@@ -183,8 +183,10 @@ def masked_upstream(orc, w, cam, dL, loss_margin=None):
 
 def bwd_compare(w, tr, orc, ref, vis, dL_masked, case):
     cam = tr.cam
-    g2, flag = orc.render_backward(vis, ref, cam, dL_masked)
+    g2, flag, gabs = orc.render_backward(vis, ref, cam, dL_masked, want_abs=True)
     gr = orc.project_backward(w.scene, cam, vis, g2, ref)
+    mags, mag_norm = orc.gradient_magnitudes(w.scene, cam, vis, gabs, ref)
+    rows = vis.astype(np.int64)
     ok = np.zeros(w.scene.n, bool)
     ok[vis] = True
     ok &= (flag & orc.FLAG_NEAR_CAP) == 0
@@ -197,13 +199,12 @@ def bwd_compare(w, tr, orc, ref, vis, dL_masked, case):
     stats = {}
     names = ["du", "dv", "dA", "dB", "dC", "dop", "dr", "dg", "db"]
     for c, nm in enumerate(names):
-        stats[nm] = assert_grads(g2_gpu[:, c], g2[:, c], ok, "grad2d." + nm)
-    for name, gp, go in zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.grads, gr.full(w.scene.n)):
-        stats[name] = assert_grads(gp.cpu().numpy(), go, ok, "grad." + name)
-    gn = tr.grad_norm.cpu().numpy()[:w.scene.n]
-    gn_ref = np.zeros(w.scene.n)
-    gn_ref[vis.astype(np.int64)] = gr.grad_norm
-    stats["grad_norm"] = assert_grads(gn, gn_ref, ok, "grad_norm")
+        stats[nm] = assert_grads(g2_gpu[:, c], g2[:, c], ok, "grad2d." + nm, mag=gabs[:, c])
+    okr = ok[rows]
+    for name, gp, go, mg in zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.grads, gr.groups(), mags):
+        stats[name] = assert_grads(gp.cpu().numpy()[rows], go, okr, "grad." + name, mag=mg)
+    gn = tr.grad_norm.cpu().numpy()[rows]
+    stats["grad_norm"] = assert_grads(gn, gr.grad_norm, okr, "grad_norm", mag=mag_norm)
     _say(case, {k: (round(v.get("max_rel", 0), 6), round(v.get("norm_rel", 0), 8)) for k, v in stats.items()})
     return gr
 
