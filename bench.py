@@ -135,7 +135,7 @@ def main():
     apply_bytes = V_mean * (4 + row_bytes) + 2 * V_mean * row_bytes + 4 * V_mean
     roofs = {
         "raster_fwd": ("alu", fwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
-        "raster_bwd": ("alu", bwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
+        "raster_bwd_pixels": ("alu", bwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
         "adam": ("hbm", adam_bytes_delta / 1e9, HBM_PEAK_GBS, "GB/s"),
         "pack": ("hbm", pack_bytes / 1e9, HBM_PEAK_GBS, "GB/s"),
         "apply": ("hbm", apply_bytes / 1e9, HBM_PEAK_GBS, "GB/s"),

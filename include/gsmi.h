@@ -142,7 +142,8 @@ enum {
 /*
  * Workspace bytes a call needs, for a pool of n primitives, a pair capacity
  * (gs_bin_sort, gs_raster_bwd) and an image size.  Workspaces are caller-
- * owned device memory, 256-byte aligned, with no state kept between calls.
+ * owned device memory, 256-byte aligned; only the gs_raster_bwd_pixels ->
+ * gs_raster_bwd_project pair hands data from one call to the next.
  */
 size_t gs_workspace_bytes(int32_t which, int32_t n, uint32_t capacity, int32_t width, int32_t height);
 
@@ -245,6 +246,25 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
                         const uint32_t* vis_count, uint32_t capacity, const float* final_T,
                         const uint32_t* n_contrib, const float* dL_dimg, const float* bg, const gs_scene* grads,
                         float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * The two halves of gs_raster_bwd, for callers that schedule or time them
+ * separately.  gs_raster_bwd_pixels runs the per-pixel replay and leaves one
+ * 9-float derivative per (tile, primitive) pair in the workspace;
+ * gs_raster_bwd_project sums each visible primitive's pairs and applies the
+ * chain rule.  The same workspace (gs_workspace_bytes(GS_WS_RASTER_BWD, ...))
+ * must be passed to both, on the same stream or with the ordering ensured by
+ * the caller; it carries the pair derivatives from the first call to the
+ * second.  Arguments mean what they mean in gs_raster_bwd.
+ */
+gs_status gs_raster_bwd_pixels(const gs_proj* proj, const gs_camera* cam, const uint32_t* vals,
+                               const uint32_t* ranges, uint32_t capacity, const float* final_T,
+                               const uint32_t* n_contrib, const float* dL_dimg, const float* bg, void* ws,
+                               size_t ws_bytes, void* stream);
+gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj,
+                                const uint32_t* pair_offset, const uint32_t* pair_perm, const uint32_t* vis_idx,
+                                const uint32_t* vis_count, uint32_t capacity, const gs_scene* grads, float* grad2d,
+                                float* grad_norm, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Optimizer update (U in Figure 6; Shadow Graph step 5): Adam on the rows in

@@ -190,9 +190,48 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
     return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, vals, ranges, pair_offset, pair_perm, vis_idx,
                                               vis_count, capacity,
-                                              final_T, n_contrib, dL_dimg, bg, *grads, grad2d, grad_norm, ws,
+                                              final_T, n_contrib, dL_dimg, bg, *grads, grad2d, grad_norm, ws, 3,
                                               static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd");
+}
+
+gs_status gs_raster_bwd_pixels(const gs_proj* proj, const gs_camera* cam, const uint32_t* vals, const uint32_t* ranges,
+                               uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
+                               const float* dL_dimg, const float* bg, void* ws, size_t ws_bytes, void* stream) {
+    gs_status s;
+    if ((s = check_camera(cam, "gs_raster_bwd_pixels")) != GS_OK) return s;
+    if ((s = check_proj(proj, false, "gs_raster_bwd_pixels")) != GS_OK) return s;
+    GS_REQUIRE(vals && ranges && final_T && n_contrib && dL_dimg && bg && ws, "gs_raster_bwd_pixels: null pointer");
+    if (ws_bytes < gsmi::raster_bwd_ws_bytes(0, capacity))
+        return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_pixels: workspace too small");
+    const gsmi::CamArgs c = gsmi::make_cam_args(cam);
+    gs_scene none = {0, 0, nullptr, nullptr, nullptr, nullptr, nullptr};
+    return hip_status(gsmi::launch_raster_bwd(none, c, *proj, vals, ranges, nullptr, nullptr, nullptr, nullptr,
+                                              capacity, final_T, n_contrib, dL_dimg, bg, none, nullptr, nullptr, ws, 1,
+                                              static_cast<hipStream_t>(stream)),
+                      "gs_raster_bwd_pixels");
+}
+
+gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj,
+                                const uint32_t* pair_offset, const uint32_t* pair_perm, const uint32_t* vis_idx,
+                                const uint32_t* vis_count, uint32_t capacity, const gs_scene* grads, float* grad2d,
+                                float* grad_norm, void* ws, size_t ws_bytes, void* stream) {
+    gs_status s;
+    if ((s = check_scene(scene, "gs_raster_bwd_project")) != GS_OK) return s;
+    if ((s = check_scene(grads, "gs_raster_bwd_project(grads)")) != GS_OK) return s;
+    GS_REQUIRE(grads->n == scene->n && grads->sh_degree == scene->sh_degree,
+               "gs_raster_bwd_project: grads shape differs");
+    if ((s = check_camera(cam, "gs_raster_bwd_project")) != GS_OK) return s;
+    if ((s = check_proj(proj, true, "gs_raster_bwd_project")) != GS_OK) return s;
+    GS_REQUIRE(pair_offset && pair_perm && vis_idx && vis_count && ws, "gs_raster_bwd_project: null pointer");
+    if (ws_bytes < gsmi::raster_bwd_ws_bytes(scene->n, capacity))
+        return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_project: workspace too small");
+    const gsmi::CamArgs c = gsmi::make_cam_args(cam);
+    const float bg0[3] = {0.0f, 0.0f, 0.0f};
+    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, nullptr, nullptr, pair_offset, pair_perm, vis_idx,
+                                              vis_count, capacity, nullptr, nullptr, nullptr, bg0, *grads, grad2d,
+                                              grad_norm, ws, 2, static_cast<hipStream_t>(stream)),
+                      "gs_raster_bwd_project");
 }
 
 gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx, const uint32_t* count,

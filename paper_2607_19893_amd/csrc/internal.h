@@ -50,7 +50,8 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
                              const uint32_t* vis_idx,
                              const uint32_t* vis_count, uint32_t capacity, const float* final_T,
                              const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
-                             const gs_scene& grads, float* grad2d, float* grad_norm, void* ws, hipStream_t st);
+                             const gs_scene& grads, float* grad2d, float* grad_norm, void* ws, int stages,
+                             hipStream_t st);
 
 // adam.hip
 hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,

@@ -756,16 +756,16 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
                              const uint32_t* vis_idx,
                              const uint32_t* vis_count, uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
                              const float* dL_dimg, const float bg[3], const gs_scene& grads, float* grad2d,
-                             float* grad_norm, void* ws, hipStream_t st) {
+                             float* grad_norm, void* ws, int stages, hipStream_t st) {
     float* slots = static_cast<float*>(ws);
     const int32_t T = cam.tiles_x * cam.tiles_y;
-    if (T > 0)
+    if ((stages & 1) && T > 0)
         hipLaunchKernelGGL(k_raster_bwd, dim3(T), dim3(GS_BLOCK), 0, st, ranges, vals,
                            reinterpret_cast<const float2*>(proj.mean2d),
                            reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, cam.width, cam.height,
                            cam.tiles_x, bg[0], bg[1], bg[2], final_T, n_contrib, dL_dimg, slots);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || scene.n == 0) return e;
+    if (e != hipSuccess || scene.n == 0 || !(stages & 2)) return e;
     const dim3 grid(div_up(scene.n, GS_BLOCK));
 #define GS_LAUNCH_PBWD(D)                                                                                        \
     hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset, \

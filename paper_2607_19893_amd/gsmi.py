@@ -70,17 +70,21 @@ _lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, 
 _lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
 _lib.gs_raster_bwd.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P, P, P,
                                P, P, P, u32, P, P, P, P, ctypes.POINTER(gs_scene), P, P, P, sz, P]
+_lib.gs_raster_bwd_pixels.argtypes = [ctypes.POINTER(gs_proj), ctypes.POINTER(gs_camera), P, P, u32, P, P, P, P, P,
+                                      sz, P]
+_lib.gs_raster_bwd_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj),
+                                       P, P, P, P, u32, ctypes.POINTER(gs_scene), P, P, P, sz, P]
 _lib.gs_sparse_adam.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, i32, ctypes.c_double,
                                 ctypes.c_double, ctypes.c_double, P]
 _lib.gs_delta_pack.argtypes = [P, P, i32, ctypes.POINTER(gs_group), i32, u32, P, sz, P, P]
 _lib.gs_delta_apply.argtypes = [P, sz, ctypes.POINTER(gs_group), i32, i32, i32, i32, P, P, P]
 for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
-              "gs_sparse_adam", "gs_delta_pack", "gs_delta_apply"):
+              "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_delta_pack", "gs_delta_apply"):
     getattr(_lib, _name).restype = i32
 
 EXPORTS = ["gs_abi_version", "gs_status_string", "gs_last_error", "gs_workspace_bytes", "gs_delta_msg_bytes",
            "gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
-           "gs_sparse_adam", "gs_delta_pack", "gs_delta_apply"]
+           "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_delta_pack", "gs_delta_apply"]
 
 
 class GsmiError(RuntimeError):
@@ -206,6 +210,23 @@ def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, 
                                                       ptr(grad2d), ptr(grad_norm), ptr(ws),
                                                       ws.numel() * ws.element_size(),
                                                       stream if stream is not None else current_stream()))
+
+
+def gs_raster_bwd_pixels(proj: gs_proj, cam: gs_camera, vals, ranges, capacity, final_T, n_contrib, dL_dimg, bg, ws,
+                         stream=None):
+    b = _bg(bg)
+    return _check("gs_raster_bwd_pixels", _lib.gs_raster_bwd_pixels(
+        ctypes.byref(proj), ctypes.byref(cam), ptr(vals), ptr(ranges), int(capacity), ptr(final_T), ptr(n_contrib),
+        ptr(dL_dimg), ctypes.cast(b, P), ptr(ws), ws.numel() * ws.element_size(),
+        stream if stream is not None else current_stream()))
+
+
+def gs_raster_bwd_project(scene: gs_scene, cam: gs_camera, proj: gs_proj, pair_offset, pair_perm, vis_idx, vis_count,
+                          capacity, grads: gs_scene, grad2d, grad_norm, ws, stream=None):
+    return _check("gs_raster_bwd_project", _lib.gs_raster_bwd_project(
+        ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj), ptr(pair_offset), ptr(pair_perm), ptr(vis_idx),
+        ptr(vis_count), int(capacity), ctypes.byref(grads), ptr(grad2d), ptr(grad_norm), ptr(ws),
+        ws.numel() * ws.element_size(), stream if stream is not None else current_stream()))
 
 
 def make_adam_groups(groups):

@@ -174,6 +174,16 @@ class ViewTrainer:
                            self.pair_perm, self.vis_idx, self.counts[0:1], self.capacity, fT, nc, dL, bg, self.grads_s,
                            self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
 
+    def raster_bwd_pixels(self, bg=(0.0, 0.0, 0.0)):
+        _, fT, nc, dL, _ = self._img_views()
+        gsmi.gs_raster_bwd_pixels(self.proj_s, self.cam_c, self.vals, self.ranges, self.capacity, fT, nc, dL, bg,
+                                  self.ws_bwd)
+
+    def raster_bwd_project(self, grad2d=False):
+        gsmi.gs_raster_bwd_project(self.scene_s, self.cam_c, self.proj_s, self.pair_offset, self.pair_perm,
+                                   self.vis_idx, self.counts[0:1], self.capacity, self.grads_s,
+                                   self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
+
     def active_set(self):
         gsmi.gs_visible_set(gsmi.GS_PRED_U8_NONZERO, self.active, self.n, self.act_idx, self.counts[2:3], self.ws_vis)
 
@@ -188,33 +198,24 @@ class ViewTrainer:
         gsmi.gs_delta_apply(self.msg, self.replica_arr, 5, self.n, self.n, mode, self.version, self.status)
 
     # -- whole view ----------------------------------------------------------
-    PHASES = ("project", "visible", "bin_sort", "raster_fwd", "loss_l1", "raster_bwd", "adam", "pack", "apply")
+    PHASES = ("project", "visible", "bin_sort", "raster_fwd", "loss_l1", "raster_bwd_pixels", "raster_bwd_project",
+              "adam", "pack", "apply")
 
     def step(self, cam, step, version=1, publish=True, active=False, target=None, events=None):
         """Project, visible set, bin+sort, forward, L1, backward, Adam, pack + apply.
         target: device tensor (3*H*W) or None for the set_target buffer.
         events: optional list of len(PHASES)+1 torch.cuda.Event recorded around the phases."""
         ev = events
-        if ev: ev[0].record()
-        self.project(cam)
-        if ev: ev[1].record()
-        self.visible()
-        if ev: ev[2].record()
-        self.bin_sort()
-        if ev: ev[3].record()
-        self.raster_fwd(active=active)
-        if ev: ev[4].record()
-        self.loss_l1(target)
-        if ev: ev[5].record()
-        self.raster_bwd(grad2d=False)
-        if ev: ev[6].record()
-        self.adam(step)
-        if ev: ev[7].record()
-        if publish:
-            self.pack(version)
-            if ev: ev[8].record()
-            self.apply()
-        if ev: ev[9].record()
+        calls = (lambda: self.project(cam), self.visible, self.bin_sort, lambda: self.raster_fwd(active=active),
+                 lambda: self.loss_l1(target), self.raster_bwd_pixels, self.raster_bwd_project,
+                 lambda: self.adam(step), lambda: self.pack(version), self.apply)
+        if ev:
+            ev[0].record()
+        for i, fn in enumerate(calls):
+            if publish or i < 8:
+                fn()
+            if ev:
+                ev[i + 1].record()
 
     def ensure_capacity(self, cams, margin=1.25):
         """Size the pair buffers for the given cameras (synchronizes)."""

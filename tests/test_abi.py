@@ -24,7 +24,7 @@ def gs():
 
 def test_exports_every_declared_symbol(gs):
     names = declared_symbols()
-    assert len(names) >= 14
+    assert len(names) >= 16
     for nm in names:
         assert hasattr(gs.raw(), nm), nm
         assert nm in gs.EXPORTS, nm

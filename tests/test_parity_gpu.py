@@ -340,3 +340,24 @@ def test_empty_and_degenerate(torch_gpu, orc):
     hw = w.cameras[0].width * w.cameras[0].height
     assert float(tr.img.view(-1)[:3 * hw].abs().max()) == 0.0
     assert float(tr.final_T.view(-1)[:hw].min()) == 1.0
+
+
+def test_backward_halves_match_combined(torch_gpu, orc):
+    """gs_raster_bwd_pixels + gs_raster_bwd_project give gs_raster_bwd's result bit for bit."""
+    w = get_case("room-60k-392x216")
+    tr = trainer_for(w, torch_gpu)
+    cam = w.cameras[0]
+    tr.set_target(w.target(0))
+    tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd(); tr.loss_l1()
+    tr.raster_bwd(grad2d=True)
+    torch_gpu.cuda.synchronize()
+    ref = [g.clone() for g in tr.grads] + [tr.grad2d.clone(), tr.grad_norm.clone()]
+    for g in tr.grads:
+        g.zero_()
+    tr.grad2d.zero_(); tr.grad_norm.zero_()
+    tr.raster_bwd_pixels()
+    tr.raster_bwd_project(grad2d=True)
+    torch_gpu.cuda.synchronize()
+    got = list(tr.grads) + [tr.grad2d, tr.grad_norm]
+    for a, b in zip(got, ref):
+        assert torch_gpu.equal(a, b)
