@@ -2,8 +2,8 @@
 
 A step is one training view through every phase: projection, visible-set
 extraction, tile binning + sort, forward raster, L1 loss, backward, sparse
-Adam over the visible rows, and pack + apply of the Adam deltas into a
-replica (the pending-update publication).  The workload is the 1M-Gaussian
+Adam over the visible rows with its steps staged as a publication message,
+and the apply of that message to a replica (the pending-update publication).  The workload is the 1M-Gaussian
 SH-degree-3 room scene with 32 forward-facing 1920x1080 cameras; steps cycle
 through the cameras.  Inputs (scene, Adam state, all 32 targets) are resident
 in HBM before the timed region.
@@ -48,6 +48,9 @@ def main():
     ap.add_argument("--workload", default="room")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-views", type=int, default=8, help="views of the CPU oracle sample")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device copy (read + write of this many MiB, 4 times) and exit; "
+                         "its HBM counters calibrate the traffic counters of the path's kernels")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (collectives and sharding are "
@@ -55,6 +58,9 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_probe_mib > 0:
+        copy_probe(args.copy_probe_mib)
+        return
     from paper_2607_19893_amd import scenes
     from paper_2607_19893_amd.pipeline import ViewTrainer, to_u32
 
@@ -129,15 +135,15 @@ def main():
     names = list(ViewTrainer.PHASES)
     fwd_flops = FWD_FLOP_EVAL * ev_mean + FWD_FLOP_INC * inc_mean
     bwd_flops = BWD_FLOP_EVAL * ev_mean + BWD_FLOP_INC * inc_mean
-    adam_bytes = V_mean * row_bytes * 7 + 4 * V_mean            # p g m v read; p m v write; ids
-    adam_bytes_delta = adam_bytes + V_mean * row_bytes           # + delta write
-    pack_bytes = 2 * V_mean * (4 + row_bytes) + 4 * V_mean
-    apply_bytes = V_mean * (4 + row_bytes) + 2 * V_mean * row_bytes + 4 * V_mean
+    # Adam + staging per visible row: p, g, m, v read and p, m, v written (7 row
+    # reads/writes), the message row and id written, the id read
+    adam_bytes = V_mean * (8 * row_bytes + 8)
+    # apply per row: message row + id read, replica row read and written, version written
+    apply_bytes = V_mean * (3 * row_bytes + 8)
     roofs = {
         "raster_fwd": ("alu", fwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
         "raster_bwd_pixels": ("alu", bwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
-        "adam": ("hbm", adam_bytes_delta / 1e9, HBM_PEAK_GBS, "GB/s"),
-        "pack": ("hbm", pack_bytes / 1e9, HBM_PEAK_GBS, "GB/s"),
+        "adam_publish": ("hbm", adam_bytes / 1e9, HBM_PEAK_GBS, "GB/s"),
         "apply": ("hbm", apply_bytes / 1e9, HBM_PEAK_GBS, "GB/s"),
     }
     per_phase = {}
@@ -177,12 +183,24 @@ def main():
         "config": {"workload": w.name, "gaussians": w.scene.n, "sh_degree": w.scene.sh_degree,
                    "width": cams[0].width, "height": cams[0].height, "views": nviews,
                    "mean_visible": round(V_mean), "mean_pairs": round(M_mean),
-                   "step": "project+visible+bin_sort+fwd+L1+bwd+sparse_adam+delta_pack+delta_apply"},
+                   "step": "project+visible+bin_sort+fwd+L1+bwd+sparse_adam_publish+delta_apply"},
         "roofline": roofline,
         "phases_ms": {k: v["ms"] for k, v in per_phase.items()},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def copy_probe(mib):
+    """A plain elementwise copy of known size: reads and writes `mib` MiB per launch."""
+    import torch
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(4):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n, "launches": 4}), flush=True)
 
 
 def cpu_baseline(w, nviews):

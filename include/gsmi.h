@@ -28,7 +28,8 @@
  *    larger buffers after its next synchronization.
  *  - Counts produced on the device (visible-set size, pair count) stay on the
  *    device; later calls read them from there.
- *  - Row-major layouts: a "[n,c]" array holds row i at elements [i*c, i*c+c).
+ *  - Row-major layouts: a "[n,c]" array holds row i at elements [i*c, i*c+c);
+ *    "[n,c] with leading dimension ld" (written [n,ld]) at [i*ld, i*ld+c).
  *  - Thread safety: calls on different streams may run concurrently if they
  *    do not share output buffers.
  */
@@ -42,7 +43,7 @@
 extern "C" {
 #endif
 
-#define GSMI_ABI_VERSION 1
+#define GSMI_ABI_VERSION 2
 #define GS_TILE 16            /* pixels per tile side */
 #define GS_MAX_SH_DEGREE 3
 #define GS_MAX_GROUPS 8
@@ -64,18 +65,19 @@ typedef struct {
 } gs_device_status;
 
 #define GS_DEV_PAIR_OVERFLOW 1u     /* gs_bin_sort: pairs > capacity */
-#define GS_DEV_MSG_OVERFLOW 2u      /* gs_delta_pack: message > msg_capacity */
+#define GS_DEV_MSG_OVERFLOW 2u      /* gs_delta_pack, gs_sparse_adam_publish: message > msg_capacity */
 #define GS_DEV_MSG_MISMATCH 4u      /* gs_delta_apply: bad magic / widths / ids */
 
 /*
  * Primitive pool Theta (Section 2.1): five aligned fp32 tensors, one row per
- * primitive.  The same struct describes gradients and optimizer moments.
+ * primitive.
  *   mean      [n,3] world position
  *   log_scale [n,3] log standard deviation per axis
  *   quat      [n,4] rotation quaternion (w,x,y,z), any non-zero length
  *   opacity   [n]   opacity logit
  *   sh        [n,(sh_degree+1)^2,3] colour coefficients, coefficient
  *             k = l*l + l + m (m = -l..l), channel fastest
+ * quat and sh must be 16-byte aligned.
  */
 typedef struct {
     int32_t n;
@@ -235,17 +237,21 @@ gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32
  * chained through projection and colour to the parameters.  grad_norm is the
  * per-primitive gradient evidence g(p) of Section 2.1 that the post-backward
  * hook of Section 5 reports: |dL/d(u,v)| of this view.
- *   grads: same layout as the scene; only rows in vis_idx are written
- *   grad2d [n,9] fp32 or NULL: (du, dv, dA, dB, dC, dopacity, dr, dg, db) per visible row
- *   grad_norm [n] fp32 or NULL (visible rows)
+ *   grad_rows [V,grad_ld] fp32: one record per visible row r (the r-th entry
+ *     of vis_idx, V = *vis_count): [dmean 3, dlog_scale 3, dquat 4, dopacity 1,
+ *     dsh 3(L+1)^2] (row_len = 11 + 3(L+1)^2 floats, the pool's groups in
+ *     order); columns row_len..grad_ld-1 are set to 0.  grad_ld is a multiple
+ *     of 4 and >= row_len; grad_rows is 16-byte aligned and holds n rows.
+ *   grad2d [n,9] fp32 or NULL: (du, dv, dA, dB, dC, dopacity, dr, dg, db) per visible id
+ *   grad_norm [n] fp32 or NULL (visible ids)
  *   ws: gs_workspace_bytes(GS_WS_RASTER_BWD, n, capacity, W, H); capacity as in gs_bin_sort
  */
 gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
                         const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
                         const uint32_t* vis_idx,
                         const uint32_t* vis_count, uint32_t capacity, const float* final_T,
-                        const uint32_t* n_contrib, const float* dL_dimg, const float* bg, const gs_scene* grads,
-                        float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream);
+                        const uint32_t* n_contrib, const float* dL_dimg, const float* bg, float* grad_rows,
+                        int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * The two halves of gs_raster_bwd, for callers that schedule or time them
@@ -263,8 +269,8 @@ gs_status gs_raster_bwd_pixels(const gs_proj* proj, const gs_camera* cam, const 
                                size_t ws_bytes, void* stream);
 gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj,
                                 const uint32_t* pair_offset, const uint32_t* pair_perm, const uint32_t* vis_idx,
-                                const uint32_t* vis_count, uint32_t capacity, const gs_scene* grads, float* grad2d,
-                                float* grad_norm, void* ws, size_t ws_bytes, void* stream);
+                                const uint32_t* vis_count, uint32_t capacity, float* grad_rows, int32_t grad_ld,
+                                float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Optimizer update (U in Figure 6; Shadow Graph step 5): Adam on the rows in
@@ -274,24 +280,48 @@ gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, con
  *   delta = -(lr/(1-b1^t)) m / (sqrt(v)/sqrt(1-b2^t) + eps);  p += delta
  * The hyper-parameters are taken in fp64; b, 1-b, the bias corrections and
  * lr/(1-b1^t) are formed in fp64 and rounded to fp32 once (the arithmetic per
- * element is fp32).  max_rows bounds *count (launch size).
- * Rows not in idx are not touched.  delta (if not NULL) receives the step of
- * every updated row ([n,cols] layout) -- the pending update that
- * gs_delta_pack publishes.
+ * element is fp32).
+ *   groups: the pool tensors p [n,cols] with their learning rates; a row's
+ *     columns are the groups' columns concatenated (row_len = sum of cols <= 64)
+ *   idx/count: the ascending ids to update (*count on the device, <= max_rows,
+ *     which also sizes the launch)
+ *   grad_rows [*,grad_ld]: row r holds the gradient of primitive idx[r] (the
+ *     layout gs_raster_bwd writes); grad_ld >= row_len
+ *   m, v [n,state_ld]: the moments, one row per primitive id (columns in
+ *     group order); state_ld >= row_len
+ *   delta_rows [*,delta_ld] or NULL: row r receives the step of idx[r] -- the
+ *     pending update that a later publication carries; delta_ld >= row_len
+ * Rows not in idx are not touched.  Errors: GS_ERR_INVALID_ARG for null
+ * pointers, step < 1, betas outside [0,1), eps < 0, or a leading dimension
+ * below row_len; GS_ERR_UNSUPPORTED for row_len > 64.
  */
 typedef struct {
-    float* p;
-    const float* g;
-    float* m;
-    float* v;
-    float* delta;             /* may be NULL */
+    float* p;                 /* [n, cols] */
     int32_t cols;
     float lr;
 } gs_adam_group;
 
 gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
-                         const uint32_t* count, int32_t max_rows, int32_t step, double beta1, double beta2,
-                         double eps, void* stream);
+                         const uint32_t* count, int32_t max_rows, const float* grad_rows, int32_t grad_ld, float* m,
+                         float* v, int32_t state_ld, int32_t step, double beta1, double beta2, double eps,
+                         float* delta_rows, int32_t delta_ld, void* stream);
+
+/*
+ * The optimizer update fused with the staging of its pending update (Shadow
+ * Graph steps 3 and 5 of Section 4.3): the same update as gs_sparse_adam, and
+ * the steps of the updated rows written as one publication message (layout
+ * below; ids = idx, rows = the steps), byte for byte the message that
+ * gs_delta_pack would build from gs_sparse_adam's delta_rows scattered back to
+ * the pool layout.  If the message would not fit in msg_capacity bytes,
+ * NOTHING is written (parameters, moments and message stay as they were) and
+ * GS_DEV_MSG_OVERFLOW is set with the required bytes, so the call can be
+ * repeated with a larger buffer.  msg is 16-byte aligned.
+ */
+gs_status gs_sparse_adam_publish(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
+                                 const uint32_t* count, int32_t max_rows, const float* grad_rows, int32_t grad_ld,
+                                 float* m, float* v, int32_t state_ld, int32_t step, double beta1, double beta2,
+                                 double eps, uint32_t version, void* msg, size_t msg_capacity,
+                                 gs_device_status* status, void* stream);
 
 /*
  * Staged publication (Shadow Graph steps 3-4 of Section 4.3; publication

@@ -44,7 +44,7 @@ gs_status check_scene(const gs_scene* s, const char* what) {
                s->sh_degree);
     if (s->n > 0) {
         GS_REQUIRE(s->mean && s->log_scale && s->quat && s->opacity && s->sh, "%s: null parameter pointer", what);
-        GS_REQUIRE(aligned(s->quat, 16), "%s: quat must be 16-byte aligned", what);
+        GS_REQUIRE(aligned(s->quat, 16) && aligned(s->sh, 16), "%s: quat and sh must be 16-byte aligned", what);
     }
     return GS_OK;
 }
@@ -64,6 +64,16 @@ gs_status check_proj(const gs_proj* p, bool need_all, const char* what) {
     if (need_all) GS_REQUIRE(p->radius && p->clamp, "%s: null proj array", what);
     GS_REQUIRE(aligned(p->rect, 8) && aligned(p->mean2d, 8) && aligned(p->conic_opacity, 16),
                "%s: proj arrays misaligned (rect 8, mean2d 8, conic_opacity 16 bytes)", what);
+    return GS_OK;
+}
+
+int32_t scene_row_len(const gs_scene* s) { return 11 + 3 * (s->sh_degree + 1) * (s->sh_degree + 1); }
+
+gs_status check_grad_rows(const gs_scene* s, const float* grad_rows, int32_t grad_ld, const char* what) {
+    GS_REQUIRE(grad_rows != nullptr || s->n == 0, "%s: null grad_rows", what);
+    GS_REQUIRE(aligned(grad_rows, 16), "%s: grad_rows must be 16-byte aligned", what);
+    GS_REQUIRE(grad_ld % 4 == 0 && grad_ld >= scene_row_len(s), "%s: grad_ld %d must be a multiple of 4 and >= %d",
+               what, grad_ld, scene_row_len(s));
     return GS_OK;
 }
 
@@ -172,26 +182,24 @@ gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32
 
 gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
                         const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
-                        const uint32_t* vis_idx,
-                        const uint32_t* vis_count, uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
-                        const float* dL_dimg, const float* bg, const gs_scene* grads, float* grad2d, float* grad_norm,
-                        void* ws, size_t ws_bytes, void* stream) {
+                        const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity, const float* final_T,
+                        const uint32_t* n_contrib, const float* dL_dimg, const float* bg, float* grad_rows,
+                        int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream) {
     gs_status s;
     if ((s = check_scene(scene, "gs_raster_bwd")) != GS_OK) return s;
-    if ((s = check_scene(grads, "gs_raster_bwd(grads)")) != GS_OK) return s;
-    GS_REQUIRE(grads->n == scene->n && grads->sh_degree == scene->sh_degree, "gs_raster_bwd: grads shape differs");
+    if ((s = check_grad_rows(scene, grad_rows, grad_ld, "gs_raster_bwd")) != GS_OK) return s;
     if ((s = check_camera(cam, "gs_raster_bwd")) != GS_OK) return s;
     if ((s = check_proj(proj, true, "gs_raster_bwd")) != GS_OK) return s;
     GS_REQUIRE(vals && ranges && pair_offset && pair_perm && vis_idx && vis_count && final_T && n_contrib && dL_dimg &&
                    bg && ws,
                "gs_raster_bwd: null pointer");
+    GS_REQUIRE(aligned(ws, 256), "gs_raster_bwd: workspace must be 256-byte aligned");
     if (ws_bytes < gsmi::raster_bwd_ws_bytes(scene->n, capacity))
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
     return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, vals, ranges, pair_offset, pair_perm, vis_idx,
-                                              vis_count, capacity,
-                                              final_T, n_contrib, dL_dimg, bg, *grads, grad2d, grad_norm, ws, 3,
-                                              static_cast<hipStream_t>(stream)),
+                                              vis_count, capacity, final_T, n_contrib, dL_dimg, bg, grad_rows,
+                                              grad_ld, grad2d, grad_norm, ws, 3, static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd");
 }
 
@@ -202,56 +210,92 @@ gs_status gs_raster_bwd_pixels(const gs_proj* proj, const gs_camera* cam, const 
     if ((s = check_camera(cam, "gs_raster_bwd_pixels")) != GS_OK) return s;
     if ((s = check_proj(proj, false, "gs_raster_bwd_pixels")) != GS_OK) return s;
     GS_REQUIRE(vals && ranges && final_T && n_contrib && dL_dimg && bg && ws, "gs_raster_bwd_pixels: null pointer");
+    GS_REQUIRE(aligned(ws, 256), "gs_raster_bwd_pixels: workspace must be 256-byte aligned");
     if (ws_bytes < gsmi::raster_bwd_ws_bytes(0, capacity))
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_pixels: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
     gs_scene none = {0, 0, nullptr, nullptr, nullptr, nullptr, nullptr};
     return hip_status(gsmi::launch_raster_bwd(none, c, *proj, vals, ranges, nullptr, nullptr, nullptr, nullptr,
-                                              capacity, final_T, n_contrib, dL_dimg, bg, none, nullptr, nullptr, ws, 1,
-                                              static_cast<hipStream_t>(stream)),
+                                              capacity, final_T, n_contrib, dL_dimg, bg, nullptr, 0, nullptr, nullptr,
+                                              ws, 1, static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd_pixels");
 }
 
 gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj,
                                 const uint32_t* pair_offset, const uint32_t* pair_perm, const uint32_t* vis_idx,
-                                const uint32_t* vis_count, uint32_t capacity, const gs_scene* grads, float* grad2d,
-                                float* grad_norm, void* ws, size_t ws_bytes, void* stream) {
+                                const uint32_t* vis_count, uint32_t capacity, float* grad_rows, int32_t grad_ld,
+                                float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream) {
     gs_status s;
     if ((s = check_scene(scene, "gs_raster_bwd_project")) != GS_OK) return s;
-    if ((s = check_scene(grads, "gs_raster_bwd_project(grads)")) != GS_OK) return s;
-    GS_REQUIRE(grads->n == scene->n && grads->sh_degree == scene->sh_degree,
-               "gs_raster_bwd_project: grads shape differs");
+    if ((s = check_grad_rows(scene, grad_rows, grad_ld, "gs_raster_bwd_project")) != GS_OK) return s;
     if ((s = check_camera(cam, "gs_raster_bwd_project")) != GS_OK) return s;
     if ((s = check_proj(proj, true, "gs_raster_bwd_project")) != GS_OK) return s;
     GS_REQUIRE(pair_offset && pair_perm && vis_idx && vis_count && ws, "gs_raster_bwd_project: null pointer");
+    GS_REQUIRE(aligned(ws, 256), "gs_raster_bwd_project: workspace must be 256-byte aligned");
     if (ws_bytes < gsmi::raster_bwd_ws_bytes(scene->n, capacity))
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_project: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
     const float bg0[3] = {0.0f, 0.0f, 0.0f};
     return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, nullptr, nullptr, pair_offset, pair_perm, vis_idx,
-                                              vis_count, capacity, nullptr, nullptr, nullptr, bg0, *grads, grad2d,
-                                              grad_norm, ws, 2, static_cast<hipStream_t>(stream)),
+                                              vis_count, capacity, nullptr, nullptr, nullptr, bg0, grad_rows, grad_ld,
+                                              grad2d, grad_norm, ws, 2, static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd_project");
 }
 
-gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx, const uint32_t* count,
-                         int32_t max_rows, int32_t step, double beta1, double beta2, double eps, void* stream) {
-    GS_REQUIRE(groups && n_groups > 0 && n_groups <= GS_MAX_GROUPS, "gs_sparse_adam: 1..%d groups", GS_MAX_GROUPS);
-    GS_REQUIRE(idx && count, "gs_sparse_adam: null index list");
-    GS_REQUIRE(max_rows >= 0, "gs_sparse_adam: max_rows < 0");
-    GS_REQUIRE(step >= 1, "gs_sparse_adam: step must be >= 1");
-    GS_REQUIRE(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0, "gs_sparse_adam: betas outside [0,1)");
-    GS_REQUIRE(eps >= 0.0, "gs_sparse_adam: eps < 0");
+static gs_status check_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx, const uint32_t* count,
+                            int32_t max_rows, const float* grad_rows, int32_t grad_ld, const float* m, const float* v,
+                            int32_t state_ld, int32_t step, double beta1, double beta2, double eps,
+                            const char* what) {
+    GS_REQUIRE(groups && n_groups > 0 && n_groups <= GS_MAX_GROUPS, "%s: 1..%d groups", what, GS_MAX_GROUPS);
+    GS_REQUIRE(idx && count, "%s: null index list", what);
+    GS_REQUIRE(grad_rows && m && v, "%s: null gradient or moment table", what);
+    GS_REQUIRE(max_rows >= 0, "%s: max_rows < 0", what);
+    GS_REQUIRE(step >= 1, "%s: step must be >= 1", what);
+    GS_REQUIRE(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0, "%s: betas outside [0,1)", what);
+    GS_REQUIRE(eps >= 0.0, "%s: eps < 0", what);
     int32_t row_len = 0;
     for (int i = 0; i < n_groups; ++i) {
-        GS_REQUIRE(groups[i].p && groups[i].g && groups[i].m && groups[i].v, "gs_sparse_adam: group %d null", i);
-        GS_REQUIRE(groups[i].cols > 0, "gs_sparse_adam: group %d cols <= 0", i);
+        GS_REQUIRE(groups[i].p, "%s: group %d null", what, i);
+        GS_REQUIRE(groups[i].cols > 0, "%s: group %d cols <= 0", what, i);
         row_len += groups[i].cols;
     }
-    if (row_len > 64) return fail(GS_ERR_UNSUPPORTED, "gs_sparse_adam: row length %d above 64", row_len);
-    return hip_status(gsmi::launch_sparse_adam(groups, n_groups, idx, count, max_rows, step, beta1, beta2, eps,
+    if (row_len > 64) return fail(GS_ERR_UNSUPPORTED, "%s: row length %d above 64", what, row_len);
+    GS_REQUIRE(grad_ld >= row_len && state_ld >= row_len, "%s: grad_ld and state_ld must be >= row length %d", what,
+               row_len);
+    return GS_OK;
+}
+
+gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx, const uint32_t* count,
+                         int32_t max_rows, const float* grad_rows, int32_t grad_ld, float* m, float* v,
+                         int32_t state_ld, int32_t step, double beta1, double beta2, double eps, float* delta_rows,
+                         int32_t delta_ld, void* stream) {
+    gs_status s = check_adam(groups, n_groups, idx, count, max_rows, grad_rows, grad_ld, m, v, state_ld, step, beta1,
+                             beta2, eps, "gs_sparse_adam");
+    if (s != GS_OK) return s;
+    int32_t row_len = 0;
+    for (int i = 0; i < n_groups; ++i) row_len += groups[i].cols;
+    GS_REQUIRE(delta_rows == nullptr || delta_ld >= row_len, "gs_sparse_adam: delta_ld must be >= row length %d",
+               row_len);
+    return hip_status(gsmi::launch_sparse_adam(groups, n_groups, idx, count, max_rows, grad_rows, grad_ld, m, v,
+                                               state_ld, step, beta1, beta2, eps, delta_rows, delta_ld,
                                                static_cast<hipStream_t>(stream)),
                       "gs_sparse_adam");
+}
+
+gs_status gs_sparse_adam_publish(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
+                                 const uint32_t* count, int32_t max_rows, const float* grad_rows, int32_t grad_ld,
+                                 float* m, float* v, int32_t state_ld, int32_t step, double beta1, double beta2,
+                                 double eps, uint32_t version, void* msg, size_t msg_capacity,
+                                 gs_device_status* status, void* stream) {
+    gs_status s = check_adam(groups, n_groups, idx, count, max_rows, grad_rows, grad_ld, m, v, state_ld, step, beta1,
+                             beta2, eps, "gs_sparse_adam_publish");
+    if (s != GS_OK) return s;
+    GS_REQUIRE(msg && status, "gs_sparse_adam_publish: null message or status");
+    GS_REQUIRE(aligned(msg, 16), "gs_sparse_adam_publish: msg must be 16-byte aligned");
+    return hip_status(gsmi::launch_sparse_adam_publish(groups, n_groups, idx, count, max_rows, grad_rows, grad_ld, m,
+                                                       v, state_ld, step, beta1, beta2, eps, version, msg,
+                                                       msg_capacity, status, static_cast<hipStream_t>(stream)),
+                      "gs_sparse_adam_publish");
 }
 
 static gs_status check_groups(const gs_group* g, int32_t n, const char* what) {

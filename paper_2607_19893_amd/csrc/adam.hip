@@ -1,11 +1,14 @@
-// Optimizer update over the visible rows only (sparse Adam).
+// Optimizer update over the visible rows only (sparse Adam), optionally fused
+// with the staging of its pending update as a publication message.
 //
-// Layout: one primitive row spans all parameter groups (3+3+4+1+48 = 59
-// floats at SH degree 3).  A wave takes floor(64 / row_len) rows at a time;
-// lane l owns column l % row_len of sub-row l / row_len, so the lanes of one
-// row read each group's contiguous row segment together.  The group and
-// column of every lane are fixed once; the loop over rows is grid-strided.
-// Bound by HBM: 16 bytes read (p, g, m, v) and 12-16 written per element.
+// Layout: a primitive's row spans all parameter groups (3+3+4+1+48 = 59
+// floats at SH degree 3).  The gradient arrives as compact rows (row r ->
+// primitive idx[r]) and the moments are row-major tables indexed by id, so a
+// row's g, m and v are each one contiguous segment; only the parameters keep
+// the pool's per-group tensors.  A wave takes floor(64 / row_len) rows at a
+// time and lane l owns column l % row_len of sub-row l / row_len.  Each lane
+// works on kUnroll rows per iteration, issuing all their loads before any
+// arithmetic, so that enough rows are in flight to cover HBM latency.
 #include "common.h"
 #include "internal.h"
 
@@ -13,22 +16,68 @@ namespace gsmi {
 
 namespace {
 
+constexpr int kUnroll = 4;
+
 struct AdamArgs {
     float* p[GS_MAX_GROUPS];
-    const float* g[GS_MAX_GROUPS];
-    float* m[GS_MAX_GROUPS];
-    float* v[GS_MAX_GROUPS];
-    float* d[GS_MAX_GROUPS];
     int32_t cols[GS_MAX_GROUPS];
     float step[GS_MAX_GROUPS];     // lr / (1 - beta1^t)
     int32_t n_groups;
     int32_t row_len;
     int32_t rows_per_wave;
+    const float* g;
+    int32_t gld;
+    float* m;
+    float* v;
+    int32_t sld;
+    float* d;                      // step rows (row r), or nullptr
+    int32_t dld;
+    uint32_t* msg;                 // publication message (PUBLISH only)
+    uint64_t msg_capacity;
+    uint32_t version;
+    gs_device_status* status;
     float beta1, beta2, one_m_b1, one_m_b2, sqrt_bc2, eps;
 };
 
+template <bool PUBLISH>
 __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint32_t* __restrict__ idx,
                                                           const uint32_t* __restrict__ count) {
+    const uint32_t K = *count;
+    float* __restrict__ drows = a.d;
+    int32_t dld = a.dld;
+    uint32_t* __restrict__ ids = nullptr;
+    if (PUBLISH) {
+        const uint64_t need = msg_bytes(K, a.row_len, a.n_groups);
+        if (need > a.msg_capacity) {
+            // all or nothing: no block touches parameters, moments or message
+            if (blockIdx.x == 0 && threadIdx.x == 0) {
+                atomicOr(&a.status->flags, GS_DEV_MSG_OVERFLOW);
+                atomicMax(&a.status->required, (uint32_t)(need > 0xFFFFFFFFull ? 0xFFFFFFFFull : need));
+            }
+            return;
+        }
+        const uint32_t gw = (uint32_t)((a.n_groups + 3) / 4) * 4;
+        const uint64_t row0 = msg_words_before_rows(K, a.n_groups);
+        if (blockIdx.x == 0) {
+            const uint32_t t = threadIdx.x;
+            if (t < 8 + gw) {
+                uint32_t val = 0;
+                if (t == 0) val = GS_MSG_MAGIC;
+                else if (t == 1) val = K;
+                else if (t == 2) val = a.version;
+                else if (t == 3) val = (uint32_t)a.row_len;
+                else if (t == 4) val = (uint32_t)a.n_groups;
+                else if (t >= 8 && t - 8 < (uint32_t)a.n_groups) val = (uint32_t)a.cols[t - 8];
+                a.msg[t] = val;
+            } else if (t < 8 + gw + 4) {
+                const uint64_t pw = 8 + gw + K + (t - 8 - gw);     // zero padding between ids and rows
+                if (pw < row0) a.msg[pw] = 0;
+            }
+        }
+        ids = a.msg + 8 + gw;
+        drows = reinterpret_cast<float*>(a.msg + row0);
+        dld = a.row_len;
+    }
     const int lane = lane_id();
     const int sub = lane / a.row_len;
     const int col = lane - sub * a.row_len;
@@ -39,44 +88,58 @@ __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint
         ++grp;
     }
     float* __restrict__ P = a.p[grp];
-    const float* __restrict__ G = a.g[grp];
-    float* __restrict__ Mm = a.m[grp];
-    float* __restrict__ Vv = a.v[grp];
-    float* __restrict__ D = a.d[grp];
     const int cols = a.cols[grp];
     const float step = a.step[grp];
-    const uint32_t K = *count;
+    const float* __restrict__ G = a.g;
+    float* __restrict__ Mm = a.m;
+    float* __restrict__ Vv = a.v;
     const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
     const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
-    for (uint32_t r = wave * a.rows_per_wave + sub; r < K; r += waves * a.rows_per_wave) {
-        const size_t o = (size_t)idx[r] * cols + c;
-        const float gr = G[o];
-        const float mn = a.beta1 * Mm[o] + a.one_m_b1 * gr;
-        const float vn = a.beta2 * Vv[o] + a.one_m_b2 * gr * gr;
-        const float den = sqrtf(vn) / a.sqrt_bc2 + a.eps;
-        const float delta = -step * (mn / den);
-        Mm[o] = mn;
-        Vv[o] = vn;
-        P[o] = P[o] + delta;
-        if (D) D[o] = delta;
+    const uint32_t stride = waves * a.rows_per_wave;
+    for (uint32_t r0 = wave * a.rows_per_wave + sub; r0 < K; r0 += kUnroll * stride) {
+        uint32_t id[kUnroll];
+        float gr[kUnroll], mo[kUnroll], vo[kUnroll], po[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const uint32_t r = r0 + u * stride;
+            id[u] = r < K ? idx[r] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const uint32_t r = r0 + u * stride;
+            if (r < K) {
+                gr[u] = G[(size_t)r * a.gld + col];
+                mo[u] = Mm[(size_t)id[u] * a.sld + col];
+                vo[u] = Vv[(size_t)id[u] * a.sld + col];
+                po[u] = P[(size_t)id[u] * cols + c];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const uint32_t r = r0 + u * stride;
+            if (r < K) {
+                const float mn = a.beta1 * mo[u] + a.one_m_b1 * gr[u];
+                const float vn = a.beta2 * vo[u] + a.one_m_b2 * gr[u] * gr[u];
+                const float den = sqrtf(vn) / a.sqrt_bc2 + a.eps;
+                const float delta = -step * (mn / den);
+                Mm[(size_t)id[u] * a.sld + col] = mn;
+                Vv[(size_t)id[u] * a.sld + col] = vn;
+                P[(size_t)id[u] * cols + c] = po[u] + delta;
+                if (drows) drows[(size_t)r * dld + col] = delta;
+                if (PUBLISH && col == 0) ids[r] = id[u];
+            }
+        }
     }
 }
 
-}  // namespace
-
-hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
-                              const uint32_t* count, int32_t max_rows, int32_t step, double beta1, double beta2,
-                              double eps, hipStream_t st) {
+AdamArgs make_args(const gs_adam_group* groups, int32_t n_groups, const float* grad_rows, int32_t grad_ld, float* m,
+                   float* v, int32_t state_ld, int32_t step, double beta1, double beta2, double eps) {
     AdamArgs a = {};
     int32_t row_len = 0;
     const double bc1 = 1.0 - pow(beta1, (double)step);
     const double bc2 = 1.0 - pow(beta2, (double)step);
     for (int i = 0; i < n_groups; ++i) {
         a.p[i] = groups[i].p;
-        a.g[i] = groups[i].g;
-        a.m[i] = groups[i].m;
-        a.v[i] = groups[i].v;
-        a.d[i] = groups[i].delta;
         a.cols[i] = groups[i].cols;
         a.step[i] = (float)((double)groups[i].lr / bc1);
         row_len += groups[i].cols;
@@ -84,17 +147,55 @@ hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, con
     a.n_groups = n_groups;
     a.row_len = row_len;
     a.rows_per_wave = GS_WAVE / row_len;
+    a.g = grad_rows;
+    a.gld = grad_ld;
+    a.m = m;
+    a.v = v;
+    a.sld = state_ld;
     a.beta1 = (float)beta1;
     a.beta2 = (float)beta2;
     a.one_m_b1 = (float)(1.0 - beta1);
     a.one_m_b2 = (float)(1.0 - beta2);
     a.sqrt_bc2 = (float)sqrt(bc2);
     a.eps = (float)eps;
-    if (max_rows <= 0) return hipSuccess;
-    const uint64_t waves_needed = div_up((uint64_t)max_rows, (uint64_t)a.rows_per_wave);
+    return a;
+}
+
+uint32_t adam_blocks(int32_t max_rows, int32_t rows_per_wave) {
+    const uint64_t waves_needed = div_up(div_up((uint64_t)max_rows, (uint64_t)rows_per_wave), kUnroll);
     uint32_t blocks = div_up(waves_needed, GS_BLOCK / GS_WAVE);
     if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(k_sparse_adam, dim3(blocks), dim3(GS_BLOCK), 0, st, a, idx, count);
+    return blocks > 0 ? blocks : 1;
+}
+
+}  // namespace
+
+hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
+                              const uint32_t* count, int32_t max_rows, const float* grad_rows, int32_t grad_ld,
+                              float* m, float* v, int32_t state_ld, int32_t step, double beta1, double beta2,
+                              double eps, float* delta_rows, int32_t delta_ld, hipStream_t st) {
+    AdamArgs a = make_args(groups, n_groups, grad_rows, grad_ld, m, v, state_ld, step, beta1, beta2, eps);
+    a.d = delta_rows;
+    a.dld = delta_ld;
+    if (max_rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_sparse_adam<false>, dim3(adam_blocks(max_rows, a.rows_per_wave)), dim3(GS_BLOCK), 0, st, a,
+                       idx, count);
+    return hipGetLastError();
+}
+
+hipError_t launch_sparse_adam_publish(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
+                                      const uint32_t* count, int32_t max_rows, const float* grad_rows,
+                                      int32_t grad_ld, float* m, float* v, int32_t state_ld, int32_t step,
+                                      double beta1, double beta2, double eps, uint32_t version, void* msg,
+                                      size_t msg_capacity, gs_device_status* status, hipStream_t st) {
+    AdamArgs a = make_args(groups, n_groups, grad_rows, grad_ld, m, v, state_ld, step, beta1, beta2, eps);
+    a.msg = static_cast<uint32_t*>(msg);
+    a.msg_capacity = (uint64_t)msg_capacity;
+    a.version = version;
+    a.status = status;
+    // launched even for max_rows == 0: the (empty) message header is still written
+    hipLaunchKernelGGL(k_sparse_adam<true>, dim3(adam_blocks(max_rows > 0 ? max_rows : 1, a.rows_per_wave)),
+                       dim3(GS_BLOCK), 0, st, a, idx, count);
     return hipGetLastError();
 }
 

@@ -33,17 +33,21 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
     return v;
 }
 
-// Sum over a wave; every lane gets the result.  DPP row reductions followed
-// by a combination of the four 16-lane rows through readlane.
+// Sum over each 16-lane row; every lane of the row gets its row's sum.
+// quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror.  The
+// permuted operand is taken with old = 0 and bound_ctrl set (a lane outside
+// EXEC contributes 0), which lets the compiler fold each step into a single
+// v_add_f32 with a DPP source and interleave independent reductions.
 __device__ __forceinline__ float dpp_row_sum(float v) {
-    // quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror
-    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, true));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, true));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, true));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, true));
     return v;
 }
 
+// Sum over a wave; every lane gets the result.  DPP row reductions followed
+// by a combination of the four 16-lane rows through readlane.
 __device__ __forceinline__ float wave_sum(float v) {
     v = dpp_row_sum(v);
     float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
@@ -87,6 +91,18 @@ __device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* scratch)
 // ---------------------------------------------------------------------------
 
 namespace gsmi {
+
+// Publication message layout (see gs_delta_pack): 8 header words, the group
+// widths padded to a multiple of 4 words, K ids, zero padding to 16 bytes,
+// then K rows of row_len floats.
+__host__ __device__ inline uint64_t msg_words_before_rows(uint64_t count, int32_t n_groups) {
+    const uint64_t gw = (uint64_t)((n_groups + 3) / 4) * 4;
+    return ((8 + gw + count) + 3) / 4 * 4;
+}
+
+__host__ __device__ inline uint64_t msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups) {
+    return 4 * (msg_words_before_rows(count, n_groups) + count * (uint64_t)row_len);
+}
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 inline uint32_t div_up(uint64_t a, uint64_t b) { return (uint32_t)((a + b - 1) / b); }

@@ -20,15 +20,6 @@ struct GroupArgs {
     int32_t rows_per_wave;
 };
 
-__host__ __device__ inline uint64_t msg_words_before_rows(uint64_t count, int32_t n_groups) {
-    const uint64_t gw = (uint64_t)((n_groups + 3) / 4) * 4;
-    return ((8 + gw + count) + 3) / 4 * 4;
-}
-
-__host__ __device__ inline uint64_t msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups) {
-    return 4 * (msg_words_before_rows(count, n_groups) + count * (uint64_t)row_len);
-}
-
 __device__ __forceinline__ void lane_group(const GroupArgs& a, int lane, int& sub, int& grp, int& c) {
     sub = lane / a.row_len;
     c = lane - sub * a.row_len;

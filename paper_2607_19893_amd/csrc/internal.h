@@ -47,16 +47,21 @@ hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, 
 size_t raster_bwd_ws_bytes(int32_t n, uint32_t capacity);
 hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
                              const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
-                             const uint32_t* vis_idx,
-                             const uint32_t* vis_count, uint32_t capacity, const float* final_T,
-                             const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
-                             const gs_scene& grads, float* grad2d, float* grad_norm, void* ws, int stages,
+                             const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity,
+                             const float* final_T, const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
+                             float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, int stages,
                              hipStream_t st);
 
 // adam.hip
 hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
-                              const uint32_t* count, int32_t max_rows, int32_t step, double beta1, double beta2,
-                              double eps, hipStream_t st);
+                              const uint32_t* count, int32_t max_rows, const float* grad_rows, int32_t grad_ld,
+                              float* m, float* v, int32_t state_ld, int32_t step, double beta1, double beta2,
+                              double eps, float* delta_rows, int32_t delta_ld, hipStream_t st);
+hipError_t launch_sparse_adam_publish(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
+                                      const uint32_t* count, int32_t max_rows, const float* grad_rows,
+                                      int32_t grad_ld, float* m, float* v, int32_t state_ld, int32_t step,
+                                      double beta1, double beta2, double eps, uint32_t version, void* msg,
+                                      size_t msg_capacity, gs_device_status* status, hipStream_t st);
 
 // delta.hip
 size_t delta_msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups);

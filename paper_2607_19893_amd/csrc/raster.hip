@@ -3,18 +3,19 @@
 //
 // Forward: one 256-thread workgroup per 16x16 tile, one pixel per thread.
 // The tile's sorted pairs are staged through LDS in batches of 256
-// (id, mean2d, conic+opacity, rgb); a workgroup-wide count of finished
-// pixels ends the batch loop early.
+// (mean2d, conic+opacity, rgb, footprint half-extents); a workgroup-wide
+// count of finished pixels ends the batch loop early.
 //
 // Backward: same tile/pixel mapping, walking each tile's pairs back to front.
 // Each pixel recovers the transmittance in front of a pair by dividing by
 // (1 - alpha) and keeps the suffix colour sum; per pair, the 9 partial
-// derivatives are summed across each wave with DPP row reductions and across
-// the 4 waves through LDS, then written to the pair's own slot (the pair's
-// position in emission order).  A second kernel, one thread per visible
-// primitive, sums its slots in a fixed order -- the result is deterministic,
-// no floating-point atomics -- and applies the projection and colour chain
-// rule in fp32.
+// derivatives are summed across each wave (LDS atomics for a few lanes, DPP
+// row reductions otherwise) and across the 4 waves in a fixed order, then
+// written to the pair's slot at its sorted position.  Per visible primitive,
+// k_slot_sums adds its slots in emission order (through the sorted position
+// of every emitted pair) -- deterministic, no floating-point atomics in global
+// memory -- and k_project_bwd applies the projection and colour chain rule
+// (geometry in fp64) and writes one compact gradient row.
 #include "common.h"
 #include "internal.h"
 
@@ -428,46 +429,33 @@ __device__ __forceinline__ void sh_basis_grad(float x, float y, float z, float* 
 
 __device__ __forceinline__ float dot3(const float* a, const float* b) { return a[0] * b[0] + a[1] * b[1] + a[2] * b[2]; }
 
-// Per-primitive row I/O goes through LDS: a block stages the parameter rows of
-// its 256 primitives with row-contiguous loads (lanes walk along a row, so a
-// 192-byte SH row is read by consecutive lanes), each thread works on its own
-// row in LDS (odd row stride: conflict-free), and the gradient rows leave the
-// same way.
+// Per-primitive work runs in two kernels.  k_slot_sums (one thread per
+// visible row, small register footprint, high occupancy) adds each
+// primitive's pair slots in a fixed order and writes a compact 12-float record
+// per row; k_project_bwd (one thread per visible row) then reads that record
+// and the parameter row and applies the chain rule.  Lists of up to
+// kSerialSlots slots are summed by their own lane with kSlotUnroll slots in
+// flight; longer ones (a primitive spanning many tiles) by the whole wave.
 constexpr uint32_t kSerialSlots = 32;
+constexpr int kSlotUnroll = 4;
+constexpr int kG2 = 12;     // floats per row of the compact 2D-gradient record (9 used)
 
 template <int DEG>
 struct RowLayout {
     static constexpr int K = (DEG + 1) * (DEG + 1);
     static constexpr int SH = 3 * K;
     static constexpr int ROW = 11 + SH;                        // mean 3, log_scale 3, quat 4, opacity 1, sh
-    static constexpr int STRIDE = (ROW % 2 == 0) ? ROW + 1 : ROW;
+    static constexpr int ROW4 = (ROW + 3) / 4 * 4;
 };
 
-template <int COLS, int OFF, int STRIDE>
-__device__ __forceinline__ void rows_to_lds(const float* __restrict__ src, const uint32_t* s_id, uint32_t nrows,
-                                            float* s_row) {
-    for (uint32_t e = threadIdx.x; e < nrows * COLS; e += GS_BLOCK) {
-        const uint32_t r = e / COLS, c = e - r * COLS;
-        s_row[r * STRIDE + OFF + c] = src[(size_t)s_id[r] * COLS + c];
-    }
-}
-
-template <int COLS, int OFF, int STRIDE>
-__device__ __forceinline__ void lds_to_rows(float* __restrict__ dst, const uint32_t* s_id, uint32_t nrows,
-                                            const float* s_row) {
-    for (uint32_t e = threadIdx.x; e < nrows * COLS; e += GS_BLOCK) {
-        const uint32_t r = e / COLS, c = e - r * COLS;
-        dst[(size_t)s_id[r] * COLS + c] = s_row[r * STRIDE + OFF + c];
-    }
-}
-
 // Chain rule from one primitive's 2D gradient (du, dv, dA, dB, dC in g2) back
-// to mean, log-scale and quaternion, evaluated in scalar type Rl.  gmu holds
-// the colour path's contribution to dL/dmean; out receives mean (0..2),
-// log_scale (3..5) and quat (6..9) gradients.
+// to mean, log-scale and quaternion, evaluated in scalar type Rl.  gpw
+// receives the projection path's camera-space mean gradient (the world-space
+// one is R^T gpw, formed by the caller together with the colour path's part);
+// out receives log_scale (3..5) and quat (6..9) gradients.
 template <typename Rl>
 __device__ __forceinline__ void geometry_bwd(const float* mu_f, const float* ls_f, const float* qr_f,
-                                             const float* g2, const CamArgs& c, const float* gmu, float* out) {
+                                             const float* g2, const CamArgs& c, Rl* gpw, float* out) {
     Rl R[9];
 #pragma unroll
     for (int k = 0; k < 9; ++k) R[k] = (Rl)c.R[k];
@@ -552,8 +540,9 @@ __device__ __forceinline__ void geometry_bwd(const float* mu_f, const float* ls_
     gp[0] += gu * fx * itz;
     gp[1] += gv * fy * itz;
     gp[2] -= (gu * fx * p[0] + gv * fy * p[1]) * itz2;
-#pragma unroll
-    for (int k = 0; k < 3; ++k) out[k] = (float)((Rl)gmu[k] + R[k] * gp[0] + R[3 + k] * gp[1] + R[6 + k] * gp[2]);
+    gpw[0] = gp[0];
+    gpw[1] = gp[1];
+    gpw[2] = gp[2];
     // Sigma = M M^T with symmetric gradient Gs = ga T0T0^T + gb (T0T1^T + T1T0^T)/2 + gc T1T1^T
     Rl Gs[3][3];
 #pragma unroll
@@ -587,126 +576,175 @@ __device__ __forceinline__ void geometry_bwd(const float* mu_f, const float* ls_
     out[9] = (float)((gz - z * along) * iq);
 }
 
+// pos comes from pair_perm; after a pair-list overflow that array holds
+// whatever an earlier view (or the allocator) left there, so every position is
+// clamped into the slot array before use.
+__device__ __forceinline__ void add_slot(float* g, const float* __restrict__ slots, uint32_t pos, uint32_t capacity) {
+    pos = min(pos, capacity - 1u);
+    const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)pos * kSlot);
+    const float4 v0 = sl[0], v1 = sl[1], v2 = sl[2];
+    g[0] += v0.x; g[1] += v0.y; g[2] += v0.z; g[3] += v0.w;
+    g[4] += v1.x; g[5] += v1.y; g[6] += v1.z; g[7] += v1.w; g[8] += v2.x;
+}
+
+// Per visible row r: the primitive's 2D gradient, the sum of its pair slots in
+// emission order (none if the pair list overflowed its capacity).
+__global__ void __launch_bounds__(GS_BLOCK) k_slot_sums(
+    const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
+    const uint32_t* __restrict__ pair_offset, const uint32_t* __restrict__ pair_perm,
+    const float* __restrict__ slots, uint32_t capacity, float* __restrict__ g2c, float* __restrict__ grad2d,
+    float* __restrict__ grad_norm) {
+    const uint32_t V = *vis_count;
+    if (blockIdx.x * GS_BLOCK >= V) return;
+    const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
+    const bool valid = r < V;
+    const uint32_t id = valid ? vis_idx[r] : 0u;
+    const uint32_t first = valid ? pair_offset[id] : 0u;
+    const uint32_t nt = valid ? tiles[id] : 0u;
+    const bool fits = (uint64_t)first + nt <= capacity;
+    float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+    if (fits && nt <= kSerialSlots) {
+        uint32_t k = 0;
+        for (; k + kSlotUnroll <= nt; k += kSlotUnroll) {
+            uint32_t pos[kSlotUnroll];
+#pragma unroll
+            for (int u = 0; u < kSlotUnroll; ++u) pos[u] = min(pair_perm[first + k + u], capacity - 1u);
+            float4 v[kSlotUnroll][3];
+#pragma unroll
+            for (int u = 0; u < kSlotUnroll; ++u) {
+                const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)pos[u] * kSlot);
+                v[u][0] = sl[0];
+                v[u][1] = sl[1];
+                v[u][2] = sl[2];
+            }
+#pragma unroll
+            for (int u = 0; u < kSlotUnroll; ++u) {
+                g2[0] += v[u][0].x; g2[1] += v[u][0].y; g2[2] += v[u][0].z; g2[3] += v[u][0].w;
+                g2[4] += v[u][1].x; g2[5] += v[u][1].y; g2[6] += v[u][1].z; g2[7] += v[u][1].w;
+                g2[8] += v[u][2].x;
+            }
+        }
+        for (; k < nt; ++k) add_slot(g2, slots, pair_perm[first + k], capacity);
+    }
+    uint64_t big = __ballot(fits && nt > kSerialSlots);
+    while (big) {
+        const int owner = __ffsll((unsigned long long)big) - 1;
+        big &= big - 1;
+        const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)first, owner);
+        const uint32_t nb = (uint32_t)__builtin_amdgcn_readlane((int)nt, owner);
+        float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+        for (uint32_t k = lane_id(); k < nb; k += GS_WAVE) add_slot(acc, slots, pair_perm[f + k], capacity);
+#pragma unroll
+        for (int q = 0; q < kG; ++q) {
+            const float v = wave_sum(acc[q]);
+            if (lane_id() == owner) g2[q] = v;
+        }
+    }
+    if (!valid) return;
+    float4* dst = reinterpret_cast<float4*>(g2c + (size_t)r * kG2);
+    dst[0] = make_float4(g2[0], g2[1], g2[2], g2[3]);
+    dst[1] = make_float4(g2[4], g2[5], g2[6], g2[7]);
+    dst[2] = make_float4(g2[8], 0.0f, 0.0f, 0.0f);
+    if (grad2d) {
+#pragma unroll
+        for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
+    }
+    if (grad_norm) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
+}
+
+template <int N>
+__device__ __forceinline__ void load_row(const float* __restrict__ src, float* dst) {
+    if constexpr (N % 4 == 0) {
+        const float4* s4 = reinterpret_cast<const float4*>(src);
+#pragma unroll
+        for (int k = 0; k < N / 4; ++k) {
+            const float4 v = s4[k];
+            dst[4 * k] = v.x; dst[4 * k + 1] = v.y; dst[4 * k + 2] = v.z; dst[4 * k + 3] = v.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < N; ++k) dst[k] = src[k];
+    }
+}
+
+// Per visible row r: chain rule from the compact 2D gradient to the
+// parameters; writes the row's gradient record at grad_rows + r * ld.
 template <int DEG>
 __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
-    const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
-    const uint32_t* __restrict__ pair_offset, const uint32_t* __restrict__ pair_perm, const float* __restrict__ slots,
-    const uint8_t* __restrict__ clampm,
-    const float* __restrict__ mean, const float* __restrict__ log_scale, const float* __restrict__ quat,
-    const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c, uint32_t capacity,
-    float* __restrict__ g_mean, float* __restrict__ g_ls, float* __restrict__ g_quat, float* __restrict__ g_op,
-    float* __restrict__ g_sh, float* __restrict__ grad2d, float* __restrict__ grad_norm) {
+    const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const float* __restrict__ g2c,
+    const uint8_t* __restrict__ clampm, const float* __restrict__ mean, const float* __restrict__ log_scale,
+    const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c,
+    float* __restrict__ grad_rows, int32_t ld) {
     using L = RowLayout<DEG>;
-    constexpr int K = L::K, ST = L::STRIDE;
-    __shared__ float s_row[GS_BLOCK * ST];
-    __shared__ uint32_t s_id[GS_BLOCK];
+    constexpr int K = L::K;
     const uint32_t V = *vis_count;
-    const uint32_t r0 = blockIdx.x * GS_BLOCK;
-    if (r0 >= V) return;
-    const uint32_t nrows = min((uint32_t)GS_BLOCK, V - r0);
-    const int tid = threadIdx.x;
-    const bool valid = (uint32_t)tid < nrows;
-    const uint32_t id = valid ? vis_idx[r0 + tid] : 0u;
-    s_id[tid] = id;
-    __syncthreads();
-    rows_to_lds<3, 0, ST>(mean, s_id, nrows, s_row);
-    rows_to_lds<3, 3, ST>(log_scale, s_id, nrows, s_row);
-    rows_to_lds<4, 6, ST>(quat, s_id, nrows, s_row);
-    rows_to_lds<1, 10, ST>(opacity, s_id, nrows, s_row);
-    rows_to_lds<L::SH, 11, ST>(sh, s_id, nrows, s_row);
-    // 1. this primitive's 2D gradient: the sum of its pair slots (none if the
-    //    pair list overflowed its capacity).  Short lists are summed by their
-    //    own lane; long ones (a primitive spanning many tiles) by the whole
-    //    wave, 64 slots at a time, so no lane walks thousands of slots alone.
-    float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+    const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
+    if (r >= V) return;
+    const uint32_t id = vis_idx[r];
+    float g2[kG];
     {
-        const uint32_t first = valid ? pair_offset[id] : 0u;
-        const uint32_t nt = valid ? tiles[id] : 0u;
-        const bool fits = (uint64_t)first + nt <= capacity;
-        if (fits && nt <= kSerialSlots) {
-            for (uint32_t k = 0; k < nt; ++k) {
-                const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)pair_perm[first + k] * kSlot);
-                const float4 v0 = sl[0], v1 = sl[1], v2 = sl[2];
-                g2[0] += v0.x; g2[1] += v0.y; g2[2] += v0.z; g2[3] += v0.w;
-                g2[4] += v1.x; g2[5] += v1.y; g2[6] += v1.z; g2[7] += v1.w; g2[8] += v2.x;
-            }
-        }
-        uint64_t big = __ballot(fits && nt > kSerialSlots);
-        while (big) {
-            const int owner = __ffsll((unsigned long long)big) - 1;
-            big &= big - 1;
-            const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)first, owner);
-            const uint32_t nb = (uint32_t)__builtin_amdgcn_readlane((int)nt, owner);
-            float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-            for (uint32_t k = lane_id(); k < nb; k += GS_WAVE) {
-                const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)pair_perm[f + k] * kSlot);
-                const float4 v0 = sl[0], v1 = sl[1], v2 = sl[2];
-                acc[0] += v0.x; acc[1] += v0.y; acc[2] += v0.z; acc[3] += v0.w;
-                acc[4] += v1.x; acc[5] += v1.y; acc[6] += v1.z; acc[7] += v1.w; acc[8] += v2.x;
-            }
-#pragma unroll
-            for (int q = 0; q < kG; ++q) {
-                const float v = wave_sum(acc[q]);
-                if (lane_id() == owner) g2[q] = v;
-            }
-        }
+        const float4* s4 = reinterpret_cast<const float4*>(g2c + (size_t)r * kG2);
+        const float4 a = s4[0], b = s4[1], d = s4[2];
+        g2[0] = a.x; g2[1] = a.y; g2[2] = a.z; g2[3] = a.w;
+        g2[4] = b.x; g2[5] = b.y; g2[6] = b.z; g2[7] = b.w; g2[8] = d.x;
     }
-    __syncthreads();
-    if (valid) {
-        float* row = s_row + tid * ST;
-        if (grad2d) {
+    float mu[3], ls[3], qr[4];
+    load_row<3>(mean + (size_t)id * 3, mu);
+    load_row<3>(log_scale + (size_t)id * 3, ls);
+    load_row<4>(quat + (size_t)id * 4, qr);
+    const float logit = opacity[id];
+    const uint8_t cm = clampm[id];
+    float out[L::ROW4];
+
+    // 1. geometry, in fp64: for wide footprints the conic gradient is large
+    //    while the scale / rotation gradients it produces are tiny, and the
+    //    chain cancels too much for fp32
+    double gp[3];
+    geometry_bwd<double>(mu, ls, qr, g2, c, gp, out);
+
+    // 2. opacity
+    const float o = 1.0f / (1.0f + expf(-logit));
+    out[10] = g2[5] * o * (1.0f - o);
+
+    // 3. colour: dL/dsh and the view-direction path to the mean
+    float gmu[3];
+    {
+        float v[3] = {mu[0] - c.campos[0], mu[1] - c.campos[1], mu[2] - c.campos[2]};
+        const float len = sqrtf(dot3(v, v));
+        const float il = 1.0f / len;
+        const float d[3] = {v[0] * il, v[1] * il, v[2] * il};
+        float Y[16], G[16][3];
+        sh_basis_grad<DEG>(d[0], d[1], d[2], Y, G);
+        const float gc[3] = {(cm & 1) ? 0.0f : g2[6], (cm & 2) ? 0.0f : g2[7], (cm & 4) ? 0.0f : g2[8]};
+        float co[3 * K];
+        load_row<3 * K>(sh + (size_t)id * 3 * K, co);
+        float gd[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
-            for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
+        for (int k = 0; k < K; ++k) {
+            const float a = gc[0] * co[3 * k] + gc[1] * co[3 * k + 1] + gc[2] * co[3 * k + 2];
+            gd[0] += a * G[k][0];
+            gd[1] += a * G[k][1];
+            gd[2] += a * G[k][2];
+            out[11 + 3 * k + 0] = gc[0] * Y[k];
+            out[11 + 3 * k + 1] = gc[1] * Y[k];
+            out[11 + 3 * k + 2] = gc[2] * Y[k];
         }
-        if (grad_norm) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
-
-        const float mu[3] = {row[0], row[1], row[2]};
-        const float ls[3] = {row[3], row[4], row[5]};
-        const float qr[4] = {row[6], row[7], row[8], row[9]};
-        // 2. opacity
-        const float o = 1.0f / (1.0f + expf(-row[10]));
-        row[10] = g2[5] * o * (1.0f - o);
-
-        // 3. colour: dL/dsh (written over the coefficients) and the view-direction path
-        float gmu[3];
-        {
-            float v[3] = {mu[0] - c.campos[0], mu[1] - c.campos[1], mu[2] - c.campos[2]};
-            const float len = sqrtf(dot3(v, v));
-            const float il = 1.0f / len;
-            const float d[3] = {v[0] * il, v[1] * il, v[2] * il};
-            float Y[16], G[16][3];
-            sh_basis_grad<DEG>(d[0], d[1], d[2], Y, G);
-            const uint8_t cm = clampm[id];
-            const float gc[3] = {(cm & 1) ? 0.0f : g2[6], (cm & 2) ? 0.0f : g2[7], (cm & 4) ? 0.0f : g2[8]};
-            float* co = row + 11;
-            float gd[3] = {0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const float a = gc[0] * co[3 * k] + gc[1] * co[3 * k + 1] + gc[2] * co[3 * k + 2];
-                gd[0] += a * G[k][0];
-                gd[1] += a * G[k][1];
-                gd[2] += a * G[k][2];
-                co[3 * k + 0] = gc[0] * Y[k];
-                co[3 * k + 1] = gc[1] * Y[k];
-                co[3 * k + 2] = gc[2] * Y[k];
-            }
-            const float rad = dot3(gd, d);
-            gmu[0] = (gd[0] - d[0] * rad) * il;
-            gmu[1] = (gd[1] - d[1] * rad) * il;
-            gmu[2] = (gd[2] - d[2] * rad) * il;
-        }
-
-        // 4. geometry, in fp64: for wide footprints the conic gradient is large
-        //    while the scale / rotation gradients it produces are tiny, and the
-        //    chain cancels too much for fp32
-        geometry_bwd<double>(mu, ls, qr, g2, c, gmu, row);
+        const float rad = dot3(gd, d);
+        gmu[0] = (gd[0] - d[0] * rad) * il;
+        gmu[1] = (gd[1] - d[1] * rad) * il;
+        gmu[2] = (gd[2] - d[2] * rad) * il;
     }
-    __syncthreads();
-    lds_to_rows<3, 0, ST>(g_mean, s_id, nrows, s_row);
-    lds_to_rows<3, 3, ST>(g_ls, s_id, nrows, s_row);
-    lds_to_rows<4, 6, ST>(g_quat, s_id, nrows, s_row);
-    lds_to_rows<1, 10, ST>(g_op, s_id, nrows, s_row);
-    lds_to_rows<L::SH, 11, ST>(g_sh, s_id, nrows, s_row);
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        out[k] = (float)((double)gmu[k] + (double)c.R[k] * gp[0] + (double)c.R[3 + k] * gp[1] +
+                         (double)c.R[6 + k] * gp[2]);
+#pragma unroll
+    for (int k = L::ROW; k < L::ROW4; ++k) out[k] = 0.0f;
+
+    float4* dst = reinterpret_cast<float4*>(grad_rows + (size_t)r * ld);
+#pragma unroll
+    for (int k = 0; k < L::ROW4 / 4; ++k) dst[k] = make_float4(out[4 * k], out[4 * k + 1], out[4 * k + 2], out[4 * k + 3]);
+    for (int k = L::ROW4 / 4; k < ld / 4; ++k) dst[k] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 }
 
 }  // namespace
@@ -747,17 +785,24 @@ hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, 
     return hipGetLastError();
 }
 
-size_t raster_bwd_ws_bytes(int32_t, uint32_t capacity) {
+// Workspace: the pair slots (capacity x kSlot floats), then the compact 2D
+// gradient records of the visible rows (n x kG2 floats).
+static size_t slots_bytes(uint32_t capacity) {
     return align256(sizeof(float) * kSlot * (size_t)(capacity > 0 ? capacity : 1));
+}
+
+size_t raster_bwd_ws_bytes(int32_t n, uint32_t capacity) {
+    return slots_bytes(capacity) + align256(sizeof(float) * kG2 * (size_t)(n > 0 ? n : 1));
 }
 
 hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
                              const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
-                             const uint32_t* vis_idx,
-                             const uint32_t* vis_count, uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
-                             const float* dL_dimg, const float bg[3], const gs_scene& grads, float* grad2d,
-                             float* grad_norm, void* ws, int stages, hipStream_t st) {
+                             const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity,
+                             const float* final_T, const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
+                             float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, int stages,
+                             hipStream_t st) {
     float* slots = static_cast<float*>(ws);
+    float* g2c = reinterpret_cast<float*>(static_cast<char*>(ws) + slots_bytes(capacity));
     const int32_t T = cam.tiles_x * cam.tiles_y;
     if ((stages & 1) && T > 0)
         hipLaunchKernelGGL(k_raster_bwd, dim3(T), dim3(GS_BLOCK), 0, st, ranges, vals,
@@ -767,10 +812,11 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || scene.n == 0 || !(stages & 2)) return e;
     const dim3 grid(div_up(scene.n, GS_BLOCK));
+    hipLaunchKernelGGL(k_slot_sums, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset,
+                       pair_perm, slots, capacity, g2c, grad2d, grad_norm);
 #define GS_LAUNCH_PBWD(D)                                                                                        \
-    hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset, \
-                       pair_perm, slots, proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam,     \
-                       capacity, grads.mean, grads.log_scale, grads.quat, grads.opacity, grads.sh, grad2d, grad_norm)
+    hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, g2c, proj.clamp,        \
+                       scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam, grad_rows, grad_ld)
     switch (scene.sh_degree) {
         case 0: GS_LAUNCH_PBWD(0); break;
         case 1: GS_LAUNCH_PBWD(1); break;

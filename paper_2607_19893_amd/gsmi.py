@@ -48,7 +48,7 @@ class gs_proj(ctypes.Structure):
 
 
 class gs_adam_group(ctypes.Structure):
-    _fields_ = [("p", P), ("g", P), ("m", P), ("v", P), ("delta", P), ("cols", i32), ("lr", f32)]
+    _fields_ = [("p", P), ("cols", i32), ("lr", f32)]
 
 
 class gs_group(ctypes.Structure):
@@ -69,22 +69,26 @@ _lib.gs_bin_sort.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, u32, 
 _lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, P, P, P, P, P, P]
 _lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
 _lib.gs_raster_bwd.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P, P, P,
-                               P, P, P, u32, P, P, P, P, ctypes.POINTER(gs_scene), P, P, P, sz, P]
+                               P, P, P, u32, P, P, P, P, P, i32, P, P, P, sz, P]
 _lib.gs_raster_bwd_pixels.argtypes = [ctypes.POINTER(gs_proj), ctypes.POINTER(gs_camera), P, P, u32, P, P, P, P, P,
                                       sz, P]
 _lib.gs_raster_bwd_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj),
-                                       P, P, P, P, u32, ctypes.POINTER(gs_scene), P, P, P, sz, P]
-_lib.gs_sparse_adam.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, i32, ctypes.c_double,
-                                ctypes.c_double, ctypes.c_double, P]
+                                       P, P, P, P, u32, P, i32, P, P, P, sz, P]
+_lib.gs_sparse_adam.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, P, i32, P, P, i32, i32,
+                                ctypes.c_double, ctypes.c_double, ctypes.c_double, P, i32, P]
+_lib.gs_sparse_adam_publish.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, P, i32, P, P, i32, i32,
+                                        ctypes.c_double, ctypes.c_double, ctypes.c_double, u32, P, sz, P, P]
 _lib.gs_delta_pack.argtypes = [P, P, i32, ctypes.POINTER(gs_group), i32, u32, P, sz, P, P]
 _lib.gs_delta_apply.argtypes = [P, sz, ctypes.POINTER(gs_group), i32, i32, i32, i32, P, P, P]
 for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
-              "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_delta_pack", "gs_delta_apply"):
+              "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
+              "gs_delta_pack", "gs_delta_apply"):
     getattr(_lib, _name).restype = i32
 
 EXPORTS = ["gs_abi_version", "gs_status_string", "gs_last_error", "gs_workspace_bytes", "gs_delta_msg_bytes",
            "gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
-           "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_delta_pack", "gs_delta_apply"]
+           "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
+           "gs_delta_pack", "gs_delta_apply"]
 
 
 class GsmiError(RuntimeError):
@@ -199,16 +203,15 @@ def gs_loss_l1(img, target, width, height, loss, dL_dimg, ws, stream=None):
 
 
 def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, pair_offset, pair_perm, vis_idx,
-                  vis_count, capacity, final_T, n_contrib, dL_dimg, bg, grads: gs_scene, grad2d, grad_norm, ws,
+                  vis_count, capacity, final_T, n_contrib, dL_dimg, bg, grad_rows, grad_ld, grad2d, grad_norm, ws,
                   stream=None):
     b = _bg(bg)
     return _check("gs_raster_bwd", _lib.gs_raster_bwd(ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj),
                                                       ptr(vals), ptr(ranges), ptr(pair_offset), ptr(pair_perm),
-                                                      ptr(vis_idx),
-                                                      ptr(vis_count), int(capacity), ptr(final_T), ptr(n_contrib),
-                                                      ptr(dL_dimg), ctypes.cast(b, P), ctypes.byref(grads),
-                                                      ptr(grad2d), ptr(grad_norm), ptr(ws),
-                                                      ws.numel() * ws.element_size(),
+                                                      ptr(vis_idx), ptr(vis_count), int(capacity), ptr(final_T),
+                                                      ptr(n_contrib), ptr(dL_dimg), ctypes.cast(b, P),
+                                                      ptr(grad_rows), int(grad_ld), ptr(grad2d), ptr(grad_norm),
+                                                      ptr(ws), ws.numel() * ws.element_size(),
                                                       stream if stream is not None else current_stream()))
 
 
@@ -222,25 +225,35 @@ def gs_raster_bwd_pixels(proj: gs_proj, cam: gs_camera, vals, ranges, capacity, 
 
 
 def gs_raster_bwd_project(scene: gs_scene, cam: gs_camera, proj: gs_proj, pair_offset, pair_perm, vis_idx, vis_count,
-                          capacity, grads: gs_scene, grad2d, grad_norm, ws, stream=None):
+                          capacity, grad_rows, grad_ld, grad2d, grad_norm, ws, stream=None):
     return _check("gs_raster_bwd_project", _lib.gs_raster_bwd_project(
         ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj), ptr(pair_offset), ptr(pair_perm), ptr(vis_idx),
-        ptr(vis_count), int(capacity), ctypes.byref(grads), ptr(grad2d), ptr(grad_norm), ptr(ws),
+        ptr(vis_count), int(capacity), ptr(grad_rows), int(grad_ld), ptr(grad2d), ptr(grad_norm), ptr(ws),
         ws.numel() * ws.element_size(), stream if stream is not None else current_stream()))
 
 
 def make_adam_groups(groups):
-    """groups: list of (p, g, m, v, delta_or_None, lr) tensors [n, cols]."""
+    """groups: list of (p [n, cols] tensor, lr)."""
     arr = (gs_adam_group * len(groups))()
-    for i, (p, g, m, v, d, lr) in enumerate(groups):
-        arr[i] = gs_adam_group(ptr(p), ptr(g), ptr(m), ptr(v), ptr(d), int(p.shape[1]), float(lr))
+    for i, (p, lr) in enumerate(groups):
+        arr[i] = gs_adam_group(ptr(p), int(p.shape[1]), float(lr))
     return arr
 
 
-def gs_sparse_adam(groups_arr, n_groups, idx, count, max_rows, step, beta1, beta2, eps, stream=None):
-    return _check("gs_sparse_adam", _lib.gs_sparse_adam(groups_arr, int(n_groups), ptr(idx), ptr(count),
-                                                        int(max_rows), int(step), float(beta1), float(beta2),
-                                                        float(eps), stream if stream is not None else current_stream()))
+def gs_sparse_adam(groups_arr, n_groups, idx, count, max_rows, grad_rows, grad_ld, m, v, state_ld, step, beta1,
+                   beta2, eps, delta_rows=None, delta_ld=0, stream=None):
+    return _check("gs_sparse_adam", _lib.gs_sparse_adam(
+        groups_arr, int(n_groups), ptr(idx), ptr(count), int(max_rows), ptr(grad_rows), int(grad_ld), ptr(m), ptr(v),
+        int(state_ld), int(step), float(beta1), float(beta2), float(eps), ptr(delta_rows), int(delta_ld),
+        stream if stream is not None else current_stream()))
+
+
+def gs_sparse_adam_publish(groups_arr, n_groups, idx, count, max_rows, grad_rows, grad_ld, m, v, state_ld, step,
+                           beta1, beta2, eps, version, msg, status, stream=None):
+    return _check("gs_sparse_adam_publish", _lib.gs_sparse_adam_publish(
+        groups_arr, int(n_groups), ptr(idx), ptr(count), int(max_rows), ptr(grad_rows), int(grad_ld), ptr(m), ptr(v),
+        int(state_ld), int(step), float(beta1), float(beta2), float(eps), int(version), ptr(msg),
+        msg.numel() * msg.element_size(), ptr(status), stream if stream is not None else current_stream()))
 
 
 def make_groups(tensors):

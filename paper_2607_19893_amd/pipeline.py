@@ -33,15 +33,19 @@ class ViewTrainer:
         self.K = (self.deg + 1) ** 2
         self.cols = [3, 3, 4, 1, 3 * self.K]
         self.row_len = sum(self.cols)
+        # gradient rows, moments and step rows: one row per primitive (moments)
+        # or per visible row (gradients, steps), padded to 16/32/64 floats
+        self.ld = next(w for w in (16, 32, 64) if w >= self.row_len)
+        self.col_off = [sum(self.cols[:i]) for i in range(len(self.cols))]
         self.lr, self.beta1, self.beta2, self.eps = lr, beta1, beta2, eps
         n = self.n
         host = [scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh]
         self.params = [torch.from_numpy(np.ascontiguousarray(a, np.float32).reshape(n, c)).to(self.dev)
                        for a, c in zip(host, self.cols)]
-        self.grads = [torch.zeros(n, c, device=self.dev) for c in self.cols]
-        self.m = [torch.zeros(n, c, device=self.dev) for c in self.cols]
-        self.v = [torch.zeros(n, c, device=self.dev) for c in self.cols]
-        self.delta = [torch.zeros(n, c, device=self.dev) for c in self.cols]
+        self.grad_rows = torch.zeros(max(1, n), self.ld, device=self.dev)
+        self.m = torch.zeros(max(1, n), self.ld, device=self.dev)
+        self.v = torch.zeros(max(1, n), self.ld, device=self.dev)
+        self.delta_rows = torch.zeros(max(1, n), self.ld, device=self.dev)
         self.replica = [p.clone() for p in self.params] if with_replica else None
         self.version = _u32(n, self.dev)
         # projection
@@ -71,12 +75,10 @@ class ViewTrainer:
         self._set_image(max(1, max_width), max(1, max_height))
         self._set_capacity(max(1, capacity))
         self.scene_s = gsmi.make_scene(n, self.deg, *self.params)
-        self.grads_s = gsmi.make_scene(n, self.deg, *self.grads)
         self.proj_s = gsmi.make_proj(self.radius, self.tiles, self.rect, self.depth, self.mean2d, self.conic,
                                      self.rgb, self.clamp)
-        self.adam_arr = gsmi.make_adam_groups([(p, g, m, v, d, lr) for p, g, m, v, d in
-                                               zip(self.params, self.grads, self.m, self.v, self.delta)])
-        self.delta_arr = gsmi.make_groups(self.delta)
+        self.adam_arr = gsmi.make_adam_groups([(p, lr) for p in self.params])
+        self.params_arr = gsmi.make_groups(self.params)
         self.replica_arr = gsmi.make_groups(self.replica) if with_replica else None
         self.msg = torch.zeros((gsmi.gs_delta_msg_bytes(n, self.row_len, 5) + 15) // 16 * 4, dtype=torch.int32,
                                device=self.dev)
@@ -171,8 +173,8 @@ class ViewTrainer:
     def raster_bwd(self, bg=(0.0, 0.0, 0.0), grad2d=True):
         _, fT, nc, dL, _ = self._img_views()
         gsmi.gs_raster_bwd(self.scene_s, self.cam_c, self.proj_s, self.vals, self.ranges, self.pair_offset,
-                           self.pair_perm, self.vis_idx, self.counts[0:1], self.capacity, fT, nc, dL, bg, self.grads_s,
-                           self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
+                           self.pair_perm, self.vis_idx, self.counts[0:1], self.capacity, fT, nc, dL, bg,
+                           self.grad_rows, self.ld, self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
 
     def raster_bwd_pixels(self, bg=(0.0, 0.0, 0.0)):
         _, fT, nc, dL, _ = self._img_views()
@@ -181,39 +183,65 @@ class ViewTrainer:
 
     def raster_bwd_project(self, grad2d=False):
         gsmi.gs_raster_bwd_project(self.scene_s, self.cam_c, self.proj_s, self.pair_offset, self.pair_perm,
-                                   self.vis_idx, self.counts[0:1], self.capacity, self.grads_s,
+                                   self.vis_idx, self.counts[0:1], self.capacity, self.grad_rows, self.ld,
                                    self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
 
     def active_set(self):
         gsmi.gs_visible_set(gsmi.GS_PRED_U8_NONZERO, self.active, self.n, self.act_idx, self.counts[2:3], self.ws_vis)
 
     def adam(self, step):
-        gsmi.gs_sparse_adam(self.adam_arr, 5, self.vis_idx, self.counts[0:1], self.n, step, self.beta1, self.beta2,
-                            self.eps)
+        """Sparse Adam over the visible rows; the steps go to delta_rows."""
+        gsmi.gs_sparse_adam(self.adam_arr, 5, self.vis_idx, self.counts[0:1], self.n, self.grad_rows, self.ld, self.m,
+                            self.v, self.ld, step, self.beta1, self.beta2, self.eps, self.delta_rows, self.ld)
 
-    def pack(self, version):
-        gsmi.gs_delta_pack(self.vis_idx, self.counts[0:1], self.n, self.delta_arr, 5, version, self.msg, self.status)
+    def adam_publish(self, step, version):
+        """Sparse Adam over the visible rows, its steps staged as a message."""
+        gsmi.gs_sparse_adam_publish(self.adam_arr, 5, self.vis_idx, self.counts[0:1], self.n, self.grad_rows,
+                                    self.ld, self.m, self.v, self.ld, step, self.beta1, self.beta2, self.eps,
+                                    version, self.msg, self.status)
+
+    def pack_params(self, version):
+        """Stage the current parameter rows of the visible set (for an overwrite replica)."""
+        gsmi.gs_delta_pack(self.vis_idx, self.counts[0:1], self.n, self.params_arr, 5, version, self.msg,
+                           self.status)
+
+    # -- host views of compact rows ------------------------------------------
+    def rows_by_group(self, t, count):
+        """Per-group numpy arrays [count, cols] of a [*, ld] row table (gradients, moments, steps)."""
+        a = t[:count].cpu().numpy()
+        return [a[:, o:o + c] for o, c in zip(self.col_off, self.cols)]
+
+    def set_state(self, m_groups, v_groups):
+        """Fill the moment tables from per-group [n, cols] arrays."""
+        m = np.zeros((max(1, self.n), self.ld), np.float32)
+        v = np.zeros((max(1, self.n), self.ld), np.float32)
+        for o, c, a, b in zip(self.col_off, self.cols, m_groups, v_groups):
+            m[:self.n, o:o + c] = a.reshape(self.n, c)
+            v[:self.n, o:o + c] = b.reshape(self.n, c)
+        self.m.copy_(torch.from_numpy(m))
+        self.v.copy_(torch.from_numpy(v))
 
     def apply(self, mode=gsmi.GS_APPLY_ADD):
         gsmi.gs_delta_apply(self.msg, self.replica_arr, 5, self.n, self.n, mode, self.version, self.status)
 
     # -- whole view ----------------------------------------------------------
     PHASES = ("project", "visible", "bin_sort", "raster_fwd", "loss_l1", "raster_bwd_pixels", "raster_bwd_project",
-              "adam", "pack", "apply")
+              "adam_publish", "apply")
 
     def step(self, cam, step, version=1, publish=True, active=False, target=None, events=None):
-        """Project, visible set, bin+sort, forward, L1, backward, Adam, pack + apply.
+        """Project, visible set, bin+sort, forward, L1, backward, Adam staged as a message, apply to the replica.
+        publish=False runs plain Adam (steps to delta_rows) and no apply.
         target: device tensor (3*H*W) or None for the set_target buffer.
         events: optional list of len(PHASES)+1 torch.cuda.Event recorded around the phases."""
         ev = events
         calls = (lambda: self.project(cam), self.visible, self.bin_sort, lambda: self.raster_fwd(active=active),
                  lambda: self.loss_l1(target), self.raster_bwd_pixels, self.raster_bwd_project,
-                 lambda: self.adam(step), lambda: self.pack(version), self.apply)
+                 (lambda: self.adam_publish(step, version)) if publish else (lambda: self.adam(step)),
+                 self.apply if publish else (lambda: None))
         if ev:
             ev[0].record()
         for i, fn in enumerate(calls):
-            if publish or i < 8:
-                fn()
+            fn()
             if ev:
                 ev[i + 1].record()
 

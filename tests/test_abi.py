@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol(gs):
     for nm in names:
         assert hasattr(gs.raw(), nm), nm
         assert nm in gs.EXPORTS, nm
-    assert gs.gs_abi_version() == 1
+    assert gs.gs_abi_version() == 2
 
 
 def test_status_strings(gs):
@@ -40,7 +40,7 @@ def test_null_and_range_arguments_rejected(gs):
     L = gs.raw()
     assert L.gs_project(None, None, None, None) == gs.GS_ERR_INVALID_ARG
     assert "null scene" in gs.gs_last_error()
-    sc = gs.gs_scene(10, 4, 1, 1, 16, 1, 1)
+    sc = gs.gs_scene(10, 4, 1, 1, 16, 1, 16)
     cam = gs.gs_camera()
     pr = gs.gs_proj(16, 16, 16, 16, 16, 16, 16, 16)
     assert L.gs_project(ctypes.byref(sc), ctypes.byref(cam), ctypes.byref(pr), None) == gs.GS_ERR_INVALID_ARG
@@ -50,11 +50,28 @@ def test_null_and_range_arguments_rejected(gs):
     assert L.gs_project(ctypes.byref(sc), ctypes.byref(cam), ctypes.byref(pr), None) == gs.GS_ERR_UNSUPPORTED
     assert L.gs_visible_set(7, None, 0, None, None, None, 0, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_visible_set(0, 16, 100, 16, 16, 16, 0, None) == gs.GS_ERR_WORKSPACE
-    assert L.gs_sparse_adam(None, 0, None, None, 0, 1, 0.9, 0.999, 1e-15, None) == gs.GS_ERR_INVALID_ARG
-    grp = (gs.gs_adam_group * 1)(gs.gs_adam_group(16, 16, 16, 16, None, 70, 1e-3))
-    assert L.gs_sparse_adam(grp, 1, 16, 16, 10, 1, 0.9, 0.999, 1e-15, None) == gs.GS_ERR_UNSUPPORTED
+    A = (16, 16, 10, 16, 64, 16, 16, 64)          # idx, count, max_rows, grad_rows, grad_ld, m, v, state_ld
+    assert L.gs_sparse_adam(None, 0, *A, 1, 0.9, 0.999, 1e-15, None, 0, None) == gs.GS_ERR_INVALID_ARG
+    grp = (gs.gs_adam_group * 1)(gs.gs_adam_group(16, 70, 1e-3))
+    assert L.gs_sparse_adam(grp, 1, *A, 1, 0.9, 0.999, 1e-15, None, 0, None) == gs.GS_ERR_UNSUPPORTED
     grp[0].cols = 3
-    assert L.gs_sparse_adam(grp, 1, 16, 16, 10, 0, 0.9, 0.999, 1e-15, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_sparse_adam(grp, 1, *A, 0, 0.9, 0.999, 1e-15, None, 0, None) == gs.GS_ERR_INVALID_ARG
+    assert "step" in gs.gs_last_error()
+    assert L.gs_sparse_adam(grp, 1, 16, 16, 10, 16, 2, 16, 16, 64, 1, 0.9, 0.999, 1e-15, None, 0,
+                            None) == gs.GS_ERR_INVALID_ARG
+    assert "grad_ld" in gs.gs_last_error()
+    assert L.gs_sparse_adam(grp, 1, *A, 1, 0.9, 0.999, 1e-15, 16, 2, None) == gs.GS_ERR_INVALID_ARG
+    assert "delta_ld" in gs.gs_last_error()
+    assert L.gs_sparse_adam_publish(grp, 1, *A, 1, 0.9, 0.999, 1e-15, 1, None, 1024, 16,
+                                    None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_sparse_adam_publish(grp, 1, *A, 1, 0.9, 0.999, 1e-15, 1, 8, 1024, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert "aligned" in gs.gs_last_error()
+    # gradient rows of the backward: leading dimension a multiple of 4, at least the row length
+    sc3 = gs.gs_scene(10, 3, 16, 16, 16, 16, 16)
+    cam3 = gs.gs_camera()
+    assert L.gs_raster_bwd_project(ctypes.byref(sc3), ctypes.byref(cam3), ctypes.byref(pr), 16, 16, 16, 16, 100, 16,
+                                   58, None, None, 256, 1 << 20, None) == gs.GS_ERR_INVALID_ARG
+    assert "grad_ld" in gs.gs_last_error()
     g = (gs.gs_group * 1)(gs.gs_group(16, 3))
     assert L.gs_delta_apply(16, 4096, g, 1, 10, 10, 5, None, 16, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_delta_apply(16, 8, g, 1, 10, 10, 0, None, 16, None) == gs.GS_ERR_INVALID_ARG
@@ -67,6 +84,8 @@ def test_workspace_sizes_monotone(gs):
     b = gs.gs_workspace_bytes(gs.GS_WS_BIN_SORT, 2000, 10000, 256, 256)
     assert 0 < a < b and a % 256 == 0
     assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 0, 100) >= 9 * 4 * 100
+    assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 1000, 100) >= gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 0,
+                                                                                           100) + 9 * 4 * 1000
     assert gs.gs_workspace_bytes(99, 10, 10) == 0
 
 

@@ -93,34 +93,35 @@ def test_full_view(name, orc):
     _say(name, "dL zeroed at %d pixels; gradient rows checked %d of %d" % (int(amb_all.sum()), int(ok_rows.sum()), V))
     assert ok_rows.mean() > 0.999
     rows = vis.astype(np.int64)
-    for gi, (gname, gp, go, mg) in enumerate(zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.grads,
-                                                 grm.groups(), mags)):
-        st = assert_grads(gp.cpu().numpy()[rows], go, ok_rows, "grad." + gname, mag=mg)
+    for gi, (gname, gp, go, mg) in enumerate(zip(["mean", "log_scale", "quat", "opacity", "sh"],
+                                                 tr.rows_by_group(tr.grad_rows, V), grm.groups(), mags)):
+        st = assert_grads(gp, go, ok_rows, "grad." + gname, mag=mg)
         _say(name, gname, st)
     # the chain itself: recompute the loss gradient on the GPU and run backward,
-    # Adam, pack and apply exactly as the benchmark does
-    tr.loss_l1(); tr.raster_bwd(grad2d=False); tr.adam(1); tr.pack(1); tr.apply()
+    # Adam with its staged message, and apply exactly as the benchmark does
+    tr.loss_l1(); tr.raster_bwd(grad2d=False); tr.adam_publish(1, 1); tr.apply()
     torch.cuda.synchronize()
     assert to_u32(tr.status)[0] == 0
     # primitives that no ambiguous pixel examined take exactly the oracle's chain gradient
     ok_rows = (ref.flag[vis] == 0) & (ref.proj.clamp_margin[vis] > 1e-5) & (ref.proj.jclamp_margin[vis] > 1e-5)
 
-    # Adam step and the published message
+    # the published message: header and ids bit-exact, rows = the Adam steps
+    msg = tr.msg.cpu().numpy().view(np.uint32)
+    head = 8 + 8 + V
+    np.testing.assert_array_equal(msg[:head], ref.msg[:head])
+    r0 = (head + 3) // 4 * 4
+    rows_gpu = msg[r0:r0 + V * tr.row_len].view(np.float32).reshape(V, tr.row_len)
+    offs = np.cumsum([0] + tr.cols)
     lr = w.lr
     for gi, (p, d_orc, g_orc, p0) in enumerate(zip(tr.params, ref.deltas, ref.grads.groups(),
                                                    [a for _, a in w.scene.groups()])):
-        d_gpu = tr.delta[gi].cpu().numpy()[rows].astype(np.float64)
+        d_gpu = rows_gpu[:, offs[gi]:offs[gi + 1]].astype(np.float64)
         sure = ok_rows[:, None] & (np.abs(g_orc) > grad_floor(g_orc))
         err = np.abs(d_gpu - d_orc)
         assert np.all(err[sure] <= GRAD_RTOL * lr), (gi, err[sure].max())
         assert np.all(err <= 2 * lr * (1 + GRAD_RTOL)), (gi, err.max())
         pn = p.cpu().numpy()[rows].astype(np.float64)
         np.testing.assert_allclose(pn, p0[rows].astype(np.float64) + d_gpu, rtol=0, atol=1e-6 * (1 + np.abs(pn).max()))
-    msg = tr.msg.cpu().numpy().view(np.uint32)
-    head = 8 + 8 + V
-    np.testing.assert_array_equal(msg[:head], ref.msg[:head])
-    r0 = (head + 3) // 4 * 4
-    rows_gpu = msg[r0:r0 + V * tr.row_len].view(np.float32).reshape(V, tr.row_len)
     rows_orc = np.concatenate(ref.deltas, axis=1)
     assert np.all(np.abs(rows_gpu - rows_orc) <= 2 * lr * (1 + GRAD_RTOL))
     # the replica received exactly the published rows (one fp32 add each)

@@ -201,8 +201,13 @@ def bwd_compare(w, tr, orc, ref, vis, dL_masked, case):
     for c, nm in enumerate(names):
         stats[nm] = assert_grads(g2_gpu[:, c], g2[:, c], ok, "grad2d." + nm, mag=gabs[:, c])
     okr = ok[rows]
-    for name, gp, go, mg in zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.grads, gr.groups(), mags):
-        stats[name] = assert_grads(gp.cpu().numpy()[rows], go, okr, "grad." + name, mag=mg)
+    V = vis.size
+    assert int(u32(tr.counts[0:1])[0]) == V
+    for name, gp, go, mg in zip(["mean", "log_scale", "quat", "opacity", "sh"], tr.rows_by_group(tr.grad_rows, V),
+                                gr.groups(), mags):
+        stats[name] = assert_grads(gp, go, okr, "grad." + name, mag=mg)
+    # the padding columns of every gradient row are zero
+    assert float(tr.grad_rows[:V, tr.row_len:].abs().max()) == 0.0 if tr.ld > tr.row_len else True
     gn = tr.grad_norm.cpu().numpy()[rows]
     stats["grad_norm"] = assert_grads(gn, gr.grad_norm, okr, "grad_norm", mag=mag_norm)
     _say(case, {k: (round(v.get("max_rel", 0), 6), round(v.get("norm_rel", 0), 8)) for k, v in stats.items()})
@@ -225,45 +230,144 @@ def test_raster_backward(case, torch_gpu, orc):
     bwd_compare(w, tr, orc, ref, vis, dLm.astype(np.float32).astype(np.float64), case)
 
 
-def test_sparse_adam(torch_gpu, orc):
-    import torch
-    from paper_2607_19893_amd import gsmi, scenes
-    rng = np.random.default_rng(3)
-    n = 5000
+def _adam_case(n=5000, K=1234, seed=3):
+    from paper_2607_19893_amd import scenes
+    rng = np.random.default_rng(seed)
     cols = [3, 3, 4, 1, 48]
     p = [rng.standard_normal((n, c)).astype(np.float32) for c in cols]
     g = [(rng.standard_normal((n, c)) * 1e-3).astype(np.float32) for c in cols]
     mv = [scenes.adam_state(5, n, c) for c in cols]
-    idx = np.sort(rng.choice(n, 1234, replace=False)).astype(np.uint32)
-    dev = torch.device("cuda")
-    P = [torch.from_numpy(a).to(dev) for a in p]
-    G = [torch.from_numpy(a).to(dev) for a in g]
-    M = [torch.from_numpy(a[0]).to(dev) for a in mv]
-    Vv = [torch.from_numpy(a[1]).to(dev) for a in mv]
-    D = [torch.zeros(n, c, device=dev) for c in cols]
+    idx = np.sort(rng.choice(n, K, replace=False)).astype(np.uint32)
     lrs = [1e-3, 2e-3, 1e-3, 5e-2, 2.5e-3]
-    arr = gsmi.make_adam_groups([(a, b, c, d, e, lr) for a, b, c, d, e, lr in zip(P, G, M, Vv, D, lrs)])
-    I = torch.from_numpy(idx.view(np.int32)).to(dev)
-    cnt = torch.tensor([idx.size], dtype=torch.int32, device=dev)
+    return cols, p, g, mv, idx, lrs
+
+
+def _rows_table(groups, ld, rows=None):
+    """Concatenate per-group arrays [*, cols] (optionally gathered at rows) into a [*, ld] table."""
+    parts = [a if rows is None else a[rows] for a in groups]
+    t = np.concatenate(parts, axis=1)
+    out = np.zeros((t.shape[0], ld), np.float32)
+    out[:, :t.shape[1]] = t
+    return out
+
+
+def _split(table, cols):
+    offs = np.cumsum([0] + cols)
+    return [table[:, offs[i]:offs[i + 1]] for i in range(len(cols))]
+
+
+class _AdamGpu:
+    """Device state of one sparse-Adam case: pool groups, compact gradient rows, moment tables."""
+
+    def __init__(self, cols, p, g, mv, idx, lrs, ld=64):
+        import torch
+        from paper_2607_19893_amd import gsmi
+        dev = torch.device("cuda")
+        self.cols, self.ld, self.n = cols, ld, p[0].shape[0]
+        self.P = [torch.from_numpy(a.copy()).to(dev) for a in p]
+        gt = _rows_table(g, ld, idx.astype(np.int64))
+        self.G = torch.from_numpy(gt if gt.shape[0] else np.zeros((1, ld), np.float32)).to(dev)
+        self.M = torch.from_numpy(_rows_table([a[0] for a in mv], ld)).to(dev)
+        self.Vv = torch.from_numpy(_rows_table([a[1] for a in mv], ld)).to(dev)
+        self.D = torch.zeros(max(1, idx.size), ld, device=dev)
+        self.arr = gsmi.make_adam_groups([(a, lr) for a, lr in zip(self.P, lrs)])
+        self.I = torch.from_numpy(idx.view(np.int32).copy() if idx.size else np.zeros(1, np.int32)).to(dev)
+        self.cnt = torch.tensor([idx.size], dtype=torch.int32, device=dev)
+        self.K = idx.size
+
+    def adam(self, step):
+        from paper_2607_19893_amd import gsmi
+        gsmi.gs_sparse_adam(self.arr, 5, self.I, self.cnt, self.n, self.G, self.ld, self.M, self.Vv, self.ld, step,
+                            0.9, 0.999, 1e-15, self.D, self.ld)
+
+    def publish(self, step, version, msg, status):
+        from paper_2607_19893_amd import gsmi
+        gsmi.gs_sparse_adam_publish(self.arr, 5, self.I, self.cnt, self.n, self.G, self.ld, self.M, self.Vv, self.ld,
+                                    step, 0.9, 0.999, 1e-15, version, msg, status)
+
+
+def test_sparse_adam(torch_gpu, orc):
+    import torch
+    cols, p, g, mv, idx, lrs = _adam_case()
+    n = p[0].shape[0]
+    st = _AdamGpu(cols, p, g, mv, idx, lrs)
+    rows = np.zeros(n, bool); rows[idx] = True
     for step in (1, 7):
-        gsmi.gs_sparse_adam(arr, 5, I, cnt, n, step, 0.9, 0.999, 1e-15)
+        st.adam(step)
         torch.cuda.synchronize()
+        m_gpu = _split(st.M.cpu().numpy()[:n], cols)
+        v_gpu = _split(st.Vv.cpu().numpy()[:n], cols)
+        d_gpu = _split(st.D.cpu().numpy()[:idx.size], cols)
+        assert float(st.M[:, sum(cols):].abs().max()) == 0.0     # padding columns untouched
         for k in range(5):
             pr, mr, vr, dr = orc.adam(p[k], g[k], mv[k][0], mv[k][1], idx, step, lrs[k], 0.9, 0.999, 1e-15)
-            rows = np.zeros(n, bool); rows[idx] = True
-            gp = P[k].cpu().numpy()
+            gp = st.P[k].cpu().numpy()
             np.testing.assert_array_equal(gp[~rows], p[k][~rows])        # untouched rows
+            np.testing.assert_array_equal(m_gpu[k][~rows], mv[k][0][~rows])
             # fp32 rounding of b*m + (1-b)*g is relative to the operands' magnitudes
             g64 = g[k].astype(np.float64)
             fm = 0.9 * np.abs(mv[k][0]) + 0.1 * np.abs(g64)
             fv = 0.999 * np.abs(mv[k][1]) + 0.001 * g64 * g64
-            assert_grads(M[k].cpu().numpy(), mr, rows, "m%d" % k, rtol=1e-5, floor=fm)
-            assert_grads(Vv[k].cpu().numpy(), vr, rows, "v%d" % k, rtol=1e-5, floor=fv)
-            assert_grads(D[k].cpu().numpy()[idx], dr, np.ones(idx.size, bool), "delta%d" % k, rtol=2e-5)
+            assert_grads(m_gpu[k], mr, rows, "m%d" % k, rtol=1e-5, floor=fm)
+            assert_grads(v_gpu[k], vr, rows, "v%d" % k, rtol=1e-5, floor=fv)
+            assert_grads(d_gpu[k], dr, np.ones(idx.size, bool), "delta%d" % k, rtol=2e-5)
             assert_grads(gp, pr, rows, "p%d" % k, rtol=1e-6)
             p[k], mv[k] = pr.astype(np.float32), (mr.astype(np.float32), vr.astype(np.float32))
-            P[k].copy_(torch.from_numpy(p[k])); M[k].copy_(torch.from_numpy(mv[k][0]))
-            Vv[k].copy_(torch.from_numpy(mv[k][1]))
+        # continue from the oracle's state
+        for k in range(5):
+            st.P[k].copy_(torch.from_numpy(p[k]))
+        st.M.copy_(torch.from_numpy(_rows_table([a[0] for a in mv], st.ld)))
+        st.Vv.copy_(torch.from_numpy(_rows_table([a[1] for a in mv], st.ld)))
+
+
+@pytest.mark.parametrize("K", [0, 1, 777, 5000])
+def test_sparse_adam_publish(K, torch_gpu, orc):
+    """The fused update + staging: same parameters and moments as gs_sparse_adam bit for bit, a message whose
+    header and ids equal the oracle's and whose rows are the oracle's steps (and gs_sparse_adam's, bit for bit)."""
+    import torch
+    from paper_2607_19893_amd import gsmi
+    cols, p, g, mv, idx, lrs = _adam_case(K=K, seed=11 + K)
+    n = p[0].shape[0]
+    a = _AdamGpu(cols, p, g, mv, idx, lrs)
+    b = _AdamGpu(cols, p, g, mv, idx, lrs)
+    row_len = sum(cols)
+    nbytes = gsmi.gs_delta_msg_bytes(K, row_len, len(cols))
+    msg = torch.full(((nbytes + 15) // 16 * 4,), -1, dtype=torch.int32, device="cuda")
+    status = torch.zeros(4, dtype=torch.int32, device="cuda")
+    a.adam(3)
+    b.publish(3, 42, msg, status)
+    torch.cuda.synchronize()
+    assert int(status[0]) == 0
+    for k in range(5):
+        assert torch.equal(a.P[k], b.P[k])
+    assert torch.equal(a.M, b.M) and torch.equal(a.Vv, b.Vv)
+    words = msg.cpu().numpy().view(np.uint32)[:nbytes // 4]
+    deltas = []
+    for k in range(5):
+        _, _, _, dr = orc.adam(p[k], g[k], mv[k][0], mv[k][1], idx, 3, lrs[k], 0.9, 0.999, 1e-15)
+        full = np.zeros((n, cols[k]))
+        full[idx.astype(np.int64)] = dr
+        deltas.append(full)
+    ref = orc.delta_pack(idx, deltas, 42)
+    head = ref.size - K * row_len
+    np.testing.assert_array_equal(words[:head], ref[:head])
+    rows_gpu = words[head:].view(np.float32).reshape(K, row_len)
+    np.testing.assert_array_equal(rows_gpu, a.D.cpu().numpy()[:K, :row_len])
+    rows_orc = np.concatenate([d[idx.astype(np.int64)] for d in deltas], axis=1) if K else np.zeros((0, row_len))
+    assert_grads(rows_gpu.astype(np.float64), rows_orc, np.ones(K, bool), "msg rows", rtol=2e-5)
+    # too small a buffer: nothing is written, the required size is reported
+    if K > 0:
+        c = _AdamGpu(cols, p, g, mv, idx, lrs)
+        small = torch.zeros(((nbytes - 16) // 4,), dtype=torch.int32, device="cuda")
+        st2 = torch.zeros(4, dtype=torch.int32, device="cuda")
+        c.publish(3, 42, small, st2)
+        torch.cuda.synchronize()
+        s2 = st2.cpu().numpy().view(np.uint32)
+        assert s2[0] & gsmi.GS_DEV_MSG_OVERFLOW and s2[1] == nbytes
+        assert int(small.abs().max()) == 0
+        for k in range(5):
+            np.testing.assert_array_equal(c.P[k].cpu().numpy(), p[k])
+        np.testing.assert_array_equal(c.M.cpu().numpy(), _rows_table([x[0] for x in mv], c.ld))
 
 
 def test_delta_pack_apply(torch_gpu, orc):
@@ -351,13 +455,11 @@ def test_backward_halves_match_combined(torch_gpu, orc):
     tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd(); tr.loss_l1()
     tr.raster_bwd(grad2d=True)
     torch_gpu.cuda.synchronize()
-    ref = [g.clone() for g in tr.grads] + [tr.grad2d.clone(), tr.grad_norm.clone()]
-    for g in tr.grads:
-        g.zero_()
-    tr.grad2d.zero_(); tr.grad_norm.zero_()
+    ref = [tr.grad_rows.clone(), tr.grad2d.clone(), tr.grad_norm.clone()]
+    tr.grad_rows.zero_(); tr.grad2d.zero_(); tr.grad_norm.zero_()
     tr.raster_bwd_pixels()
     tr.raster_bwd_project(grad2d=True)
     torch_gpu.cuda.synchronize()
-    got = list(tr.grads) + [tr.grad2d, tr.grad_norm]
+    got = [tr.grad_rows, tr.grad2d, tr.grad_norm]
     for a, b in zip(got, ref):
         assert torch_gpu.equal(a, b)
