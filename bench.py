@@ -83,7 +83,7 @@ def main():
     log("targets resident (%.1fs)" % (time.time() - t0))
 
     # pair statistics per view (untimed): evaluated / included (pixel, pair) counts
-    ev_pairs, inc_pairs, vis_counts, pair_counts = [], [], [], []
+    ev_pairs, inc_pairs, vis_counts, pair_counts, w_iters, w_hits = [], [], [], [], [], []
     for i, c in enumerate(cams):
         tr.project(c); tr.visible(); tr.bin_sort()
         tr.pair_stats.zero_()
@@ -91,6 +91,7 @@ def main():
         torch.cuda.synchronize()
         st = tr.pair_stats.cpu().numpy()
         ev_pairs.append(int(st[0])); inc_pairs.append(int(st[1]))
+        w_iters.append(int(st[2])); w_hits.append(int(st[3]))
         vis_counts.append(int(to_u32(tr.counts[0:1])[0])); pair_counts.append(int(to_u32(tr.counts[1:2])[0]))
 
     step = 0
@@ -161,7 +162,12 @@ def main():
     roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
                 "frac": round(ach / peak, 5), "traffic": None}
     log("phase rooflines: " + json.dumps(per_phase))
-    log("mean per view: V=%.0f M=%.0f evaluated=%.3g included=%.3g" % (V_mean, M_mean, ev_mean, inc_mean))
+    wi_mean = float(np.mean([w_iters[v] for v in views]))
+    wh_mean = float(np.mean([w_hits[v] for v in views]))
+    log("mean per view: V=%.0f M=%.0f evaluated=%.3g included=%.3g; forward (wave, pair) iterations %.3g, "
+        "with an included pixel %.3g (%.1f%%), included lanes per such iteration %.1f"
+        % (V_mean, M_mean, ev_mean, inc_mean, wi_mean, wh_mean, 100 * wh_mean / max(wi_mean, 1),
+           inc_mean / max(wh_mean, 1)))
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -213,8 +213,10 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
  *   range) of the last included pair, 0 if none
  *   active [n] uint8 or NULL: set to 1 for every primitive included in at least
  *   one pixel (never cleared: zero it before the call)
- *   pair_stats [2] uint64 or NULL: += number of (pixel, pair) evaluations and
- *   of included pairs (accumulated: zero it before the call)
+ *   pair_stats [4] uint64 or NULL (accumulated: zero it before the call):
+ *   += number of (pixel, pair) evaluations, of included pairs, of (wave, pair)
+ *   iterations the kernel executed (a wave is a 16x4 pixel strip of a tile),
+ *   and of those iterations in which at least one pixel included the pair
  *   bg: 3 floats on the HOST
  */
 gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,

@@ -9,8 +9,8 @@
 // Backward: same tile/pixel mapping, walking each tile's pairs back to front.
 // Each pixel recovers the transmittance in front of a pair by dividing by
 // (1 - alpha) and keeps the suffix colour sum; per pair, the 9 partial
-// derivatives are summed across each wave (LDS atomics for a few lanes, DPP
-// row reductions otherwise) and across the 4 waves in a fixed order, then
+// derivatives are summed over each 16-lane pixel row with DPP, over the rows
+// of a wave with LDS atomics, and over the 4 waves in a fixed order, then
 // written to the pair's slot at its sorted position.  Per visible primitive,
 // k_slot_sums adds its slots in emission order (through the sorted position
 // of every emitted pair) -- deterministic, no floating-point atomics in global
@@ -28,19 +28,33 @@ constexpr float kAlphaMax = 0.99f;
 constexpr float kTMin = 1e-4f;
 constexpr float kCutMargin = 1e-3f;   // extra sigma beyond the 1/255 cut-off when bounding a footprint
 
-// One pair's primitive as staged in LDS (48 bytes, all lanes read the same
-// record): (u, v, A/2, B), (C/2, opacity, r, g), (b, hx, hy, -).  hx, hy bound
-// the pixel offsets at which o*exp(-sigma) can reach 1/255: for
+// One pair's primitive as staged in LDS: 64 bytes in four 16-byte arrays,
+// every lane of a wave reading the same record (a broadcast):
+//   P (u, v) and Q (A/2, B) in fp64, R = (C/2 in fp64, opacity, hx),
+//   S = (r, g, b, hy).
+// The pixel-space mean and conic are fp32 values held exactly in fp64, so
+// that the quadratic form is evaluated in fp64 without per-pair conversions.
+// hx, hy bound the pixel offsets at which o*exp(-sigma) can reach 1/255: for
 // sigma = d^T Q d / 2 <= s the offsets obey |dx| <= sqrt(2 s C / det Q) and
 // |dy| <= sqrt(2 s A / det Q); s = ln(255 o) + kCutMargin keeps every skipped
 // pair at least 0.1% below the threshold, far outside fp32 rounding.
-struct Splat {
-    float4 a, b, c;
+struct __align__(16) SplatR {
+    double c2;
+    float o;
+    float hx;
 };
 
-__device__ __forceinline__ Splat make_splat(float2 m, float4 co, const float* __restrict__ rgb3) {
-    Splat s;
-    s.a = make_float4(m.x, m.y, 0.5f * co.x, co.y);
+template <int NB>
+struct SplatLds {
+    double2 P[NB];
+    double2 Q[NB];
+    SplatR R[NB];
+    float4 S[NB];
+};
+
+template <int NB>
+__device__ __forceinline__ void stage_splat(SplatLds<NB>& L, int k, float2 m, float4 co,
+                                            const float* __restrict__ rgb3) {
     const float cut = logf(255.0f * co.w) + kCutMargin;
     const float det = co.x * co.z - co.y * co.y;
     float hx, hy;
@@ -52,32 +66,60 @@ __device__ __forceinline__ Splat make_splat(float2 m, float4 co, const float* __
         hx = sqrtf(2.0f * cut * co.z / det);
         hy = sqrtf(2.0f * cut * co.x / det);
     }
-    s.b = make_float4(0.5f * co.z, co.w, rgb3[0], rgb3[1]);
-    s.c = make_float4(rgb3[2], hx, hy, 0.0f);
-    return s;
+    L.P[k] = make_double2((double)m.x, (double)m.y);
+    L.Q[k] = make_double2(0.5 * (double)co.x, (double)co.y);
+    SplatR r;
+    r.c2 = 0.5 * (double)co.z;
+    r.o = co.w;
+    r.hx = hx;
+    L.R[k] = r;
+    L.S[k] = make_float4(rgb3[0], rgb3[1], rgb3[2], hy);
 }
 
 // Can any pixel centre of the wave's strip [x0,x1] x [y0,y1] reach the cut-off?
-__device__ __forceinline__ bool splat_touches(float4 a, float4 c, float x0, float x1, float y0, float y1) {
-    return (a.x + c.y >= x0) && (a.x - c.y <= x1) && (a.y + c.z >= y0) && (a.y - c.z <= y1);
+template <int NB>
+__device__ __forceinline__ bool splat_touches(const SplatLds<NB>& L, int k, float x0, float x1, float y0, float y1) {
+    const double2 p = L.P[k];
+    const float u = (float)p.x, v = (float)p.y;        // exact: staged from fp32
+    const float hx = L.R[k].hx, hy = L.S[k].w;
+    return (u + hx >= x0) && (u - hx <= x1) && (v + hy >= y0) && (v - hy <= y1);
 }
 
-// sigma of one (pixel, primitive) pair.  The quadratic form is evaluated in
-// fp64: for elongated footprints far from their centre its three terms are
-// large and cancel, and fp32 loses up to ~1e-3 of sigma there (the error grows
-// with the conic's condition number).  Forward and backward both call this on
-// the same staged record, built without contraction, so they take identical
-// decisions.  px, py are the pixel centre in fp64.
+// sigma of one (pixel, primitive) pair, in fp64: for elongated footprints far
+// from their centre the three terms of the quadratic form are large and
+// cancel, and fp32 loses up to ~1e-3 of sigma there (the error grows with the
+// conic's condition number).  The offsets are exact in fp64.  Forward and
+// backward both call this on the same staged record, so they take identical
+// decisions.  bdy = B dy and cdy = (C/2) dy are returned for the backward's
+// d sigma / d(u, v).  px, py are the pixel centre.
 #pragma clang fp contract(off)
-__device__ __forceinline__ float splat_sigma(float4 a, float4 b, double px, double py, float& dx, float& dy) {
-    const double ddx = (double)a.x - px;
-    const double ddy = (double)a.y - py;
-    const double s = fma(ddx, fma((double)a.z, ddx, (double)a.w * ddy), ((double)b.x * ddy) * ddy);
-    dx = (float)ddx;
-    dy = (float)ddy;
-    return (float)s;
+__device__ __forceinline__ float splat_sigma(double2 P, double2 Q, double c2, double px, double py, double& ddx,
+                                             double& ddy, double& inner, double& cdy) {
+    ddx = P.x - px;
+    ddy = P.y - py;
+    inner = fma(Q.x, ddx, Q.y * ddy);            // A/2 dx + B dy
+    cdy = c2 * ddy;                              // C/2 dy
+    return (float)fma(ddx, inner, cdy * ddy);
 }
 #pragma clang fp contract(on)
+
+// exp(-sigma) with range reduction: 2^-t, t = sigma log2(e) carried as hi + lo
+// (log2(e) split into an fp32 head and tail), t = n + f with n an integer and
+// |f| <= 1/2 + tiny, so the hardware base-2 exponential only sees f and the
+// power 2^-n is exact.  sigma is clamped to [0, 100] first (e^-100 is far
+// below any 1/255 threshold), so no overflow or NaN case arises.  Relative
+// error about one ulp of the hardware exponential.
+__device__ __forceinline__ float exp_neg(float sigma) {
+    constexpr float kLog2eHi = 1.44269502162933349609375f;    // log2(e) rounded to fp32
+    constexpr float kLog2eLo = 1.925963033500011e-08f;        // log2(e) - kLog2eHi
+    const float x = fminf(fmaxf(sigma, 0.0f), 100.0f);
+    const float hi = x * kLog2eHi;
+    float lo = fmaf(x, kLog2eHi, -hi);
+    lo = fmaf(x, kLog2eLo, lo);
+    const float n = __builtin_rintf(hi);
+    const float f = (hi - n) + lo;
+    return __builtin_ldexpf(__builtin_amdgcn_exp2f(-f), -(int)n);
+}
 
 __device__ __forceinline__ bool wave_any(bool p) { return __ballot(p) != 0ull; }
 __device__ __forceinline__ bool uniform(bool p) { return __builtin_amdgcn_readfirstlane((int)p) != 0; }
@@ -86,16 +128,16 @@ __device__ __forceinline__ bool uniform(bool p) { return __builtin_amdgcn_readfi
 // reach its 16x4 strip into a wave-private LDS list (ascending, via ballots),
 // then walks only that list.  Only the wave itself reads its list, so a
 // wave-level barrier orders the writes before the reads.
-__device__ __forceinline__ uint32_t compact_touching(const float4* s_a, const float4* s_c, int nb, float x0,
-                                                     float x1, float y0, float y1, uint32_t limit,
-                                                     uint8_t* list) {
+template <int NB>
+__device__ __forceinline__ uint32_t compact_touching(const SplatLds<NB>& L, int nb, float x0, float x1, float y0,
+                                                     float y1, uint32_t limit, uint8_t* list) {
     const int lane = lane_id();
     const uint64_t lt = lanemask_lt();
     uint32_t cnt = 0;
 #pragma unroll
-    for (int r = 0; r < GS_BLOCK / GS_WAVE; ++r) {
+    for (int r = 0; r < NB / GS_WAVE; ++r) {
         const int k = r * GS_WAVE + lane;
-        const bool t = k < nb && (uint32_t)k < limit && splat_touches(s_a[k], s_c[k], x0, x1, y0, y1);
+        const bool t = k < nb && (uint32_t)k < limit && splat_touches(L, k, x0, x1, y0, y1);
         const uint64_t m = __ballot(t);
         if (t) list[cnt + popc64(m & lt)] = (uint8_t)k;
         cnt += popc64(m);
@@ -112,11 +154,11 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, float* __restrict__ img, float* __restrict__ final_T, uint32_t* __restrict__ n_contrib,
     uint8_t* __restrict__ active, unsigned long long* __restrict__ pair_stats) {
-    __shared__ float4 s_a[GS_BLOCK], s_b[GS_BLOCK], s_c[GS_BLOCK];
+    __shared__ SplatLds<GS_BLOCK> L;
     __shared__ uint32_t s_id[GS_BLOCK];
     __shared__ uint32_t s_hit[GS_BLOCK];
     __shared__ uint8_t s_list[4][GS_BLOCK];
-    __shared__ uint32_t s_stat[2][4];
+    __shared__ uint32_t s_stat[4][4];
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
     const int w = tid / GS_WAVE;
@@ -130,31 +172,27 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const float wy0 = ty * GS_TILE + 4 * w + 0.5f, wy1 = wy0 + 3.0f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
     float T = 1.0f, c0 = 0.0f, c1 = 0.0f, c2 = 0.0f;
-    uint32_t last = 0, n_inc = 0, term_at = 0;
+    uint32_t last = 0, n_inc = 0, term_at = 0, w_iter = 0, w_hit = 0;
     bool done = !inside, terminated = false;
     for (uint32_t bs = start; bs < end; bs += GS_BLOCK) {
         if (__syncthreads_count(done) == GS_BLOCK) break;
         const uint32_t j = bs + tid;
         if (j < end) {
             const uint32_t g = vals[j];
-            const Splat sp = make_splat(mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
+            stage_splat(L, tid, mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
             s_id[tid] = g;
-            s_a[tid] = sp.a;
-            s_b[tid] = sp.b;
-            s_c[tid] = sp.c;
         }
         s_hit[tid] = 0;
         __syncthreads();
         const int nb = (int)min((uint32_t)GS_BLOCK, end - bs);
-        const uint32_t cnt = wave_any(!done) ? compact_touching(s_a, s_c, nb, wx0, wx1, wy0, wy1, GS_BLOCK, s_list[w])
-                                              : 0u;
+        const uint32_t cnt = wave_any(!done) ? compact_touching(L, nb, wx0, wx1, wy0, wy1, GS_BLOCK, s_list[w]) : 0u;
         for (uint32_t i = 0; i < cnt; ++i) {
             if (!wave_any(!done)) break;
             const int k = s_list[w][i];
-            const float4 a = s_a[k], b = s_b[k], c = s_c[k];
-            float dx, dy;
-            const float sigma = splat_sigma(a, b, fx, fy, dx, dy);
-            const float alpha = fminf(kAlphaMax, b.y * expf(-sigma));
+            const SplatR R = L.R[k];
+            double ddx, ddy, inner, cdy;
+            const float sigma = splat_sigma(L.P[k], L.Q[k], R.c2, fx, fy, ddx, ddy, inner, cdy);
+            const float alpha = fminf(kAlphaMax, R.o * exp_neg(sigma));
             bool ok = !done && !(sigma < 0.0f) && !(alpha < kAlphaMin);
             const float Tn = T * (1.0f - alpha);
             const bool term = ok && (Tn < kTMin);
@@ -163,13 +201,18 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
             terminated = terminated || term;
             done = done || term;
             ok = ok && !term;
+            const float4 col = L.S[k];
             const float wgt = ok ? alpha * T : 0.0f;
-            c0 = fmaf(wgt, b.z, c0);
-            c1 = fmaf(wgt, b.w, c1);
-            c2 = fmaf(wgt, c.x, c2);
+            c0 = fmaf(wgt, col.x, c0);
+            c1 = fmaf(wgt, col.y, c1);
+            c2 = fmaf(wgt, col.z, c2);
             T = ok ? Tn : T;
             last = ok ? pos + 1u : last;
-            if (STATS) n_inc += ok ? 1u : 0u;
+            if (STATS) {
+                n_inc += ok ? 1u : 0u;
+                w_iter += 1u;
+                w_hit += wave_any(ok) ? 1u : 0u;
+            }
             if (active != nullptr && wave_any(ok) && lane_id() == 0) s_hit[k] = 1u;
         }
         __syncthreads();
@@ -183,12 +226,13 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
         if (lane_id() == 0) {
             s_stat[0][w] = e;
             s_stat[1][w] = i;
+            s_stat[2][w] = w_iter;      // wave-uniform counts
+            s_stat[3][w] = w_hit;
         }
         __syncthreads();
-        if (tid == 0) {
-            atomicAdd(&pair_stats[0], (unsigned long long)s_stat[0][0] + s_stat[0][1] + s_stat[0][2] + s_stat[0][3]);
-            atomicAdd(&pair_stats[1], (unsigned long long)s_stat[1][0] + s_stat[1][1] + s_stat[1][2] + s_stat[1][3]);
-        }
+        if (tid < 4)
+            atomicAdd(&pair_stats[tid], (unsigned long long)s_stat[tid][0] + s_stat[tid][1] + s_stat[tid][2] +
+                                            s_stat[tid][3]);
     }
     if (inside) {
         const size_t HW = (size_t)W * H, p = (size_t)py * W + px;
@@ -244,18 +288,26 @@ __global__ void __launch_bounds__(GS_BLOCK) k_loss_final(const float* __restrict
 // ---------------------------------------------------------------------------
 
 constexpr int kG = 9;   // du dv dA dB dC dopacity dr dg db
-constexpr int kAtomicLanes = 4;    // up to this many contributing lanes: LDS atomics, else row sums first
 constexpr int kSlot = 12;          // floats per pair slot (9 used, padded for 16-byte stores)
+// Pairs staged per batch.  The per-wave accumulators (4 x 9 floats per staged
+// pair) dominate the workgroup's LDS; 128 keeps it near 27 KB so that the
+// registers, not LDS, bound the workgroups per CU.
+constexpr int kBwdBatch = 128;
 
+// Per pixel, walking back to front: T is recovered in front of each included
+// pair as T / (1 - alpha), and instead of the three suffix colour sums S_c
+// (the colour still to come behind the pair, background included) the pixel
+// keeps their projection gS = sum_c dL/dC_c S_c on its upstream gradient,
+// which is all that d alpha needs:
+//   dL/dalpha = T_k (g . rgb) - gS / (1 - alpha),  gS += alpha T_k (g . rgb).
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, const float* __restrict__ final_T, const uint32_t* __restrict__ n_contrib,
     const float* __restrict__ dL_dimg, float* __restrict__ slots) {
-    __shared__ float4 s_a[GS_BLOCK], s_b[GS_BLOCK], s_c[GS_BLOCK];
-    __shared__ uint32_t s_id[GS_BLOCK];
-    __shared__ float s_acc[4][kG][GS_BLOCK];
-    __shared__ uint8_t s_list[4][GS_BLOCK];
+    __shared__ SplatLds<kBwdBatch> L;
+    __shared__ float s_acc[4][kG][kBwdBatch];
+    __shared__ uint8_t s_list[4][kBwdBatch];
     __shared__ uint32_t s_max;
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
@@ -274,7 +326,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const float gC0 = inside ? dL_dimg[pix] : 0.0f;
     const float gC1 = inside ? dL_dimg[HW + pix] : 0.0f;
     const float gC2 = inside ? dL_dimg[2 * HW + pix] : 0.0f;
-    float S0 = T * bg0, S1 = T * bg1, S2 = T * bg2;
+    float gS = T * (gC0 * bg0 + gC1 * bg1 + gC2 * bg2);
     if (tid == 0) s_max = 0;
     __syncthreads();
     if (last > 0) atomicMax(&s_max, last);
@@ -284,20 +336,15 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) wave_last = max(wave_last, (uint32_t)__shfl_xor((int)wave_last, d, GS_WAVE));
     const uint32_t n = end - start;
-    for (int64_t be = n; be > 0; be -= GS_BLOCK) {
-        const uint32_t bs = (uint32_t)(be > GS_BLOCK ? be - GS_BLOCK : 0);
+    for (int64_t be = n; be > 0; be -= kBwdBatch) {
+        const uint32_t bs = (uint32_t)(be > kBwdBatch ? be - kBwdBatch : 0);
         const uint32_t cnt = (uint32_t)be - bs;
         const bool work = bs < maxlast;
-        if ((uint32_t)tid < cnt) {
+        if ((uint32_t)tid < cnt && work) {
             const uint32_t g = vals[start + bs + tid];
-            if (work) {
-                const Splat sp = make_splat(mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
-                s_a[tid] = sp.a;
-                s_b[tid] = sp.b;
-                s_c[tid] = sp.c;
-            }
+            stage_splat(L, tid, mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
         }
-        if (work) {
+        if (work && tid < kBwdBatch) {
 #pragma unroll
             for (int ww = 0; ww < 4; ++ww)
 #pragma unroll
@@ -306,58 +353,58 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
         __syncthreads();
         if (work) {
             const uint32_t limit = wave_last > bs ? wave_last - bs : 0u;
-            const uint32_t nl = limit ? compact_touching(s_a, s_c, (int)cnt, wx0, wx1, wy0, wy1, limit, s_list[w]) : 0u;
+            const uint32_t nl = limit ? compact_touching(L, (int)cnt, wx0, wx1, wy0, wy1, limit, s_list[w]) : 0u;
             for (int i = (int)nl - 1; i >= 0; --i) {
                 const int k = s_list[w][i];
-                const float4 a = s_a[k], b = s_b[k], c = s_c[k];
-                const bool in_range = bs + (uint32_t)k < last;
-                float dx, dy;
-                const float sigma = splat_sigma(a, b, fx, fy, dx, dy);
-                const float e = expf(-sigma);
-                const float gv = b.y * e;
+                const SplatR R = L.R[k];
+                const double2 Q = L.Q[k];
+                double ddx, ddy, inner, cdy;
+                const float sigma = splat_sigma(L.P[k], Q, R.c2, fx, fy, ddx, ddy, inner, cdy);
+                const float e = exp_neg(sigma);
+                const float gv = R.o * e;
                 const float alpha = fminf(kAlphaMax, gv);
-                const bool ok = in_range && !(sigma < 0.0f) && !(alpha < kAlphaMin);
+                const bool ok = bs + (uint32_t)k < last && !(sigma < 0.0f) && !(alpha < kAlphaMin);
                 const uint64_t mask = __ballot(ok);
                 if (mask == 0ull) continue;
+                const float4 col = L.S[k];
                 const float inv_om = __builtin_amdgcn_rcpf(1.0f - alpha);
                 const float Tk = ok ? T * inv_om : T;
-                const float wgt = alpha * Tk;
-                const float dalpha = gC0 * (Tk * b.z - S0 * inv_om) + gC1 * (Tk * b.w - S1 * inv_om) +
-                                     gC2 * (Tk * c.x - S2 * inv_om);
-                if (ok) {
-                    S0 = fmaf(wgt, b.z, S0);
-                    S1 = fmaf(wgt, b.w, S1);
-                    S2 = fmaf(wgt, c.x, S2);
-                    T = Tk;
-                }
+                const float gcol = gC0 * col.x + gC1 * col.y + gC2 * col.z;
+                const float dalpha = Tk * gcol - gS * inv_om;
+                const float wgt = ok ? alpha * Tk : 0.0f;
+                gS = fmaf(wgt, gcol, gS);
+                T = Tk;
                 const bool geo = ok && gv < kAlphaMax;      // the 0.99 cap stops d/d(opacity, sigma)
                 const float ds = geo ? -dalpha * alpha : 0.0f;
+                // d sigma / d(u, v) = (A dx + B dy, B dx + C dy), from sigma's own terms
+                const float dsdu = (float)fma(Q.x, ddx, inner);
+                const float dsdv = (float)fma(Q.y, ddx, cdy + cdy);
+                const float dx = (float)ddx, dy = (float)ddy;
+                const float hds = 0.5f * ds;
+                const float hdx = hds * dx;
                 float gr[kG];
-                gr[0] = ds * (2.0f * a.z * dx + a.w * dy);
-                gr[1] = ds * (a.w * dx + 2.0f * b.x * dy);
-                gr[2] = ds * 0.5f * dx * dx;
-                gr[3] = ds * dx * dy;
-                gr[4] = ds * 0.5f * dy * dy;
+                gr[0] = ds * dsdu;
+                gr[1] = ds * dsdv;
+                gr[2] = hdx * dx;
+                gr[3] = (ds * dx) * dy;
+                gr[4] = (hds * dy) * dy;
                 gr[5] = geo ? dalpha * e : 0.0f;
-                gr[6] = ok ? gC0 * wgt : 0.0f;
-                gr[7] = ok ? gC1 * wgt : 0.0f;
-                gr[8] = ok ? gC2 * wgt : 0.0f;
-                if (popc64(mask) <= kAtomicLanes) {
-                    // few contributing lanes: add them straight into the wave's accumulator
-                    if (ok) {
+                gr[6] = gC0 * wgt;
+                gr[7] = gC1 * wgt;
+                gr[8] = gC2 * wgt;
+                // sum each 16-lane row (one pixel row of the strip) with DPP, then
+                // one lane per contributing row adds the row sum to the wave's accumulator
 #pragma unroll
-                        for (int q = 0; q < kG; ++q) atomicAdd(&s_acc[w][q][k], gr[q]);
-                    }
-                } else {
-                    // sum each 16-lane row (one pixel row of the strip) with DPP, then
-                    // one lane per contributing row adds the row sum
+                for (int q = 0; q < kG; ++q) {
+                    gr[q] = dpp_row_sum(gr[q]);
+                    // keep the last add in front of the branch (all lanes active), where
+                    // it folds into the DPP instruction
+                    asm volatile("" : "+v"(gr[q]));
+                }
+                const int lane = lane_id();
+                if ((lane & 15) == 0 && ((mask >> lane) & 0xFFFFull) != 0ull) {
 #pragma unroll
-                    for (int q = 0; q < kG; ++q) gr[q] = dpp_row_sum(gr[q]);
-                    const int lane = lane_id();
-                    if ((lane & 15) == 0 && ((mask >> lane) & 0xFFFFull) != 0ull) {
-#pragma unroll
-                        for (int q = 0; q < kG; ++q) atomicAdd(&s_acc[w][q][k], gr[q]);
-                    }
+                    for (int q = 0; q < kG; ++q) atomicAdd(&s_acc[w][q][k], gr[q]);
                 }
             }
         }

@@ -66,7 +66,7 @@ class ViewTrainer:
         self.grad2d = torch.zeros(max(1, n), 9, device=self.dev)
         self.grad_norm = torch.zeros(max(1, n), device=self.dev)
         self.loss = torch.zeros(1, device=self.dev)
-        self.pair_stats = torch.zeros(2, dtype=torch.int64, device=self.dev)
+        self.pair_stats = torch.zeros(4, dtype=torch.int64, device=self.dev)
         self.with_keys = with_keys
         self.ws_vis = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_VISIBLE_SET, n), dtype=torch.uint8,
                                   device=self.dev)
