@@ -214,9 +214,10 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
  *   active [n] uint8 or NULL: set to 1 for every primitive included in at least
  *   one pixel (never cleared: zero it before the call)
  *   pair_stats [4] uint64 or NULL (accumulated: zero it before the call):
- *   += number of (pixel, pair) evaluations, of included pairs, of (wave, pair)
- *   iterations the kernel executed (a wave is a 16x4 pixel strip of a tile),
- *   and of those iterations in which at least one pixel included the pair
+ *   += number of (pixel, pair) evaluations, of included pairs, of (row, pair)
+ *   steps the kernel executed (a row is 16 pixels of a tile row, the unit the
+ *   kernel walks pairs in), and of those steps in which at least one pixel
+ *   included the pair
  *   bg: 3 floats on the HOST
  */
 gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,

@@ -148,6 +148,46 @@ __device__ __forceinline__ uint32_t compact_touching(const SplatLds<NB>& L, int 
     return cnt;
 }
 
+// Row-wise lists: each 16-lane row of a wave (one pixel row of the tile)
+// keeps its own ascending list of the batch entries whose footprint box
+// reaches that row's pixel centres (and lie below the row's limit).  The four
+// rows of a wave then walk their lists in lockstep, so an entry costs a
+// quarter of a wave step for every pixel row it reaches instead of a whole
+// step for every 16x4 strip.  cnt[r] receives the length of row r's list.
+template <int NB>
+__device__ __forceinline__ void compact_rows(const SplatLds<NB>& L, int nb, float x0, float x1, float y0,
+                                             const uint32_t* lim, uint8_t (*list)[NB], uint32_t* cnt) {
+    const int lane = lane_id();
+    const uint64_t lt = lanemask_lt();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) cnt[q] = 0;
+#pragma unroll
+    for (int r = 0; r < NB / GS_WAVE; ++r) {
+        const int k = r * GS_WAVE + lane;
+        const bool valid = k < nb;
+        const double2 p = L.P[valid ? k : 0];
+        const float u = (float)p.x, v = (float)p.y;
+        const float hx = L.R[valid ? k : 0].hx, hy = L.S[valid ? k : 0].w;
+        const bool bx = valid && (u + hx >= x0) && (u - hx <= x1);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float y = y0 + (float)q;
+            const bool t = bx && (uint32_t)k < lim[q] && (v + hy >= y) && (v - hy <= y);
+            const uint64_t m = __ballot(t);
+            if (t) list[q][cnt[q] + popc64(m & lt)] = (uint8_t)k;
+            cnt[q] += popc64(m);
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The value of a wave-uniform per-row quantity for this lane's row.
+__device__ __forceinline__ uint32_t for_row(const uint32_t* v, int row) {
+    return row == 0 ? v[0] : (row == 1 ? v[1] : (row == 2 ? v[2] : v[3]));
+}
+
 template <bool STATS>
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
@@ -157,11 +197,13 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     __shared__ SplatLds<GS_BLOCK> L;
     __shared__ uint32_t s_id[GS_BLOCK];
     __shared__ uint32_t s_hit[GS_BLOCK];
-    __shared__ uint8_t s_list[4][GS_BLOCK];
+    __shared__ uint8_t s_list[4][4][GS_BLOCK];
     __shared__ uint32_t s_stat[4][4];
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
     const int w = tid / GS_WAVE;
+    const int lane = lane_id();
+    const int row = lane >> 4;
     const int tx = tile % TX, ty = tile / TX;
     const int px = tx * GS_TILE + (tid % GS_TILE);
     const int py = ty * GS_TILE + (tid / GS_TILE);
@@ -169,7 +211,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const double fx = px + 0.5, fy = py + 0.5;
     // pixel-centre bounds of this wave's 16x4 strip
     const float wx0 = tx * GS_TILE + 0.5f, wx1 = wx0 + 15.0f;
-    const float wy0 = ty * GS_TILE + 4 * w + 0.5f, wy1 = wy0 + 3.0f;
+    const float wy0 = ty * GS_TILE + 4 * w + 0.5f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
     float T = 1.0f, c0 = 0.0f, c1 = 0.0f, c2 = 0.0f;
     uint32_t last = 0, n_inc = 0, term_at = 0, w_iter = 0, w_hit = 0;
@@ -185,15 +227,23 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
         s_hit[tid] = 0;
         __syncthreads();
         const int nb = (int)min((uint32_t)GS_BLOCK, end - bs);
-        const uint32_t cnt = wave_any(!done) ? compact_touching(L, nb, wx0, wx1, wy0, wy1, GS_BLOCK, s_list[w]) : 0u;
-        for (uint32_t i = 0; i < cnt; ++i) {
+        // rows whose 16 pixels are all finished take no entries
+        const uint64_t live = __ballot(!done);
+        uint32_t lim[4], nl[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) lim[q] = ((live >> (16 * q)) & 0xFFFFull) ? (uint32_t)GS_BLOCK : 0u;
+        if (live) compact_rows(L, nb, wx0, wx1, wy0, lim, s_list[w], nl);
+        const uint32_t my_n = for_row(nl, row);
+        const uint32_t steps = max(max(nl[0], nl[1]), max(nl[2], nl[3]));
+        for (uint32_t jj = 0; jj < steps; ++jj) {
             if (!wave_any(!done)) break;
-            const int k = s_list[w][i];
+            const bool act = jj < my_n;
+            const int k = act ? s_list[w][row][jj] : 0;
             const SplatR R = L.R[k];
             double ddx, ddy, inner, cdy;
             const float sigma = splat_sigma(L.P[k], L.Q[k], R.c2, fx, fy, ddx, ddy, inner, cdy);
             const float alpha = fminf(kAlphaMax, R.o * exp_neg(sigma));
-            bool ok = !done && !(sigma < 0.0f) && !(alpha < kAlphaMin);
+            bool ok = act && !done && !(sigma < 0.0f) && !(alpha < kAlphaMin);
             const float Tn = T * (1.0f - alpha);
             const bool term = ok && (Tn < kTMin);
             const uint32_t pos = bs - start + (uint32_t)k;
@@ -210,10 +260,14 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
             last = ok ? pos + 1u : last;
             if (STATS) {
                 n_inc += ok ? 1u : 0u;
-                w_iter += 1u;
-                w_hit += wave_any(ok) ? 1u : 0u;
+                const uint64_t am = __ballot(act), om = __ballot(ok);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    w_iter += ((am >> (16 * q)) & 0xFFFFull) ? 1u : 0u;
+                    w_hit += ((om >> (16 * q)) & 0xFFFFull) ? 1u : 0u;
+                }
             }
-            if (active != nullptr && wave_any(ok) && lane_id() == 0) s_hit[k] = 1u;
+            if (active != nullptr && ok) s_hit[k] = 1u;
         }
         __syncthreads();
         if (active && j < end && s_hit[tid]) active[s_id[tid]] = 1;
@@ -300,6 +354,8 @@ constexpr int kBwdBatch = 128;
 // keeps their projection gS = sum_c dL/dC_c S_c on its upstream gradient,
 // which is all that d alpha needs:
 //   dL/dalpha = T_k (g . rgb) - gS / (1 - alpha),  gS += alpha T_k (g . rgb).
+// Each 16-lane pixel row walks its own list of the batch (compact_rows),
+// back to front, only up to the last pair any of its pixels included.
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
@@ -307,18 +363,20 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const float* __restrict__ dL_dimg, float* __restrict__ slots) {
     __shared__ SplatLds<kBwdBatch> L;
     __shared__ float s_acc[4][kG][kBwdBatch];
-    __shared__ uint8_t s_list[4][kBwdBatch];
+    __shared__ uint8_t s_list[4][4][kBwdBatch];
     __shared__ uint32_t s_max;
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
     const int w = tid / GS_WAVE;
+    const int lane = lane_id();
+    const int row = lane >> 4;
     const int tx = tile % TX, ty = tile / TX;
     const int px = tx * GS_TILE + (tid % GS_TILE);
     const int py = ty * GS_TILE + (tid / GS_TILE);
     const bool inside = px < W && py < H;
     const double fx = px + 0.5, fy = py + 0.5;
     const float wx0 = tx * GS_TILE + 0.5f, wx1 = wx0 + 15.0f;
-    const float wy0 = ty * GS_TILE + 4 * w + 0.5f, wy1 = wy0 + 3.0f;
+    const float wy0 = ty * GS_TILE + 4 * w + 0.5f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
     const size_t HW = (size_t)W * H, pix = (size_t)py * W + px;
     float T = inside ? final_T[pix] : 1.0f;
@@ -332,9 +390,13 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     if (last > 0) atomicMax(&s_max, last);
     __syncthreads();
     const uint32_t maxlast = s_max;
-    uint32_t wave_last = last;     // largest n_contrib among this wave's pixels
+    // largest n_contrib of each pixel row of this wave (wave-uniform values)
+    uint32_t rl = last;
 #pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) wave_last = max(wave_last, (uint32_t)__shfl_xor((int)wave_last, d, GS_WAVE));
+    for (int d = 8; d >= 1; d >>= 1) rl = max(rl, (uint32_t)__shfl_xor((int)rl, d, GS_WAVE));
+    uint32_t row_last[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) row_last[q] = (uint32_t)__builtin_amdgcn_readlane((int)rl, 16 * q);
     const uint32_t n = end - start;
     for (int64_t be = n; be > 0; be -= kBwdBatch) {
         const uint32_t bs = (uint32_t)(be > kBwdBatch ? be - kBwdBatch : 0);
@@ -351,61 +413,67 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
                 for (int q = 0; q < kG; ++q) s_acc[ww][q][tid] = 0.0f;
         }
         __syncthreads();
-        if (work) {
-            const uint32_t limit = wave_last > bs ? wave_last - bs : 0u;
-            const uint32_t nl = limit ? compact_touching(L, (int)cnt, wx0, wx1, wy0, wy1, limit, s_list[w]) : 0u;
-            for (int i = (int)nl - 1; i >= 0; --i) {
-                const int k = s_list[w][i];
-                const SplatR R = L.R[k];
-                const double2 Q = L.Q[k];
-                double ddx, ddy, inner, cdy;
-                const float sigma = splat_sigma(L.P[k], Q, R.c2, fx, fy, ddx, ddy, inner, cdy);
-                const float e = exp_neg(sigma);
-                const float gv = R.o * e;
-                const float alpha = fminf(kAlphaMax, gv);
-                const bool ok = bs + (uint32_t)k < last && !(sigma < 0.0f) && !(alpha < kAlphaMin);
-                const uint64_t mask = __ballot(ok);
-                if (mask == 0ull) continue;
-                const float4 col = L.S[k];
-                const float inv_om = __builtin_amdgcn_rcpf(1.0f - alpha);
-                const float Tk = ok ? T * inv_om : T;
-                const float gcol = gC0 * col.x + gC1 * col.y + gC2 * col.z;
-                const float dalpha = Tk * gcol - gS * inv_om;
-                const float wgt = ok ? alpha * Tk : 0.0f;
-                gS = fmaf(wgt, gcol, gS);
-                T = Tk;
-                const bool geo = ok && gv < kAlphaMax;      // the 0.99 cap stops d/d(opacity, sigma)
-                const float ds = geo ? -dalpha * alpha : 0.0f;
-                // d sigma / d(u, v) = (A dx + B dy, B dx + C dy), from sigma's own terms
-                const float dsdu = (float)fma(Q.x, ddx, inner);
-                const float dsdv = (float)fma(Q.y, ddx, cdy + cdy);
-                const float dx = (float)ddx, dy = (float)ddy;
-                const float hds = 0.5f * ds;
-                const float hdx = hds * dx;
-                float gr[kG];
-                gr[0] = ds * dsdu;
-                gr[1] = ds * dsdv;
-                gr[2] = hdx * dx;
-                gr[3] = (ds * dx) * dy;
-                gr[4] = (hds * dy) * dy;
-                gr[5] = geo ? dalpha * e : 0.0f;
-                gr[6] = gC0 * wgt;
-                gr[7] = gC1 * wgt;
-                gr[8] = gC2 * wgt;
-                // sum each 16-lane row (one pixel row of the strip) with DPP, then
-                // one lane per contributing row adds the row sum to the wave's accumulator
+        uint32_t lim[4], nl[4] = {0u, 0u, 0u, 0u};
+        bool any = false;
 #pragma unroll
-                for (int q = 0; q < kG; ++q) {
-                    gr[q] = dpp_row_sum(gr[q]);
-                    // keep the last add in front of the branch (all lanes active), where
-                    // it folds into the DPP instruction
-                    asm volatile("" : "+v"(gr[q]));
-                }
-                const int lane = lane_id();
-                if ((lane & 15) == 0 && ((mask >> lane) & 0xFFFFull) != 0ull) {
+        for (int q = 0; q < 4; ++q) {
+            lim[q] = row_last[q] > bs ? row_last[q] - bs : 0u;
+            any = any || lim[q] > 0u;
+        }
+        if (work && any) compact_rows(L, (int)cnt, wx0, wx1, wy0, lim, s_list[w], nl);
+        const uint32_t my_n = for_row(nl, row);
+        const uint32_t steps = max(max(nl[0], nl[1]), max(nl[2], nl[3]));
+        for (uint32_t jj = 0; jj < steps; ++jj) {
+            const bool act = jj < my_n;
+            const int k = act ? s_list[w][row][my_n - 1u - jj] : 0;
+            const SplatR R = L.R[k];
+            const double2 Q = L.Q[k];
+            double ddx, ddy, inner, cdy;
+            const float sigma = splat_sigma(L.P[k], Q, R.c2, fx, fy, ddx, ddy, inner, cdy);
+            const float e = exp_neg(sigma);
+            const float gv = R.o * e;
+            const float alpha = fminf(kAlphaMax, gv);
+            const bool ok = act && bs + (uint32_t)k < last && !(sigma < 0.0f) && !(alpha < kAlphaMin);
+            const uint64_t mask = __ballot(ok);
+            if (mask == 0ull) continue;
+            const float4 col = L.S[k];
+            const float inv_om = __builtin_amdgcn_rcpf(1.0f - alpha);
+            const float Tk = ok ? T * inv_om : T;
+            const float gcol = gC0 * col.x + gC1 * col.y + gC2 * col.z;
+            const float dalpha = Tk * gcol - gS * inv_om;
+            const float wgt = ok ? alpha * Tk : 0.0f;
+            gS = fmaf(wgt, gcol, gS);
+            T = Tk;
+            const bool geo = ok && gv < kAlphaMax;      // the 0.99 cap stops d/d(opacity, sigma)
+            const float ds = geo ? -dalpha * alpha : 0.0f;
+            // d sigma / d(u, v) = (A dx + B dy, B dx + C dy), from sigma's own terms
+            const float dsdu = (float)fma(Q.x, ddx, inner);
+            const float dsdv = (float)fma(Q.y, ddx, cdy + cdy);
+            const float dx = (float)ddx, dy = (float)ddy;
+            const float hds = 0.5f * ds;
+            const float hdx = hds * dx;
+            float gr[kG];
+            gr[0] = ds * dsdu;
+            gr[1] = ds * dsdv;
+            gr[2] = hdx * dx;
+            gr[3] = (ds * dx) * dy;
+            gr[4] = (hds * dy) * dy;
+            gr[5] = geo ? dalpha * e : 0.0f;
+            gr[6] = gC0 * wgt;
+            gr[7] = gC1 * wgt;
+            gr[8] = gC2 * wgt;
+            // sum each 16-lane row (all its lanes hold the same entry) with DPP, then
+            // one lane per contributing row adds the row sum to the wave's accumulator
 #pragma unroll
-                    for (int q = 0; q < kG; ++q) atomicAdd(&s_acc[w][q][k], gr[q]);
-                }
+            for (int q = 0; q < kG; ++q) {
+                gr[q] = dpp_row_sum(gr[q]);
+                // keep the last add in front of the branch (all lanes active), where
+                // it folds into the DPP instruction
+                asm volatile("" : "+v"(gr[q]));
+            }
+            if ((lane & 15) == 0 && ((mask >> lane) & 0xFFFFull) != 0ull) {
+#pragma unroll
+                for (int q = 0; q < kG; ++q) atomicAdd(&s_acc[w][q][k], gr[q]);
             }
         }
         __syncthreads();
