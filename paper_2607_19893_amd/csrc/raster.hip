@@ -544,15 +544,11 @@ __device__ __forceinline__ void sh_basis_grad(float x, float y, float z, float* 
 
 __device__ __forceinline__ float dot3(const float* a, const float* b) { return a[0] * b[0] + a[1] * b[1] + a[2] * b[2]; }
 
-// Per-primitive work runs in two kernels.  k_slot_sums (one thread per
+// Per-primitive work runs in two kernels.  k_slot_sums (four lanes per
 // visible row, small register footprint, high occupancy) adds each
 // primitive's pair slots in a fixed order and writes a compact 12-float record
 // per row; k_project_bwd (one thread per visible row) then reads that record
-// and the parameter row and applies the chain rule.  Lists of up to
-// kSerialSlots slots are summed by their own lane with kSlotUnroll slots in
-// flight; longer ones (a primitive spanning many tiles) by the whole wave.
-constexpr uint32_t kSerialSlots = 32;
-constexpr int kSlotUnroll = 4;
+// and the parameter row and applies the chain rule.
 constexpr int kG2 = 12;     // floats per row of the compact 2D-gradient record (9 used)
 
 template <int DEG>
@@ -703,45 +699,56 @@ __device__ __forceinline__ void add_slot(float* g, const float* __restrict__ slo
 }
 
 // Per visible row r: the primitive's 2D gradient, the sum of its pair slots in
-// emission order (none if the pair list overflowed its capacity).
+// emission order (none if the pair list overflowed its capacity).  Four lanes
+// share a row: lane s of the quad adds slots s, s+4, s+8, ... and the quad
+// combines its four partial sums with two DPP steps (a fixed order, so the
+// result is deterministic).  Rows with more than kQuadSlots slots are summed
+// by the whole wave instead.
+constexpr int kRowLanes = 4;
+constexpr uint32_t kQuadSlots = 64;
+
+__device__ __forceinline__ float quad_sum(float v) {
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, true));   // [1,0,3,2]
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, true));   // [2,3,0,1]
+    return v;
+}
+
 __global__ void __launch_bounds__(GS_BLOCK) k_slot_sums(
     const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
     const uint32_t* __restrict__ pair_offset, const uint32_t* __restrict__ pair_perm,
     const float* __restrict__ slots, uint32_t capacity, float* __restrict__ g2c, float* __restrict__ grad2d,
     float* __restrict__ grad_norm) {
+    constexpr uint32_t kRowsPerBlock = GS_BLOCK / kRowLanes;
     const uint32_t V = *vis_count;
-    if (blockIdx.x * GS_BLOCK >= V) return;
-    const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
+    if (blockIdx.x * kRowsPerBlock >= V) return;
+    const uint32_t r = blockIdx.x * kRowsPerBlock + threadIdx.x / kRowLanes;
+    const uint32_t sub = threadIdx.x % kRowLanes;
     const bool valid = r < V;
     const uint32_t id = valid ? vis_idx[r] : 0u;
     const uint32_t first = valid ? pair_offset[id] : 0u;
     const uint32_t nt = valid ? tiles[id] : 0u;
     const bool fits = (uint64_t)first + nt <= capacity;
     float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-    if (fits && nt <= kSerialSlots) {
-        uint32_t k = 0;
-        for (; k + kSlotUnroll <= nt; k += kSlotUnroll) {
-            uint32_t pos[kSlotUnroll];
-#pragma unroll
-            for (int u = 0; u < kSlotUnroll; ++u) pos[u] = min(pair_perm[first + k + u], capacity - 1u);
-            float4 v[kSlotUnroll][3];
-#pragma unroll
-            for (int u = 0; u < kSlotUnroll; ++u) {
-                const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)pos[u] * kSlot);
-                v[u][0] = sl[0];
-                v[u][1] = sl[1];
-                v[u][2] = sl[2];
-            }
-#pragma unroll
-            for (int u = 0; u < kSlotUnroll; ++u) {
-                g2[0] += v[u][0].x; g2[1] += v[u][0].y; g2[2] += v[u][0].z; g2[3] += v[u][0].w;
-                g2[4] += v[u][1].x; g2[5] += v[u][1].y; g2[6] += v[u][1].z; g2[7] += v[u][1].w;
-                g2[8] += v[u][2].x;
-            }
+    if (fits && nt <= kQuadSlots) {
+        uint32_t k = sub;
+        for (; k + kRowLanes < nt; k += 2 * kRowLanes) {
+            const uint32_t p0 = min(pair_perm[first + k], capacity - 1u);
+            const uint32_t p1 = min(pair_perm[first + k + kRowLanes], capacity - 1u);
+            const float4* s0 = reinterpret_cast<const float4*>(slots + (size_t)p0 * kSlot);
+            const float4* s1 = reinterpret_cast<const float4*>(slots + (size_t)p1 * kSlot);
+            const float4 a0 = s0[0], a1 = s0[1], a2 = s0[2];
+            const float4 b0 = s1[0], b1 = s1[1], b2 = s1[2];
+            g2[0] += a0.x; g2[1] += a0.y; g2[2] += a0.z; g2[3] += a0.w;
+            g2[4] += a1.x; g2[5] += a1.y; g2[6] += a1.z; g2[7] += a1.w; g2[8] += a2.x;
+            g2[0] += b0.x; g2[1] += b0.y; g2[2] += b0.z; g2[3] += b0.w;
+            g2[4] += b1.x; g2[5] += b1.y; g2[6] += b1.z; g2[7] += b1.w; g2[8] += b2.x;
         }
-        for (; k < nt; ++k) add_slot(g2, slots, pair_perm[first + k], capacity);
+        if (k < nt) add_slot(g2, slots, pair_perm[first + k], capacity);
     }
-    uint64_t big = __ballot(fits && nt > kSerialSlots);
+#pragma unroll
+    for (int q = 0; q < kG; ++q) g2[q] = quad_sum(g2[q]);
+    // long lists: the whole wave, 64 slots at a time, for one row after another
+    uint64_t big = __ballot(fits && nt > kQuadSlots && sub == 0);
     while (big) {
         const int owner = __ffsll((unsigned long long)big) - 1;
         big &= big - 1;
@@ -752,19 +759,20 @@ __global__ void __launch_bounds__(GS_BLOCK) k_slot_sums(
 #pragma unroll
         for (int q = 0; q < kG; ++q) {
             const float v = wave_sum(acc[q]);
-            if (lane_id() == owner) g2[q] = v;
+            if ((lane_id() & ~(kRowLanes - 1)) == owner) g2[q] = v;
         }
     }
     if (!valid) return;
     float4* dst = reinterpret_cast<float4*>(g2c + (size_t)r * kG2);
-    dst[0] = make_float4(g2[0], g2[1], g2[2], g2[3]);
-    dst[1] = make_float4(g2[4], g2[5], g2[6], g2[7]);
-    dst[2] = make_float4(g2[8], 0.0f, 0.0f, 0.0f);
+    if (sub == 0) dst[0] = make_float4(g2[0], g2[1], g2[2], g2[3]);
+    if (sub == 1) dst[1] = make_float4(g2[4], g2[5], g2[6], g2[7]);
+    if (sub == 2) dst[2] = make_float4(g2[8], 0.0f, 0.0f, 0.0f);
     if (grad2d) {
 #pragma unroll
-        for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
+        for (int q = 0; q < kG; ++q)
+            if ((uint32_t)q % kRowLanes == sub) grad2d[(size_t)id * kG + q] = g2[q];
     }
-    if (grad_norm) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
+    if (grad_norm && sub == 3) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
 }
 
 template <int N>
@@ -927,7 +935,8 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || scene.n == 0 || !(stages & 2)) return e;
     const dim3 grid(div_up(scene.n, GS_BLOCK));
-    hipLaunchKernelGGL(k_slot_sums, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset,
+    hipLaunchKernelGGL(k_slot_sums, dim3(div_up(scene.n, GS_BLOCK / kRowLanes)), dim3(GS_BLOCK), 0, st, vis_idx,
+                       vis_count, proj.tiles, pair_offset,
                        pair_perm, slots, capacity, g2c, grad2d, grad_norm);
 #define GS_LAUNCH_PBWD(D)                                                                                        \
     hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, g2c, proj.clamp,        \
