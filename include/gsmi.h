@@ -190,16 +190,17 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
  *   vals   [capacity] uint32  primitive id of every sorted pair
  *   ranges [T,2] uint32       [start, end) of each tile's pairs, T = tiles in the image
  *   pair_offset [n] uint32    per visible primitive: first of its pairs in
- *                             emission order (rectangle row-major); read by gs_raster_bwd
- *   pair_perm [capacity] uint32  sorted position of every pair, indexed by
- *                             emission order (pair_offset[id] + tile number in the rectangle)
+ *                             emission order (primitives in depth order, each one's
+ *                             rectangle row-major); read by gs_raster_bwd
+ *   pair_emit [capacity] uint32  emission position of every sorted pair
+ *                             (pair_offset[id] + tile number in id's rectangle)
  *   keys   [capacity] uint64 or NULL: (tile << 32) | bits(depth) per sorted pair
  *   num_pairs: one uint32 on the device (the pair count, also on overflow)
  *   ws: gs_workspace_bytes(GS_WS_BIN_SORT, n, capacity, width, height) bytes
  */
 gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                       int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                      uint32_t* pair_offset, uint32_t* pair_perm, uint64_t* keys, uint32_t* num_pairs,
+                      uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys, uint32_t* num_pairs,
                       gs_device_status* status, void* ws, size_t ws_bytes, void* stream);
 
 /*
@@ -250,7 +251,7 @@ gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32
  *   ws: gs_workspace_bytes(GS_WS_RASTER_BWD, n, capacity, W, H); capacity as in gs_bin_sort
  */
 gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
-                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
+                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_emit,
                         const uint32_t* vis_idx,
                         const uint32_t* vis_count, uint32_t capacity, const float* final_T,
                         const uint32_t* n_contrib, const float* dL_dimg, const float* bg, float* grad_rows,
@@ -259,7 +260,8 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
 /*
  * The two halves of gs_raster_bwd, for callers that schedule or time them
  * separately.  gs_raster_bwd_pixels runs the per-pixel replay and leaves one
- * 9-float derivative per (tile, primitive) pair in the workspace;
+ * 9-float derivative per (tile, primitive) pair in the workspace, at the
+ * pair's emission position;
  * gs_raster_bwd_project sums each visible primitive's pairs and applies the
  * chain rule.  The same workspace (gs_workspace_bytes(GS_WS_RASTER_BWD, ...))
  * must be passed to both, on the same stream or with the ordering ensured by
@@ -267,11 +269,12 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
  * second.  Arguments mean what they mean in gs_raster_bwd.
  */
 gs_status gs_raster_bwd_pixels(const gs_proj* proj, const gs_camera* cam, const uint32_t* vals,
-                               const uint32_t* ranges, uint32_t capacity, const float* final_T,
+                               const uint32_t* ranges, const uint32_t* pair_emit, uint32_t capacity,
+                               const float* final_T,
                                const uint32_t* n_contrib, const float* dL_dimg, const float* bg, void* ws,
                                size_t ws_bytes, void* stream);
 gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj,
-                                const uint32_t* pair_offset, const uint32_t* pair_perm, const uint32_t* vis_idx,
+                                const uint32_t* pair_offset, const uint32_t* vis_idx,
                                 const uint32_t* vis_count, uint32_t capacity, float* grad_rows, int32_t grad_ld,
                                 float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream);
 

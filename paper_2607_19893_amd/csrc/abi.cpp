@@ -137,7 +137,7 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
 
 gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                       int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                      uint32_t* pair_offset, uint32_t* pair_perm, uint64_t* keys, uint32_t* num_pairs,
+                      uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys, uint32_t* num_pairs,
                       gs_device_status* status, void* ws, size_t ws_bytes, void* stream) {
     gs_status s;
     if ((s = check_proj(proj, false, "gs_bin_sort")) != GS_OK) return s;
@@ -146,11 +146,11 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
         return fail(GS_ERR_UNSUPPORTED, "gs_bin_sort: image side above %d", GS_MAX_IMAGE_SIDE);
     GS_REQUIRE(vis_idx && vis_count && ranges && pair_offset && num_pairs && status && ws,
                "gs_bin_sort: null pointer");
-    GS_REQUIRE(capacity == 0 || (vals && pair_perm), "gs_bin_sort: null vals / pair_perm");
+    GS_REQUIRE(capacity == 0 || (vals && pair_emit), "gs_bin_sort: null vals / pair_emit");
     if (ws_bytes < gsmi::binsort_ws_bytes(n, capacity, width, height))
         return fail(GS_ERR_WORKSPACE, "gs_bin_sort: workspace too small");
     return hip_status(gsmi::launch_binsort(*proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges,
-                                           pair_offset, pair_perm, keys, num_pairs, status, ws,
+                                           pair_offset, pair_emit, keys, num_pairs, status, ws,
                                            static_cast<hipStream_t>(stream)),
                       "gs_bin_sort");
 }
@@ -181,7 +181,7 @@ gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32
 }
 
 gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
-                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
+                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_emit,
                         const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity, const float* final_T,
                         const uint32_t* n_contrib, const float* dL_dimg, const float* bg, float* grad_rows,
                         int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream) {
@@ -190,39 +190,41 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
     if ((s = check_grad_rows(scene, grad_rows, grad_ld, "gs_raster_bwd")) != GS_OK) return s;
     if ((s = check_camera(cam, "gs_raster_bwd")) != GS_OK) return s;
     if ((s = check_proj(proj, true, "gs_raster_bwd")) != GS_OK) return s;
-    GS_REQUIRE(vals && ranges && pair_offset && pair_perm && vis_idx && vis_count && final_T && n_contrib && dL_dimg &&
+    GS_REQUIRE(vals && ranges && pair_offset && pair_emit && vis_idx && vis_count && final_T && n_contrib && dL_dimg &&
                    bg && ws,
                "gs_raster_bwd: null pointer");
     GS_REQUIRE(aligned(ws, 256), "gs_raster_bwd: workspace must be 256-byte aligned");
     if (ws_bytes < gsmi::raster_bwd_ws_bytes(scene->n, capacity))
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
-    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, vals, ranges, pair_offset, pair_perm, vis_idx,
+    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, vals, ranges, pair_offset, pair_emit, vis_idx,
                                               vis_count, capacity, final_T, n_contrib, dL_dimg, bg, grad_rows,
                                               grad_ld, grad2d, grad_norm, ws, 3, static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd");
 }
 
 gs_status gs_raster_bwd_pixels(const gs_proj* proj, const gs_camera* cam, const uint32_t* vals, const uint32_t* ranges,
-                               uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
-                               const float* dL_dimg, const float* bg, void* ws, size_t ws_bytes, void* stream) {
+                               const uint32_t* pair_emit, uint32_t capacity, const float* final_T,
+                               const uint32_t* n_contrib, const float* dL_dimg, const float* bg, void* ws,
+                               size_t ws_bytes, void* stream) {
     gs_status s;
     if ((s = check_camera(cam, "gs_raster_bwd_pixels")) != GS_OK) return s;
     if ((s = check_proj(proj, false, "gs_raster_bwd_pixels")) != GS_OK) return s;
-    GS_REQUIRE(vals && ranges && final_T && n_contrib && dL_dimg && bg && ws, "gs_raster_bwd_pixels: null pointer");
+    GS_REQUIRE(vals && ranges && pair_emit && final_T && n_contrib && dL_dimg && bg && ws,
+               "gs_raster_bwd_pixels: null pointer");
     GS_REQUIRE(aligned(ws, 256), "gs_raster_bwd_pixels: workspace must be 256-byte aligned");
     if (ws_bytes < gsmi::raster_bwd_ws_bytes(0, capacity))
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_pixels: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
     gs_scene none = {0, 0, nullptr, nullptr, nullptr, nullptr, nullptr};
-    return hip_status(gsmi::launch_raster_bwd(none, c, *proj, vals, ranges, nullptr, nullptr, nullptr, nullptr,
+    return hip_status(gsmi::launch_raster_bwd(none, c, *proj, vals, ranges, nullptr, pair_emit, nullptr, nullptr,
                                               capacity, final_T, n_contrib, dL_dimg, bg, nullptr, 0, nullptr, nullptr,
                                               ws, 1, static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd_pixels");
 }
 
 gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj,
-                                const uint32_t* pair_offset, const uint32_t* pair_perm, const uint32_t* vis_idx,
+                                const uint32_t* pair_offset, const uint32_t* vis_idx,
                                 const uint32_t* vis_count, uint32_t capacity, float* grad_rows, int32_t grad_ld,
                                 float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream) {
     gs_status s;
@@ -230,13 +232,13 @@ gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, con
     if ((s = check_grad_rows(scene, grad_rows, grad_ld, "gs_raster_bwd_project")) != GS_OK) return s;
     if ((s = check_camera(cam, "gs_raster_bwd_project")) != GS_OK) return s;
     if ((s = check_proj(proj, true, "gs_raster_bwd_project")) != GS_OK) return s;
-    GS_REQUIRE(pair_offset && pair_perm && vis_idx && vis_count && ws, "gs_raster_bwd_project: null pointer");
+    GS_REQUIRE(pair_offset && vis_idx && vis_count && ws, "gs_raster_bwd_project: null pointer");
     GS_REQUIRE(aligned(ws, 256), "gs_raster_bwd_project: workspace must be 256-byte aligned");
     if (ws_bytes < gsmi::raster_bwd_ws_bytes(scene->n, capacity))
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_project: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
     const float bg0[3] = {0.0f, 0.0f, 0.0f};
-    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, nullptr, nullptr, pair_offset, pair_perm, vis_idx,
+    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, nullptr, nullptr, pair_offset, nullptr, vis_idx,
                                               vis_count, capacity, nullptr, nullptr, nullptr, bg0, grad_rows, grad_ld,
                                               grad2d, grad_norm, ws, 2, static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd_project");

@@ -14,7 +14,8 @@
 //
 // Each LSD pass is three launches: per-block digit histograms (digit-major
 // matrix), a per-digit scan across blocks, and a scatter whose in-block rank
-// comes from a 64-lane match built from ballots (stable: round, wave, lane).
+// comes from a 64-lane match built from ballots; every wave of a block owns a
+// contiguous quarter of the block's keys, so the order is stable.
 #include "common.h"
 #include "internal.h"
 
@@ -22,15 +23,20 @@ namespace gsmi {
 
 namespace {
 
-constexpr int kRadixBits = 8;
-constexpr int kRadix = 1 << kRadixBits;
+// Digit widths (8 bits: wider digits cost more per pass in these small,
+// latency-bound launches than the pass they save).  Every kernel takes the
+// digit width as a template parameter; a block holds 2^BITS counters in LDS.
+constexpr int kDepthBits = 8;
+constexpr int kTileBits = 8;
 
+template <int BITS>
 __global__ void __launch_bounds__(GS_BLOCK) k_radix_hist(const uint32_t* __restrict__ keys,
                                                          const uint32_t* __restrict__ count_ptr, int shift,
                                                          uint32_t mask, uint32_t* __restrict__ hist,
                                                          uint32_t nblocks) {
-    __shared__ uint32_t h[kRadix];
-    h[threadIdx.x] = 0;
+    constexpr int R = 1 << BITS;
+    __shared__ uint32_t h[R];
+    for (int d = threadIdx.x; d < R; d += GS_BLOCK) h[d] = 0;
     __syncthreads();
     const uint32_t cnt = *count_ptr;
     const uint32_t base = blockIdx.x * GS_TILE_ITEMS;
@@ -42,7 +48,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_radix_hist(const uint32_t* __restr
         }
     }
     __syncthreads();
-    hist[threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
+    for (int d = threadIdx.x; d < R; d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = h[d];
 }
 
 // One workgroup per digit row: exclusive scan across blocks, row total -> totals[d].
@@ -72,59 +78,109 @@ __global__ void __launch_bounds__(GS_BLOCK) k_radix_scan(uint32_t* __restrict__ 
     if (threadIdx.x == 0) totals[blockIdx.x] = carry;
 }
 
+// Lanes of a wave whose digit equals this lane's digit (a 64-lane match built
+// from one ballot per digit bit), restricted to the valid lanes.
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid, int nbits) {
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < nbits; ++b) {
+        const bool bit = (d >> b) & 1u;
+        const uint64_t bb = __ballot(bit);
+        peers &= bit ? bb : ~bb;
+    }
+    return peers;
+}
+
+// Stable scatter of block b's 2048 keys.  Wave w ranks its own 512 keys
+// (contiguous, 64 per round) against a wave-private running count per digit,
+// so the rounds need no block barrier; one barrier then turns the four
+// waves' digit counts into per-wave offsets.  Position of a key = start of
+// its digit over all blocks + its block's offset (from the scanned matrix) +
+// the keys of earlier waves with that digit + its rank inside its wave.
+template <int BITS>
 __global__ void __launch_bounds__(GS_BLOCK) k_radix_scatter(
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, uint32_t* __restrict__ keys_out,
     uint32_t* __restrict__ vals_out, const uint32_t* __restrict__ count_ptr, int shift, uint32_t mask,
     int nbits, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals, uint32_t nblocks) {
-    __shared__ uint32_t s_base[kRadix];
-    __shared__ uint32_t s_run[kRadix];
-    __shared__ uint32_t s_wc[4][kRadix];
+    constexpr int R = 1 << BITS;
+    constexpr int PER = (R + GS_BLOCK - 1) / GS_BLOCK;    // digits per thread in the per-digit steps
+    __shared__ uint32_t s_base[R];
+    __shared__ uint32_t s_wc[4][R];
     __shared__ uint32_t scratch[4];
     const uint32_t cnt = *count_ptr;
-    const uint32_t base = blockIdx.x * GS_TILE_ITEMS;
-    if (base >= cnt) return;
+    if (blockIdx.x * GS_TILE_ITEMS >= cnt) return;
     const int tid = threadIdx.x;
     const int w = tid / GS_WAVE;
-    uint32_t tot;
-    const uint32_t dex = block_excl_scan(totals[tid], scratch, &tot);
-    s_base[tid] = dex + hist[tid * nblocks + blockIdx.x];
-    s_run[tid] = 0;
-    s_wc[0][tid] = 0; s_wc[1][tid] = 0; s_wc[2][tid] = 0; s_wc[3][tid] = 0;
-    uint32_t key[GS_ITEMS], val[GS_ITEMS];
+    const int lane = lane_id();
+    // digit starts: exclusive scan of the digit totals, thread t owning digits [t*PER, t*PER+PER)
+    {
+        uint32_t tv[PER];
+        uint32_t sum = 0;
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int d = tid * PER + q;
+            tv[q] = d < R ? totals[d] : 0u;
+            sum += tv[q];
+        }
+        uint32_t tot;
+        uint32_t run = block_excl_scan(sum, scratch, &tot);
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int d = tid * PER + q;
+            if (d < R) {
+                s_base[d] = run + hist[(size_t)d * nblocks + blockIdx.x];
+                s_wc[0][d] = 0; s_wc[1][d] = 0; s_wc[2][d] = 0; s_wc[3][d] = 0;
+            }
+            run += tv[q];
+        }
+    }
+    const uint32_t base = blockIdx.x * GS_TILE_ITEMS + w * (GS_WAVE * GS_ITEMS);
+    uint32_t key[GS_ITEMS], val[GS_ITEMS], rk[GS_ITEMS];
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t i = base + k * GS_BLOCK + tid;
+        const uint32_t i = base + k * GS_WAVE + lane;
         key[k] = (i < cnt) ? keys_in[i] : 0u;
-        val[k] = (i < cnt) ? vals_in[i] : 0u;
+        val[k] = (i < cnt) ? (vals_in ? vals_in[i] : i) : 0u;    // no input values: the input position
     }
     __syncthreads();
     const uint64_t lt = lanemask_lt();
+    uint32_t* wc = s_wc[w];
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t i = base + k * GS_BLOCK + tid;
+        const uint32_t i = base + k * GS_WAVE + lane;
         const bool valid = i < cnt;
         const uint32_t d = (key[k] >> shift) & mask;
-        uint64_t peers = __ballot(valid);
-        for (int b = 0; b < nbits; ++b) {
-            const bool bit = (d >> b) & 1u;
-            const uint64_t bb = __ballot(bit);
-            peers &= bit ? bb : ~bb;
+        const uint64_t peers = match_digit(d, valid, nbits);
+        const uint32_t before = valid ? wc[d] : 0u;
+        rk[k] = before + (uint32_t)popc64(peers & lt);
+        // all reads of this round precede the leaders' updates
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (valid && (peers & lt) == 0ull) wc[d] = before + (uint32_t)popc64(peers);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    __syncthreads();
+    // per digit: offsets of waves 1..3 folded into s_wc (wave 0 takes 0)
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const int d = tid * PER + q;
+        if (d < R) {
+            const uint32_t c0 = s_wc[0][d], c1 = s_wc[1][d], c2 = s_wc[2][d];
+            s_wc[0][d] = 0;
+            s_wc[1][d] = c0;
+            s_wc[2][d] = c0 + c1;
+            s_wc[3][d] = c0 + c1 + c2;
         }
-        const uint32_t rank = (uint32_t)popc64(peers & lt);
-        if (valid && rank == 0) s_wc[w][d] = (uint32_t)popc64(peers);
-        __syncthreads();
-        uint32_t pos = 0;
-        if (valid) {
-            pos = s_base[d] + s_run[d] + rank;
-            if (w > 0) pos += s_wc[0][d];
-            if (w > 1) pos += s_wc[1][d];
-            if (w > 2) pos += s_wc[2][d];
-        }
-        __syncthreads();
-        s_run[tid] += s_wc[0][tid] + s_wc[1][tid] + s_wc[2][tid] + s_wc[3][tid];
-        s_wc[0][tid] = 0; s_wc[1][tid] = 0; s_wc[2][tid] = 0; s_wc[3][tid] = 0;
-        __syncthreads();
-        if (valid) {
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        const uint32_t i = base + k * GS_WAVE + lane;
+        if (i < cnt) {
+            const uint32_t d = (key[k] >> shift) & mask;
+            const uint32_t pos = s_base[d] + wc[d] + rk[k];
             keys_out[pos] = key[k];
             vals_out[pos] = val[k];
         }
@@ -258,32 +314,31 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
     }
 }
 
-// Tile ranges, optional 64-bit keys, and the emission->sorted permutation
-// (pair_perm[pair_offset[id] + local tile number] = sorted position).
+// Tile ranges, primitive ids and optional 64-bit keys of the sorted pairs.
+// The tile sort carried every pair's emission position as its value, so the
+// primitive id is a gather from the emission-ordered ids.
 __global__ void __launch_bounds__(GS_BLOCK) k_finalize(const uint32_t* __restrict__ skeys,
-                                                       const uint32_t* __restrict__ svals,
+                                                       const uint32_t* __restrict__ pair_emit,
+                                                       const uint32_t* __restrict__ emit_vals,
                                                        const uint32_t* __restrict__ sort_count,
                                                        const float* __restrict__ depth,
-                                                       const ushort4* __restrict__ rect,
-                                                       const uint32_t* __restrict__ pair_offset, int32_t tiles_x,
                                                        uint32_t* __restrict__ ranges, uint64_t* __restrict__ keys64,
-                                                       uint32_t* __restrict__ pair_perm) {
+                                                       uint32_t* __restrict__ vals) {
     const uint32_t M = *sort_count;
     const uint32_t i = blockIdx.x * GS_BLOCK + threadIdx.x;
     if (i >= M) return;
     const uint32_t t = skeys[i];
-    const uint32_t g = svals[i];
+    const uint32_t g = emit_vals[pair_emit[i]];
+    vals[i] = g;
     if (i == 0 || skeys[i - 1] != t) ranges[2 * t] = i;
     if (i == M - 1 || skeys[i + 1] != t) ranges[2 * t + 1] = i + 1;
     if (keys64) keys64[i] = ((uint64_t)t << 32) | (uint64_t)__float_as_uint(depth[g]);
-    const ushort4 rc = rect[g];
-    const uint32_t ty = t / (uint32_t)tiles_x, tx = t - ty * (uint32_t)tiles_x;
-    pair_perm[pair_offset[g] + (ty - rc.y) * (uint32_t)(rc.z - rc.x) + (tx - rc.x)] = i;
 }
 
 struct BinsortLayout {
     size_t dk[3], dv[3];      // depth sort: in, tmp, out
-    size_t pk[3], pv[2];      // pair sort: in, tmp, out (values out = caller's vals)
+    size_t pk[3], pv[3];      // pair sort keys: in, tmp, out; pv[0] = primitive of each emitted pair,
+                              // pv[1..2] = value ping-pong (values out = caller's pair_emit)
     size_t hist, totals, bsum, offs, counters;
     size_t bytes;
     uint32_t nblocks_hist;
@@ -296,10 +351,10 @@ BinsortLayout binsort_layout(int32_t n, uint32_t capacity) {
     for (int i = 0; i < 3; ++i) { L.dk[i] = o; o += align256(4 * nn); }
     for (int i = 0; i < 3; ++i) { L.dv[i] = o; o += align256(4 * nn); }
     for (int i = 0; i < 3; ++i) { L.pk[i] = o; o += align256(4 * cc); }
-    for (int i = 0; i < 2; ++i) { L.pv[i] = o; o += align256(4 * cc); }
+    for (int i = 0; i < 3; ++i) { L.pv[i] = o; o += align256(4 * cc); }
     L.nblocks_hist = div_up(nn > cc ? nn : cc, GS_TILE_ITEMS);
-    L.hist = o; o += align256(4 * (size_t)kRadix * L.nblocks_hist);
-    L.totals = o; o += align256(4 * kRadix);
+    L.hist = o; o += align256(4 * ((size_t)1 << kDepthBits) * L.nblocks_hist);
+    L.totals = o; o += align256(4 * ((size_t)1 << kDepthBits));
     L.bsum = o; o += align256(4 * ((size_t)div_up(nn, GS_TILE_ITEMS) + 1));
     L.offs = o; o += align256(4 * (nn + 1));
     L.counters = o; o += 256;
@@ -310,26 +365,31 @@ BinsortLayout binsort_layout(int32_t n, uint32_t capacity) {
 template <typename T>
 T* at(void* ws, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(ws) + off); }
 
-// LSD passes over bits [0, total_bits) of `count` keys.  Buffers: in, tmp, out.
-hipError_t radix_sort(uint32_t* kin, uint32_t* vin, uint32_t* ktmp, uint32_t* vtmp, uint32_t* kout, uint32_t* vout,
-                      const uint32_t* count, uint32_t max_count, int total_bits, uint32_t* hist,
-                      uint32_t* totals, hipStream_t st) {
+// LSD passes over bits [0, total_bits) of `count` keys, BITS per pass.
+// Buffers: in, tmp, out.
+// vin may be null: the values are then the input positions.  Value buffers
+// ping-pong between vtmp0 and vtmp1.
+template <int BITS>
+hipError_t radix_sort(uint32_t* kin, const uint32_t* vin, uint32_t* ktmp, uint32_t* vtmp0, uint32_t* vtmp1,
+                      uint32_t* kout, uint32_t* vout, const uint32_t* count, uint32_t max_count, int total_bits,
+                      uint32_t* hist, uint32_t* totals, hipStream_t st) {
     const uint32_t nblocks = div_up(max_count > 0 ? max_count : 1, GS_TILE_ITEMS);
-    const int passes = (total_bits + kRadixBits - 1) / kRadixBits;
+    const int passes = (total_bits + BITS - 1) / BITS;
     uint32_t* kb[2] = {ktmp, kin};
-    uint32_t* vb[2] = {vtmp, vin};
+    uint32_t* vb[2] = {vtmp0, vtmp1};
     for (int p = 0; p < passes; ++p) {
-        const int shift = p * kRadixBits;
-        const int nbits = (total_bits - shift) < kRadixBits ? (total_bits - shift) : kRadixBits;
+        const int shift = p * BITS;
+        const int nbits = (total_bits - shift) < BITS ? (total_bits - shift) : BITS;
         const uint32_t mask = (1u << nbits) - 1u;
         const uint32_t* ks = (p == 0) ? kin : kb[(p - 1) & 1];
         const uint32_t* vs = (p == 0) ? vin : vb[(p - 1) & 1];
         uint32_t* kd = (p == passes - 1) ? kout : kb[p & 1];
         uint32_t* vd = (p == passes - 1) ? vout : vb[p & 1];
-        hipLaunchKernelGGL(k_radix_hist, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, count, shift, mask, hist, nblocks);
-        hipLaunchKernelGGL(k_radix_scan, dim3(kRadix), dim3(GS_BLOCK), 0, st, hist, nblocks, totals);
-        hipLaunchKernelGGL(k_radix_scatter, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, vs, kd, vd, count, shift, mask,
-                           nbits, hist, totals, nblocks);
+        hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, count, shift, mask, hist,
+                           nblocks);
+        hipLaunchKernelGGL(k_radix_scan, dim3(1u << nbits), dim3(GS_BLOCK), 0, st, hist, nblocks, totals);
+        hipLaunchKernelGGL(k_radix_scatter<BITS>, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, vs, kd, vd, count, shift,
+                           mask, nbits, hist, totals, nblocks);
     }
     return hipGetLastError();
 }
@@ -340,7 +400,7 @@ size_t binsort_ws_bytes(int32_t n, uint32_t capacity, int32_t, int32_t) { return
 
 hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                           int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                          uint32_t* pair_offset, uint32_t* pair_perm, uint64_t* keys, uint32_t* num_pairs,
+                          uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys, uint32_t* num_pairs,
                           gs_device_status* status, void* ws, hipStream_t st) {
     const BinsortLayout L = binsort_layout(n, capacity);
     const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
@@ -358,8 +418,9 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     // 1. depth order of the visible set
     hipLaunchKernelGGL(k_depth_keys, dim3(div_up(n, GS_BLOCK)), dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.depth,
                        at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]));
-    e = radix_sort(at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]), at<uint32_t>(ws, L.dk[1]),
-                   at<uint32_t>(ws, L.dv[1]), at<uint32_t>(ws, L.dk[2]), at<uint32_t>(ws, L.dv[2]), vis_count,
+    e = radix_sort<kDepthBits>(at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]), at<uint32_t>(ws, L.dk[1]),
+                   at<uint32_t>(ws, L.dv[1]), at<uint32_t>(ws, L.dv[0]), at<uint32_t>(ws, L.dk[2]),
+                   at<uint32_t>(ws, L.dv[2]), vis_count,
                    (uint32_t)n, 31, hist, totals, st);
     if (e != hipSuccess) return e;
     const uint32_t* order = at<uint32_t>(ws, L.dv[2]);
@@ -378,15 +439,16 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     // 3. stable sort of the pairs by tile id
     int tbits = 1;
     while (tbits < 32 && (1u << tbits) < T) ++tbits;
-    e = radix_sort(at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), at<uint32_t>(ws, L.pk[1]),
-                   at<uint32_t>(ws, L.pv[1]), at<uint32_t>(ws, L.pk[2]), vals, ctr + 1, capacity, tbits, hist,
-                   totals, st);
+    //    carrying every pair's emission position as its value
+    e = radix_sort<kTileBits>(at<uint32_t>(ws, L.pk[0]), nullptr, at<uint32_t>(ws, L.pk[1]), at<uint32_t>(ws, L.pv[1]),
+                              at<uint32_t>(ws, L.pv[2]), at<uint32_t>(ws, L.pk[2]), pair_emit, ctr + 1, capacity,
+                              tbits, hist, totals, st);
     if (e != hipSuccess) return e;
-    // 4. tile ranges (+ optional 64-bit keys)
+    // 4. tile ranges, primitive ids (+ optional 64-bit keys)
     if (capacity > 0)
         hipLaunchKernelGGL(k_finalize, dim3(div_up(capacity, GS_BLOCK)), dim3(GS_BLOCK), 0, st,
-                           at<uint32_t>(ws, L.pk[2]), vals, ctr + 1, proj.depth,
-                           reinterpret_cast<const ushort4*>(proj.rect), pair_offset, TX, ranges, keys, pair_perm);
+                           at<uint32_t>(ws, L.pk[2]), pair_emit, at<uint32_t>(ws, L.pv[0]), ctr + 1, proj.depth,
+                           ranges, keys, vals);
     return hipGetLastError();
 }
 

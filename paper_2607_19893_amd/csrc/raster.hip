@@ -11,10 +11,10 @@
 // (1 - alpha) and keeps the suffix colour sum; per pair, the 9 partial
 // derivatives are summed over each 16-lane pixel row with DPP, over the rows
 // of a wave with LDS atomics, and over the 4 waves in a fixed order, then
-// written to the pair's slot at its sorted position.  Per visible primitive,
-// k_slot_sums adds its slots in emission order (through the sorted position
-// of every emitted pair) -- deterministic, no floating-point atomics in global
-// memory -- and k_project_bwd applies the projection and colour chain rule
+// written to the pair's slot at its emission position (a primitive's pairs
+// side by side).  Per visible primitive, k_slot_sums adds its slots in order
+// -- deterministic, no floating-point atomics in global memory -- and
+// k_project_bwd applies the projection and colour chain rule
 // (geometry in fp64) and writes one compact gradient row.
 #include "common.h"
 #include "internal.h"
@@ -360,7 +360,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, const float* __restrict__ final_T, const uint32_t* __restrict__ n_contrib,
-    const float* __restrict__ dL_dimg, float* __restrict__ slots) {
+    const float* __restrict__ dL_dimg, const uint32_t* __restrict__ pair_emit, float* __restrict__ slots) {
     __shared__ SplatLds<kBwdBatch> L;
     __shared__ float s_acc[4][kG][kBwdBatch];
     __shared__ uint8_t s_list[4][4][kBwdBatch];
@@ -478,14 +478,15 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
         }
         __syncthreads();
         if ((uint32_t)tid < cnt) {
-            // the pair's slot is its sorted position: consecutive threads write consecutive slots
+            // the pair's slot is its emission position: a primitive's pairs end up
+            // side by side, for k_slot_sums to read contiguously
             float v[kSlot] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
             if (work) {
 #pragma unroll
                 for (int q = 0; q < kG; ++q)
                     v[q] = (s_acc[0][q][tid] + s_acc[1][q][tid]) + (s_acc[2][q][tid] + s_acc[3][q][tid]);
             }
-            float4* dst = reinterpret_cast<float4*>(slots + (size_t)(start + bs + tid) * kSlot);
+            float4* dst = reinterpret_cast<float4*>(slots + (size_t)pair_emit[start + bs + tid] * kSlot);
             dst[0] = make_float4(v[0], v[1], v[2], v[3]);
             dst[1] = make_float4(v[4], v[5], v[6], v[7]);
             dst[2] = make_float4(v[8], v[9], v[10], v[11]);
@@ -687,23 +688,20 @@ __device__ __forceinline__ void geometry_bwd(const float* mu_f, const float* ls_
     out[9] = (float)((gz - z * along) * iq);
 }
 
-// pos comes from pair_perm; after a pair-list overflow that array holds
-// whatever an earlier view (or the allocator) left there, so every position is
-// clamped into the slot array before use.
-__device__ __forceinline__ void add_slot(float* g, const float* __restrict__ slots, uint32_t pos, uint32_t capacity) {
-    pos = min(pos, capacity - 1u);
+__device__ __forceinline__ void add_slot(float* g, const float* __restrict__ slots, uint32_t pos) {
     const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)pos * kSlot);
     const float4 v0 = sl[0], v1 = sl[1], v2 = sl[2];
     g[0] += v0.x; g[1] += v0.y; g[2] += v0.z; g[3] += v0.w;
     g[4] += v1.x; g[5] += v1.y; g[6] += v1.z; g[7] += v1.w; g[8] += v2.x;
 }
 
-// Per visible row r: the primitive's 2D gradient, the sum of its pair slots in
-// emission order (none if the pair list overflowed its capacity).  Four lanes
-// share a row: lane s of the quad adds slots s, s+4, s+8, ... and the quad
-// combines its four partial sums with two DPP steps (a fixed order, so the
-// result is deterministic).  Rows with more than kQuadSlots slots are summed
-// by the whole wave instead.
+// Per visible row r: the primitive's 2D gradient, the sum of its pair slots
+// (emission positions pair_offset[id] .. + tiles[id], side by side) in order;
+// none if the pair list overflowed its capacity.  Four lanes share a row:
+// lane s of the quad adds slots s, s+4, s+8, ... and the quad combines its
+// four partial sums with two DPP steps (a fixed order, so the result is
+// deterministic).  Rows with more than kQuadSlots slots are summed by the
+// whole wave instead.
 constexpr int kRowLanes = 4;
 constexpr uint32_t kQuadSlots = 64;
 
@@ -715,9 +713,8 @@ __device__ __forceinline__ float quad_sum(float v) {
 
 __global__ void __launch_bounds__(GS_BLOCK) k_slot_sums(
     const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
-    const uint32_t* __restrict__ pair_offset, const uint32_t* __restrict__ pair_perm,
-    const float* __restrict__ slots, uint32_t capacity, float* __restrict__ g2c, float* __restrict__ grad2d,
-    float* __restrict__ grad_norm) {
+    const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, uint32_t capacity,
+    float* __restrict__ g2c, float* __restrict__ grad2d, float* __restrict__ grad_norm) {
     constexpr uint32_t kRowsPerBlock = GS_BLOCK / kRowLanes;
     const uint32_t V = *vis_count;
     if (blockIdx.x * kRowsPerBlock >= V) return;
@@ -732,10 +729,8 @@ __global__ void __launch_bounds__(GS_BLOCK) k_slot_sums(
     if (fits && nt <= kQuadSlots) {
         uint32_t k = sub;
         for (; k + kRowLanes < nt; k += 2 * kRowLanes) {
-            const uint32_t p0 = min(pair_perm[first + k], capacity - 1u);
-            const uint32_t p1 = min(pair_perm[first + k + kRowLanes], capacity - 1u);
-            const float4* s0 = reinterpret_cast<const float4*>(slots + (size_t)p0 * kSlot);
-            const float4* s1 = reinterpret_cast<const float4*>(slots + (size_t)p1 * kSlot);
+            const float4* s0 = reinterpret_cast<const float4*>(slots + (size_t)(first + k) * kSlot);
+            const float4* s1 = reinterpret_cast<const float4*>(slots + (size_t)(first + k + kRowLanes) * kSlot);
             const float4 a0 = s0[0], a1 = s0[1], a2 = s0[2];
             const float4 b0 = s1[0], b1 = s1[1], b2 = s1[2];
             g2[0] += a0.x; g2[1] += a0.y; g2[2] += a0.z; g2[3] += a0.w;
@@ -743,7 +738,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_slot_sums(
             g2[0] += b0.x; g2[1] += b0.y; g2[2] += b0.z; g2[3] += b0.w;
             g2[4] += b1.x; g2[5] += b1.y; g2[6] += b1.z; g2[7] += b1.w; g2[8] += b2.x;
         }
-        if (k < nt) add_slot(g2, slots, pair_perm[first + k], capacity);
+        if (k < nt) add_slot(g2, slots, first + k);
     }
 #pragma unroll
     for (int q = 0; q < kG; ++q) g2[q] = quad_sum(g2[q]);
@@ -755,7 +750,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_slot_sums(
         const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)first, owner);
         const uint32_t nb = (uint32_t)__builtin_amdgcn_readlane((int)nt, owner);
         float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-        for (uint32_t k = lane_id(); k < nb; k += GS_WAVE) add_slot(acc, slots, pair_perm[f + k], capacity);
+        for (uint32_t k = lane_id(); k < nb; k += GS_WAVE) add_slot(acc, slots, f + k);
 #pragma unroll
         for (int q = 0; q < kG; ++q) {
             const float v = wave_sum(acc[q]);
@@ -919,7 +914,7 @@ size_t raster_bwd_ws_bytes(int32_t n, uint32_t capacity) {
 }
 
 hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
-                             const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_perm,
+                             const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_emit,
                              const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity,
                              const float* final_T, const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
                              float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, int stages,
@@ -931,13 +926,12 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
         hipLaunchKernelGGL(k_raster_bwd, dim3(T), dim3(GS_BLOCK), 0, st, ranges, vals,
                            reinterpret_cast<const float2*>(proj.mean2d),
                            reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, cam.width, cam.height,
-                           cam.tiles_x, bg[0], bg[1], bg[2], final_T, n_contrib, dL_dimg, slots);
+                           cam.tiles_x, bg[0], bg[1], bg[2], final_T, n_contrib, dL_dimg, pair_emit, slots);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || scene.n == 0 || !(stages & 2)) return e;
     const dim3 grid(div_up(scene.n, GS_BLOCK));
     hipLaunchKernelGGL(k_slot_sums, dim3(div_up(scene.n, GS_BLOCK / kRowLanes)), dim3(GS_BLOCK), 0, st, vis_idx,
-                       vis_count, proj.tiles, pair_offset,
-                       pair_perm, slots, capacity, g2c, grad2d, grad_norm);
+                       vis_count, proj.tiles, pair_offset, slots, capacity, g2c, grad2d, grad_norm);
 #define GS_LAUNCH_PBWD(D)                                                                                        \
     hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, g2c, proj.clamp,        \
                        scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam, grad_rows, grad_ld)

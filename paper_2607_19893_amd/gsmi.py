@@ -70,10 +70,10 @@ _lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, 
 _lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
 _lib.gs_raster_bwd.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P, P, P,
                                P, P, P, u32, P, P, P, P, P, i32, P, P, P, sz, P]
-_lib.gs_raster_bwd_pixels.argtypes = [ctypes.POINTER(gs_proj), ctypes.POINTER(gs_camera), P, P, u32, P, P, P, P, P,
-                                      sz, P]
+_lib.gs_raster_bwd_pixels.argtypes = [ctypes.POINTER(gs_proj), ctypes.POINTER(gs_camera), P, P, P, u32, P, P, P, P,
+                                      P, sz, P]
 _lib.gs_raster_bwd_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj),
-                                       P, P, P, P, u32, P, i32, P, P, P, sz, P]
+                                       P, P, P, u32, P, i32, P, P, P, sz, P]
 _lib.gs_sparse_adam.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, P, i32, P, P, i32, i32,
                                 ctypes.c_double, ctypes.c_double, ctypes.c_double, P, i32, P]
 _lib.gs_sparse_adam_publish.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, P, i32, P, P, i32, i32,
@@ -173,10 +173,10 @@ def gs_visible_set(kind, src, n, out_idx, out_count, ws, stream=None):
 
 
 def gs_bin_sort(proj: gs_proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges, pair_offset,
-                pair_perm, keys, num_pairs, status, ws, stream=None):
+                pair_emit, keys, num_pairs, status, ws, stream=None):
     return _check("gs_bin_sort", _lib.gs_bin_sort(ctypes.byref(proj), int(n), ptr(vis_idx), ptr(vis_count),
                                                   int(width), int(height), int(capacity), ptr(vals), ptr(ranges),
-                                                  ptr(pair_offset), ptr(pair_perm), ptr(keys), ptr(num_pairs),
+                                                  ptr(pair_offset), ptr(pair_emit), ptr(keys), ptr(num_pairs),
                                                   ptr(status), ptr(ws),
                                                   ws.numel() * ws.element_size(),
                                                   stream if stream is not None else current_stream()))
@@ -202,12 +202,12 @@ def gs_loss_l1(img, target, width, height, loss, dL_dimg, ws, stream=None):
                                                 stream if stream is not None else current_stream()))
 
 
-def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, pair_offset, pair_perm, vis_idx,
+def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, pair_offset, pair_emit, vis_idx,
                   vis_count, capacity, final_T, n_contrib, dL_dimg, bg, grad_rows, grad_ld, grad2d, grad_norm, ws,
                   stream=None):
     b = _bg(bg)
     return _check("gs_raster_bwd", _lib.gs_raster_bwd(ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj),
-                                                      ptr(vals), ptr(ranges), ptr(pair_offset), ptr(pair_perm),
+                                                      ptr(vals), ptr(ranges), ptr(pair_offset), ptr(pair_emit),
                                                       ptr(vis_idx), ptr(vis_count), int(capacity), ptr(final_T),
                                                       ptr(n_contrib), ptr(dL_dimg), ctypes.cast(b, P),
                                                       ptr(grad_rows), int(grad_ld), ptr(grad2d), ptr(grad_norm),
@@ -215,19 +215,20 @@ def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, 
                                                       stream if stream is not None else current_stream()))
 
 
-def gs_raster_bwd_pixels(proj: gs_proj, cam: gs_camera, vals, ranges, capacity, final_T, n_contrib, dL_dimg, bg, ws,
-                         stream=None):
+def gs_raster_bwd_pixels(proj: gs_proj, cam: gs_camera, vals, ranges, pair_emit, capacity, final_T, n_contrib, dL_dimg,
+                         bg, ws, stream=None):
     b = _bg(bg)
     return _check("gs_raster_bwd_pixels", _lib.gs_raster_bwd_pixels(
-        ctypes.byref(proj), ctypes.byref(cam), ptr(vals), ptr(ranges), int(capacity), ptr(final_T), ptr(n_contrib),
+        ctypes.byref(proj), ctypes.byref(cam), ptr(vals), ptr(ranges), ptr(pair_emit), int(capacity), ptr(final_T),
+        ptr(n_contrib),
         ptr(dL_dimg), ctypes.cast(b, P), ptr(ws), ws.numel() * ws.element_size(),
         stream if stream is not None else current_stream()))
 
 
-def gs_raster_bwd_project(scene: gs_scene, cam: gs_camera, proj: gs_proj, pair_offset, pair_perm, vis_idx, vis_count,
+def gs_raster_bwd_project(scene: gs_scene, cam: gs_camera, proj: gs_proj, pair_offset, vis_idx, vis_count,
                           capacity, grad_rows, grad_ld, grad2d, grad_norm, ws, stream=None):
     return _check("gs_raster_bwd_project", _lib.gs_raster_bwd_project(
-        ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj), ptr(pair_offset), ptr(pair_perm), ptr(vis_idx),
+        ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj), ptr(pair_offset), ptr(vis_idx),
         ptr(vis_count), int(capacity), ptr(grad_rows), int(grad_ld), ptr(grad2d), ptr(grad_norm), ptr(ws),
         ws.numel() * ws.element_size(), stream if stream is not None else current_stream()))
 

@@ -106,7 +106,7 @@ class ViewTrainer:
             return
         self.capacity = int(cap)
         self.vals = _u32(cap, self.dev)
-        self.pair_perm = _u32(cap, self.dev)
+        self.pair_emit = _u32(cap, self.dev)
         self.keys = torch.zeros(max(1, cap), dtype=torch.int64, device=self.dev) if self.with_keys else None
         self.ws_sort = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_BIN_SORT, self.n, cap, self.width,
                                                            self.height), dtype=torch.uint8, device=self.dev)
@@ -132,7 +132,7 @@ class ViewTrainer:
     def bin_sort(self):
         w, h = self.cam.width, self.cam.height
         gsmi.gs_bin_sort(self.proj_s, self.n, self.vis_idx, self.counts[0:1], w, h, self.capacity, self.vals,
-                         self.ranges, self.pair_offset, self.pair_perm, self.keys, self.counts[1:2], self.status,
+                         self.ranges, self.pair_offset, self.pair_emit, self.keys, self.counts[1:2], self.status,
                          self.ws_sort)
 
     def _img_views(self):
@@ -173,16 +173,16 @@ class ViewTrainer:
     def raster_bwd(self, bg=(0.0, 0.0, 0.0), grad2d=True):
         _, fT, nc, dL, _ = self._img_views()
         gsmi.gs_raster_bwd(self.scene_s, self.cam_c, self.proj_s, self.vals, self.ranges, self.pair_offset,
-                           self.pair_perm, self.vis_idx, self.counts[0:1], self.capacity, fT, nc, dL, bg,
+                           self.pair_emit, self.vis_idx, self.counts[0:1], self.capacity, fT, nc, dL, bg,
                            self.grad_rows, self.ld, self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
 
     def raster_bwd_pixels(self, bg=(0.0, 0.0, 0.0)):
         _, fT, nc, dL, _ = self._img_views()
-        gsmi.gs_raster_bwd_pixels(self.proj_s, self.cam_c, self.vals, self.ranges, self.capacity, fT, nc, dL, bg,
-                                  self.ws_bwd)
+        gsmi.gs_raster_bwd_pixels(self.proj_s, self.cam_c, self.vals, self.ranges, self.pair_emit, self.capacity, fT,
+                                  nc, dL, bg, self.ws_bwd)
 
     def raster_bwd_project(self, grad2d=False):
-        gsmi.gs_raster_bwd_project(self.scene_s, self.cam_c, self.proj_s, self.pair_offset, self.pair_perm,
+        gsmi.gs_raster_bwd_project(self.scene_s, self.cam_c, self.proj_s, self.pair_offset,
                                    self.vis_idx, self.counts[0:1], self.capacity, self.grad_rows, self.ld,
                                    self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
 

@@ -69,7 +69,7 @@ def test_null_and_range_arguments_rejected(gs):
     # gradient rows of the backward: leading dimension a multiple of 4, at least the row length
     sc3 = gs.gs_scene(10, 3, 16, 16, 16, 16, 16)
     cam3 = gs.gs_camera()
-    assert L.gs_raster_bwd_project(ctypes.byref(sc3), ctypes.byref(cam3), ctypes.byref(pr), 16, 16, 16, 16, 100, 16,
+    assert L.gs_raster_bwd_project(ctypes.byref(sc3), ctypes.byref(cam3), ctypes.byref(pr), 16, 16, 16, 100, 16,
                                    58, None, None, 256, 1 << 20, None) == gs.GS_ERR_INVALID_ARG
     assert "grad_ld" in gs.gs_last_error()
     g = (gs.gs_group * 1)(gs.gs_group(16, 3))

@@ -111,17 +111,18 @@ def test_project_visible_sort(case, torch_gpu, orc):
         order = vis_ref[np.lexsort((vis_ref, ref.depth[vis_ref].view(np.uint32)))]
         offs = np.concatenate([[0], np.cumsum(ref.tiles[order].astype(np.int64))[:-1]])
         np.testing.assert_array_equal(u32(tr.pair_offset)[order], offs)
-        # pair_perm: emission position -> sorted position, a permutation that maps
-        # each primitive's k-th rectangle tile (row-major) to its sorted pair
-        perm = u32(tr.pair_perm)[:M].astype(np.int64)
-        assert np.array_equal(np.sort(perm), np.arange(M))
+        # pair_emit: sorted position -> emission position, a permutation under which
+        # sorted pair i is tile number k of its primitive's rectangle (row-major),
+        # emitted at pair_offset[id] + k
+        emit = u32(tr.pair_emit)[:M].astype(np.int64)
+        assert np.array_equal(np.sort(emit), np.arange(M))
         gid_of_e = np.repeat(order, ref.tiles[order].astype(np.int64))
-        np.testing.assert_array_equal(vals_ref[perm], gid_of_e)
+        np.testing.assert_array_equal(gid_of_e[emit], vals_ref)
         k_local = np.arange(M) - np.repeat(offs, ref.tiles[order].astype(np.int64))
         rc = ref.rect[gid_of_e]
         wdt = rc[:, 2] - rc[:, 0]
         tile_e = (rc[:, 1] + k_local // wdt) * cam.tiles_x + rc[:, 0] + k_local % wdt
-        np.testing.assert_array_equal((keys_ref[perm] >> np.uint64(32)).astype(np.int64), tile_e)
+        np.testing.assert_array_equal(tile_e[emit], (keys_ref >> np.uint64(32)).astype(np.int64))
         _say(case, "view", vi, "V", V, "M", M, "ok")
 
 
