@@ -166,7 +166,19 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
     constexpr int K = (DEG + 1) * (DEG + 1);
     float Y[16];
     sh_basis(DEG, dx, dy, dz, Y);
-    const float* co = sh + (size_t)i * K * 3;
+    // the row's coefficients, as float4 loads when a row is a whole number of them
+    float co[3 * K];
+    if constexpr ((3 * K) % 4 == 0) {
+        const float4* s4 = reinterpret_cast<const float4*>(sh + (size_t)i * K * 3);
+#pragma unroll
+        for (int k = 0; k < 3 * K / 4; ++k) {
+            const float4 v4 = s4[k];
+            co[4 * k] = v4.x; co[4 * k + 1] = v4.y; co[4 * k + 2] = v4.z; co[4 * k + 3] = v4.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 3 * K; ++k) co[k] = sh[(size_t)i * K * 3 + k];
+    }
     float acc0 = 0.5f, acc1 = 0.5f, acc2 = 0.5f;
 #pragma unroll
     for (int k = 0; k < K; ++k) {

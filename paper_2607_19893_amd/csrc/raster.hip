@@ -302,19 +302,56 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
 // L1 loss
 // ---------------------------------------------------------------------------
 
+__device__ __forceinline__ float l1_elem(float a, float t, float inv, float& dl) {
+    const float d = a - t;
+    dl = d > 0.0f ? inv : (d < 0.0f ? -inv : 0.0f);
+    return fabsf(d);
+}
+
+// Block b covers elements [b*2048, b*2048+2048): with VEC, as 512 float4
+// (all three arrays 16-byte aligned; elements past the last whole float4
+// are done one by one by the last block), else element by element.
+template <bool VEC>
 __global__ void __launch_bounds__(GS_BLOCK) k_loss_l1(const float* __restrict__ img, const float* __restrict__ tgt,
                                                       uint32_t total, float inv, float* __restrict__ dL,
                                                       float* __restrict__ partial) {
     __shared__ float s_red[4];
-    const uint32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x;
     float acc = 0.0f;
+    if (VEC) {
+        const uint32_t n4 = total / 4;
+        const float4* a4 = reinterpret_cast<const float4*>(img);
+        const float4* t4 = reinterpret_cast<const float4*>(tgt);
+        float4* d4 = reinterpret_cast<float4*>(dL);
+        const uint32_t base = blockIdx.x * (GS_TILE_ITEMS / 4) + threadIdx.x;
 #pragma unroll
-    for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t i = base + k * GS_BLOCK;
-        if (i < total) {
-            const float d = img[i] - tgt[i];
-            dL[i] = d > 0.0f ? inv : (d < 0.0f ? -inv : 0.0f);
-            acc += fabsf(d);
+        for (int k = 0; k < GS_ITEMS / 4; ++k) {
+            const uint32_t i = base + k * GS_BLOCK;
+            if (i < n4) {
+                const float4 a = a4[i], t = t4[i];
+                float4 g;
+                acc += l1_elem(a.x, t.x, inv, g.x);
+                acc += l1_elem(a.y, t.y, inv, g.y);
+                acc += l1_elem(a.z, t.z, inv, g.z);
+                acc += l1_elem(a.w, t.w, inv, g.w);
+                d4[i] = g;
+            }
+        }
+        if (blockIdx.x == gridDim.x - 1 && threadIdx.x < total - 4 * n4) {
+            const uint32_t i = 4 * n4 + threadIdx.x;
+            float g;
+            acc += l1_elem(img[i], tgt[i], inv, g);
+            dL[i] = g;
+        }
+    } else {
+        const uint32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x;
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) {
+            const uint32_t i = base + k * GS_BLOCK;
+            if (i < total) {
+                float g;
+                acc += l1_elem(img[i], tgt[i], inv, g);
+                dL[i] = g;
+            }
         }
     }
     acc = wave_sum(acc);
@@ -897,7 +934,16 @@ hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, 
     float* partial = static_cast<float*>(ws);
     const float inv = (float)(1.0 / (double)total);
     if (nb > 0)
-        hipLaunchKernelGGL(k_loss_l1, dim3(nb), dim3(GS_BLOCK), 0, st, img, target, (uint32_t)total, inv, dL, partial);
+    {
+        const bool vec = ((reinterpret_cast<uintptr_t>(img) | reinterpret_cast<uintptr_t>(target) |
+                           reinterpret_cast<uintptr_t>(dL)) & 15u) == 0;
+        if (vec)
+            hipLaunchKernelGGL(k_loss_l1<true>, dim3(nb), dim3(GS_BLOCK), 0, st, img, target, (uint32_t)total, inv,
+                               dL, partial);
+        else
+            hipLaunchKernelGGL(k_loss_l1<false>, dim3(nb), dim3(GS_BLOCK), 0, st, img, target, (uint32_t)total, inv,
+                               dL, partial);
+    }
     hipLaunchKernelGGL(k_loss_final, dim3(1), dim3(GS_BLOCK), 0, st, partial, nb,
                        total ? 1.0 / (double)total : 0.0, loss);
     return hipGetLastError();
