@@ -187,16 +187,32 @@ __global__ void __launch_bounds__(GS_BLOCK) k_radix_scatter(
     }
 }
 
-// depth keys of the visible primitives (key = fp32 bits, value = id)
+// Depth keys of the visible primitives (key = fp32 bits, value = id), in the
+// sort's 2048-key blocks, with each block's histogram of the first digit
+// (bits 0-7) written as column b of the digit-major matrix -- the first
+// pass's histogram launch is not needed.
 __global__ void __launch_bounds__(GS_BLOCK) k_depth_keys(const uint32_t* __restrict__ vis_idx,
                                                          const uint32_t* __restrict__ vis_count,
                                                          const float* __restrict__ depth,
-                                                         uint32_t* __restrict__ keys, uint32_t* __restrict__ vals) {
-    const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
-    if (r >= *vis_count) return;
-    const uint32_t g = vis_idx[r];
-    keys[r] = __float_as_uint(depth[g]);
-    vals[r] = g;
+                                                         uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                                         uint32_t* __restrict__ hist, uint32_t nblocks) {
+    __shared__ uint32_t h[1 << kDepthBits];
+    for (int d = threadIdx.x; d < (1 << kDepthBits); d += GS_BLOCK) h[d] = 0;
+    __syncthreads();
+    const uint32_t V = *vis_count;
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        const uint32_t r = blockIdx.x * GS_TILE_ITEMS + k * GS_BLOCK + threadIdx.x;
+        if (r < V) {
+            const uint32_t g = vis_idx[r];
+            const uint32_t key = __float_as_uint(depth[g]);
+            keys[r] = key;
+            vals[r] = g;
+            atomicAdd(&h[key & ((1u << kDepthBits) - 1u)], 1u);
+        }
+    }
+    __syncthreads();
+    for (int d = threadIdx.x; d < (1 << kDepthBits); d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = h[d];
 }
 
 // per-block sums of tiles[] in depth order
@@ -262,18 +278,26 @@ __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
 // offs_r[r+1] and covers tile number i - offs_r[r] of that primitive's
 // rectangle (row-major).  Each block locates its rank range once, stages the
 // offsets, ids and rectangles of those ranks in LDS and binary-searches
-// there; key (tile id) and value (primitive id) stores are contiguous.
+// there; key (tile id) and value (primitive id) stores are contiguous.  Each
+// block also writes its histogram of the tile sort's first digit (key & mask0)
+// as column b of the digit-major matrix (zeros past the last pair).
 __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
     const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ offs_r,
     const ushort4* __restrict__ rect, const uint32_t* __restrict__ sort_count, int32_t tiles_x,
-    uint32_t* __restrict__ pkeys, uint32_t* __restrict__ pvals) {
+    uint32_t* __restrict__ pkeys, uint32_t* __restrict__ pvals, uint32_t mask0, uint32_t* __restrict__ hist,
+    uint32_t nblocks) {
     __shared__ uint32_t s_off[GS_TILE_ITEMS + 1];
     __shared__ uint32_t s_gid[GS_TILE_ITEMS + 1];
     __shared__ ushort4 s_rect[GS_TILE_ITEMS + 1];
     __shared__ uint32_t s_range[2];
+    __shared__ uint32_t h[1 << kTileBits];
+    for (int d = threadIdx.x; d < (1 << kTileBits); d += GS_BLOCK) h[d] = 0;
     const uint32_t M = *sort_count;
     const uint32_t base = blockIdx.x * GS_TILE_ITEMS;
-    if (base >= M) return;
+    if (base >= M) {
+        for (int d = threadIdx.x; d < (1 << kTileBits); d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = 0u;
+        return;
+    }
     const uint32_t hi = min(base + (uint32_t)GS_TILE_ITEMS, M);
     if (threadIdx.x < 2) {
         // largest r in [0, V) with offs_r[r] <= key
@@ -309,9 +333,13 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
         const uint32_t w = (uint32_t)(rc.z - rc.x);
         const uint32_t ty = rc.y + local / w;
         const uint32_t tx = rc.x + local % w;
-        pkeys[i] = ty * (uint32_t)tiles_x + tx;
+        const uint32_t key = ty * (uint32_t)tiles_x + tx;
+        pkeys[i] = key;
         pvals[i] = s_gid[lo];
+        atomicAdd(&h[key & mask0], 1u);
     }
+    __syncthreads();
+    for (int d = threadIdx.x; d < (1 << kTileBits); d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = h[d];
 }
 
 // Tile ranges, primitive ids and optional 64-bit keys of the sorted pairs.
@@ -369,6 +397,8 @@ T* at(void* ws, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(ws)
 // Buffers: in, tmp, out.
 // vin may be null: the values are then the input positions.  Value buffers
 // ping-pong between vtmp0 and vtmp1.
+// The first pass's histogram matrix is already in hist (written by the
+// kernel that produced the keys).
 template <int BITS>
 hipError_t radix_sort(uint32_t* kin, const uint32_t* vin, uint32_t* ktmp, uint32_t* vtmp0, uint32_t* vtmp1,
                       uint32_t* kout, uint32_t* vout, const uint32_t* count, uint32_t max_count, int total_bits,
@@ -385,8 +415,9 @@ hipError_t radix_sort(uint32_t* kin, const uint32_t* vin, uint32_t* ktmp, uint32
         const uint32_t* vs = (p == 0) ? vin : vb[(p - 1) & 1];
         uint32_t* kd = (p == passes - 1) ? kout : kb[p & 1];
         uint32_t* vd = (p == passes - 1) ? vout : vb[p & 1];
-        hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, count, shift, mask, hist,
-                           nblocks);
+        if (p > 0)
+            hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, count, shift, mask, hist,
+                               nblocks);
         hipLaunchKernelGGL(k_radix_scan, dim3(1u << nbits), dim3(GS_BLOCK), 0, st, hist, nblocks, totals);
         hipLaunchKernelGGL(k_radix_scatter<BITS>, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, vs, kd, vd, count, shift,
                            mask, nbits, hist, totals, nblocks);
@@ -416,8 +447,9 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
         return e;
     }
     // 1. depth order of the visible set
-    hipLaunchKernelGGL(k_depth_keys, dim3(div_up(n, GS_BLOCK)), dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.depth,
-                       at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]));
+    hipLaunchKernelGGL(k_depth_keys, dim3(div_up(n, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, vis_idx, vis_count,
+                       proj.depth, at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]), hist,
+                       div_up(n, GS_TILE_ITEMS));
     e = radix_sort<kDepthBits>(at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]), at<uint32_t>(ws, L.dk[1]),
                    at<uint32_t>(ws, L.dv[1]), at<uint32_t>(ws, L.dv[0]), at<uint32_t>(ws, L.dk[2]),
                    at<uint32_t>(ws, L.dv[2]), vis_count,
@@ -432,13 +464,15 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     uint32_t* offs_r = at<uint32_t>(ws, L.offs);
     hipLaunchKernelGGL(k_offsets, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles, bsum, ctr + 0,
                        capacity, pair_offset, offs_r, ctr + 1, num_pairs, status);
+    int tbits = 1;
+    while (tbits < 32 && (1u << tbits) < T) ++tbits;
+    const uint32_t mask0 = (1u << (tbits < kTileBits ? tbits : kTileBits)) - 1u;
     if (capacity > 0)
         hipLaunchKernelGGL(k_emit_pairs, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, order,
                            vis_count, offs_r, reinterpret_cast<const ushort4*>(proj.rect), ctr + 1, TX,
-                           at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]));
+                           at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), mask0, hist,
+                           div_up(capacity, GS_TILE_ITEMS));
     // 3. stable sort of the pairs by tile id
-    int tbits = 1;
-    while (tbits < 32 && (1u << tbits) < T) ++tbits;
     //    carrying every pair's emission position as its value
     e = radix_sort<kTileBits>(at<uint32_t>(ws, L.pk[0]), nullptr, at<uint32_t>(ws, L.pk[1]), at<uint32_t>(ws, L.pv[1]),
                               at<uint32_t>(ws, L.pv[2]), at<uint32_t>(ws, L.pk[2]), pair_emit, ctr + 1, capacity,

@@ -103,22 +103,22 @@ __device__ __forceinline__ float splat_sigma(double2 P, double2 Q, double c2, do
 }
 #pragma clang fp contract(on)
 
-// exp(-sigma) with range reduction: 2^-t, t = sigma log2(e) carried as hi + lo
-// (log2(e) split into an fp32 head and tail), t = n + f with n an integer and
-// |f| <= 1/2 + tiny, so the hardware base-2 exponential only sees f and the
-// power 2^-n is exact.  sigma is clamped to [0, 100] first (e^-100 is far
-// below any 1/255 threshold), so no overflow or NaN case arises.  Relative
-// error about one ulp of the hardware exponential.
+// exp(-sigma) = 2^-t with t = sigma log2(e) carried as hi + lo (log2(e)
+// split into an fp32 head and tail; hi = sigma * head rounded, lo its exact
+// rounding error plus sigma * tail, |lo| < 2e-5 for the sigmas that matter).
+// 2^-t = 2^-hi * 2^-lo with 2^-lo = 1 - lo ln2 up to (lo ln2)^2 / 2 < 1e-10;
+// the hardware base-2 exponential (1 ulp) takes -hi directly.  About two ulps
+// in all, far inside the alpha decision band; forward and backward call the
+// same code, so they take identical decisions.  Very large sigmas give 0,
+// negative ones are rejected by the caller.
 __device__ __forceinline__ float exp_neg(float sigma) {
     constexpr float kLog2eHi = 1.44269502162933349609375f;    // log2(e) rounded to fp32
     constexpr float kLog2eLo = 1.925963033500011e-08f;        // log2(e) - kLog2eHi
-    const float x = fminf(fmaxf(sigma, 0.0f), 100.0f);
-    const float hi = x * kLog2eHi;
-    float lo = fmaf(x, kLog2eHi, -hi);
-    lo = fmaf(x, kLog2eLo, lo);
-    const float n = __builtin_rintf(hi);
-    const float f = (hi - n) + lo;
-    return __builtin_ldexpf(__builtin_amdgcn_exp2f(-f), -(int)n);
+    constexpr float kLn2 = 0.693147180559945309417f;
+    const float hi = sigma * kLog2eHi;
+    float lo = fmaf(sigma, kLog2eHi, -hi);
+    lo = fmaf(sigma, kLog2eLo, lo);
+    return __builtin_amdgcn_exp2f(-hi) * fmaf(-lo, kLn2, 1.0f);
 }
 
 __device__ __forceinline__ bool wave_any(bool p) { return __ballot(p) != 0ull; }
