@@ -36,6 +36,35 @@ BWD_FLOP_EVAL = 13.0           # per replayed (pixel, pair): alpha recomputation
 BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/dalpha, 9 partials + their sum
 
 
+# HBM traffic of the dominant kernel (k_raster_bwd) on this workload, from two
+# rocprofv3 --pmc passes (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch, mean
+# of the 10 dispatches of an 8-step run), each scaled by what the same counter
+# reads for a plain device copy of known size (a 1 GiB read registers as 0.5
+# GiB of FETCH_SIZE, a 1 GiB write as 1 GiB of WRITE_SIZE).  Valid only for the
+# kernel source it was measured on: reported as null once raster.hip changes.
+TRAFFIC = {
+    "kernel": "k_raster_bwd",
+    "source": "paper_2607_19893_amd/csrc/raster.hip",
+    "source_sha256": "f4c79abcd32416a3b8764feb0be92fd0bf7ec5ec75cad059fa1b1e5bc24abd79",
+    "fetch_kib": 206369.35, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 98472.9, "write_scale": 1048576.0 / 1048576.0,
+    "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
+}
+
+
+def traffic_bytes():
+    """HBM bytes per launch of the dominant kernel, or None if its source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, TRAFFIC["source"])
+    try:
+        digest = hashlib.sha256(open(path, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    if digest != TRAFFIC["source_sha256"]:
+        return None
+    return 1024.0 * (TRAFFIC["fetch_kib"] * TRAFFIC["fetch_scale"] + TRAFFIC["write_kib"] * TRAFFIC["write_scale"])
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -159,8 +188,9 @@ def main():
     dom = max(roofs, key=lambda n: phase_ms[names.index(n)])
     bound, work, peak, unit = roofs[dom]
     ach = work / (phase_ms[names.index(dom)] * 1e-3)
+    tb = traffic_bytes() if dom == "raster_bwd_pixels" else None
     roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
-                "frac": round(ach / peak, 5), "traffic": None}
+                "frac": round(ach / peak, 5), "traffic": round(tb) if tb is not None else None}
     log("phase rooflines: " + json.dumps(per_phase))
     wi_mean = float(np.mean([w_iters[v] for v in views]))
     wh_mean = float(np.mean([w_hits[v] for v in views]))
