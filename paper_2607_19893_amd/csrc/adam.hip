@@ -124,6 +124,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint
                 const float delta = -step * (mn / den);
                 Mm[(size_t)id[u] * a.sld + col] = mn;
                 Vv[(size_t)id[u] * a.sld + col] = vn;
+                // a plain rounded add of the published step (this file is built
+                // without contraction): a replica that adds the message's rows stays
+                // bit-identical to the parameters
                 P[(size_t)id[u] * cols + c] = po[u] + delta;
                 if (drows) drows[(size_t)r * dld + col] = delta;
                 if (PUBLISH && col == 0) ids[r] = id[u];

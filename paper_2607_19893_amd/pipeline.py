@@ -194,11 +194,11 @@ class ViewTrainer:
         gsmi.gs_sparse_adam(self.adam_arr, 5, self.vis_idx, self.counts[0:1], self.n, self.grad_rows, self.ld, self.m,
                             self.v, self.ld, step, self.beta1, self.beta2, self.eps, self.delta_rows, self.ld)
 
-    def adam_publish(self, step, version):
+    def adam_publish(self, step, version, msg=None):
         """Sparse Adam over the visible rows, its steps staged as a message."""
         gsmi.gs_sparse_adam_publish(self.adam_arr, 5, self.vis_idx, self.counts[0:1], self.n, self.grad_rows,
                                     self.ld, self.m, self.v, self.ld, step, self.beta1, self.beta2, self.eps,
-                                    version, self.msg, self.status)
+                                    version, self.msg if msg is None else msg, self.status)
 
     def pack_params(self, version):
         """Stage the current parameter rows of the visible set (for an overwrite replica)."""
@@ -221,19 +221,86 @@ class ViewTrainer:
         self.m.copy_(torch.from_numpy(m))
         self.v.copy_(torch.from_numpy(v))
 
-    def apply(self, mode=gsmi.GS_APPLY_ADD):
-        gsmi.gs_delta_apply(self.msg, self.replica_arr, 5, self.n, self.n, mode, self.version, self.status)
+    def apply(self, mode=gsmi.GS_APPLY_ADD, msg=None):
+        gsmi.gs_delta_apply(self.msg if msg is None else msg, self.replica_arr, 5, self.n, self.n, mode,
+                            self.version, self.status)
+
+    def enable_overlap(self):
+        """Run each view's apply to the replica on a second stream (default
+        priority), issued once the next view's projection, visible set and
+        binning are queued, so that it runs beside that view's raster kernels
+        (arithmetic-bound, light on HBM), which read projection outputs, not the
+        replica.  Messages alternate between two buffers; a view's staging waits
+        until the apply that read its buffer two views earlier has finished."""
+        if getattr(self, "apply_stream", None) is not None:
+            return
+        self.apply_stream = torch.cuda.Stream(device=self.dev)
+        self.msgs = [self.msg, torch.zeros_like(self.msg)]
+        self.pub_ev = [torch.cuda.Event(), torch.cuda.Event()]
+        self.app_ev = [torch.cuda.Event(), torch.cuda.Event()]
+        self._slot = 0
+        self._pending = None
+        self.front_ev = torch.cuda.Event()
+
+    def flush_apply(self, after=None):
+        """Issue the deferred apply of the last view, if any (overlap mode); it
+        starts on the device once its message is staged and, if given, once the
+        event `after` has been reached."""
+        pend = getattr(self, "_pending", None)
+        if pend is None:
+            return
+        self._pending = None
+        k, ev = pend
+        with torch.cuda.stream(self.apply_stream):
+            self.apply_stream.wait_event(self.pub_ev[k])
+            if after is not None:
+                self.apply_stream.wait_event(after)
+            if ev:
+                ev[-2].record(self.apply_stream)
+            self.apply(msg=self.msgs[k])
+            self.app_ev[k].record(self.apply_stream)
+            if ev:
+                ev[-1].record(self.apply_stream)
 
     # -- whole view ----------------------------------------------------------
     PHASES = ("project", "visible", "bin_sort", "raster_fwd", "loss_l1", "raster_bwd_pixels", "raster_bwd_project",
               "adam_publish", "apply")
 
-    def step(self, cam, step, version=1, publish=True, active=False, target=None, events=None):
+    def step(self, cam, step, version=1, publish=True, active=False, target=None, events=None, overlap=False):
         """Project, visible set, bin+sort, forward, L1, backward, Adam staged as a message, apply to the replica.
         publish=False runs plain Adam (steps to delta_rows) and no apply.
         target: device tensor (3*H*W) or None for the set_target buffer.
-        events: optional list of len(PHASES)+1 torch.cuda.Event recorded around the phases."""
+        events: optional list of len(PHASES)+1 torch.cuda.Event recorded around the phases.
+        overlap: apply on the second stream, deferred into the next step (enable_overlap; call
+        flush_apply after the last step); events then holds len(PHASES)+2 events: the first
+        len(PHASES) bracket the other phases on the current stream, the last two bracket the
+        apply on the second stream."""
         ev = events
+        if overlap and publish:
+            self.enable_overlap()
+            k = self._slot
+            self._slot ^= 1
+            msg = self.msgs[k]
+            main = torch.cuda.current_stream()
+            calls = (lambda: self.project(cam), self.visible, self.bin_sort, lambda: self.raster_fwd(active=active),
+                     lambda: self.loss_l1(target), self.raster_bwd_pixels, self.raster_bwd_project)
+            if ev:
+                ev[0].record()
+            for i, fn in enumerate(calls):
+                fn()
+                if ev:
+                    ev[i + 1].record()
+                if i == 2:
+                    # the previous view's apply, once this view's binning is done on the device
+                    self.front_ev.record(main)
+                    self.flush_apply(after=self.front_ev)
+            main.wait_event(self.app_ev[k])          # the apply that read this buffer two views ago
+            self.adam_publish(step, version, msg)
+            self.pub_ev[k].record(main)
+            if ev:
+                ev[len(calls) + 1].record()
+            self._pending = (k, ev)
+            return
         calls = (lambda: self.project(cam), self.visible, self.bin_sort, lambda: self.raster_fwd(active=active),
                  lambda: self.loss_l1(target), self.raster_bwd_pixels, self.raster_bwd_project,
                  (lambda: self.adam_publish(step, version)) if publish else (lambda: self.adam(step)),

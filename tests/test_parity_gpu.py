@@ -464,3 +464,29 @@ def test_backward_halves_match_combined(torch_gpu, orc):
     got = [tr.grad_rows, tr.grad2d, tr.grad_norm]
     for a, b in zip(got, ref):
         assert torch_gpu.equal(a, b)
+
+
+def test_overlapped_publication_matches_sequential(torch_gpu, orc):
+    """Applies on the second stream (deferred into the next view) leave parameters, moments,
+    replica and publication versions bit-identical to the one-stream schedule, over several views."""
+    w = get_case("room-60k-392x216")
+    cam = w.cameras[0]
+    runs = []
+    for overlap in (False, True):
+        tr = trainer_for(w, torch_gpu)
+        tr.set_target(w.target(0))
+        for s in range(1, 6):
+            tr.step(cam, step=s, version=s, overlap=overlap)
+        tr.flush_apply()
+        torch_gpu.cuda.synchronize()
+        assert int(u32(tr.status)[0]) == 0
+        runs.append([t.clone() for t in tr.params] + [tr.m.clone(), tr.v.clone()] +
+                    [t.clone() for t in tr.replica] + [tr.version.clone()])
+    for a, b in zip(*runs):
+        assert torch_gpu.equal(a, b)
+    # the replica received every step as published: the same fp32 adds as the parameters,
+    # so replica and parameters are bit-identical; versions name the last publishing view
+    ver = u32(runs[1][-1])
+    assert (ver > 0).sum() > 0 and ver.max() == 5
+    for p, r in zip(runs[1][:5], runs[1][7:12]):
+        assert torch_gpu.equal(p, r)
