@@ -12,9 +12,9 @@
 // derivatives are summed over each 16-lane pixel row with DPP, over the rows
 // of a wave with LDS atomics, and over the 4 waves in a fixed order, then
 // written to the pair's slot at its emission position (a primitive's pairs
-// side by side).  Per visible primitive, k_slot_sums adds its slots in order
+// side by side).  Per visible primitive, k_project_bwd adds its slots in order
 // -- deterministic, no floating-point atomics in global memory -- and
-// k_project_bwd applies the projection and colour chain rule
+// applies the projection and colour chain rule
 // (geometry in fp64) and writes one compact gradient row.
 #include "common.h"
 #include "internal.h"
@@ -516,7 +516,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
         __syncthreads();
         if ((uint32_t)tid < cnt) {
             // the pair's slot is its emission position: a primitive's pairs end up
-            // side by side, for k_slot_sums to read contiguously
+            // side by side, for k_project_bwd to read contiguously
             float v[kSlot] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
             if (work) {
 #pragma unroll
@@ -582,12 +582,8 @@ __device__ __forceinline__ void sh_basis_grad(float x, float y, float z, float* 
 
 __device__ __forceinline__ float dot3(const float* a, const float* b) { return a[0] * b[0] + a[1] * b[1] + a[2] * b[2]; }
 
-// Per-primitive work runs in two kernels.  k_slot_sums (four lanes per
-// visible row, small register footprint, high occupancy) adds each
-// primitive's pair slots in a fixed order and writes a compact 12-float record
-// per row; k_project_bwd (one thread per visible row) then reads that record
-// and the parameter row and applies the chain rule.
-constexpr int kG2 = 12;     // floats per row of the compact 2D-gradient record (9 used)
+// Per-primitive work: k_project_bwd, one thread per visible row, adds the
+// primitive's pair slots and applies the chain rule.     // floats per row of the compact 2D-gradient record (9 used)
 
 template <int DEG>
 struct RowLayout {
@@ -732,80 +728,10 @@ __device__ __forceinline__ void add_slot(float* g, const float* __restrict__ slo
     g[4] += v1.x; g[5] += v1.y; g[6] += v1.z; g[7] += v1.w; g[8] += v2.x;
 }
 
-// Per visible row r: the primitive's 2D gradient, the sum of its pair slots
-// (emission positions pair_offset[id] .. + tiles[id], side by side) in order;
-// none if the pair list overflowed its capacity.  Four lanes share a row:
-// lane s of the quad adds slots s, s+4, s+8, ... and the quad combines its
-// four partial sums with two DPP steps (a fixed order, so the result is
-// deterministic).  Rows with more than kQuadSlots slots are summed by the
-// whole wave instead.
-constexpr int kRowLanes = 4;
-constexpr uint32_t kQuadSlots = 64;
-
-__device__ __forceinline__ float quad_sum(float v) {
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, true));   // [1,0,3,2]
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, true));   // [2,3,0,1]
-    return v;
-}
-
-__global__ void __launch_bounds__(GS_BLOCK) k_slot_sums(
-    const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
-    const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, uint32_t capacity,
-    float* __restrict__ g2c, float* __restrict__ grad2d, float* __restrict__ grad_norm) {
-    constexpr uint32_t kRowsPerBlock = GS_BLOCK / kRowLanes;
-    const uint32_t V = *vis_count;
-    if (blockIdx.x * kRowsPerBlock >= V) return;
-    const uint32_t r = blockIdx.x * kRowsPerBlock + threadIdx.x / kRowLanes;
-    const uint32_t sub = threadIdx.x % kRowLanes;
-    const bool valid = r < V;
-    const uint32_t id = valid ? vis_idx[r] : 0u;
-    const uint32_t first = valid ? pair_offset[id] : 0u;
-    const uint32_t nt = valid ? tiles[id] : 0u;
-    const bool fits = (uint64_t)first + nt <= capacity;
-    float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-    if (fits && nt <= kQuadSlots) {
-        uint32_t k = sub;
-        for (; k + kRowLanes < nt; k += 2 * kRowLanes) {
-            const float4* s0 = reinterpret_cast<const float4*>(slots + (size_t)(first + k) * kSlot);
-            const float4* s1 = reinterpret_cast<const float4*>(slots + (size_t)(first + k + kRowLanes) * kSlot);
-            const float4 a0 = s0[0], a1 = s0[1], a2 = s0[2];
-            const float4 b0 = s1[0], b1 = s1[1], b2 = s1[2];
-            g2[0] += a0.x; g2[1] += a0.y; g2[2] += a0.z; g2[3] += a0.w;
-            g2[4] += a1.x; g2[5] += a1.y; g2[6] += a1.z; g2[7] += a1.w; g2[8] += a2.x;
-            g2[0] += b0.x; g2[1] += b0.y; g2[2] += b0.z; g2[3] += b0.w;
-            g2[4] += b1.x; g2[5] += b1.y; g2[6] += b1.z; g2[7] += b1.w; g2[8] += b2.x;
-        }
-        if (k < nt) add_slot(g2, slots, first + k);
-    }
-#pragma unroll
-    for (int q = 0; q < kG; ++q) g2[q] = quad_sum(g2[q]);
-    // long lists: the whole wave, 64 slots at a time, for one row after another
-    uint64_t big = __ballot(fits && nt > kQuadSlots && sub == 0);
-    while (big) {
-        const int owner = __ffsll((unsigned long long)big) - 1;
-        big &= big - 1;
-        const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)first, owner);
-        const uint32_t nb = (uint32_t)__builtin_amdgcn_readlane((int)nt, owner);
-        float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-        for (uint32_t k = lane_id(); k < nb; k += GS_WAVE) add_slot(acc, slots, f + k);
-#pragma unroll
-        for (int q = 0; q < kG; ++q) {
-            const float v = wave_sum(acc[q]);
-            if ((lane_id() & ~(kRowLanes - 1)) == owner) g2[q] = v;
-        }
-    }
-    if (!valid) return;
-    float4* dst = reinterpret_cast<float4*>(g2c + (size_t)r * kG2);
-    if (sub == 0) dst[0] = make_float4(g2[0], g2[1], g2[2], g2[3]);
-    if (sub == 1) dst[1] = make_float4(g2[4], g2[5], g2[6], g2[7]);
-    if (sub == 2) dst[2] = make_float4(g2[8], 0.0f, 0.0f, 0.0f);
-    if (grad2d) {
-#pragma unroll
-        for (int q = 0; q < kG; ++q)
-            if ((uint32_t)q % kRowLanes == sub) grad2d[(size_t)id * kG + q] = g2[q];
-    }
-    if (grad_norm && sub == 3) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
-}
+// Lists of up to kSerialSlots slots are summed by their own thread; longer
+// ones (a primitive spanning many tiles) by the whole wave, 64 slots at a
+// time.  Either way the order is fixed, so the result is deterministic.
+constexpr uint32_t kSerialSlots = 32;
 
 template <int N>
 __device__ __forceinline__ void load_row(const float* __restrict__ src, float* dst) {
@@ -822,27 +748,62 @@ __device__ __forceinline__ void load_row(const float* __restrict__ src, float* d
     }
 }
 
-// Per visible row r: chain rule from the compact 2D gradient to the
-// parameters; writes the row's gradient record at grad_rows + r * ld.
+// Per visible row r: the primitive's 2D gradient (the sum of its pair slots,
+// emission positions pair_offset[id] .. + tiles[id], side by side; none if the
+// pair list overflowed its capacity), then the chain rule to the parameters;
+// writes the row's gradient record at grad_rows + r * ld.
 template <int DEG>
 __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
-    const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const float* __restrict__ g2c,
+    const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
+    const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, uint32_t capacity,
     const uint8_t* __restrict__ clampm, const float* __restrict__ mean, const float* __restrict__ log_scale,
     const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c,
-    float* __restrict__ grad_rows, int32_t ld) {
+    float* __restrict__ grad_rows, int32_t ld, float* __restrict__ grad2d, float* __restrict__ grad_norm) {
     using L = RowLayout<DEG>;
     constexpr int K = L::K;
     const uint32_t V = *vis_count;
+    if (blockIdx.x * GS_BLOCK >= V) return;
     const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
-    if (r >= V) return;
-    const uint32_t id = vis_idx[r];
-    float g2[kG];
+    const bool valid = r < V;
+    const uint32_t id = valid ? vis_idx[r] : 0u;
+    float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
     {
-        const float4* s4 = reinterpret_cast<const float4*>(g2c + (size_t)r * kG2);
-        const float4 a = s4[0], b = s4[1], d = s4[2];
-        g2[0] = a.x; g2[1] = a.y; g2[2] = a.z; g2[3] = a.w;
-        g2[4] = b.x; g2[5] = b.y; g2[6] = b.z; g2[7] = b.w; g2[8] = d.x;
+        const uint32_t first = valid ? pair_offset[id] : 0u;
+        const uint32_t nt = valid ? tiles[id] : 0u;
+        const bool fits = (uint64_t)first + nt <= capacity;
+        if (fits && nt <= kSerialSlots) {
+            uint32_t k = 0;
+            for (; k + 2 <= nt; k += 2) {
+                const float4* s0 = reinterpret_cast<const float4*>(slots + (size_t)(first + k) * kSlot);
+                const float4 a0 = s0[0], a1 = s0[1], a2 = s0[2], b0 = s0[3], b1 = s0[4], b2 = s0[5];
+                g2[0] += a0.x; g2[1] += a0.y; g2[2] += a0.z; g2[3] += a0.w;
+                g2[4] += a1.x; g2[5] += a1.y; g2[6] += a1.z; g2[7] += a1.w; g2[8] += a2.x;
+                g2[0] += b0.x; g2[1] += b0.y; g2[2] += b0.z; g2[3] += b0.w;
+                g2[4] += b1.x; g2[5] += b1.y; g2[6] += b1.z; g2[7] += b1.w; g2[8] += b2.x;
+            }
+            if (k < nt) add_slot(g2, slots, first + k);
+        }
+        uint64_t big = __ballot(fits && nt > kSerialSlots);
+        while (big) {
+            const int owner = __ffsll((unsigned long long)big) - 1;
+            big &= big - 1;
+            const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)first, owner);
+            const uint32_t nb = (uint32_t)__builtin_amdgcn_readlane((int)nt, owner);
+            float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+            for (uint32_t k = lane_id(); k < nb; k += GS_WAVE) add_slot(acc, slots, f + k);
+#pragma unroll
+            for (int q = 0; q < kG; ++q) {
+                const float v = wave_sum(acc[q]);
+                if (lane_id() == owner) g2[q] = v;
+            }
+        }
     }
+    if (!valid) return;
+    if (grad2d) {
+#pragma unroll
+        for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
+    }
+    if (grad_norm) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
     float mu[3], ls[3], qr[4];
     load_row<3>(mean + (size_t)id * 3, mu);
     load_row<3>(log_scale + (size_t)id * 3, ls);
@@ -949,14 +910,9 @@ hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, 
     return hipGetLastError();
 }
 
-// Workspace: the pair slots (capacity x kSlot floats), then the compact 2D
-// gradient records of the visible rows (n x kG2 floats).
-static size_t slots_bytes(uint32_t capacity) {
+// Workspace: the pair slots (capacity x kSlot floats).
+size_t raster_bwd_ws_bytes(int32_t, uint32_t capacity) {
     return align256(sizeof(float) * kSlot * (size_t)(capacity > 0 ? capacity : 1));
-}
-
-size_t raster_bwd_ws_bytes(int32_t n, uint32_t capacity) {
-    return slots_bytes(capacity) + align256(sizeof(float) * kG2 * (size_t)(n > 0 ? n : 1));
 }
 
 hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
@@ -966,7 +922,6 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
                              float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, int stages,
                              hipStream_t st) {
     float* slots = static_cast<float*>(ws);
-    float* g2c = reinterpret_cast<float*>(static_cast<char*>(ws) + slots_bytes(capacity));
     const int32_t T = cam.tiles_x * cam.tiles_y;
     if ((stages & 1) && T > 0)
         hipLaunchKernelGGL(k_raster_bwd, dim3(T), dim3(GS_BLOCK), 0, st, ranges, vals,
@@ -976,11 +931,10 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || scene.n == 0 || !(stages & 2)) return e;
     const dim3 grid(div_up(scene.n, GS_BLOCK));
-    hipLaunchKernelGGL(k_slot_sums, dim3(div_up(scene.n, GS_BLOCK / kRowLanes)), dim3(GS_BLOCK), 0, st, vis_idx,
-                       vis_count, proj.tiles, pair_offset, slots, capacity, g2c, grad2d, grad_norm);
 #define GS_LAUNCH_PBWD(D)                                                                                        \
-    hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, g2c, proj.clamp,        \
-                       scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam, grad_rows, grad_ld)
+    hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset,  \
+                       slots, capacity, proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, \
+                       cam, grad_rows, grad_ld, grad2d, grad_norm)
     switch (scene.sh_degree) {
         case 0: GS_LAUNCH_PBWD(0); break;
         case 1: GS_LAUNCH_PBWD(1); break;

@@ -84,8 +84,9 @@ def test_workspace_sizes_monotone(gs):
     b = gs.gs_workspace_bytes(gs.GS_WS_BIN_SORT, 2000, 10000, 256, 256)
     assert 0 < a < b and a % 256 == 0
     assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 0, 100) >= 9 * 4 * 100
-    assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 1000, 100) >= gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 0,
-                                                                                           100) + 9 * 4 * 1000
+    # the backward's workspace holds one padded 9-float slot per pair of the capacity
+    assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 1000, 100) >= 12 * 4 * 100
+    assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 0, 5000) > gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 0, 100)
     assert gs.gs_workspace_bytes(99, 10, 10) == 0
 
 
