@@ -8,9 +8,9 @@ SH-degree-3 room scene with 32 forward-facing 1920x1080 cameras; steps cycle
 through the cameras.  Inputs (scene, Adam state, all 32 targets) are resident
 in HBM before the timed region.
 
-Each view's apply to the replica runs on a second stream, issued after the
-next view's binning so that it runs beside that view's raster kernels (which
-read projection outputs, not the replica); --no-overlap runs everything on
+Each view's apply to the replica runs on a second stream, started after the
+next view's loss so that it runs beside that view's backward raster (which
+reads projection outputs, not the replica); --no-overlap runs everything on
 one stream.  Every timed view's apply completes inside the timed region.
 
 Prints one JSON line (the driver's contract) with a roofline entry for the
@@ -84,7 +84,7 @@ def main():
     ap.add_argument("--cpu-views", type=int, default=8, help="views of the CPU oracle sample")
     ap.add_argument("--no-overlap", action="store_true",
                     help="run every phase on one stream (by default each view's apply to the replica runs on a "
-                         "second stream, beside the next view's raster kernels)")
+                         "second stream, beside the next view's backward raster)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy (read + write of this many MiB, 4 times) and exit; "
                          "its HBM counters calibrate the traffic counters of the path's kernels")

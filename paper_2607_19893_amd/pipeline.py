@@ -227,10 +227,9 @@ class ViewTrainer:
 
     def enable_overlap(self):
         """Run each view's apply to the replica on a second stream (default
-        priority), issued once the next view's projection, visible set and
-        binning are queued, so that it runs beside that view's raster kernels
-        (arithmetic-bound, light on HBM), which read projection outputs, not the
-        replica.  Messages alternate between two buffers; a view's staging waits
+        priority), started once the next view's loss is done on the device, so
+        that it runs beside that view's backward raster (arithmetic-bound, light
+        on HBM), which reads projection outputs, not the replica.  Messages alternate between two buffers; a view's staging waits
         until the apply that read its buffer two views earlier has finished."""
         if getattr(self, "apply_stream", None) is not None:
             return
@@ -263,6 +262,7 @@ class ViewTrainer:
                 ev[-1].record(self.apply_stream)
 
     # -- whole view ----------------------------------------------------------
+    APPLY_AFTER = 4       # overlap mode: a view's apply starts once the next view's loss is done
     PHASES = ("project", "visible", "bin_sort", "raster_fwd", "loss_l1", "raster_bwd_pixels", "raster_bwd_project",
               "adam_publish", "apply")
 
@@ -290,8 +290,8 @@ class ViewTrainer:
                 fn()
                 if ev:
                     ev[i + 1].record()
-                if i == 2:
-                    # the previous view's apply, once this view's binning is done on the device
+                if i == self.APPLY_AFTER:
+                    # the previous view's apply, once this view reaches that phase on the device
                     self.front_ev.record(main)
                     self.flush_apply(after=self.front_ev)
             main.wait_event(self.app_ev[k])          # the apply that read this buffer two views ago
