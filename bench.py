@@ -50,9 +50,9 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 TRAFFIC = {
     "kernel": "k_raster_bwd",
     "source": "paper_2607_19893_amd/csrc/raster.hip",
-    "source_sha256": "f4c79abcd32416a3b8764feb0be92fd0bf7ec5ec75cad059fa1b1e5bc24abd79",
-    "fetch_kib": 206369.35, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 98472.9, "write_scale": 1048576.0 / 1048576.0,
+    "source_sha256": "ef4ce98e8c60f8221de6319d990c0fde516949879baab54e6b7aae79c3b83f6d",
+    "fetch_kib": 206371.92, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 98490.26, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
