@@ -46,26 +46,36 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 # of the 10 dispatches of an 8-step run), each scaled by what the same counter
 # reads for a plain device copy of known size (a 1 GiB read registers as 0.5
 # GiB of FETCH_SIZE, a 1 GiB write as 1 GiB of WRITE_SIZE).  Valid only for the
-# kernel source it was measured on: reported as null once raster.hip changes.
+# kernel code it was measured on (comments aside): reported as null once the
+# code of raster.hip changes.
 TRAFFIC = {
     "kernel": "k_raster_bwd",
     "source": "paper_2607_19893_amd/csrc/raster.hip",
-    "source_sha256": "ef4ce98e8c60f8221de6319d990c0fde516949879baab54e6b7aae79c3b83f6d",
+    "code_sha256": "28946c75930d90cc0d1970e2a434db05380b20471cc571db15232da79441b9f9",
     "fetch_kib": 206371.92, "fetch_scale": 1048576.0 / 524294.5,
     "write_kib": 98490.26, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
 
-def traffic_bytes():
-    """HBM bytes per launch of the dominant kernel, or None if its source changed since the counters were taken."""
+def code_digest(text):
+    """sha256 of a C/C++ source with comments, blank lines and trailing blanks removed."""
     import hashlib
+    import re
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    text = "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
+    return hashlib.sha256(text.encode()).hexdigest()
+
+
+def traffic_bytes():
+    """HBM bytes per launch of the dominant kernel, or None if its code changed since the counters were taken."""
     path = os.path.join(ROOT, TRAFFIC["source"])
     try:
-        digest = hashlib.sha256(open(path, "rb").read()).hexdigest()
+        digest = code_digest(open(path).read())
     except OSError:
         return None
-    if digest != TRAFFIC["source_sha256"]:
+    if digest != TRAFFIC["code_sha256"]:
         return None
     return 1024.0 * (TRAFFIC["fetch_kib"] * TRAFFIC["fetch_scale"] + TRAFFIC["write_kib"] * TRAFFIC["write_scale"])
 

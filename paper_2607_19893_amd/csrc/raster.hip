@@ -583,7 +583,7 @@ __device__ __forceinline__ void sh_basis_grad(float x, float y, float z, float* 
 __device__ __forceinline__ float dot3(const float* a, const float* b) { return a[0] * b[0] + a[1] * b[1] + a[2] * b[2]; }
 
 // Per-primitive work: k_project_bwd, one thread per visible row, adds the
-// primitive's pair slots and applies the chain rule.     // floats per row of the compact 2D-gradient record (9 used)
+// primitive's pair slots and applies the chain rule.
 
 template <int DEG>
 struct RowLayout {
