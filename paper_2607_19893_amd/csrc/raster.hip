@@ -380,10 +380,11 @@ __global__ void __launch_bounds__(GS_BLOCK) k_loss_final(const float* __restrict
 
 constexpr int kG = 9;   // du dv dA dB dC dopacity dr dg db
 constexpr int kSlot = 12;          // floats per pair slot (9 used, padded for 16-byte stores)
-// Pairs staged per batch.  The per-wave accumulators (4 x 9 floats per staged
-// pair) dominate the workgroup's LDS; 128 keeps it near 27 KB so that the
-// registers, not LDS, bound the workgroups per CU.
-constexpr int kBwdBatch = 128;
+constexpr int kRowSums = 6;        // per-row sums: sum ds, sum ds dx, sum ds dx^2, three colour sums
+// Pairs staged per batch: one per lane, so that after the walk each wave adds
+// its four rows' sums of entry k in lane k.  The per-row sums (16 rows x 6
+// floats per staged pair, 24 KB) dominate the workgroup's LDS.
+constexpr int kBwdBatch = GS_WAVE;
 
 // Per pixel, walking back to front: T is recovered in front of each included
 // pair as T / (1 - alpha), and instead of the three suffix colour sums S_c
@@ -393,15 +394,34 @@ constexpr int kBwdBatch = 128;
 //   dL/dalpha = T_k (g . rgb) - gS / (1 - alpha),  gS += alpha T_k (g . rgb).
 // Each 16-lane pixel row walks its own list of the batch (compact_rows),
 // back to front, only up to the last pair any of its pixels included.
+//
+// The 2D gradient of a pair is linear in moments of ds = dL/dsigma over its
+// pixels: with sigma = (A dx^2 + 2B dx dy + C dy^2) / 2 and (dx, dy) the offset
+// of the splat centre from the pixel centre,
+//   dL/du = A m_x + B m_y,  dL/dv = B m_x + C m_y,
+//   dL/dA = m_xx / 2,  dL/dB = m_xy,  dL/dC = m_yy / 2,  dL/dopacity = -m / o,
+// with m = sum ds, m_x = sum ds dx, m_xy = sum ds dx dy and so on (the opacity
+// line because ds = -dL/dalpha * o e^-sigma below the 0.99 cap, and both are 0
+// at it).  A pixel row shares dy, so a row needs only m, m_x and m_xx (plus
+// the three colour sums) over its lanes.  A row visits an entry at most once
+// per batch, so its leader stores the six sums with plain LDS writes into the
+// row's own record of that entry (no atomics); after the walk lane k of each
+// wave scales its four rows' records of entry k by their dy and adds them,
+// and the four waves' results are added in a fixed order.  A pair slot holds
+// (m_x, m_y, m_xx, m_xy, m_yy, m, colour); k_project_bwd expands it with the
+// conic once per primitive.
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, const float* __restrict__ final_T, const uint32_t* __restrict__ n_contrib,
     const float* __restrict__ dL_dimg, const uint32_t* __restrict__ pair_emit, float* __restrict__ slots) {
     __shared__ SplatLds<kBwdBatch> L;
-    __shared__ float s_acc[4][kG][kBwdBatch];
+    // [wave][row][sum][entry]; after the walk a wave's part holds its 9 combined
+    // sums per entry, [q][entry]
+    __shared__ float s_row[4][4][kRowSums][kBwdBatch];
     __shared__ uint8_t s_list[4][4][kBwdBatch];
     __shared__ uint32_t s_max;
+    static_assert(kG * kBwdBatch <= 4 * kRowSums * kBwdBatch, "combined sums fit a wave's row records");
     const int tile = blockIdx.x;
     const int tid = threadIdx.x;
     const int w = tid / GS_WAVE;
@@ -443,11 +463,12 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             const uint32_t g = vals[start + bs + tid];
             stage_splat(L, tid, mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
         }
-        if (work && tid < kBwdBatch) {
+        if (work) {
+            // rows that never take an entry leave its record at zero
+            float4* z = reinterpret_cast<float4*>(&s_row[w][0][0][0]);
 #pragma unroll
-            for (int ww = 0; ww < 4; ++ww)
-#pragma unroll
-                for (int q = 0; q < kG; ++q) s_acc[ww][q][tid] = 0.0f;
+            for (int i = 0; i < 4 * kRowSums * kBwdBatch / 4 / GS_WAVE; ++i)
+                z[i * GS_WAVE + lane] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         }
         __syncthreads();
         uint32_t lim[4], nl[4] = {0u, 0u, 0u, 0u};
@@ -483,26 +504,18 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             T = Tk;
             const bool geo = ok && gv < kAlphaMax;      // the 0.99 cap stops d/d(opacity, sigma)
             const float ds = geo ? -dalpha * alpha : 0.0f;
-            // d sigma / d(u, v) = (A dx + B dy, B dx + C dy), from sigma's own terms
-            const float dsdu = (float)fma(Q.x, ddx, inner);
-            const float dsdv = (float)fma(Q.y, ddx, cdy + cdy);
-            const float dx = (float)ddx, dy = (float)ddy;
-            const float hds = 0.5f * ds;
-            const float hdx = hds * dx;
-            float gr[kG];
-            gr[0] = ds * dsdu;
-            gr[1] = ds * dsdv;
-            gr[2] = hdx * dx;
-            gr[3] = (ds * dx) * dy;
-            gr[4] = (hds * dy) * dy;
-            gr[5] = geo ? dalpha * e : 0.0f;
-            gr[6] = gC0 * wgt;
-            gr[7] = gC1 * wgt;
-            gr[8] = gC2 * wgt;
+            const float dsx = ds * (float)ddx;
+            float gr[kRowSums];
+            gr[0] = ds;
+            gr[1] = dsx;
+            gr[2] = dsx * (float)ddx;
+            gr[3] = gC0 * wgt;
+            gr[4] = gC1 * wgt;
+            gr[5] = gC2 * wgt;
             // sum each 16-lane row (all its lanes hold the same entry) with DPP, then
-            // one lane per contributing row adds the row sum to the wave's accumulator
+            // one lane per contributing row stores the sums in the row's record
 #pragma unroll
-            for (int q = 0; q < kG; ++q) {
+            for (int q = 0; q < kRowSums; ++q) {
                 gr[q] = dpp_row_sum(gr[q]);
                 // keep the last add in front of the branch (all lanes active), where
                 // it folds into the DPP instruction
@@ -510,8 +523,38 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             }
             if ((lane & 15) == 0 && ((mask >> lane) & 0xFFFFull) != 0ull) {
 #pragma unroll
-                for (int q = 0; q < kG; ++q) atomicAdd(&s_acc[w][q][k], gr[q]);
+                for (int q = 0; q < kRowSums; ++q) s_row[w][row][q][k] = gr[q];
             }
+        }
+        // lane k adds this wave's four row records of entry k: only this wave
+        // wrote them, so a wave-level barrier orders the writes before the reads
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (work) {
+            float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+            const double vk = L.P[lane].y;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float dy = (float)(vk - (double)(wy0 + (float)q));   // the row's common offset
+                const float m = s_row[w][q][0][lane], mx = s_row[w][q][1][lane];
+                const float my = dy * m;
+                acc[0] += mx;
+                acc[1] += my;
+                acc[2] += s_row[w][q][2][lane];
+                acc[3] += dy * mx;
+                acc[4] += dy * my;
+                acc[5] += m;
+                acc[6] += s_row[w][q][3][lane];
+                acc[7] += s_row[w][q][4][lane];
+                acc[8] += s_row[w][q][5][lane];
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            float* comb = &s_row[w][0][0][0];
+#pragma unroll
+            for (int q = 0; q < kG; ++q) comb[q * kBwdBatch + lane] = acc[q];
         }
         __syncthreads();
         if ((uint32_t)tid < cnt) {
@@ -519,9 +562,15 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             // side by side, for k_project_bwd to read contiguously
             float v[kSlot] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
             if (work) {
+                const float* c0 = &s_row[0][0][0][0];
+                const float* c1 = &s_row[1][0][0][0];
+                const float* c2 = &s_row[2][0][0][0];
+                const float* c3 = &s_row[3][0][0][0];
 #pragma unroll
-                for (int q = 0; q < kG; ++q)
-                    v[q] = (s_acc[0][q][tid] + s_acc[1][q][tid]) + (s_acc[2][q][tid] + s_acc[3][q][tid]);
+                for (int q = 0; q < kG; ++q) {
+                    const int i = q * kBwdBatch + tid;
+                    v[q] = (c0[i] + c1[i]) + (c2[i] + c3[i]);
+                }
             }
             float4* dst = reinterpret_cast<float4*>(slots + (size_t)pair_emit[start + bs + tid] * kSlot);
             dst[0] = make_float4(v[0], v[1], v[2], v[3]);
@@ -756,7 +805,7 @@ template <int DEG>
 __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
     const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
     const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, uint32_t capacity,
-    const uint8_t* __restrict__ clampm, const float* __restrict__ mean, const float* __restrict__ log_scale,
+    const float4* __restrict__ conic_op, const uint8_t* __restrict__ clampm, const float* __restrict__ mean, const float* __restrict__ log_scale,
     const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c,
     float* __restrict__ grad_rows, int32_t ld, float* __restrict__ grad2d, float* __restrict__ grad_norm) {
     using L = RowLayout<DEG>;
@@ -799,6 +848,17 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
         }
     }
     if (!valid) return;
+    {
+        // moments -> 2D gradient, with the conic the pixels used; fp64 because
+        // A m_x and B m_y can nearly cancel for elongated footprints
+        const float4 co = conic_op[id];
+        const double mx = g2[0], my = g2[1];
+        g2[0] = (float)((double)co.x * mx + (double)co.y * my);
+        g2[1] = (float)((double)co.y * mx + (double)co.z * my);
+        g2[2] = 0.5f * g2[2];
+        g2[4] = 0.5f * g2[4];
+        g2[5] = co.w > 0.0f ? -g2[5] / co.w : 0.0f;
+    }
     if (grad2d) {
 #pragma unroll
         for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
@@ -933,8 +993,9 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
     const dim3 grid(div_up(scene.n, GS_BLOCK));
 #define GS_LAUNCH_PBWD(D)                                                                                        \
     hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset,  \
-                       slots, capacity, proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, \
-                       cam, grad_rows, grad_ld, grad2d, grad_norm)
+                       slots, capacity, reinterpret_cast<const float4*>(proj.conic_opacity), proj.clamp,          \
+                       scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam, grad_rows, grad_ld,  \
+                       grad2d, grad_norm)
     switch (scene.sh_degree) {
         case 0: GS_LAUNCH_PBWD(0); break;
         case 1: GS_LAUNCH_PBWD(1); break;
