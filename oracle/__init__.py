@@ -500,3 +500,121 @@ def train_view(scene, cam, target, m_groups, v_groups, step, lr=1e-3, beta1=0.9,
         tm["pack"] = time.perf_counter() - t0
     return ViewResult(proj, vis, keys, vals, ranges, rnd, loss, dL, lm, grad2d, flag, grads, newp, newm, newv,
                       deltas, msg, tm)
+
+
+# ---------------------------------------------------------------------------
+# primitive scopes: hazard sets and throughput-first admission (Section 4.3)
+# ---------------------------------------------------------------------------
+# Scopes are sets of primitive ids (Section 2.1: the dependency unit is the
+# primitive index).  Here they are plain Python sets built from id arrays; the
+# results are returned as ascending uint32 arrays.
+
+GATE_NO_DELAY = 0        # D+ is empty: there is no RAW wait to admit
+GATE_ADMIT = 1           # both admission tests pass: B may read the last published versions
+GATE_WAIT_RHO = 2        # |D+| / |R+(B)| > tau
+GATE_WAIT_NO_ACTIVE = 3  # C_A is empty: the gradient gate cannot be evaluated
+GATE_WAIT_MISSING = 4    # a delayed primitive has no producer evidence
+GATE_WAIT_SECOND = 5     # a delayed primitive already carries another producer's skipped update
+GATE_WAIT_GRADIENT = 6   # a delayed primitive's ||g_A|| exceeds tau times the active-set mean
+
+
+def _idset(a):
+    return set(int(x) for x in np.asarray(a, np.int64).reshape(-1))
+
+
+def _sorted_u32(s):
+    return np.array(sorted(s), dtype=np.uint32)
+
+
+def scope_conflicts(RA, WA, RB, WB):
+    """Quality-first primitive-state hazards between an earlier unit A and a
+    later unit B (Section 4.3, "Quality-first path"), from their conservative
+    read and update scopes:
+        C_WAW = W+(B) & W+(A)
+        C_RAW = (R+(B) - W+(B)) & W+(A)
+        C_WAR = W+(B) & (R+(A) - W+(A))
+    Returns (waw, raw, war) as ascending id arrays."""
+    RA, WA, RB, WB = (_idset(x) for x in (RA, WA, RB, WB))
+    waw = WB & WA
+    raw = (RB - WB) & WA
+    war = WB & (RA - WA)
+    if _MUT == 8:
+        raw = RB & WA                      # planted: B's own update scope not excluded
+    if _MUT == 9:
+        war = WA & (RB - WB)               # planted: A and B swapped
+    return _sorted_u32(waw), _sorted_u32(raw), _sorted_u32(war)
+
+
+@dataclasses.dataclass
+class GateResult:
+    admit: int
+    reason: int
+    n_delayed: int
+    n_read: int
+    n_active: int
+    n_missing: int
+    n_second: int
+    rho: float
+    mean_g: float
+    max_g: float
+    threshold: float
+
+
+def admission_gate(RB, D, CA, g, tau, evidence=None, skip=None, producer_version=0):
+    """Throughput-first admission of a delayed read (Section 4.3,
+    "Throughput-first path") for the delayed-read set D = C_RAW(A, B).
+
+      * D empty (which includes an empty R+(B)): nothing to admit (GATE_NO_DELAY);
+      * rho = |D| / |R+(B)| must not exceed tau;
+      * the gradient gate needs a non-empty active set C_A and producer
+        evidence for every delayed primitive (`evidence`: the ids whose
+        ||g_A|| the producer reported; None means C_A);
+      * publication metadata (`skip`, per primitive: the version of a pending
+        update an admitted read has already skipped, 0 if none) must show no
+        other producer's skipped update on a delayed primitive, so a read
+        skips at most one unpublished update;
+      * every delayed p needs ||g_A(p)|| <= tau * (1/|C_A|) sum_{q in C_A} ||g_A(q)||.
+    Tests are taken in the order listed; the first that fails names the reason.
+    g is indexed by primitive id.  The sum is exact (math.fsum), the mean and
+    the threshold are then rounded to fp64 once each.
+
+    Returns (GateResult, skip'): on admission skip'[p] = producer_version for
+    every p in D; otherwise skip' equals skip."""
+    import math
+    RB, D, CA = _idset(RB), _idset(D), _idset(CA)
+    E = CA if evidence is None else _idset(evidence)
+    g = np.asarray(g, np.float32)
+    nD, nR, nC = len(D), len(RB), len(CA)
+    rho = (nD / nR) if nR > 0 else 0.0
+    missing = sum(1 for p in D if p not in E)
+    second = 0
+    if skip is not None:
+        second = sum(1 for p in D if int(skip[p]) != 0 and int(skip[p]) != int(producer_version))
+    sum_g = math.fsum(float(g[q]) for q in CA)
+    mean_g = sum_g / nC if nC > 0 else 0.0
+    if _MUT == 10 and nD > 0:
+        mean_g = math.fsum(float(g[q]) for q in D) / nD     # planted: mean over the delayed set
+    thr = float(tau) * mean_g
+    max_g = max((float(g[p]) for p in D), default=0.0)
+    if nD == 0:
+        reason = GATE_NO_DELAY
+    elif rho > tau or (_MUT == 11 and rho >= tau):
+        reason = GATE_WAIT_RHO
+    elif nC == 0:
+        reason = GATE_WAIT_NO_ACTIVE
+    elif missing:
+        reason = GATE_WAIT_MISSING
+    elif second and _MUT != 12:
+        reason = GATE_WAIT_SECOND
+    elif max_g > thr:
+        reason = GATE_WAIT_GRADIENT
+    else:
+        reason = GATE_ADMIT
+    admit = 1 if reason in (GATE_NO_DELAY, GATE_ADMIT) else 0
+    new_skip = None
+    if skip is not None:
+        new_skip = np.array(skip, np.uint32, copy=True)
+        if reason == GATE_ADMIT:
+            for p in D:
+                new_skip[p] = producer_version
+    return GateResult(admit, reason, nD, nR, nC, missing, second, rho, mean_g, max_g, thr), new_skip
