@@ -139,7 +139,8 @@ enum {
     GS_WS_VISIBLE_SET = 1,
     GS_WS_BIN_SORT = 2,
     GS_WS_RASTER_BWD = 3,
-    GS_WS_LOSS = 4
+    GS_WS_LOSS = 4,
+    GS_WS_SCOPE = 5
 };
 /*
  * Workspace bytes a call needs, for a pool of n primitives, a pair capacity
@@ -172,12 +173,13 @@ gs_status gs_project(const gs_scene* scene, const gs_camera* cam, const gs_proj*
  * result is the projection-visible set (a superset of the realized active
  * set C_i of Section 2.1); with the active flags of gs_raster_fwd it is C_i
  * itself; any caller mask works the same way.
- *   kind: GS_PRED_U32_NONZERO (src is uint32[n]) or GS_PRED_U8_NONZERO (uint8[n])
+ *   kind: GS_PRED_U32_NONZERO (src is uint32[n]), GS_PRED_U8_NONZERO (uint8[n])
+ *     or GS_PRED_BITMAP (src is a scope bitmap, see gs_scope_from_ids)
  *   out_idx [n] uint32 (the first *out_count entries are written)
  *   out_count: one uint32 on the device
  *   ws: gs_workspace_bytes(GS_WS_VISIBLE_SET, n, 0, 0, 0) bytes
  */
-enum { GS_PRED_U32_NONZERO = 0, GS_PRED_U8_NONZERO = 1 };
+enum { GS_PRED_U32_NONZERO = 0, GS_PRED_U8_NONZERO = 1, GS_PRED_BITMAP = 2 };
 gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count,
                          void* ws, size_t ws_bytes, void* stream);
 
@@ -366,6 +368,116 @@ enum { GS_APPLY_ADD = 0, GS_APPLY_OVERWRITE = 1 };
 gs_status gs_delta_apply(const void* msg, size_t msg_capacity, const gs_group* dst, int32_t n_groups, int32_t n_rows,
                          int32_t max_rows, int32_t mode, uint32_t* prim_version, gs_device_status* status,
                          void* stream);
+
+/*
+ * Primitive scopes (Section 2.1: the dependency unit is the primitive index;
+ * a task unit's conservative read and update scopes R+ and W+, its realized
+ * active set C and gradient evidence g).  A scope is a bitmap over primitive
+ * ids: bit (i & 31) of uint32 word (i >> 5), GS_SCOPE_WORDS(n) words, device
+ * memory.  Bits at or beyond n are ignored on input and written as 0.
+ *
+ * gs_scope_from_ids: the scope of ids idx[0 .. min(*count, max_rows)) (any
+ * order; ids >= n are ignored).  accumulate = 0 clears the scope first,
+ * accumulate = 1 adds the ids to it (the union over a task unit's views,
+ * R+(U) = union of R+_i, Section 2.1).  count is one uint32 on the device.
+ * gs_scope_from_pred: the same from a per-primitive predicate array
+ * (GS_PRED_U32_NONZERO: uint32[n], GS_PRED_U8_NONZERO: uint8[n]), e.g. the
+ * tile counts of gs_project (projection-visible scope) or the active flags of
+ * gs_raster_fwd (realized active set).
+ * Errors: GS_ERR_INVALID_ARG for null pointers, n < 0, a bad kind.
+ */
+#define GS_SCOPE_WORDS(n) (((uint32_t)(n) + 31u) / 32u)
+gs_status gs_scope_from_ids(const uint32_t* idx, const uint32_t* count, int32_t max_rows, int32_t n,
+                            int32_t accumulate, uint32_t* scope, void* stream);
+gs_status gs_scope_from_pred(int32_t kind, const void* src, int32_t n, int32_t accumulate, uint32_t* scope,
+                             void* stream);
+
+/*
+ * Quality-first primitive-state hazards (Section 4.3, "Quality-first path")
+ * between an earlier task unit A and a later unit B:
+ *   C_WAW = W+(B) & W+(A)
+ *   C_RAW = (R+(B) \ W+(B)) & W+(A)
+ *   C_WAR = W+(B) & (R+(A) \ W+(A))
+ * RAW and WAW ids wait for A's publication, WAR ids for the end of A's
+ * state-observing phase; with all three empty B may proceed.
+ *   RA, WA, RB, WB: the four scopes (bitmaps of GS_SCOPE_WORDS(n) words)
+ *   waw, raw, war: output bitmaps, each may be NULL
+ *   waw_idx, raw_idx, war_idx: the same sets as ascending ids ([n] uint32
+ *     each, the first count entries written), each may be NULL
+ *   counts: 4 uint32 on the device: |C_WAW|, |C_RAW|, |C_WAR|, |R+(B)|
+ *   ws: gs_workspace_bytes(GS_WS_SCOPE, n, 0, 0, 0) bytes
+ * Errors: GS_ERR_INVALID_ARG for a null scope, counts or workspace, n < 0;
+ * GS_ERR_WORKSPACE.
+ */
+gs_status gs_scope_conflicts(const uint32_t* RA, const uint32_t* WA, const uint32_t* RB, const uint32_t* WB,
+                             int32_t n, uint32_t* waw, uint32_t* raw, uint32_t* war, uint32_t* waw_idx,
+                             uint32_t* raw_idx, uint32_t* war_idx, uint32_t* counts, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/*
+ * Throughput-first admission of B's delayed reads (Section 4.3,
+ * "Throughput-first path") for the delayed-read set D+ = C_RAW(A, B).  The
+ * tests, in this order (the first that fails names the reason):
+ *   D+ empty (also when R+(B) is empty): nothing to admit -> GS_GATE_NO_DELAY
+ *   rho = |D+| / |R+(B)| <= tau                       else GS_GATE_WAIT_RHO
+ *   C_A non-empty                                     else GS_GATE_WAIT_NO_ACTIVE
+ *   every delayed id has producer evidence            else GS_GATE_WAIT_MISSING
+ *   no delayed id's publication metadata names another producer's skipped
+ *   update (a read skips at most one unpublished update)  else GS_GATE_WAIT_SECOND
+ *   max over D+ of ||g_A(p)|| <= tau * mean over C_A of ||g_A(q)||
+ *                                                     else GS_GATE_WAIT_GRADIENT
+ *   -> GS_GATE_ADMIT
+ * rho, the mean (an fp64 sum of the fp32 magnitudes) and the threshold are
+ * formed in fp64.  On GS_GATE_ADMIT, skip[p] = producer_version for every p in
+ * D+ (the per-primitive publication metadata; gs_delta_apply_versioned clears
+ * it when that version is published).
+ *   RB, D: scopes (bitmaps); args->active: the scope C_A; args->evidence: the
+ *     scope of ids whose ||g_A|| the producer reported, or NULL for C_A;
+ *     args->g: [n] fp32 ||g_A(p)|| by id (finite, >= 0; read at ids in C_A or
+ *     D+ only; gs_raster_bwd's grad_norm is this for the visible ids);
+ *     args->skip: [n] uint32 metadata, or NULL (no metadata: that test passes
+ *     and nothing is stamped); args->tau in [0, 1]
+ *   result: one gs_gate_result in device memory
+ *   ws: gs_workspace_bytes(GS_WS_SCOPE, n, 0, 0, 0) bytes
+ * Errors: GS_ERR_INVALID_ARG for null pointers, n < 0, tau outside [0, 1],
+ * skip without a non-zero producer_version; GS_ERR_WORKSPACE.
+ */
+enum {
+    GS_GATE_NO_DELAY = 0,
+    GS_GATE_ADMIT = 1,
+    GS_GATE_WAIT_RHO = 2,
+    GS_GATE_WAIT_NO_ACTIVE = 3,
+    GS_GATE_WAIT_MISSING = 4,
+    GS_GATE_WAIT_SECOND = 5,
+    GS_GATE_WAIT_GRADIENT = 6
+};
+
+typedef struct {
+    const uint32_t* active;
+    const uint32_t* evidence;
+    const float* g;
+    uint32_t* skip;
+    uint32_t producer_version;
+    double tau;
+} gs_gate_args;
+
+typedef struct {
+    uint32_t admit;           /* 1 for GS_GATE_NO_DELAY and GS_GATE_ADMIT */
+    uint32_t reason;          /* GS_GATE_* */
+    uint32_t n_read;          /* |R+(B)| */
+    uint32_t n_delayed;       /* |D+| */
+    uint32_t n_active;        /* |C_A| */
+    uint32_t n_missing;       /* delayed ids without evidence */
+    uint32_t n_second;        /* delayed ids whose metadata names another producer */
+    uint32_t reserved;
+    double rho;               /* |D+| / |R+(B)|, 0 if R+(B) is empty */
+    double mean_g;            /* mean of ||g_A|| over C_A, 0 if empty */
+    double max_g;             /* max of ||g_A|| over D+, 0 if empty */
+    double threshold;         /* tau * mean_g */
+} gs_gate_result;
+
+gs_status gs_admission_gate(const uint32_t* RB, const uint32_t* D, const gs_gate_args* args, int32_t n,
+                            gs_gate_result* result, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

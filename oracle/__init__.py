@@ -618,3 +618,20 @@ def admission_gate(RB, D, CA, g, tau, evidence=None, skip=None, producer_version
             for p in D:
                 new_skip[p] = producer_version
     return GateResult(admit, reason, nD, nR, nC, missing, second, rho, mean_g, max_g, thr), new_skip
+
+
+def scope_bitmap(ids, n):
+    """A set of ids as uint32 words, bit (i & 31) of word (i >> 5), ids >= n
+    dropped (the scope layout of the C boundary; used to compare with it)."""
+    ids = np.asarray(ids, np.int64).reshape(-1)
+    ids = ids[(ids >= 0) & (ids < n)]
+    words = np.zeros((int(n) + 31) // 32, np.uint32)
+    np.bitwise_or.at(words, ids >> 5, (np.uint32(1) << (ids & 31).astype(np.uint32)))
+    return words
+
+
+def scope_ids(words, n):
+    """Inverse of scope_bitmap: the ascending ids whose bit is set (ids < n)."""
+    words = np.asarray(words, np.uint32)
+    bits = ((words[:, None] >> np.arange(32, dtype=np.uint32)[None, :]) & 1).reshape(-1)
+    return np.flatnonzero(bits[:int(n)]).astype(np.uint32)

@@ -20,7 +20,8 @@ OUT = os.path.join(HERE, "libgsmi.so")
 BUILD_DIR = os.path.join(os.path.dirname(HERE), "_build", "gsmi")
 ARCH = os.environ.get("GSMI_ARCH", "gfx950")
 
-SOURCES = ["project.hip", "compact.hip", "binsort.hip", "raster.hip", "adam.hip", "delta.hip", "abi.cpp"]
+SOURCES = ["project.hip", "compact.hip", "binsort.hip", "raster.hip", "adam.hip", "delta.hip", "scope.hip",
+           "abi.cpp"]
 STRICT_FP = {"project.hip", "adam.hip"}
 
 

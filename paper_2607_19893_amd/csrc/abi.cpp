@@ -103,6 +103,7 @@ size_t gs_workspace_bytes(int32_t which, int32_t n, uint32_t capacity, int32_t w
         case GS_WS_BIN_SORT: return gsmi::binsort_ws_bytes(n, capacity, width, height);
         case GS_WS_RASTER_BWD: return gsmi::raster_bwd_ws_bytes(n, capacity);
         case GS_WS_LOSS: return gsmi::loss_ws_bytes(width, height);
+        case GS_WS_SCOPE: return gsmi::scope_ws_bytes(n);
         default: return 0;
     }
 }
@@ -123,12 +124,14 @@ gs_status gs_project(const gs_scene* scene, const gs_camera* cam, const gs_proj*
 
 gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count, void* ws,
                          size_t ws_bytes, void* stream) {
-    GS_REQUIRE(kind == GS_PRED_U32_NONZERO || kind == GS_PRED_U8_NONZERO, "gs_visible_set: bad kind %d", kind);
+    GS_REQUIRE(kind == GS_PRED_U32_NONZERO || kind == GS_PRED_U8_NONZERO || kind == GS_PRED_BITMAP,
+               "gs_visible_set: bad kind %d", kind);
     GS_REQUIRE(n >= 0, "gs_visible_set: n < 0");
     GS_REQUIRE(out_count != nullptr, "gs_visible_set: null out_count");
     if (n > 0) {
         GS_REQUIRE(src && out_idx && ws, "gs_visible_set: null pointer");
-        GS_REQUIRE(aligned(src, kind == GS_PRED_U32_NONZERO ? 16 : 8), "gs_visible_set: src misaligned");
+        GS_REQUIRE(aligned(src, kind == GS_PRED_U32_NONZERO ? 16 : (kind == GS_PRED_BITMAP ? 4 : 8)),
+                   "gs_visible_set: src misaligned");
     }
     if (ws_bytes < gsmi::visible_ws_bytes(n)) return fail(GS_ERR_WORKSPACE, "gs_visible_set: workspace too small");
     return hip_status(gsmi::launch_visible(kind, src, n, out_idx, out_count, ws, static_cast<hipStream_t>(stream)),
@@ -337,6 +340,54 @@ gs_status gs_delta_apply(const void* msg, size_t msg_capacity, const gs_group* d
     return hip_status(gsmi::launch_delta_apply(msg, msg_capacity, dst, n_groups, n_rows, max_rows, mode, prim_version, status,
                                                static_cast<hipStream_t>(stream)),
                       "gs_delta_apply");
+}
+
+gs_status gs_scope_from_ids(const uint32_t* idx, const uint32_t* count, int32_t max_rows, int32_t n,
+                            int32_t accumulate, uint32_t* scope, void* stream) {
+    GS_REQUIRE(n >= 0 && max_rows >= 0, "gs_scope_from_ids: negative size");
+    if (n == 0) return ok();
+    GS_REQUIRE(scope != nullptr, "gs_scope_from_ids: null scope");
+    GS_REQUIRE(max_rows == 0 || (idx && count), "gs_scope_from_ids: null idx / count");
+    return hip_status(gsmi::launch_scope_from_ids(idx, count, max_rows, n, accumulate != 0, scope,
+                                                  static_cast<hipStream_t>(stream)),
+                      "gs_scope_from_ids");
+}
+
+gs_status gs_scope_from_pred(int32_t kind, const void* src, int32_t n, int32_t accumulate, uint32_t* scope,
+                             void* stream) {
+    GS_REQUIRE(kind == GS_PRED_U32_NONZERO || kind == GS_PRED_U8_NONZERO, "gs_scope_from_pred: bad kind %d", kind);
+    GS_REQUIRE(n >= 0, "gs_scope_from_pred: n < 0");
+    if (n == 0) return ok();
+    GS_REQUIRE(src && scope, "gs_scope_from_pred: null pointer");
+    return hip_status(gsmi::launch_scope_from_pred(kind, src, n, accumulate != 0, scope,
+                                                   static_cast<hipStream_t>(stream)),
+                      "gs_scope_from_pred");
+}
+
+gs_status gs_scope_conflicts(const uint32_t* RA, const uint32_t* WA, const uint32_t* RB, const uint32_t* WB,
+                             int32_t n, uint32_t* waw, uint32_t* raw, uint32_t* war, uint32_t* waw_idx,
+                             uint32_t* raw_idx, uint32_t* war_idx, uint32_t* counts, void* ws, size_t ws_bytes,
+                             void* stream) {
+    GS_REQUIRE(n >= 0, "gs_scope_conflicts: n < 0");
+    GS_REQUIRE(counts != nullptr, "gs_scope_conflicts: null counts");
+    if (n > 0) GS_REQUIRE(RA && WA && RB && WB && ws, "gs_scope_conflicts: null scope or workspace");
+    if (ws_bytes < gsmi::scope_ws_bytes(n)) return fail(GS_ERR_WORKSPACE, "gs_scope_conflicts: workspace too small");
+    return hip_status(gsmi::launch_scope_conflicts(RA, WA, RB, WB, n, waw, raw, war, waw_idx, raw_idx, war_idx,
+                                                   counts, ws, static_cast<hipStream_t>(stream)),
+                      "gs_scope_conflicts");
+}
+
+gs_status gs_admission_gate(const uint32_t* RB, const uint32_t* D, const gs_gate_args* args, int32_t n,
+                            gs_gate_result* result, void* ws, size_t ws_bytes, void* stream) {
+    GS_REQUIRE(n >= 0, "gs_admission_gate: n < 0");
+    GS_REQUIRE(args != nullptr && result != nullptr && ws != nullptr, "gs_admission_gate: null pointer");
+    GS_REQUIRE(args->tau >= 0.0 && args->tau <= 1.0, "gs_admission_gate: tau outside [0, 1]");
+    GS_REQUIRE(args->skip == nullptr || args->producer_version != 0,
+               "gs_admission_gate: metadata given without a producer version");
+    if (n > 0) GS_REQUIRE(RB && D && args->active && args->g, "gs_admission_gate: null scope or evidence");
+    if (ws_bytes < gsmi::scope_ws_bytes(n)) return fail(GS_ERR_WORKSPACE, "gs_admission_gate: workspace too small");
+    return hip_status(gsmi::launch_admission_gate(RB, D, *args, n, result, ws, static_cast<hipStream_t>(stream)),
+                      "gs_admission_gate");
 }
 
 }  // extern "C"

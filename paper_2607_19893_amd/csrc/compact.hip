@@ -1,5 +1,5 @@
 // Scope extraction: ordered (ascending) stream compaction of a per-primitive
-// predicate, plus the small device-wide scan used by several passes.
+// predicate (a uint32 or uint8 array, or a scope bitmap), plus the small device-wide scan used by several passes.
 //
 // Three launches: per-block counts (blocked arrangement, 2048 items per
 // block), one single-workgroup exclusive scan of the block counts, and the
@@ -24,6 +24,11 @@ __device__ __forceinline__ void load_pred(const void* src, int32_t n, int32_t ba
 #pragma unroll
             for (int k = 0; k < GS_ITEMS; ++k) on[k] = (base + k < n) ? (s[base + k] != 0) : 0;
         }
+    } else if (KIND == GS_PRED_BITMAP) {
+        // bit i & 31 of word i >> 5; base is a multiple of 8, so the 8 items share a word
+        const uint32_t word = base < n ? static_cast<const uint32_t*>(src)[base >> 5] >> (base & 31) : 0u;
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) on[k] = (base + k < n) ? ((word >> k) & 1u) : 0u;
     } else {
         const uint8_t* s = static_cast<const uint8_t*>(src);
         if (base + GS_ITEMS <= n) {
@@ -131,6 +136,8 @@ hipError_t launch_visible(int kind, const void* src, int32_t n, uint32_t* out_id
     if (nb == 0) return launch_fill_u32(out_count, 0u, 1, st);
     if (kind == GS_PRED_U32_NONZERO)
         hipLaunchKernelGGL(k_vis_count<GS_PRED_U32_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
+    else if (kind == GS_PRED_BITMAP)
+        hipLaunchKernelGGL(k_vis_count<GS_PRED_BITMAP>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
     else
         hipLaunchKernelGGL(k_vis_count<GS_PRED_U8_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
     hipError_t e = hipGetLastError();
@@ -139,6 +146,9 @@ hipError_t launch_visible(int kind, const void* src, int32_t n, uint32_t* out_id
     if (e != hipSuccess) return e;
     if (kind == GS_PRED_U32_NONZERO)
         hipLaunchKernelGGL(k_vis_scatter<GS_PRED_U32_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,
+                           out_idx);
+    else if (kind == GS_PRED_BITMAP)
+        hipLaunchKernelGGL(k_vis_scatter<GS_PRED_BITMAP>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,
                            out_idx);
     else
         hipLaunchKernelGGL(k_vis_scatter<GS_PRED_U8_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,

@@ -63,6 +63,18 @@ hipError_t launch_sparse_adam_publish(const gs_adam_group* groups, int32_t n_gro
                                       double beta1, double beta2, double eps, uint32_t version, void* msg,
                                       size_t msg_capacity, gs_device_status* status, hipStream_t st);
 
+// scope.hip
+size_t scope_ws_bytes(int32_t n);
+hipError_t launch_scope_from_ids(const uint32_t* idx, const uint32_t* count, int32_t max_rows, int32_t n,
+                                 int32_t accumulate, uint32_t* scope, hipStream_t st);
+hipError_t launch_scope_from_pred(int kind, const void* src, int32_t n, int32_t accumulate, uint32_t* scope,
+                                  hipStream_t st);
+hipError_t launch_scope_conflicts(const uint32_t* RA, const uint32_t* WA, const uint32_t* RB, const uint32_t* WB,
+                                  int32_t n, uint32_t* waw, uint32_t* raw, uint32_t* war, uint32_t* waw_idx,
+                                  uint32_t* raw_idx, uint32_t* war_idx, uint32_t* counts, void* ws, hipStream_t st);
+hipError_t launch_admission_gate(const uint32_t* RB, const uint32_t* D, const gs_gate_args& a, int32_t n,
+                                 gs_gate_result* result, void* ws, hipStream_t st);
+
 // delta.hip
 size_t delta_msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups);
 hipError_t launch_delta_pack(const uint32_t* idx, const uint32_t* count, int32_t max_rows, const gs_group* src,

@@ -23,8 +23,10 @@ P = ctypes.c_void_p
 i32, u32, i64, f32, sz = ctypes.c_int32, ctypes.c_uint32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
 
 GS_OK, GS_ERR_INVALID_ARG, GS_ERR_UNSUPPORTED, GS_ERR_WORKSPACE, GS_ERR_HIP = range(5)
-GS_WS_VISIBLE_SET, GS_WS_BIN_SORT, GS_WS_RASTER_BWD, GS_WS_LOSS = 1, 2, 3, 4
-GS_PRED_U32_NONZERO, GS_PRED_U8_NONZERO = 0, 1
+GS_WS_VISIBLE_SET, GS_WS_BIN_SORT, GS_WS_RASTER_BWD, GS_WS_LOSS, GS_WS_SCOPE = 1, 2, 3, 4, 5
+GS_PRED_U32_NONZERO, GS_PRED_U8_NONZERO, GS_PRED_BITMAP = 0, 1, 2
+(GS_GATE_NO_DELAY, GS_GATE_ADMIT, GS_GATE_WAIT_RHO, GS_GATE_WAIT_NO_ACTIVE, GS_GATE_WAIT_MISSING, GS_GATE_WAIT_SECOND,
+ GS_GATE_WAIT_GRADIENT) = range(7)
 GS_APPLY_ADD, GS_APPLY_OVERWRITE = 0, 1
 GS_DEV_PAIR_OVERFLOW, GS_DEV_MSG_OVERFLOW, GS_DEV_MSG_MISMATCH = 1, 2, 4
 GS_MSG_MAGIC = 0x47534D31
@@ -55,6 +57,22 @@ class gs_group(ctypes.Structure):
     _fields_ = [("ptr", P), ("cols", i32)]
 
 
+class gs_gate_args(ctypes.Structure):
+    _fields_ = [("active", P), ("evidence", P), ("g", P), ("skip", P), ("producer_version", u32),
+                ("tau", ctypes.c_double)]
+
+
+class gs_gate_result(ctypes.Structure):
+    """Mirror of the device-side result record (64 bytes)."""
+    _fields_ = [("admit", u32), ("reason", u32), ("n_read", u32), ("n_delayed", u32), ("n_active", u32),
+                ("n_missing", u32), ("n_second", u32), ("reserved", u32), ("rho", ctypes.c_double),
+                ("mean_g", ctypes.c_double), ("max_g", ctypes.c_double), ("threshold", ctypes.c_double)]
+
+
+def scope_words(n) -> int:
+    return (int(n) + 31) // 32
+
+
 _lib.gs_abi_version.restype = i32
 _lib.gs_status_string.restype = ctypes.c_char_p
 _lib.gs_status_string.argtypes = [i32]
@@ -80,15 +98,21 @@ _lib.gs_sparse_adam_publish.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P
                                         ctypes.c_double, ctypes.c_double, ctypes.c_double, u32, P, sz, P, P]
 _lib.gs_delta_pack.argtypes = [P, P, i32, ctypes.POINTER(gs_group), i32, u32, P, sz, P, P]
 _lib.gs_delta_apply.argtypes = [P, sz, ctypes.POINTER(gs_group), i32, i32, i32, i32, P, P, P]
+_lib.gs_scope_from_ids.argtypes = [P, P, i32, i32, i32, P, P]
+_lib.gs_scope_from_pred.argtypes = [i32, P, i32, i32, P, P]
+_lib.gs_scope_conflicts.argtypes = [P, P, P, P, i32, P, P, P, P, P, P, P, P, sz, P]
+_lib.gs_admission_gate.argtypes = [P, P, ctypes.POINTER(gs_gate_args), i32, P, P, sz, P]
 for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
               "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
-              "gs_delta_pack", "gs_delta_apply"):
+              "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
+              "gs_admission_gate"):
     getattr(_lib, _name).restype = i32
 
 EXPORTS = ["gs_abi_version", "gs_status_string", "gs_last_error", "gs_workspace_bytes", "gs_delta_msg_bytes",
            "gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
            "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
-           "gs_delta_pack", "gs_delta_apply"]
+           "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
+           "gs_admission_gate"]
 
 
 class GsmiError(RuntimeError):
@@ -275,6 +299,44 @@ def gs_delta_apply(msg, groups_arr, n_groups, n_rows, max_rows, mode, prim_versi
                                                         int(n_groups), int(n_rows),
                                                         int(max_rows), int(mode), ptr(prim_version), ptr(status),
                                                         stream if stream is not None else current_stream()))
+
+
+def gs_scope_from_ids(idx, count, max_rows, n, accumulate, scope, stream=None):
+    return _check("gs_scope_from_ids", _lib.gs_scope_from_ids(ptr(idx), ptr(count), int(max_rows), int(n),
+                                                              int(accumulate), ptr(scope),
+                                                              stream if stream is not None else current_stream()))
+
+
+def gs_scope_from_pred(kind, src, n, accumulate, scope, stream=None):
+    return _check("gs_scope_from_pred", _lib.gs_scope_from_pred(int(kind), ptr(src), int(n), int(accumulate),
+                                                                ptr(scope),
+                                                                stream if stream is not None else current_stream()))
+
+
+def gs_scope_conflicts(RA, WA, RB, WB, n, waw, raw_, war, waw_idx, raw_idx, war_idx, counts, ws, stream=None):
+    return _check("gs_scope_conflicts", _lib.gs_scope_conflicts(
+        ptr(RA), ptr(WA), ptr(RB), ptr(WB), int(n), ptr(waw), ptr(raw_), ptr(war), ptr(waw_idx), ptr(raw_idx),
+        ptr(war_idx), ptr(counts), ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
+        stream if stream is not None else current_stream()))
+
+
+def make_gate_args(active, g, tau, evidence=None, skip=None, producer_version=0) -> gs_gate_args:
+    return gs_gate_args(ptr(active), ptr(evidence), ptr(g), ptr(skip), int(producer_version), float(tau))
+
+
+def gs_admission_gate(RB, D, args: gs_gate_args, n, result, ws, stream=None):
+    """result: a device tensor of >= 64 bytes (see gate_result_from)."""
+    return _check("gs_admission_gate", _lib.gs_admission_gate(
+        ptr(RB), ptr(D), ctypes.byref(args), int(n), ptr(result), ptr(ws),
+        ws.numel() * ws.element_size() if ws is not None else 0,
+        stream if stream is not None else current_stream()))
+
+
+def gate_result_from(buf) -> gs_gate_result:
+    """Decode a result record copied to the host (bytes-like or a tensor)."""
+    if hasattr(buf, "cpu"):
+        buf = buf.detach().cpu().numpy().tobytes()
+    return gs_gate_result.from_buffer_copy(bytes(buf)[:ctypes.sizeof(gs_gate_result)])
 
 
 def raw():

@@ -77,6 +77,27 @@ def test_null_and_range_arguments_rejected(gs):
     assert L.gs_delta_apply(16, 8, g, 1, 10, 10, 0, None, 16, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_delta_pack(16, 16, 10, g, 1, 1, 8, 1024, 16, None) == gs.GS_ERR_INVALID_ARG  # misaligned msg
     assert L.gs_loss_l1(None, None, 4, 4, None, None, None, 0, None) == gs.GS_ERR_INVALID_ARG
+    # scopes, hazards and admission
+    assert L.gs_scope_from_ids(None, None, 5, 100, 0, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_scope_from_ids(16, 16, 5, -1, 0, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_scope_from_pred(5, 16, 100, 0, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_scope_from_pred(0, None, 100, 0, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_scope_conflicts(16, 16, 16, 16, 100, None, None, None, None, None, None, None, 16, 1 << 20,
+                                None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_scope_conflicts(16, 16, 16, None, 100, None, None, None, None, None, None, 16, 16, 1 << 20,
+                                None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_scope_conflicts(16, 16, 16, 16, 1 << 20, None, None, None, None, None, None, 16, 16, 0,
+                                None) == gs.GS_ERR_WORKSPACE
+    args = gs.gs_gate_args(16, None, 16, None, 0, 1.5)
+    assert L.gs_admission_gate(16, 16, ctypes.byref(args), 100, 16, 16, 1 << 20, None) == gs.GS_ERR_INVALID_ARG
+    assert "tau" in gs.gs_last_error()
+    args = gs.gs_gate_args(16, None, 16, 16, 0, 0.2)
+    assert L.gs_admission_gate(16, 16, ctypes.byref(args), 100, 16, 16, 1 << 20, None) == gs.GS_ERR_INVALID_ARG
+    assert "producer version" in gs.gs_last_error()
+    args = gs.gs_gate_args(None, None, 16, None, 0, 0.2)
+    assert L.gs_admission_gate(16, 16, ctypes.byref(args), 100, 16, 16, 1 << 20, None) == gs.GS_ERR_INVALID_ARG
+    args = gs.gs_gate_args(16, None, 16, None, 0, 0.2)
+    assert L.gs_admission_gate(16, 16, ctypes.byref(args), 1 << 20, 16, 16, 0, None) == gs.GS_ERR_WORKSPACE
 
 
 def test_workspace_sizes_monotone(gs):
@@ -88,6 +109,7 @@ def test_workspace_sizes_monotone(gs):
     assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 1000, 100) >= 12 * 4 * 100
     assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 0, 5000) > gs.gs_workspace_bytes(gs.GS_WS_RASTER_BWD, 0, 100)
     assert gs.gs_workspace_bytes(99, 10, 10) == 0
+    assert 0 < gs.gs_workspace_bytes(gs.GS_WS_SCOPE, 100) <= gs.gs_workspace_bytes(gs.GS_WS_SCOPE, 10_000_000)
 
 
 def test_message_size_matches_oracle_layout(gs, orc):

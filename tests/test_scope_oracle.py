@@ -219,3 +219,13 @@ def test_scope_planted_mistake_is_caught(orc, k):
             SCOPE_MUTATIONS[k](orc)
     finally:
         orc.set_mutation(0)
+
+
+def test_bitmap_layout_round_trip(orc):
+    # bit i & 31 of word i >> 5: id 0 is the lowest bit of word 0, id 33 bit 1 of word 1
+    w = orc.scope_bitmap([0, 33, 63, 64], 70)
+    assert list(w) == [1, (1 << 1) | (1 << 31), 1]
+    rng = np.random.default_rng(3)
+    for n in (1, 31, 32, 33, 1000):
+        s = np.flatnonzero(rng.random(n) < 0.3)
+        np.testing.assert_array_equal(orc.scope_ids(orc.scope_bitmap(s, n), n), s)
