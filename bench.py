@@ -131,6 +131,7 @@ def main():
 
     # pair statistics per view (untimed): evaluated / included (pixel, pair) counts
     ev_pairs, inc_pairs, vis_counts, pair_counts, w_iters, w_hits = [], [], [], [], [], []
+    front = [in_front(w.scene.mean, c) for c in cams]
     for i, c in enumerate(cams):
         tr.project(c); tr.visible(); tr.bin_sort()
         tr.pair_stats.zero_()
@@ -162,9 +163,12 @@ def main():
         views.append(v)
         tr.step(cams[v], step, version=step, target=targets[v], events=evs[k], overlap=not args.no_overlap)
     tr.flush_apply()
+    t_issued = time.perf_counter()
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     wall = t_end - t_start
+    log("host issue time %.3f ms per step (device %.3f ms per step)"
+        % (1e3 * (t_issued - t_start) / args.steps, 1e3 * wall / args.steps))
     assert to_u32(tr.status)[0] == 0, "device status flags set during the timed steps"
 
     phase_ms = np.zeros(nph)
@@ -187,28 +191,52 @@ def main():
 
     # roofline of each timed phase; the dominant one is reported
     names = list(ViewTrainer.PHASES)
+    N = w.scene.n
+    F_mean = float(np.mean([front[v] for v in views]))
+    H, Wd = cams[0].height, cams[0].width
+    T_tiles = cams[0].num_tiles
     fwd_flops = FWD_FLOP_EVAL * ev_mean + FWD_FLOP_INC * inc_mean
     bwd_flops = BWD_FLOP_EVAL * ev_mean + BWD_FLOP_INC * inc_mean
+    # projection: means of every primitive; log-scale, quaternion of those in
+    # front of the near plane; opacity + colour coefficients of the visible
+    # ones; radius + tile count of every primitive; the 2D record of the visible
+    proj_bytes = 12 * N + 28 * F_mean + 4 * (tr.row_len - 10) * V_mean + 8 * N + 40 * V_mean
+    # visible set: the per-primitive predicate read, the ids written
+    vis_bytes = 4 * N + 4 * V_mean
+    # binning as a 64-bit (tile, depth) key sort: duplication (16 B per visible
+    # primitive, 12 B per pair), LSD radix passes of 24 B per pair each (key +
+    # value, read + write), one per 11 bits of the 31 depth + ceil(log2 T) tile
+    # bits, and the range extraction (8 B per pair)
+    key_bits = 31 + int(np.ceil(np.log2(max(T_tiles, 2))))
+    sort_bytes = 16 * V_mean + 12 * M_mean + 24 * M_mean * int(np.ceil(key_bits / 11)) + 8 * M_mean
+    # loss: image and target read, dL/dimg written
+    loss_bytes = 12 * 3 * H * Wd
+    # per-primitive backward: the 48-byte pair slots, then per visible row the
+    # parameters read (4P), the 2D record and id (68 B) and the gradient row written (4P)
+    pbwd_bytes = 48 * M_mean + V_mean * (2 * row_bytes + 68)
     # Adam + staging per visible row: p, g, m, v read and p, m, v written (7 row
     # reads/writes), the message row and id written, the id read
     adam_bytes = V_mean * (8 * row_bytes + 8)
     # apply per row: message row + id read, replica row read and written, version written
     apply_bytes = V_mean * (3 * row_bytes + 8)
+    hbm = lambda b: ("hbm", b / 1e9, HBM_PEAK_GBS, "GB/s")
     roofs = {
+        "project": hbm(proj_bytes),
+        "visible": hbm(vis_bytes),
+        "bin_sort": hbm(sort_bytes),
         "raster_fwd": ("alu", fwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
+        "loss_l1": hbm(loss_bytes),
         "raster_bwd_pixels": ("alu", bwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
-        "adam_publish": ("hbm", adam_bytes / 1e9, HBM_PEAK_GBS, "GB/s"),
-        "apply": ("hbm", apply_bytes / 1e9, HBM_PEAK_GBS, "GB/s"),
+        "raster_bwd_project": hbm(pbwd_bytes),
+        "adam_publish": hbm(adam_bytes),
+        "apply": hbm(apply_bytes),
     }
     per_phase = {}
     for name, t in zip(names, phase_ms):
-        if name in roofs:
-            bound, work, peak, unit = roofs[name]
-            ach = work / (t * 1e-3)
-            per_phase[name] = {"ms": round(float(t), 4), "bound": bound, "achieved": round(ach, 2), "peak": peak,
-                               "unit": unit, "frac": round(ach / peak, 4)}
-        else:
-            per_phase[name] = {"ms": round(float(t), 4)}
+        bound, work, peak, unit = roofs[name]
+        ach = work / (t * 1e-3)
+        per_phase[name] = {"ms": round(float(t), 4), "bound": bound, "achieved": round(ach, 2), "peak": peak,
+                           "unit": unit, "frac": round(ach / peak, 4)}
     dom = max(roofs, key=lambda n: phase_ms[names.index(n)])
     bound, work, peak, unit = roofs[dom]
     ach = work / (phase_ms[names.index(dom)] * 1e-3)
@@ -247,9 +275,17 @@ def main():
                    "apply_overlapped": not args.no_overlap},
         "roofline": roofline,
         "phases_ms": {k: v["ms"] for k, v in per_phase.items()},
+        "phases_frac": {k: v["frac"] for k, v in per_phase.items()},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def in_front(mean, cam):
+    """Primitives whose camera-space depth lies beyond the near plane (the ones projection reads further)."""
+    R = np.asarray(cam.R, np.float64).reshape(3, 3)
+    z = mean.astype(np.float64) @ R[2] + float(cam.t[2])
+    return int(np.count_nonzero(z > cam.near_z))
 
 
 def copy_probe(mib):
