@@ -635,3 +635,81 @@ def scope_ids(words, n):
     words = np.asarray(words, np.uint32)
     bits = ((words[:, None] >> np.arange(32, dtype=np.uint32)[None, :]) & 1).reshape(-1)
     return np.flatnonzero(bits[:int(n)]).astype(np.uint32)
+
+
+# ---------------------------------------------------------------------------
+# versioned two-slot staging (Section 4.3, Shadow Graph steps 3-4 and the
+# per-primitive publication metadata of the throughput-first path)
+# ---------------------------------------------------------------------------
+
+COMMIT_OK = 0
+COMMIT_MISMATCH = 4      # the slot does not hold a well-formed message of this version for these groups
+COMMIT_ORDER = 8         # the version is not the one after the last committed version
+
+
+def parse_message(msg):
+    """(K, version, row_len, cols, ids, rows) of a message (see delta_message)."""
+    msg = np.asarray(msg, np.uint32)
+    K, version, row_len, ng = int(msg[1]), int(msg[2]), int(msg[3]), int(msg[4])
+    ncw = ((ng + 3) // 4) * 4
+    cols = [int(c) for c in msg[8:8 + ng]]
+    off = 8 + ncw
+    ids = msg[off:off + K].astype(np.int64)
+    r0 = (off + K + 3) // 4 * 4
+    rows = msg[r0:r0 + K * row_len].view(np.float32).reshape(K, row_len)
+    return K, version, row_len, cols, ids, rows
+
+
+def publish_commit(ring_state, slots, version, groups, mode, prim_version, skip=None, n_rows=None):
+    """Commit the update staged for `version` in slot (version & 1) of a
+    two-slot ring into a replica (Shadow Graph step 4: the produced slot is
+    committed once its publication condition holds).
+
+      * the slot must hold a message with this version, the replica's group
+        widths and ids below n_rows, else COMMIT_MISMATCH;
+      * versions are committed in order: ring_state[0] (the last committed
+        version) must be version - 1, else COMMIT_ORDER;
+      * a row is applied (ADD: one fp32 add; OVERWRITE: copy) only if the
+        primitive's published version is older than `version`, and then
+        stamped with it; rows already at or past it are left as they are;
+      * skip metadata naming this version is cleared for every row of the
+        message: the update a delayed read skipped is now published.
+    On any failure nothing changes.  Returns (groups, prim_version, skip,
+    ring_state, flags) with ring_state = [committed, applied, left, 0]."""
+    ring_state = np.array(ring_state, np.uint32, copy=True)
+    msg = np.asarray(slots[version & 1], np.uint32)
+    n_rows = int(groups[0].shape[0]) if n_rows is None else int(n_rows)
+    ok = int(msg[0]) == MSG_MAGIC and int(msg[2]) == int(version)
+    if ok:
+        K, v, row_len, cols, ids, rows = parse_message(msg)
+        ok = cols == [int(a.shape[1]) for a in groups] and bool(np.all(ids < n_rows))
+    if not ok:
+        return groups, prim_version, skip, ring_state, COMMIT_MISMATCH
+    if int(ring_state[0]) + 1 != int(version):
+        return groups, prim_version, skip, ring_state, COMMIT_ORDER
+    prim_version = np.array(prim_version, np.uint32, copy=True)
+    newer = prim_version[ids] < version
+    if _MUT == 14:
+        newer = np.ones(ids.size, bool)        # planted: published versions not checked
+    take = ids[newer]
+    out = []
+    c0 = 0
+    for a, c in zip(groups, cols):
+        a = np.array(a, np.float32, copy=True)
+        r = rows[newer, c0:c0 + c]
+        if mode == "add":
+            a[take] = (a[take].astype(np.float64) + r.astype(np.float64)).astype(np.float32)
+        else:
+            a[take] = r
+        out.append(a)
+        c0 += c
+    prim_version[take] = version
+    if skip is not None:
+        skip = np.array(skip, np.uint32, copy=True)
+        hit = ids[skip[ids] == version]
+        if _MUT != 13:                         # planted (13): markers never cleared
+            skip[hit] = 0
+    ring_state[0] = version
+    ring_state[1] = int(newer.sum())
+    ring_state[2] = int((~newer).sum())
+    return out, prim_version, skip, ring_state, COMMIT_OK
