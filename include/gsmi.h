@@ -66,7 +66,8 @@ typedef struct {
 
 #define GS_DEV_PAIR_OVERFLOW 1u     /* gs_bin_sort: pairs > capacity */
 #define GS_DEV_MSG_OVERFLOW 2u      /* gs_delta_pack, gs_sparse_adam_publish: message > msg_capacity */
-#define GS_DEV_MSG_MISMATCH 4u      /* gs_delta_apply: bad magic / widths / ids */
+#define GS_DEV_MSG_MISMATCH 4u      /* gs_delta_apply, gs_publish_commit: bad magic / widths / ids / version */
+#define GS_DEV_MSG_ORDER 8u         /* gs_publish_commit: not the version after the last committed one */
 
 /*
  * Primitive pool Theta (Section 2.1): five aligned fp32 tensors, one row per
@@ -370,6 +371,47 @@ gs_status gs_delta_apply(const void* msg, size_t msg_capacity, const gs_group* d
                          void* stream);
 
 /*
+ * Versioned two-slot publication ring (Section 4.3, Shadow Graph steps 3-4:
+ * updates are staged in a shared two-slot ring that is also the
+ * communication source, and a slot is committed once its publication
+ * condition holds; throughput-first path: per-primitive publication metadata
+ * so that a read skips at most one unpublished update).
+ *   slot[0], slot[1]: device message buffers of slot_bytes each, 16-byte
+ *     aligned; the update of version v is staged (gs_sparse_adam_publish or
+ *     gs_delta_pack with that version) in slot[v & 1]
+ *   state: 8 uint32 of device memory, zeroed by the caller once before the
+ *     first commit: [0] last committed version, [1] rows applied and [2] rows
+ *     left by the last commit, [3] reserved, [4..7] the library's (keep zero)
+ * gs_publish_commit commits version `version` from slot[version & 1] into the
+ * replica dst:
+ *   - the slot must hold a message of this version whose group widths match
+ *     dst, with count <= max_rows and ids < n_rows, else GS_DEV_MSG_MISMATCH;
+ *   - versions commit in order: state[0] must be version - 1, else
+ *     GS_DEV_MSG_ORDER (a repeated or early commit);
+ *   - a row is applied (GS_APPLY_ADD: one fp32 add; GS_APPLY_OVERWRITE: copy)
+ *     only if prim_version[id] < version, and prim_version[id] is then set to
+ *     version; rows already at or past it are left (counted in state[2]);
+ *   - skip[id] == version is cleared to 0 for every row of the message (the
+ *     update that delayed reads skipped is now published; see
+ *     gs_admission_gate);
+ *   - on success state[0] = version.
+ * After a flagged refusal nothing is written (replica, versions, skip, state).
+ *   prim_version [n_rows] uint32 (required); skip [n_rows] uint32 or NULL
+ * Errors: GS_ERR_INVALID_ARG for null pointers, misaligned slots, slots
+ * smaller than a message header, version 0, a bad mode or group list;
+ * GS_ERR_UNSUPPORTED for rows longer than 64 floats.
+ */
+typedef struct {
+    void* slot[2];
+    size_t slot_bytes;
+    uint32_t* state;
+} gs_ring;
+
+gs_status gs_publish_commit(const gs_ring* ring, uint32_t version, const gs_group* dst, int32_t n_groups,
+                            int32_t n_rows, int32_t max_rows, int32_t mode, uint32_t* prim_version, uint32_t* skip,
+                            gs_device_status* status, void* stream);
+
+/*
  * Primitive scopes (Section 2.1: the dependency unit is the primitive index;
  * a task unit's conservative read and update scopes R+ and W+, its realized
  * active set C and gradient evidence g).  A scope is a bitmap over primitive
@@ -429,7 +471,7 @@ gs_status gs_scope_conflicts(const uint32_t* RA, const uint32_t* WA, const uint3
  *   -> GS_GATE_ADMIT
  * rho, the mean (an fp64 sum of the fp32 magnitudes) and the threshold are
  * formed in fp64.  On GS_GATE_ADMIT, skip[p] = producer_version for every p in
- * D+ (the per-primitive publication metadata; gs_delta_apply_versioned clears
+ * D+ (the per-primitive publication metadata; gs_publish_commit clears
  * it when that version is published).
  *   RB, D: scopes (bitmaps); args->active: the scope C_A; args->evidence: the
  *     scope of ids whose ||g_A|| the producer reported, or NULL for C_A;

@@ -342,6 +342,24 @@ gs_status gs_delta_apply(const void* msg, size_t msg_capacity, const gs_group* d
                       "gs_delta_apply");
 }
 
+gs_status gs_publish_commit(const gs_ring* ring, uint32_t version, const gs_group* dst, int32_t n_groups,
+                            int32_t n_rows, int32_t max_rows, int32_t mode, uint32_t* prim_version, uint32_t* skip,
+                            gs_device_status* status, void* stream) {
+    gs_status s;
+    if ((s = check_groups(dst, n_groups, "gs_publish_commit")) != GS_OK) return s;
+    GS_REQUIRE(ring && ring->slot[0] && ring->slot[1] && ring->state, "gs_publish_commit: null ring");
+    GS_REQUIRE(aligned(ring->slot[0], 16) && aligned(ring->slot[1], 16), "gs_publish_commit: slots must be 16-byte aligned");
+    GS_REQUIRE(ring->slot_bytes >= gsmi::delta_msg_bytes(0, 0, n_groups),
+               "gs_publish_commit: slots below the message header size");
+    GS_REQUIRE(prim_version && status, "gs_publish_commit: null prim_version / status");
+    GS_REQUIRE(version >= 1, "gs_publish_commit: version 0");
+    GS_REQUIRE(mode == GS_APPLY_ADD || mode == GS_APPLY_OVERWRITE, "gs_publish_commit: bad mode %d", mode);
+    GS_REQUIRE(n_rows >= 0 && max_rows >= 0, "gs_publish_commit: negative size");
+    return hip_status(gsmi::launch_publish_commit(*ring, version, dst, n_groups, n_rows, max_rows, mode, prim_version,
+                                                  skip, status, static_cast<hipStream_t>(stream)),
+                      "gs_publish_commit");
+}
+
 gs_status gs_scope_from_ids(const uint32_t* idx, const uint32_t* count, int32_t max_rows, int32_t n,
                             int32_t accumulate, uint32_t* scope, void* stream) {
     GS_REQUIRE(n >= 0 && max_rows >= 0, "gs_scope_from_ids: negative size");

@@ -1,6 +1,8 @@
 // Staged publication of pending updates: pack the rows of an ascending id
 // list into one message, and commit a message into a replica (add or copy),
-// stamping the per-primitive publication version.
+// stamping the per-primitive publication version; the versioned commit of a
+// two-slot ring checks the order of versions and each primitive's published
+// version and clears the skip markers of delayed reads.
 //
 // Same lane layout as the optimizer: one row per floor(64/row_len) lanes,
 // lane -> (group, column) fixed once, grid-strided rows.  Message writes are
@@ -125,6 +127,73 @@ __global__ void __launch_bounds__(GS_BLOCK) k_apply(GroupArgs a, const uint32_t*
     }
 }
 
+// Commit of a ring slot (Shadow Graph step 4): the message check above plus
+// the slot's version and the commit order; then the rows of primitives whose
+// published version is older than the message's, each stamped with it, and
+// the skip markers that name this version cleared; finally the ring's
+// committed version and the counts of applied / left rows.
+__global__ void k_commit_order(const uint32_t* __restrict__ msg, uint32_t version,
+                               const uint32_t* __restrict__ ring_state, gs_device_status* __restrict__ status) {
+    if (msg[2] != version) atomicOr(&status->flags, GS_DEV_MSG_MISMATCH);
+    else if (ring_state[0] + 1u != version) atomicOr(&status->flags, GS_DEV_MSG_ORDER);
+}
+
+__global__ void __launch_bounds__(GS_BLOCK) k_commit(GroupArgs a, const uint32_t* __restrict__ msg, int32_t mode,
+                                                     uint32_t* __restrict__ prim_version, uint32_t* __restrict__ skip,
+                                                     uint32_t* __restrict__ ring_state,
+                                                     const gs_device_status* __restrict__ status) {
+    if (status->flags & (GS_DEV_MSG_MISMATCH | GS_DEV_MSG_ORDER)) return;
+    const uint32_t K = msg[1];
+    const uint32_t version = msg[2];
+    const uint64_t gw = (uint64_t)((a.n_groups + 3) / 4) * 4;
+    const uint32_t* __restrict__ ids = msg + 8 + gw;
+    const float* __restrict__ rows = reinterpret_cast<const float*>(msg + msg_words_before_rows(K, a.n_groups));
+    const int lane = lane_id();
+    int sub, grp, c;
+    lane_group(a, lane, sub, grp, c);
+    const bool in_row = sub < a.rows_per_wave;
+    float* __restrict__ dst = a.ptr[in_row ? grp : 0];
+    const int cols = a.cols[in_row ? grp : 0];
+    const int col = lane - sub * a.row_len;
+    const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
+    const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
+    uint32_t left = 0;
+    // every lane of the wave runs the same number of iterations (rows are
+    // strided by whole waves), so the wave-level counts below see all lanes
+    for (uint32_t r0 = wave * a.rows_per_wave; r0 < K; r0 += waves * a.rows_per_wave) {
+        const uint32_t r = r0 + (uint32_t)sub;
+        if (!in_row || r >= K) continue;
+        const uint32_t id = ids[r];
+        const bool newer = prim_version[id] < version;   // read by every lane of the row before lane 0 stamps
+        if (newer) {
+            const float val = rows[(size_t)r * a.row_len + col];
+            float* q = dst + (size_t)id * cols + c;
+            *q = (mode == GS_APPLY_ADD) ? (*q + val) : val;
+        }
+        if (col == 0) {
+            if (newer)
+                prim_version[id] = version;
+            else
+                ++left;
+            if (skip && skip[id] == version) skip[id] = 0u;
+        }
+    }
+    // rows left behind are rare (a later version already published them):
+    // only waves that saw one touch the shared counter
+    left = wave_sum_u32(left);
+    if (lane == 0 && left) atomicAdd(&ring_state[5], left);
+}
+
+__global__ void k_commit_finish(const uint32_t* __restrict__ msg, uint32_t version, uint32_t* __restrict__ ring_state,
+                                const gs_device_status* __restrict__ status) {
+    if (status->flags & (GS_DEV_MSG_MISMATCH | GS_DEV_MSG_ORDER)) return;
+    const uint32_t left = ring_state[5];
+    ring_state[0] = version;
+    ring_state[1] = msg[1] - left;
+    ring_state[2] = left;
+    ring_state[5] = 0u;
+}
+
 GroupArgs make_group_args(const gs_group* g, int32_t n) {
     GroupArgs a = {};
     int32_t rl = 0;
@@ -146,6 +215,22 @@ uint32_t row_blocks(int32_t max_rows, int32_t rpw) {
 }
 
 }  // namespace
+
+hipError_t launch_publish_commit(const gs_ring& ring, uint32_t version, const gs_group* dst, int32_t n_groups,
+                                 int32_t n_rows, int32_t max_rows, int32_t mode, uint32_t* prim_version,
+                                 uint32_t* skip, gs_device_status* status, hipStream_t st) {
+    const GroupArgs a = make_group_args(dst, n_groups);
+    const uint32_t* msg = static_cast<const uint32_t*>(ring.slot[version & 1u]);
+    uint32_t cb = div_up((uint64_t)(max_rows > 0 ? max_rows : 1), GS_BLOCK);
+    if (cb > 4096) cb = 4096;
+    hipLaunchKernelGGL(k_apply_check, dim3(cb), dim3(GS_BLOCK), 0, st, a, msg, (uint64_t)ring.slot_bytes, n_rows,
+                       max_rows, status);
+    hipLaunchKernelGGL(k_commit_order, dim3(1), dim3(1), 0, st, msg, version, ring.state, status);
+    hipLaunchKernelGGL(k_commit, dim3(row_blocks(max_rows, a.rows_per_wave)), dim3(GS_BLOCK), 0, st, a, msg, mode,
+                       prim_version, skip, ring.state, status);
+    hipLaunchKernelGGL(k_commit_finish, dim3(1), dim3(1), 0, st, msg, version, ring.state, status);
+    return hipGetLastError();
+}
 
 size_t delta_msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups) {
     return (size_t)msg_bytes(count, row_len, n_groups);

@@ -80,6 +80,9 @@ size_t delta_msg_bytes(uint64_t count, int32_t row_len, int32_t n_groups);
 hipError_t launch_delta_pack(const uint32_t* idx, const uint32_t* count, int32_t max_rows, const gs_group* src,
                              int32_t n_groups, uint32_t version, void* msg, size_t msg_capacity,
                              gs_device_status* status, hipStream_t st);
+hipError_t launch_publish_commit(const gs_ring& ring, uint32_t version, const gs_group* dst, int32_t n_groups,
+                                 int32_t n_rows, int32_t max_rows, int32_t mode, uint32_t* prim_version,
+                                 uint32_t* skip, gs_device_status* status, hipStream_t st);
 hipError_t launch_delta_apply(const void* msg, size_t msg_capacity, const gs_group* dst, int32_t n_groups,
                               int32_t n_rows, int32_t max_rows, int32_t mode, uint32_t* prim_version,
                               gs_device_status* status, hipStream_t st);

@@ -28,7 +28,7 @@ GS_PRED_U32_NONZERO, GS_PRED_U8_NONZERO, GS_PRED_BITMAP = 0, 1, 2
 (GS_GATE_NO_DELAY, GS_GATE_ADMIT, GS_GATE_WAIT_RHO, GS_GATE_WAIT_NO_ACTIVE, GS_GATE_WAIT_MISSING, GS_GATE_WAIT_SECOND,
  GS_GATE_WAIT_GRADIENT) = range(7)
 GS_APPLY_ADD, GS_APPLY_OVERWRITE = 0, 1
-GS_DEV_PAIR_OVERFLOW, GS_DEV_MSG_OVERFLOW, GS_DEV_MSG_MISMATCH = 1, 2, 4
+GS_DEV_PAIR_OVERFLOW, GS_DEV_MSG_OVERFLOW, GS_DEV_MSG_MISMATCH, GS_DEV_MSG_ORDER = 1, 2, 4, 8
 GS_MSG_MAGIC = 0x47534D31
 GS_MAX_GROUPS = 8
 
@@ -55,6 +55,10 @@ class gs_adam_group(ctypes.Structure):
 
 class gs_group(ctypes.Structure):
     _fields_ = [("ptr", P), ("cols", i32)]
+
+
+class gs_ring(ctypes.Structure):
+    _fields_ = [("slot", P * 2), ("slot_bytes", sz), ("state", P)]
 
 
 class gs_gate_args(ctypes.Structure):
@@ -98,6 +102,8 @@ _lib.gs_sparse_adam_publish.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P
                                         ctypes.c_double, ctypes.c_double, ctypes.c_double, u32, P, sz, P, P]
 _lib.gs_delta_pack.argtypes = [P, P, i32, ctypes.POINTER(gs_group), i32, u32, P, sz, P, P]
 _lib.gs_delta_apply.argtypes = [P, sz, ctypes.POINTER(gs_group), i32, i32, i32, i32, P, P, P]
+_lib.gs_publish_commit.argtypes = [ctypes.POINTER(gs_ring), u32, ctypes.POINTER(gs_group), i32, i32, i32, i32, P, P,
+                                   P, P]
 _lib.gs_scope_from_ids.argtypes = [P, P, i32, i32, i32, P, P]
 _lib.gs_scope_from_pred.argtypes = [i32, P, i32, i32, P, P]
 _lib.gs_scope_conflicts.argtypes = [P, P, P, P, i32, P, P, P, P, P, P, P, P, sz, P]
@@ -105,14 +111,14 @@ _lib.gs_admission_gate.argtypes = [P, P, ctypes.POINTER(gs_gate_args), i32, P, P
 for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
               "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
               "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
-              "gs_admission_gate"):
+              "gs_admission_gate", "gs_publish_commit"):
     getattr(_lib, _name).restype = i32
 
 EXPORTS = ["gs_abi_version", "gs_status_string", "gs_last_error", "gs_workspace_bytes", "gs_delta_msg_bytes",
            "gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
            "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
            "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
-           "gs_admission_gate"]
+           "gs_admission_gate", "gs_publish_commit"]
 
 
 class GsmiError(RuntimeError):
@@ -299,6 +305,23 @@ def gs_delta_apply(msg, groups_arr, n_groups, n_rows, max_rows, mode, prim_versi
                                                         int(n_groups), int(n_rows),
                                                         int(max_rows), int(mode), ptr(prim_version), ptr(status),
                                                         stream if stream is not None else current_stream()))
+
+
+def make_ring(slots, state) -> gs_ring:
+    """slots: two device tensors of equal byte size (slot v & 1 holds version v); state: >= 8 uint32 words."""
+    nb = min(t.numel() * t.element_size() for t in slots)
+    r = gs_ring()
+    r.slot[0], r.slot[1] = slots[0].data_ptr(), slots[1].data_ptr()
+    r.slot_bytes = nb
+    r.state = state.data_ptr()
+    return r
+
+
+def gs_publish_commit(ring: gs_ring, version, groups_arr, n_groups, n_rows, max_rows, mode, prim_version, skip, status,
+                      stream=None):
+    return _check("gs_publish_commit", _lib.gs_publish_commit(
+        ctypes.byref(ring), int(version), groups_arr, int(n_groups), int(n_rows), int(max_rows), int(mode),
+        ptr(prim_version), ptr(skip), ptr(status), stream if stream is not None else current_stream()))
 
 
 def gs_scope_from_ids(idx, count, max_rows, n, accumulate, scope, stream=None):

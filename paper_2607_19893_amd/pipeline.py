@@ -80,8 +80,13 @@ class ViewTrainer:
         self.adam_arr = gsmi.make_adam_groups([(p, lr) for p in self.params])
         self.params_arr = gsmi.make_groups(self.params)
         self.replica_arr = gsmi.make_groups(self.replica) if with_replica else None
-        self.msg = torch.zeros((gsmi.gs_delta_msg_bytes(n, self.row_len, 5) + 15) // 16 * 4, dtype=torch.int32,
-                               device=self.dev)
+        # the two-slot publication ring: version v is staged in msgs[v & 1]
+        self.msgs = [torch.zeros((gsmi.gs_delta_msg_bytes(n, self.row_len, 5) + 15) // 16 * 4, dtype=torch.int32,
+                                 device=self.dev) for _ in range(2)]
+        self.msg = self.msgs[0]
+        self.ring_state = _u32(8, self.dev)
+        self.ring = gsmi.make_ring(self.msgs, self.ring_state)
+        self.skip = None            # per-primitive skip metadata of admitted delayed reads (optional)
 
     # -- buffers -------------------------------------------------------------
     def _set_image(self, w, h):
@@ -225,6 +230,11 @@ class ViewTrainer:
         gsmi.gs_delta_apply(self.msg if msg is None else msg, self.replica_arr, 5, self.n, self.n, mode,
                             self.version, self.status)
 
+    def commit(self, version, mode=gsmi.GS_APPLY_ADD):
+        """Commit the update staged for `version` (in msgs[version & 1]) into the replica, in version order."""
+        gsmi.gs_publish_commit(self.ring, version, self.replica_arr, 5, self.n, self.n, mode, self.version, self.skip,
+                               self.status)
+
     def enable_overlap(self):
         """Run each view's apply to the replica on a second stream (default
         priority), started once the next view's loss is done on the device, so
@@ -234,10 +244,8 @@ class ViewTrainer:
         if getattr(self, "apply_stream", None) is not None:
             return
         self.apply_stream = torch.cuda.Stream(device=self.dev)
-        self.msgs = [self.msg, torch.zeros_like(self.msg)]
         self.pub_ev = [torch.cuda.Event(), torch.cuda.Event()]
         self.app_ev = [torch.cuda.Event(), torch.cuda.Event()]
-        self._slot = 0
         self._pending = None
         self.front_ev = torch.cuda.Event()
 
@@ -249,14 +257,15 @@ class ViewTrainer:
         if pend is None:
             return
         self._pending = None
-        k, ev = pend
+        version, ev = pend
+        k = version & 1
         with torch.cuda.stream(self.apply_stream):
             self.apply_stream.wait_event(self.pub_ev[k])
             if after is not None:
                 self.apply_stream.wait_event(after)
             if ev:
                 ev[-2].record(self.apply_stream)
-            self.apply(msg=self.msgs[k])
+            self.commit(version)
             self.app_ev[k].record(self.apply_stream)
             if ev:
                 ev[-1].record(self.apply_stream)
@@ -267,8 +276,9 @@ class ViewTrainer:
               "adam_publish", "apply")
 
     def step(self, cam, step, version=1, publish=True, active=False, target=None, events=None, overlap=False):
-        """Project, visible set, bin+sort, forward, L1, backward, Adam staged as a message, apply to the replica.
-        publish=False runs plain Adam (steps to delta_rows) and no apply.
+        """Project, visible set, bin+sort, forward, L1, backward, Adam staged as the message of `version` in
+        ring slot version & 1, and its commit to the replica (versions must follow each other by one).
+        publish=False runs plain Adam (steps to delta_rows) and no commit.
         target: device tensor (3*H*W) or None for the set_target buffer.
         events: optional list of len(PHASES)+1 torch.cuda.Event recorded around the phases.
         overlap: apply on the second stream, deferred into the next step (enable_overlap; call
@@ -278,8 +288,7 @@ class ViewTrainer:
         ev = events
         if overlap and publish:
             self.enable_overlap()
-            k = self._slot
-            self._slot ^= 1
+            k = version & 1
             msg = self.msgs[k]
             main = torch.cuda.current_stream()
             calls = (lambda: self.project(cam), self.visible, self.bin_sort, lambda: self.raster_fwd(active=active),
@@ -294,17 +303,18 @@ class ViewTrainer:
                     # the previous view's apply, once this view reaches that phase on the device
                     self.front_ev.record(main)
                     self.flush_apply(after=self.front_ev)
-            main.wait_event(self.app_ev[k])          # the apply that read this buffer two views ago
+            main.wait_event(self.app_ev[k])          # the commit that read this slot two versions ago
             self.adam_publish(step, version, msg)
             self.pub_ev[k].record(main)
             if ev:
                 ev[len(calls) + 1].record()
-            self._pending = (k, ev)
+            self._pending = (version, ev)
             return
         calls = (lambda: self.project(cam), self.visible, self.bin_sort, lambda: self.raster_fwd(active=active),
                  lambda: self.loss_l1(target), self.raster_bwd_pixels, self.raster_bwd_project,
-                 (lambda: self.adam_publish(step, version)) if publish else (lambda: self.adam(step)),
-                 self.apply if publish else (lambda: None))
+                 (lambda: self.adam_publish(step, version, self.msgs[version & 1])) if publish
+                 else (lambda: self.adam(step)),
+                 (lambda: self.commit(version)) if publish else (lambda: None))
         if ev:
             ev[0].record()
         for i, fn in enumerate(calls):

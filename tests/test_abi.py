@@ -77,6 +77,20 @@ def test_null_and_range_arguments_rejected(gs):
     assert L.gs_delta_apply(16, 8, g, 1, 10, 10, 0, None, 16, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_delta_pack(16, 16, 10, g, 1, 1, 8, 1024, 16, None) == gs.GS_ERR_INVALID_ARG  # misaligned msg
     assert L.gs_loss_l1(None, None, 4, 4, None, None, None, 0, None) == gs.GS_ERR_INVALID_ARG
+    # versioned commit of a ring slot
+    ring = gs.gs_ring()
+    ring.slot[0], ring.slot[1], ring.slot_bytes, ring.state = 16, 32, 4096, 16
+    g5 = (gs.gs_group * 1)(gs.gs_group(16, 3))
+    assert L.gs_publish_commit(None, 1, g5, 1, 10, 10, 0, 16, None, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_publish_commit(ctypes.byref(ring), 0, g5, 1, 10, 10, 0, 16, None, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert "version 0" in gs.gs_last_error()
+    assert L.gs_publish_commit(ctypes.byref(ring), 1, g5, 1, 10, 10, 0, None, None, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_publish_commit(ctypes.byref(ring), 1, g5, 1, 10, 10, 3, 16, None, 16, None) == gs.GS_ERR_INVALID_ARG
+    ring.slot[1] = 40
+    assert L.gs_publish_commit(ctypes.byref(ring), 1, g5, 1, 10, 10, 0, 16, None, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert "aligned" in gs.gs_last_error()
+    ring.slot[1], ring.slot_bytes = 32, 8
+    assert L.gs_publish_commit(ctypes.byref(ring), 1, g5, 1, 10, 10, 0, 16, None, 16, None) == gs.GS_ERR_INVALID_ARG
     # scopes, hazards and admission
     assert L.gs_scope_from_ids(None, None, 5, 100, 0, 16, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_scope_from_ids(16, 16, 5, -1, 0, 16, None) == gs.GS_ERR_INVALID_ARG
