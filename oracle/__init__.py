@@ -713,3 +713,74 @@ def publish_commit(ring_state, slots, version, groups, mode, prim_version, skip=
     ring_state[1] = int(newer.sum())
     ring_state[2] = int((~newer).sum())
     return out, prim_version, skip, ring_state, COMMIT_OK
+
+
+# ---------------------------------------------------------------------------
+# a task unit of several views (Section 2.1)
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class UnitResult:
+    union: np.ndarray          # ascending union of the views' visible sets
+    grads: list                # per group [|union|, cols] fp64: the views' gradients summed
+    grad_norm: np.ndarray      # [n]: sum over the views of |dL/d(u,v)| (visible views only)
+    views: list                # per view: (vis, proj, render, dL_dimg, loss, flag)
+    new_params: list           # union rows, fp64
+    new_m: list
+    new_v: list
+    deltas: list
+    msg: Optional[np.ndarray]
+
+
+def unit_gradients(scene, cams, targets=None, dL_list=None, mode=0):
+    """Gradient of a task unit: the sum over its views of each view's loss
+    gradient (a task unit is a small batch of training views, and its active
+    set and gradient evidence are the union and accumulation over its views,
+    Section 2.1).  Each view's loss is the L1 mean of that view (targets), or
+    its upstream image gradient is given (dL_list).  Rows are those of the
+    ascending union of the views' visible sets.  mode selects the projection's
+    geometry (0: the fixed-order fp32 geometry, 1: fp64).  Returns (union,
+    grads per group by union row, grad_norm by id, per-view records)."""
+    n = scene.n
+    views = []
+    for k, cam in enumerate(cams):
+        proj = project(scene, cam, mode)
+        vis = visible(proj.tiles)
+        rnd = render(vis, proj, cam)
+        if dL_list is None:
+            loss, dL, lm = loss_l1(rnd.img.astype(np.float32), targets[k])
+        else:
+            loss, dL, lm = float("nan"), np.asarray(dL_list[k], np.float64), None
+        g2, flag = render_backward(vis, proj, cam, dL, loss_margin=lm)
+        gr = project_backward(scene, cam, vis, g2, proj)
+        views.append((vis, proj, rnd, dL, loss, flag, gr, lm))
+    union = np.unique(np.concatenate([v[0] for v in views]).astype(np.int64)).astype(np.uint32) \
+        if views else np.zeros(0, np.uint32)
+    cols = [3, 3, 4, 1, 3 * (scene.sh_degree + 1) ** 2]
+    grads = [np.zeros((union.size, c)) for c in cols]
+    gnorm = np.zeros(n)
+    for vis, proj, rnd, dL, loss, flag, gr, lm in views:
+        rows = np.searchsorted(union, vis)
+        if _MUT == 15:
+            rows = np.arange(vis.size)             # planted: view rows taken as union rows
+        for G, g in zip(grads, gr.groups()):
+            G[rows] += g
+        gnorm[vis.astype(np.int64)] += gr.grad_norm
+    return union, grads, gnorm, views
+
+
+def train_unit(scene, cams, targets, m_groups, v_groups, step, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-15,
+               version=1, dL_list=None, with_msg=True):
+    """A task unit: the views' gradients summed over the union of their visible
+    sets, then one Adam step over that union (rows outside it untouched) and
+    its steps staged as one message."""
+    union, grads, gnorm, views = unit_gradients(scene, cams, targets, dL_list)
+    rows = union.astype(np.int64)
+    params = [a.reshape(scene.n, -1) for _, a in scene.groups()]
+    newp, newm, newv, deltas = [], [], [], []
+    for p, g, m, v in zip(params, grads, m_groups, v_groups):
+        pn, mn, vn, d = adam_rows(p[rows], g, np.asarray(m).reshape(scene.n, -1)[rows],
+                                  np.asarray(v).reshape(scene.n, -1)[rows], step, lr, beta1, beta2, eps)
+        newp.append(pn); newm.append(mn); newv.append(vn); deltas.append(d)
+    msg = delta_message(union, [d.astype(np.float32) for d in deltas], version) if with_msg else None
+    return UnitResult(union, grads, gnorm, [v[:6] for v in views], newp, newm, newv, deltas, msg)
