@@ -51,9 +51,9 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 TRAFFIC = {
     "kernel": "k_raster_bwd",
     "source": "paper_2607_19893_amd/csrc/raster.hip",
-    "code_sha256": "7d49ad364f5e8965cc46b1f9828c4fce0194dc39216a923aacb033495b221d63",
-    "fetch_kib": 206337.91, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 98543.95, "write_scale": 1048576.0 / 1048576.0,
+    "code_sha256": "2e7f01d6b63d559b7e5794e07e78f398810e906e7a3e24270b6f3daac8b3ab1d",
+    "fetch_kib": 206249.82, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 98549.66, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 

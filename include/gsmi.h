@@ -282,6 +282,31 @@ gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, con
                                 float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * A task unit of several views (Section 2.1: a task unit is a small batch of
+ * training views whose scopes, active sets and gradient evidence are unions
+ * and accumulations over its views): gs_raster_bwd_project for one view of
+ * the unit, adding into the unit's gradient instead of writing a view's.
+ *   union_idx/union_count: the unit's ascending union of visible sets (e.g.
+ *     gs_scope_from_pred over the views' tile counts, then gs_visible_set with
+ *     GS_PRED_BITMAP); it must contain this view's visible ids (ids missing
+ *     from it are left out)
+ *   grad_rows [*,grad_ld]: row u accumulates the gradient of union_idx[u]
+ *     (same record layout as gs_raster_bwd); grad_norm [n]: grad_norm[id]
+ *     accumulates |dL/d(u,v)| of each view (the unit's g_U evidence), or NULL
+ *   first != 0 (the unit's first view): the |U| rows (all grad_ld columns) and
+ *     grad_norm at the union ids are cleared before this view's terms are added
+ * Other arguments as in gs_raster_bwd_project (its workspace, written by
+ * gs_raster_bwd_pixels for this view).  Views must be added one after the
+ * other (same stream); the result is the fp32 sum of the views' gradients in
+ * view order.
+ */
+gs_status gs_raster_bwd_project_accum(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj,
+                                      const uint32_t* pair_offset, const uint32_t* vis_idx, const uint32_t* vis_count,
+                                      uint32_t capacity, const uint32_t* union_idx, const uint32_t* union_count,
+                                      int32_t first, float* grad_rows, int32_t grad_ld, float* grad_norm, void* ws,
+                                      size_t ws_bytes, void* stream);
+
+/*
  * Optimizer update (U in Figure 6; Shadow Graph step 5): Adam on the rows in
  * idx only ("updating only visible primitives", Introduction), torch.optim.Adam
  * form with one global step t >= 1:

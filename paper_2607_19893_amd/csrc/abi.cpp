@@ -247,6 +247,30 @@ gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, con
                       "gs_raster_bwd_project");
 }
 
+gs_status gs_raster_bwd_project_accum(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj,
+                                      const uint32_t* pair_offset, const uint32_t* vis_idx, const uint32_t* vis_count,
+                                      uint32_t capacity, const uint32_t* union_idx, const uint32_t* union_count,
+                                      int32_t first, float* grad_rows, int32_t grad_ld, float* grad_norm, void* ws,
+                                      size_t ws_bytes, void* stream) {
+    gs_status s;
+    if ((s = check_scene(scene, "gs_raster_bwd_project_accum")) != GS_OK) return s;
+    if ((s = check_grad_rows(scene, grad_rows, grad_ld, "gs_raster_bwd_project_accum")) != GS_OK) return s;
+    if ((s = check_camera(cam, "gs_raster_bwd_project_accum")) != GS_OK) return s;
+    if ((s = check_proj(proj, true, "gs_raster_bwd_project_accum")) != GS_OK) return s;
+    GS_REQUIRE(pair_offset && vis_idx && vis_count && union_idx && union_count && ws,
+               "gs_raster_bwd_project_accum: null pointer");
+    GS_REQUIRE(aligned(ws, 256), "gs_raster_bwd_project_accum: workspace must be 256-byte aligned");
+    if (ws_bytes < gsmi::raster_bwd_ws_bytes(scene->n, capacity))
+        return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_project_accum: workspace too small");
+    const gsmi::CamArgs c = gsmi::make_cam_args(cam);
+    const float bg0[3] = {0.0f, 0.0f, 0.0f};
+    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, nullptr, nullptr, pair_offset, nullptr, vis_idx,
+                                              vis_count, capacity, nullptr, nullptr, nullptr, bg0, grad_rows, grad_ld,
+                                              nullptr, grad_norm, ws, 2, static_cast<hipStream_t>(stream), union_idx,
+                                              union_count, first != 0),
+                      "gs_raster_bwd_project_accum");
+}
+
 static gs_status check_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx, const uint32_t* count,
                             int32_t max_rows, const float* grad_rows, int32_t grad_ld, const float* m, const float* v,
                             int32_t state_ld, int32_t step, double beta1, double beta2, double eps,

@@ -164,12 +164,14 @@ __global__ void __launch_bounds__(GS_BLOCK) k_commit(GroupArgs a, const uint32_t
         const uint32_t r = r0 + (uint32_t)sub;
         if (!in_row || r >= K) continue;
         const uint32_t id = ids[r];
-        const bool newer = prim_version[id] < version;   // read by every lane of the row before lane 0 stamps
-        if (newer) {
-            const float val = rows[(size_t)r * a.row_len + col];
-            float* q = dst + (size_t)id * cols + c;
-            *q = (mode == GS_APPLY_ADD) ? (*q + val) : val;
-        }
+        // the three loads depend only on id, so they are in flight together;
+        // every lane of the row reads the version before lane 0 stamps it
+        const uint32_t pv = prim_version[id];
+        const float val = rows[(size_t)r * a.row_len + col];
+        float* q = dst + (size_t)id * cols + c;
+        const float old = *q;
+        const bool newer = pv < version;
+        if (newer) *q = (mode == GS_APPLY_ADD) ? (old + val) : val;
         if (col == 0) {
             if (newer)
                 prim_version[id] = version;

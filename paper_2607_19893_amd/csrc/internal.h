@@ -50,7 +50,8 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
                              const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity,
                              const float* final_T, const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
                              float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, int stages,
-                             hipStream_t st);
+                             hipStream_t st, const uint32_t* union_idx = nullptr,
+                             const uint32_t* union_count = nullptr, int first = 0);
 
 // adam.hip
 hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,

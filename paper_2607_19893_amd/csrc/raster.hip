@@ -797,17 +797,31 @@ __device__ __forceinline__ void load_row(const float* __restrict__ src, float* d
     }
 }
 
+// Position of id in the ascending list u[0..m), or m if absent.
+__device__ __forceinline__ uint32_t find_row(const uint32_t* __restrict__ u, uint32_t m, uint32_t id) {
+    uint32_t lo = 0, hi = m;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (u[mid] < id) lo = mid + 1; else hi = mid;
+    }
+    return (lo < m && u[lo] == id) ? lo : m;
+}
+
 // Per visible row r: the primitive's 2D gradient (the sum of its pair slots,
 // emission positions pair_offset[id] .. + tiles[id], side by side; none if the
 // pair list overflowed its capacity), then the chain rule to the parameters;
-// writes the row's gradient record at grad_rows + r * ld.
-template <int DEG>
+// writes the row's gradient record at grad_rows + r * ld.  ACCUM (a task unit
+// of several views): the record is added to row u instead, u the position of
+// id in the unit's ascending union list, and |dL/d(u,v)| is added to
+// grad_norm[id].
+template <int DEG, bool ACCUM>
 __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
     const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
     const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, uint32_t capacity,
     const float4* __restrict__ conic_op, const uint8_t* __restrict__ clampm, const float* __restrict__ mean, const float* __restrict__ log_scale,
     const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c,
-    float* __restrict__ grad_rows, int32_t ld, float* __restrict__ grad2d, float* __restrict__ grad_norm) {
+    float* __restrict__ grad_rows, int32_t ld, float* __restrict__ grad2d, float* __restrict__ grad_norm,
+    const uint32_t* __restrict__ union_idx, const uint32_t* __restrict__ union_count) {
     using L = RowLayout<DEG>;
     constexpr int K = L::K;
     const uint32_t V = *vis_count;
@@ -859,11 +873,20 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
         g2[4] = 0.5f * g2[4];
         g2[5] = co.w > 0.0f ? -g2[5] / co.w : 0.0f;
     }
+    uint32_t row = r;
+    if (ACCUM) {
+        const uint32_t m = *union_count;
+        row = find_row(union_idx, m, id);
+        if (row == m) return;                 // not in the unit's union: nothing to add to
+    }
     if (grad2d) {
 #pragma unroll
         for (int q = 0; q < kG; ++q) grad2d[(size_t)id * kG + q] = g2[q];
     }
-    if (grad_norm) grad_norm[id] = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
+    if (grad_norm) {
+        const float gn = sqrtf(g2[0] * g2[0] + g2[1] * g2[1]);
+        grad_norm[id] = ACCUM ? grad_norm[id] + gn : gn;
+    }
     float mu[3], ls[3], qr[4];
     load_row<3>(mean + (size_t)id * 3, mu);
     load_row<3>(log_scale + (size_t)id * 3, ls);
@@ -917,10 +940,34 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
 #pragma unroll
     for (int k = L::ROW; k < L::ROW4; ++k) out[k] = 0.0f;
 
-    float4* dst = reinterpret_cast<float4*>(grad_rows + (size_t)r * ld);
+    float4* dst = reinterpret_cast<float4*>(grad_rows + (size_t)row * ld);
+    if (ACCUM) {
+#pragma unroll
+        for (int k = 0; k < L::ROW4 / 4; ++k) {
+            const float4 a = dst[k];
+            dst[k] = make_float4(a.x + out[4 * k], a.y + out[4 * k + 1], a.z + out[4 * k + 2], a.w + out[4 * k + 3]);
+        }
+        return;
+    }
 #pragma unroll
     for (int k = 0; k < L::ROW4 / 4; ++k) dst[k] = make_float4(out[4 * k], out[4 * k + 1], out[4 * k + 2], out[4 * k + 3]);
     for (int k = L::ROW4 / 4; k < ld / 4; ++k) dst[k] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+}
+
+// First view of a task unit: the union's gradient rows (all ld columns) and
+// the grad_norm entries of its ids start at zero.
+__global__ void __launch_bounds__(GS_BLOCK) k_clear_union_rows(const uint32_t* __restrict__ union_idx,
+                                                               const uint32_t* __restrict__ union_count,
+                                                               float* __restrict__ grad_rows, int32_t ld,
+                                                               float* __restrict__ grad_norm) {
+    const uint32_t m = *union_count;
+    const uint32_t q4 = (uint32_t)ld / 4;
+    const uint64_t total = (uint64_t)m * q4;
+    float4* rows = reinterpret_cast<float4*>(grad_rows);
+    for (uint64_t i = (uint64_t)blockIdx.x * GS_BLOCK + threadIdx.x; i < total; i += (uint64_t)gridDim.x * GS_BLOCK) {
+        rows[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (grad_norm && i % q4 == 0) grad_norm[union_idx[i / q4]] = 0.0f;
+    }
 }
 
 }  // namespace
@@ -980,7 +1027,7 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
                              const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity,
                              const float* final_T, const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
                              float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, int stages,
-                             hipStream_t st) {
+                             hipStream_t st, const uint32_t* union_idx, const uint32_t* union_count, int first) {
     float* slots = static_cast<float*>(ws);
     const int32_t T = cam.tiles_x * cam.tiles_y;
     if ((stages & 1) && T > 0)
@@ -991,16 +1038,33 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || scene.n == 0 || !(stages & 2)) return e;
     const dim3 grid(div_up(scene.n, GS_BLOCK));
-#define GS_LAUNCH_PBWD(D)                                                                                        \
-    hipLaunchKernelGGL(k_project_bwd<D>, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset,  \
-                       slots, capacity, reinterpret_cast<const float4*>(proj.conic_opacity), proj.clamp,          \
-                       scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam, grad_rows, grad_ld,  \
-                       grad2d, grad_norm)
-    switch (scene.sh_degree) {
-        case 0: GS_LAUNCH_PBWD(0); break;
-        case 1: GS_LAUNCH_PBWD(1); break;
-        case 2: GS_LAUNCH_PBWD(2); break;
-        default: GS_LAUNCH_PBWD(3); break;
+    if (union_idx) {
+        if (first) {
+            uint32_t cb = div_up((uint64_t)scene.n * (uint64_t)(grad_ld / 4), GS_BLOCK);
+            if (cb > 8192) cb = 8192;
+            hipLaunchKernelGGL(k_clear_union_rows, dim3(cb), dim3(GS_BLOCK), 0, st, union_idx, union_count, grad_rows,
+                               grad_ld, grad_norm);
+        }
+    }
+#define GS_LAUNCH_PBWD(D, A)                                                                                     \
+    hipLaunchKernelGGL((k_project_bwd<D, A>), grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles,        \
+                       pair_offset, slots, capacity, reinterpret_cast<const float4*>(proj.conic_opacity),         \
+                       proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam,         \
+                       grad_rows, grad_ld, grad2d, grad_norm, union_idx, union_count)
+    if (union_idx) {
+        switch (scene.sh_degree) {
+            case 0: GS_LAUNCH_PBWD(0, true); break;
+            case 1: GS_LAUNCH_PBWD(1, true); break;
+            case 2: GS_LAUNCH_PBWD(2, true); break;
+            default: GS_LAUNCH_PBWD(3, true); break;
+        }
+    } else {
+        switch (scene.sh_degree) {
+            case 0: GS_LAUNCH_PBWD(0, false); break;
+            case 1: GS_LAUNCH_PBWD(1, false); break;
+            case 2: GS_LAUNCH_PBWD(2, false); break;
+            default: GS_LAUNCH_PBWD(3, false); break;
+        }
     }
 #undef GS_LAUNCH_PBWD
     return hipGetLastError();

@@ -96,6 +96,8 @@ _lib.gs_raster_bwd_pixels.argtypes = [ctypes.POINTER(gs_proj), ctypes.POINTER(gs
                                       P, sz, P]
 _lib.gs_raster_bwd_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj),
                                        P, P, P, u32, P, i32, P, P, P, sz, P]
+_lib.gs_raster_bwd_project_accum.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera),
+                                             ctypes.POINTER(gs_proj), P, P, P, u32, P, P, i32, P, i32, P, P, sz, P]
 _lib.gs_sparse_adam.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, P, i32, P, P, i32, i32,
                                 ctypes.c_double, ctypes.c_double, ctypes.c_double, P, i32, P]
 _lib.gs_sparse_adam_publish.argtypes = [ctypes.POINTER(gs_adam_group), i32, P, P, i32, P, i32, P, P, i32, i32,
@@ -111,14 +113,14 @@ _lib.gs_admission_gate.argtypes = [P, P, ctypes.POINTER(gs_gate_args), i32, P, P
 for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
               "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
               "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
-              "gs_admission_gate", "gs_publish_commit"):
+              "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum"):
     getattr(_lib, _name).restype = i32
 
 EXPORTS = ["gs_abi_version", "gs_status_string", "gs_last_error", "gs_workspace_bytes", "gs_delta_msg_bytes",
            "gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
            "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
            "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
-           "gs_admission_gate", "gs_publish_commit"]
+           "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum"]
 
 
 class GsmiError(RuntimeError):
@@ -261,6 +263,14 @@ def gs_raster_bwd_project(scene: gs_scene, cam: gs_camera, proj: gs_proj, pair_o
         ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj), ptr(pair_offset), ptr(vis_idx),
         ptr(vis_count), int(capacity), ptr(grad_rows), int(grad_ld), ptr(grad2d), ptr(grad_norm), ptr(ws),
         ws.numel() * ws.element_size(), stream if stream is not None else current_stream()))
+
+
+def gs_raster_bwd_project_accum(scene: gs_scene, cam: gs_camera, proj: gs_proj, pair_offset, vis_idx, vis_count,
+                                capacity, union_idx, union_count, first, grad_rows, grad_ld, grad_norm, ws, stream=None):
+    return _check("gs_raster_bwd_project_accum", _lib.gs_raster_bwd_project_accum(
+        ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj), ptr(pair_offset), ptr(vis_idx), ptr(vis_count),
+        int(capacity), ptr(union_idx), ptr(union_count), int(first), ptr(grad_rows), int(grad_ld), ptr(grad_norm),
+        ptr(ws), ws.numel() * ws.element_size(), stream if stream is not None else current_stream()))
 
 
 def make_adam_groups(groups):

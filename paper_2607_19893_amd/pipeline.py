@@ -210,6 +210,75 @@ class ViewTrainer:
         gsmi.gs_delta_pack(self.vis_idx, self.counts[0:1], self.n, self.params_arr, 5, version, self.msg,
                            self.status)
 
+    # -- task units of several views --------------------------------------------
+    _SLOT_ATTRS = ("radius", "tiles", "rect", "depth", "mean2d", "conic", "rgb", "clamp", "vis_idx", "counts",
+                   "proj_s")
+
+    def view_slot(self, k):
+        """Switch the projection outputs, visible set and counts to those of view k of a task unit (each
+        view of a unit keeps its own until the unit's backward is done; pair lists and images are reused)."""
+        if not hasattr(self, "_slots"):
+            self._slots = [{a: getattr(self, a) for a in self._SLOT_ATTRS}]
+        while len(self._slots) <= k:
+            n, dev = self.n, self.dev
+            d = dict(radius=_u32(n, dev), tiles=_u32(n, dev), rect=torch.zeros(max(1, n), 4, dtype=torch.int16, device=dev),
+                     depth=torch.zeros(max(1, n), device=dev), mean2d=torch.zeros(max(1, n), 2, device=dev),
+                     conic=torch.zeros(max(1, n), 4, device=dev), rgb=torch.zeros(max(1, n), 3, device=dev),
+                     clamp=torch.zeros(max(1, n), dtype=torch.uint8, device=dev), vis_idx=_u32(n, dev),
+                     counts=_u32(8, dev))
+            d["proj_s"] = gsmi.make_proj(d["radius"], d["tiles"], d["rect"], d["depth"], d["mean2d"], d["conic"],
+                                         d["rgb"], d["clamp"])
+            self._slots.append(d)
+        for a, t in self._slots[k].items():
+            setattr(self, a, t)
+
+    def _unit_buffers(self):
+        if getattr(self, "union_scope", None) is None:
+            self.union_scope = _u32(gsmi.scope_words(self.n), self.dev)
+            self.union_idx = _u32(self.n, self.dev)
+            self.union_count = _u32(4, self.dev)
+
+    def unit_scopes(self, cams):
+        """Project every view of a unit into its own slot, and form the unit's union of visible sets."""
+        self._unit_buffers()
+        for k, cam in enumerate(cams):
+            self.view_slot(k)
+            self.project(cam)
+            self.visible()
+            gsmi.gs_scope_from_pred(gsmi.GS_PRED_U32_NONZERO, self.tiles, self.n, 1 if k else 0, self.union_scope)
+        gsmi.gs_visible_set(gsmi.GS_PRED_BITMAP, self.union_scope, self.n, self.union_idx, self.union_count[0:1],
+                            self.ws_vis)
+
+    def unit_view_backward(self, k, cam, target=None, dL=None):
+        """Render view k of the unit (its slot holds its projection), take its L1 loss (or a given upstream
+        gradient) and add its gradient into the unit's rows."""
+        self.view_slot(k)
+        self.cam, self.cam_c = cam, gsmi.make_camera(cam)
+        self.bin_sort()
+        self.raster_fwd(active=False)
+        if dL is None:
+            self.loss_l1(target)
+        else:
+            self.set_dL(dL)
+        self.raster_bwd_pixels()
+        gsmi.gs_raster_bwd_project_accum(self.scene_s, self.cam_c, self.proj_s, self.pair_offset, self.vis_idx,
+                                         self.counts[0:1], self.capacity, self.union_idx, self.union_count[0:1],
+                                         1 if k == 0 else 0, self.grad_rows, self.ld, self.grad_norm, self.ws_bwd)
+
+    def step_unit(self, cams, step, version, targets=None):
+        """One task unit: every view rendered and back-propagated, the gradients summed over the union of the
+        views' visible sets, one sparse Adam over that union staged as the message of `version`, and its
+        commit to the replica."""
+        self.unit_scopes(cams)
+        for k, cam in enumerate(cams):
+            self.unit_view_backward(k, cam, target=None if targets is None else targets[k])
+        self.view_slot(0)
+        msg = self.msgs[version & 1]
+        gsmi.gs_sparse_adam_publish(self.adam_arr, 5, self.union_idx, self.union_count[0:1], self.n, self.grad_rows,
+                                    self.ld, self.m, self.v, self.ld, step, self.beta1, self.beta2, self.eps,
+                                    version, msg, self.status)
+        self.commit(version)
+
     # -- host views of compact rows ------------------------------------------
     def rows_by_group(self, t, count):
         """Per-group numpy arrays [count, cols] of a [*, ld] row table (gradients, moments, steps)."""
