@@ -95,6 +95,8 @@ def main():
     ap.add_argument("--no-overlap", action="store_true",
                     help="run every phase on one stream (by default each view's apply to the replica runs on a "
                          "second stream, beside the next view's backward raster)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the separate timings of the scope hazards / admission gate and of two-view task units")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy (read + write of this many MiB, 4 times) and exit; "
                          "its HBM counters calibrate the traffic counters of the path's kernels")
@@ -251,6 +253,12 @@ def main():
         % (V_mean, M_mean, ev_mean, inc_mean, wi_mean, wh_mean, 100 * wh_mean / max(wi_mean, 1),
            inc_mean / max(wh_mean, 1)))
 
+    extras = {}
+    if not args.no_extras:
+        extras["scope_gate"] = bench_scope_gate(tr, cams, targets, args.steps)
+        extras["unit2"] = bench_unit(tr, cams, targets, args.steps, step)
+        log("extras: " + json.dumps(extras))
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, args.cpu_views)
@@ -277,8 +285,98 @@ def main():
         "phases_ms": {k: v["ms"] for k, v in per_phase.items()},
         "phases_frac": {k: v["frac"] for k, v in per_phase.items()},
         "cpu_baseline": cpu,
+        "extras": extras,
     }
     print(json.dumps(out), flush=True)
+
+
+def bench_scope_gate(tr, cams, targets, steps):
+    """Hazard sets and throughput-first admission between consecutive views
+    A -> B of the workload: read scope = projection-visible set, update scope =
+    realized active set, evidence = the backward's |dL/d(u,v)| of A (tau 0.2).
+    Scopes and evidence are prepared untimed; the timed part is one
+    gs_scope_conflicts (bitmaps and id lists out) and one gs_admission_gate per
+    transition, on the current stream."""
+    import torch
+    from paper_2607_19893_amd import gsmi
+    n = tr.n
+    words = gsmi.scope_words(n)
+    nv = len(cams)
+    R = torch.zeros(nv, max(1, words), dtype=torch.int32, device=tr.dev)
+    Wr = torch.zeros_like(R)
+    G = torch.zeros(nv, max(1, n), device=tr.dev)
+    for i, c in enumerate(cams):
+        tr.project(c); tr.visible(); tr.bin_sort(); tr.raster_fwd(active=True); tr.loss_l1(targets[i])
+        tr.raster_bwd(grad2d=False)
+        gsmi.gs_scope_from_pred(gsmi.GS_PRED_U32_NONZERO, tr.tiles, n, 0, R[i])
+        gsmi.gs_scope_from_pred(gsmi.GS_PRED_U8_NONZERO, tr.active, n, 0, Wr[i])
+        G[i].copy_(tr.grad_norm)
+    out_bm = [torch.zeros(max(1, words), dtype=torch.int32, device=tr.dev) for _ in range(3)]
+    out_id = [torch.zeros(max(1, n), dtype=torch.int32, device=tr.dev) for _ in range(3)]
+    counts = torch.zeros(4, dtype=torch.int32, device=tr.dev)
+    res = torch.zeros(16, dtype=torch.int32, device=tr.dev)
+    ws = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_SCOPE, n), dtype=torch.uint8, device=tr.dev)
+    args_ = [gsmi.make_gate_args(Wr[i], G[i], 0.2, evidence=R[i]) for i in range(nv)]
+    torch.cuda.synchronize()
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    t_conf = t_gate = 0.0
+    hz = np.zeros(4)
+    reasons = {}
+    moved = 0.0
+    for k in range(steps):
+        a, b = k % nv, (k + 1) % nv
+        e0.record()
+        gsmi.gs_scope_conflicts(R[a], Wr[a], R[b], Wr[b], n, out_bm[0], out_bm[1], out_bm[2], out_id[0], out_id[1],
+                                out_id[2], counts, ws)
+        e1.record()
+        gsmi.gs_admission_gate(R[b], out_bm[1], args_[a], n, res, ws)
+        e2.record()
+        torch.cuda.synchronize()
+        t_conf += e0.elapsed_time(e1)
+        t_gate += e1.elapsed_time(e2)
+        c = counts.cpu().numpy().view(np.uint32).astype(np.float64)
+        hz += c
+        r = gsmi.gate_result_from(res)
+        reasons[r.reason] = reasons.get(r.reason, 0) + 1
+        # bytes: conflicts read 4 scopes and write 3 bitmaps and the id lists;
+        # the gate reads 4 scopes and ||g_A|| at C_A and D+
+        moved += 7 * words * 4 + 4 * float(c[:3].sum()) + 4 * words * 4 + 4 * (r.n_active + r.n_delayed)
+    t_conf /= steps
+    t_gate /= steps
+    hz /= steps
+    ms = t_conf + t_gate
+    gbs = moved / steps / (ms * 1e-3) / 1e9
+    return {"transitions": steps, "ms_conflicts": round(t_conf, 4), "ms_gate": round(t_gate, 4),
+            "mean_waw": round(hz[0]), "mean_raw": round(hz[1]), "mean_war": round(hz[2]), "mean_read": round(hz[3]),
+            "gate_reasons": {str(k): v for k, v in sorted(reasons.items())}, "hbm_gbs": round(gbs, 1),
+            "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def bench_unit(tr, cams, targets, steps, step0):
+    """Task units of two consecutive views (gradients summed over the union of
+    their visible sets, one sparse Adam + staging + commit per unit), timed
+    over `steps` views on one stream."""
+    import torch
+    nv = len(cams)
+    units = max(1, steps // 2)
+    version = int(tr.ring_state.cpu().numpy().view(np.uint32)[0])
+    step = step0
+    for u in range(2):                                   # warm-up
+        step += 1; version += 1
+        v = (2 * u) % nv
+        tr.step_unit([cams[v], cams[(v + 1) % nv]], step, version, [targets[v], targets[(v + 1) % nv]])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for u in range(units):
+        step += 1; version += 1
+        v = (2 * u) % nv
+        tr.step_unit([cams[v], cams[(v + 1) % nv]], step, version, [targets[v], targets[(v + 1) % nv]])
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    from paper_2607_19893_amd.pipeline import to_u32
+    assert to_u32(tr.status)[0] == 0, "device status flags set during the task units"
+    return {"units": units, "views_per_unit": 2, "views_per_s": round(2 * units / dt, 2),
+            "ms_per_unit": round(1e3 * dt / units, 4)}
 
 
 def in_front(mean, cam):
