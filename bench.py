@@ -211,8 +211,6 @@ def main():
     # bits, and the range extraction (8 B per pair)
     key_bits = 31 + int(np.ceil(np.log2(max(T_tiles, 2))))
     sort_bytes = 16 * V_mean + 12 * M_mean + 24 * M_mean * int(np.ceil(key_bits / 11)) + 8 * M_mean
-    # loss: image and target read, dL/dimg written
-    loss_bytes = 12 * 3 * H * Wd
     # per-primitive backward: the 48-byte pair slots, then per visible row the
     # parameters read (4P), the 2D record and id (68 B) and the gradient row written (4P)
     pbwd_bytes = 48 * M_mean + V_mean * (2 * row_bytes + 68)
@@ -226,8 +224,7 @@ def main():
         "project": hbm(proj_bytes),
         "visible": hbm(vis_bytes),
         "bin_sort": hbm(sort_bytes),
-        "raster_fwd": ("alu", fwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
-        "loss_l1": hbm(loss_bytes),
+        "raster_fwd_l1": ("alu", fwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
         "raster_bwd_pixels": ("alu", bwd_flops / 1e12, FP32_PEAK_TFLOPS, "TFLOP/s"),
         "raster_bwd_project": hbm(pbwd_bytes),
         "adam_publish": hbm(adam_bytes),
@@ -279,7 +276,7 @@ def main():
         "config": {"workload": w.name, "gaussians": w.scene.n, "sh_degree": w.scene.sh_degree,
                    "width": cams[0].width, "height": cams[0].height, "views": nviews,
                    "mean_visible": round(V_mean), "mean_pairs": round(M_mean),
-                   "step": "project+visible+bin_sort+fwd+L1+bwd+sparse_adam_publish+delta_apply",
+                   "step": "project+visible+bin_sort+fwd_l1+bwd+sparse_adam_publish+commit",
                    "apply_overlapped": not args.no_overlap},
         "roofline": roofline,
         "phases_ms": {k: v["ms"] for k, v in per_phase.items()},

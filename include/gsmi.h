@@ -141,7 +141,8 @@ enum {
     GS_WS_BIN_SORT = 2,
     GS_WS_RASTER_BWD = 3,
     GS_WS_LOSS = 4,
-    GS_WS_SCOPE = 5
+    GS_WS_SCOPE = 5,
+    GS_WS_RASTER_FWD_L1 = 6
 };
 /*
  * Workspace bytes a call needs, for a pool of n primitives, a pair capacity
@@ -227,6 +228,21 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
 gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,
                         int32_t width, int32_t height, const float* bg, float* img, float* final_T,
                         uint32_t* n_contrib, uint8_t* active, uint64_t* pair_stats, void* stream);
+
+/*
+ * gs_raster_fwd followed by gs_loss_l1 in one pass over the image (the
+ * render and the image loss of one training view, Section 2.1): img, final_T,
+ * n_contrib and active are gs_raster_fwd's; dL_dimg is gs_loss_l1's, bit for
+ * bit (the same fp32 comparison per channel); loss is the same mean, summed
+ * per 16x16 tile and then over the tiles in fp64, so it can differ from
+ * gs_loss_l1's value in the last fp32 bits.
+ *   target [3,H,W] fp32; loss: one float on the device
+ *   ws: gs_workspace_bytes(GS_WS_RASTER_FWD_L1, 0, 0, W, H) bytes
+ */
+gs_status gs_raster_fwd_l1(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,
+                           int32_t width, int32_t height, const float* bg, const float* target, float* img,
+                           float* final_T, uint32_t* n_contrib, uint8_t* active, float* loss, float* dL_dimg, void* ws,
+                           size_t ws_bytes, void* stream);
 
 /*
  * Image loss (Section 2.1): L = mean over all 3*H*W entries of |img - target|;

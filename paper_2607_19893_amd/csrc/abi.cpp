@@ -104,6 +104,7 @@ size_t gs_workspace_bytes(int32_t which, int32_t n, uint32_t capacity, int32_t w
         case GS_WS_RASTER_BWD: return gsmi::raster_bwd_ws_bytes(n, capacity);
         case GS_WS_LOSS: return gsmi::loss_ws_bytes(width, height);
         case GS_WS_SCOPE: return gsmi::scope_ws_bytes(n);
+        case GS_WS_RASTER_FWD_L1: return gsmi::raster_fwd_l1_ws_bytes(width, height);
         default: return 0;
     }
 }
@@ -171,6 +172,25 @@ gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, co
     return hip_status(gsmi::launch_raster_fwd(*proj, vals, ranges, width, height, bg, img, final_T, n_contrib, active,
                                               pair_stats, static_cast<hipStream_t>(stream)),
                       "gs_raster_fwd");
+}
+
+gs_status gs_raster_fwd_l1(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,
+                           int32_t width, int32_t height, const float* bg, const float* target, float* img,
+                           float* final_T, uint32_t* n_contrib, uint8_t* active, float* loss, float* dL_dimg, void* ws,
+                           size_t ws_bytes, void* stream) {
+    gs_status s;
+    if ((s = check_proj(proj, false, "gs_raster_fwd_l1")) != GS_OK) return s;
+    GS_REQUIRE(n >= 0 && width >= 0 && height >= 0, "gs_raster_fwd_l1: negative size");
+    if (width > GS_MAX_IMAGE_SIDE || height > GS_MAX_IMAGE_SIDE)
+        return fail(GS_ERR_UNSUPPORTED, "gs_raster_fwd_l1: image side above %d", GS_MAX_IMAGE_SIDE);
+    GS_REQUIRE(vals && ranges && bg && target && img && final_T && n_contrib && loss && dL_dimg && ws,
+               "gs_raster_fwd_l1: null pointer");
+    if (ws_bytes < gsmi::raster_fwd_l1_ws_bytes(width, height))
+        return fail(GS_ERR_WORKSPACE, "gs_raster_fwd_l1: workspace too small");
+    return hip_status(gsmi::launch_raster_fwd_l1(*proj, vals, ranges, width, height, bg, target, img, final_T,
+                                                 n_contrib, active, loss, dL_dimg, ws,
+                                                 static_cast<hipStream_t>(stream)),
+                      "gs_raster_fwd_l1");
 }
 
 gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32_t height, float* loss,

@@ -41,6 +41,11 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
 hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
                              int32_t height, const float bg[3], float* img, float* final_T, uint32_t* n_contrib,
                              uint8_t* active, uint64_t* pair_stats, hipStream_t st);
+size_t raster_fwd_l1_ws_bytes(int32_t width, int32_t height);
+hipError_t launch_raster_fwd_l1(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
+                                int32_t height, const float bg[3], const float* target, float* img, float* final_T,
+                                uint32_t* n_contrib, uint8_t* active, float* loss, float* dL, void* ws,
+                                hipStream_t st);
 size_t loss_ws_bytes(int32_t width, int32_t height);
 hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, int32_t height, float* loss,
                           float* dL, void* ws, hipStream_t st);

@@ -188,12 +188,24 @@ __device__ __forceinline__ uint32_t for_row(const uint32_t* v, int row) {
     return row == 0 ? v[0] : (row == 1 ? v[1] : (row == 2 ? v[2] : v[3]));
 }
 
-template <bool STATS>
+// |a - t| and the sign of a - t scaled by inv (0 for a tie): one L1 term and its derivative.
+__device__ __forceinline__ float l1_elem(float a, float t, float inv, float& dl) {
+    const float d = a - t;
+    dl = d > 0.0f ? inv : (d < 0.0f ? -inv : 0.0f);
+    return fabsf(d);
+}
+
+// LOSS: the L1 loss of the view is taken in the same pass (the image loss of
+// the view, Section 2.1): each pixel compares its three fp32 channels with
+// the target exactly as k_loss_l1 does, writes dL/dimg, and each tile leaves
+// its sum of |img - target| in loss_partial[tile] for k_loss_final.
+template <bool STATS, bool LOSS>
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, float* __restrict__ img, float* __restrict__ final_T, uint32_t* __restrict__ n_contrib,
-    uint8_t* __restrict__ active, unsigned long long* __restrict__ pair_stats) {
+    uint8_t* __restrict__ active, unsigned long long* __restrict__ pair_stats, const float* __restrict__ target,
+    float inv_total, float* __restrict__ dL, float* __restrict__ loss_partial) {
     __shared__ SplatLds<GS_BLOCK> L;
     __shared__ uint32_t s_id[GS_BLOCK];
     __shared__ uint32_t s_hit[GS_BLOCK];
@@ -288,13 +300,31 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
             atomicAdd(&pair_stats[tid], (unsigned long long)s_stat[tid][0] + s_stat[tid][1] + s_stat[tid][2] +
                                             s_stat[tid][3]);
     }
+    float lsum = 0.0f;
     if (inside) {
         const size_t HW = (size_t)W * H, p = (size_t)py * W + px;
-        img[p] = fmaf(T, bg0, c0);
-        img[HW + p] = fmaf(T, bg1, c1);
-        img[2 * HW + p] = fmaf(T, bg2, c2);
+        const float o0 = fmaf(T, bg0, c0), o1 = fmaf(T, bg1, c1), o2 = fmaf(T, bg2, c2);
+        img[p] = o0;
+        img[HW + p] = o1;
+        img[2 * HW + p] = o2;
         final_T[p] = T;
         n_contrib[p] = last;
+        if (LOSS) {
+            float g0, g1, g2;
+            lsum += l1_elem(o0, target[p], inv_total, g0);
+            lsum += l1_elem(o1, target[HW + p], inv_total, g1);
+            lsum += l1_elem(o2, target[2 * HW + p], inv_total, g2);
+            dL[p] = g0;
+            dL[HW + p] = g1;
+            dL[2 * HW + p] = g2;
+        }
+    }
+    if (LOSS) {
+        __shared__ float s_loss[4];
+        lsum = wave_sum(lsum);
+        if (lane_id() == 0) s_loss[w] = lsum;
+        __syncthreads();
+        if (tid == 0) loss_partial[tile] = (s_loss[0] + s_loss[1]) + (s_loss[2] + s_loss[3]);
     }
 }
 
@@ -302,11 +332,6 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
 // L1 loss
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ float l1_elem(float a, float t, float inv, float& dl) {
-    const float d = a - t;
-    dl = d > 0.0f ? inv : (d < 0.0f ? -inv : 0.0f);
-    return fabsf(d);
-}
 
 // Block b covers elements [b*2048, b*2048+2048): with VEC, as 512 float4
 // (all three arrays 16-byte aligned; elements past the last whole float4
@@ -978,16 +1003,40 @@ hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const ui
     const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
     if (TX * TY == 0) return hipSuccess;
     if (pair_stats)
-        hipLaunchKernelGGL(k_raster_fwd<true>, dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
+        hipLaunchKernelGGL((k_raster_fwd<true, false>), dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
                            reinterpret_cast<const float2*>(proj.mean2d),
                            reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, width, height, TX, bg[0],
                            bg[1], bg[2], img, final_T, n_contrib, active,
-                           reinterpret_cast<unsigned long long*>(pair_stats));
+                           reinterpret_cast<unsigned long long*>(pair_stats), nullptr, 0.0f, nullptr, nullptr);
     else
-        hipLaunchKernelGGL(k_raster_fwd<false>, dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
+        hipLaunchKernelGGL((k_raster_fwd<false, false>), dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
                            reinterpret_cast<const float2*>(proj.mean2d),
                            reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, width, height, TX, bg[0],
-                           bg[1], bg[2], img, final_T, n_contrib, active, nullptr);
+                           bg[1], bg[2], img, final_T, n_contrib, active, nullptr, nullptr, 0.0f, nullptr, nullptr);
+    return hipGetLastError();
+}
+
+size_t raster_fwd_l1_ws_bytes(int32_t width, int32_t height) {
+    const uint64_t T = (uint64_t)div_up((uint64_t)(width > 0 ? width : 0), GS_TILE) *
+                       div_up((uint64_t)(height > 0 ? height : 0), GS_TILE);
+    return align256(sizeof(float) * (T + 1));
+}
+
+hipError_t launch_raster_fwd_l1(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
+                                int32_t height, const float bg[3], const float* target, float* img, float* final_T,
+                                uint32_t* n_contrib, uint8_t* active, float* loss, float* dL, void* ws,
+                                hipStream_t st) {
+    const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
+    const uint64_t total = 3ull * (uint64_t)width * (uint64_t)height;
+    float* partial = static_cast<float*>(ws);
+    if (TX * TY > 0)
+        hipLaunchKernelGGL((k_raster_fwd<false, true>), dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
+                           reinterpret_cast<const float2*>(proj.mean2d),
+                           reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, width, height, TX, bg[0],
+                           bg[1], bg[2], img, final_T, n_contrib, active, nullptr, target,
+                           (float)(1.0 / (double)(total ? total : 1)), dL, partial);
+    hipLaunchKernelGGL(k_loss_final, dim3(1), dim3(GS_BLOCK), 0, st, partial, (uint32_t)(TX * TY),
+                       total ? 1.0 / (double)total : 0.0, loss);
     return hipGetLastError();
 }
 

@@ -23,7 +23,7 @@ P = ctypes.c_void_p
 i32, u32, i64, f32, sz = ctypes.c_int32, ctypes.c_uint32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
 
 GS_OK, GS_ERR_INVALID_ARG, GS_ERR_UNSUPPORTED, GS_ERR_WORKSPACE, GS_ERR_HIP = range(5)
-GS_WS_VISIBLE_SET, GS_WS_BIN_SORT, GS_WS_RASTER_BWD, GS_WS_LOSS, GS_WS_SCOPE = 1, 2, 3, 4, 5
+GS_WS_VISIBLE_SET, GS_WS_BIN_SORT, GS_WS_RASTER_BWD, GS_WS_LOSS, GS_WS_SCOPE, GS_WS_RASTER_FWD_L1 = 1, 2, 3, 4, 5, 6
 GS_PRED_U32_NONZERO, GS_PRED_U8_NONZERO, GS_PRED_BITMAP = 0, 1, 2
 (GS_GATE_NO_DELAY, GS_GATE_ADMIT, GS_GATE_WAIT_RHO, GS_GATE_WAIT_NO_ACTIVE, GS_GATE_WAIT_MISSING, GS_GATE_WAIT_SECOND,
  GS_GATE_WAIT_GRADIENT) = range(7)
@@ -90,6 +90,7 @@ _lib.gs_visible_set.argtypes = [i32, P, i32, P, P, P, sz, P]
 _lib.gs_bin_sort.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, u32, P, P, P, P, P, P, P, P, sz, P]
 _lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, P, P, P, P, P, P]
 _lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
+_lib.gs_raster_fwd_l1.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, P, P, P, P, P, P, P, P, sz, P]
 _lib.gs_raster_bwd.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P, P, P,
                                P, P, P, u32, P, P, P, P, P, i32, P, P, P, sz, P]
 _lib.gs_raster_bwd_pixels.argtypes = [ctypes.POINTER(gs_proj), ctypes.POINTER(gs_camera), P, P, P, u32, P, P, P, P,
@@ -113,14 +114,14 @@ _lib.gs_admission_gate.argtypes = [P, P, ctypes.POINTER(gs_gate_args), i32, P, P
 for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
               "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
               "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
-              "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum"):
+              "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum", "gs_raster_fwd_l1"):
     getattr(_lib, _name).restype = i32
 
 EXPORTS = ["gs_abi_version", "gs_status_string", "gs_last_error", "gs_workspace_bytes", "gs_delta_msg_bytes",
            "gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
            "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
            "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
-           "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum"]
+           "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum", "gs_raster_fwd_l1"]
 
 
 class GsmiError(RuntimeError):
@@ -226,6 +227,15 @@ def gs_raster_fwd(proj: gs_proj, n, vals, ranges, width, height, bg, img, final_
                                                       int(height), ctypes.cast(b, P), ptr(img), ptr(final_T),
                                                       ptr(n_contrib), ptr(active), ptr(pair_stats),
                                                       stream if stream is not None else current_stream()))
+
+
+def gs_raster_fwd_l1(proj: gs_proj, n, vals, ranges, width, height, bg, target, img, final_T, n_contrib, active, loss,
+                     dL_dimg, ws, stream=None):
+    b = _bg(bg)
+    return _check("gs_raster_fwd_l1", _lib.gs_raster_fwd_l1(
+        ctypes.byref(proj), int(n), ptr(vals), ptr(ranges), int(width), int(height), ctypes.cast(b, P), ptr(target),
+        ptr(img), ptr(final_T), ptr(n_contrib), ptr(active), ptr(loss), ptr(dL_dimg), ptr(ws),
+        ws.numel() * ws.element_size(), stream if stream is not None else current_stream()))
 
 
 def gs_loss_l1(img, target, width, height, loss, dL_dimg, ws, stream=None):

@@ -103,6 +103,8 @@ class ViewTrainer:
         self.ranges = _u32(2 * T, self.dev)
         self.ws_loss = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_LOSS, 0, 0, w, h), dtype=torch.uint8,
                                    device=self.dev)
+        self.ws_fwd_l1 = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_RASTER_FWD_L1, 0, 0, w, h),
+                                     dtype=torch.uint8, device=self.dev)
         if self.capacity:
             self._set_capacity(self.capacity, force=True)
 
@@ -156,6 +158,16 @@ class ViewTrainer:
             self.active.zero_()
         gsmi.gs_raster_fwd(self.proj_s, self.n, self.vals, self.ranges, self.cam.width, self.cam.height, bg, img, fT,
                            nc, self.active if active else None, self.pair_stats if stats else None)
+
+    def raster_fwd_l1(self, target=None, bg=(0.0, 0.0, 0.0), active=False):
+        """Forward raster and the L1 loss in one pass (target: device tensor of 3*H*W floats, or None for the
+        set_target buffer)."""
+        img, fT, nc, dL, tgt = self._img_views()
+        if active:
+            self.active.zero_()
+        gsmi.gs_raster_fwd_l1(self.proj_s, self.n, self.vals, self.ranges, self.cam.width, self.cam.height, bg,
+                              tgt if target is None else target, img, fT, nc, self.active if active else None,
+                              self.loss, dL, self.ws_fwd_l1)
 
     def set_target(self, target_np):
         """Copy a [3,H,W] target into the target buffer (planar, first 3*H*W floats)."""
@@ -255,10 +267,10 @@ class ViewTrainer:
         self.view_slot(k)
         self.cam, self.cam_c = cam, gsmi.make_camera(cam)
         self.bin_sort()
-        self.raster_fwd(active=False)
         if dL is None:
-            self.loss_l1(target)
+            self.raster_fwd_l1(target)
         else:
+            self.raster_fwd(active=False)
             self.set_dL(dL)
         self.raster_bwd_pixels()
         gsmi.gs_raster_bwd_project_accum(self.scene_s, self.cam_c, self.proj_s, self.pair_offset, self.vis_idx,
@@ -340,8 +352,8 @@ class ViewTrainer:
                 ev[-1].record(self.apply_stream)
 
     # -- whole view ----------------------------------------------------------
-    APPLY_AFTER = 4       # overlap mode: a view's apply starts once the next view's loss is done
-    PHASES = ("project", "visible", "bin_sort", "raster_fwd", "loss_l1", "raster_bwd_pixels", "raster_bwd_project",
+    APPLY_AFTER = 3       # overlap mode: a view's apply starts once the next view's loss is done
+    PHASES = ("project", "visible", "bin_sort", "raster_fwd_l1", "raster_bwd_pixels", "raster_bwd_project",
               "adam_publish", "apply")
 
     def step(self, cam, step, version=1, publish=True, active=False, target=None, events=None, overlap=False):
@@ -360,8 +372,9 @@ class ViewTrainer:
             k = version & 1
             msg = self.msgs[k]
             main = torch.cuda.current_stream()
-            calls = (lambda: self.project(cam), self.visible, self.bin_sort, lambda: self.raster_fwd(active=active),
-                     lambda: self.loss_l1(target), self.raster_bwd_pixels, self.raster_bwd_project)
+            calls = (lambda: self.project(cam), self.visible, self.bin_sort,
+                     lambda: self.raster_fwd_l1(target, active=active), self.raster_bwd_pixels,
+                     self.raster_bwd_project)
             if ev:
                 ev[0].record()
             for i, fn in enumerate(calls):
@@ -379,8 +392,8 @@ class ViewTrainer:
                 ev[len(calls) + 1].record()
             self._pending = (version, ev)
             return
-        calls = (lambda: self.project(cam), self.visible, self.bin_sort, lambda: self.raster_fwd(active=active),
-                 lambda: self.loss_l1(target), self.raster_bwd_pixels, self.raster_bwd_project,
+        calls = (lambda: self.project(cam), self.visible, self.bin_sort,
+                 lambda: self.raster_fwd_l1(target, active=active), self.raster_bwd_pixels, self.raster_bwd_project,
                  (lambda: self.adam_publish(step, version, self.msgs[version & 1])) if publish
                  else (lambda: self.adam(step)),
                  (lambda: self.commit(version)) if publish else (lambda: None))

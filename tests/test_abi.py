@@ -77,6 +77,12 @@ def test_null_and_range_arguments_rejected(gs):
     assert L.gs_delta_apply(16, 8, g, 1, 10, 10, 0, None, 16, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_delta_pack(16, 16, 10, g, 1, 1, 8, 1024, 16, None) == gs.GS_ERR_INVALID_ARG  # misaligned msg
     assert L.gs_loss_l1(None, None, 4, 4, None, None, None, 0, None) == gs.GS_ERR_INVALID_ARG
+    # fused forward + loss: workspace sized per tile
+    assert L.gs_raster_fwd_l1(ctypes.byref(pr), 10, 16, 16, 256, 256, 16, 16, 16, 16, 16, None, 16, 16, 16, 0,
+                              None) == gs.GS_ERR_WORKSPACE
+    assert L.gs_raster_fwd_l1(ctypes.byref(pr), 10, 16, 16, 256, 256, 16, None, 16, 16, 16, None, 16, 16, 16, 1 << 20,
+                              None) == gs.GS_ERR_INVALID_ARG
+    assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_FWD_L1, 0, 0, 1920, 1080) >= 4 * 120 * 68
     # versioned commit of a ring slot
     ring = gs.gs_ring()
     ring.slot[0], ring.slot[1], ring.slot_bytes, ring.state = 16, 32, 4096, 16

@@ -171,6 +171,31 @@ def test_loss_l1(case, torch_gpu, orc):
     assert abs(tr.loss.item() - loss) <= 1e-5 * abs(loss)
 
 
+@pytest.mark.parametrize("case", CASES)
+def test_raster_fwd_l1_matches_separate_calls(case, torch_gpu, orc):
+    """gs_raster_fwd_l1 = gs_raster_fwd then gs_loss_l1: image, transmittance,
+    contributor counts, active flags and dL/dimg bit for bit; the loss to the
+    last fp32 bits (tile partial sums instead of 2048-element blocks)."""
+    w = get_case(case)
+    tr = trainer_for(w, torch_gpu)
+    cam = w.cameras[0]
+    tr.set_target(w.target(0))
+    tr.project(cam); tr.visible(); tr.bin_sort()
+    tr.raster_fwd(active=True); tr.loss_l1()
+    torch_gpu.cuda.synchronize()
+    ref = [t.clone() for t in (tr.img, tr.final_T, tr.n_contrib, tr.dL, tr.active)]
+    loss_ref = float(tr.loss.item())
+    for t in (tr.img, tr.final_T, tr.n_contrib, tr.dL, tr.active, tr.loss):
+        t.fill_(7)
+    tr.raster_fwd_l1(active=True)
+    torch_gpu.cuda.synchronize()
+    H, W = cam.height, cam.width
+    for a, b, k in zip((tr.img, tr.final_T, tr.n_contrib, tr.dL, tr.active), ref, (3 * H * W, H * W, H * W,
+                                                                                   3 * H * W, w.scene.n)):
+        assert torch_gpu.equal(a.reshape(-1)[:k], b.reshape(-1)[:k])
+    assert abs(float(tr.loss.item()) - loss_ref) <= 1e-6 * abs(loss_ref)
+
+
 def masked_upstream(orc, w, cam, dL, loss_margin=None):
     """dL with the ambiguous pixels zeroed: a pixel's decisions reach the
     gradients only through its own upstream gradient, so with dL = 0 there the
