@@ -124,36 +124,20 @@ __device__ __forceinline__ float exp_neg(float sigma) {
 __device__ __forceinline__ bool wave_any(bool p) { return __ballot(p) != 0ull; }
 __device__ __forceinline__ bool uniform(bool p) { return __builtin_amdgcn_readfirstlane((int)p) != 0; }
 
-// Per batch, each wave first compacts the batch entries whose footprint can
-// reach its 16x4 strip into a wave-private LDS list (ascending, via ballots),
-// then walks only that list.  Only the wave itself reads its list, so a
-// wave-level barrier orders the writes before the reads.
-template <int NB>
-__device__ __forceinline__ uint32_t compact_touching(const SplatLds<NB>& L, int nb, float x0, float x1, float y0,
-                                                     float y1, uint32_t limit, uint8_t* list) {
-    const int lane = lane_id();
-    const uint64_t lt = lanemask_lt();
-    uint32_t cnt = 0;
-#pragma unroll
-    for (int r = 0; r < NB / GS_WAVE; ++r) {
-        const int k = r * GS_WAVE + lane;
-        const bool t = k < nb && (uint32_t)k < limit && splat_touches(L, k, x0, x1, y0, y1);
-        const uint64_t m = __ballot(t);
-        if (t) list[cnt + popc64(m & lt)] = (uint8_t)k;
-        cnt += popc64(m);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    return cnt;
-}
-
 // Row-wise lists: each 16-lane row of a wave (one pixel row of the tile)
-// keeps its own ascending list of the batch entries whose footprint box
-// reaches that row's pixel centres (and lie below the row's limit).  The four
-// rows of a wave then walk their lists in lockstep, so an entry costs a
-// quarter of a wave step for every pixel row it reaches instead of a whole
-// step for every 16x4 strip.  cnt[r] receives the length of row r's list.
+// keeps its own ascending list of the batch entries whose footprint reaches
+// that row's pixel centres (and lie below the row's limit).  The four rows of
+// a wave then walk their lists in lockstep, so an entry costs a quarter of a
+// wave step for every pixel row it reaches instead of a whole step for every
+// 16x4 strip.  cnt[r] receives the length of row r's list.
+//
+// An entry reaches row y if sigma <= s somewhere on the row's segment of
+// pixel centres [x0, x1] (s = ln(255 o) + kCutMargin as for hx, hy): the
+// footprint box is tested first, then the minimum of sigma over the segment,
+// which for the row's dy is the quadratic's vertex dx = -(B/A) dy clamped to
+// the segment's offsets [u - x1, u - x0], in fp64 (the staged values are
+// exact).  Any pixel of a skipped row is at least the cut-off margin below
+// the 1/255 threshold.
 template <int NB>
 __device__ __forceinline__ void compact_rows(const SplatLds<NB>& L, int nb, float x0, float x1, float y0,
                                              const uint32_t* lim, uint8_t (*list)[NB], uint32_t* cnt) {
@@ -165,14 +149,24 @@ __device__ __forceinline__ void compact_rows(const SplatLds<NB>& L, int nb, floa
     for (int r = 0; r < NB / GS_WAVE; ++r) {
         const int k = r * GS_WAVE + lane;
         const bool valid = k < nb;
-        const double2 p = L.P[valid ? k : 0];
+        const int kk = valid ? k : 0;
+        const double2 p = L.P[kk];
+        const double2 qd = L.Q[kk];
+        const SplatR R = L.R[kk];
         const float u = (float)p.x, v = (float)p.y;
-        const float hx = L.R[valid ? k : 0].hx, hy = L.S[valid ? k : 0].w;
+        const float hx = R.hx, hy = L.S[kk].w;
         const bool bx = valid && (u + hx >= x0) && (u - hx <= x1);
+        const double cut = (double)(logf(255.0f * R.o) + kCutMargin);
+        const bool convex = qd.x > 0.0;                      // A > 0 for every projected conic; else no row test
+        const double slope = convex ? -qd.y / (2.0 * qd.x) : 0.0;   // vertex offset per unit dy: -B / A
+        const double dlo = p.x - (double)x1, dhi = p.x - (double)x0;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const float y = y0 + (float)q;
-            const bool t = bx && (uint32_t)k < lim[q] && (v + hy >= y) && (v - hy <= y);
+            const double dy = p.y - (double)y;
+            const double dx = fmin(fmax(slope * dy, dlo), dhi);
+            const double smin = dx * fma(qd.x, dx, qd.y * dy) + R.c2 * dy * dy;
+            const bool t = bx && (uint32_t)k < lim[q] && (v + hy >= y) && (v - hy <= y) && (smin <= cut || !convex);
             const uint64_t m = __ballot(t);
             if (t) list[q][cnt[q] + popc64(m & lt)] = (uint8_t)k;
             cnt[q] += popc64(m);
