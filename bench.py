@@ -95,6 +95,9 @@ def main():
     ap.add_argument("--no-overlap", action="store_true",
                     help="run every phase on one stream (by default each view's apply to the replica runs on a "
                          "second stream, beside the next view's backward raster)")
+    ap.add_argument("--apply-after", type=int, default=None,
+                    help="phase index after which the previous view's commit starts on the second stream "
+                         "(default: the pipeline's choice)")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the separate timings of the scope hazards / admission gate and of two-view task units")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -120,6 +123,8 @@ def main():
     cams = w.cameras
     log("workload %s: n=%d, %d views, %dx%d (generated in %.1fs)" % (w.name, w.scene.n, len(cams), cams[0].width,
                                                                      cams[0].height, time.time() - t0))
+    if args.apply_after is not None:
+        ViewTrainer.APPLY_AFTER = args.apply_after
     tr = ViewTrainer(w.scene, capacity=1, max_width=max(c.width for c in cams),
                      max_height=max(c.height for c in cams), lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps)
     need = tr.ensure_capacity(cams)

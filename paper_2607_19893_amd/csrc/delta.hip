@@ -138,6 +138,11 @@ __global__ void k_commit_order(const uint32_t* __restrict__ msg, uint32_t versio
     else if (ring_state[0] + 1u != version) atomicOr(&status->flags, GS_DEV_MSG_ORDER);
 }
 
+// Rows are taken kCommitRows at a time per lane group, with all their loads
+// issued before any store, so a wave keeps several independent row gathers
+// in flight (the loads of one row depend only on its id).
+constexpr int kCommitRows = 4;
+
 __global__ void __launch_bounds__(GS_BLOCK) k_commit(GroupArgs a, const uint32_t* __restrict__ msg, int32_t mode,
                                                      uint32_t* __restrict__ prim_version, uint32_t* __restrict__ skip,
                                                      uint32_t* __restrict__ ring_state,
@@ -152,32 +157,49 @@ __global__ void __launch_bounds__(GS_BLOCK) k_commit(GroupArgs a, const uint32_t
     int sub, grp, c;
     lane_group(a, lane, sub, grp, c);
     const bool in_row = sub < a.rows_per_wave;
-    float* __restrict__ dst = a.ptr[in_row ? grp : 0];
-    const int cols = a.cols[in_row ? grp : 0];
-    const int col = lane - sub * a.row_len;
+    if (!in_row) grp = c = 0;                  // spare lanes read row 0's first column and store nothing
+    float* __restrict__ dst = a.ptr[grp];
+    const int cols = a.cols[grp];
+    const int col = in_row ? lane - sub * a.row_len : 0;
+    const uint32_t rpw = (uint32_t)a.rows_per_wave;
     const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
     const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
     uint32_t left = 0;
     // every lane of the wave runs the same number of iterations (rows are
-    // strided by whole waves), so the wave-level counts below see all lanes
-    for (uint32_t r0 = wave * a.rows_per_wave; r0 < K; r0 += waves * a.rows_per_wave) {
-        const uint32_t r = r0 + (uint32_t)sub;
-        if (!in_row || r >= K) continue;
-        const uint32_t id = ids[r];
-        // the three loads depend only on id, so they are in flight together;
-        // every lane of the row reads the version before lane 0 stamps it
-        const uint32_t pv = prim_version[id];
-        const float val = rows[(size_t)r * a.row_len + col];
-        float* q = dst + (size_t)id * cols + c;
-        const float old = *q;
-        const bool newer = pv < version;
-        if (newer) *q = (mode == GS_APPLY_ADD) ? (old + val) : val;
-        if (col == 0) {
-            if (newer)
-                prim_version[id] = version;
-            else
-                ++left;
-            if (skip && skip[id] == version) skip[id] = 0u;
+    // strided by whole waves), so the wave-level count below sees all lanes.
+    // Loads are unconditional (rows past the end read row 0; every id was
+    // checked against n_rows), so they are all in flight before the first use.
+    for (uint32_t r0 = wave * rpw * kCommitRows; r0 < K; r0 += waves * rpw * kCommitRows) {
+        uint32_t rr[kCommitRows], id[kCommitRows], pv[kCommitRows];
+        float val[kCommitRows], old[kCommitRows];
+        bool ok[kCommitRows];
+#pragma unroll
+        for (int u = 0; u < kCommitRows; ++u) {
+            const uint32_t r = r0 + (uint32_t)u * rpw + (uint32_t)sub;
+            ok[u] = in_row && r < K;
+            rr[u] = ok[u] ? r : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kCommitRows; ++u) id[u] = ids[rr[u]];
+#pragma unroll
+        for (int u = 0; u < kCommitRows; ++u) {
+            // every lane of the row reads the version before lane 0 stamps it
+            pv[u] = prim_version[id[u]];
+            val[u] = rows[(size_t)rr[u] * a.row_len + col];
+            old[u] = dst[(size_t)id[u] * cols + c];
+        }
+#pragma unroll
+        for (int u = 0; u < kCommitRows; ++u) {
+            if (!ok[u]) continue;
+            const bool newer = pv[u] < version;
+            if (newer) dst[(size_t)id[u] * cols + c] = (mode == GS_APPLY_ADD) ? (old[u] + val[u]) : val[u];
+            if (col == 0) {
+                if (newer)
+                    prim_version[id[u]] = version;
+                else
+                    ++left;
+                if (skip && skip[id[u]] == version) skip[id[u]] = 0u;
+            }
         }
     }
     // rows left behind are rare (a later version already published them):
@@ -228,8 +250,8 @@ hipError_t launch_publish_commit(const gs_ring& ring, uint32_t version, const gs
     hipLaunchKernelGGL(k_apply_check, dim3(cb), dim3(GS_BLOCK), 0, st, a, msg, (uint64_t)ring.slot_bytes, n_rows,
                        max_rows, status);
     hipLaunchKernelGGL(k_commit_order, dim3(1), dim3(1), 0, st, msg, version, ring.state, status);
-    hipLaunchKernelGGL(k_commit, dim3(row_blocks(max_rows, a.rows_per_wave)), dim3(GS_BLOCK), 0, st, a, msg, mode,
-                       prim_version, skip, ring.state, status);
+    hipLaunchKernelGGL(k_commit, dim3(row_blocks(max_rows, a.rows_per_wave * kCommitRows)), dim3(GS_BLOCK), 0, st, a,
+                       msg, mode, prim_version, skip, ring.state, status);
     hipLaunchKernelGGL(k_commit_finish, dim3(1), dim3(1), 0, st, msg, version, ring.state, status);
     return hipGetLastError();
 }
