@@ -446,6 +446,9 @@ typedef struct {
     void* slot[2];
     size_t slot_bytes;
     uint32_t* state;
+    int32_t background;       /* nonzero: the commit is meant to run beside compute-bound work on another
+                                 stream and is launched with one workgroup per compute unit, taking a
+                                 small share of every CU instead of all of them */
 } gs_ring;
 
 gs_status gs_publish_commit(const gs_ring* ring, uint32_t version, const gs_group* dst, int32_t n_groups,

@@ -2,11 +2,35 @@
 // No entry point allocates, frees or synchronizes.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 
 #include "internal.h"
+
+namespace gsmi {
+
+// The device-property cache: compute units per device, filled on first use.
+uint32_t compute_units() {
+    static std::atomic<uint32_t> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+    if (dev >= 64) {
+        int v = 0;
+        return hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess ? (uint32_t)v : 0;
+    }
+    uint32_t c = cache[dev].load(std::memory_order_relaxed);
+    if (c == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) return 0;
+        c = (uint32_t)v;
+        cache[dev].store(c, std::memory_order_relaxed);
+    }
+    return c;
+}
+
+}  // namespace gsmi
 
 namespace {
 

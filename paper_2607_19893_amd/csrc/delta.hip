@@ -250,8 +250,13 @@ hipError_t launch_publish_commit(const gs_ring& ring, uint32_t version, const gs
     hipLaunchKernelGGL(k_apply_check, dim3(cb), dim3(GS_BLOCK), 0, st, a, msg, (uint64_t)ring.slot_bytes, n_rows,
                        max_rows, status);
     hipLaunchKernelGGL(k_commit_order, dim3(1), dim3(1), 0, st, msg, version, ring.state, status);
-    hipLaunchKernelGGL(k_commit, dim3(row_blocks(max_rows, a.rows_per_wave * kCommitRows)), dim3(GS_BLOCK), 0, st, a,
-                       msg, mode, prim_version, skip, ring.state, status);
+    uint32_t blocks = row_blocks(max_rows, a.rows_per_wave * kCommitRows);
+    if (ring.background) {
+        const uint32_t cus = compute_units();
+        if (cus > 0 && blocks > cus) blocks = cus;
+    }
+    hipLaunchKernelGGL(k_commit, dim3(blocks), dim3(GS_BLOCK), 0, st, a, msg, mode, prim_version, skip, ring.state,
+                       status);
     hipLaunchKernelGGL(k_commit_finish, dim3(1), dim3(1), 0, st, msg, version, ring.state, status);
     return hipGetLastError();
 }

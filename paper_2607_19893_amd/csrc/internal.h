@@ -19,6 +19,9 @@ struct CamArgs {
 
 CamArgs make_cam_args(const gs_camera* c);
 
+// Compute units of the current device (cached per device; 0 if the query fails).
+uint32_t compute_units();
+
 // project.hip
 hipError_t launch_project(const gs_scene& s, const CamArgs& cam, const gs_proj& out, hipStream_t st);
 

@@ -58,7 +58,7 @@ class gs_group(ctypes.Structure):
 
 
 class gs_ring(ctypes.Structure):
-    _fields_ = [("slot", P * 2), ("slot_bytes", sz), ("state", P)]
+    _fields_ = [("slot", P * 2), ("slot_bytes", sz), ("state", P), ("background", i32)]
 
 
 class gs_gate_args(ctypes.Structure):
@@ -327,13 +327,15 @@ def gs_delta_apply(msg, groups_arr, n_groups, n_rows, max_rows, mode, prim_versi
                                                         stream if stream is not None else current_stream()))
 
 
-def make_ring(slots, state) -> gs_ring:
-    """slots: two device tensors of equal byte size (slot v & 1 holds version v); state: >= 8 uint32 words."""
+def make_ring(slots, state, background=False) -> gs_ring:
+    """slots: two device tensors of equal byte size (slot v & 1 holds version v); state: >= 8 uint32 words;
+    background: the commit runs beside compute on another stream (one workgroup per compute unit)."""
     nb = min(t.numel() * t.element_size() for t in slots)
     r = gs_ring()
     r.slot[0], r.slot[1] = slots[0].data_ptr(), slots[1].data_ptr()
     r.slot_bytes = nb
     r.state = state.data_ptr()
+    r.background = 1 if background else 0
     return r
 
 

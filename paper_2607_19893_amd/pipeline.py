@@ -86,6 +86,7 @@ class ViewTrainer:
         self.msg = self.msgs[0]
         self.ring_state = _u32(8, self.dev)
         self.ring = gsmi.make_ring(self.msgs, self.ring_state)
+        self.ring_bg = gsmi.make_ring(self.msgs, self.ring_state, background=True)
         self.skip = None            # per-primitive skip metadata of admitted delayed reads (optional)
 
     # -- buffers -------------------------------------------------------------
@@ -311,10 +312,11 @@ class ViewTrainer:
         gsmi.gs_delta_apply(self.msg if msg is None else msg, self.replica_arr, 5, self.n, self.n, mode,
                             self.version, self.status)
 
-    def commit(self, version, mode=gsmi.GS_APPLY_ADD):
-        """Commit the update staged for `version` (in msgs[version & 1]) into the replica, in version order."""
-        gsmi.gs_publish_commit(self.ring, version, self.replica_arr, 5, self.n, self.n, mode, self.version, self.skip,
-                               self.status)
+    def commit(self, version, mode=gsmi.GS_APPLY_ADD, background=False):
+        """Commit the update staged for `version` (in msgs[version & 1]) into the replica, in version order
+        (background: it runs beside compute on the second stream)."""
+        gsmi.gs_publish_commit(self.ring_bg if background else self.ring, version, self.replica_arr, 5, self.n,
+                               self.n, mode, self.version, self.skip, self.status)
 
     def enable_overlap(self):
         """Run each view's apply to the replica on a second stream (default
@@ -346,7 +348,7 @@ class ViewTrainer:
                 self.apply_stream.wait_event(after)
             if ev:
                 ev[-2].record(self.apply_stream)
-            self.commit(version)
+            self.commit(version, background=True)
             self.app_ev[k].record(self.apply_stream)
             if ev:
                 ev[-1].record(self.apply_stream)

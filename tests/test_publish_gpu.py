@@ -23,7 +23,7 @@ def u32(t):
 
 
 class Ring:
-    def __init__(self, torch, gs, n, rng):
+    def __init__(self, torch, gs, n, rng, background=False):
         self.torch, self.gs, self.n = torch, gs, n
         dev = torch.device("cuda")
         self.base = [rng.standard_normal((n, c)).astype(np.float32) for c in COLS]
@@ -31,7 +31,7 @@ class Ring:
         nbytes = gs.gs_delta_msg_bytes(n, sum(COLS), len(COLS))
         self.slots = [torch.zeros((nbytes + 15) // 4, dtype=torch.int32, device=dev) for _ in range(2)]
         self.state = torch.zeros(8, dtype=torch.int32, device=dev)
-        self.ring = gs.make_ring(self.slots, self.state)
+        self.ring = gs.make_ring(self.slots, self.state, background=background)
         self.ver = torch.zeros(n, dtype=torch.int32, device=dev)
         self.skip = torch.zeros(n, dtype=torch.int32, device=dev)
         self.status = torch.zeros(4, dtype=torch.int32, device=dev)
@@ -72,10 +72,12 @@ def check_equal(r, groups, ver, skip, state):
 
 @pytest.mark.parametrize("n", [64, 70001])
 @pytest.mark.parametrize("mode", ["add", "overwrite"])
-def test_publish_commit_in_order(n, mode, env, orc):
+@pytest.mark.parametrize("background", [False, True])
+def test_publish_commit_in_order(n, mode, background, env, orc):
+    """background: the narrow launch meant to run beside compute gives the same result."""
     torch, gs = env
     rng = np.random.default_rng(n + (mode == "add"))
-    r = Ring(torch, gs, n, rng)
+    r = Ring(torch, gs, n, rng, background=background)
     groups = [a.copy() for a in r.base]
     ver = np.zeros(n, np.uint32)
     ver[rng.integers(0, n, max(1, n // 50))] = 100          # rows already carrying a later publication
