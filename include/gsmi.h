@@ -194,7 +194,7 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
  *   vals   [capacity] uint32  primitive id of every sorted pair
  *   ranges [T,2] uint32       [start, end) of each tile's pairs, T = tiles in the image
  *   pair_offset [n] uint32    per visible primitive: first of its pairs in
- *                             emission order (primitives in depth order, each one's
+ *                             emission order (primitives in ascending id order, each one's
  *                             rectangle row-major); read by gs_raster_bwd
  *   pair_emit [capacity] uint32  emission position of every sorted pair
  *                             (pair_offset[id] + tile number in id's rectangle)

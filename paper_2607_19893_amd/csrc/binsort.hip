@@ -1,16 +1,19 @@
 // Rendering phase, part 1: duplicate visible primitives per touched tile and
 // order the pairs by (tile, depth, primitive id).
 //
-// Instead of one wide radix sort over 64-bit (tile, depth) keys, the order is
-// built in two narrow steps:
-//   1. sort the V visible primitives by the bits of their fp32 depth (31
-//      significant bits, 4 LSD passes over V keys, stable, so equal depths
-//      keep ascending ids because the visible list is ascending);
-//   2. emit every primitive's tile pairs in that depth order and stable-sort
-//      the M pairs by tile id only (ceil(log2 T) bits: 1-2 passes).
-// Stability of step 2 keeps the depth order inside each tile, so the result
-// is exactly the (tile, depth bits, id) order, with M-sized passes cut from
-// 4-6 to 1-2.
+// Instead of one wide radix sort over 64-bit (tile, depth) keys:
+//   1. every visible primitive's tile pairs are emitted in visible-set order
+//      (ascending ids), each primitive's rectangle row-major, so a primitive's
+//      pairs are contiguous ("emission order");
+//   2. the M pairs are sorted by tile id only (ceil(log2 T) bits: 1-2 LSD
+//      passes), carrying each pair's emission position;
+//   3. each tile's segment is sorted by (depth bits, emission position) in LDS
+//      by one workgroup (a bitonic network; segments longer than the LDS
+//      capacity are sorted in global memory by the same workgroup).  Emission
+//      positions grow with the primitive id inside a tile, so this is exactly
+//      the (tile, depth bits, id) order.
+// Step 3 replaces a 4-pass radix sort of the visible set by depth (12
+// latency-bound launches) with one launch whose work is local to a tile.
 //
 // Each LSD pass is three launches: per-block digit histograms (digit-major
 // matrix), a per-digit scan across blocks, and a scatter whose in-block rank
@@ -26,7 +29,6 @@ namespace {
 // Digit widths (8 bits: wider digits cost more per pass in these small,
 // latency-bound launches than the pass they save).  Every kernel takes the
 // digit width as a template parameter; a block holds 2^BITS counters in LDS.
-constexpr int kDepthBits = 8;
 constexpr int kTileBits = 8;
 
 template <int BITS>
@@ -187,35 +189,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_radix_scatter(
     }
 }
 
-// Depth keys of the visible primitives (key = fp32 bits, value = id), in the
-// sort's 2048-key blocks, with each block's histogram of the first digit
-// (bits 0-7) written as column b of the digit-major matrix -- the first
-// pass's histogram launch is not needed.
-__global__ void __launch_bounds__(GS_BLOCK) k_depth_keys(const uint32_t* __restrict__ vis_idx,
-                                                         const uint32_t* __restrict__ vis_count,
-                                                         const float* __restrict__ depth,
-                                                         uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
-                                                         uint32_t* __restrict__ hist, uint32_t nblocks) {
-    __shared__ uint32_t h[1 << kDepthBits];
-    for (int d = threadIdx.x; d < (1 << kDepthBits); d += GS_BLOCK) h[d] = 0;
-    __syncthreads();
-    const uint32_t V = *vis_count;
-#pragma unroll
-    for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t r = blockIdx.x * GS_TILE_ITEMS + k * GS_BLOCK + threadIdx.x;
-        if (r < V) {
-            const uint32_t g = vis_idx[r];
-            const uint32_t key = __float_as_uint(depth[g]);
-            keys[r] = key;
-            vals[r] = g;
-            atomicAdd(&h[key & ((1u << kDepthBits) - 1u)], 1u);
-        }
-    }
-    __syncthreads();
-    for (int d = threadIdx.x; d < (1 << kDepthBits); d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = h[d];
-}
-
-// per-block sums of tiles[] in depth order
+// per-block sums of tiles[] in visible-set order
 __global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restrict__ order,
                                                         const uint32_t* __restrict__ vis_count,
                                                         const uint32_t* __restrict__ tiles,
@@ -233,8 +207,8 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restri
     if (threadIdx.x == 0) bsum[blockIdx.x] = t;
 }
 
-// Exclusive offsets in depth order: pair_offset[id] and offs_r[rank], with
-// offs_r[V] = M as a sentinel.  Also publishes the pair count and the
+// Exclusive offsets in visible-set order: pair_offset[id] and offs_r[rank],
+// with offs_r[V] = M as a sentinel.  Also publishes the pair count and the
 // overflow flag.
 __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
     const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
@@ -342,31 +316,130 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
     for (int d = threadIdx.x; d < (1 << kTileBits); d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = h[d];
 }
 
-// Tile ranges, primitive ids and optional 64-bit keys of the sorted pairs.
-// The tile sort carried every pair's emission position as its value, so the
-// primitive id is a gather from the emission-ordered ids.
-__global__ void __launch_bounds__(GS_BLOCK) k_finalize(const uint32_t* __restrict__ skeys,
-                                                       const uint32_t* __restrict__ pair_emit,
-                                                       const uint32_t* __restrict__ emit_vals,
-                                                       const uint32_t* __restrict__ sort_count,
-                                                       const float* __restrict__ depth,
-                                                       uint32_t* __restrict__ ranges, uint64_t* __restrict__ keys64,
-                                                       uint32_t* __restrict__ vals) {
+// Per-tile ordering: LDS capacity in pairs (8 per thread) and the largest key.
+constexpr int kSortCap = GS_TILE_ITEMS;
+constexpr unsigned long long kKeyMax = ~0ull;
+
+__device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* __restrict__ a, uint32_t n, uint32_t x) {
+    uint32_t lo = 0, hi = n;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (a[mid] < x) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
+
+// Bitonic network over s[0..np) (np a power of two, entries past the data
+// hold kKeyMax), in the variant whose compare-exchanges all put the smaller
+// key at the lower index: each merge of width k first compares i with its
+// mirror i ^ (k - 1), then i with i ^ j for j = k/4 .. 1.
+__device__ __forceinline__ void bitonic_lds(unsigned long long* s, uint32_t np) {
+    for (uint32_t k = 2; k <= np; k <<= 1) {
+        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+            const uint32_t mask = (j == (k >> 1)) ? (k - 1) : j;
+            for (uint32_t c = threadIdx.x; c < (np >> 1); c += GS_BLOCK) {
+                // c-th compare-exchange: lower index i has bit log2(j) clear
+                const uint32_t i = ((c & ~(j - 1)) << 1) | (c & (j - 1));
+                const uint32_t q = i ^ mask;
+                const unsigned long long a = s[i], b = s[q];
+                if (b < a) {
+                    s[i] = b;
+                    s[q] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// The same network on a segment of global memory of any length n: entries
+// at n and beyond are taken as kKeyMax, so a compare-exchange that reaches
+// past the data leaves the lower (real) entry in place.
+__device__ void bitonic_global(unsigned long long* s, uint32_t n) {
+    uint32_t np = 1;
+    while (np < n) np <<= 1;
+    for (uint32_t k = 2; k <= np; k <<= 1) {
+        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+            const uint32_t mask = (j == (k >> 1)) ? (k - 1) : j;
+            for (uint32_t c = threadIdx.x; c < (np >> 1); c += GS_BLOCK) {
+                const uint32_t i = ((c & ~(j - 1)) << 1) | (c & (j - 1));
+                const uint32_t q = i ^ mask;
+                if (q >= n) continue;
+                const unsigned long long a = s[i], b = s[q];
+                if (b < a) {
+                    s[i] = b;
+                    s[q] = a;
+                }
+            }
+            __threadfence_block();
+            __syncthreads();
+        }
+    }
+}
+
+// One workgroup per tile: find the tile's segment of the tile-sorted pairs,
+// order it by (depth bits, emission position), and write the tile's range,
+// the primitive ids, the sorted -> emission map and the optional 64-bit keys.
+// pair_emit holds the segment's emission positions on entry (any order).
+__global__ void __launch_bounds__(GS_BLOCK) k_tile_depth_sort(const uint32_t* __restrict__ skeys,
+                                                              const uint32_t* __restrict__ sort_count,
+                                                              const uint32_t* __restrict__ emit_id,
+                                                              const float* __restrict__ depth,
+                                                              uint32_t* __restrict__ pair_emit,
+                                                              uint32_t* __restrict__ vals,
+                                                              uint32_t* __restrict__ ranges,
+                                                              uint64_t* __restrict__ keys64,
+                                                              unsigned long long* __restrict__ scratch) {
+    __shared__ unsigned long long s_key[kSortCap];
+    __shared__ uint32_t s_range[2];
+    const uint32_t t = blockIdx.x;
     const uint32_t M = *sort_count;
-    const uint32_t i = blockIdx.x * GS_BLOCK + threadIdx.x;
-    if (i >= M) return;
-    const uint32_t t = skeys[i];
-    const uint32_t g = emit_vals[pair_emit[i]];
-    vals[i] = g;
-    if (i == 0 || skeys[i - 1] != t) ranges[2 * t] = i;
-    if (i == M - 1 || skeys[i + 1] != t) ranges[2 * t + 1] = i + 1;
-    if (keys64) keys64[i] = ((uint64_t)t << 32) | (uint64_t)__float_as_uint(depth[g]);
+    if (threadIdx.x < 2) s_range[threadIdx.x] = lower_bound_u32(skeys, M, t + threadIdx.x);
+    __syncthreads();
+    const uint32_t start = s_range[0], end = s_range[1];
+    const uint32_t n = end - start;
+    if (threadIdx.x == 0) {
+        ranges[2 * t] = n ? start : 0u;
+        ranges[2 * t + 1] = n ? end : 0u;
+    }
+    if (n == 0) return;
+    unsigned long long* key = s_key;
+    if (n <= (uint32_t)kSortCap) {
+        uint32_t np = 2;
+        while (np < n) np <<= 1;
+        for (uint32_t i = threadIdx.x; i < np; i += GS_BLOCK) {
+            unsigned long long k = kKeyMax;
+            if (i < n) {
+                const uint32_t e = pair_emit[start + i];
+                k = ((unsigned long long)__float_as_uint(depth[emit_id[e]]) << 32) | e;
+            }
+            s_key[i] = k;
+        }
+        __syncthreads();
+        bitonic_lds(s_key, np);
+    } else {
+        key = scratch + start;
+        for (uint32_t i = threadIdx.x; i < n; i += GS_BLOCK) {
+            const uint32_t e = pair_emit[start + i];
+            key[i] = ((unsigned long long)__float_as_uint(depth[emit_id[e]]) << 32) | e;
+        }
+        __threadfence_block();
+        __syncthreads();
+        bitonic_global(key, n);
+    }
+    for (uint32_t i = threadIdx.x; i < n; i += GS_BLOCK) {
+        const unsigned long long k = key[i];
+        const uint32_t e = (uint32_t)k;
+        vals[start + i] = emit_id[e];
+        pair_emit[start + i] = e;
+        if (keys64) keys64[start + i] = ((uint64_t)t << 32) | (k >> 32);
+    }
 }
 
 struct BinsortLayout {
-    size_t dk[3], dv[3];      // depth sort: in, tmp, out
     size_t pk[3], pv[3];      // pair sort keys: in, tmp, out; pv[0] = primitive of each emitted pair,
                               // pv[1..2] = value ping-pong (values out = caller's pair_emit)
+    size_t scratch;           // 64-bit keys of tiles longer than the LDS sort
     size_t hist, totals, bsum, offs, counters;
     size_t bytes;
     uint32_t nblocks_hist;
@@ -376,13 +449,12 @@ BinsortLayout binsort_layout(int32_t n, uint32_t capacity) {
     BinsortLayout L;
     size_t o = 0;
     const size_t nn = (size_t)(n > 0 ? n : 1), cc = (size_t)(capacity > 0 ? capacity : 1);
-    for (int i = 0; i < 3; ++i) { L.dk[i] = o; o += align256(4 * nn); }
-    for (int i = 0; i < 3; ++i) { L.dv[i] = o; o += align256(4 * nn); }
     for (int i = 0; i < 3; ++i) { L.pk[i] = o; o += align256(4 * cc); }
     for (int i = 0; i < 3; ++i) { L.pv[i] = o; o += align256(4 * cc); }
+    L.scratch = o; o += align256(8 * cc);
     L.nblocks_hist = div_up(nn > cc ? nn : cc, GS_TILE_ITEMS);
-    L.hist = o; o += align256(4 * ((size_t)1 << kDepthBits) * L.nblocks_hist);
-    L.totals = o; o += align256(4 * ((size_t)1 << kDepthBits));
+    L.hist = o; o += align256(4 * ((size_t)1 << kTileBits) * L.nblocks_hist);
+    L.totals = o; o += align256(4 * ((size_t)1 << kTileBits));
     L.bsum = o; o += align256(4 * ((size_t)div_up(nn, GS_TILE_ITEMS) + 1));
     L.offs = o; o += align256(4 * (nn + 1));
     L.counters = o; o += 256;
@@ -440,26 +512,16 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     uint32_t* totals = at<uint32_t>(ws, L.totals);
     uint32_t* bsum = at<uint32_t>(ws, L.bsum);
     uint32_t* ctr = at<uint32_t>(ws, L.counters);   // [0] M, [1] sort count
-    hipError_t e = launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
-    if (e != hipSuccess) return e;
     if (n == 0) {
-        e = launch_fill_u32(num_pairs, 0u, 1, st);
-        return e;
+        hipError_t e = launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
+        if (e != hipSuccess) return e;
+        return launch_fill_u32(num_pairs, 0u, 1, st);
     }
-    // 1. depth order of the visible set
-    hipLaunchKernelGGL(k_depth_keys, dim3(div_up(n, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, vis_idx, vis_count,
-                       proj.depth, at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]), hist,
-                       div_up(n, GS_TILE_ITEMS));
-    e = radix_sort<kDepthBits>(at<uint32_t>(ws, L.dk[0]), at<uint32_t>(ws, L.dv[0]), at<uint32_t>(ws, L.dk[1]),
-                   at<uint32_t>(ws, L.dv[1]), at<uint32_t>(ws, L.dv[0]), at<uint32_t>(ws, L.dk[2]),
-                   at<uint32_t>(ws, L.dv[2]), vis_count,
-                   (uint32_t)n, 31, hist, totals, st);
-    if (e != hipSuccess) return e;
-    const uint32_t* order = at<uint32_t>(ws, L.dv[2]);
-    // 2. offsets in depth order + emission
+    // 1. emission offsets in visible-set order
+    const uint32_t* order = vis_idx;
     const uint32_t nb = div_up(n, GS_TILE_ITEMS);
     hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles, bsum);
-    e = launch_scan_blocks(bsum, nb, ctr + 0, nullptr, st);
+    hipError_t e = launch_scan_blocks(bsum, nb, ctr + 0, nullptr, st);
     if (e != hipSuccess) return e;
     uint32_t* offs_r = at<uint32_t>(ws, L.offs);
     hipLaunchKernelGGL(k_offsets, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles, bsum, ctr + 0,
@@ -467,22 +529,21 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     int tbits = 1;
     while (tbits < 32 && (1u << tbits) < T) ++tbits;
     const uint32_t mask0 = (1u << (tbits < kTileBits ? tbits : kTileBits)) - 1u;
-    if (capacity > 0)
-        hipLaunchKernelGGL(k_emit_pairs, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, order,
-                           vis_count, offs_r, reinterpret_cast<const ushort4*>(proj.rect), ctr + 1, TX,
-                           at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), mask0, hist,
-                           div_up(capacity, GS_TILE_ITEMS));
-    // 3. stable sort of the pairs by tile id
-    //    carrying every pair's emission position as its value
+    if (capacity == 0 || T == 0) return launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
+    // 2. emission: one (tile, primitive) pair per touched tile
+    hipLaunchKernelGGL(k_emit_pairs, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, order,
+                       vis_count, offs_r, reinterpret_cast<const ushort4*>(proj.rect), ctr + 1, TX,
+                       at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), mask0, hist,
+                       div_up(capacity, GS_TILE_ITEMS));
+    // 3. sort of the pairs by tile id, carrying every pair's emission position
     e = radix_sort<kTileBits>(at<uint32_t>(ws, L.pk[0]), nullptr, at<uint32_t>(ws, L.pk[1]), at<uint32_t>(ws, L.pv[1]),
                               at<uint32_t>(ws, L.pv[2]), at<uint32_t>(ws, L.pk[2]), pair_emit, ctr + 1, capacity,
                               tbits, hist, totals, st);
     if (e != hipSuccess) return e;
-    // 4. tile ranges, primitive ids (+ optional 64-bit keys)
-    if (capacity > 0)
-        hipLaunchKernelGGL(k_finalize, dim3(div_up(capacity, GS_BLOCK)), dim3(GS_BLOCK), 0, st,
-                           at<uint32_t>(ws, L.pk[2]), pair_emit, at<uint32_t>(ws, L.pv[0]), ctr + 1, proj.depth,
-                           ranges, keys, vals);
+    // 4. per tile: depth order, ranges, primitive ids (+ optional 64-bit keys)
+    hipLaunchKernelGGL(k_tile_depth_sort, dim3(T), dim3(GS_BLOCK), 0, st, at<uint32_t>(ws, L.pk[2]), ctr + 1,
+                       at<uint32_t>(ws, L.pv[0]), proj.depth, pair_emit, vals, ranges, keys,
+                       at<unsigned long long>(ws, L.scratch));
     return hipGetLastError();
 }
 

@@ -107,8 +107,8 @@ def test_project_visible_sort(case, torch_gpu, orc):
         np.testing.assert_array_equal(tr.keys.cpu().numpy()[:M].view(np.uint64), keys_ref)
         T = cam.num_tiles
         np.testing.assert_array_equal(u32(tr.ranges)[:2 * T].reshape(T, 2), ranges_ref)
-        # emission offsets: exclusive sums of tiles in (depth bits, id) order
-        order = vis_ref[np.lexsort((vis_ref, ref.depth[vis_ref].view(np.uint32)))]
+        # emission offsets: exclusive sums of tiles in visible-set (ascending id) order
+        order = vis_ref
         offs = np.concatenate([[0], np.cumsum(ref.tiles[order].astype(np.int64))[:-1]])
         np.testing.assert_array_equal(u32(tr.pair_offset)[order], offs)
         # pair_emit: sorted position -> emission position, a permutation under which
@@ -442,6 +442,37 @@ def test_delta_pack_apply(torch_gpu, orc):
     torch.cuda.synchronize()
     assert st.cpu().numpy()[0] & gsmi.GS_DEV_MSG_MISMATCH
     assert all(float(t.abs().sum()) == 0.0 for t in wrong)
+
+
+def test_long_tile_lists(torch_gpu, orc):
+    """Tiles whose pair lists exceed the per-tile LDS sort (thousands of wide
+    primitives over the image centre) take the global-memory path; the order
+    is still exactly (tile, depth bits, id), including equal depths."""
+    from paper_2607_19893_amd import scenes
+    rng = np.random.default_rng(21)
+    w = scenes.tiny(n=9000)
+    sc = w.scene
+    sc.mean[:] = (rng.standard_normal((sc.n, 3)) * [0.05, 0.05, 0.3]).astype(np.float32)
+    sc.mean[:3000, 2] = 0.5                      # equal depths: ties broken by id
+    sc.log_scale[:] = np.float32(-2.5)
+    tr = trainer_for(w, torch_gpu)
+    cam = w.cameras[0]
+    tr.status.zero_()
+    tr.project(cam); tr.visible(); tr.bin_sort()
+    torch_gpu.cuda.synchronize()
+    assert u32(tr.status)[0] == 0
+    ref = orc.project(sc, cam, 0)
+    vis_ref = orc.visible(ref.tiles)
+    keys_ref, vals_ref, ranges_ref = orc.sorted_pairs(vis_ref, ref, cam)
+    lengths = ranges_ref[:, 1].astype(np.int64) - ranges_ref[:, 0]
+    _say("longest tile list", int(lengths.max()), "tiles above 2048:", int((lengths > 2048).sum()))
+    assert lengths.max() > 2048
+    M = int(u32(tr.counts[1:2])[0])
+    assert M == keys_ref.size
+    np.testing.assert_array_equal(u32(tr.vals)[:M], vals_ref)
+    np.testing.assert_array_equal(tr.keys.cpu().numpy()[:M].view(np.uint64), keys_ref)
+    T = cam.num_tiles
+    np.testing.assert_array_equal(u32(tr.ranges)[:2 * T].reshape(T, 2), ranges_ref)
 
 
 def test_pair_overflow_flag(torch_gpu, orc):
