@@ -522,6 +522,29 @@ def test_backward_halves_match_combined(torch_gpu, orc):
         assert torch_gpu.equal(a, b)
 
 
+def test_step_matches_phase_calls(torch_gpu, orc):
+    """The training step's prepared-argument launches give the phase-by-phase
+    calls' results bit for bit (parameters, moments, replica, versions, image,
+    gradients), over two views of two cameras."""
+    w = get_case("room-60k-392x216")
+    runs = []
+    for fast in (True, False):
+        tr = trainer_for(w, torch_gpu)
+        for s, cam in enumerate(w.cameras[:2], start=1):
+            tgt = torch_gpu.from_numpy(w.target(s - 1).reshape(-1)).cuda()
+            if fast:
+                tr.step(cam, step=s, version=s, target=tgt)
+            else:
+                tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd_l1(tgt); tr.raster_bwd_pixels()
+                tr.raster_bwd_project(); tr.adam_publish(s, s, tr.msgs[s & 1]); tr.commit(s)
+        torch_gpu.cuda.synchronize()
+        assert int(u32(tr.status)[0]) == 0
+        runs.append([t.clone() for t in tr.params] + [tr.m.clone(), tr.v.clone()] +
+                    [t.clone() for t in tr.replica] + [tr.version.clone(), tr.img.clone(), tr.grad_rows.clone()])
+    for a, b in zip(*runs):
+        assert torch_gpu.equal(a, b)
+
+
 def test_overlapped_publication_matches_sequential(torch_gpu, orc):
     """Applies on the second stream (deferred into the next view) leave parameters, moments,
     replica and publication versions bit-identical to the one-stream schedule, over several views."""
