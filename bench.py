@@ -43,17 +43,17 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 
 # HBM traffic of the dominant kernel (k_raster_bwd) on this workload, from two
 # rocprofv3 --pmc passes (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch, mean
-# of the 10 dispatches of an 8-step run), each scaled by what the same counter
-# reads for a plain device copy of known size (a 1 GiB read registers as 0.5
-# GiB of FETCH_SIZE, a 1 GiB write as 1 GiB of WRITE_SIZE).  Valid only for the
-# kernel code it was measured on (comments aside): reported as null once the
-# code of raster.hip changes.
+# of the first 10 dispatches of an 8-step run: 2 warm-up and 8 timed views),
+# each scaled by what the same counter reads for a plain device copy of known
+# size (a 1 GiB read registers as 0.5 GiB of FETCH_SIZE, a 1 GiB write as
+# 1 GiB of WRITE_SIZE).  Valid only for the kernel code it was measured on
+# (comments aside): reported as null once the code of raster.hip changes.
 TRAFFIC = {
     "kernel": "k_raster_bwd",
     "source": "paper_2607_19893_amd/csrc/raster.hip",
-    "code_sha256": "2e7f01d6b63d559b7e5794e07e78f398810e906e7a3e24270b6f3daac8b3ab1d",
-    "fetch_kib": 206249.82, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 98549.66, "write_scale": 1048576.0 / 1048576.0,
+    "code_sha256": "9ba419c340b5a24ce2c37fe03c9c59bfac1f6b13d0ecfbdfa7d323e7b10afea1",
+    "fetch_kib": 205965.09, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 98510.76, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
@@ -100,6 +100,9 @@ def main():
                          "(default: the pipeline's choice)")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the separate timings of the scope hazards / admission gate and of two-view task units")
+    ap.add_argument("--dense-params", action="store_true",
+                    help="hold the parameter groups as five dense tensors instead of dense means and SH beside one "
+                         "[n, 8] head table of quat, log_scale and opacity (same arithmetic, different addresses)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy (read + write of this many MiB, 4 times) and exit; "
                          "its HBM counters calibrate the traffic counters of the path's kernels")
@@ -126,7 +129,8 @@ def main():
     if args.apply_after is not None:
         ViewTrainer.APPLY_AFTER = args.apply_after
     tr = ViewTrainer(w.scene, capacity=1, max_width=max(c.width for c in cams),
-                     max_height=max(c.height for c in cams), lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps)
+                     max_height=max(c.height for c in cams), lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps,
+                     packed=not args.dense_params)
     need = tr.ensure_capacity(cams)
     log("pair capacity %d (max pairs over the views %d)" % (tr.capacity, need))
     t0 = time.time()
@@ -282,7 +286,8 @@ def main():
                    "width": cams[0].width, "height": cams[0].height, "views": nviews,
                    "mean_visible": round(V_mean), "mean_pairs": round(M_mean),
                    "step": "project+visible+bin_sort+fwd_l1+bwd+sparse_adam_publish+commit",
-                   "apply_overlapped": not args.no_overlap},
+                   "apply_overlapped": not args.no_overlap,
+                   "param_layout": "dense" if args.dense_params else "head8"},
         "roofline": roofline,
         "phases_ms": {k: v["ms"] for k, v in per_phase.items()},
         "phases_frac": {k: v["frac"] for k, v in per_phase.items()},

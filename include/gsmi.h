@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define GSMI_ABI_VERSION 2
+#define GSMI_ABI_VERSION 3
 #define GS_TILE 16            /* pixels per tile side */
 #define GS_MAX_SH_DEGREE 3
 #define GS_MAX_GROUPS 8
@@ -78,7 +78,13 @@ typedef struct {
  *   opacity   [n]   opacity logit
  *   sh        [n,(sh_degree+1)^2,3] colour coefficients, coefficient
  *             k = l*l + l + m (m = -l..l), channel fastest
- * quat and sh must be 16-byte aligned.
+ * Row i of a group starts ld_<group> floats after row i-1 (0 = the group's
+ * width, a dense tensor), so groups may be column ranges of one table: with
+ * quat, log_scale and opacity as floats 0..3, 4..6 and 7 of a [n, 8] table
+ * (ld 8 for all three) a primitive's geometry and opacity are one 32-byte
+ * record, read and updated as one memory segment.  quat and sh
+ * must be 16-byte aligned; ld_quat a multiple of 4, ld_sh the dense width
+ * 3(sh_degree+1)^2 or a multiple of 4 above it.
  */
 typedef struct {
     int32_t n;
@@ -88,6 +94,7 @@ typedef struct {
     float* quat;
     float* opacity;
     float* sh;
+    int32_t ld_mean, ld_log_scale, ld_quat, ld_opacity, ld_sh;
 } gs_scene;
 
 /*
@@ -346,9 +353,10 @@ gs_status gs_raster_bwd_project_accum(const gs_scene* scene, const gs_camera* ca
  * below row_len; GS_ERR_UNSUPPORTED for row_len > 64.
  */
 typedef struct {
-    float* p;                 /* [n, cols] */
+    float* p;                 /* [n, cols] with leading dimension ld */
     int32_t cols;
     float lr;
+    int32_t ld;               /* floats between rows (0 = cols) */
 } gs_adam_group;
 
 gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
@@ -390,8 +398,9 @@ gs_status gs_sparse_adam_publish(const gs_adam_group* groups, int32_t n_groups, 
  *   gs_delta_msg_bytes(K, row_len, n_groups) gives the size.
  */
 typedef struct {
-    float* ptr;               /* [rows, cols] */
+    float* ptr;               /* [rows, cols] with leading dimension ld */
     int32_t cols;
+    int32_t ld;               /* floats between rows (0 = cols) */
 } gs_group;
 
 #define GS_MSG_MAGIC 0x47534D31u

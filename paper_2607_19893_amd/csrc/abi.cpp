@@ -70,6 +70,14 @@ gs_status check_scene(const gs_scene* s, const char* what) {
         GS_REQUIRE(s->mean && s->log_scale && s->quat && s->opacity && s->sh, "%s: null parameter pointer", what);
         GS_REQUIRE(aligned(s->quat, 16) && aligned(s->sh, 16), "%s: quat and sh must be 16-byte aligned", what);
     }
+    const int32_t K3 = 3 * (s->sh_degree + 1) * (s->sh_degree + 1);
+    GS_REQUIRE(s->ld_mean == 0 || s->ld_mean >= 3, "%s: ld_mean %d below 3", what, s->ld_mean);
+    GS_REQUIRE(s->ld_log_scale == 0 || s->ld_log_scale >= 3, "%s: ld_log_scale %d below 3", what, s->ld_log_scale);
+    GS_REQUIRE(s->ld_opacity >= 0, "%s: ld_opacity < 0", what);
+    GS_REQUIRE(s->ld_quat == 0 || (s->ld_quat >= 4 && s->ld_quat % 4 == 0),
+               "%s: ld_quat %d must be a multiple of 4 and >= 4", what, s->ld_quat);
+    GS_REQUIRE(s->ld_sh == 0 || s->ld_sh == K3 || (s->ld_sh > K3 && s->ld_sh % 4 == 0),
+               "%s: ld_sh %d must be %d or a multiple of 4 above it", what, s->ld_sh, K3);
     return GS_OK;
 }
 
@@ -330,6 +338,8 @@ static gs_status check_adam(const gs_adam_group* groups, int32_t n_groups, const
     for (int i = 0; i < n_groups; ++i) {
         GS_REQUIRE(groups[i].p, "%s: group %d null", what, i);
         GS_REQUIRE(groups[i].cols > 0, "%s: group %d cols <= 0", what, i);
+        GS_REQUIRE(groups[i].ld == 0 || groups[i].ld >= groups[i].cols, "%s: group %d ld %d below cols %d", what, i,
+                   groups[i].ld, groups[i].cols);
         row_len += groups[i].cols;
     }
     if (row_len > 64) return fail(GS_ERR_UNSUPPORTED, "%s: row length %d above 64", what, row_len);
@@ -376,6 +386,8 @@ static gs_status check_groups(const gs_group* g, int32_t n, const char* what) {
     int32_t rl = 0;
     for (int i = 0; i < n; ++i) {
         GS_REQUIRE(g[i].ptr && g[i].cols > 0, "%s: group %d invalid", what, i);
+        GS_REQUIRE(g[i].ld == 0 || g[i].ld >= g[i].cols, "%s: group %d ld %d below cols %d", what, i, g[i].ld,
+                   g[i].cols);
         rl += g[i].cols;
     }
     if (rl > 64) return fail(GS_ERR_UNSUPPORTED, "%s: row length %d above 64", what, rl);

@@ -21,6 +21,7 @@ constexpr int kUnroll = 4;
 struct AdamArgs {
     float* p[GS_MAX_GROUPS];
     int32_t cols[GS_MAX_GROUPS];
+    int32_t ld[GS_MAX_GROUPS];     // row stride of each parameter group
     float step[GS_MAX_GROUPS];     // lr / (1 - beta1^t)
     int32_t n_groups;
     int32_t row_len;
@@ -88,7 +89,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint
         ++grp;
     }
     float* __restrict__ P = a.p[grp];
-    const int cols = a.cols[grp];
+    const int pld = a.ld[grp];
     const float step = a.step[grp];
     const float* __restrict__ G = a.g;
     float* __restrict__ Mm = a.m;
@@ -111,7 +112,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint
                 gr[u] = G[(size_t)r * a.gld + col];
                 mo[u] = Mm[(size_t)id[u] * a.sld + col];
                 vo[u] = Vv[(size_t)id[u] * a.sld + col];
-                po[u] = P[(size_t)id[u] * cols + c];
+                po[u] = P[(size_t)id[u] * pld + c];
             }
         }
 #pragma unroll
@@ -127,7 +128,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint
                 // a plain rounded add of the published step (this file is built
                 // without contraction): a replica that adds the message's rows stays
                 // bit-identical to the parameters
-                P[(size_t)id[u] * cols + c] = po[u] + delta;
+                P[(size_t)id[u] * pld + c] = po[u] + delta;
                 if (drows) drows[(size_t)r * dld + col] = delta;
                 if (PUBLISH && col == 0) ids[r] = id[u];
             }
@@ -144,6 +145,7 @@ AdamArgs make_args(const gs_adam_group* groups, int32_t n_groups, const float* g
     for (int i = 0; i < n_groups; ++i) {
         a.p[i] = groups[i].p;
         a.cols[i] = groups[i].cols;
+        a.ld[i] = groups[i].ld ? groups[i].ld : groups[i].cols;
         a.step[i] = (float)((double)groups[i].lr / bc1);
         row_len += groups[i].cols;
     }

@@ -17,6 +17,7 @@ namespace {
 struct GroupArgs {
     float* ptr[GS_MAX_GROUPS];
     int32_t cols[GS_MAX_GROUPS];
+    int32_t ld[GS_MAX_GROUPS];     // row stride of each group
     int32_t n_groups;
     int32_t row_len;
     int32_t rows_per_wave;
@@ -70,13 +71,13 @@ __global__ void __launch_bounds__(GS_BLOCK) k_pack(GroupArgs a, const uint32_t* 
     lane_group(a, lane, sub, grp, c);
     if (sub >= a.rows_per_wave) return;
     const float* __restrict__ src = a.ptr[grp];
-    const int cols = a.cols[grp];
+    const int gld = a.ld[grp];
     const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
     const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
     for (uint32_t r = wave * a.rows_per_wave + sub; r < K; r += waves * a.rows_per_wave) {
         const uint32_t id = idx[r];
         if (lane - sub * a.row_len == 0) ids[r] = id;
-        rows[(size_t)r * a.row_len + (lane - sub * a.row_len)] = src[(size_t)id * cols + c];
+        rows[(size_t)r * a.row_len + (lane - sub * a.row_len)] = src[(size_t)id * gld + c];
     }
 }
 
@@ -114,14 +115,14 @@ __global__ void __launch_bounds__(GS_BLOCK) k_apply(GroupArgs a, const uint32_t*
     lane_group(a, lane, sub, grp, c);
     if (sub >= a.rows_per_wave) return;
     float* __restrict__ dst = a.ptr[grp];
-    const int cols = a.cols[grp];
+    const int gld = a.ld[grp];
     const int col = lane - sub * a.row_len;
     const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
     const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
     for (uint32_t r = wave * a.rows_per_wave + sub; r < K; r += waves * a.rows_per_wave) {
         const uint32_t id = ids[r];
         const float val = rows[(size_t)r * a.row_len + col];
-        float* q = dst + (size_t)id * cols + c;
+        float* q = dst + (size_t)id * gld + c;
         *q = (mode == GS_APPLY_ADD) ? (*q + val) : val;
         if (col == 0 && prim_version) prim_version[id] = version;
     }
@@ -159,7 +160,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_commit(GroupArgs a, const uint32_t
     const bool in_row = sub < a.rows_per_wave;
     if (!in_row) grp = c = 0;                  // spare lanes read row 0's first column and store nothing
     float* __restrict__ dst = a.ptr[grp];
-    const int cols = a.cols[grp];
+    const int gld = a.ld[grp];
     const int col = in_row ? lane - sub * a.row_len : 0;
     const uint32_t rpw = (uint32_t)a.rows_per_wave;
     const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
@@ -186,13 +187,13 @@ __global__ void __launch_bounds__(GS_BLOCK) k_commit(GroupArgs a, const uint32_t
             // every lane of the row reads the version before lane 0 stamps it
             pv[u] = prim_version[id[u]];
             val[u] = rows[(size_t)rr[u] * a.row_len + col];
-            old[u] = dst[(size_t)id[u] * cols + c];
+            old[u] = dst[(size_t)id[u] * gld + c];
         }
 #pragma unroll
         for (int u = 0; u < kCommitRows; ++u) {
             if (!ok[u]) continue;
             const bool newer = pv[u] < version;
-            if (newer) dst[(size_t)id[u] * cols + c] = (mode == GS_APPLY_ADD) ? (old[u] + val[u]) : val[u];
+            if (newer) dst[(size_t)id[u] * gld + c] = (mode == GS_APPLY_ADD) ? (old[u] + val[u]) : val[u];
             if (col == 0) {
                 if (newer)
                     prim_version[id[u]] = version;
@@ -224,6 +225,7 @@ GroupArgs make_group_args(const gs_group* g, int32_t n) {
     for (int i = 0; i < n; ++i) {
         a.ptr[i] = g[i].ptr;
         a.cols[i] = g[i].cols;
+        a.ld[i] = g[i].ld ? g[i].ld : g[i].cols;
         rl += g[i].cols;
     }
     a.n_groups = n;

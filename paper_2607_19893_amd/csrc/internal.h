@@ -19,6 +19,25 @@ struct CamArgs {
 
 CamArgs make_cam_args(const gs_camera* c);
 
+// Row strides (floats) of the pool's groups, the dense widths filled in for 0.
+struct SceneLd {
+    int32_t mean, log_scale, quat, opacity, sh;
+    int32_t head;   // 1: log_scale and opacity are floats 4..7 of quat's 16-byte-aligned row
+};
+
+inline SceneLd scene_ld(const gs_scene& s) {
+    const int32_t K3 = 3 * (s.sh_degree + 1) * (s.sh_degree + 1);
+    SceneLd l;
+    l.mean = s.ld_mean ? s.ld_mean : 3;
+    l.log_scale = s.ld_log_scale ? s.ld_log_scale : 3;
+    l.quat = s.ld_quat ? s.ld_quat : 4;
+    l.opacity = s.ld_opacity ? s.ld_opacity : 1;
+    l.sh = s.ld_sh ? s.ld_sh : K3;
+    l.head = s.log_scale == s.quat + 4 && s.opacity == s.quat + 7 && l.log_scale == l.quat &&
+             l.opacity == l.quat && l.quat % 4 == 0;
+    return l;
+}
+
 // Compute units of the current device (cached per device; 0 if the query fails).
 uint32_t compute_units();
 

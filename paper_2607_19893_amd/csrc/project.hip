@@ -54,13 +54,14 @@ __device__ __forceinline__ void sh_basis(int deg, float x, float y, float z, flo
 template <int DEG>
 __global__ void __launch_bounds__(GS_BLOCK) k_project(
     int32_t n, const float* __restrict__ mean, const float* __restrict__ log_scale,
-    const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c,
+    const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, SceneLd ld, CamArgs c,
     int32_t* __restrict__ radius, uint32_t* __restrict__ tiles, ushort4* __restrict__ rect,
     float* __restrict__ depth, float2* __restrict__ mean2d, float4* __restrict__ conic_opacity,
     float* __restrict__ rgb, uint8_t* __restrict__ clampm) {
     const int32_t i = blockIdx.x * GS_BLOCK + threadIdx.x;
     if (i >= n) return;
-    const float mx = mean[3 * i + 0], my = mean[3 * i + 1], mz = mean[3 * i + 2];
+    const float* mrow = mean + (size_t)i * ld.mean;
+    const float mx = mrow[0], my = mrow[1], mz = mrow[2];
 
     // camera space
     const float p0 = ((c.R[0] * mx + c.R[1] * my) + c.R[2] * mz) + c.t[0];
@@ -73,10 +74,20 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
     }
 
     // 3D covariance  Sigma = (Rq S)(Rq S)^T
-    const float s0 = (float)exp((double)log_scale[3 * i + 0]);
-    const float s1 = (float)exp((double)log_scale[3 * i + 1]);
-    const float s2 = (float)exp((double)log_scale[3 * i + 2]);
-    const float4 q = reinterpret_cast<const float4*>(quat)[i];
+    const float4 q = *reinterpret_cast<const float4*>(quat + (size_t)i * ld.quat);
+    float l0, l1, l2, logit;
+    if (ld.head) {
+        // the record's head: one 16-byte load for log_scale and the opacity logit
+        const float4 h = *reinterpret_cast<const float4*>(quat + (size_t)i * ld.quat + 4);
+        l0 = h.x; l1 = h.y; l2 = h.z; logit = h.w;
+    } else {
+        const float* lrow = log_scale + (size_t)i * ld.log_scale;
+        l0 = lrow[0]; l1 = lrow[1]; l2 = lrow[2];
+        logit = 0.0f;
+    }
+    const float s0 = (float)exp((double)l0);
+    const float s1 = (float)exp((double)l1);
+    const float s2 = (float)exp((double)l2);
     const float qn = sqrtf(((q.x * q.x + q.y * q.y) + q.z * q.z) + q.w * q.w);
     const float w = q.x / qn, x = q.y / qn, y = q.z / qn, z = q.w / qn;
     float Rq[3][3];
@@ -158,7 +169,8 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
     mean2d[i] = make_float2(u, v);
 
     // appearance (fp32, not part of any integer decision)
-    const float o = 1.0f / (1.0f + expf(-opacity[i]));
+    if (!ld.head) logit = opacity[(size_t)i * ld.opacity];
+    const float o = 1.0f / (1.0f + expf(-logit));
     conic_opacity[i] = make_float4(cA, cB, cC, o);
     float dx = mx - c.campos[0], dy = my - c.campos[1], dz = mz - c.campos[2];
     const float inv = 1.0f / sqrtf(dx * dx + dy * dy + dz * dz);
@@ -169,7 +181,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
     // the row's coefficients, as float4 loads when a row is a whole number of them
     float co[3 * K];
     if constexpr ((3 * K) % 4 == 0) {
-        const float4* s4 = reinterpret_cast<const float4*>(sh + (size_t)i * K * 3);
+        const float4* s4 = reinterpret_cast<const float4*>(sh + (size_t)i * ld.sh);
 #pragma unroll
         for (int k = 0; k < 3 * K / 4; ++k) {
             const float4 v4 = s4[k];
@@ -177,7 +189,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
         }
     } else {
 #pragma unroll
-        for (int k = 0; k < 3 * K; ++k) co[k] = sh[(size_t)i * K * 3 + k];
+        for (int k = 0; k < 3 * K; ++k) co[k] = sh[(size_t)i * ld.sh + k];
     }
     float acc0 = 0.5f, acc1 = 0.5f, acc2 = 0.5f;
 #pragma unroll
@@ -213,7 +225,7 @@ hipError_t launch_project(const gs_scene& s, const CamArgs& cam, const gs_proj& 
     const dim3 grid(div_up(s.n, GS_BLOCK));
 #define GS_LAUNCH_PROJECT(D)                                                                                   \
     hipLaunchKernelGGL(k_project<D>, grid, dim3(GS_BLOCK), 0, st, s.n, s.mean, s.log_scale, s.quat, s.opacity,   \
-                       s.sh, cam, o.radius, o.tiles, reinterpret_cast<ushort4*>(o.rect), o.depth,                \
+                       s.sh, scene_ld(s), cam, o.radius, o.tiles, reinterpret_cast<ushort4*>(o.rect), o.depth,   \
                        reinterpret_cast<float2*>(o.mean2d), reinterpret_cast<float4*>(o.conic_opacity), o.rgb,  \
                        o.clamp)
     switch (s.sh_degree) {

@@ -838,8 +838,8 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
     const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
     const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, uint32_t capacity,
     const float4* __restrict__ conic_op, const uint8_t* __restrict__ clampm, const float* __restrict__ mean, const float* __restrict__ log_scale,
-    const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, CamArgs c,
-    float* __restrict__ grad_rows, int32_t ld, float* __restrict__ grad2d, float* __restrict__ grad_norm,
+    const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, SceneLd pld,
+    CamArgs c, float* __restrict__ grad_rows, int32_t ld, float* __restrict__ grad2d, float* __restrict__ grad_norm,
     const uint32_t* __restrict__ union_idx, const uint32_t* __restrict__ union_count) {
     using L = RowLayout<DEG>;
     constexpr int K = L::K;
@@ -907,10 +907,17 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
         grad_norm[id] = ACCUM ? grad_norm[id] + gn : gn;
     }
     float mu[3], ls[3], qr[4];
-    load_row<3>(mean + (size_t)id * 3, mu);
-    load_row<3>(log_scale + (size_t)id * 3, ls);
-    load_row<4>(quat + (size_t)id * 4, qr);
-    const float logit = opacity[id];
+    load_row<3>(mean + (size_t)id * pld.mean, mu);
+    load_row<4>(quat + (size_t)id * pld.quat, qr);
+    float logit;
+    if (pld.head) {
+        float h[4];
+        load_row<4>(quat + (size_t)id * pld.quat + 4, h);
+        ls[0] = h[0]; ls[1] = h[1]; ls[2] = h[2]; logit = h[3];
+    } else {
+        load_row<3>(log_scale + (size_t)id * pld.log_scale, ls);
+        logit = opacity[(size_t)id * pld.opacity];
+    }
     const uint8_t cm = clampm[id];
     float out[L::ROW4];
 
@@ -935,7 +942,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
         sh_basis_grad<DEG>(d[0], d[1], d[2], Y, G);
         const float gc[3] = {(cm & 1) ? 0.0f : g2[6], (cm & 2) ? 0.0f : g2[7], (cm & 4) ? 0.0f : g2[8]};
         float co[3 * K];
-        load_row<3 * K>(sh + (size_t)id * 3 * K, co);
+        load_row<3 * K>(sh + (size_t)id * pld.sh, co);
         float gd[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int k = 0; k < K; ++k) {
@@ -1092,7 +1099,8 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
 #define GS_LAUNCH_PBWD(D, A)                                                                                     \
     hipLaunchKernelGGL((k_project_bwd<D, A>), grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles,        \
                        pair_offset, slots, capacity, reinterpret_cast<const float4*>(proj.conic_opacity),         \
-                       proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh, cam,         \
+                       proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh,              \
+                       scene_ld(scene), cam,                                                                      \
                        grad_rows, grad_ld, grad2d, grad_norm, union_idx, union_count)
     if (union_idx) {
         switch (scene.sh_degree) {

@@ -35,7 +35,8 @@ GS_MAX_GROUPS = 8
 
 class gs_scene(ctypes.Structure):
     _fields_ = [("n", i32), ("sh_degree", i32), ("mean", P), ("log_scale", P), ("quat", P), ("opacity", P),
-                ("sh", P)]
+                ("sh", P), ("ld_mean", i32), ("ld_log_scale", i32), ("ld_quat", i32), ("ld_opacity", i32),
+                ("ld_sh", i32)]
 
 
 class gs_camera(ctypes.Structure):
@@ -50,11 +51,11 @@ class gs_proj(ctypes.Structure):
 
 
 class gs_adam_group(ctypes.Structure):
-    _fields_ = [("p", P), ("cols", i32), ("lr", f32)]
+    _fields_ = [("p", P), ("cols", i32), ("lr", f32), ("ld", i32)]
 
 
 class gs_group(ctypes.Structure):
-    _fields_ = [("ptr", P), ("cols", i32)]
+    _fields_ = [("ptr", P), ("cols", i32), ("ld", i32)]
 
 
 class gs_ring(ctypes.Structure):
@@ -78,6 +79,12 @@ def scope_words(n) -> int:
 
 
 _lib.gs_abi_version.restype = i32
+# the structs above mirror this version of the header; a library built from
+# another one would read them with a different layout
+ABI_VERSION = 3
+if _lib.gs_abi_version() != ABI_VERSION:
+    raise ImportError("libgsmi ABI version %d, binding expects %d: rebuild the library"
+                      % (_lib.gs_abi_version(), ABI_VERSION))
 _lib.gs_status_string.restype = ctypes.c_char_p
 _lib.gs_status_string.argtypes = [i32]
 _lib.gs_last_error.restype = ctypes.c_char_p
@@ -163,8 +170,21 @@ def make_camera(cam) -> gs_camera:
     return c
 
 
+def row_stride(t) -> int:
+    """Floats between consecutive rows of a parameter group: the first-dim
+    stride of a tensor whose rows are contiguous (a dense tensor or a column
+    range of a wider table)."""
+    if t is None or t.numel() == 0:
+        return 0
+    per_row = t[0].numel() if t.dim() > 1 else 1
+    if t.dim() > 1 and not t[0].is_contiguous():
+        raise ValueError("rows of a parameter group must be contiguous")
+    return int(t.stride(0)) if t.shape[0] > 1 else per_row
+
+
 def make_scene(n, sh_degree, mean, log_scale, quat, opacity, sh) -> gs_scene:
-    return gs_scene(int(n), int(sh_degree), ptr(mean), ptr(log_scale), ptr(quat), ptr(opacity), ptr(sh))
+    return gs_scene(int(n), int(sh_degree), ptr(mean), ptr(log_scale), ptr(quat), ptr(opacity), ptr(sh),
+                    row_stride(mean), row_stride(log_scale), row_stride(quat), row_stride(opacity), row_stride(sh))
 
 
 def make_proj(radius, tiles, rect, depth, mean2d, conic_opacity, rgb, clamp) -> gs_proj:
@@ -287,7 +307,7 @@ def make_adam_groups(groups):
     """groups: list of (p [n, cols] tensor, lr)."""
     arr = (gs_adam_group * len(groups))()
     for i, (p, lr) in enumerate(groups):
-        arr[i] = gs_adam_group(ptr(p), int(p.shape[1]), float(lr))
+        arr[i] = gs_adam_group(ptr(p), int(p.shape[1]), float(lr), row_stride(p))
     return arr
 
 
@@ -310,7 +330,7 @@ def gs_sparse_adam_publish(groups_arr, n_groups, idx, count, max_rows, grad_rows
 def make_groups(tensors):
     arr = (gs_group * len(tensors))()
     for i, t in enumerate(tensors):
-        arr[i] = gs_group(ptr(t), int(t.shape[1]))
+        arr[i] = gs_group(ptr(t), int(t.shape[1]), row_stride(t))
     return arr
 
 

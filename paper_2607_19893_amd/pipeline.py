@@ -24,9 +24,38 @@ def to_u32(t) -> np.ndarray:
     return t.detach().cpu().numpy().view(np.uint32)
 
 
+HEAD_OFF = {"quat": 0, "log_scale": 4, "opacity": 7}   # columns of the 32-byte head record
+HEAD_LD = 8
+
+
+def alloc_groups(host, deg, n, device, packed=True):
+    """Device parameter groups in GROUPS order from host arrays.
+
+    dense: five tensors.  packed: quat, log_scale and opacity as column views
+    of one [n, 8] head table (32 bytes a primitive: the projection reads quat
+    and log_scale for every primitive in front of the camera, and the
+    optimizer and the commit update the three together, so one segment
+    serves them instead of three partial ones), the means and the SH
+    coefficients dense ([n, 3]: read for every primitive; [n, 3K]: 192-byte
+    rows at SH degree 3, whole 64-byte segments)."""
+    k3 = 3 * (deg + 1) ** 2
+    cols = [3, 3, 4, 1, k3]
+    arrs = [torch.from_numpy(np.ascontiguousarray(a, np.float32).reshape(n, c)) for a, c in zip(host, cols)]
+    if not packed:
+        return [a.to(device) for a in arrs], None
+    head = torch.zeros(max(1, n), HEAD_LD, device=device)
+    views = [arrs[0].to(device)]
+    for name, a, c in zip(GROUPS[1:4], arrs[1:4], cols[1:4]):
+        v = head[:n, HEAD_OFF[name]:HEAD_OFF[name] + c]
+        v.copy_(a.to(device))
+        views.append(v)
+    views.append(arrs[4].to(device))
+    return views, head
+
+
 class ViewTrainer:
     def __init__(self, scene, capacity: int = 0, max_width: int = 0, max_height: int = 0, device="cuda",
-                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-15, with_replica=True, with_keys=False):
+                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-15, with_replica=True, with_keys=False, packed=True):
         self.dev = torch.device(device)
         self.n = int(scene.n)
         self.deg = int(scene.sh_degree)
@@ -40,13 +69,16 @@ class ViewTrainer:
         self.lr, self.beta1, self.beta2, self.eps = lr, beta1, beta2, eps
         n = self.n
         host = [scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh]
-        self.params = [torch.from_numpy(np.ascontiguousarray(a, np.float32).reshape(n, c)).to(self.dev)
-                       for a, c in zip(host, self.cols)]
+        # parameters: quat / log_scale / opacity in one head table beside dense
+        # means and SH (packed), or five dense tensors; the replica has the same layout
+        self.packed = packed
+        self.params, self.head = alloc_groups(host, self.deg, n, self.dev, packed)
         self.grad_rows = torch.zeros(max(1, n), self.ld, device=self.dev)
         self.m = torch.zeros(max(1, n), self.ld, device=self.dev)
         self.v = torch.zeros(max(1, n), self.ld, device=self.dev)
         self.delta_rows = torch.zeros(max(1, n), self.ld, device=self.dev)
-        self.replica = [p.clone() for p in self.params] if with_replica else None
+        self.replica, self.replica_head = (alloc_groups(host, self.deg, n, self.dev, packed) if with_replica
+                                            else (None, None))
         self.version = _u32(n, self.dev)
         # projection
         self.radius = _u32(n, self.dev)

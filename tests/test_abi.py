@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol(gs):
     for nm in names:
         assert hasattr(gs.raw(), nm), nm
         assert nm in gs.EXPORTS, nm
-    assert gs.gs_abi_version() == 2
+    assert gs.gs_abi_version() == gs.ABI_VERSION == 3
 
 
 def test_status_strings(gs):
@@ -77,6 +77,22 @@ def test_null_and_range_arguments_rejected(gs):
     assert L.gs_delta_apply(16, 8, g, 1, 10, 10, 0, None, 16, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_delta_pack(16, 16, 10, g, 1, 1, 8, 1024, 16, None) == gs.GS_ERR_INVALID_ARG  # misaligned msg
     assert L.gs_loss_l1(None, None, 4, 4, None, None, None, 0, None) == gs.GS_ERR_INVALID_ARG
+    # row strides of the parameter groups: at least the group's width, quat and sh a multiple of 4
+    cam.width = 64
+    for field, bad, word in (("ld_mean", 2, "ld_mean"), ("ld_quat", 6, "ld_quat"), ("ld_sh", 44, "ld_sh"),
+                             ("ld_sh", 50, "ld_sh"), ("ld_sh", 3, "ld_sh"), ("ld_log_scale", 1, "ld_log_scale"),
+                             ("ld_opacity", -1, "ld_opacity")):
+        scl = gs.gs_scene(10, 3, 16, 16, 16, 16, 16)
+        setattr(scl, field, bad)
+        assert L.gs_project(ctypes.byref(scl), ctypes.byref(cam), ctypes.byref(pr), None) == gs.GS_ERR_INVALID_ARG
+        assert word in gs.gs_last_error()
+    grp[0].ld = 2
+    assert L.gs_sparse_adam(grp, 1, *A, 1, 0.9, 0.999, 1e-15, None, 0, None) == gs.GS_ERR_INVALID_ARG
+    assert "ld 2 below cols 3" in gs.gs_last_error()
+    g[0].ld = 1
+    assert L.gs_delta_apply(16, 4096, g, 1, 10, 10, 0, None, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert "ld 1 below cols 3" in gs.gs_last_error()
+    g[0].ld = 0
     # fused forward + loss: workspace sized per tile
     assert L.gs_raster_fwd_l1(ctypes.byref(pr), 10, 16, 16, 256, 256, 16, 16, 16, 16, 16, None, 16, 16, 16, 0,
                               None) == gs.GS_ERR_WORKSPACE
