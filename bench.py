@@ -1,21 +1,25 @@
 """Throughput of the one-GPU 3DGS training-view hot path.
 
 A step is one training view through every phase: projection, visible-set
-extraction, tile binning + sort, forward raster, L1 loss, backward, sparse
-Adam over the visible rows with its steps staged as a publication message,
-and the apply of that message to a replica (the pending-update publication).  The workload is the 1M-Gaussian
+extraction, tile binning + sort, forward raster fused with the L1 loss,
+backward, sparse Adam over the visible rows with its steps staged as a
+publication message, and the commit of that message to a replica (the
+pending-update publication).  The workload is the 1M-Gaussian
 SH-degree-3 room scene with 32 forward-facing 1920x1080 cameras; steps cycle
 through the cameras.  Inputs (scene, Adam state, all 32 targets) are resident
 in HBM before the timed region.
 
-Each view's apply to the replica runs on a second stream, started after the
-next view's loss so that it runs beside that view's backward raster (which
-reads projection outputs, not the replica); --no-overlap runs everything on
-one stream.  Every timed view's apply completes inside the timed region.
+Each view's commit to the replica runs on a second stream, started after the
+next view's forward + loss so that it runs beside that view's backward raster
+(which reads projection outputs, not the replica); --no-overlap runs
+everything on one stream.  Every timed view's apply completes inside the timed region.
 
 Prints one JSON line (the driver's contract) with a roofline entry for the
 dominant kernel (timed with HIP events on the stream it runs on) and the CPU
-oracle timed on a bounded sample of the same workload.
+oracle timed on a bounded sample of the same workload.  Extras beside it
+(--no-extras skips them): the scope hazards and admission gate between
+consecutive views, two-view task units, and the host planner (graph,
+partition, schedule) on synthetic captures of 1,000 to 50,000 images.
 """
 from __future__ import annotations
 
@@ -263,11 +267,14 @@ def main():
     if not args.no_extras:
         extras["scope_gate"] = bench_scope_gate(tr, cams, targets, args.steps)
         extras["unit2"] = bench_unit(tr, cams, targets, args.steps, step)
+        extras["planner"] = bench_planner()
         log("extras: " + json.dumps(extras))
 
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, args.cpu_views)
+        if "planner" in extras:
+            extras["planner"]["oracle"] = planner_oracle_time(PLAN_ORACLE_VIEWS)
 
     out = {
         "metric": "train views/sec (fwd+bwd+sparse Adam), 1M Gaussians 1080p",
@@ -384,6 +391,48 @@ def bench_unit(tr, cams, targets, steps, step0):
     assert to_u32(tr.status)[0] == 0, "device status flags set during the task units"
     return {"units": units, "views_per_unit": 2, "views_per_s": round(2 * units / dt, 2),
             "ms_per_unit": round(1e3 * dt / units, 4)}
+
+
+# the planner's settings: outlier cap, neighbours kept per view, logical
+# regions, task-unit size (K = 4 and two views per unit are the paper's
+# defaults; the cap and top-k are this build's choice)
+PLAN = {"track_cap": 64, "top_k": 16, "K": 4, "unit_size": 2, "max_iters": 20}
+PLAN_SIZES = (1000, 2000, 5000, 10000, 20000, 50000)   # image counts the paper times its planner at
+PLAN_ORACLE_VIEWS = 1000
+
+
+def bench_planner():
+    """Wall time of the native planner (graph, partition, schedule) on
+    synthetic aerial captures of each size, host arrays resident."""
+    from paper_2607_19893_amd import gsmi, scenes
+    out = {"settings": PLAN, "threads": os.cpu_count(), "sizes": {}}
+    for n in PLAN_SIZES:
+        c = scenes.capture_tracks(n, seed=5)
+        t0 = time.perf_counter()
+        G = gsmi.gs_rlg_build(c.item_ptr, c.item_tracks, c.n_tracks, PLAN["track_cap"], PLAN["top_k"])
+        t1 = time.perf_counter()
+        group, C, rounds = gsmi.gs_lp_partition(c.position, G, PLAN["K"], PLAN["max_iters"])
+        t2 = time.perf_counter()
+        cycle, order, ug, tr = gsmi.gs_sds_order(group, C, G, PLAN["unit_size"])
+        t3 = time.perf_counter()
+        out["sizes"][str(n)] = {"observations": int(c.item_ptr[-1]), "edges": int(G.edge_dst.size),
+                                "rounds": rounds, "s_graph": round(t1 - t0, 4), "s_partition": round(t2 - t1, 4),
+                                "s_schedule": round(t3 - t2, 4), "s_total": round(t3 - t0, 4),
+                                "zero_transitions": round(float(np.mean(tr[1:] == 0.0)), 4)}
+        log("planner %d views: %s" % (n, out["sizes"][str(n)]))
+    return out
+
+
+def planner_oracle_time(n):
+    """The oracle planner on the same kind of capture (one size), for comparison."""
+    import oracle
+    from paper_2607_19893_amd import scenes
+    c = scenes.capture_tracks(n, seed=5)
+    t0 = time.perf_counter()
+    R = oracle.rlg_build([c.tracks_of(i) for i in range(c.n)], c.n_tracks, PLAN["track_cap"], PLAN["top_k"])
+    P = oracle.lp_partition(c.position, R, PLAN["K"], PLAN["max_iters"])
+    oracle.sds_order(P.group, P.coupling, PLAN["K"], R, PLAN["unit_size"])
+    return {"views": n, "s_total": round(time.perf_counter() - t0, 3)}
 
 
 def in_front(mean, cam):

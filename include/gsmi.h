@@ -574,6 +574,89 @@ typedef struct {
 gs_status gs_admission_gate(const uint32_t* RB, const uint32_t* D, const gs_gate_args* args, int32_t n,
                             gs_gate_result* result, void* ws, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Ahead-of-time planner (host).  The three calls below run on the CPU over
+ * host memory, synchronously, before training; they take no stream and
+ * allocate host scratch internally.  Views are items 0..n-1.  Results are
+ * deterministic: they do not depend on the number of threads used.
+ * ------------------------------------------------------------------------ */
+
+/*
+ * Relative locality graph (Section 4.1.1, Eq. 1).  The weight of views i and
+ * j is the Jaccard similarity |P_i & P_j| / |P_i | P_j| of their track sets
+ * (0 for an empty union; a missing edge means weight 0, not independence).
+ * Shared-track counts are taken through the inverse track -> view mapping.
+ * Tracks seen by more than track_cap views are outliers and are left out
+ * of every view's set (track_cap <= 0: no cap).  Each view keeps its top_k
+ * strongest neighbours (weight descending, then view id ascending;
+ * top_k <= 0 keeps all) and an edge is retained when either end keeps it,
+ * so the graph is symmetric.
+ *
+ *   item_ptr [n_items+1]  CSR offsets into item_tracks, item_ptr[0] = 0
+ *   item_tracks           track ids of each view, strictly ascending,
+ *                         in [0, n_tracks)
+ *   edge_ptr [n_items+1]  out: CSR offsets of the retained graph
+ *   edge_dst, edge_w      out: neighbours (ascending) and weights in (0, 1],
+ *                         edge_capacity entries available
+ *   n_edges               out: entries the graph needs
+ * At most 2 * n_items * top_k entries when top_k > 0.  Errors:
+ * GS_ERR_INVALID_ARG for null pointers or a malformed track list;
+ * GS_ERR_WORKSPACE (with *n_edges set, outputs untouched) if edge_capacity is
+ * too small.
+ */
+gs_status gs_rlg_build(int32_t n_items, int32_t n_tracks, const int64_t* item_ptr, const int32_t* item_tracks,
+                       int32_t track_cap, int32_t top_k, int64_t* edge_ptr, int32_t* edge_dst, double* edge_w,
+                       int64_t edge_capacity, int64_t* n_edges);
+
+/*
+ * Logical partitioning (Section 4.2, LP): K balanced groups of views by
+ * k-means over the camera centres.  Seeds are view 0 and then, one at a
+ * time, the view farthest from every seed so far (squared distance, lowest
+ * id on ties).  Each round assigns (distance, view, group) triples in
+ * ascending order, each group taking at most ceil(n / K) views, and moves
+ * each centre to its members' mean (summed in ascending view order).  It
+ * stops when a round repeats the previous assignment or after max_iters
+ * rounds.  The region-level coupling summary coupling[a*K + b] is the sum
+ * of the retained edge weights between groups a and b (within group a for
+ * a = b), summed by ascending view, then neighbour.
+ *
+ *   position [n_items,3]  camera centres (finite)
+ *   edge_*                a graph from gs_rlg_build (or any symmetric one
+ *                         with ascending neighbours and weights in (0, 1])
+ *   group [n_items]       out: group of each view
+ *   coupling [K*K]        out
+ *   iters_run             out: assignment rounds run
+ * Errors: GS_ERR_INVALID_ARG for null pointers, K < 1, max_iters < 1, a
+ * non-finite centre or a malformed graph.
+ */
+gs_status gs_lp_partition(int32_t n_items, const double* position, const int64_t* edge_ptr,
+                          const int32_t* edge_dst, const double* edge_w, int32_t K, int32_t max_iters,
+                          int32_t* group, double* coupling, int32_t* iters_run);
+
+/*
+ * Static data scheduling (Section 4.2, SDS, Eq. 2).  The traversal starts
+ * at the lowest-numbered non-empty group and repeatedly moves to the
+ * unvisited non-empty group least coupled to the last one (lowest id on
+ * ties).  Task units of unit_size views take turns over that cycle.  Each
+ * unit is filled from its group with the views of lowest score
+ * s(v | U_prev) = sum of w_uv over the previous unit (view id breaks ties),
+ * and topped up from the next groups of the cycle when its group runs out,
+ * so every unit but the last has unit_size views.  transition[t] is the
+ * largest retained weight between units t-1 and t (0 for t = 0).
+ *
+ *   group [n_items]       from gs_lp_partition (values in [0, K))
+ *   coupling [K*K]        the region-level summary
+ *   cycle [K]             out: the traversal, -1 after its n_cycle entries
+ *   order [n_items]       out: the views, unit after unit
+ *   unit_group, transition  out: [ceil(n_items / unit_size)] each
+ * Errors: GS_ERR_INVALID_ARG for null pointers, K < 1, unit_size < 1, a
+ * group outside [0, K) or a malformed graph.
+ */
+gs_status gs_sds_order(int32_t n_items, const int32_t* group, int32_t K, const double* coupling,
+                       const int64_t* edge_ptr, const int32_t* edge_dst, const double* edge_w, int32_t unit_size,
+                       int32_t* cycle, int32_t* n_cycle, int32_t* order, int32_t* unit_group, double* transition,
+                       int32_t* n_units);
+
 #ifdef __cplusplus
 }
 #endif

@@ -784,3 +784,8 @@ def train_unit(scene, cams, targets, m_groups, v_groups, step, lr=1e-3, beta1=0.
         newp.append(pn); newm.append(mn); newv.append(vn); deltas.append(d)
     msg = delta_message(union, [d.astype(np.float32) for d in deltas], version) if with_msg else None
     return UnitResult(union, grads, gnorm, [v[:6] for v in views], newp, newm, newv, deltas, msg)
+
+
+# the ahead-of-time planner (Sections 4.1.1 and 4.2)
+from .planner import (RLG, Partition, Schedule, group_cycle, jaccard, lp_partition, rlg_build,  # noqa: E402
+                      score, sds_order, track_sets)

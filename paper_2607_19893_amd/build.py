@@ -3,8 +3,9 @@
 Every kernel file is compiled with packed-FP32 instructions disabled
 (-Xclang -target-feature -Xclang -packed-fp32-ops); the projection file is
 also built with -ffp-contract=off because its fp32 geometry must follow a
-fixed operation order, and the optimizer file because a parameter must
-change by exactly the step it publishes (no fused multiply-add).  Usage:  python -m paper_2607_19893_amd.build
+fixed operation order, the optimizer file because a parameter must
+change by exactly the step it publishes (no fused multiply-add), and the
+host planner because its doubles follow a fixed operation order.  Usage:  python -m paper_2607_19893_amd.build
 """
 from __future__ import annotations
 
@@ -21,8 +22,8 @@ BUILD_DIR = os.path.join(os.path.dirname(HERE), "_build", "gsmi")
 ARCH = os.environ.get("GSMI_ARCH", "gfx950")
 
 SOURCES = ["project.hip", "compact.hip", "binsort.hip", "raster.hip", "adam.hip", "delta.hip", "scope.hip",
-           "abi.cpp"]
-STRICT_FP = {"project.hip", "adam.hip"}
+           "planner.cpp", "abi.cpp"]
+STRICT_FP = {"project.hip", "adam.hip", "planner.cpp"}
 
 
 def hipcc() -> str:

@@ -488,4 +488,53 @@ gs_status gs_admission_gate(const uint32_t* RB, const uint32_t* D, const gs_gate
                       "gs_admission_gate");
 }
 
+gs_status gs_rlg_build(int32_t n_items, int32_t n_tracks, const int64_t* item_ptr, const int32_t* item_tracks,
+                       int32_t track_cap, int32_t top_k, int64_t* edge_ptr, int32_t* edge_dst, double* edge_w,
+                       int64_t edge_capacity, int64_t* n_edges) {
+    GS_REQUIRE(n_items >= 0 && n_tracks >= 0, "gs_rlg_build: negative size");
+    GS_REQUIRE(item_ptr && edge_ptr && n_edges, "gs_rlg_build: null pointer");
+    GS_REQUIRE(item_tracks || item_ptr[n_items] == 0, "gs_rlg_build: null item_tracks");
+    GS_REQUIRE(edge_capacity >= 0 && ((edge_dst && edge_w) || edge_capacity == 0),
+               "gs_rlg_build: null edge arrays");
+    char msg[160] = "";
+    const int s = gsmi::rlg_build(n_items, n_tracks, item_ptr, item_tracks, track_cap, top_k, edge_ptr, edge_dst,
+                                  edge_w, edge_capacity, n_edges, msg, sizeof msg);
+    if (s == GS_ERR_WORKSPACE)
+        return fail(GS_ERR_WORKSPACE, "gs_rlg_build: %lld edge entries needed, %lld available",
+                    (long long)*n_edges, (long long)edge_capacity);
+    if (s != GS_OK) return fail((gs_status)s, "gs_rlg_build: %s", msg);
+    return ok();
+}
+
+gs_status gs_lp_partition(int32_t n_items, const double* position, const int64_t* edge_ptr,
+                          const int32_t* edge_dst, const double* edge_w, int32_t K, int32_t max_iters,
+                          int32_t* group, double* coupling, int32_t* iters_run) {
+    GS_REQUIRE(n_items >= 0, "gs_lp_partition: n_items < 0");
+    GS_REQUIRE(K >= 1 && max_iters >= 1, "gs_lp_partition: K and max_iters must be >= 1");
+    GS_REQUIRE(edge_ptr && coupling && iters_run, "gs_lp_partition: null pointer");
+    if (n_items > 0) GS_REQUIRE(position && group, "gs_lp_partition: null pointer");
+    GS_REQUIRE(edge_ptr[n_items] == 0 || (edge_dst && edge_w), "gs_lp_partition: null edge arrays");
+    char msg[160] = "";
+    const int s = gsmi::lp_partition(n_items, position, edge_ptr, edge_dst, edge_w, K, max_iters, group, coupling,
+                                     iters_run, msg, sizeof msg);
+    if (s != GS_OK) return fail((gs_status)s, "gs_lp_partition: %s", msg);
+    return ok();
+}
+
+gs_status gs_sds_order(int32_t n_items, const int32_t* group, int32_t K, const double* coupling,
+                       const int64_t* edge_ptr, const int32_t* edge_dst, const double* edge_w, int32_t unit_size,
+                       int32_t* cycle, int32_t* n_cycle, int32_t* order, int32_t* unit_group, double* transition,
+                       int32_t* n_units) {
+    GS_REQUIRE(n_items >= 0, "gs_sds_order: n_items < 0");
+    GS_REQUIRE(K >= 1 && unit_size >= 1, "gs_sds_order: K and unit_size must be >= 1");
+    GS_REQUIRE(coupling && edge_ptr && cycle && n_cycle && n_units, "gs_sds_order: null pointer");
+    if (n_items > 0) GS_REQUIRE(group && order && unit_group && transition, "gs_sds_order: null pointer");
+    GS_REQUIRE(edge_ptr[n_items] == 0 || (edge_dst && edge_w), "gs_sds_order: null edge arrays");
+    char msg[160] = "";
+    const int s = gsmi::sds_order(n_items, group, K, coupling, edge_ptr, edge_dst, edge_w, unit_size, cycle,
+                                  n_cycle, order, unit_group, transition, n_units, msg, sizeof msg);
+    if (s != GS_OK) return fail((gs_status)s, "gs_sds_order: %s", msg);
+    return ok();
+}
+
 }  // extern "C"

@@ -118,17 +118,22 @@ _lib.gs_scope_from_ids.argtypes = [P, P, i32, i32, i32, P, P]
 _lib.gs_scope_from_pred.argtypes = [i32, P, i32, i32, P, P]
 _lib.gs_scope_conflicts.argtypes = [P, P, P, P, i32, P, P, P, P, P, P, P, P, sz, P]
 _lib.gs_admission_gate.argtypes = [P, P, ctypes.POINTER(gs_gate_args), i32, P, P, sz, P]
+_lib.gs_rlg_build.argtypes = [i32, i32, P, P, i32, i32, P, P, P, ctypes.c_int64, P]
+_lib.gs_lp_partition.argtypes = [i32, P, P, P, P, i32, i32, P, P, P]
+_lib.gs_sds_order.argtypes = [i32, P, i32, P, P, P, P, i32, P, P, P, P, P, P]
 for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
               "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
               "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
-              "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum", "gs_raster_fwd_l1"):
+              "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum", "gs_raster_fwd_l1",
+              "gs_rlg_build", "gs_lp_partition", "gs_sds_order"):
     getattr(_lib, _name).restype = i32
 
 EXPORTS = ["gs_abi_version", "gs_status_string", "gs_last_error", "gs_workspace_bytes", "gs_delta_msg_bytes",
            "gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
            "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
            "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
-           "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum", "gs_raster_fwd_l1"]
+           "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum", "gs_raster_fwd_l1",
+           "gs_rlg_build", "gs_lp_partition", "gs_sds_order"]
 
 
 class GsmiError(RuntimeError):
@@ -407,3 +412,82 @@ def gate_result_from(buf) -> gs_gate_result:
 def raw():
     """The loaded ctypes library (for tests of argument validation)."""
     return _lib
+
+
+# ---- the ahead-of-time planner (host arrays) --------------------------------
+
+def _np(a, dtype):
+    """A C-contiguous numpy array of dtype and its pointer (kept alive by the caller)."""
+    import numpy as np
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, ctypes.c_void_p(a.ctypes.data)
+
+
+class PlanGraph:
+    """The retained relative locality graph in CSR form (numpy arrays)."""
+
+    def __init__(self, edge_ptr, edge_dst, edge_w):
+        self.edge_ptr, self.edge_dst, self.edge_w = edge_ptr, edge_dst, edge_w
+
+    def ptrs(self):
+        return (ctypes.c_void_p(self.edge_ptr.ctypes.data), ctypes.c_void_p(self.edge_dst.ctypes.data),
+                ctypes.c_void_p(self.edge_w.ctypes.data))
+
+
+def gs_rlg_build(item_ptr, item_tracks, n_tracks, track_cap, top_k) -> PlanGraph:
+    import numpy as np
+    ip, ip_p = _np(item_ptr, np.int64)
+    it, it_p = _np(item_tracks if len(item_tracks) else np.zeros(1, np.int32), np.int32)
+    n = ip.size - 1
+    cap = 2 * n * int(top_k) if top_k > 0 else 0
+    for _ in range(2):
+        eptr = np.zeros(n + 1, np.int64)
+        edst = np.zeros(max(cap, 1), np.int32)
+        ew = np.zeros(max(cap, 1), np.float64)
+        ne = ctypes.c_int64(0)
+        st = _lib.gs_rlg_build(int(n), int(n_tracks), ip_p, it_p, int(track_cap), int(top_k),
+                               ctypes.c_void_p(eptr.ctypes.data), ctypes.c_void_p(edst.ctypes.data),
+                               ctypes.c_void_p(ew.ctypes.data), int(cap), ctypes.byref(ne))
+        if st == GS_ERR_WORKSPACE and cap < ne.value:
+            cap = int(ne.value)
+            continue
+        _check("gs_rlg_build", st)
+        return PlanGraph(eptr, edst[:ne.value].copy(), ew[:ne.value].copy())
+    raise GsmiError("gs_rlg_build", GS_ERR_WORKSPACE)
+
+
+def gs_lp_partition(position, graph: PlanGraph, K, max_iters):
+    """Returns (group [n] int32, coupling [K, K] float64, rounds run)."""
+    import numpy as np
+    pos, pos_p = _np(np.asarray(position, np.float64).reshape(-1, 3), np.float64)
+    n = pos.shape[0]
+    group = np.zeros(max(n, 1), np.int32)
+    coupling = np.zeros((K, K), np.float64)
+    it = ctypes.c_int32(0)
+    ep, ed, ew = graph.ptrs()
+    _check("gs_lp_partition", _lib.gs_lp_partition(int(n), pos_p, ep, ed, ew, int(K), int(max_iters),
+                                                   ctypes.c_void_p(group.ctypes.data),
+                                                   ctypes.c_void_p(coupling.ctypes.data), ctypes.byref(it)))
+    return group[:n], coupling, int(it.value)
+
+
+def gs_sds_order(group, coupling, graph: PlanGraph, unit_size):
+    """Returns (cycle, order, unit_group, transition) as numpy arrays."""
+    import numpy as np
+    g, g_p = _np(group, np.int32)
+    K = int(np.asarray(coupling).shape[0])
+    C, C_p = _np(coupling, np.float64)
+    n = g.size
+    units = -(-n // int(unit_size)) if n else 0
+    cycle = np.zeros(K, np.int32)
+    order = np.zeros(max(n, 1), np.int32)
+    ug = np.zeros(max(units, 1), np.int32)
+    tr = np.zeros(max(units, 1), np.float64)
+    nc, nu = ctypes.c_int32(0), ctypes.c_int32(0)
+    ep, ed, ew = graph.ptrs()
+    _check("gs_sds_order", _lib.gs_sds_order(int(n), g_p, K, C_p, ep, ed, ew, int(unit_size),
+                                             ctypes.c_void_p(cycle.ctypes.data), ctypes.byref(nc),
+                                             ctypes.c_void_p(order.ctypes.data), ctypes.c_void_p(ug.ctypes.data),
+                                             ctypes.c_void_p(tr.ctypes.data), ctypes.byref(nu)))
+    assert nu.value == units
+    return cycle[:nc.value], order[:n], ug[:units], tr[:units]

@@ -343,3 +343,75 @@ def adam_state(seed: int, n: int, cols: int, scale_m: float = 1e-4, scale_v: flo
     m = (rng.standard_normal((n, cols)) * scale_m).astype(np.float32)
     v = (np.abs(rng.standard_normal((n, cols))) * scale_v).astype(np.float32)
     return m, v
+
+
+@dataclasses.dataclass
+class Capture:
+    """Camera centres and feature tracks of a synthetic image capture.
+
+    item_ptr / item_tracks are a CSR list of each image's track ids
+    (ascending, no repeats); position holds the camera centres [n, 3]."""
+    name: str
+    position: np.ndarray       # [n, 3] float64
+    item_ptr: np.ndarray       # [n + 1] int64
+    item_tracks: np.ndarray    # int32
+    n_tracks: int
+
+    @property
+    def n(self) -> int:
+        return int(self.position.shape[0])
+
+    def tracks_of(self, i: int) -> np.ndarray:
+        return self.item_tracks[self.item_ptr[i]:self.item_ptr[i + 1]]
+
+
+def capture_tracks(n_images: int, seed: int = 5, obs_per_image: float = 300.0, long_frac: float = 0.01,
+                   spacing: float = 10.0, altitude: float = 120.0) -> Capture:
+    """Stand-in for the SfM tracks of an aerial survey (the paper's planner
+    input; no SfM reconstruction is available here).  Images sit on a
+    lawn-mower flight grid (ids follow the flight path, every other row
+    reversed) with jittered centres.  A track is a scene point seen by the
+    images of an a x b block of neighbouring grid cells, a, b in 1..3
+    (lengths 1-9, mean 4); a fraction ``long_frac`` of tracks are outliers
+    seen by blocks of 8-20 cells a side (the long tracks an outlier cap
+    removes).  About ``obs_per_image`` observations per image."""
+    rng = np.random.default_rng(seed)
+    n = int(n_images)
+    side = max(1, int(math.ceil(math.sqrt(n))))
+    rows = -(-n // side)
+    # grid cell -> image id along the flight path (cells past n are empty)
+    gy, gx = np.divmod(np.arange(rows * side), side)
+    path_x = np.where(gy % 2 == 0, gx, side - 1 - gx)
+    cell_id = np.full(rows * side, -1, np.int64)
+    flat = gy * side + path_x
+    cell_id[flat] = np.arange(rows * side)
+    cell_id[cell_id >= n] = -1
+    pos = np.zeros((n, 3))
+    ids = cell_id[cell_id >= 0]
+    cells = np.nonzero(cell_id >= 0)[0]
+    pos[ids, 0] = (cells % side) * spacing + rng.normal(0.0, 0.1 * spacing, ids.size)
+    pos[ids, 1] = (cells // side) * spacing + rng.normal(0.0, 0.1 * spacing, ids.size)
+    pos[ids, 2] = altitude + rng.normal(0.0, 0.02 * altitude, ids.size)
+    n_tracks = max(1, int(n * obs_per_image / 4.0))
+    a = rng.integers(1, 4, n_tracks)
+    b = rng.integers(1, 4, n_tracks)
+    big = rng.random(n_tracks) < long_frac
+    a[big] = rng.integers(8, 21, int(big.sum()))
+    b[big] = rng.integers(8, 21, int(big.sum()))
+    x0 = rng.integers(0, side, n_tracks)
+    y0 = rng.integers(0, rows, n_tracks)
+    cnt = a * b
+    tr = np.repeat(np.arange(n_tracks), cnt)
+    local = np.arange(int(cnt.sum())) - np.repeat(np.cumsum(cnt) - cnt, cnt)
+    cx = np.repeat(x0, cnt) + local % np.repeat(a, cnt)
+    cy = np.repeat(y0, cnt) + local // np.repeat(a, cnt)
+    ok = (cx < side) & (cy < rows)
+    img = np.full(tr.size, -1, np.int64)
+    img[ok] = cell_id[cy[ok] * side + cx[ok]]
+    ok = img >= 0
+    img, tr = img[ok], tr[ok]
+    o = np.argsort(img, kind="stable")       # track ids were generated ascending
+    img, tr = img[o], tr[o]
+    ptr = np.zeros(n + 1, np.int64)
+    np.cumsum(np.bincount(img, minlength=n), out=ptr[1:])
+    return Capture("aerial-%d" % n, pos, ptr, tr.astype(np.int32), n_tracks)
