@@ -258,8 +258,8 @@ def main():
     log("phase rooflines: " + json.dumps(per_phase))
     wi_mean = float(np.mean([w_iters[v] for v in views]))
     wh_mean = float(np.mean([w_hits[v] for v in views]))
-    log("mean per view: V=%.0f M=%.0f evaluated=%.3g included=%.3g; forward (wave, pair) iterations %.3g, "
-        "with an included pixel %.3g (%.1f%%), included lanes per such iteration %.1f"
+    log("mean per view: V=%.0f M=%.0f evaluated=%.3g included=%.3g; forward (pixel row, pair) steps %.3g, "
+        "with an included pixel %.3g (%.1f%%), included lanes per such step %.1f of 16"
         % (V_mean, M_mean, ev_mean, inc_mean, wi_mean, wh_mean, 100 * wh_mean / max(wi_mean, 1),
            inc_mean / max(wh_mean, 1)))
 
