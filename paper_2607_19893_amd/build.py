@@ -11,6 +11,7 @@ from __future__ import annotations
 
 import concurrent.futures as cf
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -45,11 +46,29 @@ def _flags(src: str):
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, src + ".o")
-    cmd = [hipcc()] + _flags(src) + ["-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc()] + _flags(src) + ["-Rpass-analysis=kernel-resource-usage", "-c", os.path.join(CSRC, src),
+                                     "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), r.stderr[-6000:]))
+    check_no_scratch(src, r.stderr)
     return obj
+
+
+def check_no_scratch(src: str, remarks: str) -> None:
+    """Refuse kernels that use private (scratch) memory: besides the slow
+    memory path, a launch that needs scratch can stall the launching thread
+    while the runtime sets scratch up for the queue, which showed up as gaps
+    of up to 43 ms between kernels of a training step."""
+    name = None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) > 0:
+            raise RuntimeError("%s: kernel %s uses %s bytes of scratch per lane" % (src, name, m.group(1)))
 
 
 def build(verbose: bool = False) -> str:
