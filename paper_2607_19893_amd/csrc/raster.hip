@@ -194,7 +194,7 @@ __device__ __forceinline__ float l1_elem(float a, float t, float inv, float& dl)
 // the target exactly as k_loss_l1 does, writes dL/dimg, and each tile leaves
 // its sum of |img - target| in loss_partial[tile] for k_loss_final.
 template <bool STATS, bool LOSS>
-__global__ void __launch_bounds__(GS_BLOCK) k_raster_fwd(
+__global__ void __launch_bounds__(GS_BLOCK, 7) k_raster_fwd(
     const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, float* __restrict__ img, float* __restrict__ final_T, uint32_t* __restrict__ n_contrib,
