@@ -47,7 +47,7 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 
 # HBM traffic of the dominant kernel (k_raster_bwd) on this workload, from two
 # rocprofv3 --pmc passes (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch, mean
-# of the first 10 dispatches of an 8-step run: 2 warm-up and 8 timed views),
+# of the 10 dispatches of an 8-step run without extras: 2 warm-up and 8 timed),
 # each scaled by what the same counter reads for a plain device copy of known
 # size (a 1 GiB read registers as 0.5 GiB of FETCH_SIZE, a 1 GiB write as
 # 1 GiB of WRITE_SIZE).  Valid only for the kernel code it was measured on
@@ -55,9 +55,9 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 TRAFFIC = {
     "kernel": "k_raster_bwd",
     "source": "paper_2607_19893_amd/csrc/raster.hip",
-    "code_sha256": "9ba419c340b5a24ce2c37fe03c9c59bfac1f6b13d0ecfbdfa7d323e7b10afea1",
-    "fetch_kib": 205965.09, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 98510.76, "write_scale": 1048576.0 / 1048576.0,
+    "code_sha256": "6c562d74f0f9a21dc9f2d7e07fc29aaa6ea7773cd987bc5101486f34bd6e6960",
+    "fetch_kib": 205945.17, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 98519.49, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
