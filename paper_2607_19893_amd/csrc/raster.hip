@@ -381,16 +381,33 @@ __global__ void __launch_bounds__(GS_BLOCK) k_loss_l1(const float* __restrict__ 
 
 __global__ void __launch_bounds__(GS_BLOCK) k_loss_final(const float* __restrict__ partial, uint32_t nb,
                                                          double inv_total, float* __restrict__ loss) {
-    __shared__ double s[GS_BLOCK];
+    __shared__ double s[GS_BLOCK / GS_WAVE];
+    constexpr int U = 8;
     double acc = 0.0;
-    for (uint32_t i = threadIdx.x; i < nb; i += GS_BLOCK) acc += (double)partial[i];
-    s[threadIdx.x] = acc;
-    __syncthreads();
-    for (int w = GS_BLOCK / 2; w > 0; w >>= 1) {
-        if (threadIdx.x < w) s[threadIdx.x] += s[threadIdx.x + w];
-        __syncthreads();
+    // all of a thread's loads are issued before its sums (float4 when aligned)
+    uint32_t done = 0;
+    if ((reinterpret_cast<uintptr_t>(partial) & 15u) == 0u) {
+        const uint32_t n4 = nb / 4u;
+        const float4* p4 = reinterpret_cast<const float4*>(partial);
+        for (uint32_t i0 = threadIdx.x; i0 < n4; i0 += U * GS_BLOCK) {
+            float4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint32_t i = i0 + (uint32_t)u * GS_BLOCK;
+                v[u] = i < n4 ? p4[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                acc += ((double)v[u].x + (double)v[u].y) + ((double)v[u].z + (double)v[u].w);
+        }
+        done = 4u * n4;
     }
-    if (threadIdx.x == 0) *loss = (float)(s[0] * inv_total);
+    for (uint32_t i = done + threadIdx.x; i < nb; i += GS_BLOCK) acc += (double)partial[i];
+#pragma unroll
+    for (int d = GS_WAVE / 2; d >= 1; d >>= 1) acc += __shfl_xor(acc, d, GS_WAVE);
+    if (lane_id() == 0) s[threadIdx.x / GS_WAVE] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) *loss = (float)(((s[0] + s[1]) + (s[2] + s[3])) * inv_total);
 }
 
 // ---------------------------------------------------------------------------
