@@ -24,6 +24,7 @@ partition, schedule) on synthetic captures of 1,000 to 50,000 images.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -60,6 +61,15 @@ TRAFFIC = {
     "write_kib": 98519.49, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
+
+
+def no_collector():
+    """Run a full collector pass now and switch the collector off (until
+    gc.enable()): a pass over the process's Python objects inside a timed
+    loop can hold the issuing thread for tens of milliseconds and idle the
+    GPU at a random phase."""
+    gc.collect()
+    gc.disable()
 
 
 def code_digest(text):
@@ -177,6 +187,7 @@ def main():
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
     views = []
     torch.cuda.synchronize()
+    no_collector()
     t_start = time.perf_counter()
     for k in range(args.steps):
         step += 1
@@ -187,6 +198,7 @@ def main():
     t_issued = time.perf_counter()
     torch.cuda.synchronize()
     t_end = time.perf_counter()
+    gc.enable()
     wall = t_end - t_start
     log("host issue time %.3f ms per step (device %.3f ms per step)"
         % (1e3 * (t_issued - t_start) / args.steps, 1e3 * wall / args.steps))
@@ -343,6 +355,7 @@ def bench_scope_gate(tr, cams, targets, steps):
     hz = np.zeros(4)
     reasons = {}
     moved = 0.0
+    no_collector()
     for k in range(steps):
         a, b = k % nv, (k + 1) % nv
         e0.record()
@@ -361,6 +374,7 @@ def bench_scope_gate(tr, cams, targets, steps):
         # bytes: conflicts read 4 scopes and write 3 bitmaps and the id lists;
         # the gate reads 4 scopes and ||g_A|| at C_A and D+
         moved += 7 * words * 4 + 4 * float(c[:3].sum()) + 4 * words * 4 + 4 * (r.n_active + r.n_delayed)
+    gc.enable()
     t_conf /= steps
     t_gate /= steps
     hz /= steps
@@ -386,6 +400,7 @@ def bench_unit(tr, cams, targets, steps, step0):
         v = (2 * u) % nv
         tr.step_unit([cams[v], cams[(v + 1) % nv]], step, version, [targets[v], targets[(v + 1) % nv]])
     torch.cuda.synchronize()
+    no_collector()
     t0 = time.perf_counter()
     for u in range(units):
         step += 1; version += 1
@@ -393,6 +408,7 @@ def bench_unit(tr, cams, targets, steps, step0):
         tr.step_unit([cams[v], cams[(v + 1) % nv]], step, version, [targets[v], targets[(v + 1) % nv]])
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    gc.enable()
     from paper_2607_19893_amd.pipeline import to_u32
     assert to_u32(tr.status)[0] == 0, "device status flags set during the task units"
     return {"units": units, "views_per_unit": 2, "views_per_s": round(2 * units / dt, 2),
