@@ -56,9 +56,9 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 TRAFFIC = {
     "kernel": "k_raster_bwd",
     "source": "paper_2607_19893_amd/csrc/raster.hip",
-    "code_sha256": "6c562d74f0f9a21dc9f2d7e07fc29aaa6ea7773cd987bc5101486f34bd6e6960",
-    "fetch_kib": 205945.17, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 98519.49, "write_scale": 1048576.0 / 1048576.0,
+    "code_sha256": "f568ca3b0ad8456752f580f6a033a8c2dcf07ab0713fe7146ac1aaaf2effdfd9",
+    "fetch_kib": 205952.91, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 98524.06, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
