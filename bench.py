@@ -117,6 +117,9 @@ def main():
     ap.add_argument("--dense-params", action="store_true",
                     help="hold the parameter groups as five dense tensors instead of dense means and SH beside one "
                          "[n, 8] head table of quat, log_scale and opacity (same arithmetic, different addresses)")
+    ap.add_argument("--row-major-tiles", action="store_true",
+                    help="let the raster workgroups take the tiles in row-major order instead of the bin sort's "
+                         "longest-first dispatch order (same results)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy (read + write of this many MiB, 4 times) and exit; "
                          "its HBM counters calibrate the traffic counters of the path's kernels")
@@ -145,6 +148,7 @@ def main():
     tr = ViewTrainer(w.scene, capacity=1, max_width=max(c.width for c in cams),
                      max_height=max(c.height for c in cams), lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps,
                      packed=not args.dense_params)
+    tr.longest_first = not args.row_major_tiles
     need = tr.ensure_capacity(cams)
     log("pair capacity %d (max pairs over the views %d)" % (tr.capacity, need))
     t0 = time.time()
@@ -312,7 +316,8 @@ def main():
                    "mean_visible": round(V_mean), "mean_pairs": round(M_mean),
                    "step": "project+visible+bin_sort+fwd_l1+bwd+sparse_adam_publish+commit",
                    "apply_overlapped": not args.no_overlap,
-                   "param_layout": "dense" if args.dense_params else "head8"},
+                   "param_layout": "dense" if args.dense_params else "head8",
+                   "tile_dispatch": "row_major" if args.row_major_tiles else "longest_first"},
         "roofline": roofline,
         "phases_ms": {k: v["ms"] for k, v in per_phase.items()},
         "phases_frac": {k: v["frac"] for k, v in per_phase.items()},

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define GSMI_ABI_VERSION 3
+#define GSMI_ABI_VERSION 4
 #define GS_TILE 16            /* pixels per tile side */
 #define GS_MAX_SH_DEGREE 3
 #define GS_MAX_GROUPS 8
@@ -200,6 +200,14 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
  *   capacity: length of vals (and keys); more pairs set GS_DEV_PAIR_OVERFLOW
  *   vals   [capacity] uint32  primitive id of every sorted pair
  *   ranges [T,2] uint32       [start, end) of each tile's pairs, T = tiles in the image
+ *   tile_order [T] uint32 or NULL: a dispatch order for the per-tile kernels,
+ *                             the tile ids by pair count descending (counts
+ *                             compared through an 8-bit code: exact below 16,
+ *                             then 16 steps per octave, one code from 2^19 on),
+ *                             equal codes by ascending id.  It changes no result
+ *                             of any call that takes it; it lets the longest
+ *                             tiles start first.  Written even when there are
+ *                             no pairs (then it is 0..T-1).
  *   pair_offset [n] uint32    per visible primitive: first of its pairs in
  *                             emission order (primitives in ascending id order, each one's
  *                             rectangle row-major); read by gs_raster_bwd
@@ -211,8 +219,8 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
  */
 gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                       int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                      uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys, uint32_t* num_pairs,
-                      gs_device_status* status, void* ws, size_t ws_bytes, void* stream);
+                      uint32_t* tile_order, uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys,
+                      uint32_t* num_pairs, gs_device_status* status, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Phase "rendering", part 2 (R in Figure 6): front-to-back alpha blending of
@@ -231,10 +239,13 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
  *   kernel walks pairs in), and of those steps in which at least one pixel
  *   included the pair
  *   bg: 3 floats on the HOST
+ *   tile_order [T] uint32 or NULL: the order in which workgroups take the
+ *   tiles (gs_bin_sort's tile_order, any permutation of 0..T-1, or NULL for
+ *   row-major); results do not depend on it.  Entries >= T are skipped.
  */
 gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,
-                        int32_t width, int32_t height, const float* bg, float* img, float* final_T,
-                        uint32_t* n_contrib, uint8_t* active, uint64_t* pair_stats, void* stream);
+                        const uint32_t* tile_order, int32_t width, int32_t height, const float* bg, float* img,
+                        float* final_T, uint32_t* n_contrib, uint8_t* active, uint64_t* pair_stats, void* stream);
 
 /*
  * gs_raster_fwd followed by gs_loss_l1 in one pass over the image (the
@@ -243,13 +254,13 @@ gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, co
  * bit (the same fp32 comparison per channel); loss is the same mean, summed
  * per 16x16 tile and then over the tiles in fp64, so it can differ from
  * gs_loss_l1's value in the last fp32 bits.
- *   target [3,H,W] fp32; loss: one float on the device
+ *   target [3,H,W] fp32; loss: one float on the device; tile_order as in gs_raster_fwd
  *   ws: gs_workspace_bytes(GS_WS_RASTER_FWD_L1, 0, 0, W, H) bytes
  */
 gs_status gs_raster_fwd_l1(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,
-                           int32_t width, int32_t height, const float* bg, const float* target, float* img,
-                           float* final_T, uint32_t* n_contrib, uint8_t* active, float* loss, float* dL_dimg, void* ws,
-                           size_t ws_bytes, void* stream);
+                           const uint32_t* tile_order, int32_t width, int32_t height, const float* bg,
+                           const float* target, float* img, float* final_T, uint32_t* n_contrib, uint8_t* active,
+                           float* loss, float* dL_dimg, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Image loss (Section 2.1): L = mean over all 3*H*W entries of |img - target|;
@@ -275,13 +286,14 @@ gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32
  *   grad2d [n,9] fp32 or NULL: (du, dv, dA, dB, dC, dopacity, dr, dg, db) per visible id
  *   grad_norm [n] fp32 or NULL (visible ids)
  *   ws: gs_workspace_bytes(GS_WS_RASTER_BWD, n, capacity, W, H); capacity as in gs_bin_sort
+ *   tile_order: as in gs_raster_fwd (the per-pixel replay's dispatch order)
  */
 gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
-                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_emit,
-                        const uint32_t* vis_idx,
-                        const uint32_t* vis_count, uint32_t capacity, const float* final_T,
-                        const uint32_t* n_contrib, const float* dL_dimg, const float* bg, float* grad_rows,
-                        int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream);
+                        const uint32_t* ranges, const uint32_t* tile_order, const uint32_t* pair_offset,
+                        const uint32_t* pair_emit, const uint32_t* vis_idx, const uint32_t* vis_count,
+                        uint32_t capacity, const float* final_T, const uint32_t* n_contrib, const float* dL_dimg,
+                        const float* bg, float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws,
+                        size_t ws_bytes, void* stream);
 
 /*
  * The two halves of gs_raster_bwd, for callers that schedule or time them
@@ -295,10 +307,9 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
  * second.  Arguments mean what they mean in gs_raster_bwd.
  */
 gs_status gs_raster_bwd_pixels(const gs_proj* proj, const gs_camera* cam, const uint32_t* vals,
-                               const uint32_t* ranges, const uint32_t* pair_emit, uint32_t capacity,
-                               const float* final_T,
-                               const uint32_t* n_contrib, const float* dL_dimg, const float* bg, void* ws,
-                               size_t ws_bytes, void* stream);
+                               const uint32_t* ranges, const uint32_t* tile_order, const uint32_t* pair_emit,
+                               uint32_t capacity, const float* final_T, const uint32_t* n_contrib,
+                               const float* dL_dimg, const float* bg, void* ws, size_t ws_bytes, void* stream);
 gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj,
                                 const uint32_t* pair_offset, const uint32_t* vis_idx,
                                 const uint32_t* vis_count, uint32_t capacity, float* grad_rows, int32_t grad_ld,

@@ -173,8 +173,8 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
 
 gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                       int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                      uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys, uint32_t* num_pairs,
-                      gs_device_status* status, void* ws, size_t ws_bytes, void* stream) {
+                      uint32_t* tile_order, uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys,
+                      uint32_t* num_pairs, gs_device_status* status, void* ws, size_t ws_bytes, void* stream) {
     gs_status s;
     if ((s = check_proj(proj, false, "gs_bin_sort")) != GS_OK) return s;
     GS_REQUIRE(n >= 0 && width >= 0 && height >= 0, "gs_bin_sort: negative size");
@@ -186,14 +186,14 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
     if (ws_bytes < gsmi::binsort_ws_bytes(n, capacity, width, height))
         return fail(GS_ERR_WORKSPACE, "gs_bin_sort: workspace too small");
     return hip_status(gsmi::launch_binsort(*proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges,
-                                           pair_offset, pair_emit, keys, num_pairs, status, ws,
+                                           tile_order, pair_offset, pair_emit, keys, num_pairs, status, ws,
                                            static_cast<hipStream_t>(stream)),
                       "gs_bin_sort");
 }
 
-gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges, int32_t width,
-                        int32_t height, const float* bg, float* img, float* final_T, uint32_t* n_contrib,
-                        uint8_t* active, uint64_t* pair_stats, void* stream) {
+gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,
+                        const uint32_t* tile_order, int32_t width, int32_t height, const float* bg, float* img,
+                        float* final_T, uint32_t* n_contrib, uint8_t* active, uint64_t* pair_stats, void* stream) {
     gs_status s;
     if ((s = check_proj(proj, false, "gs_raster_fwd")) != GS_OK) return s;
     GS_REQUIRE(n >= 0 && width >= 0 && height >= 0, "gs_raster_fwd: negative size");
@@ -201,14 +201,15 @@ gs_status gs_raster_fwd(const gs_proj* proj, int32_t n, const uint32_t* vals, co
         return fail(GS_ERR_UNSUPPORTED, "gs_raster_fwd: image side above %d", GS_MAX_IMAGE_SIDE);
     GS_REQUIRE(vals && ranges && bg && img && final_T && n_contrib, "gs_raster_fwd: null pointer");
     GS_REQUIRE(pair_stats == nullptr || aligned(pair_stats, 8), "gs_raster_fwd: pair_stats misaligned");
-    return hip_status(gsmi::launch_raster_fwd(*proj, vals, ranges, width, height, bg, img, final_T, n_contrib, active,
-                                              pair_stats, static_cast<hipStream_t>(stream)),
+    return hip_status(gsmi::launch_raster_fwd(*proj, vals, ranges, tile_order, width, height, bg, img, final_T,
+                                              n_contrib, active, pair_stats, static_cast<hipStream_t>(stream)),
                       "gs_raster_fwd");
 }
 
 gs_status gs_raster_fwd_l1(const gs_proj* proj, int32_t n, const uint32_t* vals, const uint32_t* ranges,
-                           int32_t width, int32_t height, const float* bg, const float* target, float* img,
-                           float* final_T, uint32_t* n_contrib, uint8_t* active, float* loss, float* dL_dimg, void* ws,
+                           const uint32_t* tile_order, int32_t width, int32_t height, const float* bg,
+                           const float* target, float* img, float* final_T, uint32_t* n_contrib, uint8_t* active,
+                           float* loss, float* dL_dimg, void* ws,
                            size_t ws_bytes, void* stream) {
     gs_status s;
     if ((s = check_proj(proj, false, "gs_raster_fwd_l1")) != GS_OK) return s;
@@ -219,8 +220,8 @@ gs_status gs_raster_fwd_l1(const gs_proj* proj, int32_t n, const uint32_t* vals,
                "gs_raster_fwd_l1: null pointer");
     if (ws_bytes < gsmi::raster_fwd_l1_ws_bytes(width, height))
         return fail(GS_ERR_WORKSPACE, "gs_raster_fwd_l1: workspace too small");
-    return hip_status(gsmi::launch_raster_fwd_l1(*proj, vals, ranges, width, height, bg, target, img, final_T,
-                                                 n_contrib, active, loss, dL_dimg, ws,
+    return hip_status(gsmi::launch_raster_fwd_l1(*proj, vals, ranges, tile_order, width, height, bg, target, img,
+                                                 final_T, n_contrib, active, loss, dL_dimg, ws,
                                                  static_cast<hipStream_t>(stream)),
                       "gs_raster_fwd_l1");
 }
@@ -236,10 +237,11 @@ gs_status gs_loss_l1(const float* img, const float* target, int32_t width, int32
 }
 
 gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_proj* proj, const uint32_t* vals,
-                        const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_emit,
-                        const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity, const float* final_T,
-                        const uint32_t* n_contrib, const float* dL_dimg, const float* bg, float* grad_rows,
-                        int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, size_t ws_bytes, void* stream) {
+                        const uint32_t* ranges, const uint32_t* tile_order, const uint32_t* pair_offset,
+                        const uint32_t* pair_emit, const uint32_t* vis_idx, const uint32_t* vis_count,
+                        uint32_t capacity, const float* final_T, const uint32_t* n_contrib, const float* dL_dimg,
+                        const float* bg, float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws,
+                        size_t ws_bytes, void* stream) {
     gs_status s;
     if ((s = check_scene(scene, "gs_raster_bwd")) != GS_OK) return s;
     if ((s = check_grad_rows(scene, grad_rows, grad_ld, "gs_raster_bwd")) != GS_OK) return s;
@@ -252,16 +254,17 @@ gs_status gs_raster_bwd(const gs_scene* scene, const gs_camera* cam, const gs_pr
     if (ws_bytes < gsmi::raster_bwd_ws_bytes(scene->n, capacity))
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
-    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, vals, ranges, pair_offset, pair_emit, vis_idx,
-                                              vis_count, capacity, final_T, n_contrib, dL_dimg, bg, grad_rows,
-                                              grad_ld, grad2d, grad_norm, ws, 3, static_cast<hipStream_t>(stream)),
+    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, vals, ranges, tile_order, pair_offset, pair_emit,
+                                              vis_idx, vis_count, capacity, final_T, n_contrib, dL_dimg, bg,
+                                              grad_rows, grad_ld, grad2d, grad_norm, ws, 3,
+                                              static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd");
 }
 
 gs_status gs_raster_bwd_pixels(const gs_proj* proj, const gs_camera* cam, const uint32_t* vals, const uint32_t* ranges,
-                               const uint32_t* pair_emit, uint32_t capacity, const float* final_T,
-                               const uint32_t* n_contrib, const float* dL_dimg, const float* bg, void* ws,
-                               size_t ws_bytes, void* stream) {
+                               const uint32_t* tile_order, const uint32_t* pair_emit, uint32_t capacity,
+                               const float* final_T, const uint32_t* n_contrib, const float* dL_dimg, const float* bg,
+                               void* ws, size_t ws_bytes, void* stream) {
     gs_status s;
     if ((s = check_camera(cam, "gs_raster_bwd_pixels")) != GS_OK) return s;
     if ((s = check_proj(proj, false, "gs_raster_bwd_pixels")) != GS_OK) return s;
@@ -272,9 +275,9 @@ gs_status gs_raster_bwd_pixels(const gs_proj* proj, const gs_camera* cam, const 
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_pixels: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
     gs_scene none = {0, 0, nullptr, nullptr, nullptr, nullptr, nullptr};
-    return hip_status(gsmi::launch_raster_bwd(none, c, *proj, vals, ranges, nullptr, pair_emit, nullptr, nullptr,
-                                              capacity, final_T, n_contrib, dL_dimg, bg, nullptr, 0, nullptr, nullptr,
-                                              ws, 1, static_cast<hipStream_t>(stream)),
+    return hip_status(gsmi::launch_raster_bwd(none, c, *proj, vals, ranges, tile_order, nullptr, pair_emit, nullptr,
+                                              nullptr, capacity, final_T, n_contrib, dL_dimg, bg, nullptr, 0, nullptr,
+                                              nullptr, ws, 1, static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd_pixels");
 }
 
@@ -293,9 +296,9 @@ gs_status gs_raster_bwd_project(const gs_scene* scene, const gs_camera* cam, con
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_project: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
     const float bg0[3] = {0.0f, 0.0f, 0.0f};
-    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, nullptr, nullptr, pair_offset, nullptr, vis_idx,
-                                              vis_count, capacity, nullptr, nullptr, nullptr, bg0, grad_rows, grad_ld,
-                                              grad2d, grad_norm, ws, 2, static_cast<hipStream_t>(stream)),
+    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, nullptr, nullptr, nullptr, pair_offset, nullptr,
+                                              vis_idx, vis_count, capacity, nullptr, nullptr, nullptr, bg0, grad_rows,
+                                              grad_ld, grad2d, grad_norm, ws, 2, static_cast<hipStream_t>(stream)),
                       "gs_raster_bwd_project");
 }
 
@@ -316,10 +319,10 @@ gs_status gs_raster_bwd_project_accum(const gs_scene* scene, const gs_camera* ca
         return fail(GS_ERR_WORKSPACE, "gs_raster_bwd_project_accum: workspace too small");
     const gsmi::CamArgs c = gsmi::make_cam_args(cam);
     const float bg0[3] = {0.0f, 0.0f, 0.0f};
-    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, nullptr, nullptr, pair_offset, nullptr, vis_idx,
-                                              vis_count, capacity, nullptr, nullptr, nullptr, bg0, grad_rows, grad_ld,
-                                              nullptr, grad_norm, ws, 2, static_cast<hipStream_t>(stream), union_idx,
-                                              union_count, first != 0),
+    return hip_status(gsmi::launch_raster_bwd(*scene, c, *proj, nullptr, nullptr, nullptr, pair_offset, nullptr,
+                                              vis_idx, vis_count, capacity, nullptr, nullptr, nullptr, bg0, grad_rows,
+                                              grad_ld, nullptr, grad_norm, ws, 2, static_cast<hipStream_t>(stream),
+                                              union_idx, union_count, first != 0),
                       "gs_raster_bwd_project_accum");
 }
 

@@ -320,13 +320,75 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
 constexpr int kSortCap = GS_TILE_ITEMS;
 constexpr unsigned long long kKeyMax = ~0ull;
 
-__device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* __restrict__ a, uint32_t n, uint32_t x) {
-    uint32_t lo = 0, hi = n;
-    while (lo < hi) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (a[mid] < x) lo = mid + 1; else hi = mid;
+// Dispatch key of a tile from its pair count: an 8-bit code that never
+// decreases with the count (exact below 16, then 16 steps per octave; counts
+// of 2^19 and more share the top code), inverted so that an ascending radix
+// pass puts the longest tiles first.
+__device__ __forceinline__ uint32_t tile_order_key(uint32_t n) {
+    uint32_t code = n;
+    if (n >= 16u) {
+        const uint32_t e = 31u - (uint32_t)__clz(n);      // >= 4
+        code = e > 18u ? 255u : 16u * (e - 3u) + ((n >> (e - 4u)) & 15u);
     }
-    return lo;
+    return 255u - code;
+}
+
+constexpr int kRangeSearches = GS_ITEMS + 1;
+
+// Tile ranges from the M tile-sorted pair keys, and every tile's dispatch key.
+// Block b covers tiles [b*2048, b*2048+2048).  A thread finds the first pair
+// of its eight tiles and of the tile after the block (the same for every
+// thread) with a branch-free lower bound whose searches all advance one level
+// per round (the step lengths depend on M only).  The block's per-digit
+// counts of the dispatch keys go to the digit-major histogram matrix that the
+// radix scan reads.  sort_count may be null: no pairs.
+__global__ void __launch_bounds__(GS_BLOCK) k_tile_ranges(const uint32_t* __restrict__ skeys,
+                                                          const uint32_t* __restrict__ sort_count, uint32_t T,
+                                                          uint32_t* __restrict__ ranges, uint32_t* __restrict__ tkeys,
+                                                          uint32_t* __restrict__ hist, uint32_t nblocks,
+                                                          uint32_t* __restrict__ tile_count) {
+    static_assert(GS_BLOCK == 256, "one digit counter per thread");
+    __shared__ uint32_t s_start[GS_TILE_ITEMS + 1];
+    __shared__ uint32_t h[256];
+    const uint32_t tid = threadIdx.x;
+    const uint32_t M = sort_count ? *sort_count : 0u;
+    const uint32_t b0 = blockIdx.x * GS_TILE_ITEMS;
+    h[tid] = 0;
+    if (blockIdx.x == 0 && tid == 0) *tile_count = T;
+    uint32_t v[kRangeSearches], pos[kRangeSearches];
+#pragma unroll
+    for (int k = 0; k < kRangeSearches; ++k) {
+        v[k] = b0 + (k < GS_ITEMS ? k * GS_BLOCK + tid : GS_TILE_ITEMS);
+        pos[k] = 0;
+    }
+    if (M > 0) {
+        for (uint32_t len = M; len > 1;) {
+            const uint32_t half = len >> 1;
+#pragma unroll
+            for (int k = 0; k < kRangeSearches; ++k) pos[k] = skeys[pos[k] + half] < v[k] ? pos[k] + half : pos[k];
+            len -= half;
+        }
+#pragma unroll
+        for (int k = 0; k < kRangeSearches; ++k) pos[k] += skeys[pos[k]] < v[k] ? 1u : 0u;
+    }
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) s_start[k * GS_BLOCK + tid] = pos[k];
+    if (tid == 0) s_start[GS_TILE_ITEMS] = pos[GS_ITEMS];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        const uint32_t i = k * GS_BLOCK + tid, t = b0 + i;
+        if (t < T) {
+            const uint32_t s = s_start[i], e = s_start[i + 1], n = e - s;
+            ranges[2 * t] = n ? s : 0u;
+            ranges[2 * t + 1] = n ? e : 0u;
+            const uint32_t key = tile_order_key(n);
+            tkeys[t] = key;
+            atomicAdd(&h[key], 1u);
+        }
+    }
+    __syncthreads();
+    hist[(size_t)tid * nblocks + blockIdx.x] = h[tid];
 }
 
 // Bitonic network over s[0..np) (np a power of two, entries past the data
@@ -377,31 +439,23 @@ __device__ void bitonic_global(unsigned long long* s, uint32_t n) {
     }
 }
 
-// One workgroup per tile: find the tile's segment of the tile-sorted pairs,
-// order it by (depth bits, emission position), and write the tile's range,
-// the primitive ids, the sorted -> emission map and the optional 64-bit keys.
-// pair_emit holds the segment's emission positions on entry (any order).
-__global__ void __launch_bounds__(GS_BLOCK) k_tile_depth_sort(const uint32_t* __restrict__ skeys,
-                                                              const uint32_t* __restrict__ sort_count,
+// One workgroup per tile, tiles taken in dispatch order (longest first):
+// order the tile's segment of the tile-sorted pairs by (depth bits, emission
+// position) and write the primitive ids, the sorted -> emission map and the
+// optional 64-bit keys.  pair_emit holds the segment's emission positions on
+// entry (any order).
+__global__ void __launch_bounds__(GS_BLOCK) k_tile_depth_sort(const uint32_t* __restrict__ tile_order,
+                                                              const uint32_t* __restrict__ ranges,
                                                               const uint32_t* __restrict__ emit_id,
                                                               const float* __restrict__ depth,
                                                               uint32_t* __restrict__ pair_emit,
                                                               uint32_t* __restrict__ vals,
-                                                              uint32_t* __restrict__ ranges,
                                                               uint64_t* __restrict__ keys64,
                                                               unsigned long long* __restrict__ scratch) {
     __shared__ unsigned long long s_key[kSortCap];
-    __shared__ uint32_t s_range[2];
-    const uint32_t t = blockIdx.x;
-    const uint32_t M = *sort_count;
-    if (threadIdx.x < 2) s_range[threadIdx.x] = lower_bound_u32(skeys, M, t + threadIdx.x);
-    __syncthreads();
-    const uint32_t start = s_range[0], end = s_range[1];
+    const uint32_t t = tile_order[blockIdx.x];
+    const uint32_t start = ranges[2 * t], end = ranges[2 * t + 1];
     const uint32_t n = end - start;
-    if (threadIdx.x == 0) {
-        ranges[2 * t] = n ? start : 0u;
-        ranges[2 * t + 1] = n ? end : 0u;
-    }
     if (n == 0) return;
     unsigned long long* key = s_key;
     if (n <= (uint32_t)kSortCap) {
@@ -440,19 +494,30 @@ struct BinsortLayout {
     size_t pk[3], pv[3];      // pair sort keys: in, tmp, out; pv[0] = primitive of each emitted pair,
                               // pv[1..2] = value ping-pong (values out = caller's pair_emit)
     size_t scratch;           // 64-bit keys of tiles longer than the LDS sort
+    size_t tkey[2], order;    // tile dispatch keys (in, sorted) and the order when the caller keeps none
     size_t hist, totals, bsum, offs, counters;
     size_t bytes;
     uint32_t nblocks_hist;
 };
 
-BinsortLayout binsort_layout(int32_t n, uint32_t capacity) {
+uint32_t tile_count(int32_t width, int32_t height) {
+    const int64_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
+    return (uint32_t)(TX * TY);
+}
+
+BinsortLayout binsort_layout(int32_t n, uint32_t capacity, int32_t width, int32_t height) {
     BinsortLayout L;
     size_t o = 0;
     const size_t nn = (size_t)(n > 0 ? n : 1), cc = (size_t)(capacity > 0 ? capacity : 1);
+    const size_t tt = (size_t)(width > 0 && height > 0 ? tile_count(width, height) : 1u);
     for (int i = 0; i < 3; ++i) { L.pk[i] = o; o += align256(4 * cc); }
     for (int i = 0; i < 3; ++i) { L.pv[i] = o; o += align256(4 * cc); }
     L.scratch = o; o += align256(8 * cc);
-    L.nblocks_hist = div_up(nn > cc ? nn : cc, GS_TILE_ITEMS);
+    for (int i = 0; i < 2; ++i) { L.tkey[i] = o; o += align256(4 * tt); }
+    L.order = o; o += align256(4 * tt);
+    size_t most = nn > cc ? nn : cc;
+    most = most > tt ? most : tt;
+    L.nblocks_hist = div_up(most, GS_TILE_ITEMS);
     L.hist = o; o += align256(4 * ((size_t)1 << kTileBits) * L.nblocks_hist);
     L.totals = o; o += align256(4 * ((size_t)1 << kTileBits));
     L.bsum = o; o += align256(4 * ((size_t)div_up(nn, GS_TILE_ITEMS) + 1));
@@ -499,39 +564,59 @@ hipError_t radix_sort(uint32_t* kin, const uint32_t* vin, uint32_t* ktmp, uint32
 
 }  // namespace
 
-size_t binsort_ws_bytes(int32_t n, uint32_t capacity, int32_t, int32_t) { return binsort_layout(n, capacity).bytes; }
+size_t binsort_ws_bytes(int32_t n, uint32_t capacity, int32_t width, int32_t height) {
+    return binsort_layout(n, capacity, width, height).bytes;
+}
 
 hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                           int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                          uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys, uint32_t* num_pairs,
-                          gs_device_status* status, void* ws, hipStream_t st) {
-    const BinsortLayout L = binsort_layout(n, capacity);
-    const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
-    const uint32_t T = (uint32_t)TX * (uint32_t)TY;
+                          uint32_t* tile_order, uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys,
+                          uint32_t* num_pairs, gs_device_status* status, void* ws, hipStream_t st) {
+    const BinsortLayout L = binsort_layout(n, capacity, width, height);
+    const int32_t TX = (width + GS_TILE - 1) / GS_TILE;
+    const uint32_t T = tile_count(width, height);
     uint32_t* hist = at<uint32_t>(ws, L.hist);
     uint32_t* totals = at<uint32_t>(ws, L.totals);
     uint32_t* bsum = at<uint32_t>(ws, L.bsum);
-    uint32_t* ctr = at<uint32_t>(ws, L.counters);   // [0] M, [1] sort count
+    uint32_t* ctr = at<uint32_t>(ws, L.counters);   // [0] M, [1] sort count, [2] T
+    uint32_t* order = tile_order ? tile_order : at<uint32_t>(ws, L.order);
+    // ranges, dispatch keys and the dispatch order (tiles by pair count
+    // descending, ties by tile id: one stable radix pass over 8-bit keys)
+    auto tile_pass = [&](const uint32_t* skeys, const uint32_t* sort_count) {
+        const uint32_t nbT = div_up(T, GS_TILE_ITEMS);
+        hipLaunchKernelGGL(k_tile_ranges, dim3(nbT), dim3(GS_BLOCK), 0, st, skeys, sort_count, T, ranges,
+                           at<uint32_t>(ws, L.tkey[0]), hist, nbT, ctr + 2);
+        hipLaunchKernelGGL(k_radix_scan, dim3(256), dim3(GS_BLOCK), 0, st, hist, nbT, totals);
+        hipLaunchKernelGGL(k_radix_scatter<8>, dim3(nbT), dim3(GS_BLOCK), 0, st, at<uint32_t>(ws, L.tkey[0]),
+                           nullptr, at<uint32_t>(ws, L.tkey[1]), order, ctr + 2, 0, 255u, 8, hist, totals, nbT);
+        return hipGetLastError();
+    };
+    // no pairs: empty ranges, and the order (then the tile ids) when the caller keeps it
+    auto no_pairs = [&]() {
+        if (T == 0) return hipGetLastError();
+        if (tile_order) return tile_pass(nullptr, nullptr);
+        return launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
+    };
     if (n == 0) {
-        hipError_t e = launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
+        hipError_t e = launch_fill_u32(num_pairs, 0u, 1, st);
         if (e != hipSuccess) return e;
-        return launch_fill_u32(num_pairs, 0u, 1, st);
+        return no_pairs();
     }
     // 1. emission offsets in visible-set order
-    const uint32_t* order = vis_idx;
+    const uint32_t* vorder = vis_idx;
     const uint32_t nb = div_up(n, GS_TILE_ITEMS);
-    hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles, bsum);
+    hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum);
     hipError_t e = launch_scan_blocks(bsum, nb, ctr + 0, nullptr, st);
     if (e != hipSuccess) return e;
     uint32_t* offs_r = at<uint32_t>(ws, L.offs);
-    hipLaunchKernelGGL(k_offsets, dim3(nb), dim3(GS_BLOCK), 0, st, order, vis_count, proj.tiles, bsum, ctr + 0,
+    hipLaunchKernelGGL(k_offsets, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum, ctr + 0,
                        capacity, pair_offset, offs_r, ctr + 1, num_pairs, status);
     int tbits = 1;
     while (tbits < 32 && (1u << tbits) < T) ++tbits;
     const uint32_t mask0 = (1u << (tbits < kTileBits ? tbits : kTileBits)) - 1u;
-    if (capacity == 0 || T == 0) return launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
+    if (capacity == 0 || T == 0) return no_pairs();
     // 2. emission: one (tile, primitive) pair per touched tile
-    hipLaunchKernelGGL(k_emit_pairs, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, order,
+    hipLaunchKernelGGL(k_emit_pairs, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, vorder,
                        vis_count, offs_r, reinterpret_cast<const ushort4*>(proj.rect), ctr + 1, TX,
                        at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), mask0, hist,
                        div_up(capacity, GS_TILE_ITEMS));
@@ -540,10 +625,12 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
                               at<uint32_t>(ws, L.pv[2]), at<uint32_t>(ws, L.pk[2]), pair_emit, ctr + 1, capacity,
                               tbits, hist, totals, st);
     if (e != hipSuccess) return e;
-    // 4. per tile: depth order, ranges, primitive ids (+ optional 64-bit keys)
-    hipLaunchKernelGGL(k_tile_depth_sort, dim3(T), dim3(GS_BLOCK), 0, st, at<uint32_t>(ws, L.pk[2]), ctr + 1,
-                       at<uint32_t>(ws, L.pv[0]), proj.depth, pair_emit, vals, ranges, keys,
-                       at<unsigned long long>(ws, L.scratch));
+    // 4. tile ranges and the dispatch order
+    e = tile_pass(at<uint32_t>(ws, L.pk[2]), ctr + 1);
+    if (e != hipSuccess) return e;
+    // 5. per tile, longest first: depth order, primitive ids (+ optional 64-bit keys)
+    hipLaunchKernelGGL(k_tile_depth_sort, dim3(T), dim3(GS_BLOCK), 0, st, order, ranges, at<uint32_t>(ws, L.pv[0]),
+                       proj.depth, pair_emit, vals, keys, at<unsigned long long>(ws, L.scratch));
     return hipGetLastError();
 }
 

@@ -56,24 +56,26 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, size_t n, hipStream_t st
 size_t binsort_ws_bytes(int32_t n, uint32_t capacity, int32_t width, int32_t height);
 hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                           int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
-                          uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys, uint32_t* num_pairs,
-                          gs_device_status* status, void* ws, hipStream_t st);
+                          uint32_t* tile_order, uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys,
+                          uint32_t* num_pairs, gs_device_status* status, void* ws, hipStream_t st);
 
 // raster.hip
-hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
-                             int32_t height, const float bg[3], float* img, float* final_T, uint32_t* n_contrib,
-                             uint8_t* active, uint64_t* pair_stats, hipStream_t st);
+hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges,
+                             const uint32_t* tile_order, int32_t width, int32_t height, const float bg[3],
+                             float* img, float* final_T, uint32_t* n_contrib, uint8_t* active, uint64_t* pair_stats,
+                             hipStream_t st);
 size_t raster_fwd_l1_ws_bytes(int32_t width, int32_t height);
-hipError_t launch_raster_fwd_l1(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
-                                int32_t height, const float bg[3], const float* target, float* img, float* final_T,
-                                uint32_t* n_contrib, uint8_t* active, float* loss, float* dL, void* ws,
-                                hipStream_t st);
+hipError_t launch_raster_fwd_l1(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges,
+                                const uint32_t* tile_order, int32_t width, int32_t height, const float bg[3],
+                                const float* target, float* img, float* final_T, uint32_t* n_contrib, uint8_t* active,
+                                float* loss, float* dL, void* ws, hipStream_t st);
 size_t loss_ws_bytes(int32_t width, int32_t height);
 hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, int32_t height, float* loss,
                           float* dL, void* ws, hipStream_t st);
 size_t raster_bwd_ws_bytes(int32_t n, uint32_t capacity);
 hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
-                             const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_emit,
+                             const uint32_t* ranges, const uint32_t* tile_order, const uint32_t* pair_offset,
+                             const uint32_t* pair_emit,
                              const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity,
                              const float* final_T, const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
                              float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, int stages,

@@ -189,13 +189,22 @@ __device__ __forceinline__ float l1_elem(float a, float t, float inv, float& dl)
     return fabsf(d);
 }
 
+// The tile a workgroup renders: the grid covers the tiles once, in the
+// caller's dispatch order (longest first from gs_bin_sort), else row-major.
+// Pixels, losses and pair records are per tile, so the order changes no
+// result, only how the longest tiles overlap the rest.
+__device__ __forceinline__ uint32_t dispatch_tile(const uint32_t* __restrict__ tile_order) {
+    return tile_order ? tile_order[blockIdx.x] : blockIdx.x;
+}
+
 // LOSS: the L1 loss of the view is taken in the same pass (the image loss of
 // the view, Section 2.1): each pixel compares its three fp32 channels with
 // the target exactly as k_loss_l1 does, writes dL/dimg, and each tile leaves
 // its sum of |img - target| in loss_partial[tile] for k_loss_final.
 template <bool STATS, bool LOSS>
 __global__ void __launch_bounds__(GS_BLOCK, 7) k_raster_fwd(
-    const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
+    const uint32_t* __restrict__ tile_order, const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals,
+    const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, float* __restrict__ img, float* __restrict__ final_T, uint32_t* __restrict__ n_contrib,
     uint8_t* __restrict__ active, unsigned long long* __restrict__ pair_stats, const float* __restrict__ target,
@@ -205,12 +214,13 @@ __global__ void __launch_bounds__(GS_BLOCK, 7) k_raster_fwd(
     __shared__ uint32_t s_hit[GS_BLOCK];
     __shared__ uint8_t s_list[4][4][GS_BLOCK];
     __shared__ uint32_t s_stat[4][4];
-    const int tile = blockIdx.x;
+    const uint32_t tile = dispatch_tile(tile_order);
+    if (tile >= gridDim.x) return;
     const int tid = threadIdx.x;
     const int w = tid / GS_WAVE;
     const int lane = lane_id();
     const int row = lane >> 4;
-    const int tx = tile % TX, ty = tile / TX;
+    const int tx = (int)tile % TX, ty = (int)tile / TX;
     const int px = tx * GS_TILE + (tid % GS_TILE);
     const int py = ty * GS_TILE + (tid / GS_TILE);
     const bool inside = px < W && py < H;
@@ -447,7 +457,8 @@ constexpr int kBwdBatch = GS_WAVE;
 // (m_x, m_y, m_xx, m_xy, m_yy, m, colour); k_project_bwd expands it with the
 // conic once per primitive.
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
-    const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals, const float2* __restrict__ mean2d,
+    const uint32_t* __restrict__ tile_order, const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals,
+    const float2* __restrict__ mean2d,
     const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, const float* __restrict__ final_T, const uint32_t* __restrict__ n_contrib,
     const float* __restrict__ dL_dimg, const uint32_t* __restrict__ pair_emit, float* __restrict__ slots) {
@@ -458,12 +469,13 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     __shared__ uint8_t s_list[4][4][kBwdBatch];
     __shared__ uint32_t s_max;
     static_assert(kG * kBwdBatch <= 4 * kRowSums * kBwdBatch, "combined sums fit a wave's row records");
-    const int tile = blockIdx.x;
+    const uint32_t tile = dispatch_tile(tile_order);
+    if (tile >= gridDim.x) return;
     const int tid = threadIdx.x;
     const int w = tid / GS_WAVE;
     const int lane = lane_id();
     const int row = lane >> 4;
-    const int tx = tile % TX, ty = tile / TX;
+    const int tx = (int)tile % TX, ty = (int)tile / TX;
     const int px = tx * GS_TILE + (tid % GS_TILE);
     const int py = ty * GS_TILE + (tid / GS_TILE);
     const bool inside = px < W && py < H;
@@ -1015,19 +1027,20 @@ __global__ void __launch_bounds__(GS_BLOCK) k_clear_union_rows(const uint32_t* _
 
 }  // namespace
 
-hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
-                             int32_t height, const float bg[3], float* img, float* final_T, uint32_t* n_contrib,
-                             uint8_t* active, uint64_t* pair_stats, hipStream_t st) {
+hipError_t launch_raster_fwd(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges,
+                             const uint32_t* tile_order, int32_t width, int32_t height, const float bg[3],
+                             float* img, float* final_T, uint32_t* n_contrib, uint8_t* active, uint64_t* pair_stats,
+                             hipStream_t st) {
     const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
     if (TX * TY == 0) return hipSuccess;
     if (pair_stats)
-        hipLaunchKernelGGL((k_raster_fwd<true, false>), dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
+        hipLaunchKernelGGL((k_raster_fwd<true, false>), dim3(TX * TY), dim3(GS_BLOCK), 0, st, tile_order, ranges, vals,
                            reinterpret_cast<const float2*>(proj.mean2d),
                            reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, width, height, TX, bg[0],
                            bg[1], bg[2], img, final_T, n_contrib, active,
                            reinterpret_cast<unsigned long long*>(pair_stats), nullptr, 0.0f, nullptr, nullptr);
     else
-        hipLaunchKernelGGL((k_raster_fwd<false, false>), dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
+        hipLaunchKernelGGL((k_raster_fwd<false, false>), dim3(TX * TY), dim3(GS_BLOCK), 0, st, tile_order, ranges, vals,
                            reinterpret_cast<const float2*>(proj.mean2d),
                            reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, width, height, TX, bg[0],
                            bg[1], bg[2], img, final_T, n_contrib, active, nullptr, nullptr, 0.0f, nullptr, nullptr);
@@ -1040,15 +1053,15 @@ size_t raster_fwd_l1_ws_bytes(int32_t width, int32_t height) {
     return align256(sizeof(float) * (T + 1));
 }
 
-hipError_t launch_raster_fwd_l1(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges, int32_t width,
-                                int32_t height, const float bg[3], const float* target, float* img, float* final_T,
-                                uint32_t* n_contrib, uint8_t* active, float* loss, float* dL, void* ws,
-                                hipStream_t st) {
+hipError_t launch_raster_fwd_l1(const gs_proj& proj, const uint32_t* vals, const uint32_t* ranges,
+                                const uint32_t* tile_order, int32_t width, int32_t height, const float bg[3],
+                                const float* target, float* img, float* final_T, uint32_t* n_contrib, uint8_t* active,
+                                float* loss, float* dL, void* ws, hipStream_t st) {
     const int32_t TX = (width + GS_TILE - 1) / GS_TILE, TY = (height + GS_TILE - 1) / GS_TILE;
     const uint64_t total = 3ull * (uint64_t)width * (uint64_t)height;
     float* partial = static_cast<float*>(ws);
     if (TX * TY > 0)
-        hipLaunchKernelGGL((k_raster_fwd<false, true>), dim3(TX * TY), dim3(GS_BLOCK), 0, st, ranges, vals,
+        hipLaunchKernelGGL((k_raster_fwd<false, true>), dim3(TX * TY), dim3(GS_BLOCK), 0, st, tile_order, ranges, vals,
                            reinterpret_cast<const float2*>(proj.mean2d),
                            reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, width, height, TX, bg[0],
                            bg[1], bg[2], img, final_T, n_contrib, active, nullptr, target,
@@ -1090,15 +1103,15 @@ size_t raster_bwd_ws_bytes(int32_t, uint32_t capacity) {
 }
 
 hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
-                             const uint32_t* ranges, const uint32_t* pair_offset, const uint32_t* pair_emit,
-                             const uint32_t* vis_idx, const uint32_t* vis_count, uint32_t capacity,
-                             const float* final_T, const uint32_t* n_contrib, const float* dL_dimg, const float bg[3],
-                             float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm, void* ws, int stages,
-                             hipStream_t st, const uint32_t* union_idx, const uint32_t* union_count, int first) {
+                             const uint32_t* ranges, const uint32_t* tile_order, const uint32_t* pair_offset,
+                             const uint32_t* pair_emit, const uint32_t* vis_idx, const uint32_t* vis_count,
+                             uint32_t capacity, const float* final_T, const uint32_t* n_contrib, const float* dL_dimg,
+                             const float bg[3], float* grad_rows, int32_t grad_ld, float* grad2d, float* grad_norm,
+                             void* ws, int stages, hipStream_t st, const uint32_t* union_idx, const uint32_t* union_count, int first) {
     float* slots = static_cast<float*>(ws);
     const int32_t T = cam.tiles_x * cam.tiles_y;
     if ((stages & 1) && T > 0)
-        hipLaunchKernelGGL(k_raster_bwd, dim3(T), dim3(GS_BLOCK), 0, st, ranges, vals,
+        hipLaunchKernelGGL(k_raster_bwd, dim3(T), dim3(GS_BLOCK), 0, st, tile_order, ranges, vals,
                            reinterpret_cast<const float2*>(proj.mean2d),
                            reinterpret_cast<const float4*>(proj.conic_opacity), proj.rgb, cam.width, cam.height,
                            cam.tiles_x, bg[0], bg[1], bg[2], final_T, n_contrib, dL_dimg, pair_emit, slots);

@@ -81,7 +81,7 @@ def scope_words(n) -> int:
 _lib.gs_abi_version.restype = i32
 # the structs above mirror this version of the header; a library built from
 # another one would read them with a different layout
-ABI_VERSION = 3
+ABI_VERSION = 4
 if _lib.gs_abi_version() != ABI_VERSION:
     raise ImportError("libgsmi ABI version %d, binding expects %d: rebuild the library"
                       % (_lib.gs_abi_version(), ABI_VERSION))
@@ -94,14 +94,14 @@ _lib.gs_delta_msg_bytes.restype = sz
 _lib.gs_delta_msg_bytes.argtypes = [u32, i32, i32]
 _lib.gs_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P]
 _lib.gs_visible_set.argtypes = [i32, P, i32, P, P, P, sz, P]
-_lib.gs_bin_sort.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, u32, P, P, P, P, P, P, P, P, sz, P]
-_lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, P, P, P, P, P, P]
+_lib.gs_bin_sort.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, u32, P, P, P, P, P, P, P, P, P, sz, P]
+_lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, P, i32, i32, P, P, P, P, P, P, P]
 _lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
-_lib.gs_raster_fwd_l1.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, P, P, P, P, P, P, P, P, P, sz, P]
+_lib.gs_raster_fwd_l1.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, P, i32, i32, P, P, P, P, P, P, P, P, P, sz, P]
 _lib.gs_raster_bwd.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P, P, P,
-                               P, P, P, u32, P, P, P, P, P, i32, P, P, P, sz, P]
-_lib.gs_raster_bwd_pixels.argtypes = [ctypes.POINTER(gs_proj), ctypes.POINTER(gs_camera), P, P, P, u32, P, P, P, P,
-                                      P, sz, P]
+                               P, P, P, P, u32, P, P, P, P, P, i32, P, P, P, sz, P]
+_lib.gs_raster_bwd_pixels.argtypes = [ctypes.POINTER(gs_proj), ctypes.POINTER(gs_camera), P, P, P, P, u32, P, P, P,
+                                      P, P, sz, P]
 _lib.gs_raster_bwd_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj),
                                        P, P, P, u32, P, i32, P, P, P, sz, P]
 _lib.gs_raster_bwd_project_accum.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera),
@@ -231,11 +231,11 @@ def gs_visible_set(kind, src, n, out_idx, out_count, ws, stream=None):
 
 
 def gs_bin_sort(proj: gs_proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges, pair_offset,
-                pair_emit, keys, num_pairs, status, ws, stream=None):
+                pair_emit, keys, num_pairs, status, ws, stream=None, tile_order=None):
     return _check("gs_bin_sort", _lib.gs_bin_sort(ctypes.byref(proj), int(n), ptr(vis_idx), ptr(vis_count),
                                                   int(width), int(height), int(capacity), ptr(vals), ptr(ranges),
-                                                  ptr(pair_offset), ptr(pair_emit), ptr(keys), ptr(num_pairs),
-                                                  ptr(status), ptr(ws),
+                                                  ptr(tile_order), ptr(pair_offset), ptr(pair_emit), ptr(keys),
+                                                  ptr(num_pairs), ptr(status), ptr(ws),
                                                   ws.numel() * ws.element_size(),
                                                   stream if stream is not None else current_stream()))
 
@@ -246,20 +246,22 @@ def _bg(bg):
 
 
 def gs_raster_fwd(proj: gs_proj, n, vals, ranges, width, height, bg, img, final_T, n_contrib, active=None,
-                  pair_stats=None, stream=None):
+                  pair_stats=None, stream=None, tile_order=None):
     b = _bg(bg)
-    return _check("gs_raster_fwd", _lib.gs_raster_fwd(ctypes.byref(proj), int(n), ptr(vals), ptr(ranges), int(width),
-                                                      int(height), ctypes.cast(b, P), ptr(img), ptr(final_T),
-                                                      ptr(n_contrib), ptr(active), ptr(pair_stats),
+    return _check("gs_raster_fwd", _lib.gs_raster_fwd(ctypes.byref(proj), int(n), ptr(vals), ptr(ranges),
+                                                      ptr(tile_order), int(width), int(height), ctypes.cast(b, P),
+                                                      ptr(img), ptr(final_T), ptr(n_contrib), ptr(active),
+                                                      ptr(pair_stats),
                                                       stream if stream is not None else current_stream()))
 
 
 def gs_raster_fwd_l1(proj: gs_proj, n, vals, ranges, width, height, bg, target, img, final_T, n_contrib, active, loss,
-                     dL_dimg, ws, stream=None):
+                     dL_dimg, ws, stream=None, tile_order=None):
     b = _bg(bg)
     return _check("gs_raster_fwd_l1", _lib.gs_raster_fwd_l1(
-        ctypes.byref(proj), int(n), ptr(vals), ptr(ranges), int(width), int(height), ctypes.cast(b, P), ptr(target),
-        ptr(img), ptr(final_T), ptr(n_contrib), ptr(active), ptr(loss), ptr(dL_dimg), ptr(ws),
+        ctypes.byref(proj), int(n), ptr(vals), ptr(ranges), ptr(tile_order), int(width), int(height),
+        ctypes.cast(b, P), ptr(target), ptr(img), ptr(final_T), ptr(n_contrib), ptr(active), ptr(loss),
+        ptr(dL_dimg), ptr(ws),
         ws.numel() * ws.element_size(), stream if stream is not None else current_stream()))
 
 
@@ -271,11 +273,12 @@ def gs_loss_l1(img, target, width, height, loss, dL_dimg, ws, stream=None):
 
 def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, pair_offset, pair_emit, vis_idx,
                   vis_count, capacity, final_T, n_contrib, dL_dimg, bg, grad_rows, grad_ld, grad2d, grad_norm, ws,
-                  stream=None):
+                  stream=None, tile_order=None):
     b = _bg(bg)
     return _check("gs_raster_bwd", _lib.gs_raster_bwd(ctypes.byref(scene), ctypes.byref(cam), ctypes.byref(proj),
-                                                      ptr(vals), ptr(ranges), ptr(pair_offset), ptr(pair_emit),
-                                                      ptr(vis_idx), ptr(vis_count), int(capacity), ptr(final_T),
+                                                      ptr(vals), ptr(ranges), ptr(tile_order), ptr(pair_offset),
+                                                      ptr(pair_emit), ptr(vis_idx), ptr(vis_count), int(capacity),
+                                                      ptr(final_T),
                                                       ptr(n_contrib), ptr(dL_dimg), ctypes.cast(b, P),
                                                       ptr(grad_rows), int(grad_ld), ptr(grad2d), ptr(grad_norm),
                                                       ptr(ws), ws.numel() * ws.element_size(),
@@ -283,12 +286,11 @@ def gs_raster_bwd(scene: gs_scene, cam: gs_camera, proj: gs_proj, vals, ranges, 
 
 
 def gs_raster_bwd_pixels(proj: gs_proj, cam: gs_camera, vals, ranges, pair_emit, capacity, final_T, n_contrib, dL_dimg,
-                         bg, ws, stream=None):
+                         bg, ws, stream=None, tile_order=None):
     b = _bg(bg)
     return _check("gs_raster_bwd_pixels", _lib.gs_raster_bwd_pixels(
-        ctypes.byref(proj), ctypes.byref(cam), ptr(vals), ptr(ranges), ptr(pair_emit), int(capacity), ptr(final_T),
-        ptr(n_contrib),
-        ptr(dL_dimg), ctypes.cast(b, P), ptr(ws), ws.numel() * ws.element_size(),
+        ctypes.byref(proj), ctypes.byref(cam), ptr(vals), ptr(ranges), ptr(tile_order), ptr(pair_emit), int(capacity),
+        ptr(final_T), ptr(n_contrib), ptr(dL_dimg), ctypes.cast(b, P), ptr(ws), ws.numel() * ws.element_size(),
         stream if stream is not None else current_stream()))
 
 

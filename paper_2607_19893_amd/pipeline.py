@@ -104,6 +104,7 @@ class ViewTrainer:
                                   device=self.dev)
         self.capacity = 0
         self.width = self.height = 0
+        self.longest_first = True   # raster workgroups take the tiles in gs_bin_sort's dispatch order
         self._set_image(max(1, max_width), max(1, max_height))
         self._set_capacity(max(1, capacity))
         self.scene_s = gsmi.make_scene(n, self.deg, *self.params)
@@ -134,6 +135,7 @@ class ViewTrainer:
         self.dL = torch.zeros(3, h, w, device=self.dev)
         self.target = torch.zeros(3, h, w, device=self.dev)
         self.ranges = _u32(2 * T, self.dev)
+        self.tile_order = _u32(T, self.dev)
         self.ws_loss = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_LOSS, 0, 0, w, h), dtype=torch.uint8,
                                    device=self.dev)
         self.ws_fwd_l1 = torch.zeros(gsmi.gs_workspace_bytes(gsmi.GS_WS_RASTER_FWD_L1, 0, 0, w, h),
@@ -173,7 +175,10 @@ class ViewTrainer:
         w, h = self.cam.width, self.cam.height
         gsmi.gs_bin_sort(self.proj_s, self.n, self.vis_idx, self.counts[0:1], w, h, self.capacity, self.vals,
                          self.ranges, self.pair_offset, self.pair_emit, self.keys, self.counts[1:2], self.status,
-                         self.ws_sort)
+                         self.ws_sort, tile_order=self.tile_order)
+
+    def _order(self):
+        return self.tile_order if self.longest_first else None
 
     def _img_views(self):
         w, h = self.cam.width, self.cam.height
@@ -190,7 +195,8 @@ class ViewTrainer:
         if active:
             self.active.zero_()
         gsmi.gs_raster_fwd(self.proj_s, self.n, self.vals, self.ranges, self.cam.width, self.cam.height, bg, img, fT,
-                           nc, self.active if active else None, self.pair_stats if stats else None)
+                           nc, self.active if active else None, self.pair_stats if stats else None,
+                           tile_order=self._order())
 
     def raster_fwd_l1(self, target=None, bg=(0.0, 0.0, 0.0), active=False):
         """Forward raster and the L1 loss in one pass (target: device tensor of 3*H*W floats, or None for the
@@ -200,7 +206,7 @@ class ViewTrainer:
             self.active.zero_()
         gsmi.gs_raster_fwd_l1(self.proj_s, self.n, self.vals, self.ranges, self.cam.width, self.cam.height, bg,
                               tgt if target is None else target, img, fT, nc, self.active if active else None,
-                              self.loss, dL, self.ws_fwd_l1)
+                              self.loss, dL, self.ws_fwd_l1, tile_order=self._order())
 
     def set_target(self, target_np):
         """Copy a [3,H,W] target into the target buffer (planar, first 3*H*W floats)."""
@@ -224,12 +230,13 @@ class ViewTrainer:
         _, fT, nc, dL, _ = self._img_views()
         gsmi.gs_raster_bwd(self.scene_s, self.cam_c, self.proj_s, self.vals, self.ranges, self.pair_offset,
                            self.pair_emit, self.vis_idx, self.counts[0:1], self.capacity, fT, nc, dL, bg,
-                           self.grad_rows, self.ld, self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
+                           self.grad_rows, self.ld, self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd,
+                           tile_order=self._order())
 
     def raster_bwd_pixels(self, bg=(0.0, 0.0, 0.0)):
         _, fT, nc, dL, _ = self._img_views()
         gsmi.gs_raster_bwd_pixels(self.proj_s, self.cam_c, self.vals, self.ranges, self.pair_emit, self.capacity, fT,
-                                  nc, dL, bg, self.ws_bwd)
+                                  nc, dL, bg, self.ws_bwd, tile_order=self._order())
 
     def raster_bwd_project(self, grad2d=False):
         gsmi.gs_raster_bwd_project(self.scene_s, self.cam_c, self.proj_s, self.pair_offset,

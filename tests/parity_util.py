@@ -74,3 +74,20 @@ def assert_grads(gpu, ref, rows_ok, name, rtol=GRAD_RTOL, floor=None, mag=None):
         name, int(bad.sum()), rtol, float(np.max(fl)), err[bad].max(), r[bad][np.argmax(err[bad])])
     assert nrm <= rtol, "%s: normwise error %.3g" % (name, nrm)
     return stats
+
+
+def order_code(n):
+    """The dispatch code of a tile's pair count that gs_bin_sort documents:
+    the count itself below 16, then 16 steps per octave, 255 from 2^19 on."""
+    n = int(n)
+    if n < 16:
+        return n
+    e = n.bit_length() - 1
+    return 255 if e > 18 else 16 * (e - 3) + ((n >> (e - 4)) & 15)
+
+
+def expected_tile_order(ranges):
+    """Tile ids by dispatch code descending, equal codes by ascending id."""
+    ranges = np.asarray(ranges, np.int64).reshape(-1, 2)
+    codes = np.array([order_code(e - s) for s, e in ranges], np.int64)
+    return np.lexsort((np.arange(codes.size), -codes)).astype(np.uint32)

@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol(gs):
     for nm in names:
         assert hasattr(gs.raw(), nm), nm
         assert nm in gs.EXPORTS, nm
-    assert gs.gs_abi_version() == gs.ABI_VERSION == 3
+    assert gs.gs_abi_version() == gs.ABI_VERSION == 4
 
 
 def test_status_strings(gs):
@@ -94,9 +94,10 @@ def test_null_and_range_arguments_rejected(gs):
     assert "ld 1 below cols 3" in gs.gs_last_error()
     g[0].ld = 0
     # fused forward + loss: workspace sized per tile
-    assert L.gs_raster_fwd_l1(ctypes.byref(pr), 10, 16, 16, 256, 256, 16, 16, 16, 16, 16, None, 16, 16, 16, 0,
+    assert L.gs_raster_fwd_l1(ctypes.byref(pr), 10, 16, 16, None, 256, 256, 16, 16, 16, 16, 16, None, 16, 16, 16, 0,
                               None) == gs.GS_ERR_WORKSPACE
-    assert L.gs_raster_fwd_l1(ctypes.byref(pr), 10, 16, 16, 256, 256, 16, None, 16, 16, 16, None, 16, 16, 16, 1 << 20,
+    assert L.gs_raster_fwd_l1(ctypes.byref(pr), 10, 16, 16, None, 256, 256, 16, None, 16, 16, 16, None, 16, 16, 16,
+                              1 << 20,
                               None) == gs.GS_ERR_INVALID_ARG
     assert gs.gs_workspace_bytes(gs.GS_WS_RASTER_FWD_L1, 0, 0, 1920, 1080) >= 4 * 120 * 68
     # versioned commit of a ring slot

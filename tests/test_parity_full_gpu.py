@@ -14,7 +14,7 @@ import time
 import numpy as np
 import pytest
 
-from parity_util import GRAD_RTOL, assert_grads, assert_pixels, grad_floor
+from parity_util import GRAD_RTOL, assert_grads, assert_pixels, expected_tile_order, grad_floor
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -63,6 +63,7 @@ def test_full_view(name, orc):
     np.testing.assert_array_equal(to_u32(tr.vals)[:M], ref.vals)
     T = cam.num_tiles
     np.testing.assert_array_equal(to_u32(tr.ranges)[:2 * T].reshape(T, 2), ref.ranges)
+    np.testing.assert_array_equal(to_u32(tr.tile_order)[:T], expected_tile_order(ref.ranges))
     _say(name, "V=%d M=%d bit-exact" % (V, M))
 
     # image

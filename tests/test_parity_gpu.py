@@ -10,7 +10,7 @@ import sys
 import numpy as np
 import pytest
 
-from parity_util import assert_grads, assert_pixels
+from parity_util import assert_grads, assert_pixels, expected_tile_order
 
 pytestmark = pytest.mark.gpu
 
@@ -106,6 +106,7 @@ def test_project_visible_sort(case, torch_gpu, orc):
         np.testing.assert_array_equal(tr.keys.cpu().numpy()[:M].view(np.uint64), keys_ref)
         T = cam.num_tiles
         np.testing.assert_array_equal(u32(tr.ranges)[:2 * T].reshape(T, 2), ranges_ref)
+        np.testing.assert_array_equal(u32(tr.tile_order)[:T], expected_tile_order(ranges_ref))
         # emission offsets: exclusive sums of tiles in visible-set (ascending id) order
         order = vis_ref
         offs = np.concatenate([[0], np.cumsum(ref.tiles[order].astype(np.int64))[:-1]])
@@ -472,6 +473,9 @@ def test_long_tile_lists(torch_gpu, orc):
     np.testing.assert_array_equal(tr.keys.cpu().numpy()[:M].view(np.uint64), keys_ref)
     T = cam.num_tiles
     np.testing.assert_array_equal(u32(tr.ranges)[:2 * T].reshape(T, 2), ranges_ref)
+    order = u32(tr.tile_order)[:T]
+    np.testing.assert_array_equal(order, expected_tile_order(ranges_ref))
+    assert lengths[order[0]] == lengths.max()
 
 
 def test_pair_overflow_flag(torch_gpu, orc):
@@ -485,6 +489,8 @@ def test_pair_overflow_flag(torch_gpu, orc):
     M = int(u32(tr.counts[1:2])[0])
     assert s[0] & 1 and s[1] == M and M > 1000
     assert np.all(u32(tr.ranges) == 0)
+    T = w.cameras[0].num_tiles
+    np.testing.assert_array_equal(u32(tr.tile_order)[:T], np.arange(T))
 
 
 def test_empty_and_degenerate(torch_gpu, orc):
@@ -500,6 +506,35 @@ def test_empty_and_degenerate(torch_gpu, orc):
     hw = w.cameras[0].width * w.cameras[0].height
     assert float(tr.img.view(-1)[:3 * hw].abs().max()) == 0.0
     assert float(tr.final_T.view(-1)[:hw].min()) == 1.0
+    T = w.cameras[0].num_tiles
+    np.testing.assert_array_equal(u32(tr.tile_order)[:T], np.arange(T))
+
+
+@pytest.mark.parametrize("case", ["room-60k-392x216", "ring-20k-328x184"])
+def test_dispatch_order_changes_no_result(case, torch_gpu, orc):
+    """The raster kernels in the longest-first tile order and in row-major
+    order give the same image, transmittance, contributor counts, active
+    flags, pair statistics, loss, dL/dimg and gradients, bit for bit."""
+    w = get_case(case)
+    runs = []
+    for longest_first in (True, False):
+        tr = trainer_for(w, torch_gpu)
+        tr.longest_first = longest_first
+        cam = w.cameras[1]
+        tr.set_target(w.target(1))
+        tr.pair_stats.zero_()
+        tr.project(cam); tr.visible(); tr.bin_sort()
+        tr.raster_fwd(active=True, stats=True)
+        out = [t.clone() for t in (tr.img, tr.final_T, tr.n_contrib, tr.active, tr.pair_stats)]
+        tr.raster_fwd_l1()
+        tr.raster_bwd(grad2d=True)
+        torch_gpu.cuda.synchronize()
+        out += [t.clone() for t in (tr.loss, tr.dL, tr.grad_rows, tr.grad2d, tr.grad_norm)]
+        order = u32(tr.tile_order)[:cam.num_tiles]
+        assert np.array_equal(np.sort(order), np.arange(cam.num_tiles))
+        runs.append(out)
+    for a, b in zip(*runs):
+        assert torch_gpu.equal(a, b)
 
 
 def test_backward_halves_match_combined(torch_gpu, orc):
