@@ -7,13 +7,20 @@
 //      pairs are contiguous ("emission order");
 //   2. the M pairs are sorted by tile id only (ceil(log2 T) bits: 1-2 LSD
 //      passes), carrying each pair's emission position;
-//   3. each tile's segment is sorted by (depth bits, emission position) in LDS
+//   3. the tile ranges come from the segment bounds of the sorted keys, and
+//      one stable 8-bit radix pass over a code of each tile's pair count gives
+//      the dispatch order: the longest tiles first;
+//   4. each tile's segment is sorted by (depth bits, emission position) in LDS
 //      by one workgroup (a bitonic network; segments longer than the LDS
-//      capacity are sorted in global memory by the same workgroup).  Emission
-//      positions grow with the primitive id inside a tile, so this is exactly
-//      the (tile, depth bits, id) order.
-// Step 3 replaces a 4-pass radix sort of the visible set by depth (12
+//      capacity are sorted in global memory by the same workgroup), tiles
+//      taken in the dispatch order.  Emission positions grow with the
+//      primitive id inside a tile, so this is exactly the (tile, depth bits,
+//      id) order.
+// Step 4 replaces a 4-pass radix sort of the visible set by depth (12
 // latency-bound launches) with one launch whose work is local to a tile.
+// The per-tile kernels that follow (this sort, the forward and backward
+// raster) end when their longest tile ends; taking the longest first lets
+// the short ones fill in beside it instead of after it.
 //
 // Each LSD pass is three launches: per-block digit histograms (digit-major
 // matrix), a per-digit scan across blocks, and a scatter whose in-block rank
@@ -190,11 +197,15 @@ __global__ void __launch_bounds__(GS_BLOCK) k_radix_scatter(
 }
 
 // per-block sums of tiles[] in visible-set order
+// The grid also zeroes the tile ranges (n_ranges words) for the segment
+// bounds written later.
 __global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restrict__ order,
                                                         const uint32_t* __restrict__ vis_count,
                                                         const uint32_t* __restrict__ tiles,
-                                                        uint32_t* __restrict__ bsum) {
+                                                        uint32_t* __restrict__ bsum, uint32_t* __restrict__ ranges,
+                                                        uint32_t n_ranges) {
     __shared__ uint32_t scratch[4];
+    for (uint32_t i = blockIdx.x * GS_BLOCK + threadIdx.x; i < n_ranges; i += gridDim.x * GS_BLOCK) ranges[i] = 0u;
     const uint32_t V = *vis_count;
     const uint32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x * GS_ITEMS;
     uint32_t s = 0;
@@ -333,56 +344,44 @@ __device__ __forceinline__ uint32_t tile_order_key(uint32_t n) {
     return 255u - code;
 }
 
-constexpr int kRangeSearches = GS_ITEMS + 1;
+// Segment bounds of the M tile-sorted pair keys: the pair that opens tile
+// t's segment writes ranges[2t], the pair that closes it ranges[2t+1]; tiles
+// without pairs keep the zeros written before.  Thread i of block b looks at
+// pairs b*2048 + k*256 + i and their neighbours.
+__global__ void __launch_bounds__(GS_BLOCK) k_tile_bounds(const uint32_t* __restrict__ skeys,
+                                                          const uint32_t* __restrict__ sort_count,
+                                                          uint32_t* __restrict__ ranges) {
+    const uint32_t M = *sort_count;
+    const uint32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x;
+    if (blockIdx.x * GS_TILE_ITEMS >= M) return;
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        const uint32_t i = base + k * GS_BLOCK;
+        if (i < M) {
+            const uint32_t t = skeys[i];
+            if (i == 0 || skeys[i - 1] != t) ranges[2 * t] = i;
+            if (i + 1 == M || skeys[i + 1] != t) ranges[2 * t + 1] = i + 1;
+        }
+    }
+}
 
-// Tile ranges from the M tile-sorted pair keys, and every tile's dispatch key.
-// Block b covers tiles [b*2048, b*2048+2048).  A thread finds the first pair
-// of its eight tiles and of the tile after the block (the same for every
-// thread) with a branch-free lower bound whose searches all advance one level
-// per round (the step lengths depend on M only).  The block's per-digit
-// counts of the dispatch keys go to the digit-major histogram matrix that the
-// radix scan reads.  sort_count may be null: no pairs.
-__global__ void __launch_bounds__(GS_BLOCK) k_tile_ranges(const uint32_t* __restrict__ skeys,
-                                                          const uint32_t* __restrict__ sort_count, uint32_t T,
-                                                          uint32_t* __restrict__ ranges, uint32_t* __restrict__ tkeys,
-                                                          uint32_t* __restrict__ hist, uint32_t nblocks,
-                                                          uint32_t* __restrict__ tile_count) {
+// Every tile's dispatch key from its range; block b covers tiles
+// [b*2048, b*2048+2048) and leaves its per-digit key counts in column b of the
+// digit-major histogram matrix that the radix scan reads.
+__global__ void __launch_bounds__(GS_BLOCK) k_tile_keys(const uint32_t* __restrict__ ranges, uint32_t T,
+                                                        uint32_t* __restrict__ tkeys, uint32_t* __restrict__ hist,
+                                                        uint32_t nblocks, uint32_t* __restrict__ tile_count) {
     static_assert(GS_BLOCK == 256, "one digit counter per thread");
-    __shared__ uint32_t s_start[GS_TILE_ITEMS + 1];
     __shared__ uint32_t h[256];
     const uint32_t tid = threadIdx.x;
-    const uint32_t M = sort_count ? *sort_count : 0u;
-    const uint32_t b0 = blockIdx.x * GS_TILE_ITEMS;
     h[tid] = 0;
     if (blockIdx.x == 0 && tid == 0) *tile_count = T;
-    uint32_t v[kRangeSearches], pos[kRangeSearches];
-#pragma unroll
-    for (int k = 0; k < kRangeSearches; ++k) {
-        v[k] = b0 + (k < GS_ITEMS ? k * GS_BLOCK + tid : GS_TILE_ITEMS);
-        pos[k] = 0;
-    }
-    if (M > 0) {
-        for (uint32_t len = M; len > 1;) {
-            const uint32_t half = len >> 1;
-#pragma unroll
-            for (int k = 0; k < kRangeSearches; ++k) pos[k] = skeys[pos[k] + half] < v[k] ? pos[k] + half : pos[k];
-            len -= half;
-        }
-#pragma unroll
-        for (int k = 0; k < kRangeSearches; ++k) pos[k] += skeys[pos[k]] < v[k] ? 1u : 0u;
-    }
-#pragma unroll
-    for (int k = 0; k < GS_ITEMS; ++k) s_start[k * GS_BLOCK + tid] = pos[k];
-    if (tid == 0) s_start[GS_TILE_ITEMS] = pos[GS_ITEMS];
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t i = k * GS_BLOCK + tid, t = b0 + i;
+        const uint32_t t = blockIdx.x * GS_TILE_ITEMS + k * GS_BLOCK + tid;
         if (t < T) {
-            const uint32_t s = s_start[i], e = s_start[i + 1], n = e - s;
-            ranges[2 * t] = n ? s : 0u;
-            ranges[2 * t + 1] = n ? e : 0u;
-            const uint32_t key = tile_order_key(n);
+            const uint32_t key = tile_order_key(ranges[2 * t + 1] - ranges[2 * t]);
             tkeys[t] = key;
             atomicAdd(&h[key], 1u);
         }
@@ -582,10 +581,14 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     uint32_t* order = tile_order ? tile_order : at<uint32_t>(ws, L.order);
     // ranges, dispatch keys and the dispatch order (tiles by pair count
     // descending, ties by tile id: one stable radix pass over 8-bit keys)
+    // (ranges must hold zeros on entry)
     auto tile_pass = [&](const uint32_t* skeys, const uint32_t* sort_count) {
         const uint32_t nbT = div_up(T, GS_TILE_ITEMS);
-        hipLaunchKernelGGL(k_tile_ranges, dim3(nbT), dim3(GS_BLOCK), 0, st, skeys, sort_count, T, ranges,
-                           at<uint32_t>(ws, L.tkey[0]), hist, nbT, ctr + 2);
+        if (skeys)
+            hipLaunchKernelGGL(k_tile_bounds, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, skeys,
+                               sort_count, ranges);
+        hipLaunchKernelGGL(k_tile_keys, dim3(nbT), dim3(GS_BLOCK), 0, st, ranges, T, at<uint32_t>(ws, L.tkey[0]),
+                           hist, nbT, ctr + 2);
         hipLaunchKernelGGL(k_radix_scan, dim3(256), dim3(GS_BLOCK), 0, st, hist, nbT, totals);
         hipLaunchKernelGGL(k_radix_scatter<8>, dim3(nbT), dim3(GS_BLOCK), 0, st, at<uint32_t>(ws, L.tkey[0]),
                            nullptr, at<uint32_t>(ws, L.tkey[1]), order, ctr + 2, 0, 255u, 8, hist, totals, nbT);
@@ -594,8 +597,9 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     // no pairs: empty ranges, and the order (then the tile ids) when the caller keeps it
     auto no_pairs = [&]() {
         if (T == 0) return hipGetLastError();
-        if (tile_order) return tile_pass(nullptr, nullptr);
-        return launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
+        hipError_t e = launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
+        if (e != hipSuccess || !tile_order) return e;
+        return tile_pass(nullptr, nullptr);
     };
     if (n == 0) {
         hipError_t e = launch_fill_u32(num_pairs, 0u, 1, st);
@@ -605,7 +609,8 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     // 1. emission offsets in visible-set order
     const uint32_t* vorder = vis_idx;
     const uint32_t nb = div_up(n, GS_TILE_ITEMS);
-    hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum);
+    hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum, ranges,
+                       2 * T);
     hipError_t e = launch_scan_blocks(bsum, nb, ctr + 0, nullptr, st);
     if (e != hipSuccess) return e;
     uint32_t* offs_r = at<uint32_t>(ws, L.offs);
