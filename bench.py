@@ -51,14 +51,17 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 # of the 10 dispatches of an 8-step run without extras: 2 warm-up and 8 timed),
 # each scaled by what the same counter reads for a plain device copy of known
 # size (a 1 GiB read registers as 0.5 GiB of FETCH_SIZE, a 1 GiB write as
-# 1 GiB of WRITE_SIZE).  Valid only for the kernel code it was measured on
-# (comments aside): reported as null once the code of raster.hip changes.
+# 1 GiB of WRITE_SIZE).  Valid only for the workload and the code it was
+# measured on (comments aside): the kernel's source and the bin sort, whose
+# tile dispatch order decides what the kernel finds in L2; reported as null
+# for other workloads and once either source changes.
 TRAFFIC = {
     "kernel": "k_raster_bwd",
-    "source": "paper_2607_19893_amd/csrc/raster.hip",
-    "code_sha256": "e3a58f567ca2bc9603e7667148362930dd5277221349c81506abe89457c74894",
-    "fetch_kib": 258715.71, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 96878.44, "write_scale": 1048576.0 / 1048576.0,
+    "workload": "room-1M-L3-1080p",
+    "sources": ["paper_2607_19893_amd/csrc/raster.hip", "paper_2607_19893_amd/csrc/binsort.hip"],
+    "code_sha256": "0ec08619fad4a3c96e3c4a1897080b06c500f947c659adfcc162a1b23cdd17af",
+    "fetch_kib": 258695.14, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 96865.70, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
@@ -82,11 +85,17 @@ def code_digest(text):
     return hashlib.sha256(text.encode()).hexdigest()
 
 
-def traffic_bytes():
-    """HBM bytes per launch of the dominant kernel, or None if its code changed since the counters were taken."""
-    path = os.path.join(ROOT, TRAFFIC["source"])
+def traffic_digest():
+    return code_digest("\n".join(open(os.path.join(ROOT, f)).read() for f in TRAFFIC["sources"]))
+
+
+def traffic_bytes(workload):
+    """HBM bytes per launch of the dominant kernel on `workload`, or None if the counters were taken on
+    another workload or the code changed since."""
+    if workload != TRAFFIC["workload"]:
+        return None
     try:
-        digest = code_digest(open(path).read())
+        digest = traffic_digest()
     except OSError:
         return None
     if digest != TRAFFIC["code_sha256"]:
@@ -277,7 +286,7 @@ def main():
     dom = max(on_path, key=lambda n: phase_ms[names.index(n)])
     bound, work, peak, unit = roofs[dom]
     ach = work / (phase_ms[names.index(dom)] * 1e-3)
-    tb = traffic_bytes() if dom == "raster_bwd_pixels" else None
+    tb = traffic_bytes(w.name) if dom == "raster_bwd_pixels" else None
     roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
                 "frac": round(ach / peak, 5), "traffic": round(tb) if tb is not None else None}
     log("phase rooflines: " + json.dumps(per_phase))

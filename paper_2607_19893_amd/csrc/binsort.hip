@@ -37,6 +37,9 @@ namespace {
 // latency-bound launches than the pass they save).  Every kernel takes the
 // digit width as a template parameter; a block holds 2^BITS counters in LDS.
 constexpr int kTileBits = 8;
+// Up to this many 2048-item blocks (32768 tiles: a 4K image has 32400)
+// the tile-order scatter sums its digit offsets itself instead of a scan launch.
+constexpr uint32_t kSelfScanBlocks = 16;
 
 template <int BITS>
 __global__ void __launch_bounds__(GS_BLOCK) k_radix_hist(const uint32_t* __restrict__ keys,
@@ -99,13 +102,15 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid, int nbit
     return peers;
 }
 
-// Stable scatter of block b's 2048 keys.  Wave w ranks its own 512 keys
+// Stable scatter of block b's 2048 keys.  With SELF_SCAN the histogram
+// matrix is the unscanned per-block counts and each block sums its digit
+// offsets from it (for a few blocks: saves the scan launch).  Wave w ranks its own 512 keys
 // (contiguous, 64 per round) against a wave-private running count per digit,
 // so the rounds need no block barrier; one barrier then turns the four
 // waves' digit counts into per-wave offsets.  Position of a key = start of
 // its digit over all blocks + its block's offset (from the scanned matrix) +
 // the keys of earlier waves with that digit + its rank inside its wave.
-template <int BITS>
+template <int BITS, bool SELF_SCAN = false>
 __global__ void __launch_bounds__(GS_BLOCK) k_radix_scatter(
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, uint32_t* __restrict__ keys_out,
     uint32_t* __restrict__ vals_out, const uint32_t* __restrict__ count_ptr, int shift, uint32_t mask,
@@ -122,12 +127,24 @@ __global__ void __launch_bounds__(GS_BLOCK) k_radix_scatter(
     const int lane = lane_id();
     // digit starts: exclusive scan of the digit totals, thread t owning digits [t*PER, t*PER+PER)
     {
-        uint32_t tv[PER];
+        uint32_t tv[PER], bq[PER];
         uint32_t sum = 0;
 #pragma unroll
         for (int q = 0; q < PER; ++q) {
             const int d = tid * PER + q;
-            tv[q] = d < R ? totals[d] : 0u;
+            if (SELF_SCAN) {
+                uint32_t before = 0, all = 0;
+                if (d < R)
+                    for (uint32_t j = 0; j < nblocks; ++j) {
+                        const uint32_t c = hist[(size_t)d * nblocks + j];
+                        before += j < blockIdx.x ? c : 0u;
+                        all += c;
+                    }
+                tv[q] = all;
+                bq[q] = before;
+            } else {
+                tv[q] = d < R ? totals[d] : 0u;
+            }
             sum += tv[q];
         }
         uint32_t tot;
@@ -136,7 +153,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_radix_scatter(
         for (int q = 0; q < PER; ++q) {
             const int d = tid * PER + q;
             if (d < R) {
-                s_base[d] = run + hist[(size_t)d * nblocks + blockIdx.x];
+                s_base[d] = run + (SELF_SCAN ? bq[q] : hist[(size_t)d * nblocks + blockIdx.x]);
                 s_wc[0][d] = 0; s_wc[1][d] = 0; s_wc[2][d] = 0; s_wc[3][d] = 0;
             }
             run += tv[q];
@@ -589,9 +606,15 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
                                sort_count, ranges);
         hipLaunchKernelGGL(k_tile_keys, dim3(nbT), dim3(GS_BLOCK), 0, st, ranges, T, at<uint32_t>(ws, L.tkey[0]),
                            hist, nbT, ctr + 2);
-        hipLaunchKernelGGL(k_radix_scan, dim3(256), dim3(GS_BLOCK), 0, st, hist, nbT, totals);
-        hipLaunchKernelGGL(k_radix_scatter<8>, dim3(nbT), dim3(GS_BLOCK), 0, st, at<uint32_t>(ws, L.tkey[0]),
-                           nullptr, at<uint32_t>(ws, L.tkey[1]), order, ctr + 2, 0, 255u, 8, hist, totals, nbT);
+        if (nbT <= kSelfScanBlocks) {
+            hipLaunchKernelGGL((k_radix_scatter<8, true>), dim3(nbT), dim3(GS_BLOCK), 0, st,
+                               at<uint32_t>(ws, L.tkey[0]), nullptr, at<uint32_t>(ws, L.tkey[1]), order, ctr + 2, 0,
+                               255u, 8, hist, totals, nbT);
+        } else {
+            hipLaunchKernelGGL(k_radix_scan, dim3(256), dim3(GS_BLOCK), 0, st, hist, nbT, totals);
+            hipLaunchKernelGGL(k_radix_scatter<8>, dim3(nbT), dim3(GS_BLOCK), 0, st, at<uint32_t>(ws, L.tkey[0]),
+                               nullptr, at<uint32_t>(ws, L.tkey[1]), order, ctr + 2, 0, 255u, 8, hist, totals, nbT);
+        }
         return hipGetLastError();
     };
     // no pairs: empty ranges, and the order (then the tile ids) when the caller keeps it

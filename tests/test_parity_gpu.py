@@ -537,6 +537,35 @@ def test_dispatch_order_changes_no_result(case, torch_gpu, orc):
         assert torch_gpu.equal(a, b)
 
 
+def test_tile_order_large_image(torch_gpu, orc):
+    """An image of more than 32768 tiles (4100x2320: 37265) takes the tile
+    order's scanned path: ranges, pair order and tile order bit-exact, and
+    the forward image the same in either dispatch order."""
+    from paper_2607_19893_amd import scenes
+    w = scenes.ring(n=20000, width=4100, height=2320)
+    cam = w.cameras[0]
+    T = cam.num_tiles
+    assert T > 32768
+    ref = orc.project(w.scene, cam, 0)
+    vis_ref = orc.visible(ref.tiles)
+    keys_ref, vals_ref, ranges_ref = orc.sorted_pairs(vis_ref, ref, cam)
+    imgs = []
+    for longest_first in (True, False):
+        tr = trainer_for(w, torch_gpu)
+        tr.longest_first = longest_first
+        tr.status.zero_()
+        tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd()
+        torch_gpu.cuda.synchronize()
+        assert u32(tr.status)[0] == 0
+        M = int(u32(tr.counts[1:2])[0])
+        assert M == keys_ref.size
+        np.testing.assert_array_equal(u32(tr.vals)[:M], vals_ref)
+        np.testing.assert_array_equal(u32(tr.ranges)[:2 * T].reshape(T, 2), ranges_ref)
+        np.testing.assert_array_equal(u32(tr.tile_order)[:T], expected_tile_order(ranges_ref))
+        imgs.append(tr.img.view(-1)[:3 * cam.width * cam.height].clone())
+    assert torch_gpu.equal(imgs[0], imgs[1])
+
+
 def test_backward_halves_match_combined(torch_gpu, orc):
     """gs_raster_bwd_pixels + gs_raster_bwd_project give gs_raster_bwd's result bit for bit."""
     w = get_case("room-60k-392x216")
