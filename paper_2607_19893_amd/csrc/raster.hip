@@ -250,11 +250,18 @@ __global__ void __launch_bounds__(GS_BLOCK, 7) k_raster_fwd(
         for (int q = 0; q < 4; ++q) lim[q] = ((live >> (16 * q)) & 0xFFFFull) ? (uint32_t)GS_BLOCK : 0u;
         if (live) compact_rows(L, nb, wx0, wx1, wy0, lim, s_list[w], nl);
         const uint32_t my_n = for_row(nl, row);
-        const uint32_t steps = max(max(nl[0], nl[1]), max(nl[2], nl[3]));
+        // the counts come from ballots, so every lane holds the same values
+        const uint32_t steps = __builtin_amdgcn_readfirstlane(max(max(nl[0], nl[1]), max(nl[2], nl[3])));
+        uint64_t live_w = live;     // lanes not yet done, kept as a scalar mask
         for (uint32_t jj = 0; jj < steps; ++jj) {
-            if (!wave_any(!done)) break;
+            if (live_w == 0ull) break;
             const bool act = jj < my_n;
-            const int k = act ? s_list[w][row][jj] : 0;
+            // the list read needs no branch (every byte indexes the 256-entry batch), but
+            // past the row's count the byte is stale and may name a slot this batch never
+            // staged, whose colour could be Inf or NaN (0 * Inf poisons the sums): such
+            // lanes take entry 0, which every batch stages
+            const int k_list = s_list[w][row][jj];
+            const int k = act ? k_list : 0;
             const SplatR R = L.R[k];
             double ddx, ddy, inner, cdy;
             const float sigma = splat_sigma(L.P[k], L.Q[k], R.c2, fx, fy, ddx, ddy, inner, cdy);
@@ -266,6 +273,10 @@ __global__ void __launch_bounds__(GS_BLOCK, 7) k_raster_fwd(
             if (STATS && term) term_at = pos;
             terminated = terminated || term;
             done = done || term;
+            // the terminating lanes, as ballots of the comparisons themselves (a ballot of
+            // a compare is its lane mask; a ballot of a combined flag costs two VALU ops)
+            live_w &= ~(__builtin_amdgcn_ballot_w64(act) & live_w & __builtin_amdgcn_ballot_w64(!(sigma < 0.0f)) &
+                        __builtin_amdgcn_ballot_w64(!(alpha < kAlphaMin)) & __builtin_amdgcn_ballot_w64(Tn < kTMin));
             ok = ok && !term;
             const float4 col = L.S[k];
             const float wgt = ok ? alpha * T : 0.0f;
@@ -528,9 +539,17 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
         }
         if (work && any) compact_rows(L, (int)cnt, wx0, wx1, wy0, lim, s_list[w], nl);
         const uint32_t my_n = for_row(nl, row);
-        const uint32_t steps = max(max(nl[0], nl[1]), max(nl[2], nl[3]));
+        // the counts come from ballots, so every lane holds the same values
+        uint32_t nls[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) nls[q] = __builtin_amdgcn_readfirstlane(nl[q]);
+        const uint32_t steps = max(max(nls[0], nls[1]), max(nls[2], nls[3]));
         for (uint32_t jj = 0; jj < steps; ++jj) {
             const bool act = jj < my_n;
+            // act's lanes from the rows' list lengths, in scalar registers
+            uint64_t act_mask = 0ull;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) act_mask |= jj < nls[q] ? 0xFFFFull << (16 * q) : 0ull;
             const int k = act ? s_list[w][row][my_n - 1u - jj] : 0;
             const SplatR R = L.R[k];
             const double2 Q = L.Q[k];
@@ -540,7 +559,11 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             const float gv = R.o * e;
             const float alpha = fminf(kAlphaMax, gv);
             const bool ok = act && bs + (uint32_t)k < last && !(sigma < 0.0f) && !(alpha < kAlphaMin);
-            const uint64_t mask = __ballot(ok);
+            // the lanes of ok, as ballots of the comparisons themselves (a ballot of a
+            // compare is its lane mask; a ballot of a combined flag costs two VALU ops)
+            const uint64_t mask = act_mask & __builtin_amdgcn_ballot_w64(bs + (uint32_t)k < last) &
+                                  __builtin_amdgcn_ballot_w64(!(sigma < 0.0f)) &
+                                  __builtin_amdgcn_ballot_w64(!(alpha < kAlphaMin));
             if (mask == 0ull) continue;
             const float4 col = L.S[k];
             const float inv_om = __builtin_amdgcn_rcpf(1.0f - alpha);
