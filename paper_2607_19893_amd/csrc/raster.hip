@@ -543,7 +543,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
         uint32_t nls[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) nls[q] = __builtin_amdgcn_readfirstlane(nl[q]);
-        const uint32_t steps = max(max(nls[0], nls[1]), max(nls[2], nls[3]));
+        const uint32_t steps = __builtin_amdgcn_readfirstlane(max(max(nls[0], nls[1]), max(nls[2], nls[3])));
         for (uint32_t jj = 0; jj < steps; ++jj) {
             const bool act = jj < my_n;
             // act's lanes from the rows' list lengths, in scalar registers
@@ -592,7 +592,10 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
                 // it folds into the DPP instruction
                 asm volatile("" : "+v"(gr[q]));
             }
-            if ((lane & 15) == 0 && ((mask >> lane) & 0xFFFFull) != 0ull) {
+            // the leader of every row that walks an entry stores: a row without a
+            // contributing pixel stores zero sums into its record, which holds zeros
+            // (records are cleared per batch and a row visits an entry once)
+            if ((lane & 15) == 0 && act) {
 #pragma unroll
                 for (int q = 0; q < kRowSums; ++q) s_row[w][row][q][k] = gr[q];
             }
