@@ -59,9 +59,9 @@ TRAFFIC = {
     "kernel": "k_raster_bwd",
     "workload": "room-1M-L3-1080p",
     "sources": ["paper_2607_19893_amd/csrc/raster.hip", "paper_2607_19893_amd/csrc/binsort.hip"],
-    "code_sha256": "0ec08619fad4a3c96e3c4a1897080b06c500f947c659adfcc162a1b23cdd17af",
-    "fetch_kib": 258695.14, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 96865.70, "write_scale": 1048576.0 / 1048576.0,
+    "code_sha256": "55572912b5ee030153a7aa3f7c0208ece44d4d299b4e7cb4fc581f712e4a40d8",
+    "fetch_kib": 258383.81, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 96881.29, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
