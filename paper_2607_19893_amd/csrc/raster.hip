@@ -121,8 +121,6 @@ __device__ __forceinline__ float exp_neg(float sigma) {
     return __builtin_amdgcn_exp2f(-hi) * fmaf(-lo, kLn2, 1.0f);
 }
 
-__device__ __forceinline__ bool wave_any(bool p) { return __ballot(p) != 0ull; }
-__device__ __forceinline__ bool uniform(bool p) { return __builtin_amdgcn_readfirstlane((int)p) != 0; }
 
 // Row-wise lists: each 16-lane row of a wave (one pixel row of the tile)
 // keeps its own ascending list of the batch entries whose footprint reaches
