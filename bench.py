@@ -59,9 +59,9 @@ TRAFFIC = {
     "kernel": "k_raster_bwd",
     "workload": "room-1M-L3-1080p",
     "sources": ["paper_2607_19893_amd/csrc/raster.hip", "paper_2607_19893_amd/csrc/binsort.hip"],
-    "code_sha256": "0c675601321d45be6cd3b1332e0d2b0c699db6be28c0c991ddc5018ccd91f1a1",
-    "fetch_kib": 258383.81, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 96881.29, "write_scale": 1048576.0 / 1048576.0,
+    "code_sha256": "edd247363b439b1763bdc96ff07979ed368b352f40eae5aee3197d1cf72cd78c",
+    "fetch_kib": 258380.44, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 96876.40, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 

@@ -237,12 +237,15 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restri
 
 // Exclusive offsets in visible-set order: pair_offset[id] and offs_r[rank],
 // with offs_r[V] = M as a sentinel.  Also publishes the pair count and the
-// overflow flag.
+// overflow flag, and for every 2048-pair emission block m the rank that holds
+// its first pair (bstart[m], m < nbs): the rank whose pairs [off, off + t)
+// contain m * 2048 writes it, so each entry has one writer.
 __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
     const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
     const uint32_t* __restrict__ bsum, const uint32_t* __restrict__ total, uint32_t capacity,
     uint32_t* __restrict__ pair_offset, uint32_t* __restrict__ offs_r, uint32_t* __restrict__ sort_count,
-    uint32_t* __restrict__ num_pairs, gs_device_status* __restrict__ status) {
+    uint32_t* __restrict__ num_pairs, gs_device_status* __restrict__ status, uint32_t* __restrict__ bstart,
+    uint32_t nbs) {
     __shared__ uint32_t scratch[4];
     const uint32_t V = *vis_count;
     const uint32_t M = *total;
@@ -272,6 +275,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
         if (base + k >= V) break;
         pair_offset[g[k]] = off;
         offs_r[base + k] = off;
+        const uint64_t end = (uint64_t)off + t[k];
+        for (uint64_t m = ((uint64_t)off + GS_TILE_ITEMS - 1) / GS_TILE_ITEMS; m < nbs && m * GS_TILE_ITEMS < end; ++m)
+            bstart[m] = base + k;
         off += t[k];
     }
 }
@@ -285,9 +291,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
 // as column b of the digit-major matrix (zeros past the last pair).
 __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
     const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ offs_r,
-    const ushort4* __restrict__ rect, const uint32_t* __restrict__ sort_count, int32_t tiles_x,
-    uint32_t* __restrict__ pkeys, uint32_t* __restrict__ pvals, uint32_t mask0, uint32_t* __restrict__ hist,
-    uint32_t nblocks) {
+    const uint32_t* __restrict__ bstart, const ushort4* __restrict__ rect, const uint32_t* __restrict__ sort_count,
+    int32_t tiles_x, uint32_t* __restrict__ pkeys, uint32_t* __restrict__ pvals, uint32_t mask0,
+    uint32_t* __restrict__ hist, uint32_t nblocks) {
     __shared__ uint32_t s_off[GS_TILE_ITEMS + 1];
     __shared__ uint32_t s_gid[GS_TILE_ITEMS + 1];
     __shared__ ushort4 s_rect[GS_TILE_ITEMS + 1];
@@ -301,15 +307,16 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
         return;
     }
     const uint32_t hi = min(base + (uint32_t)GS_TILE_ITEMS, M);
-    if (threadIdx.x < 2) {
-        // largest r in [0, V) with offs_r[r] <= key
-        const uint32_t key = threadIdx.x == 0 ? base : hi - 1;
-        uint32_t lo = 0, up = *vis_count;   // invariant: offs_r[lo] <= key < offs_r[up]
-        while (up - lo > 1) {
-            const uint32_t mid = (lo + up) >> 1;
-            if (offs_r[mid] <= key) lo = mid; else up = mid;
-        }
-        s_range[threadIdx.x] = lo;
+    if (threadIdx.x == 0) {
+        // the ranks of the block's first and last pairs: the first from the table
+        // k_offsets wrote; the last is the next block's first rank, or the one
+        // before it when that rank starts exactly at hi (the last rank for the
+        // last block), stepping back over ranks that start later
+        const uint32_t r0 = bstart[blockIdx.x];
+        uint32_t r1 = hi == M ? *vis_count - 1u : bstart[blockIdx.x + 1];
+        while (r1 > r0 && offs_r[r1] > hi - 1u) --r1;
+        s_range[0] = r0;
+        s_range[1] = r1;
     }
     __syncthreads();
     const uint32_t r0 = s_range[0];
@@ -511,7 +518,7 @@ struct BinsortLayout {
                               // pv[1..2] = value ping-pong (values out = caller's pair_emit)
     size_t scratch;           // 64-bit keys of tiles longer than the LDS sort
     size_t tkey[2], order;    // tile dispatch keys (in, sorted) and the order when the caller keeps none
-    size_t hist, totals, bsum, offs, counters;
+    size_t hist, totals, bsum, offs, bstart, counters;
     size_t bytes;
     uint32_t nblocks_hist;
 };
@@ -538,6 +545,7 @@ BinsortLayout binsort_layout(int32_t n, uint32_t capacity, int32_t width, int32_
     L.totals = o; o += align256(4 * ((size_t)1 << kTileBits));
     L.bsum = o; o += align256(4 * ((size_t)div_up(nn, GS_TILE_ITEMS) + 1));
     L.offs = o; o += align256(4 * (nn + 1));
+    L.bstart = o; o += align256(4 * ((size_t)div_up(cc, GS_TILE_ITEMS) + 1));
     L.counters = o; o += 256;
     L.bytes = o;
     return L;
@@ -637,15 +645,17 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     hipError_t e = launch_scan_blocks(bsum, nb, ctr + 0, nullptr, st);
     if (e != hipSuccess) return e;
     uint32_t* offs_r = at<uint32_t>(ws, L.offs);
+    const uint32_t nbs = div_up(capacity, GS_TILE_ITEMS) + 1u;
     hipLaunchKernelGGL(k_offsets, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum, ctr + 0,
-                       capacity, pair_offset, offs_r, ctr + 1, num_pairs, status);
+                       capacity, pair_offset, offs_r, ctr + 1, num_pairs, status, at<uint32_t>(ws, L.bstart), nbs);
     int tbits = 1;
     while (tbits < 32 && (1u << tbits) < T) ++tbits;
     const uint32_t mask0 = (1u << (tbits < kTileBits ? tbits : kTileBits)) - 1u;
     if (capacity == 0 || T == 0) return no_pairs();
     // 2. emission: one (tile, primitive) pair per touched tile
     hipLaunchKernelGGL(k_emit_pairs, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, vorder,
-                       vis_count, offs_r, reinterpret_cast<const ushort4*>(proj.rect), ctr + 1, TX,
+                       vis_count, offs_r, at<uint32_t>(ws, L.bstart), reinterpret_cast<const ushort4*>(proj.rect),
+                       ctr + 1, TX,
                        at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), mask0, hist,
                        div_up(capacity, GS_TILE_ITEMS));
     // 3. sort of the pairs by tile id, carrying every pair's emission position
