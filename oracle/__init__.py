@@ -71,7 +71,7 @@ def lib():
         L.orc_visible.restype = i64
         L.orc_sorted_pairs.argtypes = [i64, P, P, P, i32, i32, P, P, P]
         L.orc_sorted_pairs.restype = i64
-        L.orc_render.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, P, P, P, P, P, P]
+        L.orc_render.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, P, P, P, P, P, P, P]
         L.orc_render.restype = None
         L.orc_render_backward.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, i32, P, P, f64, f64, f64, P, f64,
                                           P]
@@ -196,6 +196,7 @@ class Render:
     margin_alpha: np.ndarray
     margin_T: np.ndarray
     n_hits: np.ndarray
+    capped_sig: np.ndarray   # [H,W]: sum of (list position + 1) of the included pairs at the 0.99 cap
 
 
 def render(vis, proj: Projection, cam, bg=(0.0, 0.0, 0.0)) -> Render:
@@ -205,10 +206,10 @@ def render(vis, proj: Projection, cam, bg=(0.0, 0.0, 0.0)) -> Render:
     bg = np.ascontiguousarray(bg, np.float64)
     r = Render(img=np.zeros((3, H, W)), T_final=np.zeros((H, W)), n_contrib=np.zeros((H, W), np.uint32),
                active=np.zeros(n, np.uint8), margin_alpha=np.zeros((H, W)), margin_T=np.zeros((H, W)),
-               n_hits=np.zeros((H, W), np.uint32))
+               n_hits=np.zeros((H, W), np.uint32), capped_sig=np.zeros((H, W), np.uint32))
     lib().orc_render(vis.size, _p(vis), _p(proj.rect), _p(proj.depth), _p(proj.mean2d), _p(proj.conic),
                      _p(proj.opacity), _p(proj.rgb), W, H, _p(bg), _p(r.img), _p(r.T_final), _p(r.n_contrib),
-                     _p(r.active), _p(r.margin_alpha), _p(r.margin_T), _p(r.n_hits))
+                     _p(r.active), _p(r.margin_alpha), _p(r.margin_T), _p(r.n_hits), _p(r.capped_sig))
     return r
 
 

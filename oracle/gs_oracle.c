@@ -404,7 +404,7 @@ void orc_project(int n, int deg, const float* mean, const float* ls, const float
             for (int k = 0; k < K; ++k) acc += (double)sh[((size_t)i * K + k) * 3 + ch] * Y[k];
             acc += 0.5;
             if (fabs(acc) < marg) marg = fabs(acc);
-            if (acc < 0.0) { cm |= (uint8_t)(1u << ch); acc = 0.0; }
+            if (acc < 0.0 && g_mutation != 23) { cm |= (uint8_t)(1u << ch); acc = 0.0; }
             rgb[3 * i + ch] = acc;
         }
         clamp[i] = cm;
@@ -561,6 +561,7 @@ typedef struct {
     int n_seen;        /* list entries examined (terminated pixels stop early) */
     double margin_alpha, margin_T, margin_cap;
     int nhit;
+    uint32_t capped_sig;  /* sum of (list position + 1) over the included pairs at the 0.99 cap */
 } orc_pixres;
 
 /* Front-to-back pass of pixel (px, py) over candidates L[0..nl). */
@@ -572,6 +573,7 @@ static orc_pixres composite_pixel(const orc_scene2d* s, const orc_cand* L, int n
     double T = 1.0;
     double C[3] = {0.0, 0.0, 0.0};
     double cx = px + 0.5, cy = py + 0.5;
+    const double amax = (g_mutation == 22) ? 0.999 : ORC_ALPHA_MAX;
     int k;
     for (k = 0; k < nl; ++k) {
         uint32_t j = L[k].j;
@@ -584,9 +586,9 @@ static orc_pixres composite_pixel(const orc_scene2d* s, const orc_cand* L, int n
         double gval = s->opacity[j] * e;
         double ma = fabs(gval - ORC_ALPHA_MIN) / ORC_ALPHA_MIN;
         if (ma < r.margin_alpha) r.margin_alpha = ma;
-        double mc = fabs(gval - ORC_ALPHA_MAX) / ORC_ALPHA_MAX;
+        double mc = fabs(gval - amax) / amax;
         if (mc < r.margin_cap) r.margin_cap = mc;
-        double alpha = gval < ORC_ALPHA_MAX ? gval : ORC_ALPHA_MAX;
+        double alpha = gval < amax ? gval : amax;
         if (alpha < ORC_ALPHA_MIN) continue;
         double Tn = T * (1.0 - alpha);
         double mt = fabs(Tn - ORC_T_MIN) / ORC_T_MIN;
@@ -595,8 +597,9 @@ static orc_pixres composite_pixel(const orc_scene2d* s, const orc_cand* L, int n
         if (hits) {
             orc_hit* h = &hits[r.nhit];
             h->pos = k; h->alpha = alpha; h->T = T; h->g = gval; h->e = e; h->dx = dx; h->dy = dy;
-            h->capped = !(gval < ORC_ALPHA_MAX);
+            h->capped = !(gval < amax);
         }
+        if (!(gval < amax)) r.capped_sig += (uint32_t)(k + 1);
         r.nhit++;
         for (int ch = 0; ch < 3; ++ch) C[ch] += alpha * T * s->rgb[3 * j + ch];
         T = Tn;
@@ -614,13 +617,16 @@ static orc_pixres composite_pixel(const orc_scene2d* s, const orc_cand* L, int n
  *   active [n] set to 1 for every primitive included in at least one pixel;
  *   margin_alpha / margin_T [H,W]: smallest relative distance of any
  *   decision of the pixel from its threshold (1/255 on alpha, 1e-4 on T);
- *   n_hits [H,W]: number of pairs included in the pixel.
+ *   n_hits [H,W]: number of pairs included in the pixel;
+ *   capped_sig [H,W]: sum of (list position + 1) over the pixel's included
+ *   pairs whose o*exp(-sigma) reaches the 0.99 cap (0 if none), so that a
+ *   finite-difference step can tell when a pair crosses the cap.
  */
 void orc_render(int64_t nvis, const uint32_t* vis, const int32_t* rect, const float* depth,
                 const double* mean2d, const double* conic, const double* opacity, const double* rgb,
                 int W, int H, const double* bg,
                 double* img, double* T_final, uint32_t* n_contrib, uint8_t* active,
-                double* margin_alpha, double* margin_T, uint32_t* n_hits)
+                double* margin_alpha, double* margin_T, uint32_t* n_hits, uint32_t* capped_sig)
 {
     orc_scene2d s = {nvis, vis, rect, depth, mean2d, conic, opacity, rgb, W, H,
                      (W + ORC_TILE - 1) / ORC_TILE, (H + ORC_TILE - 1) / ORC_TILE, {bg[0], bg[1], bg[2]}};
@@ -644,6 +650,7 @@ void orc_render(int64_t nvis, const uint32_t* vis, const int32_t* rect, const fl
                     if (margin_alpha) margin_alpha[p] = r.margin_alpha;
                     if (margin_T) margin_T[p] = r.margin_T;
                     if (n_hits) n_hits[p] = (uint32_t)r.nhit;
+                    if (capped_sig) capped_sig[p] = r.capped_sig;
                     if (active)
                         for (int h = 0; h < r.nhit; ++h) active[L[hits[h].pos].j] = 1;  /* benign same-value store */
                 }
@@ -742,7 +749,7 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
                             term[6 + ch] = gC[ch] * e->alpha * e->T;
                         }
                         if (fabs(e->g - ORC_ALPHA_MAX) / ORC_ALPHA_MAX < amb_cap) tf[e->pos] |= 2;
-                        if (!e->capped) {
+                        if (!e->capped || g_mutation == 24) {
                             double A = conic[3 * j], B = conic[3 * j + 1], Cc = conic[3 * j + 2];
                             term[5] = dalpha * e->e;
                             double dsig = -dalpha * e->alpha;
@@ -922,7 +929,7 @@ void orc_project_backward(int n, int deg, const float* mean, const float* ls, co
         sh_eval(deg, d, Y, dY);
         double gd[3] = {0.0, 0.0, 0.0};
         for (int ch = 0; ch < 3; ++ch) {
-            double gc = (clamp[j] >> ch & 1) ? 0.0 : g2[6 + ch];
+            double gc = ((clamp[j] >> ch & 1) && g_mutation != 26) ? 0.0 : g2[6 + ch];
             for (int k = 0; k < K; ++k) {
                 dsh[((size_t)row * K + k) * 3 + ch] = gc * Y[k];
                 double cf = sh[(j * K + k) * 3 + ch];
@@ -934,6 +941,6 @@ void orc_project_backward(int n, int deg, const float* mean, const float* ls, co
         double dd = gd[0] * d[0] + gd[1] * d[1] + gd[2] * d[2];
         for (int k = 0; k < 3; ++k) gmu[k] += (gd[k] - d[k] * dd) / nrm;
         for (int k = 0; k < 3; ++k) dmean[3 * row + k] = gmu[k];
-        grad_norm[row] = sqrt(g2[0] * g2[0] + g2[1] * g2[1]);
+        grad_norm[row] = (g_mutation == 25) ? fabs(g2[0]) + fabs(g2[1]) : sqrt(g2[0] * g2[0] + g2[1] * g2[1]);
     }
 }

@@ -12,6 +12,7 @@ fail.  Sources of truth used here:
   * brute force on tiny inputs (sorted pairs, visible ids);
   * central finite differences of the fp64 forward (every gradient).
 """
+import dataclasses
 import math
 
 import numpy as np
@@ -139,9 +140,11 @@ def test_sh_gradient_finite_difference(orc):
 # projection and compositing closed forms
 # ---------------------------------------------------------------------------
 
-def check_single_gaussian(orc, mode):
-    cam = axis_camera(64, 64, 60.0)
-    z, s, o, rgb = 4.0, 0.2, 0.8, (0.7, 0.2, 0.45)
+def check_single_gaussian(orc, mode, o=0.8, s=0.2, W=64):
+    """One on-axis isotropic Gaussian: the image is rgb * min(0.99, o exp(-rho^2 / (2 var)))
+    with var = (fx s / z)^2 + 0.3, inside the tile rectangle where alpha >= 1/255."""
+    cam = axis_camera(W, W, 60.0)
+    z, rgb = 4.0, (0.7, 0.2, 0.45)
     sc = make_scene([[0.0, 0.0, z]], [s, s, s], [1, 0, 0, 0], o, rgb=rgb)
     pr = orc.project(sc, cam, mode)
     vis = orc.visible(pr.tiles)
@@ -168,11 +171,75 @@ def check_single_gaussian(orc, mode):
         np.testing.assert_allclose(rn.img[ch][safe], exp_img[safe], rtol=1e-5, atol=1e-12)
     np.testing.assert_allclose(rn.T_final[safe], np.where(inc, 1 - alpha, 1.0)[safe], rtol=1e-5)
     assert inc.sum() > 50
+    return g, rn, rgb32, cam, sc, pr, vis
 
 
 @pytest.mark.parametrize("mode", [0, 1])
 def test_single_gaussian_closed_form(orc, mode):
     check_single_gaussian(orc, mode)
+
+
+def check_capped_closed_form(orc, mode=1):
+    """alpha = min(0.99, o e^-sigma): with o = 0.995 the pixels where
+    o e^-sigma >= 0.99 render exactly 0.99 * rgb and keep T = 1 - 0.99; the
+    capped-pair signature marks exactly those pixels (the one pair is at list
+    position 0, so its entry is 1)."""
+    g, rn, rgb32, cam, sc, pr, vis = check_single_gaussian(orc, mode, o=0.995, s=1.0, W=128)
+    core = g >= 0.99
+    assert core.sum() >= 12, core.sum()
+    for ch in range(3):
+        assert np.all(rn.img[ch][core] == 0.99 * rgb32[ch])
+    assert np.all(rn.T_final[core] == 1.0 - 0.99)
+    away = np.abs(g - 0.99) > 1e-9
+    assert np.array_equal((rn.capped_sig > 0)[away], core[away])
+    assert set(np.unique(rn.capped_sig)) <= {0, 1}
+
+
+def test_alpha_cap_closed_form(orc):
+    check_capped_closed_form(orc, 1)
+    check_capped_closed_form(orc, 0)
+
+
+def check_clamped_colour(orc, mode=1):
+    """rgb = max(0, SH(d) + 0.5): a Gaussian whose red sum is -0.3 renders
+    exactly 0 in red everywhere, carries clamp bit 0, and leaves the other
+    channels as the closed form says."""
+    cam = axis_camera(64, 64, 60.0)
+    sc = make_scene([[0.0, 0.0, 4.0]], [0.2] * 3, [1, 0, 0, 0], 0.8, rgb=(-0.3, 0.4, 0.6))
+    pr = orc.project(sc, cam, mode)
+    vis = orc.visible(pr.tiles)
+    assert list(vis) == [0]
+    assert pr.clamp[0] == 1
+    assert pr.rgb[0, 0] == 0.0
+    np.testing.assert_allclose(pr.rgb[0, 1:], [0.4, 0.6], rtol=1e-6)
+    rn = orc.render(vis, pr, cam)
+    assert np.all(rn.img[0] == 0.0)
+    assert rn.img[1].max() > 0.3 and rn.img[2].max() > 0.45
+
+
+def test_colour_clamp_closed_form(orc):
+    check_clamped_colour(orc, 1)
+    check_clamped_colour(orc, 0)
+
+
+def check_capped_backward(orc):
+    """Zero derivative through a pair held at the cap: with the upstream
+    gradient non-zero only on pixels where the single Gaussian of
+    check_capped_closed_form is capped (T = 1, nothing behind, bg = 0), the
+    derivatives w.r.t. u, v, the conic and the opacity are exactly 0, and the
+    colour derivative is sum over those pixels of alpha T w = 0.99 * sum w."""
+    g, rn, rgb32, cam, sc, pr, vis = check_single_gaussian(orc, 1, o=0.995, s=1.0, W=128)
+    core = g >= 0.99 * (1 + 1e-9)
+    rng = np.random.default_rng(4)
+    w = np.zeros((3, cam.height, cam.width))
+    w[:, core] = rng.uniform(0.5, 1.5, (3, int(core.sum())))
+    g2, _ = orc.render_backward(vis, pr, cam, w)
+    assert np.all(g2[0, :6] == 0.0), g2[0, :6]
+    np.testing.assert_allclose(g2[0, 6:], 0.99 * w[:, core].sum(axis=1), rtol=1e-14)
+
+
+def test_capped_pair_backward_is_zero(orc):
+    check_capped_backward(orc)
 
 
 def test_two_layer_composite(orc):
@@ -373,7 +440,10 @@ def _forward_loss(orc, sc, cam, wimg):
     pr = orc.project(sc, cam, 1)
     vis = orc.visible(pr.tiles)
     rn = orc.render(vis, pr, cam)
-    sig = (tuple(pr.radius), tuple(map(tuple, pr.rect)), tuple(pr.clamp), rn.n_contrib.tobytes(), rn.n_hits.tobytes())
+    # the decision signature: culling, rectangles, colour clamps, which pairs
+    # each pixel includes and which of them sit at the 0.99 cap
+    sig = (tuple(pr.radius), tuple(map(tuple, pr.rect)), tuple(pr.clamp), rn.n_contrib.tobytes(), rn.n_hits.tobytes(),
+           rn.capped_sig.tobytes())
     return float((rn.img * wimg).sum()), sig
 
 
@@ -383,6 +453,14 @@ def check_fd_gradients(orc, seed=0, n=6, deg=3, W=40, H=32, tol=1e-5):
     sc = scenes.random_scene(seed, n, deg, extent=0.5, ls_mu=-2.3, ls_sd=0.3, depth=3.0)
     sc.opacity[:] = np.clip(sc.opacity, -2.0, 2.0)    # stay clear of the 0.99 cap
     wimg = rng.standard_normal((3, H, W))
+    return fd_check(orc, sc, cam, wimg, tol)
+
+
+def fd_check(orc, sc, cam, wimg, tol=1e-5):
+    """Every parameter's analytic gradient of sum(wimg * img) against a central
+    finite difference of the fp64 forward, skipping elements whose +-h steps
+    change the decision signature.  Returns the number of elements checked."""
+    n = sc.n
     pr = orc.project(sc, cam, 1)
     vis = orc.visible(pr.tiles)
     g2, _ = orc.render_backward(vis, pr, cam, wimg)
@@ -432,6 +510,82 @@ def test_fd_gradients(orc):
     # steps of 1e-4 relative: truncation error O(h^2) ~ 1e-8 relative
     assert check_fd_gradients(orc, seed=0) > 50
     assert check_fd_gradients(orc, seed=1, n=4, deg=1) > 20
+
+
+def cap_clamp_scene():
+    """Three wide Gaussians at degree 1 in front of a 64x64 camera: two with
+    opacity logits 6 and 7.5 (o = 0.9975, 0.99945) whose cores reach the 0.99
+    cap, one at logit 0.5; the first also has a red channel whose SH sum is
+    negative (clamped).  Cores are >= 15 px apart, so no pixel holds two
+    capped pairs (their product would sit on the 1e-4 termination threshold)."""
+    rng = np.random.default_rng(21)
+    cam = axis_camera(64, 64, 60.0)
+    means = np.array([[-0.75, -0.45, 3.0], [0.8, 0.35, 3.3], [0.1, 0.7, 3.8]])
+    ls = np.log(np.array([[0.5, 0.65, 0.55], [0.6, 0.5, 0.45], [0.4, 0.55, 0.5]]))
+    q = rng.standard_normal((3, 4))
+    q /= np.linalg.norm(q, axis=1, keepdims=True)
+    logit = np.array([6.0, 7.5, 0.5])
+    sh = np.zeros((3, 4, 3))
+    sh[:, 0, :] = rng.uniform(0.2, 0.8, (3, 3))
+    sh[:, 1:, :] = rng.normal(0.0, 0.05, (3, 3, 3))
+    sh[0, 0, 0] = (-0.35 - 0.5) * SQRT_PI2          # red SH sum about -0.35 (clamped)
+    sc = scenes.Scene(mean=means.astype(np.float32), log_scale=ls.astype(np.float32),
+                      quat=q.astype(np.float32), opacity=logit.astype(np.float32), sh=sh.astype(np.float32),
+                      sh_degree=1)
+    wimg = rng.standard_normal((3, cam.height, cam.width))
+    return sc, cam, wimg
+
+
+def check_fd_cap_clamp(orc):
+    """Finite differences on a scene with capped pairs and a clamped channel:
+    no derivative flows through a capped pair (w.r.t. opacity and sigma) nor
+    through a clamped colour channel (w.r.t. its SH and the view direction)."""
+    sc, cam, wimg = cap_clamp_scene()
+    pr = orc.project(sc, cam, 1)
+    assert pr.clamp[0] & 1 and pr.rgb[0, 0] == 0.0
+    rn = orc.render(orc.visible(pr.tiles), pr, cam)
+    assert (rn.capped_sig > 0).sum() >= 6, (rn.capped_sig > 0).sum()
+    return fd_check(orc, sc, cam, wimg)
+
+
+def test_fd_gradients_at_cap_and_clamp(orc):
+    assert check_fd_cap_clamp(orc) > 50
+
+
+def check_grad_norm_fd(orc):
+    """g(p) = ||dL/d(u, v)||_2: finite differences of the render w.r.t. each
+    visible primitive's pixel mean (rectangles and candidate lists held
+    fixed), compared with the 2D gradient and with grad_norm."""
+    sc, cam, wimg = cap_clamp_scene()
+    pr = orc.project(sc, cam, 1)
+    vis = orc.visible(pr.tiles)
+    g2, _ = orc.render_backward(vis, pr, cam, wimg)
+    gr = orc.project_backward(sc, cam, vis, g2, pr)
+
+    def loss_sig(p):
+        rn = orc.render(vis, p, cam)
+        return float((rn.img * wimg).sum()), (rn.n_contrib.tobytes(), rn.n_hits.tobytes(), rn.capped_sig.tobytes())
+
+    _, base_sig = loss_sig(pr)
+    for row, j in enumerate(vis):
+        fd = []
+        for c in range(2):
+            h = 1e-5
+            vals = []
+            for sgn in (+1, -1):
+                p2 = dataclasses.replace(pr, mean2d=pr.mean2d.copy())
+                p2.mean2d[j, c] += sgn * h
+                L, sig = loss_sig(p2)
+                assert sig == base_sig
+                vals.append(L)
+            fd.append((vals[0] - vals[1]) / (2 * h))
+        np.testing.assert_allclose(g2[j, :2], fd, rtol=1e-6, atol=1e-9 * np.abs(fd).max())
+        assert abs(gr.grad_norm[row] - math.hypot(*fd)) <= 1e-6 * math.hypot(*fd), (row, gr.grad_norm[row], fd)
+    return vis.size
+
+
+def test_grad_norm_is_l2_of_uv_gradient(orc):
+    assert check_grad_norm_fd(orc) == 3
 
 
 # ---------------------------------------------------------------------------
@@ -521,7 +675,14 @@ MUTATIONS = {
     5: lambda o: check_fd_gradients(o, seed=0),      # dC/dalpha without 1/(1-alpha)
     6: lambda o: check_sh_vs_scipy(o),               # sign of one SH basis function
     7: lambda o: check_adam_vs_torch(o),             # Adam without bias correction
+    22: lambda o: check_capped_closed_form(o, 1),    # alpha cap at 0.999 instead of 0.99
+    23: lambda o: check_clamped_colour(o, 1),        # colour clamp max(0, .) dropped
+    24: lambda o: check_capped_backward(o),          # derivative passed through capped pairs
+    25: lambda o: check_grad_norm_fd(o),             # grad_norm as |du| + |dv| instead of the 2-norm
+    26: lambda o: check_fd_cap_clamp(o),             # colour gradient through a clamped channel
 }
+# the finite-difference scene catches the capped-pair mistake on its own too
+FD_ALSO = {24: check_fd_cap_clamp}
 
 
 @pytest.mark.parametrize("k", sorted(MUTATIONS))
@@ -530,5 +691,8 @@ def test_planted_mistake_is_caught(orc, k):
     try:
         with pytest.raises(AssertionError):
             MUTATIONS[k](orc)
+        if k in FD_ALSO:
+            with pytest.raises(AssertionError):
+                FD_ALSO[k](orc)
     finally:
         orc.set_mutation(0)
