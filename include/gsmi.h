@@ -193,6 +193,25 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
                          void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * gs_visible_set for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments and results as gs_visible_set, without the workspace: the
+ * compaction's block counts live in a fixed buffer of
+ * GS_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends (looked up, not allocated, on the first call on each
+ * device).  The call allocates nothing.
+ *   n <= GS_NOALLOC_MAX_N, else GS_ERR_UNSUPPORTED and nothing is enqueued.
+ * Every call on one GPU shares that GPU's buffer, which keeps the last call's
+ * contents (each call writes every word it reads, so nothing needs clearing):
+ * calls that can overlap on one GPU (different streams, or threads without
+ * ordering) race, and the caller must serialize them.
+ */
+#define GS_NOALLOC_SCRATCH_BYTES 262144
+#define GS_NOALLOC_MAX_N 134215680    /* (GS_NOALLOC_SCRATCH_BYTES / 4 - 1) blocks of 2048 ids */
+gs_status gs_visible_set_noalloc(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count,
+                                 void* stream);
+
+/*
  * Phase "rendering", part 1 (Section 4.1.2): duplicate every visible
  * primitive once per touched tile and order the (tile, primitive) pairs by
  * (tile, depth, primitive id).  Equal depths keep ascending ids.

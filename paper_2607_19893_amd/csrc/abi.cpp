@@ -171,6 +171,30 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
                       "gs_visible_set");
 }
 
+gs_status gs_visible_set_noalloc(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count,
+                                 void* stream) {
+    GS_REQUIRE(kind == GS_PRED_U32_NONZERO || kind == GS_PRED_U8_NONZERO || kind == GS_PRED_BITMAP,
+               "gs_visible_set_noalloc: bad kind %d", kind);
+    GS_REQUIRE(n >= 0, "gs_visible_set_noalloc: n < 0");
+    if (n > GS_NOALLOC_MAX_N)
+        return fail(GS_ERR_UNSUPPORTED, "gs_visible_set_noalloc: n = %d above GS_NOALLOC_MAX_N (%d)", n,
+                    GS_NOALLOC_MAX_N);
+    GS_REQUIRE(out_count != nullptr, "gs_visible_set_noalloc: null out_count");
+    if (n > 0) {
+        GS_REQUIRE(src && out_idx, "gs_visible_set_noalloc: null pointer");
+        GS_REQUIRE(aligned(src, kind == GS_PRED_U32_NONZERO ? 16 : (kind == GS_PRED_BITMAP ? 4 : 8)),
+                   "gs_visible_set_noalloc: src misaligned");
+    }
+    static_assert(GS_NOALLOC_SCRATCH_BYTES % 256 == 0, "scratch size");
+    if (gsmi::visible_ws_bytes(n) > GS_NOALLOC_SCRATCH_BYTES)
+        return fail(GS_ERR_UNSUPPORTED, "gs_visible_set_noalloc: n = %d needs more than the fixed workspace", n);
+    hipError_t e = hipSuccess;
+    void* ws = gsmi::noalloc_scratch(&e);
+    if (ws == nullptr) return hip_status(e == hipSuccess ? hipErrorInvalidSymbol : e, "gs_visible_set_noalloc");
+    return hip_status(gsmi::launch_visible(kind, src, n, out_idx, out_count, ws, static_cast<hipStream_t>(stream)),
+                      "gs_visible_set_noalloc");
+}
+
 gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                       int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,
                       uint32_t* tile_order, uint32_t* pair_offset, uint32_t* pair_emit, uint64_t* keys,

@@ -4,10 +4,19 @@
 // Three launches: per-block counts (blocked arrangement, 2048 items per
 // block), one single-workgroup exclusive scan of the block counts, and the
 // scatter that recomputes each item's rank within its block.
+#include <mutex>
+
 #include "common.h"
 #include "internal.h"
 
 namespace gsmi {
+
+// Fixed workspace of the visible-set compaction for callers that cannot
+// allocate (gs_visible_set_noalloc).  Each GPU the library runs on holds its
+// own copy until the process ends.  In host code this name is only a
+// stand-in for the device symbol: host code uses the address that
+// hipGetSymbolAddress returns for the current device, never the name.
+static __device__ __align__(256) uint32_t scratch[GS_NOALLOC_SCRATCH_BYTES / sizeof(uint32_t)];
 
 namespace {
 
@@ -123,6 +132,30 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, size_t n, hipStream_t st
     if (blocks > 4096) blocks = 4096;
     hipLaunchKernelGGL(k_fill_u32, dim3(blocks), dim3(GS_BLOCK), 0, st, p, value, n);
     return hipGetLastError();
+}
+
+void* noalloc_scratch(hipError_t* err) {
+    // One lookup per device, made with that device current; later calls read
+    // the cached address.
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* ptr[kMaxDevices] = {};
+    int dev = -1;
+    *err = hipGetDevice(&dev);
+    if (*err != hipSuccess) return nullptr;
+    if (dev < 0 || dev >= kMaxDevices) {
+        *err = hipErrorInvalidDevice;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(mu);
+    if (ptr[dev] == nullptr) {
+        void* p = nullptr;
+        *err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (*err != hipSuccess) return nullptr;
+        ptr[dev] = p;
+    }
+    *err = hipSuccess;
+    return ptr[dev];
 }
 
 size_t visible_ws_bytes(int32_t n) {

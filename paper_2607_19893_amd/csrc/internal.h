@@ -51,6 +51,10 @@ hipError_t launch_visible(int kind, const void* src, int32_t n, uint32_t* out_id
 hipError_t launch_scan_blocks(uint32_t* data, uint32_t n, uint32_t* total_out, uint32_t* aux, hipStream_t s);
 size_t scan_blocks_aux_words(uint32_t n);
 hipError_t launch_fill_u32(uint32_t* p, uint32_t value, size_t n, hipStream_t st);
+// Device address of the fixed visible-set workspace on the current device
+// (GS_NOALLOC_SCRATCH_BYTES, 256-byte aligned); nullptr with *err set if the
+// lookup fails.  Allocates nothing.
+void* noalloc_scratch(hipError_t* err);
 
 // binsort.hip
 size_t binsort_ws_bytes(int32_t n, uint32_t capacity, int32_t width, int32_t height);

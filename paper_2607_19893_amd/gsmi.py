@@ -94,6 +94,7 @@ _lib.gs_delta_msg_bytes.restype = sz
 _lib.gs_delta_msg_bytes.argtypes = [u32, i32, i32]
 _lib.gs_project.argtypes = [ctypes.POINTER(gs_scene), ctypes.POINTER(gs_camera), ctypes.POINTER(gs_proj), P]
 _lib.gs_visible_set.argtypes = [i32, P, i32, P, P, P, sz, P]
+_lib.gs_visible_set_noalloc.argtypes = [i32, P, i32, P, P, P]
 _lib.gs_bin_sort.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, i32, i32, u32, P, P, P, P, P, P, P, P, P, sz, P]
 _lib.gs_raster_fwd.argtypes = [ctypes.POINTER(gs_proj), i32, P, P, P, i32, i32, P, P, P, P, P, P, P]
 _lib.gs_loss_l1.argtypes = [P, P, i32, i32, P, P, P, sz, P]
@@ -121,7 +122,7 @@ _lib.gs_admission_gate.argtypes = [P, P, ctypes.POINTER(gs_gate_args), i32, P, P
 _lib.gs_rlg_build.argtypes = [i32, i32, P, P, i32, i32, P, P, P, ctypes.c_int64, P]
 _lib.gs_lp_partition.argtypes = [i32, P, P, P, P, i32, i32, P, P, P]
 _lib.gs_sds_order.argtypes = [i32, P, i32, P, P, P, P, i32, P, P, P, P, P, P]
-for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
+for _name in ("gs_project", "gs_visible_set", "gs_visible_set_noalloc", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
               "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
               "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
               "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum", "gs_raster_fwd_l1",
@@ -129,8 +130,8 @@ for _name in ("gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "g
     getattr(_lib, _name).restype = i32
 
 EXPORTS = ["gs_abi_version", "gs_status_string", "gs_last_error", "gs_workspace_bytes", "gs_delta_msg_bytes",
-           "gs_project", "gs_visible_set", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1", "gs_raster_bwd",
-           "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
+           "gs_project", "gs_visible_set", "gs_visible_set_noalloc", "gs_bin_sort", "gs_raster_fwd", "gs_loss_l1",
+           "gs_raster_bwd", "gs_raster_bwd_pixels", "gs_raster_bwd_project", "gs_sparse_adam", "gs_sparse_adam_publish",
            "gs_delta_pack", "gs_delta_apply", "gs_scope_from_ids", "gs_scope_from_pred", "gs_scope_conflicts",
            "gs_admission_gate", "gs_publish_commit", "gs_raster_bwd_project_accum", "gs_raster_fwd_l1",
            "gs_rlg_build", "gs_lp_partition", "gs_sds_order"]
@@ -228,6 +229,16 @@ def gs_visible_set(kind, src, n, out_idx, out_count, ws, stream=None):
     return _check("gs_visible_set", _lib.gs_visible_set(int(kind), ptr(src), int(n), ptr(out_idx), ptr(out_count),
                                                         ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
                                                         stream if stream is not None else current_stream()))
+
+
+def gs_visible_set_noalloc(kind, src, n, out_idx, out_count, stream=None):
+    return _check("gs_visible_set_noalloc",
+                  _lib.gs_visible_set_noalloc(int(kind), ptr(src), int(n), ptr(out_idx), ptr(out_count),
+                                              stream if stream is not None else current_stream()))
+
+
+GS_NOALLOC_SCRATCH_BYTES = 262144
+GS_NOALLOC_MAX_N = 134215680
 
 
 def gs_bin_sort(proj: gs_proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges, pair_offset,

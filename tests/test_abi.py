@@ -31,6 +31,17 @@ def test_exports_every_declared_symbol(gs):
     assert gs.gs_abi_version() == gs.ABI_VERSION == 4
 
 
+def test_noalloc_limits_match_header(gs):
+    src = open(os.path.join(ROOT, "include", "gsmi.h")).read()
+    d = dict(re.findall(r"#define (GS_NOALLOC_\w+) (\d+)", src))
+    assert int(d["GS_NOALLOC_SCRATCH_BYTES"]) == gs.GS_NOALLOC_SCRATCH_BYTES
+    assert int(d["GS_NOALLOC_MAX_N"]) == gs.GS_NOALLOC_MAX_N
+    # the compaction needs one count per 2048 ids plus one word
+    assert (gs.GS_NOALLOC_MAX_N // 2048 + 1) * 4 == gs.GS_NOALLOC_SCRATCH_BYTES
+    assert gs.gs_workspace_bytes(gs.GS_WS_VISIBLE_SET, gs.GS_NOALLOC_MAX_N) <= gs.GS_NOALLOC_SCRATCH_BYTES
+    assert gs.gs_workspace_bytes(gs.GS_WS_VISIBLE_SET, gs.GS_NOALLOC_MAX_N + 1) > gs.GS_NOALLOC_SCRATCH_BYTES
+
+
 def test_status_strings(gs):
     assert gs.gs_status_string(0) == "ok"
     assert "workspace" in gs.gs_status_string(3)
@@ -50,6 +61,12 @@ def test_null_and_range_arguments_rejected(gs):
     assert L.gs_project(ctypes.byref(sc), ctypes.byref(cam), ctypes.byref(pr), None) == gs.GS_ERR_UNSUPPORTED
     assert L.gs_visible_set(7, None, 0, None, None, None, 0, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_visible_set(0, 16, 100, 16, 16, 16, 0, None) == gs.GS_ERR_WORKSPACE
+    # the no-allocation variant: sizes beyond its fixed workspace are refused before any HIP call
+    assert L.gs_visible_set_noalloc(0, 16, gs.GS_NOALLOC_MAX_N + 1, 16, 16, None) == gs.GS_ERR_UNSUPPORTED
+    assert "GS_NOALLOC_MAX_N" in gs.gs_last_error()
+    assert L.gs_visible_set_noalloc(3, 16, 100, 16, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_visible_set_noalloc(0, 16, -1, 16, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_visible_set_noalloc(0, 16, 100, 16, None, None) == gs.GS_ERR_INVALID_ARG
     A = (16, 16, 10, 16, 64, 16, 16, 64)          # idx, count, max_rows, grad_rows, grad_ld, m, v, state_ld
     assert L.gs_sparse_adam(None, 0, *A, 1, 0.9, 0.999, 1e-15, None, 0, None) == gs.GS_ERR_INVALID_ARG
     grp = (gs.gs_adam_group * 1)(gs.gs_adam_group(16, 70, 1e-3))
