@@ -215,8 +215,12 @@ gs_status gs_visible_set_noalloc(int32_t kind, const void* src, int32_t n, uint3
  * Phase "rendering", part 1 (Section 4.1.2): duplicate every visible
  * primitive once per touched tile and order the (tile, primitive) pairs by
  * (tile, depth, primitive id).  Equal depths keep ascending ids.
- *   vis_idx/vis_count: ascending visible ids (gs_visible_set on `tiles`)
- *   capacity: length of vals (and keys); more pairs set GS_DEV_PAIR_OVERFLOW
+ *   vis_idx/vis_count: ascending visible ids (gs_visible_set on `tiles`); ids
+ *     whose tile count is 0 may be in the list too (they emit no pair)
+ *   capacity: length of vals (and keys); more pairs set GS_DEV_PAIR_OVERFLOW,
+ *     emit no pair (every range empty) and set pair_offset to 0xFFFFFFFF for
+ *     the listed ids, so that gs_raster_bwd_project reads no pair slot and
+ *     writes zero gradient rows
  *   vals   [capacity] uint32  primitive id of every sorted pair
  *   ranges [T,2] uint32       [start, end) of each tile's pairs, T = tiles in the image
  *   tile_order [T] uint32 or NULL: a dispatch order for the per-tile kernels,
@@ -361,7 +365,7 @@ gs_status gs_raster_bwd_project_accum(const gs_scene* scene, const gs_camera* ca
 
 /*
  * Optimizer update (U in Figure 6; Shadow Graph step 5): Adam on the rows in
- * idx only ("updating only visible primitives", Introduction), torch.optim.Adam
+ * idx only (only the primitives a view sees are updated, Introduction), torch.optim.Adam
  * form with one global step t >= 1:
  *   m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2
  *   delta = -(lr/(1-b1^t)) m / (sqrt(v)/sqrt(1-b2^t) + eps);  p += delta
@@ -403,7 +407,10 @@ gs_status gs_sparse_adam(const gs_adam_group* groups, int32_t n_groups, const ui
  * the pool layout.  If the message would not fit in msg_capacity bytes,
  * NOTHING is written (parameters, moments and message stay as they were) and
  * GS_DEV_MSG_OVERFLOW is set with the required bytes, so the call can be
- * repeated with a larger buffer.  msg is 16-byte aligned.
+ * repeated with a larger buffer.  If `status` already carries
+ * GS_DEV_PAIR_OVERFLOW (the view's gs_bin_sort, given the same status, ran out
+ * of pair capacity, so its gradient is incomplete), nothing is written either;
+ * clear the status before the next view.  msg is 16-byte aligned.
  */
 gs_status gs_sparse_adam_publish(const gs_adam_group* groups, int32_t n_groups, const uint32_t* idx,
                                  const uint32_t* count, int32_t max_rows, const float* grad_rows, int32_t grad_ld,
@@ -455,7 +462,7 @@ gs_status gs_delta_apply(const void* msg, size_t msg_capacity, const gs_group* d
  * updates are staged in a shared two-slot ring that is also the
  * communication source, and a slot is committed once its publication
  * condition holds; throughput-first path: per-primitive publication metadata
- * so that a read skips at most one unpublished update).
+ * so that no read passes over more than one pending update).
  *   slot[0], slot[1]: device message buffers of slot_bytes each, 16-byte
  *     aligned; the update of version v is staged (gs_sparse_adam_publish or
  *     gs_delta_pack with that version) in slot[v & 1]
@@ -548,7 +555,7 @@ gs_status gs_scope_conflicts(const uint32_t* RA, const uint32_t* WA, const uint3
  *   C_A non-empty                                     else GS_GATE_WAIT_NO_ACTIVE
  *   every delayed id has producer evidence            else GS_GATE_WAIT_MISSING
  *   no delayed id's publication metadata names another producer's skipped
- *   update (a read skips at most one unpublished update)  else GS_GATE_WAIT_SECOND
+ *   update (no read passes over two pending updates)   else GS_GATE_WAIT_SECOND
  *   max over D+ of ||g_A(p)|| <= tau * mean over C_A of ||g_A(q)||
  *                                                     else GS_GATE_WAIT_GRADIENT
  *   -> GS_GATE_ADMIT

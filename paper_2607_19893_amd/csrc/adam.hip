@@ -48,6 +48,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint
     int32_t dld = a.dld;
     uint32_t* __restrict__ ids = nullptr;
     if (PUBLISH) {
+        // the view's pair list overflowed (same device status as its
+        // gs_bin_sort): its gradient is incomplete, so nothing is written
+        if (a.status->flags & GS_DEV_PAIR_OVERFLOW) return;
         const uint64_t need = msg_bytes(K, a.row_len, a.n_groups);
         if (need > a.msg_capacity) {
             // all or nothing: no block touches parameters, moments or message

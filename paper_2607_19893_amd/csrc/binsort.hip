@@ -239,7 +239,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restri
 // with offs_r[V] = M as a sentinel.  Also publishes the pair count and the
 // overflow flag, and for every 2048-pair emission block m the rank that holds
 // its first pair (bstart[m], m < nbs): the rank whose pairs [off, off + t)
-// contain m * 2048 writes it, so each entry has one writer.
+// contain m * 2048 writes it, so each entry has one writer.  On overflow
+// (M > capacity) no pair is emitted and pair_offset[id] = 0xFFFFFFFF, so the
+// per-primitive backward finds none of its slots in the buffer.
 __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
     const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
     const uint32_t* __restrict__ bsum, const uint32_t* __restrict__ total, uint32_t capacity,
@@ -273,12 +275,47 @@ __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) {
         if (base + k >= V) break;
-        pair_offset[g[k]] = off;
+        pair_offset[g[k]] = M <= capacity ? off : 0xFFFFFFFFu;
         offs_r[base + k] = off;
         const uint64_t end = (uint64_t)off + t[k];
         for (uint64_t m = ((uint64_t)off + GS_TILE_ITEMS - 1) / GS_TILE_ITEMS; m < nbs && m * GS_TILE_ITEMS < end; ++m)
             bstart[m] = base + k;
         off += t[k];
+    }
+}
+
+// The pairs [base, hi) of one emission block: pair i belongs to the last of
+// the block's nr ranks whose offset is <= i (a zero-tile rank shares its
+// successor's offset and is passed over; the offset after the range is taken
+// as +inf).  STAGED: offsets, ids and rectangles are read from the block's LDS
+// copy, else from global memory (g_off, g_order: the range's first rank).
+template <bool STAGED>
+__device__ __forceinline__ void emit_block_pairs(uint32_t base, uint32_t hi, uint32_t nr, const uint32_t* s_off,
+                                                 const uint32_t* s_gid, const ushort4* s_rect,
+                                                 const uint32_t* __restrict__ g_off,
+                                                 const uint32_t* __restrict__ g_order,
+                                                 const ushort4* __restrict__ rect, int32_t tiles_x,
+                                                 uint32_t* __restrict__ pkeys, uint32_t* __restrict__ pvals,
+                                                 uint32_t mask0, uint32_t* h) {
+#pragma unroll
+    for (int k = 0; k < GS_ITEMS; ++k) {
+        const uint32_t i = base + k * GS_BLOCK + threadIdx.x;
+        if (i >= hi) break;
+        uint32_t lo = 0, up = nr;
+        while (up - lo > 1) {
+            const uint32_t mid = (lo + up) >> 1;
+            if ((STAGED ? s_off[mid] : g_off[mid]) <= i) lo = mid; else up = mid;
+        }
+        const uint32_t gid = STAGED ? s_gid[lo] : g_order[lo];
+        const ushort4 rc = STAGED ? s_rect[lo] : rect[gid];
+        const uint32_t local = i - (STAGED ? s_off[lo] : g_off[lo]);
+        const uint32_t w = (uint32_t)(rc.z - rc.x);
+        const uint32_t ty = rc.y + local / w;
+        const uint32_t tx = rc.x + local % w;
+        const uint32_t key = ty * (uint32_t)tiles_x + tx;
+        pkeys[i] = key;
+        pvals[i] = gid;
+        atomicAdd(&h[key & mask0], 1u);
     }
 }
 
@@ -320,33 +357,27 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
     }
     __syncthreads();
     const uint32_t r0 = s_range[0];
-    const uint32_t nr = s_range[1] - r0 + 1;     // <= GS_TILE_ITEMS: every rank holds >= 1 pair
-    for (uint32_t j = threadIdx.x; j < nr; j += GS_BLOCK) {
-        const uint32_t g = order[r0 + j];
-        s_off[j] = offs_r[r0 + j];
-        s_gid[j] = g;
-        s_rect[j] = rect[g];
+    // Ranks holding pairs of this block: at most GS_TILE_ITEMS + 1 when every
+    // rank holds >= 1 pair (the visible set of gs_project's tile counts); a
+    // caller list with zero-tile ids can span more, and then the block
+    // searches the offsets in global memory instead of staging them.
+    const uint32_t nr = s_range[1] - r0 + 1;
+    const bool staged = nr <= GS_TILE_ITEMS + 1;
+    if (staged) {
+        for (uint32_t j = threadIdx.x; j < nr; j += GS_BLOCK) {
+            const uint32_t g = order[r0 + j];
+            s_off[j] = offs_r[r0 + j];
+            s_gid[j] = g;
+            s_rect[j] = rect[g];
+        }
     }
     __syncthreads();
-#pragma unroll
-    for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t i = base + k * GS_BLOCK + threadIdx.x;
-        if (i >= hi) break;
-        uint32_t lo = 0, up = nr;   // s_off[lo] <= i < s_off[up] (s_off[nr] taken as +inf)
-        while (up - lo > 1) {
-            const uint32_t mid = (lo + up) >> 1;
-            if (s_off[mid] <= i) lo = mid; else up = mid;
-        }
-        const ushort4 rc = s_rect[lo];
-        const uint32_t local = i - s_off[lo];
-        const uint32_t w = (uint32_t)(rc.z - rc.x);
-        const uint32_t ty = rc.y + local / w;
-        const uint32_t tx = rc.x + local % w;
-        const uint32_t key = ty * (uint32_t)tiles_x + tx;
-        pkeys[i] = key;
-        pvals[i] = s_gid[lo];
-        atomicAdd(&h[key & mask0], 1u);
-    }
+    if (staged)
+        emit_block_pairs<true>(base, hi, nr, s_off, s_gid, s_rect, offs_r + r0, order + r0, rect, tiles_x, pkeys,
+                               pvals, mask0, h);
+    else
+        emit_block_pairs<false>(base, hi, nr, s_off, s_gid, s_rect, offs_r + r0, order + r0, rect, tiles_x, pkeys,
+                                pvals, mask0, h);
     __syncthreads();
     for (int d = threadIdx.x; d < (1 << kTileBits); d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = h[d];
 }

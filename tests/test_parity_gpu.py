@@ -493,6 +493,74 @@ def test_pair_overflow_flag(torch_gpu, orc):
     np.testing.assert_array_equal(u32(tr.tile_order)[:T], np.arange(T))
 
 
+def test_pair_overflow_leaves_state_untouched(torch_gpu, orc):
+    """A training step whose pair list overflows its capacity changes no
+    state: the backward finds no pair slot of the view (the slot buffer holds
+    another view's values here), so every gradient row it writes is zero;
+    Adam + staging sees the overflow flag in the shared device status and
+    writes nothing; the commit then finds no message of the version and
+    refuses.  Parameters, moments, message slots, replica and versions stay
+    bit-identical."""
+    torch = torch_gpu
+    w = get_case("tiny-10k-256")
+    tr = trainer_for(w, torch, capacity=1000)
+    tr.set_target(w.target(0))
+    tr.ws_bwd.view(torch.float32).fill_(1.0)        # stale slots of an earlier view
+    tr.grad_rows.fill_(7.0)
+    snap = lambda: [t.clone() for t in (*tr.params, tr.m, tr.v, *tr.msgs, *tr.replica, tr.version, tr.ring_state)]
+    before = snap()
+    tr.status.zero_()
+    tr.step(w.cameras[0], step=1, version=1)
+    torch.cuda.synchronize()
+    s = u32(tr.status)
+    M = int(u32(tr.counts[1:2])[0])
+    assert M > 1000 and s[0] & 1 and s[1] >= M
+    assert s[0] & 4                                  # the commit refused: no message of version 1
+    V = int(u32(tr.counts[0:1])[0])
+    assert V > 0
+    assert np.all(tr.grad_rows[:V].cpu().numpy() == 0.0)
+    assert np.all(u32(tr.pair_offset)[u32(tr.vis_idx)[:V]] == 0xFFFFFFFF)
+    for a, b in zip(before, snap()):
+        assert torch.equal(a, b)
+
+
+def test_zero_tile_ids_in_the_visible_list(torch_gpu, orc):
+    """gs_bin_sort over an id list that also holds primitives with no tile
+    (here every id, 90% of them culled, so one 2048-pair emission block spans
+    far more ranks than its LDS staging holds): the same pairs, order,
+    ranges, dispatch order and emission map as over the visible set."""
+    from paper_2607_19893_amd import scenes
+    torch = torch_gpu
+    w = scenes.tiny(n=20000)
+    w.scene.mean[np.arange(w.scene.n) % 10 != 0, 2] = -10.0     # behind the camera
+    tr = trainer_for(w, torch, capacity=1 << 16)
+    cam = w.cameras[0]
+    T = cam.num_tiles
+    tr.status.zero_()
+    tr.project(cam); tr.visible(); tr.bin_sort()
+    torch.cuda.synchronize()
+    V = int(u32(tr.counts[0:1])[0])
+    M = int(u32(tr.counts[1:2])[0])
+    assert 1500 < V <= 2000 and M > 2048
+    ref = [u32(t)[:k].copy() for t, k in ((tr.vals, M), (tr.pair_emit, M), (tr.ranges, 2 * T), (tr.tile_order, T))]
+    keys = tr.keys.cpu().numpy()[:M].copy()
+    vis = u32(tr.vis_idx)[:V].copy()
+    off = u32(tr.pair_offset)[vis].copy()
+    for t in (tr.vals, tr.pair_emit, tr.ranges, tr.tile_order, tr.keys, tr.pair_offset):
+        t.fill_(-1)
+    n = w.scene.n
+    tr.vis_idx.copy_(torch.arange(n, dtype=torch.int32, device=tr.vis_idx.device))
+    tr.counts[0:1].fill_(n)
+    tr.bin_sort()
+    torch.cuda.synchronize()
+    assert u32(tr.status)[0] == 0 and int(u32(tr.counts[1:2])[0]) == M
+    got = [u32(t)[:k] for t, k in ((tr.vals, M), (tr.pair_emit, M), (tr.ranges, 2 * T), (tr.tile_order, T))]
+    for a, b in zip(ref, got):
+        np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(tr.keys.cpu().numpy()[:M], keys)
+    np.testing.assert_array_equal(u32(tr.pair_offset)[vis], off)
+
+
 def test_empty_and_degenerate(torch_gpu, orc):
     """All primitives behind the camera: empty visible set, empty image."""
     from paper_2607_19893_amd import scenes
