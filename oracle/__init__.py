@@ -8,8 +8,8 @@ integers, see that file's header); the L1 loss, Adam and the pending-update
 pack/apply are plain numpy below.
 
 What each stage follows:
-  * a training view renders one camera, computes an image loss and updates
-    only the participating primitives (paper Section 2.1); the renderer is
+  * one training view draws a single camera, scores it with an image loss,
+    and changes just the primitives that took part (paper Section 2.1); the renderer is
     the cited 3D Gaussian Splatting method;
   * the loss is L1 over all 3*H*W pixel channels;
   * the update is Adam (Kingma & Ba) with torch.optim.Adam's bias-corrected
@@ -573,7 +573,7 @@ def admission_gate(RB, D, CA, g, tau, evidence=None, skip=None, producer_version
       * publication metadata (`skip`, per primitive: the version of a pending
         update an admitted read has already skipped, 0 if none) must show no
         other producer's skipped update on a delayed primitive, so a read
-        skips at most one unpublished update;
+        never passes over more than one pending (unpublished) update;
       * every delayed p needs ||g_A(p)|| <= tau * (1/|C_A|) sum_{q in C_A} ||g_A(q)||.
     Tests are taken in the order listed; the first that fails names the reason.
     g is indexed by primitive id.  The sum is exact (math.fsum), the mean and
@@ -735,7 +735,7 @@ class UnitResult:
 
 def unit_gradients(scene, cams, targets=None, dL_list=None, mode=0):
     """Gradient of a task unit: the sum over its views of each view's loss
-    gradient (a task unit is a small batch of training views, and its active
+    gradient (a task unit groups a few training views, and its active
     set and gradient evidence are the union and accumulation over its views,
     Section 2.1).  Each view's loss is the L1 mean of that view (targets), or
     its upstream image gradient is given (dL_list).  Rows are those of the
