@@ -170,7 +170,10 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
 
     // appearance (fp32, not part of any integer decision)
     if (!ld.head) logit = opacity[(size_t)i * ld.opacity];
-    const float o = 1.0f / (1.0f + expf(-logit));
+    // the sigmoid in fp64, rounded to fp32 once: the blending's transmittance
+    // error grows with alpha / (1 - alpha) times alpha's relative error, and a
+    // two-ulp fp32 sigmoid was a third of that error
+    const float o = (float)(1.0 / (1.0 + exp(-(double)logit)));
     conic_opacity[i] = make_float4(cA, cB, cC, o);
     float dx = mx - c.campos[0], dy = my - c.campos[1], dz = mz - c.campos[2];
     const float inv = 1.0f / sqrtf(dx * dx + dy * dy + dz * dz);

@@ -5,15 +5,14 @@ Bars (derivations in the design notes):
   * rendered pixels: |gpu - oracle| <= 1e-4 * max(|oracle|, PIX_FLOOR);
   * gradients and updated parameters: |gpu - oracle| <= 2e-3 * max(|oracle|, floor)
     + SUM_EPS * M, where M carries the sums of |per-pixel terms| through the
-    chain rule (an fp32 sum's rounding error is relative to them)
-    with floor = max(GRAD_FLOOR_FRAC * (99th percentile of |oracle| over the
-    group), GRAD_ROW_FRAC * |oracle row|) -- the row term covers components
-    that nearly cancel inside one primitive's gradient row, whose fp32 error
-    is relative to the row's magnitude -- plus a normwise check
-    ||gpu - oracle|| / ||oracle|| <= 2e-3.
+    chain rule (an fp32 sum's rounding error is relative to them) and
+    floor = GRAD_FLOOR_FRAC * (99th percentile of |oracle| over the group),
+    plus a normwise check ||gpu - oracle|| / ||oracle|| <= 2e-3.  The
+    comparison reports how many elements pass only because of the floor or
+    only because of the summation term.
 Pixels / primitives whose result depends on a threshold decision that the
 fp32 kernel may take differently from the fp64 oracle are excluded from the
-element-wise check and reported; their share is bounded.
+element-wise check and reported; their share is bounded by AMB_SHARE.
 """
 import numpy as np
 
@@ -21,8 +20,8 @@ PIX_RTOL = 1e-4
 PIX_FLOOR = 0.05
 GRAD_RTOL = 2e-3
 GRAD_FLOOR_FRAC = 1e-2
-GRAD_ROW_FRAC = 1e-1
 SUM_EPS = 1e-5      # fp32 summation error relative to the summed magnitudes
+AMB_SHARE = 1e-4    # largest share of pixels a threshold band may leave out
 
 
 def assert_pixels(gpu, ref, mask=None, name="img"):
@@ -46,10 +45,13 @@ def grad_floor(ref):
     return GRAD_FLOOR_FRAC * float(np.quantile(a, 0.99)) + 1e-30
 
 
-def assert_grads(gpu, ref, rows_ok, name, rtol=GRAD_RTOL, floor=None, mag=None):
+def assert_grads(gpu, ref, rows_ok, name, rtol=GRAD_RTOL, floor=None, mag=None, slack=None):
     """Element-wise on rows_ok (bool per row), normwise on the same rows.
     mag: per-element summed magnitudes (oracle.gradient_magnitudes); adds
-    SUM_EPS * mag to the element-wise bound."""
+    SUM_EPS * mag to the element-wise bound.  slack: a per-element absolute
+    allowance added to the bound (the part of the gradient that comes from
+    pixels whose decisions may go either way); the normwise check then
+    covers the elements whose error stays within the plain bound."""
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
     g, r = gpu[rows_ok], ref[rows_ok]
@@ -57,19 +59,26 @@ def assert_grads(gpu, ref, rows_ok, name, rtol=GRAD_RTOL, floor=None, mag=None):
         return {}
     if floor is None:
         fl = grad_floor(r)
-        if r.ndim == 2 and r.shape[1] > 1:
-            fl = np.maximum(fl, GRAD_ROW_FRAC * np.linalg.norm(r, axis=1, keepdims=True))
     elif np.ndim(floor) == 0:
         fl = floor
     else:
         fl = np.asarray(floor, np.float64)[rows_ok]
     err = np.abs(g - r)
     tol = rtol * np.maximum(np.abs(r), fl)
-    if mag is not None:
-        tol = tol + SUM_EPS * np.asarray(mag, np.float64)[rows_ok]
+    sum_term = SUM_EPS * np.asarray(mag, np.float64)[rows_ok] if mag is not None else 0.0
+    tol = tol + sum_term
+    plain = err <= tol
+    if slack is not None:
+        tol = tol + np.asarray(slack, np.float64)[rows_ok]
     bad = err > tol
-    nrm = float(np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-300))
+    inn = plain if slack is not None else np.ones_like(plain)
+    nrm = float(np.linalg.norm((g - r)[inn]) / max(np.linalg.norm(r[inn]), 1e-300))
     stats = {"max_rel": float((err / np.maximum(np.abs(r), fl)).max()), "norm_rel": nrm, "bad": int(bad.sum())}
+    # how many elements pass only because of the floor, only because of the summation term
+    stats["need_floor"] = int(((err > rtol * np.abs(r) + sum_term) & ~bad).sum())
+    stats["need_sum_term"] = int(((err > rtol * np.maximum(np.abs(r), fl)) & plain).sum())
+    stats["need_slack"] = int((~plain & ~bad).sum())
+    stats["n"] = int(err.size)
     assert bad.sum() == 0, "%s: %d elements beyond %.0e relative (floor %.3g): worst err %.3g ref %.3g" % (
         name, int(bad.sum()), rtol, float(np.max(fl)), err[bad].max(), r[bad][np.argmax(err[bad])])
     assert nrm <= rtol, "%s: normwise error %.3g" % (name, nrm)

@@ -1,6 +1,21 @@
-"""End-to-end parity of one training view at the five full workload sizes,
-in the launch configuration bench.py times (ViewTrainer, all phases), against
-the CPU oracle on the same seeded inputs.
+"""End-to-end parity of one training view at the five full workload sizes
+against the CPU oracle on the same seeded inputs.
+
+Two passes over view 0 of each workload:
+
+  1. every visible primitive's gradient: projection, visible set, bin sort,
+     the fused forward + L1, then the backward with the oracle's upstream
+     gradient, zeroed at the pixels whose threshold decisions lie within the
+     oracle's bands (a pixel's decisions reach the gradients only through
+     its own upstream gradient);
+  2. the benchmark's training step itself (ViewTrainer.step with the
+     overlapped commit, exactly as bench.py times it): visible set, pairs and
+     ranges bit-exact, image, dL/dimg bit-exact against the sign of the GPU
+     image's difference from the target, the step's gradient rows against the
+     oracle's backward of that same dL/dimg on every visible primitive (the
+     bound of each element widened by twice the magnitude that the ambiguous
+     pixels' own terms reach it with), the Adam steps staged as the version-1
+     message, the parameters, and the replica the overlapped commit wrote.
 
 The first Adam step (t = 1, zero moments, eps = 1e-15) gives
 delta = -lr * g / (|g| + eps): elements whose oracle gradient is above the
@@ -14,7 +29,7 @@ import time
 import numpy as np
 import pytest
 
-from parity_util import GRAD_RTOL, assert_grads, assert_pixels, expected_tile_order, grad_floor
+from parity_util import AMB_SHARE, GRAD_RTOL, assert_grads, assert_pixels, expected_tile_order, grad_floor
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -25,6 +40,10 @@ def _say(*a):
 
 
 WORKLOADS = ["tiny", "ring", "room", "spiral", "aerial"]
+
+
+def _group_rows(tr, V):
+    return tr.rows_by_group(tr.grad_rows, V)
 
 
 @pytest.mark.timeout(1100)
@@ -38,96 +57,134 @@ def test_full_view(name, orc):
     w = scenes.workload(name)
     cam = w.cameras[0]
     n = w.scene.n
+    H, W = cam.height, cam.width
     _say(name, "generated n=%d in %.1fs" % (n, time.time() - t0))
-    tr = ViewTrainer(w.scene, capacity=1, max_width=cam.width, max_height=cam.height, lr=w.lr, with_keys=True)
+    tr = ViewTrainer(w.scene, capacity=1, max_width=W, max_height=H, lr=w.lr, with_keys=True)
     tr.ensure_capacity(w.cameras[:1])
     tgt = w.target(0)
     tr.set_target(tgt)
+
+    # oracle: projection, visible set, pairs, render, and the ambiguous pixels
+    t0 = time.time()
+    pr = orc.project(w.scene, cam, 0)
+    vis_o = orc.visible(pr.tiles)
+    keys_o, vals_o, ranges_o = orc.sorted_pairs(vis_o, pr, cam)
+    rn = orc.render(vis_o, pr, cam)
+    amb = orc.ambiguous_pixels(rn)
+    _say(name, "oracle forward in %.1fs; ambiguous pixels %d of %d" % (time.time() - t0, int(amb.sum()), amb.size))
+    assert amb.mean() <= AMB_SHARE
+
+    # ---- 1. every visible primitive's gradient, with the ambiguous pixels' dL zeroed
     tr.status.zero_()
-    tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd(active=True); tr.loss_l1()
+    tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd_l1(active=True)
     torch.cuda.synchronize()
     assert to_u32(tr.status)[0] == 0
-    _say(name, "gpu view done")
-    t0 = time.time()
-    m0 = [np.zeros_like(a) for _, a in w.scene.groups()]
-    ref = orc.train_view(w.scene, cam, tgt, m0, [np.zeros_like(a) for a in m0], 1, lr=w.lr)
-    _say(name, "oracle view done in %.1fs" % (time.time() - t0), {k: round(v, 2) for k, v in ref.times.items()})
-
-    # visible set, pairs, ranges: bit-exact
-    V = int(to_u32(tr.counts[0:1])[0])
-    vis = to_u32(tr.vis_idx)[:V]
-    np.testing.assert_array_equal(vis, ref.vis)
-    M = int(to_u32(tr.counts[1:2])[0])
-    assert M == ref.keys.size
-    np.testing.assert_array_equal(tr.keys.cpu().numpy()[:M].view(np.uint64), ref.keys)
-    np.testing.assert_array_equal(to_u32(tr.vals)[:M], ref.vals)
-    T = cam.num_tiles
-    np.testing.assert_array_equal(to_u32(tr.ranges)[:2 * T].reshape(T, 2), ref.ranges)
-    np.testing.assert_array_equal(to_u32(tr.tile_order)[:T], expected_tile_order(ref.ranges))
-    _say(name, "V=%d M=%d bit-exact" % (V, M))
-
-    # image
-    H, W = cam.height, cam.width
-    img = tr.img.view(-1)[:3 * H * W].cpu().numpy().reshape(3, H, W)
-    amb = (ref.render.margin_alpha < orc.AMB_ALPHA) | (ref.render.margin_T < orc.AMB_T)
-    _say(name, "ambiguous pixels %d of %d" % (int(amb.sum()), amb.size))
-    assert amb.mean() < 2e-3
-    assert_pixels(img, ref.render.img, np.broadcast_to(~amb, img.shape), "img")
-    # loss gradient: the sign decision is taken on the fp32 image on both sides
-    _, g_gpu_img, _ = orc.loss_l1(img, tgt)
-    dL = tr.dL.view(-1)[:3 * H * W].cpu().numpy().reshape(3, H, W).copy()
-    np.testing.assert_array_equal(dL, g_gpu_img.astype(np.float32))
-    assert abs(tr.loss.item() - ref.loss) <= 1e-4 * ref.loss
-
-    # gradients: both sides take the same upstream gradient with the ambiguous
-    # pixels (threshold or loss-sign decisions within the bands) zeroed
-    amb_all = orc.ambiguous_pixels(ref.render, ref.loss_margin)
-    dLm = np.where(amb_all[None], 0.0, ref.dL_dimg).astype(np.float32)
+    _, dL_o, _ = orc.loss_l1(rn.img.astype(np.float32), tgt)
+    dLm = np.where(amb[None], 0.0, dL_o).astype(np.float32)
     tr.set_dL(dLm)
     tr.raster_bwd(grad2d=True)
     torch.cuda.synchronize()
-    g2m, flagm, gabs = orc.render_backward(ref.vis, ref.proj, cam, dLm.astype(np.float64), want_abs=True)
-    grm = orc.project_backward(w.scene, cam, ref.vis, g2m, ref.proj)
-    mags, _ = orc.gradient_magnitudes(w.scene, cam, ref.vis, gabs, ref.proj)
-    ok_rows = ((flagm[vis] & orc.FLAG_NEAR_CAP) == 0) & (ref.proj.clamp_margin[vis] > 1e-5) & \
-        (ref.proj.jclamp_margin[vis] > 1e-5)
-    _say(name, "dL zeroed at %d pixels; gradient rows checked %d of %d" % (int(amb_all.sum()), int(ok_rows.sum()), V))
+    V = int(to_u32(tr.counts[0:1])[0])
+    vis = to_u32(tr.vis_idx)[:V].copy()
+    np.testing.assert_array_equal(vis, vis_o)
+    act = tr.active.cpu().numpy()[:n].copy()
+    t0 = time.time()
+    g2m, flagm, gabs = orc.render_backward(vis_o, pr, cam, dLm.astype(np.float64), want_abs=True)
+    grm = orc.project_backward(w.scene, cam, vis_o, g2m, pr)
+    mags, mag_norm = orc.gradient_magnitudes(w.scene, cam, vis_o, gabs, pr)
+    _say(name, "oracle backward in %.1fs" % (time.time() - t0))
+    # the realized active set: a flag may differ only where an ambiguous pixel looked
+    diff = np.flatnonzero(act != rn.active)
+    assert np.all(flagm[diff] & orc.FLAG_AMB_PIXEL), diff[:10]
+    ok_rows = ((flagm[vis] & orc.FLAG_NEAR_CAP) == 0) & (pr.clamp_margin[vis] > 1e-5) & (pr.jclamp_margin[vis] > 1e-5)
+    _say(name, "dL zeroed at %d pixels; gradient rows checked %d of %d" % (int(amb.sum()), int(ok_rows.sum()), V))
     assert ok_rows.mean() > 0.999
-    rows = vis.astype(np.int64)
-    for gi, (gname, gp, go, mg) in enumerate(zip(["mean", "log_scale", "quat", "opacity", "sh"],
-                                                 tr.rows_by_group(tr.grad_rows, V), grm.groups(), mags)):
+    for gname, gp, go, mg in zip(["mean", "log_scale", "quat", "opacity", "sh"], _group_rows(tr, V), grm.groups(),
+                                 mags):
         st = assert_grads(gp, go, ok_rows, "grad." + gname, mag=mg)
         _say(name, gname, st)
-    # the chain itself: recompute the loss gradient on the GPU and run backward,
-    # Adam with its staged message, and apply exactly as the benchmark does
-    tr.loss_l1(); tr.raster_bwd(grad2d=False); tr.adam_publish(1, 1); tr.apply()
+    st = assert_grads(tr.grad_norm.cpu().numpy()[vis.astype(np.int64)], grm.grad_norm, ok_rows, "grad_norm",
+                      mag=mag_norm)
+    _say(name, "grad_norm", st)
+
+    # ---- 2. the benchmark's step: fused forward + L1, split backward, Adam staged
+    # as version 1 in ring slot 1, its commit on the second stream
+    tr.status.zero_()
+    tr.step(cam, step=1, version=1, overlap=True)
+    tr.flush_apply()
     torch.cuda.synchronize()
     assert to_u32(tr.status)[0] == 0
-    # primitives that no ambiguous pixel examined take exactly the oracle's chain gradient
-    ok_rows = (ref.flag[vis] == 0) & (ref.proj.clamp_margin[vis] > 1e-5) & (ref.proj.jclamp_margin[vis] > 1e-5)
-
-    # the published message: header and ids bit-exact, rows = the Adam steps
-    msg = tr.msg.cpu().numpy().view(np.uint32)
+    assert int(to_u32(tr.ring_state)[0]) == 1
+    assert int(to_u32(tr.counts[0:1])[0]) == V
+    np.testing.assert_array_equal(to_u32(tr.vis_idx)[:V], vis_o)
+    M = int(to_u32(tr.counts[1:2])[0])
+    assert M == keys_o.size
+    np.testing.assert_array_equal(tr.keys.cpu().numpy()[:M].view(np.uint64), keys_o)
+    np.testing.assert_array_equal(to_u32(tr.vals)[:M], vals_o)
+    T = cam.num_tiles
+    np.testing.assert_array_equal(to_u32(tr.ranges)[:2 * T].reshape(T, 2), ranges_o)
+    np.testing.assert_array_equal(to_u32(tr.tile_order)[:T], expected_tile_order(ranges_o))
+    _say(name, "V=%d M=%d bit-exact" % (V, M))
+    img = tr.img.view(-1)[:3 * H * W].cpu().numpy().reshape(3, H, W)
+    assert_pixels(img, rn.img, np.broadcast_to(~amb, img.shape), "img")
+    fT = tr.final_T.view(-1)[:H * W].cpu().numpy().reshape(H, W)
+    assert_pixels(fT, rn.T_final, ~amb, "final_T")
+    nc = to_u32(tr.n_contrib)[:H * W].reshape(H, W)
+    np.testing.assert_array_equal(nc[~amb], rn.n_contrib[~amb])
+    # the loss gradient: the sign of the GPU image's difference from the target, bit for bit
+    loss_g, dL_g, _ = orc.loss_l1(img, tgt)
+    dL = tr.dL.view(-1)[:3 * H * W].cpu().numpy().reshape(3, H, W)
+    np.testing.assert_array_equal(dL, dL_g.astype(np.float32))
+    assert abs(tr.loss.item() - loss_g) <= 1e-6 * loss_g
+    loss_o, _, _ = orc.loss_l1(rn.img.astype(np.float32), tgt)
+    assert abs(loss_g - loss_o) <= 1e-5 * loss_o
+    # the step's gradient rows against the oracle's backward of the same dL/dimg;
+    # an ambiguous pixel's terms may differ on the two sides (its decisions
+    # may go either way), so each element's bound takes twice the magnitude
+    # of the terms those pixels contribute to it (their sum of |terms| carried
+    # through the chain rule)
+    t0 = time.time()
+    g2, flag, gabs = orc.render_backward(vis_o, pr, cam, dL_g, want_abs=True)
+    gr = orc.project_backward(w.scene, cam, vis_o, g2, pr)
+    mags, _ = orc.gradient_magnitudes(w.scene, cam, vis_o, gabs, pr)
+    _, _, gabs_amb = orc.render_backward(vis_o, pr, cam, np.where(amb[None], dL_g, 0.0), want_abs=True)
+    mags_amb, _ = orc.gradient_magnitudes(w.scene, cam, vis_o, gabs_amb, pr)
+    _say(name, "oracle backward of the step's dL in %.1fs" % (time.time() - t0))
+    g_gpu = _group_rows(tr, V)
+    for gname, gp, go, mg, ma in zip(["mean", "log_scale", "quat", "opacity", "sh"], g_gpu, gr.groups(), mags,
+                                     mags_amb):
+        st = assert_grads(gp, go, ok_rows, "step grad." + gname, mag=mg, slack=2.0 * ma)
+        _say(name, "step", gname, st)
+    # the Adam steps are compared where no ambiguous pixel reached the row
+    sure_rows = ok_rows & (flag[vis] == 0)
+    _say(name, "step rows no ambiguous pixel examined: %d of %d" % (int(sure_rows.sum()), V))
+    # the Adam steps, staged as the message of version 1 in ring slot 1
+    rows = vis.astype(np.int64)
+    p0 = [a.reshape(n, -1) for _, a in w.scene.groups()]
+    lr = w.lr
+    deltas = [orc.adam_rows(p[rows], g, np.zeros_like(g), np.zeros_like(g), 1, lr)[3] for p, g in zip(p0, gr.groups())]
+    msg_o = orc.delta_message(vis_o, [d.astype(np.float32) for d in deltas], 1)
+    msg = tr.msgs[1].cpu().numpy().view(np.uint32)
     head = 8 + 8 + V
-    np.testing.assert_array_equal(msg[:head], ref.msg[:head])
+    np.testing.assert_array_equal(msg[:head], msg_o[:head])
     r0 = (head + 3) // 4 * 4
     rows_gpu = msg[r0:r0 + V * tr.row_len].view(np.float32).reshape(V, tr.row_len)
     offs = np.cumsum([0] + tr.cols)
-    lr = w.lr
-    for gi, (p, d_orc, g_orc, p0) in enumerate(zip(tr.params, ref.deltas, ref.grads.groups(),
-                                                   [a for _, a in w.scene.groups()])):
+    for gi, (p, d_orc, g_orc) in enumerate(zip(tr.params, deltas, gr.groups())):
         d_gpu = rows_gpu[:, offs[gi]:offs[gi + 1]].astype(np.float64)
-        sure = ok_rows[:, None] & (np.abs(g_orc) > grad_floor(g_orc))
+        sure = sure_rows[:, None] & (np.abs(g_orc) > grad_floor(g_orc))
         err = np.abs(d_gpu - d_orc)
         assert np.all(err[sure] <= GRAD_RTOL * lr), (gi, err[sure].max())
         assert np.all(err <= 2 * lr * (1 + GRAD_RTOL)), (gi, err.max())
-        pn = p.cpu().numpy()[rows].astype(np.float64)
-        np.testing.assert_allclose(pn, p0[rows].astype(np.float64) + d_gpu, rtol=0, atol=1e-6 * (1 + np.abs(pn).max()))
-    rows_orc = np.concatenate(ref.deltas, axis=1)
-    assert np.all(np.abs(rows_gpu - rows_orc) <= 2 * lr * (1 + GRAD_RTOL))
-    # the replica received exactly the published rows (one fp32 add each)
-    rep = np.concatenate([r.cpu().numpy()[rows] for r in tr.replica], axis=1)
-    base = np.concatenate([a.reshape(n, -1)[rows] for _, a in w.scene.groups()], axis=1)
-    np.testing.assert_allclose(rep, base.astype(np.float64) + rows_orc, rtol=0, atol=2 * lr * (1 + GRAD_RTOL) + 1e-6)
+        # the parameter moved by exactly the staged step (one fp32 add)
+        pn = p.cpu().numpy()[rows]
+        np.testing.assert_array_equal(pn, (p0[gi][rows] + rows_gpu[:, offs[gi]:offs[gi + 1]]).astype(np.float32))
+    # the replica received exactly the published rows (one fp32 add each) from the overlapped commit
+    for r, gi in zip(tr.replica, range(5)):
+        np.testing.assert_array_equal(r.cpu().numpy()[rows],
+                                      (p0[gi][rows] + rows_gpu[:, offs[gi]:offs[gi + 1]]).astype(np.float32))
     assert np.all(to_u32(tr.version)[rows] == 1)
+    untouched = np.setdiff1d(np.arange(n), rows)[:100000]
+    for r, gi in zip(tr.replica, range(5)):
+        np.testing.assert_array_equal(r.cpu().numpy()[untouched], p0[gi][untouched])
     _say(name, "ok")

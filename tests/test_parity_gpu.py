@@ -10,7 +10,7 @@ import sys
 import numpy as np
 import pytest
 
-from parity_util import assert_grads, assert_pixels, expected_tile_order
+from parity_util import AMB_SHARE, assert_grads, assert_pixels, expected_tile_order
 
 pytestmark = pytest.mark.gpu
 
@@ -92,7 +92,8 @@ def test_project_visible_sort(case, torch_gpu, orc):
         np.testing.assert_array_equal(tr.mean2d.cpu().numpy()[vis].view(np.uint32), ref.mean2d_f32[vis].view(np.uint32))
         co = tr.conic.cpu().numpy()[vis]
         np.testing.assert_array_equal(co[:, :3].view(np.uint32), ref.conic_f32[vis].view(np.uint32))
-        np.testing.assert_allclose(co[:, 3], ref.opacity[vis], rtol=2e-6, atol=1e-7)
+        # the opacity is the fp64 sigmoid rounded once: within half an fp32 ulp
+        np.testing.assert_allclose(co[:, 3], ref.opacity[vis], rtol=2.0 ** -24 * (1 + 1e-9), atol=0)
         rgb = tr.rgb.cpu().numpy()[vis]
         np.testing.assert_allclose(rgb, ref.rgb[vis], rtol=1e-5, atol=2e-6)
         cl = tr.clamp.cpu().numpy()[vis]
@@ -138,19 +139,21 @@ def test_raster_forward(case, torch_gpu, orc):
     rn = orc.render(vis, ref, cam)
     H, W = cam.height, cam.width
     img = tr.img.view(-1)[:3 * H * W].cpu().numpy().reshape(3, H, W)
-    amb = (rn.margin_alpha < orc.AMB_ALPHA) | (rn.margin_T < orc.AMB_T)
+    amb = orc.ambiguous_pixels(rn)
     ok = ~amb
-    frac = amb.mean()
     _say(case, "ambiguous pixels", int(amb.sum()), "of", amb.size)
-    assert frac < 2e-3
+    assert amb.mean() <= AMB_SHARE
     assert_pixels(img, rn.img, np.broadcast_to(ok, img.shape), "img")
     fT = tr.final_T.view(-1)[:H * W].cpu().numpy().reshape(H, W)
     assert_pixels(fT, rn.T_final, ok, "final_T")
     nc = u32(tr.n_contrib)[:H * W].reshape(H, W)
     np.testing.assert_array_equal(nc[ok], rn.n_contrib[ok])
+    # the realized active set: a flag may differ only for a primitive that an
+    # ambiguous pixel examined
     act = tr.active.cpu().numpy()[:w.scene.n]
+    _, flag = orc.render_backward(vis, ref, cam, np.zeros((3, H, W)))
     diff = np.flatnonzero(act != rn.active)
-    assert diff.size <= max(2, int(amb.sum())), diff[:10]
+    assert np.all(flag[diff] & orc.FLAG_AMB_PIXEL), diff[:10]
 
 
 @pytest.mark.parametrize("case", CASES)
@@ -237,6 +240,8 @@ def bwd_compare(w, tr, orc, ref, vis, dL_masked, case):
     gn = tr.grad_norm.cpu().numpy()[rows]
     stats["grad_norm"] = assert_grads(gn, gr.grad_norm, okr, "grad_norm", mag=mag_norm)
     _say(case, {k: (round(v.get("max_rel", 0), 6), round(v.get("norm_rel", 0), 8)) for k, v in stats.items()})
+    _say(case, "elements passing only by the floor / the summation term:",
+         {k: (v.get("need_floor"), v.get("need_sum_term"), v.get("n")) for k, v in stats.items()})
     return gr
 
 
@@ -312,6 +317,16 @@ class _AdamGpu:
                                     step, 0.9, 0.999, 1e-15, version, msg, status)
 
 
+def adam_step_floor(m_old, g, v_new, step, lr, beta1=0.9, beta2=0.999, eps=1e-15):
+    """Per element, the magnitude the fp32 rounding error of an Adam step is
+    relative to: m = b1 m + (1 - b1) g rounds relative to b1 |m| + (1 - b1) |g|
+    (the two terms can cancel), and the step scales m by
+    (lr / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps)."""
+    m_old, g, v_new = (np.asarray(a, np.float64) for a in (m_old, g, v_new))
+    fm = beta1 * np.abs(m_old) + (1 - beta1) * np.abs(g)
+    return lr / (1 - beta1 ** step) * fm / (np.sqrt(v_new / (1 - beta2 ** step)) + eps)
+
+
 def test_sparse_adam(torch_gpu, orc):
     import torch
     cols, p, g, mv, idx, lrs = _adam_case()
@@ -336,7 +351,9 @@ def test_sparse_adam(torch_gpu, orc):
             fv = 0.999 * np.abs(mv[k][1]) + 0.001 * g64 * g64
             assert_grads(m_gpu[k], mr, rows, "m%d" % k, rtol=1e-5, floor=fm)
             assert_grads(v_gpu[k], vr, rows, "v%d" % k, rtol=1e-5, floor=fv)
-            assert_grads(d_gpu[k], dr, np.ones(idx.size, bool), "delta%d" % k, rtol=2e-5)
+            rr = idx.astype(np.int64)
+            assert_grads(d_gpu[k], dr, np.ones(idx.size, bool), "delta%d" % k, rtol=2e-5,
+                         floor=adam_step_floor(mv[k][0][rr], g[k][rr], vr[rr], step, lrs[k]))
             assert_grads(gp, pr, rows, "p%d" % k, rtol=1e-6)
             p[k], mv[k] = pr.astype(np.float32), (mr.astype(np.float32), vr.astype(np.float32))
         # continue from the oracle's state
@@ -368,19 +385,22 @@ def test_sparse_adam_publish(K, torch_gpu, orc):
         assert torch.equal(a.P[k], b.P[k])
     assert torch.equal(a.M, b.M) and torch.equal(a.Vv, b.Vv)
     words = msg.cpu().numpy().view(np.uint32)[:nbytes // 4]
-    deltas = []
+    deltas, floors = [], []
+    rr = idx.astype(np.int64)
     for k in range(5):
-        _, _, _, dr = orc.adam(p[k], g[k], mv[k][0], mv[k][1], idx, 3, lrs[k], 0.9, 0.999, 1e-15)
+        _, _, vr, dr = orc.adam(p[k], g[k], mv[k][0], mv[k][1], idx, 3, lrs[k], 0.9, 0.999, 1e-15)
         full = np.zeros((n, cols[k]))
-        full[idx.astype(np.int64)] = dr
+        full[rr] = dr
         deltas.append(full)
+        floors.append(adam_step_floor(mv[k][0][rr], g[k][rr], vr[rr], 3, lrs[k]))
     ref = orc.delta_pack(idx, deltas, 42)
     head = ref.size - K * row_len
     np.testing.assert_array_equal(words[:head], ref[:head])
     rows_gpu = words[head:].view(np.float32).reshape(K, row_len)
     np.testing.assert_array_equal(rows_gpu, a.D.cpu().numpy()[:K, :row_len])
     rows_orc = np.concatenate([d[idx.astype(np.int64)] for d in deltas], axis=1) if K else np.zeros((0, row_len))
-    assert_grads(rows_gpu.astype(np.float64), rows_orc, np.ones(K, bool), "msg rows", rtol=2e-5)
+    fl = np.concatenate(floors, axis=1) if K else np.zeros((0, row_len))
+    assert_grads(rows_gpu.astype(np.float64), rows_orc, np.ones(K, bool), "msg rows", rtol=2e-5, floor=fl)
     # too small a buffer: nothing is written, the required size is reported
     if K > 0:
         c = _AdamGpu(cols, p, g, mv, idx, lrs)
