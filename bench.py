@@ -18,8 +18,12 @@ Prints one JSON line (the driver's contract) with a roofline entry for the
 dominant kernel (timed with HIP events on the stream it runs on) and the CPU
 oracle timed on a bounded sample of the same workload.  Extras beside it
 (--no-extras skips them): the scope hazards and admission gate between
-consecutive views, two-view task units, and the host planner (graph,
-partition, schedule) on synthetic captures of 1,000 to 50,000 images.
+consecutive views, two-view task units, the host planner (graph,
+partition, schedule) on synthetic captures of 1,000 to 50,000 images, the
+same training step on the other four workloads (short runs: views/s and
+per-phase fractions of peak), the publication kernels alone (pack, apply,
+versioned commit) on the 3M and 10M workloads, and the oracle's per-stage
+times on every workload's view sample.
 """
 from __future__ import annotations
 
@@ -57,6 +61,7 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 # for other workloads and once either source changes.
 TRAFFIC = {
     "kernel": "k_raster_bwd",
+    "phase": "raster_bwd_pixels",
     "workload": "room-1M-L3-1080p",
     "sources": ["paper_2607_19893_amd/csrc/raster.hip", "paper_2607_19893_amd/csrc/binsort.hip"],
     "code_sha256": "edd247363b439b1763bdc96ff07979ed368b352f40eae5aee3197d1cf72cd78c",
@@ -89,10 +94,10 @@ def traffic_digest():
     return code_digest("\n".join(open(os.path.join(ROOT, f)).read() for f in TRAFFIC["sources"]))
 
 
-def traffic_bytes(workload):
+def traffic_bytes(workload, phase):
     """HBM bytes per launch of the dominant kernel on `workload`, or None if the counters were taken on
-    another workload or the code changed since."""
-    if workload != TRAFFIC["workload"]:
+    another workload or kernel, or the code changed since."""
+    if workload != TRAFFIC["workload"] or phase != TRAFFIC["phase"]:
         return None
     try:
         digest = traffic_digest()
@@ -142,35 +147,109 @@ def main():
     if args.copy_probe_mib > 0:
         copy_probe(args.copy_probe_mib)
         return
-    from paper_2607_19893_amd import scenes
-    from paper_2607_19893_amd.pipeline import ViewTrainer, to_u32
+    from paper_2607_19893_amd.pipeline import ViewTrainer
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.apply_after is not None:
+        ViewTrainer.APPLY_AFTER = args.apply_after
+    run = run_workload(args.workload, args.steps, args.warmup, overlap=not args.no_overlap,
+                       packed=not args.dense_params, row_major=args.row_major_tiles)
+    tr, cams, targets, w = run.pop("tr"), run.pop("cams"), run.pop("targets"), run.pop("w")
+
+    extras = {}
+    if not args.no_extras:
+        extras["scope_gate"] = bench_scope_gate(tr, cams, targets, args.steps)
+        extras["unit2"] = bench_unit(tr, cams, targets, args.steps, run["step"])
+        extras["planner"] = bench_planner()
+        log("extras: " + json.dumps(extras))
+    del tr, targets
+    torch.cuda.empty_cache()
+    if not args.no_extras:
+        # every other workload through the same timed step (short runs), and the
+        # publication kernels alone on the two workloads whose step carries them
+        extras["workloads"] = {}
+        extras["delta"] = {}
+        for name in OTHER_WORKLOADS:
+            r = run_workload(name, OTHER_STEPS, OTHER_WARMUP, overlap=not args.no_overlap)
+            if name in DELTA_WORKLOADS:
+                extras["delta"][r["w"].name] = bench_delta(r["tr"], r["cams"])
+            extras["workloads"][r["w"].name] = {k: r[k] for k in ("views_per_s", "ms_per_step", "steps", "views",
+                                                                  "mean_visible", "mean_pairs", "phases_ms",
+                                                                  "phases_frac")}
+            del r
+            torch.cuda.empty_cache()
+        log("workloads: " + json.dumps(extras["workloads"]))
+        log("delta: " + json.dumps(extras["delta"]))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, args.cpu_views)
+        if not args.no_extras:
+            extras["planner"]["oracle"] = planner_oracle_time(PLAN_ORACLE_VIEWS)
+            extras["oracle_stages"] = oracle_stage_times()
+
+    out = {
+        "metric": "train views/sec (fwd+bwd+sparse Adam), 1M Gaussians 1080p",
+        "value": run["views_per_s"],
+        "unit": "views/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": run["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "gaussians": w.scene.n, "sh_degree": w.scene.sh_degree,
+                   "width": cams[0].width, "height": cams[0].height, "views": len(cams),
+                   "mean_visible": run["mean_visible"], "mean_pairs": run["mean_pairs"],
+                   "step": "project+visible+bin_sort+fwd_l1+bwd+sparse_adam_publish+commit",
+                   "apply_overlapped": not args.no_overlap,
+                   "param_layout": "dense" if args.dense_params else "head8",
+                   "tile_dispatch": "row_major" if args.row_major_tiles else "longest_first"},
+        "roofline": run["roofline"],
+        "phases_ms": run["phases_ms"],
+        "phases_frac": run["phases_frac"],
+        "cpu_baseline": cpu,
+        "extras": extras,
+    }
+    print(json.dumps(out), flush=True)
+
+
+# the other workloads of the default run: short timed runs of the same step
+OTHER_WORKLOADS = ("tiny", "ring", "spiral", "aerial")
+OTHER_STEPS, OTHER_WARMUP = 24, 6
+DELTA_WORKLOADS = ("spiral", "aerial")
+
+
+def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False):
+    """Build the workload, make its inputs resident, and time `steps` training
+    views (after `warmup` untimed ones that take the timed path exactly).
+    Returns the throughput, per-phase times and rooflines, and the trainer."""
+    import torch
+    from paper_2607_19893_amd import scenes
+    from paper_2607_19893_amd.pipeline import ViewTrainer, to_u32
     t0 = time.time()
-    w = scenes.workload(args.workload)
+    w = scenes.workload(name)
     cams = w.cameras
     log("workload %s: n=%d, %d views, %dx%d (generated in %.1fs)" % (w.name, w.scene.n, len(cams), cams[0].width,
                                                                      cams[0].height, time.time() - t0))
-    if args.apply_after is not None:
-        ViewTrainer.APPLY_AFTER = args.apply_after
     tr = ViewTrainer(w.scene, capacity=1, max_width=max(c.width for c in cams),
                      max_height=max(c.height for c in cams), lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps,
-                     packed=not args.dense_params)
-    tr.longest_first = not args.row_major_tiles
+                     packed=packed)
+    tr.longest_first = not row_major
     need = tr.ensure_capacity(cams)
     log("pair capacity %d (max pairs over the views %d)" % (tr.capacity, need))
     t0 = time.time()
-    targets = []
-    for i, c in enumerate(cams):
-        tg = torch.from_numpy(w.target(i).reshape(-1)).to(tr.dev)
-        targets.append(tg)
+    targets = [torch.from_numpy(w.target(i).reshape(-1)).to(tr.dev) for i in range(len(cams))]
     log("targets resident (%.1fs)" % (time.time() - t0))
 
     # pair statistics per view (untimed): evaluated / included (pixel, pair) counts
     ev_pairs, inc_pairs, vis_counts, pair_counts, w_iters, w_hits = [], [], [], [], [], []
     front = [in_front(w.scene.mean, c) for c in cams]
-    for i, c in enumerate(cams):
+    for c in cams:
         tr.project(c); tr.visible(); tr.bin_sort()
         tr.pair_stats.zero_()
         tr.raster_fwd(active=False, stats=True)
@@ -183,64 +262,88 @@ def main():
     step = 0
     nviews = len(cams)
     nph = len(ViewTrainer.PHASES)
-    nev = nph + (1 if args.no_overlap else 2)
+    nev = nph + (2 if overlap else 1)
     # the warm-up takes the timed path exactly, timing events included: the
     # runtime's first use of timing events on the two streams costs a one-time
     # stall of tens of milliseconds in a launch, which must not land in the
     # timed region
-    wevs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.warmup)]
-    for k in range(args.warmup):
+    wevs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(warmup)]
+    for k in range(warmup):
         step += 1
-        tr.step(cams[k % nviews], step, version=step, target=targets[k % nviews], events=wevs[k],
-                overlap=not args.no_overlap)
+        tr.step(cams[k % nviews], step, version=step, target=targets[k % nviews], events=wevs[k], overlap=overlap)
     tr.flush_apply()
     torch.cuda.synchronize()
     assert to_u32(tr.status)[0] == 0, "device status flags set during warm-up"
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(steps)]
     views = []
     torch.cuda.synchronize()
     no_collector()
     t_start = time.perf_counter()
-    for k in range(args.steps):
+    for k in range(steps):
         step += 1
-        v = (args.warmup + k) % nviews
+        v = (warmup + k) % nviews
         views.append(v)
-        tr.step(cams[v], step, version=step, target=targets[v], events=evs[k], overlap=not args.no_overlap)
+        tr.step(cams[v], step, version=step, target=targets[v], events=evs[k], overlap=overlap)
     tr.flush_apply()
     t_issued = time.perf_counter()
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     gc.enable()
     wall = t_end - t_start
-    log("host issue time %.3f ms per step (device %.3f ms per step)"
-        % (1e3 * (t_issued - t_start) / args.steps, 1e3 * wall / args.steps))
+    log("%s: host issue time %.3f ms per step (device %.3f ms per step)"
+        % (w.name, 1e3 * (t_issued - t_start) / steps, 1e3 * wall / steps))
     assert to_u32(tr.status)[0] == 0, "device status flags set during the timed steps"
 
     phase_ms = np.zeros(nph)
-    for k in range(args.steps):
+    for k in range(steps):
         for p in range(nph):
-            if p == nph - 1 and not args.no_overlap:
+            if p == nph - 1 and overlap:
                 phase_ms[p] += evs[k][-2].elapsed_time(evs[k][-1])    # the apply, on its own stream
             else:
                 phase_ms[p] += evs[k][p].elapsed_time(evs[k][p + 1])
-    phase_ms /= args.steps
-    log("per-phase ms: " + ", ".join("%s %.3f" % (n, t) for n, t in zip(ViewTrainer.PHASES, phase_ms)))
+    phase_ms /= steps
+    log("%s per-phase ms: " % w.name + ", ".join("%s %.3f" % (n, t) for n, t in zip(ViewTrainer.PHASES, phase_ms)))
 
-    ms_per_step = 1e3 * wall / args.steps
-    value = args.steps / wall
     ev_mean = float(np.mean([ev_pairs[v] for v in views]))
     inc_mean = float(np.mean([inc_pairs[v] for v in views]))
     V_mean = float(np.mean([vis_counts[v] for v in views]))
     M_mean = float(np.mean([pair_counts[v] for v in views]))
-    row_bytes = 4 * tr.row_len
-
-    # roofline of each timed phase; the dominant one is reported
-    names = list(ViewTrainer.PHASES)
-    N = w.scene.n
     F_mean = float(np.mean([front[v] for v in views]))
-    H, Wd = cams[0].height, cams[0].width
-    T_tiles = cams[0].num_tiles
+    roofs = phase_work(tr, w.scene.n, F_mean, V_mean, M_mean, ev_mean, inc_mean, cams[0].num_tiles)
+    names = list(ViewTrainer.PHASES)
+    per_phase = {}
+    for name, t in zip(names, phase_ms):
+        bound, work, peak, unit = roofs[name]
+        ach = work / (t * 1e-3)
+        per_phase[name] = {"ms": round(float(t), 4), "bound": bound, "achieved": round(ach, 2), "peak": peak,
+                           "unit": unit, "frac": round(ach / peak, 4)}
+    # the dominant kernel of the step: the longest phase on the step's stream (an
+    # overlapped apply runs on the second stream, beside the next view's phases)
+    on_path = [n for n in roofs if n != "apply" or not overlap]
+    dom = max(on_path, key=lambda n: phase_ms[names.index(n)])
+    bound, work, peak, unit = roofs[dom]
+    ach = work / (phase_ms[names.index(dom)] * 1e-3)
+    tb = traffic_bytes(w.name, dom)
+    roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
+                "frac": round(ach / peak, 5), "traffic": round(tb) if tb is not None else None}
+    log("%s phase rooflines: " % w.name + json.dumps(per_phase))
+    wi_mean = float(np.mean([w_iters[v] for v in views]))
+    wh_mean = float(np.mean([w_hits[v] for v in views]))
+    log("%s mean per view: V=%.0f M=%.0f evaluated=%.3g included=%.3g; forward (pixel row, pair) steps %.3g, "
+        "with an included pixel %.3g (%.1f%%), included lanes per such step %.1f of 16"
+        % (w.name, V_mean, M_mean, ev_mean, inc_mean, wi_mean, wh_mean, 100 * wh_mean / max(wi_mean, 1),
+           inc_mean / max(wh_mean, 1)))
+    return {"w": w, "tr": tr, "cams": cams, "targets": targets, "step": step,
+            "views_per_s": round(steps / wall, 3), "ms_per_step": round(1e3 * wall / steps, 4), "steps": steps,
+            "views": nviews, "mean_visible": round(V_mean), "mean_pairs": round(M_mean), "roofline": roofline,
+            "phases_ms": {k: v["ms"] for k, v in per_phase.items()},
+            "phases_frac": {k: v["frac"] for k, v in per_phase.items()}}
+
+
+def phase_work(tr, N, F_mean, V_mean, M_mean, ev_mean, inc_mean, T_tiles):
+    """Algorithmic work of each phase per view: (bound, work in GB or TFLOP, peak, unit)."""
+    row_bytes = 4 * tr.row_len
     fwd_flops = FWD_FLOP_EVAL * ev_mean + FWD_FLOP_INC * inc_mean
     bwd_flops = BWD_FLOP_EVAL * ev_mean + BWD_FLOP_INC * inc_mean
     # projection: means of every primitive; log-scale, quaternion of those in
@@ -261,10 +364,10 @@ def main():
     # Adam + staging per visible row: p, g, m, v read and p, m, v written (7 row
     # reads/writes), the message row and id written, the id read
     adam_bytes = V_mean * (8 * row_bytes + 8)
-    # apply per row: message row + id read, replica row read and written, version written
-    apply_bytes = V_mean * (3 * row_bytes + 8)
+    # commit per row: message row + id read, replica row read and written, published version read and written
+    apply_bytes = V_mean * (3 * row_bytes + 12)
     hbm = lambda b: ("hbm", b / 1e9, HBM_PEAK_GBS, "GB/s")
-    roofs = {
+    return {
         "project": hbm(proj_bytes),
         "visible": hbm(vis_bytes),
         "bin_sort": hbm(sort_bytes),
@@ -274,69 +377,89 @@ def main():
         "adam_publish": hbm(adam_bytes),
         "apply": hbm(apply_bytes),
     }
-    per_phase = {}
-    for name, t in zip(names, phase_ms):
-        bound, work, peak, unit = roofs[name]
-        ach = work / (t * 1e-3)
-        per_phase[name] = {"ms": round(float(t), 4), "bound": bound, "achieved": round(ach, 2), "peak": peak,
-                           "unit": unit, "frac": round(ach / peak, 4)}
-    # the dominant kernel of the step: the longest phase on the step's stream (an
-    # overlapped apply runs on the second stream, beside the next view's phases)
-    on_path = [n for n in roofs if n != "apply" or args.no_overlap]
-    dom = max(on_path, key=lambda n: phase_ms[names.index(n)])
-    bound, work, peak, unit = roofs[dom]
-    ach = work / (phase_ms[names.index(dom)] * 1e-3)
-    tb = traffic_bytes(w.name) if dom == "raster_bwd_pixels" else None
-    roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
-                "frac": round(ach / peak, 5), "traffic": round(tb) if tb is not None else None}
-    log("phase rooflines: " + json.dumps(per_phase))
-    wi_mean = float(np.mean([w_iters[v] for v in views]))
-    wh_mean = float(np.mean([w_hits[v] for v in views]))
-    log("mean per view: V=%.0f M=%.0f evaluated=%.3g included=%.3g; forward (pixel row, pair) steps %.3g, "
-        "with an included pixel %.3g (%.1f%%), included lanes per such step %.1f of 16"
-        % (V_mean, M_mean, ev_mean, inc_mean, wi_mean, wh_mean, 100 * wh_mean / max(wi_mean, 1),
-           inc_mean / max(wh_mean, 1)))
 
-    extras = {}
-    if not args.no_extras:
-        extras["scope_gate"] = bench_scope_gate(tr, cams, targets, args.steps)
-        extras["unit2"] = bench_unit(tr, cams, targets, args.steps, step)
-        extras["planner"] = bench_planner()
-        log("extras: " + json.dumps(extras))
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, args.cpu_views)
-        if "planner" in extras:
-            extras["planner"]["oracle"] = planner_oracle_time(PLAN_ORACLE_VIEWS)
+def bench_delta(tr, cams, reps=20):
+    """The publication kernels alone, each launched on all compute units on the
+    current stream: gs_delta_pack of the visible rows' parameters into a
+    message, gs_delta_apply (ADD) of that message into the replica, and the
+    versioned ring commit (gs_publish_commit, foreground) of an Adam message.
+    Rows are those of the last view's visible set; timed with HIP events over
+    `reps` launches each."""
+    import torch
+    from paper_2607_19893_amd import gsmi
+    from paper_2607_19893_amd.pipeline import to_u32
+    tr.project(cams[0]); tr.visible()
+    torch.cuda.synchronize()
+    K = int(to_u32(tr.counts[0:1])[0])
+    P4 = 4 * tr.row_len
+    version = int(to_u32(tr.ring_state)[0])
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
 
-    out = {
-        "metric": "train views/sec (fwd+bwd+sparse Adam), 1M Gaussians 1080p",
-        "value": round(value, 3),
-        "unit": "views/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": w.name, "gaussians": w.scene.n, "sh_degree": w.scene.sh_degree,
-                   "width": cams[0].width, "height": cams[0].height, "views": nviews,
-                   "mean_visible": round(V_mean), "mean_pairs": round(M_mean),
-                   "step": "project+visible+bin_sort+fwd_l1+bwd+sparse_adam_publish+commit",
-                   "apply_overlapped": not args.no_overlap,
-                   "param_layout": "dense" if args.dense_params else "head8",
-                   "tile_dispatch": "row_major" if args.row_major_tiles else "longest_first"},
-        "roofline": roofline,
-        "phases_ms": {k: v["ms"] for k, v in per_phase.items()},
-        "phases_frac": {k: v["frac"] for k, v in per_phase.items()},
-        "cpu_baseline": cpu,
-        "extras": extras,
-    }
-    print(json.dumps(out), flush=True)
+    def timed(fn):
+        fn()                                   # warm-up launch
+        torch.cuda.synchronize()
+        e[0].record()
+        for _ in range(reps):
+            fn()
+        e[1].record()
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / reps
+
+    out = {"rows": K, "row_bytes": P4}
+    # pack: ids read, rows gathered, message (ids + rows) written
+    ms = timed(lambda: tr.pack_params(version))
+    b = 2.0 * K * (4 + P4)
+    out["pack"] = {"ms": round(ms, 4), "gbs": round(b / ms / 1e6, 1), "frac": round(b / ms / 1e6 / HBM_PEAK_GBS, 4)}
+    # apply (ADD, version stamp): message read, replica rows read and written, versions written
+    ms = timed(lambda: tr.apply(gsmi.GS_APPLY_ADD))
+    b = K * (4 + P4) + 2.0 * K * P4 + 4 * K
+    out["apply"] = {"ms": round(ms, 4), "gbs": round(b / ms / 1e6, 1), "frac": round(b / ms / 1e6 / HBM_PEAK_GBS, 4)}
+    # the versioned commit: stage one Adam message per version, commit it
+    # (foreground, all CUs); the staging is outside the timed launches
+    msec = 0.0
+    for r in range(reps):
+        version += 1
+        tr.adam_publish(version, version, tr.msgs[version & 1])
+        torch.cuda.synchronize()
+        e[0].record()
+        tr.commit(version, background=False)
+        e[1].record()
+        torch.cuda.synchronize()
+        msec += e[0].elapsed_time(e[1])
+    ms = msec / reps
+    b = K * (4 + P4) + 2.0 * K * P4 + 8 * K
+    out["commit"] = {"ms": round(ms, 4), "gbs": round(b / ms / 1e6, 1), "frac": round(b / ms / 1e6 / HBM_PEAK_GBS, 4)}
+    assert to_u32(tr.status)[0] == 0, "device status flags set by the publication kernels"
+    return out
+
+
+# the oracle's view sample per workload: every view of the two small
+# workloads, the first two and the last of the others
+ORACLE_STAGE_VIEWS = {"tiny": "all", "ring": "all", "room": (0, 1, -1), "spiral": (0, 1, -1), "aerial": (0, 1, -1)}
+
+
+def oracle_stage_times():
+    """Per-stage wall time of the CPU oracle (as it stands) on each workload's view sample."""
+    import oracle
+    from paper_2607_19893_amd import scenes
+    out = {}
+    for name, sel in ORACLE_STAGE_VIEWS.items():
+        w = scenes.workload(name)
+        views = list(range(len(w.cameras))) if sel == "all" else [v % len(w.cameras) for v in sel]
+        m = [np.zeros_like(a) for _, a in w.scene.groups()]
+        v = [np.zeros_like(a) for _, a in w.scene.groups()]
+        tot = {}
+        t0 = time.perf_counter()
+        for k, i in enumerate(views):
+            r = oracle.train_view(w.scene, w.cameras[i], w.target(i), m, v, k + 1, lr=w.lr)
+            for st, t in r.times.items():
+                tot[st] = tot.get(st, 0.0) + t
+        dt = time.perf_counter() - t0
+        out[w.name] = {"views": views, "s_per_view": {k: round(t / len(views), 4) for k, t in tot.items()},
+                       "views_per_s": round(len(views) / dt, 4), "threads": oracle.num_threads()}
+        log("oracle %s: %s" % (w.name, out[w.name]))
+    return out
 
 
 def bench_scope_gate(tr, cams, targets, steps):
