@@ -384,8 +384,10 @@ def bench_delta(tr, cams, reps=20):
     current stream: gs_delta_pack of the visible rows' parameters into a
     message, gs_delta_apply (ADD) of that message into the replica, and the
     versioned ring commit (gs_publish_commit, foreground) of an Adam message.
-    Rows are those of the last view's visible set; timed with HIP events over
-    `reps` launches each."""
+    Rows are those of view 0's visible set.  Each launch is timed cold, with
+    HIP events around it alone: a 1 GiB fill before it evicts the L2 and the
+    256 MB Infinity Cache, so no launch reads what the previous one left
+    there; the mean over `reps` launches is reported."""
     import torch
     from paper_2607_19893_amd import gsmi
     from paper_2607_19893_amd.pipeline import to_u32
@@ -395,16 +397,22 @@ def bench_delta(tr, cams, reps=20):
     P4 = 4 * tr.row_len
     version = int(to_u32(tr.ring_state)[0])
     e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    evict = torch.empty(1 << 28, dtype=torch.float32, device=tr.dev)
 
-    def timed(fn):
+    def timed(fn, before=None):
         fn()                                   # warm-up launch
         torch.cuda.synchronize()
-        e[0].record()
+        total = 0.0
         for _ in range(reps):
+            if before is not None:
+                before()
+            evict.fill_(1.0)
+            e[0].record()
             fn()
-        e[1].record()
-        torch.cuda.synchronize()
-        return e[0].elapsed_time(e[1]) / reps
+            e[1].record()
+            torch.cuda.synchronize()
+            total += e[0].elapsed_time(e[1])
+        return total / reps
 
     out = {"rows": K, "row_bytes": P4}
     # pack: ids read, rows gathered, message (ids + rows) written
@@ -417,17 +425,17 @@ def bench_delta(tr, cams, reps=20):
     out["apply"] = {"ms": round(ms, 4), "gbs": round(b / ms / 1e6, 1), "frac": round(b / ms / 1e6 / HBM_PEAK_GBS, 4)}
     # the versioned commit: stage one Adam message per version, commit it
     # (foreground, all CUs); the staging is outside the timed launches
-    msec = 0.0
-    for r in range(reps):
-        version += 1
-        tr.adam_publish(version, version, tr.msgs[version & 1])
-        torch.cuda.synchronize()
-        e[0].record()
-        tr.commit(version, background=False)
-        e[1].record()
-        torch.cuda.synchronize()
-        msec += e[0].elapsed_time(e[1])
-    ms = msec / reps
+    ver = [version]
+
+    def stage():
+        ver[0] += 1
+        tr.adam_publish(ver[0], ver[0], tr.msgs[ver[0] & 1])
+
+    def commit():
+        tr.commit(ver[0], background=False)
+
+    stage()
+    ms = timed(commit, before=stage)
     b = K * (4 + P4) + 2.0 * K * P4 + 8 * K
     out["commit"] = {"ms": round(ms, 4), "gbs": round(b / ms / 1e6, 1), "frac": round(b / ms / 1e6 / HBM_PEAK_GBS, 4)}
     assert to_u32(tr.status)[0] == 0, "device status flags set by the publication kernels"

@@ -40,7 +40,10 @@ struct AdamArgs {
     float beta1, beta2, one_m_b1, one_m_b2, sqrt_bc2, eps;
 };
 
-template <bool PUBLISH>
+// UNI (rows of more than 32 floats, one row per wave): the row index and its
+// id are wave-uniform, so the id comes from a scalar load and stays in scalar
+// registers.
+template <bool PUBLISH, bool UNI>
 __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint32_t* __restrict__ idx,
                                                           const uint32_t* __restrict__ count) {
     const uint32_t K = *count;
@@ -98,25 +101,33 @@ __global__ void __launch_bounds__(GS_BLOCK) k_sparse_adam(AdamArgs a, const uint
     float* __restrict__ Mm = a.m;
     float* __restrict__ Vv = a.v;
     const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
-    const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
-    const uint32_t stride = waves * a.rows_per_wave;
-    for (uint32_t r0 = wave * a.rows_per_wave + sub; r0 < K; r0 += kUnroll * stride) {
-        uint32_t id[kUnroll];
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE);
+    const uint32_t rpw = UNI ? 1u : (uint32_t)a.rows_per_wave;
+    const uint32_t stride = waves * rpw;
+    for (uint32_t r0 = wave * rpw + (UNI ? 0u : (uint32_t)sub); r0 < K; r0 += kUnroll * stride) {
+        uint32_t id[kUnroll], rr[kUnroll];
         float gr[kUnroll], mo[kUnroll], vo[kUnroll], po[kUnroll];
+        // loads are unconditional (rows past the end re-read row 0, K >= 1 here)
+        // and all issued before any use
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const uint32_t r = r0 + u * stride;
-            id[u] = r < K ? idx[r] : 0u;
+            rr[u] = r < K ? r : 0u;
+            id[u] = idx[rr[u]];
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const uint32_t r = r0 + u * stride;
-            if (r < K) {
-                gr[u] = G[(size_t)r * a.gld + col];
-                mo[u] = Mm[(size_t)id[u] * a.sld + col];
-                vo[u] = Vv[(size_t)id[u] * a.sld + col];
-                po[u] = P[(size_t)id[u] * pld + c];
-            }
+            gr[u] = G[(size_t)rr[u] * a.gld + col];
+            mo[u] = Mm[(size_t)id[u] * a.sld + col];
+            vo[u] = Vv[(size_t)id[u] * a.sld + col];
+            po[u] = P[(size_t)id[u] * pld + c];
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            loaded(gr[u]);
+            loaded(mo[u]);
+            loaded(vo[u]);
+            loaded(po[u]);
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
@@ -186,8 +197,11 @@ hipError_t launch_sparse_adam(const gs_adam_group* groups, int32_t n_groups, con
     a.d = delta_rows;
     a.dld = delta_ld;
     if (max_rows <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_sparse_adam<false>, dim3(adam_blocks(max_rows, a.rows_per_wave)), dim3(GS_BLOCK), 0, st, a,
-                       idx, count);
+    const dim3 grid(adam_blocks(max_rows, a.rows_per_wave));
+    if (a.rows_per_wave == 1)
+        hipLaunchKernelGGL((k_sparse_adam<false, true>), grid, dim3(GS_BLOCK), 0, st, a, idx, count);
+    else
+        hipLaunchKernelGGL((k_sparse_adam<false, false>), grid, dim3(GS_BLOCK), 0, st, a, idx, count);
     return hipGetLastError();
 }
 
@@ -202,8 +216,11 @@ hipError_t launch_sparse_adam_publish(const gs_adam_group* groups, int32_t n_gro
     a.version = version;
     a.status = status;
     // launched even for max_rows == 0: the (empty) message header is still written
-    hipLaunchKernelGGL(k_sparse_adam<true>, dim3(adam_blocks(max_rows > 0 ? max_rows : 1, a.rows_per_wave)),
-                       dim3(GS_BLOCK), 0, st, a, idx, count);
+    const dim3 grid(adam_blocks(max_rows > 0 ? max_rows : 1, a.rows_per_wave));
+    if (a.rows_per_wave == 1)
+        hipLaunchKernelGGL((k_sparse_adam<true, true>), grid, dim3(GS_BLOCK), 0, st, a, idx, count);
+    else
+        hipLaunchKernelGGL((k_sparse_adam<true, false>), grid, dim3(GS_BLOCK), 0, st, a, idx, count);
     return hipGetLastError();
 }
 

@@ -22,6 +22,15 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 
 __device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
 
+// Pins a loaded value in place: the loads issued before it complete here, and
+// the compiler cannot sink them past it (a kernel that issues the loads of
+// several rows first and then stores them would otherwise get a load moved
+// into each row's store and wait for it there, one row at a time).
+template <typename T>
+__device__ __forceinline__ void loaded(T& v) {
+    asm volatile("" : "+v"(v));
+}
+
 // Inclusive prefix sum over the 64 lanes of a wave.
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
     const int l = lane_id();

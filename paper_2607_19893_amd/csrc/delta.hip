@@ -33,6 +33,12 @@ __device__ __forceinline__ void lane_group(const GroupArgs& a, int lane, int& su
     }
 }
 
+// Rows are taken kRowsInFlight at a time per lane group, with all their loads
+// issued before any store: a row's gather depends on its id, so one row per
+// iteration would leave each wave waiting two memory latencies per row.
+constexpr int kRowsInFlight = 8;
+
+template <bool UNI>
 __global__ void __launch_bounds__(GS_BLOCK) k_pack(GroupArgs a, const uint32_t* __restrict__ idx,
                                                    const uint32_t* __restrict__ count, uint32_t version,
                                                    uint32_t* __restrict__ msg, uint64_t capacity,
@@ -72,12 +78,32 @@ __global__ void __launch_bounds__(GS_BLOCK) k_pack(GroupArgs a, const uint32_t* 
     if (sub >= a.rows_per_wave) return;
     const float* __restrict__ src = a.ptr[grp];
     const int gld = a.ld[grp];
+    const int col = lane - sub * a.row_len;
+    const uint32_t rpw = UNI ? 1u : (uint32_t)a.rows_per_wave;
     const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
-    const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
-    for (uint32_t r = wave * a.rows_per_wave + sub; r < K; r += waves * a.rows_per_wave) {
-        const uint32_t id = idx[r];
-        if (lane - sub * a.row_len == 0) ids[r] = id;
-        rows[(size_t)r * a.row_len + (lane - sub * a.row_len)] = src[(size_t)id * gld + c];
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE);
+    for (uint32_t r0 = wave * rpw * kRowsInFlight; r0 < K; r0 += waves * rpw * kRowsInFlight) {
+        uint32_t rr[kRowsInFlight], id[kRowsInFlight];
+        float val[kRowsInFlight];
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+            const uint32_t r = r0 + (uint32_t)u * rpw + (UNI ? 0u : (uint32_t)sub);
+            rr[u] = r < K ? r : K - 1u;           // past the end: re-read the last row, store nothing
+        }
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) id[u] = idx[rr[u]];
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) val[u] = src[(size_t)id[u] * gld + c];
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) loaded(val[u]);
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+            const uint32_t r = r0 + (uint32_t)u * rpw + (UNI ? 0u : (uint32_t)sub);
+            if (r < K) {
+                if (col == 0) ids[r] = id[u];
+                rows[(size_t)r * a.row_len + col] = val[u];
+            }
+        }
     }
 }
 
@@ -101,6 +127,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_apply_check(GroupArgs a, const uin
     if (bad) atomicOr(&status->flags, GS_DEV_MSG_MISMATCH);
 }
 
+template <bool UNI>
 __global__ void __launch_bounds__(GS_BLOCK) k_apply(GroupArgs a, const uint32_t* __restrict__ msg, int32_t mode,
                                                     uint32_t* __restrict__ prim_version,
                                                     const gs_device_status* __restrict__ status) {
@@ -117,14 +144,38 @@ __global__ void __launch_bounds__(GS_BLOCK) k_apply(GroupArgs a, const uint32_t*
     float* __restrict__ dst = a.ptr[grp];
     const int gld = a.ld[grp];
     const int col = lane - sub * a.row_len;
+    const bool add = mode == GS_APPLY_ADD;
+    const uint32_t rpw = UNI ? 1u : (uint32_t)a.rows_per_wave;
     const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
-    const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
-    for (uint32_t r = wave * a.rows_per_wave + sub; r < K; r += waves * a.rows_per_wave) {
-        const uint32_t id = ids[r];
-        const float val = rows[(size_t)r * a.row_len + col];
-        float* q = dst + (size_t)id * gld + c;
-        *q = (mode == GS_APPLY_ADD) ? (*q + val) : val;
-        if (col == 0 && prim_version) prim_version[id] = version;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE);
+    for (uint32_t r0 = wave * rpw * kRowsInFlight; r0 < K; r0 += waves * rpw * kRowsInFlight) {
+        uint32_t rr[kRowsInFlight], id[kRowsInFlight];
+        float val[kRowsInFlight], old[kRowsInFlight];
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+            const uint32_t r = r0 + (uint32_t)u * rpw + (UNI ? 0u : (uint32_t)sub);
+            rr[u] = r < K ? r : K - 1u;           // past the end: re-read the last row, store nothing
+        }
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+            id[u] = ids[rr[u]];
+            val[u] = rows[(size_t)rr[u] * a.row_len + col];
+        }
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) old[u] = add ? dst[(size_t)id[u] * gld + c] : 0.0f;
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+            loaded(val[u]);
+            loaded(old[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+            const uint32_t r = r0 + (uint32_t)u * rpw + (UNI ? 0u : (uint32_t)sub);
+            if (r < K) {
+                dst[(size_t)id[u] * gld + c] = add ? old[u] + val[u] : val[u];
+                if (col == 0 && prim_version) prim_version[id[u]] = version;
+            }
+        }
     }
 }
 
@@ -139,11 +190,10 @@ __global__ void k_commit_order(const uint32_t* __restrict__ msg, uint32_t versio
     else if (ring_state[0] + 1u != version) atomicOr(&status->flags, GS_DEV_MSG_ORDER);
 }
 
-// Rows are taken kCommitRows at a time per lane group, with all their loads
-// issued before any store, so a wave keeps several independent row gathers
-// in flight (the loads of one row depend only on its id).
-constexpr int kCommitRows = 4;
-
+// UNI (rows of more than 32 floats, one row per wave): the row index and
+// its id are wave-uniform, so the id comes from a scalar load and stays in
+// scalar registers, which leaves room for the rows in flight.
+template <bool UNI>
 __global__ void __launch_bounds__(GS_BLOCK) k_commit(GroupArgs a, const uint32_t* __restrict__ msg, int32_t mode,
                                                      uint32_t* __restrict__ prim_version, uint32_t* __restrict__ skip,
                                                      uint32_t* __restrict__ ring_state,
@@ -162,35 +212,43 @@ __global__ void __launch_bounds__(GS_BLOCK) k_commit(GroupArgs a, const uint32_t
     float* __restrict__ dst = a.ptr[grp];
     const int gld = a.ld[grp];
     const int col = in_row ? lane - sub * a.row_len : 0;
-    const uint32_t rpw = (uint32_t)a.rows_per_wave;
+    const uint32_t rpw = UNI ? 1u : (uint32_t)a.rows_per_wave;
     const uint32_t waves = gridDim.x * (GS_BLOCK / GS_WAVE);
-    const uint32_t wave = blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (GS_BLOCK / GS_WAVE) + threadIdx.x / GS_WAVE);
     uint32_t left = 0;
     // every lane of the wave runs the same number of iterations (rows are
     // strided by whole waves), so the wave-level count below sees all lanes.
     // Loads are unconditional (rows past the end read row 0; every id was
     // checked against n_rows), so they are all in flight before the first use.
-    for (uint32_t r0 = wave * rpw * kCommitRows; r0 < K; r0 += waves * rpw * kCommitRows) {
-        uint32_t rr[kCommitRows], id[kCommitRows], pv[kCommitRows];
-        float val[kCommitRows], old[kCommitRows];
-        bool ok[kCommitRows];
+    for (uint32_t r0 = wave * rpw * kRowsInFlight; r0 < K; r0 += waves * rpw * kRowsInFlight) {
+        uint32_t rr[kRowsInFlight], id[kRowsInFlight], pv[kRowsInFlight], sk[kRowsInFlight];
+        float val[kRowsInFlight], old[kRowsInFlight];
+        bool ok[kRowsInFlight];
 #pragma unroll
-        for (int u = 0; u < kCommitRows; ++u) {
-            const uint32_t r = r0 + (uint32_t)u * rpw + (uint32_t)sub;
+        for (int u = 0; u < kRowsInFlight; ++u) {
+            const uint32_t r = r0 + (uint32_t)u * rpw + (UNI ? 0u : (uint32_t)sub);
             ok[u] = in_row && r < K;
-            rr[u] = ok[u] ? r : 0u;
+            rr[u] = r < K ? r : 0u;
         }
 #pragma unroll
-        for (int u = 0; u < kCommitRows; ++u) id[u] = ids[rr[u]];
+        for (int u = 0; u < kRowsInFlight; ++u) id[u] = ids[rr[u]];
 #pragma unroll
-        for (int u = 0; u < kCommitRows; ++u) {
+        for (int u = 0; u < kRowsInFlight; ++u) {
             // every lane of the row reads the version before lane 0 stamps it
             pv[u] = prim_version[id[u]];
             val[u] = rows[(size_t)rr[u] * a.row_len + col];
             old[u] = dst[(size_t)id[u] * gld + c];
+            sk[u] = skip ? skip[id[u]] : 0u;
         }
 #pragma unroll
-        for (int u = 0; u < kCommitRows; ++u) {
+        for (int u = 0; u < kRowsInFlight; ++u) {
+            loaded(pv[u]);
+            loaded(val[u]);
+            loaded(old[u]);
+            loaded(sk[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
             if (!ok[u]) continue;
             const bool newer = pv[u] < version;
             if (newer) dst[(size_t)id[u] * gld + c] = (mode == GS_APPLY_ADD) ? (old[u] + val[u]) : val[u];
@@ -199,7 +257,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_commit(GroupArgs a, const uint32_t
                     prim_version[id[u]] = version;
                 else
                     ++left;
-                if (skip && skip[id[u]] == version) skip[id[u]] = 0u;
+                if (skip && sk[u] == version) skip[id[u]] = 0u;
             }
         }
     }
@@ -234,10 +292,15 @@ GroupArgs make_group_args(const gs_group* g, int32_t n) {
     return a;
 }
 
-uint32_t row_blocks(int32_t max_rows, int32_t rpw) {
-    if (max_rows <= 0 || rpw <= 0) return 1;
-    uint32_t b = div_up(div_up((uint64_t)max_rows, (uint64_t)rpw), GS_BLOCK / GS_WAVE);
-    return b > 8192 ? 8192 : (b == 0 ? 1 : b);
+// Blocks for a row loop over up to max_rows rows, rows_per_iter rows per wave
+// iteration: enough to cover the rows once, at most 8 resident blocks per
+// compute unit (the loop strides over the rest).
+uint32_t row_blocks(int32_t max_rows, int32_t rows_per_iter) {
+    if (max_rows <= 0 || rows_per_iter <= 0) return 1;
+    uint32_t b = div_up(div_up((uint64_t)max_rows, (uint64_t)rows_per_iter), GS_BLOCK / GS_WAVE);
+    const uint32_t cus = compute_units();
+    const uint32_t cap = cus > 0 ? 8u * cus : 2048u;
+    return b > cap ? cap : (b == 0 ? 1 : b);
 }
 
 }  // namespace
@@ -252,13 +315,17 @@ hipError_t launch_publish_commit(const gs_ring& ring, uint32_t version, const gs
     hipLaunchKernelGGL(k_apply_check, dim3(cb), dim3(GS_BLOCK), 0, st, a, msg, (uint64_t)ring.slot_bytes, n_rows,
                        max_rows, status);
     hipLaunchKernelGGL(k_commit_order, dim3(1), dim3(1), 0, st, msg, version, ring.state, status);
-    uint32_t blocks = row_blocks(max_rows, a.rows_per_wave * kCommitRows);
+    uint32_t blocks = row_blocks(max_rows, a.rows_per_wave * kRowsInFlight);
     if (ring.background) {
         const uint32_t cus = compute_units();
         if (cus > 0 && blocks > cus) blocks = cus;
     }
-    hipLaunchKernelGGL(k_commit, dim3(blocks), dim3(GS_BLOCK), 0, st, a, msg, mode, prim_version, skip, ring.state,
-                       status);
+    if (a.rows_per_wave == 1)
+        hipLaunchKernelGGL(k_commit<true>, dim3(blocks), dim3(GS_BLOCK), 0, st, a, msg, mode, prim_version, skip,
+                           ring.state, status);
+    else
+        hipLaunchKernelGGL(k_commit<false>, dim3(blocks), dim3(GS_BLOCK), 0, st, a, msg, mode, prim_version, skip,
+                           ring.state, status);
     hipLaunchKernelGGL(k_commit_finish, dim3(1), dim3(1), 0, st, msg, version, ring.state, status);
     return hipGetLastError();
 }
@@ -271,8 +338,13 @@ hipError_t launch_delta_pack(const uint32_t* idx, const uint32_t* count, int32_t
                              int32_t n_groups, uint32_t version, void* msg, size_t msg_capacity,
                              gs_device_status* status, hipStream_t st) {
     const GroupArgs a = make_group_args(src, n_groups);
-    hipLaunchKernelGGL(k_pack, dim3(row_blocks(max_rows, a.rows_per_wave)), dim3(GS_BLOCK), 0, st, a, idx, count,
-                       version, static_cast<uint32_t*>(msg), (uint64_t)msg_capacity, status);
+    const dim3 grid(row_blocks(max_rows, a.rows_per_wave * kRowsInFlight));
+    if (a.rows_per_wave == 1)
+        hipLaunchKernelGGL(k_pack<true>, grid, dim3(GS_BLOCK), 0, st, a, idx, count, version,
+                           static_cast<uint32_t*>(msg), (uint64_t)msg_capacity, status);
+    else
+        hipLaunchKernelGGL(k_pack<false>, grid, dim3(GS_BLOCK), 0, st, a, idx, count, version,
+                           static_cast<uint32_t*>(msg), (uint64_t)msg_capacity, status);
     return hipGetLastError();
 }
 
@@ -284,8 +356,13 @@ hipError_t launch_delta_apply(const void* msg, size_t msg_capacity, const gs_gro
     if (cb > 4096) cb = 4096;
     hipLaunchKernelGGL(k_apply_check, dim3(cb), dim3(GS_BLOCK), 0, st, a, static_cast<const uint32_t*>(msg),
                        (uint64_t)msg_capacity, n_rows, max_rows, status);
-    hipLaunchKernelGGL(k_apply, dim3(row_blocks(max_rows, a.rows_per_wave)), dim3(GS_BLOCK), 0, st, a,
-                       static_cast<const uint32_t*>(msg), mode, prim_version, status);
+    const dim3 grid(row_blocks(max_rows, a.rows_per_wave * kRowsInFlight));
+    if (a.rows_per_wave == 1)
+        hipLaunchKernelGGL(k_apply<true>, grid, dim3(GS_BLOCK), 0, st, a, static_cast<const uint32_t*>(msg), mode,
+                           prim_version, status);
+    else
+        hipLaunchKernelGGL(k_apply<false>, grid, dim3(GS_BLOCK), 0, st, a, static_cast<const uint32_t*>(msg), mode,
+                           prim_version, status);
     return hipGetLastError();
 }
 
