@@ -6,8 +6,11 @@ backward, sparse Adam over the visible rows with its steps staged as a
 publication message, and the commit of that message to a replica (the
 pending-update publication).  The workload is the 1M-Gaussian
 SH-degree-3 room scene with 32 forward-facing 1920x1080 cameras; steps cycle
-through the cameras.  Inputs (scene, Adam state, all 32 targets) are resident
-in HBM before the timed region.
+through the cameras.  The primitive pool is stored in spatial (Morton) order
+of the means, a load-time layout step outside the timed region
+(--id-order given keeps the generator's order; the extras time the other
+order too).  Inputs (scene, Adam state, all 32 targets) are resident in HBM
+before the timed region.
 
 Each view's commit to the replica runs on a second stream, started after the
 next view's forward + loss so that it runs beside that view's backward raster
@@ -134,6 +137,9 @@ def main():
     ap.add_argument("--row-major-tiles", action="store_true",
                     help="let the raster workgroups take the tiles in row-major order instead of the bin sort's "
                          "longest-first dispatch order (same results)")
+    ap.add_argument("--id-order", choices=("spatial", "given"), default="spatial",
+                    help="storage order of the primitive pool: spatial (Morton order of the means, a load-time "
+                         "layout step) or given (the generator's order); the scene's content is the same")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy (read + write of this many MiB, 4 times) and exit; "
                          "its HBM counters calibrate the traffic counters of the path's kernels")
@@ -154,7 +160,7 @@ def main():
     if args.apply_after is not None:
         ViewTrainer.APPLY_AFTER = args.apply_after
     run = run_workload(args.workload, args.steps, args.warmup, overlap=not args.no_overlap,
-                       packed=not args.dense_params, row_major=args.row_major_tiles)
+                       packed=not args.dense_params, row_major=args.row_major_tiles, id_order=args.id_order)
     tr, cams, targets, w = run.pop("tr"), run.pop("cams"), run.pop("targets"), run.pop("w")
 
     extras = {}
@@ -166,15 +172,21 @@ def main():
     del tr, targets
     torch.cuda.empty_cache()
     if not args.no_extras:
+        # the same workload with the pool in the other storage order (same step, same views)
+        other = "given" if args.id_order == "spatial" else "spatial"
+        r = run_workload(args.workload, args.steps, args.warmup, overlap=not args.no_overlap, id_order=other)
+        extras["other_id_order"] = {k: r[k] for k in ("id_order", "views_per_s", "ms_per_step", "phases_ms")}
+        del r
+        torch.cuda.empty_cache()
         # every other workload through the same timed step (short runs), and the
         # publication kernels alone on the two workloads whose step carries them
         extras["workloads"] = {}
         extras["delta"] = {}
         for name in OTHER_WORKLOADS:
-            r = run_workload(name, OTHER_STEPS, OTHER_WARMUP, overlap=not args.no_overlap)
+            r = run_workload(name, OTHER_STEPS, OTHER_WARMUP, overlap=not args.no_overlap, id_order=args.id_order)
             if name in DELTA_WORKLOADS:
                 extras["delta"][r["w"].name] = bench_delta(r["tr"], r["cams"])
-            extras["workloads"][r["w"].name] = {k: r[k] for k in ("views_per_s", "ms_per_step", "steps", "views",
+            extras["workloads"][r["w"].name] = {k: r[k] for k in ("id_order", "views_per_s", "ms_per_step", "steps", "views",
                                                                   "mean_visible", "mean_pairs", "phases_ms",
                                                                   "phases_frac")}
             del r
@@ -208,6 +220,7 @@ def main():
                    "step": "project+visible+bin_sort+fwd_l1+bwd+sparse_adam_publish+commit",
                    "apply_overlapped": not args.no_overlap,
                    "param_layout": "dense" if args.dense_params else "head8",
+                   "id_order": args.id_order,
                    "tile_dispatch": "row_major" if args.row_major_tiles else "longest_first"},
         "roofline": run["roofline"],
         "phases_ms": run["phases_ms"],
@@ -224,10 +237,12 @@ OTHER_STEPS, OTHER_WARMUP = 24, 6
 DELTA_WORKLOADS = ("spiral", "aerial")
 
 
-def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False):
-    """Build the workload, make its inputs resident, and time `steps` training
-    views (after `warmup` untimed ones that take the timed path exactly).
-    Returns the throughput, per-phase times and rooflines, and the trainer."""
+def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False, id_order="spatial"):
+    """Build the workload, store its primitives in `id_order` ("spatial": the
+    pool's Morton order; "given": the generator's order), make its inputs
+    resident, and time `steps` training views (after `warmup` untimed ones that
+    take the timed path exactly).  Returns the throughput, per-phase times and
+    rooflines, and the trainer."""
     import torch
     from paper_2607_19893_amd import scenes
     from paper_2607_19893_amd.pipeline import ViewTrainer, to_u32
@@ -236,6 +251,10 @@ def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False
     cams = w.cameras
     log("workload %s: n=%d, %d views, %dx%d (generated in %.1fs)" % (w.name, w.scene.n, len(cams), cams[0].width,
                                                                      cams[0].height, time.time() - t0))
+    if id_order == "spatial":
+        t0 = time.time()
+        w = scenes.spatially_ordered(w)
+        log("primitives stored in spatial (Morton) order (%.1fs)" % (time.time() - t0))
     tr = ViewTrainer(w.scene, capacity=1, max_width=max(c.width for c in cams),
                      max_height=max(c.height for c in cams), lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps,
                      packed=packed)
@@ -334,7 +353,7 @@ def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False
         "with an included pixel %.3g (%.1f%%), included lanes per such step %.1f of 16"
         % (w.name, V_mean, M_mean, ev_mean, inc_mean, wi_mean, wh_mean, 100 * wh_mean / max(wi_mean, 1),
            inc_mean / max(wh_mean, 1)))
-    return {"w": w, "tr": tr, "cams": cams, "targets": targets, "step": step,
+    return {"w": w, "tr": tr, "cams": cams, "targets": targets, "step": step, "id_order": id_order,
             "views_per_s": round(steps / wall, 3), "ms_per_step": round(1e3 * wall / steps, 4), "steps": steps,
             "views": nviews, "mean_visible": round(V_mean), "mean_pairs": round(M_mean), "roofline": roofline,
             "phases_ms": {k: v["ms"] for k, v in per_phase.items()},

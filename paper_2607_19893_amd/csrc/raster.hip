@@ -897,8 +897,15 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
     using L = RowLayout<DEG>;
     constexpr int K = L::K;
     const uint32_t V = *vis_count;
-    if (blockIdx.x * GS_BLOCK >= V) return;
-    const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
+    // Rows in chunks of 16 consecutive ones (neighbouring rows' loads share
+    // cache lines); workgroup b takes chunks b, b + NB, b + 2 NB, ... (NB the
+    // workgroups needed), so a wave's four chunks lie across the whole list.
+    // In a spatially ordered pool the long slot lists of neighbours near the
+    // camera come in runs; taken whole by one wave they would be summed one
+    // after the other while the rest of the chip idles.
+    const uint32_t nb = (V + GS_BLOCK - 1) / GS_BLOCK;
+    if (blockIdx.x >= nb) return;
+    const uint32_t r = ((threadIdx.x >> 4) * nb + blockIdx.x) * 16u + (threadIdx.x & 15u);
     const bool valid = r < V;
     const uint32_t id = valid ? vis_idx[r] : 0u;
     float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};

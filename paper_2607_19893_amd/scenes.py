@@ -84,6 +84,12 @@ class Scene:
     def sh_coeffs(self) -> int:
         return (self.sh_degree + 1) ** 2
 
+    def permuted(self, perm) -> "Scene":
+        """The same primitives stored in another order: row i of the result is row perm[i] of this scene."""
+        perm = np.asarray(perm, np.int64)
+        return Scene(mean=self.mean[perm], log_scale=self.log_scale[perm], quat=self.quat[perm],
+                     opacity=self.opacity[perm], sh=self.sh[perm], sh_degree=self.sh_degree)
+
     def groups(self):
         """Parameter groups in the order used everywhere (name, array [N, cols])."""
         n = self.n
@@ -326,6 +332,57 @@ WORKLOADS = {"tiny": tiny, "ring": ring, "room": room, "spiral": spiral, "aerial
 
 def workload(name: str, **kw) -> Workload:
     return WORKLOADS[name](**kw)
+
+
+def _spread7_table() -> np.ndarray:
+    """For every 7-bit value, its bits moved to bits 0, 3, ..., 18."""
+    t = np.zeros(128, np.uint64)
+    for v in range(128):
+        t[v] = sum(((v >> b) & 1) << (3 * b) for b in range(7))
+    return t
+
+
+_SPREAD7 = _spread7_table()
+
+
+def _spread3(v: np.ndarray) -> np.ndarray:
+    """Bits 0..20 of v moved to bits 0, 3, 6, ..., 60 (uint64), seven bits at a time."""
+    v = np.asarray(v, np.uint32)
+    out = _SPREAD7[v & 127]
+    out |= _SPREAD7[(v >> 7) & 127] << np.uint64(21)
+    out |= _SPREAD7[(v >> 14) & 127] << np.uint64(42)
+    return out
+
+
+def morton_codes(mean: np.ndarray, bits: int = 21) -> np.ndarray:
+    """Z-order (Morton) code of each position: the coordinates quantized to
+    `bits` bits (at most 21) over the points' bounding box, interleaved x, y, z
+    from the lowest bit up."""
+    m = np.asarray(mean, np.float32).reshape(-1, 3)
+    if m.shape[0] == 0:
+        return np.zeros(0, np.uint64)
+    lo, hi = m.min(axis=0).astype(np.float64), m.max(axis=0).astype(np.float64)
+    span = np.where(hi > lo, hi - lo, 1.0)
+    code = np.zeros(m.shape[0], np.uint64)
+    for k in range(3):
+        q = ((m[:, k] - np.float32(lo[k])) * np.float32((2 ** bits - 1) / span[k])).astype(np.int64)
+        q = np.clip(q, 0, 2 ** bits - 1).astype(np.uint32)
+        code |= _spread3(q) << np.uint64(k)
+    return code
+
+
+def spatial_order(mean: np.ndarray) -> np.ndarray:
+    """The storage order that places primitives near each other in space near
+    each other in memory: ascending Morton code of the mean (equal codes keep
+    their given order).  A view's visible set, a region of space, then falls
+    into a few long runs of ids, so every per-primitive gather of the training
+    view reads mostly whole, consecutive cache lines."""
+    return np.argsort(morton_codes(mean), kind="stable")
+
+
+def spatially_ordered(w: Workload) -> Workload:
+    """The workload with its primitives stored in spatial order (same cameras, targets and content)."""
+    return dataclasses.replace(w, scene=w.scene.permuted(spatial_order(w.scene.mean)))
 
 
 def random_scene(seed: int, n: int, degree: int, extent: float = 1.0, ls_mu: float = -2.5,
