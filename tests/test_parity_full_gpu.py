@@ -1,5 +1,6 @@
 """End-to-end parity of one training view at the five full workload sizes
-against the CPU oracle on the same seeded inputs.
+against the CPU oracle on the same seeded inputs, with the pool stored in
+the spatial order the benchmark uses.
 
 Two passes over view 0 of each workload:
 
@@ -54,7 +55,7 @@ def test_full_view(name, orc):
     from paper_2607_19893_amd.pipeline import ViewTrainer, to_u32
     assert torch.cuda.is_available()
     t0 = time.time()
-    w = scenes.workload(name)
+    w = scenes.spatially_ordered(scenes.workload(name))     # the pool in the bench's storage order
     cam = w.cameras[0]
     n = w.scene.n
     H, W = cam.height, cam.width
