@@ -60,16 +60,18 @@ BWD_FLOP_INC = 54.0            # per included pair: transmittance recovery, dL/d
 # size (a 1 GiB read registers as 0.5 GiB of FETCH_SIZE, a 1 GiB write as
 # 1 GiB of WRITE_SIZE).  Valid only for the workload and the code it was
 # measured on (comments aside): the kernel's source and the bin sort, whose
-# tile dispatch order decides what the kernel finds in L2; reported as null
-# for other workloads and once either source changes.
+# tile dispatch order decides what the kernel finds in L2, and the pool's
+# storage order; reported as null for other workloads, another storage order
+# and once either source changes.
 TRAFFIC = {
     "kernel": "k_raster_bwd",
     "phase": "raster_bwd_pixels",
     "workload": "room-1M-L3-1080p",
+    "id_order": "spatial",
     "sources": ["paper_2607_19893_amd/csrc/raster.hip", "paper_2607_19893_amd/csrc/binsort.hip"],
-    "code_sha256": "edd247363b439b1763bdc96ff07979ed368b352f40eae5aee3197d1cf72cd78c",
-    "fetch_kib": 258380.44, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 96876.40, "write_scale": 1048576.0 / 1048576.0,
+    "code_sha256": "f390434199484ee194766c26630a36f721bd2465fb48e146a86d0de3a7b08614",
+    "fetch_kib": 112106.16, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 96733.56, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
@@ -97,10 +99,10 @@ def traffic_digest():
     return code_digest("\n".join(open(os.path.join(ROOT, f)).read() for f in TRAFFIC["sources"]))
 
 
-def traffic_bytes(workload, phase):
+def traffic_bytes(workload, phase, id_order):
     """HBM bytes per launch of the dominant kernel on `workload`, or None if the counters were taken on
-    another workload or kernel, or the code changed since."""
-    if workload != TRAFFIC["workload"] or phase != TRAFFIC["phase"]:
+    another workload, kernel or storage order, or the code changed since."""
+    if workload != TRAFFIC["workload"] or phase != TRAFFIC["phase"] or id_order != TRAFFIC["id_order"]:
         return None
     try:
         digest = traffic_digest()
@@ -343,7 +345,7 @@ def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False
     dom = max(on_path, key=lambda n: phase_ms[names.index(n)])
     bound, work, peak, unit = roofs[dom]
     ach = work / (phase_ms[names.index(dom)] * 1e-3)
-    tb = traffic_bytes(w.name, dom)
+    tb = traffic_bytes(w.name, dom, id_order)
     roofline = {"kernel": dom, "bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
                 "frac": round(ach / peak, 5), "traffic": round(tb) if tb is not None else None}
     log("%s phase rooflines: " % w.name + json.dumps(per_phase))
