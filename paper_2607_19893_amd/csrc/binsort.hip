@@ -4,28 +4,28 @@
 // Instead of one wide radix sort over 64-bit (tile, depth) keys:
 //   1. every visible primitive's tile pairs are emitted in visible-set order
 //      (ascending ids), each primitive's rectangle row-major, so a primitive's
-//      pairs are contiguous ("emission order");
-//   2. the M pairs are sorted by tile id only (ceil(log2 T) bits: 1-2 LSD
-//      passes), carrying each pair's emission position;
-//   3. the tile ranges come from the segment bounds of the sorted keys, and
-//      one stable 8-bit radix pass over a code of each tile's pair count gives
-//      the dispatch order: the longest tiles first;
+//      pairs are contiguous ("emission order"); each emission block also
+//      counts its pairs per tile in LDS and adds the non-zero counts to the
+//      per-tile totals (one device atomic per distinct tile of the block);
+//   2. one workgroup turns the totals into the tile ranges and the dispatch
+//      order (tiles by a code of their pair count, the longest first: a
+//      stable counting sort over 256 codes);
+//   3. the pairs are placed in their tile's range: each block ranks its pairs
+//      per tile in LDS and claims one run of slots per distinct tile from the
+//      tile's cursor (a device atomic), so the order of a tile's pairs inside
+//      its range depends on scheduling;
 //   4. each tile's segment is sorted by (depth bits, emission position) in LDS
 //      by one workgroup (a bitonic network; segments longer than the LDS
 //      capacity are sorted in global memory by the same workgroup), tiles
-//      taken in the dispatch order.  Emission positions grow with the
-//      primitive id inside a tile, so this is exactly the (tile, depth bits,
-//      id) order.
-// Step 4 replaces a 4-pass radix sort of the visible set by depth (12
-// latency-bound launches) with one launch whose work is local to a tile.
+//      taken in the dispatch order.  The key is unique per pair, so the result
+//      does not depend on the order step 3 left; emission positions grow with
+//      the primitive id inside a tile, so this is exactly the (tile, depth
+//      bits, id) order.
 // The per-tile kernels that follow (this sort, the forward and backward
 // raster) end when their longest tile ends; taking the longest first lets
 // the short ones fill in beside it instead of after it.
-//
-// Each LSD pass is three launches: per-block digit histograms (digit-major
-// matrix), a per-digit scan across blocks, and a scatter whose in-block rank
-// comes from a 64-lane match built from ballots; every wave of a block owns a
-// contiguous quarter of the block's keys, so the order is stable.
+#include <algorithm>
+
 #include "common.h"
 #include "internal.h"
 
@@ -33,62 +33,9 @@ namespace gsmi {
 
 namespace {
 
-// Digit widths (8 bits: wider digits cost more per pass in these small,
-// latency-bound launches than the pass they save).  Every kernel takes the
-// digit width as a template parameter; a block holds 2^BITS counters in LDS.
-constexpr int kTileBits = 8;
-// Up to this many 2048-item blocks (32768 tiles: a 4K image has 32400)
-// the tile-order scatter sums its digit offsets itself instead of a scan launch.
-constexpr uint32_t kSelfScanBlocks = 16;
-
-template <int BITS>
-__global__ void __launch_bounds__(GS_BLOCK) k_radix_hist(const uint32_t* __restrict__ keys,
-                                                         const uint32_t* __restrict__ count_ptr, int shift,
-                                                         uint32_t mask, uint32_t* __restrict__ hist,
-                                                         uint32_t nblocks) {
-    constexpr int R = 1 << BITS;
-    __shared__ uint32_t h[R];
-    for (int d = threadIdx.x; d < R; d += GS_BLOCK) h[d] = 0;
-    __syncthreads();
-    const uint32_t cnt = *count_ptr;
-    const uint32_t base = blockIdx.x * GS_TILE_ITEMS;
-    if (base < cnt) {
-#pragma unroll
-        for (int k = 0; k < GS_ITEMS; ++k) {
-            const uint32_t i = base + k * GS_BLOCK + threadIdx.x;
-            if (i < cnt) atomicAdd(&h[(keys[i] >> shift) & mask], 1u);
-        }
-    }
-    __syncthreads();
-    for (int d = threadIdx.x; d < R; d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = h[d];
-}
-
-// One workgroup per digit row: exclusive scan across blocks, row total -> totals[d].
-__global__ void __launch_bounds__(GS_BLOCK) k_radix_scan(uint32_t* __restrict__ hist, uint32_t nblocks,
-                                                         uint32_t* __restrict__ totals) {
-    __shared__ uint32_t scratch[4];
-    uint32_t* row = hist + (size_t)blockIdx.x * nblocks;
-    uint32_t carry = 0;
-    for (uint32_t chunk = 0; chunk < nblocks; chunk += GS_TILE_ITEMS) {
-        const uint32_t base = chunk + threadIdx.x * GS_ITEMS;
-        uint32_t v[GS_ITEMS];
-        uint32_t s = 0;
-#pragma unroll
-        for (int k = 0; k < GS_ITEMS; ++k) {
-            v[k] = (base + k < nblocks) ? row[base + k] : 0u;
-            s += v[k];
-        }
-        uint32_t tot;
-        uint32_t run = block_excl_scan(s, scratch, &tot) + carry;
-#pragma unroll
-        for (int k = 0; k < GS_ITEMS; ++k) {
-            if (base + k < nblocks) row[base + k] = run;
-            run += v[k];
-        }
-        carry += tot;
-    }
-    if (threadIdx.x == 0) totals[blockIdx.x] = carry;
-}
+// Tile counters per LDS histogram pass of the emission and placement blocks
+// (32 KB); images with more tiles take several passes over the block's keys.
+constexpr uint32_t kTileChunk = 8192;
 
 // Lanes of a wave whose digit equals this lane's digit (a 64-lane match built
 // from one ballot per digit bit), restricted to the valid lanes.
@@ -102,127 +49,16 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid, int nbit
     return peers;
 }
 
-// Stable scatter of block b's 2048 keys.  With SELF_SCAN the histogram
-// matrix is the unscanned per-block counts and each block sums its digit
-// offsets from it (for a few blocks: saves the scan launch).  Wave w ranks its own 512 keys
-// (contiguous, 64 per round) against a wave-private running count per digit,
-// so the rounds need no block barrier; one barrier then turns the four
-// waves' digit counts into per-wave offsets.  Position of a key = start of
-// its digit over all blocks + its block's offset (from the scanned matrix) +
-// the keys of earlier waves with that digit + its rank inside its wave.
-template <int BITS, bool SELF_SCAN = false>
-__global__ void __launch_bounds__(GS_BLOCK) k_radix_scatter(
-    const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, uint32_t* __restrict__ keys_out,
-    uint32_t* __restrict__ vals_out, const uint32_t* __restrict__ count_ptr, int shift, uint32_t mask,
-    int nbits, const uint32_t* __restrict__ hist, const uint32_t* __restrict__ totals, uint32_t nblocks) {
-    constexpr int R = 1 << BITS;
-    constexpr int PER = (R + GS_BLOCK - 1) / GS_BLOCK;    // digits per thread in the per-digit steps
-    __shared__ uint32_t s_base[R];
-    __shared__ uint32_t s_wc[4][R];
-    __shared__ uint32_t scratch[4];
-    const uint32_t cnt = *count_ptr;
-    if (blockIdx.x * GS_TILE_ITEMS >= cnt) return;
-    const int tid = threadIdx.x;
-    const int w = tid / GS_WAVE;
-    const int lane = lane_id();
-    // digit starts: exclusive scan of the digit totals, thread t owning digits [t*PER, t*PER+PER)
-    {
-        uint32_t tv[PER], bq[PER];
-        uint32_t sum = 0;
-#pragma unroll
-        for (int q = 0; q < PER; ++q) {
-            const int d = tid * PER + q;
-            if (SELF_SCAN) {
-                uint32_t before = 0, all = 0;
-                if (d < R)
-                    for (uint32_t j = 0; j < nblocks; ++j) {
-                        const uint32_t c = hist[(size_t)d * nblocks + j];
-                        before += j < blockIdx.x ? c : 0u;
-                        all += c;
-                    }
-                tv[q] = all;
-                bq[q] = before;
-            } else {
-                tv[q] = d < R ? totals[d] : 0u;
-            }
-            sum += tv[q];
-        }
-        uint32_t tot;
-        uint32_t run = block_excl_scan(sum, scratch, &tot);
-#pragma unroll
-        for (int q = 0; q < PER; ++q) {
-            const int d = tid * PER + q;
-            if (d < R) {
-                s_base[d] = run + (SELF_SCAN ? bq[q] : hist[(size_t)d * nblocks + blockIdx.x]);
-                s_wc[0][d] = 0; s_wc[1][d] = 0; s_wc[2][d] = 0; s_wc[3][d] = 0;
-            }
-            run += tv[q];
-        }
-    }
-    const uint32_t base = blockIdx.x * GS_TILE_ITEMS + w * (GS_WAVE * GS_ITEMS);
-    uint32_t key[GS_ITEMS], val[GS_ITEMS], rk[GS_ITEMS];
-#pragma unroll
-    for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t i = base + k * GS_WAVE + lane;
-        key[k] = (i < cnt) ? keys_in[i] : 0u;
-        val[k] = (i < cnt) ? (vals_in ? vals_in[i] : i) : 0u;    // no input values: the input position
-    }
-    __syncthreads();
-    const uint64_t lt = lanemask_lt();
-    uint32_t* wc = s_wc[w];
-#pragma unroll
-    for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t i = base + k * GS_WAVE + lane;
-        const bool valid = i < cnt;
-        const uint32_t d = (key[k] >> shift) & mask;
-        const uint64_t peers = match_digit(d, valid, nbits);
-        const uint32_t before = valid ? wc[d] : 0u;
-        rk[k] = before + (uint32_t)popc64(peers & lt);
-        // all reads of this round precede the leaders' updates
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        if (valid && (peers & lt) == 0ull) wc[d] = before + (uint32_t)popc64(peers);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    }
-    __syncthreads();
-    // per digit: offsets of waves 1..3 folded into s_wc (wave 0 takes 0)
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-        const int d = tid * PER + q;
-        if (d < R) {
-            const uint32_t c0 = s_wc[0][d], c1 = s_wc[1][d], c2 = s_wc[2][d];
-            s_wc[0][d] = 0;
-            s_wc[1][d] = c0;
-            s_wc[2][d] = c0 + c1;
-            s_wc[3][d] = c0 + c1 + c2;
-        }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t i = base + k * GS_WAVE + lane;
-        if (i < cnt) {
-            const uint32_t d = (key[k] >> shift) & mask;
-            const uint32_t pos = s_base[d] + wc[d] + rk[k];
-            keys_out[pos] = key[k];
-            vals_out[pos] = val[k];
-        }
-    }
-}
-
 // per-block sums of tiles[] in visible-set order
-// The grid also zeroes the tile ranges (n_ranges words) for the segment
-// bounds written later.
+// The grid also zeroes the per-tile pair totals (T words) that the emission
+// blocks add to.
 __global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restrict__ order,
                                                         const uint32_t* __restrict__ vis_count,
                                                         const uint32_t* __restrict__ tiles,
-                                                        uint32_t* __restrict__ bsum, uint32_t* __restrict__ ranges,
-                                                        uint32_t n_ranges) {
+                                                        uint32_t* __restrict__ bsum, uint32_t* __restrict__ tcount,
+                                                        uint32_t T) {
     __shared__ uint32_t scratch[4];
-    for (uint32_t i = blockIdx.x * GS_BLOCK + threadIdx.x; i < n_ranges; i += gridDim.x * GS_BLOCK) ranges[i] = 0u;
+    for (uint32_t i = blockIdx.x * GS_BLOCK + threadIdx.x; i < T; i += gridDim.x * GS_BLOCK) tcount[i] = 0u;
     const uint32_t V = *vis_count;
     const uint32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x * GS_ITEMS;
     uint32_t s = 0;
@@ -289,18 +125,23 @@ __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
 // successor's offset and is passed over; the offset after the range is taken
 // as +inf).  STAGED: offsets, ids and rectangles are read from the block's LDS
 // copy, else from global memory (g_off, g_order: the range's first rank).
+// Per pair: tile (pkeys), primitive (pvals) and the primitive's depth bits
+// (pdepth); the tile of each of the thread's pairs is also left in key[]
+// (0xFFFFFFFF past hi).
 template <bool STAGED>
 __device__ __forceinline__ void emit_block_pairs(uint32_t base, uint32_t hi, uint32_t nr, const uint32_t* s_off,
                                                  const uint32_t* s_gid, const ushort4* s_rect,
                                                  const uint32_t* __restrict__ g_off,
                                                  const uint32_t* __restrict__ g_order,
                                                  const ushort4* __restrict__ rect, int32_t tiles_x,
-                                                 uint32_t* __restrict__ pkeys, uint32_t* __restrict__ pvals,
-                                                 uint32_t mask0, uint32_t* h) {
+                                                 const float* __restrict__ depth, uint32_t* __restrict__ pkeys,
+                                                 uint32_t* __restrict__ pvals, uint32_t* __restrict__ pdepth,
+                                                 uint32_t (&key)[GS_ITEMS]) {
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) {
         const uint32_t i = base + k * GS_BLOCK + threadIdx.x;
-        if (i >= hi) break;
+        key[k] = 0xFFFFFFFFu;
+        if (i >= hi) continue;
         uint32_t lo = 0, up = nr;
         while (up - lo > 1) {
             const uint32_t mid = (lo + up) >> 1;
@@ -312,10 +153,10 @@ __device__ __forceinline__ void emit_block_pairs(uint32_t base, uint32_t hi, uin
         const uint32_t w = (uint32_t)(rc.z - rc.x);
         const uint32_t ty = rc.y + local / w;
         const uint32_t tx = rc.x + local % w;
-        const uint32_t key = ty * (uint32_t)tiles_x + tx;
-        pkeys[i] = key;
+        key[k] = ty * (uint32_t)tiles_x + tx;
+        pkeys[i] = key[k];
         pvals[i] = gid;
-        atomicAdd(&h[key & mask0], 1u);
+        pdepth[i] = __float_as_uint(depth[gid]);
     }
 }
 
@@ -323,26 +164,24 @@ __device__ __forceinline__ void emit_block_pairs(uint32_t base, uint32_t hi, uin
 // offs_r[r+1] and covers tile number i - offs_r[r] of that primitive's
 // rectangle (row-major).  Each block locates its rank range once, stages the
 // offsets, ids and rectangles of those ranks in LDS and binary-searches
-// there; key (tile id) and value (primitive id) stores are contiguous.  Each
-// block also writes its histogram of the tile sort's first digit (key & mask0)
-// as column b of the digit-major matrix (zeros past the last pair).
+// there; key (tile id) and value (primitive id) stores are contiguous.  Then
+// the block counts its pairs per tile in LDS (the staging memory reused) and
+// adds every non-zero count to the tile's total.
 __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
     const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ offs_r,
-    const uint32_t* __restrict__ bstart, const ushort4* __restrict__ rect, const uint32_t* __restrict__ sort_count,
-    int32_t tiles_x, uint32_t* __restrict__ pkeys, uint32_t* __restrict__ pvals, uint32_t mask0,
-    uint32_t* __restrict__ hist, uint32_t nblocks) {
-    __shared__ uint32_t s_off[GS_TILE_ITEMS + 1];
-    __shared__ uint32_t s_gid[GS_TILE_ITEMS + 1];
-    __shared__ ushort4 s_rect[GS_TILE_ITEMS + 1];
+    const uint32_t* __restrict__ bstart, const ushort4* __restrict__ rect, const float* __restrict__ depth,
+    const uint32_t* __restrict__ sort_count, int32_t tiles_x, uint32_t T, uint32_t* __restrict__ pkeys,
+    uint32_t* __restrict__ pvals, uint32_t* __restrict__ pdepth, uint32_t* __restrict__ tcount) {
+    constexpr uint32_t kStage = GS_TILE_ITEMS + 1;
+    static_assert(kStage * 16 >= kTileChunk * 4, "the tile histogram fits in the staging memory");
+    __shared__ __align__(16) unsigned char s_mem[kStage * 16];
+    ushort4* s_rect = reinterpret_cast<ushort4*>(s_mem);
+    uint32_t* s_off = reinterpret_cast<uint32_t*>(s_mem + kStage * 8);
+    uint32_t* s_gid = reinterpret_cast<uint32_t*>(s_mem + kStage * 12);
     __shared__ uint32_t s_range[2];
-    __shared__ uint32_t h[1 << kTileBits];
-    for (int d = threadIdx.x; d < (1 << kTileBits); d += GS_BLOCK) h[d] = 0;
     const uint32_t M = *sort_count;
     const uint32_t base = blockIdx.x * GS_TILE_ITEMS;
-    if (base >= M) {
-        for (int d = threadIdx.x; d < (1 << kTileBits); d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = 0u;
-        return;
-    }
+    if (base >= M) return;
     const uint32_t hi = min(base + (uint32_t)GS_TILE_ITEMS, M);
     if (threadIdx.x == 0) {
         // the ranks of the block's first and last pairs: the first from the table
@@ -362,7 +201,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
     // caller list with zero-tile ids can span more, and then the block
     // searches the offsets in global memory instead of staging them.
     const uint32_t nr = s_range[1] - r0 + 1;
-    const bool staged = nr <= GS_TILE_ITEMS + 1;
+    const bool staged = nr <= kStage;
     if (staged) {
         for (uint32_t j = threadIdx.x; j < nr; j += GS_BLOCK) {
             const uint32_t g = order[r0 + j];
@@ -372,24 +211,34 @@ __global__ void __launch_bounds__(GS_BLOCK) k_emit_pairs(
         }
     }
     __syncthreads();
+    uint32_t key[GS_ITEMS];
     if (staged)
-        emit_block_pairs<true>(base, hi, nr, s_off, s_gid, s_rect, offs_r + r0, order + r0, rect, tiles_x, pkeys,
-                               pvals, mask0, h);
+        emit_block_pairs<true>(base, hi, nr, s_off, s_gid, s_rect, offs_r + r0, order + r0, rect, tiles_x, depth,
+                               pkeys, pvals, pdepth, key);
     else
-        emit_block_pairs<false>(base, hi, nr, s_off, s_gid, s_rect, offs_r + r0, order + r0, rect, tiles_x, pkeys,
-                                pvals, mask0, h);
-    __syncthreads();
-    for (int d = threadIdx.x; d < (1 << kTileBits); d += GS_BLOCK) hist[(size_t)d * nblocks + blockIdx.x] = h[d];
+        emit_block_pairs<false>(base, hi, nr, s_off, s_gid, s_rect, offs_r + r0, order + r0, rect, tiles_x, depth,
+                                pkeys, pvals, pdepth, key);
+    uint32_t* h = reinterpret_cast<uint32_t*>(s_mem);
+    for (uint32_t c0 = 0; c0 < T; c0 += kTileChunk) {
+        const uint32_t nc = min(kTileChunk, T - c0);
+        __syncthreads();    // the staging (first chunk) or the last chunk's flush is done
+        for (uint32_t d = threadIdx.x; d < nc; d += GS_BLOCK) h[d] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k)
+            if (key[k] - c0 < nc) atomicAdd(&h[key[k] - c0], 1u);
+        __syncthreads();
+        for (uint32_t d = threadIdx.x; d < nc; d += GS_BLOCK) {
+            const uint32_t c = h[d];
+            if (c) atomicAdd(&tcount[c0 + d], c);
+        }
+    }
 }
-
-// Per-tile ordering: LDS capacity in pairs (8 per thread) and the largest key.
-constexpr int kSortCap = GS_TILE_ITEMS;
-constexpr unsigned long long kKeyMax = ~0ull;
 
 // Dispatch key of a tile from its pair count: an 8-bit code that never
 // decreases with the count (exact below 16, then 16 steps per octave; counts
-// of 2^19 and more share the top code), inverted so that an ascending radix
-// pass puts the longest tiles first.
+// of 2^19 and more share the top code), inverted so that ascending keys put
+// the longest tiles first.
 __device__ __forceinline__ uint32_t tile_order_key(uint32_t n) {
     uint32_t code = n;
     if (n >= 16u) {
@@ -399,79 +248,205 @@ __device__ __forceinline__ uint32_t tile_order_key(uint32_t n) {
     return 255u - code;
 }
 
-// Segment bounds of the M tile-sorted pair keys: the pair that opens tile
-// t's segment writes ranges[2t], the pair that closes it ranges[2t+1]; tiles
-// without pairs keep the zeros written before.  Thread i of block b looks at
-// pairs b*2048 + k*256 + i and their neighbours.
-__global__ void __launch_bounds__(GS_BLOCK) k_tile_bounds(const uint32_t* __restrict__ skeys,
-                                                          const uint32_t* __restrict__ sort_count,
-                                                          uint32_t* __restrict__ ranges) {
+// Tiles with fewer pairs than this are depth-sorted by one wave in registers;
+// the order key is monotone in the count, so these are exactly the tiles with
+// keys above kLongKey, and the dispatch order puts all others first.
+constexpr uint32_t kWaveSortMax = 512;
+constexpr uint32_t kLongKey = 255u - 96u;   // tile_order_key(512): code 16 * (9 - 3) + 0
+static_assert(kWaveSortMax == 512u, "kLongKey is the key of 512 pairs");
+
+// Exclusive scan over the 4 waves of a workgroup of GS_BLOCK threads is
+// block_excl_scan.
+
+// Tiles per workgroup of the finishing grid (4 per thread).
+constexpr uint32_t kFinishSeg = 4 * GS_BLOCK;
+
+// From the per-tile totals: the tile ranges (exclusive scan in tile order;
+// [0, 0) for a tile without pairs), the placement cursors (each range's
+// start), the dispatch order (tiles by ascending tile_order_key, equal keys
+// by ascending id) with one record per dispatch position (tile, range start,
+// pair count), and the number of tiles with kWaveSortMax pairs or more, which
+// the order puts first.  Workgroup b owns the tiles [b*kFinishSeg, ..) of one
+// segment.  It reads every total: their sum before the segment starts its
+// ranges, and the key counts over all tiles and over the tiles before the
+// segment give each key's first position for the segment.  Inside the
+// segment, wave w owns a contiguous quarter: it counts its keys, the counts
+// give every (wave, key) its first position, and the wave then places its
+// tiles 64 at a time, each lane ranked among the earlier lanes with its key.
+__global__ void __launch_bounds__(GS_BLOCK) k_tile_finish(const uint32_t* __restrict__ tcount, uint32_t T,
+                                                          uint32_t* __restrict__ ranges,
+                                                          uint32_t* __restrict__ cursor,
+                                                          uint32_t* __restrict__ order, uint4* __restrict__ rec,
+                                                          uint32_t* __restrict__ n_long) {
+    constexpr int kWaves = GS_BLOCK / GS_WAVE;
+    __shared__ uint32_t s_all[256], s_before[256];
+    __shared__ uint32_t s_wc[kWaves][256];
+    __shared__ uint32_t scratch[4];
+    const uint32_t tid = threadIdx.x;
+    const uint32_t w = tid / GS_WAVE;
+    const uint32_t lane = lane_id();
+    const uint32_t lo = blockIdx.x * kFinishSeg, hi = min(lo + kFinishSeg, T);
+    s_all[tid] = 0u;
+    s_before[tid] = 0u;
+    s_wc[0][tid] = 0u; s_wc[1][tid] = 0u; s_wc[2][tid] = 0u; s_wc[3][tid] = 0u;
+    __syncthreads();
+    // every total: key counts over all tiles and before the segment, the pairs before it
+    uint32_t before = 0;
+    for (uint32_t r0 = 0; r0 < T; r0 += GS_BLOCK * GS_ITEMS) {
+        uint32_t c[GS_ITEMS];
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) c[k] = tcount[min(r0 + k * GS_BLOCK + tid, T - 1u)];
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) loaded(c[k]);
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k) {
+            const uint32_t t = r0 + k * GS_BLOCK + tid;
+            if (t < T) {
+                const uint32_t key = tile_order_key(c[k]);
+                atomicAdd(&s_all[key], 1u);
+                if (t < lo) {
+                    atomicAdd(&s_before[key], 1u);
+                    before += c[k];
+                }
+            }
+        }
+    }
+    // the segment: 4 consecutive tiles per thread
+    const uint32_t t0 = lo + tid * 4u;
+    uint32_t c[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) c[k] = t0 + k < hi ? tcount[t0 + k] : 0u;
+    uint32_t tot;
+    const uint32_t pre = block_sum_u32(before, scratch);       // (the block's sum of `before`)
+    uint32_t run = block_excl_scan(c[0] + c[1] + c[2] + c[3], scratch, &tot) + pre;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if (t0 + k < hi) {
+            ranges[2 * (t0 + k)] = c[k] ? run : 0u;
+            ranges[2 * (t0 + k) + 1] = c[k] ? run + c[k] : 0u;
+            cursor[t0 + k] = run;
+        }
+        run += c[k];
+    }
+    // key d (thread d): its first position for the segment
+    {
+        uint32_t ktot;
+        const uint32_t kstart = block_excl_scan(s_all[tid], scratch, &ktot);
+        if (blockIdx.x == 0 && tid == kLongKey + 1u) *n_long = kstart;   // tiles with key <= kLongKey come first
+        s_all[tid] = kstart + s_before[tid];
+    }
+    // per wave: key counts of its quarter of the segment (its lanes' tiles, in order)
+    const uint32_t qlo = lo + w * (kFinishSeg / kWaves);
+    const uint32_t qhi = min(qlo + kFinishSeg / kWaves, hi);
+    uint32_t* wc = s_wc[w];
+    __syncthreads();
+    for (uint32_t t = qlo + lane; t < qhi; t += GS_WAVE) atomicAdd(&wc[tile_order_key(tcount[t])], 1u);
+    __syncthreads();
+    {
+        uint32_t b = s_all[tid];
+        const uint32_t c0 = s_wc[0][tid], c1 = s_wc[1][tid], c2 = s_wc[2][tid];
+        s_wc[0][tid] = b;
+        s_wc[1][tid] = b + c0;
+        s_wc[2][tid] = b + c0 + c1;
+        s_wc[3][tid] = b + c0 + c1 + c2;
+    }
+    __syncthreads();
+    // placement: the quarter's tiles 64 at a time (each tile's range start as
+    // this workgroup wrote it above)
+    const uint64_t lt = lanemask_lt();
+    for (uint32_t b0 = qlo; b0 < qhi; b0 += GS_WAVE) {
+        const uint32_t t = b0 + lane;
+        const bool valid = t < qhi;
+        const uint32_t cnt = valid ? tcount[t] : 0u;
+        const uint32_t sta = valid ? ranges[2 * t] : 0u;
+        const uint32_t key = tile_order_key(cnt);
+        const uint64_t peers = match_digit(key, valid, 8);
+        const uint32_t bw = valid ? wc[key] : 0u;
+        if (valid) {
+            const uint32_t pos = bw + (uint32_t)popc64(peers & lt);
+            order[pos] = t;
+            rec[pos] = make_uint4(t, cnt ? sta : 0u, cnt, 0u);
+        }
+        // all reads of this round precede the leaders' updates
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (valid && (peers & lt) == 0ull) wc[key] = bw + (uint32_t)popc64(peers);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+}
+
+// Placement of the emitted pairs in their tiles' ranges: the block ranks its
+// pairs per tile in LDS, claims one run of slots per distinct tile from the
+// tile's cursor, and writes each pair's depth-sort key at its slot (the depth
+// bits above the emission position) and the pair's primitive beside it.
+__global__ void __launch_bounds__(GS_BLOCK) k_tile_scatter(const uint32_t* __restrict__ pkeys,
+                                                           const uint32_t* __restrict__ pvals,
+                                                           const uint32_t* __restrict__ pdepth,
+                                                           const uint32_t* __restrict__ sort_count, uint32_t T,
+                                                           uint32_t* __restrict__ cursor,
+                                                           unsigned long long* __restrict__ skey,
+                                                           uint32_t* __restrict__ sval) {
+    __shared__ uint32_t h[kTileChunk];
     const uint32_t M = *sort_count;
     const uint32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x;
     if (blockIdx.x * GS_TILE_ITEMS >= M) return;
+    uint32_t key[GS_ITEMS], dep[GS_ITEMS], gid[GS_ITEMS], rk[GS_ITEMS];
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) {
         const uint32_t i = base + k * GS_BLOCK;
-        if (i < M) {
-            const uint32_t t = skeys[i];
-            if (i == 0 || skeys[i - 1] != t) ranges[2 * t] = i;
-            if (i + 1 == M || skeys[i + 1] != t) ranges[2 * t + 1] = i + 1;
-        }
+        key[k] = i < M ? pkeys[i] : 0xFFFFFFFFu;
+        dep[k] = i < M ? pdepth[i] : 0u;
+        gid[k] = i < M ? pvals[i] : 0u;
+        rk[k] = 0u;
     }
-}
-
-// Every tile's dispatch key from its range; block b covers tiles
-// [b*2048, b*2048+2048) and leaves its per-digit key counts in column b of the
-// digit-major histogram matrix that the radix scan reads.
-__global__ void __launch_bounds__(GS_BLOCK) k_tile_keys(const uint32_t* __restrict__ ranges, uint32_t T,
-                                                        uint32_t* __restrict__ tkeys, uint32_t* __restrict__ hist,
-                                                        uint32_t nblocks, uint32_t* __restrict__ tile_count) {
-    static_assert(GS_BLOCK == 256, "one digit counter per thread");
-    __shared__ uint32_t h[256];
-    const uint32_t tid = threadIdx.x;
-    h[tid] = 0;
-    if (blockIdx.x == 0 && tid == 0) *tile_count = T;
-    __syncthreads();
+    for (uint32_t c0 = 0; c0 < T; c0 += kTileChunk) {
+        const uint32_t nc = min(kTileChunk, T - c0);
+        for (uint32_t d = threadIdx.x; d < nc; d += GS_BLOCK) h[d] = 0u;
+        __syncthreads();
 #pragma unroll
-    for (int k = 0; k < GS_ITEMS; ++k) {
-        const uint32_t t = blockIdx.x * GS_TILE_ITEMS + k * GS_BLOCK + tid;
-        if (t < T) {
-            const uint32_t key = tile_order_key(ranges[2 * t + 1] - ranges[2 * t]);
-            tkeys[t] = key;
-            atomicAdd(&h[key], 1u);
+        for (int k = 0; k < GS_ITEMS; ++k)
+            if (key[k] - c0 < nc) rk[k] = atomicAdd(&h[key[k] - c0], 1u);
+        __syncthreads();
+        for (uint32_t d = threadIdx.x; d < nc; d += GS_BLOCK) {
+            const uint32_t c = h[d];
+            if (c) h[d] = atomicAdd(&cursor[c0 + d], c);
         }
-    }
-    __syncthreads();
-    hist[(size_t)tid * nblocks + blockIdx.x] = h[tid];
-}
-
-// Bitonic network over s[0..np) (np a power of two, entries past the data
-// hold kKeyMax), in the variant whose compare-exchanges all put the smaller
-// key at the lower index: each merge of width k first compares i with its
-// mirror i ^ (k - 1), then i with i ^ j for j = k/4 .. 1.
-__device__ __forceinline__ void bitonic_lds(unsigned long long* s, uint32_t np) {
-    for (uint32_t k = 2; k <= np; k <<= 1) {
-        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-            const uint32_t mask = (j == (k >> 1)) ? (k - 1) : j;
-            for (uint32_t c = threadIdx.x; c < (np >> 1); c += GS_BLOCK) {
-                // c-th compare-exchange: lower index i has bit log2(j) clear
-                const uint32_t i = ((c & ~(j - 1)) << 1) | (c & (j - 1));
-                const uint32_t q = i ^ mask;
-                const unsigned long long a = s[i], b = s[q];
-                if (b < a) {
-                    s[i] = b;
-                    s[q] = a;
-                }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < GS_ITEMS; ++k)
+            if (key[k] - c0 < nc) {
+                const uint32_t at = h[key[k] - c0] + rk[k];
+                skey[at] = ((unsigned long long)dep[k] << 32) | (base + k * GS_BLOCK);
+                sval[at] = gid[k];
             }
-            __syncthreads();
-        }
+        __syncthreads();    // before the next chunk clears the counters
     }
 }
 
-// The same network on a segment of global memory of any length n: entries
-// at n and beyond are taken as kKeyMax, so a compare-exchange that reaches
-// past the data leaves the lower (real) entry in place.
-__device__ void bitonic_global(unsigned long long* s, uint32_t n) {
+// Per-tile ordering.  A tile's pairs arrive in its range in any order, each
+// as a 64-bit key (depth bits above the emission position) and the pair's
+// primitive.  The fast paths sort the 32-bit depth bits alone, each with the
+// index of its slot as payload; pairs with equal depth bits (a run of
+// neighbours in that order) are then placed by their emission positions,
+// which gives the order by (depth bits, emission position).  A tile with a
+// run longer than kRunMax (or a depth key equal to the padding value) is
+// sorted again, exactly, on the 64-bit keys.
+constexpr unsigned long long kKeyMax = ~0ull;
+constexpr uint32_t kDepthPad = 0xFFFFFFFFu;
+constexpr uint32_t kRunMax = 64;
+
+// Bitonic network, in the variant whose compare-exchanges all put the smaller
+// key at the lower index: each merge of width k (a power of two) first
+// compares i with its mirror i ^ (k - 1), then i with i ^ j for j = k/4 .. 1.
+
+// The exact network on a segment of global memory of any length n, by a
+// whole workgroup: entries at n and beyond are taken as kKeyMax, so a
+// compare-exchange that reaches past the data leaves the lower (real) entry
+// in place.  Payloads move with their keys.
+__device__ void bitonic_global(unsigned long long* s, uint32_t* pay, uint32_t n) {
     uint32_t np = 1;
     while (np < n) np <<= 1;
     for (uint32_t k = 2; k <= np; k <<= 1) {
@@ -483,8 +458,11 @@ __device__ void bitonic_global(unsigned long long* s, uint32_t n) {
                 if (q >= n) continue;
                 const unsigned long long a = s[i], b = s[q];
                 if (b < a) {
+                    const uint32_t pa = pay[i], pb = pay[q];
                     s[i] = b;
                     s[q] = a;
+                    pay[i] = pb;
+                    pay[q] = pa;
                 }
             }
             __threadfence_block();
@@ -493,65 +471,459 @@ __device__ void bitonic_global(unsigned long long* s, uint32_t n) {
     }
 }
 
-// One workgroup per tile, tiles taken in dispatch order (longest first):
-// order the tile's segment of the tile-sorted pairs by (depth bits, emission
-// position) and write the primitive ids, the sorted -> emission map and the
-// optional 64-bit keys.  pair_emit holds the segment's emission positions on
-// entry (any order).
-__global__ void __launch_bounds__(GS_BLOCK) k_tile_depth_sort(const uint32_t* __restrict__ tile_order,
-                                                              const uint32_t* __restrict__ ranges,
-                                                              const uint32_t* __restrict__ emit_id,
-                                                              const float* __restrict__ depth,
+// LDS accesses of one wave, ordered (no other wave touches the memory).
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Writes sorted pair `at` of tile t: its emission position, primitive id and
+// optional 64-bit key.
+__device__ __forceinline__ void put_sorted(uint32_t t, uint32_t at, unsigned long long k, uint32_t gid,
+                                           uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
+                                           uint64_t* __restrict__ keys64) {
+    vals[at] = gid;
+    pair_emit[at] = (uint32_t)k;
+    if (keys64) keys64[at] = ((uint64_t)t << 32) | (k >> 32);
+}
+
+// The exact network over the n (<= 512) 64-bit keys of a tile by one wave,
+// in the wave's own LDS (sk, sv: 512 entries).
+__device__ void wave_sort_tile64(uint32_t t, uint32_t start, uint32_t n, const unsigned long long* __restrict__ skey,
+                                 const uint32_t* __restrict__ sval, unsigned long long* sk, uint32_t* sv,
+                                 uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
+                                 uint64_t* __restrict__ keys64) {
+    const uint32_t lane = lane_id();
+    uint32_t np = 2;
+    while (np < n) np <<= 1;
+    for (uint32_t i = lane; i < np; i += GS_WAVE) {
+        sk[i] = i < n ? skey[start + i] : kKeyMax;
+        sv[i] = i < n ? sval[start + i] : 0u;
+    }
+    wave_sync();
+    for (uint32_t k = 2; k <= np; k <<= 1) {
+        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+            const uint32_t mask = (j == (k >> 1)) ? (k - 1) : j;
+            for (uint32_t c = lane; c < (np >> 1); c += GS_WAVE) {
+                const uint32_t i = ((c & ~(j - 1)) << 1) | (c & (j - 1));
+                const uint32_t q = i ^ mask;
+                const unsigned long long a = sk[i], b = sk[q];
+                if (b < a) {
+                    const uint32_t pa = sv[i], pb = sv[q];
+                    sk[i] = b;
+                    sk[q] = a;
+                    sv[i] = pb;
+                    sv[q] = pa;
+                }
+            }
+            wave_sync();
+        }
+    }
+    for (uint32_t i = lane; i < n; i += GS_WAVE) put_sorted(t, start + i, sk[i], sv[i], pair_emit, vals, keys64);
+    wave_sync();
+}
+
+// Lane l's value of lane l ^ M: DPP inside rows for the masks 1, 2, 3, 7 and
+// 15, a swizzle inside 32-lane halves for the other masks below 32, a
+// permute for 32 and 63.  Every lane of the wave must be active.
+template <int M>
+__device__ __forceinline__ uint32_t lane_xor(uint32_t v) {
+    if constexpr (M == 1)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);    // quad_perm 1,0,3,2
+    else if constexpr (M == 2)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);    // quad_perm 2,3,0,1
+    else if constexpr (M == 3)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x1B, 0xF, 0xF, false);    // quad_perm 3,2,1,0
+    else if constexpr (M == 7)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);   // row_half_mirror
+    else if constexpr (M == 15)
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);   // row_mirror
+    else if constexpr (M < 32)
+        return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (M << 10) | 0x1F);            // and 31, xor M
+    else
+        return __shfl_xor(v, M, GS_WAVE);
+}
+
+// Compare-exchange inside a lane: the smaller key (and its payload) to a.
+__device__ __forceinline__ void cmpx32(uint32_t& a, uint32_t& pa, uint32_t& b, uint32_t& pb) {
+    const bool sw = b < a;
+    const uint32_t lo = sw ? b : a, hi = sw ? a : b, plo = sw ? pb : pa, phi = sw ? pa : pb;
+    a = lo;
+    b = hi;
+    pa = plo;
+    pb = phi;
+}
+
+// One side of a step across lanes or waves: the lower side keeps the
+// smaller key, the upper side the larger.
+__device__ __forceinline__ void keep32(uint32_t& v, uint32_t& p, uint32_t o, uint32_t op, bool lower) {
+    const bool take = lower ? (o < v) : (v < o);
+    v = take ? o : v;
+    p = take ? op : p;
+}
+
+// The network on the 64 K keys of one wave in registers: element i = lane * K
+// + r sits in register r of its lane, so a step at distance below K stays
+// inside a lane and one at a larger distance pairs lane l with lane l ^
+// (distance / K), same register.
+
+// Steps i against i ^ j for j = J, J/2, .. 1.
+template <int K, int J>
+__device__ __forceinline__ void tail32(uint32_t (&v)[K], uint32_t (&p)[K], uint32_t lane) {
+    if constexpr (J > 0) {
+        if constexpr (J < K) {
+#pragma unroll
+            for (int r = 0; r < K; ++r)
+                if ((r & J) == 0) cmpx32(v[r], p[r], v[r | J], p[r | J]);
+        } else {
+            const bool lower = (lane & (uint32_t)(J / K)) == 0;
+#pragma unroll
+            for (int r = 0; r < K; ++r) keep32(v[r], p[r], lane_xor<J / K>(v[r]), lane_xor<J / K>(p[r]), lower);
+        }
+        tail32<K, J / 2>(v, p, lane);
+    }
+}
+
+// Mirror step of a merge of width KK: i against i ^ (KK - 1).
+template <int K, int KK>
+__device__ __forceinline__ void mirror32(uint32_t (&v)[K], uint32_t (&p)[K], uint32_t lane) {
+    if constexpr (KK <= K) {
+#pragma unroll
+        for (int r = 0; r < K; ++r)
+            if ((r & (KK / 2)) == 0) cmpx32(v[r], p[r], v[r ^ (KK - 1)], p[r ^ (KK - 1)]);
+    } else {
+        const bool lower = (lane & (uint32_t)(KK / K / 2)) == 0;
+        uint32_t o[K], op[K];
+#pragma unroll
+        for (int r = 0; r < K; ++r) {
+            o[r] = lane_xor<KK / K - 1>(v[r ^ (K - 1)]);
+            op[r] = lane_xor<KK / K - 1>(p[r ^ (K - 1)]);
+        }
+#pragma unroll
+        for (int r = 0; r < K; ++r) keep32(v[r], p[r], o[r], op[r], lower);
+    }
+}
+
+// Merges of width 2 .. KK: every block of KK elements ascending.
+template <int K, int KK>
+__device__ __forceinline__ void net32(uint32_t (&v)[K], uint32_t (&p)[K], uint32_t lane) {
+    if constexpr (KK >= 2) {
+        net32<K, KK / 2>(v, p, lane);
+        mirror32<K, KK>(v, p, lane);
+        tail32<K, KK / 4>(v, p, lane);
+    }
+}
+
+// Depth bits and emission position of key i (its high and low words).
+__device__ __forceinline__ uint32_t key_depth(const unsigned long long* __restrict__ skey, uint32_t i) {
+    return reinterpret_cast<const uint32_t*>(skey)[2 * (size_t)i + 1];
+}
+__device__ __forceinline__ uint32_t key_emit(const unsigned long long* __restrict__ skey, uint32_t i) {
+    return reinterpret_cast<const uint32_t*>(skey)[2 * (size_t)i];
+}
+
+// Writes the pairs of a tile sorted by depth bits: sorted pair i is slot p.
+__device__ __forceinline__ void put_by_slot(uint32_t t, uint32_t start, uint32_t i, uint32_t depth, uint32_t p,
+                                            const unsigned long long* __restrict__ skey,
+                                            const uint32_t* __restrict__ sval, uint32_t* __restrict__ pair_emit,
+                                            uint32_t* __restrict__ vals, uint64_t* __restrict__ keys64) {
+    put_sorted(t, start + i, ((unsigned long long)depth << 32) | key_emit(skey, start + p), sval[start + p], pair_emit,
+               vals, keys64);
+}
+
+// Runs of equal depth bits.  sk[0..n) holds a tile's keys in the order of
+// their depth bits (ties in any order), sv their primitives.  long_run: some
+// run is longer than kRunMax (then entry i and entry i - kRunMax share their
+// depth bits).  place_runs writes sorted pair i for i = first, first + step,
+// ..: an entry outside a run stays at i; one inside a run [a, b) goes to a +
+// the number of the run's entries with a smaller key (emission position).
+__device__ __forceinline__ uint32_t hi32(unsigned long long k) { return (uint32_t)(k >> 32); }
+
+__device__ __forceinline__ bool long_run(const unsigned long long* sk, uint32_t n, uint32_t first, uint32_t step) {
+    bool bad = false;
+    for (uint32_t i = first + kRunMax; i < n; i += step) bad |= hi32(sk[i]) == hi32(sk[i - kRunMax]);
+    return bad;
+}
+
+__device__ __forceinline__ void place_runs(uint32_t t, uint32_t start, uint32_t n, const unsigned long long* sk,
+                                           const uint32_t* sv, uint32_t first, uint32_t step,
+                                           uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
+                                           uint64_t* __restrict__ keys64) {
+    for (uint32_t i = first; i < n; i += step) {
+        const unsigned long long k = sk[i];
+        const uint32_t d = hi32(k);
+        uint32_t a = i, b = i + 1;
+        while (a > 0 && hi32(sk[a - 1]) == d) --a;
+        while (b < n && hi32(sk[b]) == d) ++b;
+        uint32_t at = a;
+        for (uint32_t j = a; j < b; ++j) at += sk[j] < k ? 1u : 0u;
+        put_sorted(t, start + at, k, sv[i], pair_emit, vals, keys64);
+    }
+}
+
+// One wave sorts the n (<= 64 K) pairs of one tile: the fast path in
+// registers, else wave_sort_tile64 in the wave's LDS.
+template <int K>
+__device__ __forceinline__ void wave_sort_tile(uint32_t t, uint32_t start, uint32_t n,
+                                               const unsigned long long* __restrict__ skey,
+                                               const uint32_t* __restrict__ sval, unsigned long long* sk, uint32_t* sv,
+                                               uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
+                                               uint64_t* __restrict__ keys64) {
+    const uint32_t lane = lane_id();
+    uint32_t v[K], p[K];
+    bool odd = false;
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+        const uint32_t i = lane * K + r;
+        v[r] = i < n ? key_depth(skey, start + i) : kDepthPad;
+        p[r] = i;
+        odd |= i < n && v[r] == kDepthPad;
+    }
+    bool tie = false;
+    if (__ballot(odd) == 0ull) {
+        net32<K, GS_WAVE * K>(v, p, lane);
+        // equal neighbours in the sorted order: i and i + 1 < n
+#pragma unroll
+        for (int r = 0; r + 1 < K; ++r) tie |= lane * K + r + 1 < n && v[r] == v[r + 1];
+        const uint32_t next = __shfl_down(v[0], 1, GS_WAVE);
+        tie |= lane + 1 < GS_WAVE && (lane + 1) * K < n && v[K - 1] == next;
+    }
+    if (__ballot(odd) != 0ull) {
+        wave_sort_tile64(t, start, n, skey, sval, sk, sv, pair_emit, vals, keys64);
+        return;
+    }
+    if (__ballot(tie) == 0ull) {
+#pragma unroll
+        for (int r = 0; r < K; ++r)
+            if (lane * K + r < n) put_by_slot(t, start, lane * K + r, v[r], p[r], skey, sval, pair_emit, vals, keys64);
+        return;
+    }
+    // equal depth bits: the sorted keys to LDS, then each run placed by emission position
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+        const uint32_t i = lane * K + r;
+        if (i < n) {
+            sk[i] = ((unsigned long long)v[r] << 32) | key_emit(skey, start + p[r]);
+            sv[i] = sval[start + p[r]];
+        }
+    }
+    wave_sync();
+    if (__ballot(long_run(sk, n, lane, GS_WAVE)) != 0ull) {
+        wave_sync();
+        wave_sort_tile64(t, start, n, skey, sval, sk, sv, pair_emit, vals, keys64);
+        return;
+    }
+    place_runs(t, start, n, sk, sv, lane, GS_WAVE, pair_emit, vals, keys64);
+    wave_sync();
+}
+
+// Long tiles: kWaveSortMax .. kLongCap pairs are sorted by the workgroup's
+// waves in registers, kWaveSortMax keys each; merges wider than one wave take
+// their cross-wave steps through LDS.  Longer tiles take the exact network in
+// global memory.
+constexpr int kSortWaves = GS_BLOCK / GS_WAVE;
+constexpr uint32_t kLongCap = kSortWaves * kWaveSortMax;
+constexpr int kLongK = (int)kWaveSortMax / GS_WAVE;     // keys per lane
+// Workgroups per compute unit of the persistent depth-sort grid.
+constexpr uint32_t kDepthSortBlocksPerCU = 8;
+
+// The exact network over the n (<= kLongCap) 64-bit keys of a tile by the
+// whole workgroup in LDS.
+__device__ void block_sort_tile64(uint32_t t, uint32_t start, uint32_t n, const unsigned long long* __restrict__ skey,
+                                  const uint32_t* __restrict__ sval, unsigned long long* sk, uint32_t* sv,
+                                  uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
+                                  uint64_t* __restrict__ keys64) {
+    uint32_t np = 2;
+    while (np < n) np <<= 1;
+    for (uint32_t i = threadIdx.x; i < np; i += GS_BLOCK) {
+        sk[i] = i < n ? skey[start + i] : kKeyMax;
+        sv[i] = i < n ? sval[start + i] : 0u;
+    }
+    __syncthreads();
+    for (uint32_t k = 2; k <= np; k <<= 1) {
+        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+            const uint32_t mask = (j == (k >> 1)) ? (k - 1) : j;
+            for (uint32_t c = threadIdx.x; c < (np >> 1); c += GS_BLOCK) {
+                const uint32_t i = ((c & ~(j - 1)) << 1) | (c & (j - 1));
+                const uint32_t q = i ^ mask;
+                const unsigned long long a = sk[i], b = sk[q];
+                if (b < a) {
+                    const uint32_t pa = sv[i], pb = sv[q];
+                    sk[i] = b;
+                    sk[q] = a;
+                    sv[i] = pb;
+                    sv[q] = pa;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (uint32_t i = threadIdx.x; i < n; i += GS_BLOCK) put_sorted(t, start + i, sk[i], sv[i], pair_emit, vals, keys64);
+    __syncthreads();
+}
+
+// A tile by the whole workgroup, exactly, in place in global memory.
+__device__ void sort_huge_tile(uint32_t t, uint32_t start, uint32_t n, unsigned long long* __restrict__ skey,
+                               uint32_t* __restrict__ sval, uint32_t* __restrict__ pair_emit,
+                               uint32_t* __restrict__ vals, uint64_t* __restrict__ keys64) {
+    unsigned long long* key = skey + start;
+    uint32_t* val = sval + start;
+    bitonic_global(key, val, n);
+    for (uint32_t i = threadIdx.x; i < n; i += GS_BLOCK) put_sorted(t, start + i, key[i], val[i], pair_emit, vals, keys64);
+}
+
+// One cross-wave step of a long tile: element i (register r of lane l of
+// wave w, i = w * 512 + l * 8 + r) against element i ^ mask.  Key and slot
+// go through LDS as one word pair, r-major (address r * 256 + i / 8), so the
+// lanes of one access touch consecutive words.
+__device__ __forceinline__ void long_exchange(uint32_t (&v)[kLongK], uint32_t (&p)[kLongK], bool act, uint32_t ibase,
+                                              uint32_t mask, unsigned long long* s_kv) {
+    constexpr uint32_t kStride = kLongCap / kLongK;
+    const uint32_t hb = 1u << (31 - __clz(mask));          // the highest bit of mask decides the side
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < kLongK; ++r) s_kv[r * kStride + (ibase >> 3)] = ((unsigned long long)p[r] << 32) | v[r];
+    }
+    __syncthreads();
+    if (act) {
+        const bool lower = (ibase & hb) == 0;              // hb >= 512 > r: one side for all r
+#pragma unroll
+        for (int r = 0; r < kLongK; ++r) {
+            const uint32_t q = (ibase + r) ^ mask;
+            const unsigned long long kv = s_kv[(q & 7u) * kStride + (q >> 3)];
+            keep32(v[r], p[r], (uint32_t)kv, (uint32_t)(kv >> 32), lower);
+        }
+    }
+    __syncthreads();
+}
+
+// A long tile (n in [kWaveSortMax, kLongCap]) by the whole workgroup.
+__device__ void sort_long_tile(uint32_t t, uint32_t start, uint32_t n, unsigned long long* __restrict__ skey,
+                               uint32_t* __restrict__ sval, unsigned long long* s_kv, uint32_t* s_v,
+                               uint32_t* s_first, uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
+                               uint64_t* __restrict__ keys64) {
+    const uint32_t w = threadIdx.x / GS_WAVE, lane = lane_id();
+    uint32_t np = kWaveSortMax;
+    while (np < n) np <<= 1;
+    const bool act = w < np / kWaveSortMax;
+    const uint32_t ibase = w * kWaveSortMax + lane * kLongK;
+    uint32_t v[kLongK], p[kLongK];
+    bool odd = false;
+#pragma unroll
+    for (int r = 0; r < kLongK; ++r) {
+        const uint32_t i = ibase + r;
+        v[r] = act && i < n ? key_depth(skey, start + i) : kDepthPad;
+        p[r] = i;
+        odd |= act && i < n && v[r] == kDepthPad;
+    }
+    if (__syncthreads_or(odd)) {
+        block_sort_tile64(t, start, n, skey, sval, s_kv, s_v, pair_emit, vals, keys64);
+        return;
+    }
+    if (act) net32<kLongK, (int)kWaveSortMax>(v, p, lane);
+    for (uint32_t kk = 2 * kWaveSortMax; kk <= np; kk <<= 1) {
+        long_exchange(v, p, act, ibase, kk - 1, s_kv);
+        for (uint32_t j = kk >> 2; j >= kWaveSortMax; j >>= 1) long_exchange(v, p, act, ibase, j, s_kv);
+        if (act) tail32<kLongK, (int)kWaveSortMax / 2>(v, p, lane);
+    }
+    // equal neighbours: inside a lane, to the next lane, to the next wave
+    if (act && lane == 0) s_first[w] = v[0];
+    __syncthreads();
+    bool tie = false;
+    if (act) {
+#pragma unroll
+        for (int r = 0; r + 1 < kLongK; ++r) tie |= ibase + r + 1 < n && v[r] == v[r + 1];
+        const uint32_t next = __shfl_down(v[0], 1, GS_WAVE);
+        if (lane + 1 < GS_WAVE)
+            tie |= ibase + kLongK < n && v[kLongK - 1] == next;
+        else if (w + 1 < np / kWaveSortMax)
+            tie |= ibase + kLongK < n && v[kLongK - 1] == s_first[w + 1];
+    }
+    if (!__syncthreads_or(tie)) {
+        if (act) {
+#pragma unroll
+            for (int r = 0; r < kLongK; ++r)
+                if (ibase + r < n) put_by_slot(t, start, ibase + r, v[r], p[r], skey, sval, pair_emit, vals, keys64);
+        }
+        return;
+    }
+    // equal depth bits: the sorted keys to LDS, then each run placed by emission position
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < kLongK; ++r) {
+            const uint32_t i = ibase + r;
+            if (i < n) {
+                s_kv[i] = ((unsigned long long)v[r] << 32) | key_emit(skey, start + p[r]);
+                s_v[i] = sval[start + p[r]];
+            }
+        }
+    }
+    __syncthreads();
+    if (__syncthreads_or(long_run(s_kv, n, threadIdx.x, GS_BLOCK))) {
+        block_sort_tile64(t, start, n, skey, sval, s_kv, s_v, pair_emit, vals, keys64);
+        return;
+    }
+    place_runs(t, start, n, s_kv, s_v, threadIdx.x, GS_BLOCK, pair_emit, vals, keys64);
+    __syncthreads();
+}
+
+// Per-tile depth sort, a persistent grid over the dispatch records.  The
+// first n_long records (kWaveSortMax pairs or more) go to whole workgroups,
+// records b, b + G, .. to workgroup b; then every wave takes the remaining
+// records from the shortest up, records T-1-s for s = 4b + w, 4b + w + 4G, ..
+// Output: the tiles' pairs ordered by (depth bits, emission position), with
+// the primitive ids, the sorted -> emission map and the optional 64-bit keys.
+__global__ void __launch_bounds__(GS_BLOCK) k_tile_depth_sort(const uint4* __restrict__ rec,
+                                                              const uint32_t* __restrict__ n_long_ptr, uint32_t T,
+                                                              unsigned long long* __restrict__ skey,
+                                                              uint32_t* __restrict__ sval,
                                                               uint32_t* __restrict__ pair_emit,
                                                               uint32_t* __restrict__ vals,
-                                                              uint64_t* __restrict__ keys64,
-                                                              unsigned long long* __restrict__ scratch) {
-    __shared__ unsigned long long s_key[kSortCap];
-    const uint32_t t = tile_order[blockIdx.x];
-    const uint32_t start = ranges[2 * t], end = ranges[2 * t + 1];
-    const uint32_t n = end - start;
-    if (n == 0) return;
-    unsigned long long* key = s_key;
-    if (n <= (uint32_t)kSortCap) {
-        uint32_t np = 2;
-        while (np < n) np <<= 1;
-        for (uint32_t i = threadIdx.x; i < np; i += GS_BLOCK) {
-            unsigned long long k = kKeyMax;
-            if (i < n) {
-                const uint32_t e = pair_emit[start + i];
-                k = ((unsigned long long)__float_as_uint(depth[emit_id[e]]) << 32) | e;
-            }
-            s_key[i] = k;
-        }
-        __syncthreads();
-        bitonic_lds(s_key, np);
-    } else {
-        key = scratch + start;
-        for (uint32_t i = threadIdx.x; i < n; i += GS_BLOCK) {
-            const uint32_t e = pair_emit[start + i];
-            key[i] = ((unsigned long long)__float_as_uint(depth[emit_id[e]]) << 32) | e;
-        }
-        __threadfence_block();
-        __syncthreads();
-        bitonic_global(key, n);
+                                                              uint64_t* __restrict__ keys64) {
+    __shared__ unsigned long long s_kv[kLongCap];      // long tiles; a 512-entry quarter per wave otherwise
+    __shared__ uint32_t s_v[kLongCap];
+    __shared__ uint32_t s_first[kSortWaves];
+    const uint32_t G = gridDim.x;                             // <= T
+    const uint32_t w = threadIdx.x / GS_WAVE;
+    const uint32_t s0 = blockIdx.x * kSortWaves + w;
+    // the first records of the block and of the wave load beside the count
+    uint4 rl = rec[blockIdx.x];
+    uint4 rs = rec[T - 1u - min(s0, T - 1u)];
+    const uint32_t n_long = *n_long_ptr;
+    for (uint32_t pos = blockIdx.x; pos < n_long; pos += G) {
+        if (pos != blockIdx.x) rl = rec[pos];
+        if (rl.z <= kLongCap)
+            sort_long_tile(rl.x, rl.y, rl.z, skey, sval, s_kv, s_v, s_first, pair_emit, vals, keys64);
+        else
+            sort_huge_tile(rl.x, rl.y, rl.z, skey, sval, pair_emit, vals, keys64);
     }
-    for (uint32_t i = threadIdx.x; i < n; i += GS_BLOCK) {
-        const unsigned long long k = key[i];
-        const uint32_t e = (uint32_t)k;
-        vals[start + i] = emit_id[e];
-        pair_emit[start + i] = e;
-        if (keys64) keys64[start + i] = ((uint64_t)t << 32) | (k >> 32);
+    unsigned long long* sk = s_kv + w * kWaveSortMax;
+    uint32_t* sv = s_v + w * kWaveSortMax;
+    for (uint32_t s = s0; s < T - n_long; s += kSortWaves * G) {
+        if (s != s0) rs = rec[T - 1u - s];
+        const uint32_t t = rs.x, start = rs.y, n = rs.z;
+        if (n == 0u || n >= kWaveSortMax) continue;     // (the order puts every longer tile first)
+        if (n <= 64u)
+            wave_sort_tile<1>(t, start, n, skey, sval, sk, sv, pair_emit, vals, keys64);
+        else if (n <= 128u)
+            wave_sort_tile<2>(t, start, n, skey, sval, sk, sv, pair_emit, vals, keys64);
+        else if (n <= 256u)
+            wave_sort_tile<4>(t, start, n, skey, sval, sk, sv, pair_emit, vals, keys64);
+        else
+            wave_sort_tile<8>(t, start, n, skey, sval, sk, sv, pair_emit, vals, keys64);
     }
 }
 
 struct BinsortLayout {
-    size_t pk[3], pv[3];      // pair sort keys: in, tmp, out; pv[0] = primitive of each emitted pair,
-                              // pv[1..2] = value ping-pong (values out = caller's pair_emit)
-    size_t scratch;           // 64-bit keys of tiles longer than the LDS sort
-    size_t tkey[2], order;    // tile dispatch keys (in, sorted) and the order when the caller keeps none
-    size_t hist, totals, bsum, offs, bstart, counters;
+    size_t pkeys, emit_id;    // per emission position: tile and primitive of the pair
+    size_t pdepth;            // per emission position: the primitive's depth bits
+    size_t skey, sval;        // per sorted position: the 64-bit depth-sort key and its primitive
+    size_t order;             // the dispatch order when the caller keeps none
+    size_t rec;               // per dispatch position: tile, range start, pair count
+    size_t tcount, cursor;    // per tile: pair total, placement cursor
+    size_t bsum, offs, bstart, counters;
     size_t bytes;
-    uint32_t nblocks_hist;
 };
 
 uint32_t tile_count(int32_t width, int32_t height) {
@@ -564,16 +936,15 @@ BinsortLayout binsort_layout(int32_t n, uint32_t capacity, int32_t width, int32_
     size_t o = 0;
     const size_t nn = (size_t)(n > 0 ? n : 1), cc = (size_t)(capacity > 0 ? capacity : 1);
     const size_t tt = (size_t)(width > 0 && height > 0 ? tile_count(width, height) : 1u);
-    for (int i = 0; i < 3; ++i) { L.pk[i] = o; o += align256(4 * cc); }
-    for (int i = 0; i < 3; ++i) { L.pv[i] = o; o += align256(4 * cc); }
-    L.scratch = o; o += align256(8 * cc);
-    for (int i = 0; i < 2; ++i) { L.tkey[i] = o; o += align256(4 * tt); }
+    L.pkeys = o; o += align256(4 * cc);
+    L.emit_id = o; o += align256(4 * cc);
+    L.pdepth = o; o += align256(4 * cc);
+    L.skey = o; o += align256(8 * cc);
+    L.sval = o; o += align256(4 * cc);
     L.order = o; o += align256(4 * tt);
-    size_t most = nn > cc ? nn : cc;
-    most = most > tt ? most : tt;
-    L.nblocks_hist = div_up(most, GS_TILE_ITEMS);
-    L.hist = o; o += align256(4 * ((size_t)1 << kTileBits) * L.nblocks_hist);
-    L.totals = o; o += align256(4 * ((size_t)1 << kTileBits));
+    L.rec = o; o += align256(16 * tt);
+    L.tcount = o; o += align256(4 * tt);
+    L.cursor = o; o += align256(4 * tt);
     L.bsum = o; o += align256(4 * ((size_t)div_up(nn, GS_TILE_ITEMS) + 1));
     L.offs = o; o += align256(4 * (nn + 1));
     L.bstart = o; o += align256(4 * ((size_t)div_up(cc, GS_TILE_ITEMS) + 1));
@@ -584,38 +955,6 @@ BinsortLayout binsort_layout(int32_t n, uint32_t capacity, int32_t width, int32_
 
 template <typename T>
 T* at(void* ws, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(ws) + off); }
-
-// LSD passes over bits [0, total_bits) of `count` keys, BITS per pass.
-// Buffers: in, tmp, out.
-// vin may be null: the values are then the input positions.  Value buffers
-// ping-pong between vtmp0 and vtmp1.
-// The first pass's histogram matrix is already in hist (written by the
-// kernel that produced the keys).
-template <int BITS>
-hipError_t radix_sort(uint32_t* kin, const uint32_t* vin, uint32_t* ktmp, uint32_t* vtmp0, uint32_t* vtmp1,
-                      uint32_t* kout, uint32_t* vout, const uint32_t* count, uint32_t max_count, int total_bits,
-                      uint32_t* hist, uint32_t* totals, hipStream_t st) {
-    const uint32_t nblocks = div_up(max_count > 0 ? max_count : 1, GS_TILE_ITEMS);
-    const int passes = (total_bits + BITS - 1) / BITS;
-    uint32_t* kb[2] = {ktmp, kin};
-    uint32_t* vb[2] = {vtmp0, vtmp1};
-    for (int p = 0; p < passes; ++p) {
-        const int shift = p * BITS;
-        const int nbits = (total_bits - shift) < BITS ? (total_bits - shift) : BITS;
-        const uint32_t mask = (1u << nbits) - 1u;
-        const uint32_t* ks = (p == 0) ? kin : kb[(p - 1) & 1];
-        const uint32_t* vs = (p == 0) ? vin : vb[(p - 1) & 1];
-        uint32_t* kd = (p == passes - 1) ? kout : kb[p & 1];
-        uint32_t* vd = (p == passes - 1) ? vout : vb[p & 1];
-        if (p > 0)
-            hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, count, shift, mask, hist,
-                               nblocks);
-        hipLaunchKernelGGL(k_radix_scan, dim3(1u << nbits), dim3(GS_BLOCK), 0, st, hist, nblocks, totals);
-        hipLaunchKernelGGL(k_radix_scatter<BITS>, dim3(nblocks), dim3(GS_BLOCK), 0, st, ks, vs, kd, vd, count, shift,
-                           mask, nbits, hist, totals, nblocks);
-    }
-    return hipGetLastError();
-}
 
 }  // namespace
 
@@ -630,38 +969,23 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     const BinsortLayout L = binsort_layout(n, capacity, width, height);
     const int32_t TX = (width + GS_TILE - 1) / GS_TILE;
     const uint32_t T = tile_count(width, height);
-    uint32_t* hist = at<uint32_t>(ws, L.hist);
-    uint32_t* totals = at<uint32_t>(ws, L.totals);
     uint32_t* bsum = at<uint32_t>(ws, L.bsum);
-    uint32_t* ctr = at<uint32_t>(ws, L.counters);   // [0] M, [1] sort count, [2] T
+    uint32_t* ctr = at<uint32_t>(ws, L.counters);   // [0] M, [1] sort count, [2] long tiles
+    uint32_t* tcount = at<uint32_t>(ws, L.tcount);
+    uint32_t* cursor = at<uint32_t>(ws, L.cursor);
     uint32_t* order = tile_order ? tile_order : at<uint32_t>(ws, L.order);
-    // ranges, dispatch keys and the dispatch order (tiles by pair count
-    // descending, ties by tile id: one stable radix pass over 8-bit keys)
-    // (ranges must hold zeros on entry)
-    auto tile_pass = [&](const uint32_t* skeys, const uint32_t* sort_count) {
-        const uint32_t nbT = div_up(T, GS_TILE_ITEMS);
-        if (skeys)
-            hipLaunchKernelGGL(k_tile_bounds, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, skeys,
-                               sort_count, ranges);
-        hipLaunchKernelGGL(k_tile_keys, dim3(nbT), dim3(GS_BLOCK), 0, st, ranges, T, at<uint32_t>(ws, L.tkey[0]),
-                           hist, nbT, ctr + 2);
-        if (nbT <= kSelfScanBlocks) {
-            hipLaunchKernelGGL((k_radix_scatter<8, true>), dim3(nbT), dim3(GS_BLOCK), 0, st,
-                               at<uint32_t>(ws, L.tkey[0]), nullptr, at<uint32_t>(ws, L.tkey[1]), order, ctr + 2, 0,
-                               255u, 8, hist, totals, nbT);
-        } else {
-            hipLaunchKernelGGL(k_radix_scan, dim3(256), dim3(GS_BLOCK), 0, st, hist, nbT, totals);
-            hipLaunchKernelGGL(k_radix_scatter<8>, dim3(nbT), dim3(GS_BLOCK), 0, st, at<uint32_t>(ws, L.tkey[0]),
-                               nullptr, at<uint32_t>(ws, L.tkey[1]), order, ctr + 2, 0, 255u, 8, hist, totals, nbT);
-        }
+    // ranges, cursors and the dispatch order from the per-tile totals
+    auto finish = [&]() {
+        hipLaunchKernelGGL(k_tile_finish, dim3(div_up(T, kFinishSeg)), dim3(GS_BLOCK), 0, st, tcount, T, ranges,
+                           cursor, order, at<uint4>(ws, L.rec), ctr + 2);
         return hipGetLastError();
     };
-    // no pairs: empty ranges, and the order (then the tile ids) when the caller keeps it
+    // no pairs: empty ranges, and the order (then the tile ids)
     auto no_pairs = [&]() {
         if (T == 0) return hipGetLastError();
-        hipError_t e = launch_fill_u32(ranges, 0u, 2 * (size_t)T, st);
-        if (e != hipSuccess || !tile_order) return e;
-        return tile_pass(nullptr, nullptr);
+        hipError_t e = launch_fill_u32(tcount, 0u, T, st);
+        if (e != hipSuccess) return e;
+        return finish();
     };
     if (n == 0) {
         hipError_t e = launch_fill_u32(num_pairs, 0u, 1, st);
@@ -671,35 +995,33 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     // 1. emission offsets in visible-set order
     const uint32_t* vorder = vis_idx;
     const uint32_t nb = div_up(n, GS_TILE_ITEMS);
-    hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum, ranges,
-                       2 * T);
+    hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum, tcount, T);
     hipError_t e = launch_scan_blocks(bsum, nb, ctr + 0, nullptr, st);
     if (e != hipSuccess) return e;
     uint32_t* offs_r = at<uint32_t>(ws, L.offs);
     const uint32_t nbs = div_up(capacity, GS_TILE_ITEMS) + 1u;
     hipLaunchKernelGGL(k_offsets, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum, ctr + 0,
                        capacity, pair_offset, offs_r, ctr + 1, num_pairs, status, at<uint32_t>(ws, L.bstart), nbs);
-    int tbits = 1;
-    while (tbits < 32 && (1u << tbits) < T) ++tbits;
-    const uint32_t mask0 = (1u << (tbits < kTileBits ? tbits : kTileBits)) - 1u;
     if (capacity == 0 || T == 0) return no_pairs();
-    // 2. emission: one (tile, primitive) pair per touched tile
-    hipLaunchKernelGGL(k_emit_pairs, dim3(div_up(capacity, GS_TILE_ITEMS)), dim3(GS_BLOCK), 0, st, vorder,
-                       vis_count, offs_r, at<uint32_t>(ws, L.bstart), reinterpret_cast<const ushort4*>(proj.rect),
-                       ctr + 1, TX,
-                       at<uint32_t>(ws, L.pk[0]), at<uint32_t>(ws, L.pv[0]), mask0, hist,
-                       div_up(capacity, GS_TILE_ITEMS));
-    // 3. sort of the pairs by tile id, carrying every pair's emission position
-    e = radix_sort<kTileBits>(at<uint32_t>(ws, L.pk[0]), nullptr, at<uint32_t>(ws, L.pk[1]), at<uint32_t>(ws, L.pv[1]),
-                              at<uint32_t>(ws, L.pv[2]), at<uint32_t>(ws, L.pk[2]), pair_emit, ctr + 1, capacity,
-                              tbits, hist, totals, st);
+    // 2. emission: one (tile, primitive) pair per touched tile, and the per-tile totals
+    const uint32_t nbp = div_up(capacity, GS_TILE_ITEMS);
+    hipLaunchKernelGGL(k_emit_pairs, dim3(nbp), dim3(GS_BLOCK), 0, st, vorder, vis_count, offs_r,
+                       at<uint32_t>(ws, L.bstart), reinterpret_cast<const ushort4*>(proj.rect), proj.depth, ctr + 1,
+                       TX, T, at<uint32_t>(ws, L.pkeys), at<uint32_t>(ws, L.emit_id), at<uint32_t>(ws, L.pdepth),
+                       tcount);
+    // 3. tile ranges and the dispatch order
+    e = finish();
     if (e != hipSuccess) return e;
-    // 4. tile ranges and the dispatch order
-    e = tile_pass(at<uint32_t>(ws, L.pk[2]), ctr + 1);
-    if (e != hipSuccess) return e;
+    // 4. every pair's depth-sort key placed in its tile's range
+    unsigned long long* skey = at<unsigned long long>(ws, L.skey);
+    uint32_t* sval = at<uint32_t>(ws, L.sval);
+    hipLaunchKernelGGL(k_tile_scatter, dim3(nbp), dim3(GS_BLOCK), 0, st, at<uint32_t>(ws, L.pkeys),
+                       at<uint32_t>(ws, L.emit_id), at<uint32_t>(ws, L.pdepth), ctr + 1, T, cursor, skey, sval);
     // 5. per tile, longest first: depth order, primitive ids (+ optional 64-bit keys)
-    hipLaunchKernelGGL(k_tile_depth_sort, dim3(T), dim3(GS_BLOCK), 0, st, order, ranges, at<uint32_t>(ws, L.pv[0]),
-                       proj.depth, pair_emit, vals, keys, at<unsigned long long>(ws, L.scratch));
+    const uint32_t cus = compute_units();
+    const uint32_t grid = std::min<uint32_t>(T, (cus ? cus : 256u) * kDepthSortBlocksPerCU);
+    hipLaunchKernelGGL(k_tile_depth_sort, dim3(grid), dim3(GS_BLOCK), 0, st, at<uint4>(ws, L.rec), ctr + 2, T, skey,
+                       sval, pair_emit, vals, keys);
     return hipGetLastError();
 }
 

@@ -498,6 +498,89 @@ def test_long_tile_lists(torch_gpu, orc):
     assert lengths[order[0]] == lengths.max()
 
 
+# (tile x, tile y, primitives, short ties, long run): one cluster per tile
+# class of the per-tile depth sort, from one wave with one key per lane up to
+# tiles longer than a workgroup's register sort.  Short ties: an eighth of
+# the primitives copy a neighbour's mean (runs of equal depth bits of a few
+# pairs); long run: that many primitives share one mean (a run longer than
+# the in-place placement takes).
+DEPTH_SORT_CLUSTERS = [(1, 1, 40, True, 0), (3, 1, 40, False, 0), (5, 1, 100, True, 0), (7, 1, 200, True, 0),
+                       (9, 1, 400, True, 0), (11, 1, 400, False, 0), (13, 1, 230, False, 0),
+                       (1, 5, 1000, False, 0), (5, 5, 1000, True, 0), (9, 5, 1800, False, 0),
+                       (13, 5, 3000, False, 0), (3, 9, 700, True, 0), (7, 9, 300, False, 80),
+                       (11, 9, 900, False, 100)]
+
+
+def test_depth_sort_paths(torch_gpu, orc):
+    """Tiles of every size class of the per-tile sort (one wave with 1, 2, 4
+    or 8 keys per lane, a workgroup up to 2048 keys, global memory beyond),
+    with and without pairs of equal depth bits (copies of a primitive's
+    mean): the order is exactly (tile, depth bits, id) in every class."""
+    from paper_2607_19893_amd import scenes
+    rng = np.random.default_rng(33)
+    n_bg = 1500
+    n = n_bg + sum(c[2] for c in DEPTH_SORT_CLUSTERS)
+    w = scenes.tiny(n=n)
+    sc = w.scene
+    cam = w.cameras[0]
+    R = np.asarray(cam.R, np.float64)
+    k = n_bg
+    for tx, ty, cnt, ties, run in DEPTH_SORT_CLUSTERS:
+        # pixels inside the tile (away from its edges), camera depths in [2, 6]
+        u = tx * 16 + 8 + rng.uniform(-3, 3, cnt)
+        v = ty * 16 + 8 + rng.uniform(-3, 3, cnt)
+        z = rng.uniform(2.0, 6.0, cnt)
+        pc = np.stack([(u - cam.cx) * z / cam.fx, (v - cam.cy) * z / cam.fy, z], 1)
+        mean = (pc - np.asarray(cam.t, np.float64)) @ R           # R^T (p - t)
+        if ties:
+            dup = rng.choice(cnt, cnt // 8, replace=False)
+            mean[dup] = mean[(dup + 1) % cnt]
+        mean[1:run] = mean[0]
+        sc.mean[k:k + cnt] = mean.astype(np.float32)
+        k += cnt
+    sc.log_scale[n_bg:] = np.float32(-5.5)
+    tr = trainer_for(w, torch_gpu)
+    tr.status.zero_()
+    tr.project(cam); tr.visible(); tr.bin_sort()
+    torch_gpu.cuda.synchronize()
+    assert u32(tr.status)[0] == 0
+    ref = orc.project(sc, cam, 0)
+    vis_ref = orc.visible(ref.tiles)
+    keys_ref, vals_ref, ranges_ref = orc.sorted_pairs(vis_ref, ref, cam)
+    T = cam.num_tiles
+    lengths = ranges_ref[:, 1].astype(np.int64) - ranges_ref[:, 0]
+    tied, longest = 0, []
+    for t in range(T):
+        kk = keys_ref[ranges_ref[t, 0]:ranges_ref[t, 1]] & np.uint64(0xFFFFFFFF)
+        tied += int(kk.size != np.unique(kk).size)
+        longest.append(int(np.unique(kk, return_counts=True)[1].max()) if kk.size else 0)
+    for tx, ty, cnt, ties, run in DEPTH_SORT_CLUSTERS:
+        t = ty * cam.tiles_x + tx
+        _say("cluster tile (%d,%d): %d pairs, longest run of equal depth bits %d" % (tx, ty, lengths[t], longest[t]))
+    _say("tiles with equal depth bits:", tied)
+    cl = [lengths[ty * cam.tiles_x + tx] for tx, ty, _, _, _ in DEPTH_SORT_CLUSTERS]
+    assert min(cl) <= 64 and max(cl) > 2048 and any(512 <= c <= 2048 for c in cl)
+    assert any(256 < c < 512 for c in cl) and tied >= 4
+    runs = {(tx, ty): longest[ty * cam.tiles_x + tx] for tx, ty, _, _, _ in DEPTH_SORT_CLUSTERS}
+    assert runs[(7, 9)] > 64 and runs[(11, 9)] > 64 and 2 <= runs[(9, 1)] <= 64 and 2 <= runs[(5, 5)] <= 64
+    M = int(u32(tr.counts[1:2])[0])
+    assert M == keys_ref.size
+    np.testing.assert_array_equal(tr.keys.cpu().numpy()[:M].view(np.uint64), keys_ref)
+    np.testing.assert_array_equal(u32(tr.vals)[:M], vals_ref)
+    np.testing.assert_array_equal(u32(tr.ranges)[:2 * T].reshape(T, 2), ranges_ref)
+    np.testing.assert_array_equal(u32(tr.tile_order)[:T], expected_tile_order(ranges_ref))
+    # emission offsets, and the sorted -> emission map: sorted pair i is tile number
+    # (ty - y0) * (x1 - x0) + (tx - x0) of primitive vals[i]'s rectangle
+    off_ref = np.cumsum(ref.tiles[vis_ref].astype(np.int64)) - ref.tiles[vis_ref]
+    np.testing.assert_array_equal(u32(tr.pair_offset)[vis_ref], off_ref)
+    tile = (keys_ref >> np.uint64(32)).astype(np.int64)
+    rc = ref.rect[vals_ref].astype(np.int64)
+    local = (tile // cam.tiles_x - rc[:, 1]) * (rc[:, 2] - rc[:, 0]) + (tile % cam.tiles_x - rc[:, 0])
+    full = np.zeros(sc.n, np.int64)
+    full[vis_ref] = off_ref
+    np.testing.assert_array_equal(u32(tr.pair_emit)[:M], full[vals_ref] + local)
+
+
 def test_pair_overflow_flag(torch_gpu, orc):
     """Capacity below the pair count: the flag and the required count are set."""
     w = get_case("tiny-10k-256")
