@@ -28,16 +28,18 @@ constexpr float kAlphaMax = 0.99f;
 constexpr float kTMin = 1e-4f;
 constexpr float kCutMargin = 1e-3f;   // extra sigma beyond the 1/255 cut-off when bounding a footprint
 
-// One pair's primitive as staged in LDS: 64 bytes in four 16-byte arrays,
-// every lane of a wave reading the same record (a broadcast):
+// One pair's primitive as staged in LDS: 72 bytes in five arrays, every lane
+// of a wave reading the same record (a broadcast):
 //   P (u, v) and Q (A/2, B) in fp64, R = (C/2 in fp64, opacity, hx),
-//   S = (r, g, b, hy).
+//   S = (r, g, b, hy), T = (cut, slope) for the row lists (computed once per
+//   staged entry rather than by every wave that tests it).
 // The pixel-space mean and conic are fp32 values held exactly in fp64, so
 // that the quadratic form is evaluated in fp64 without per-pair conversions.
 // hx, hy bound the pixel offsets at which o*exp(-sigma) can reach 1/255: for
 // sigma = d^T Q d / 2 <= s the offsets obey |dx| <= sqrt(2 s C / det Q) and
-// |dy| <= sqrt(2 s A / det Q); s = ln(255 o) + kCutMargin keeps every skipped
-// pair at least 0.1% below the threshold, far outside fp32 rounding.
+// |dy| <= sqrt(2 s A / det Q); s = cut = ln(255 o) + kCutMargin keeps every
+// skipped pair at least 0.1% below the threshold, far outside fp32 rounding.
+// slope = -B/A (fp32) is the vertex of sigma along a pixel row per unit dy.
 struct __align__(16) SplatR {
     double c2;
     float o;
@@ -50,6 +52,7 @@ struct SplatLds {
     double2 Q[NB];
     SplatR R[NB];
     float4 S[NB];
+    float2 T[NB];
 };
 
 template <int NB>
@@ -74,6 +77,7 @@ __device__ __forceinline__ void stage_splat(SplatLds<NB>& L, int k, float2 m, fl
     r.hx = hx;
     L.R[k] = r;
     L.S[k] = make_float4(rgb3[0], rgb3[1], rgb3[2], hy);
+    L.T[k] = make_float2(cut, co.x > 0.0f ? -co.y * __builtin_amdgcn_rcpf(co.x) : 0.0f);
 }
 
 // Can any pixel centre of the wave's strip [x0,x1] x [y0,y1] reach the cut-off?
@@ -130,12 +134,15 @@ __device__ __forceinline__ float exp_neg(float sigma) {
 // 16x4 strip.  cnt[r] receives the length of row r's list.
 //
 // An entry reaches row y if sigma <= s somewhere on the row's segment of
-// pixel centres [x0, x1] (s = ln(255 o) + kCutMargin as for hx, hy): the
-// footprint box is tested first, then the minimum of sigma over the segment,
-// which for the row's dy is the quadratic's vertex dx = -(B/A) dy clamped to
-// the segment's offsets [u - x1, u - x0], in fp64 (the staged values are
-// exact).  Any pixel of a skipped row is at least the cut-off margin below
-// the 1/255 threshold.
+// pixel centres [x0, x1] (s = cut = ln(255 o) + kCutMargin as for hx, hy):
+// the footprint box is tested first, then sigma at the quadratic's vertex dx =
+// slope dy (slope = -B/A in fp32) clamped to the segment's offsets [u - x1,
+// u - x0], in fp64 (the staged values are exact).  Off the exact vertex by the
+// slope's rounding (a few 1e-7 relative), sigma there exceeds the segment's
+// minimum by at most about 4e-13 (B^2 / det), i.e. 4e-13 times the squared
+// axis ratio of the footprint: inside the 1e-3 margin up to ratios near 5e4,
+// where the fp32 conic itself has lost its accuracy.  Any pixel of a skipped
+// row stays below the 1/255 threshold.
 template <int NB>
 __device__ __forceinline__ void compact_rows(const SplatLds<NB>& L, int nb, float x0, float x1, float y0,
                                              const uint32_t* lim, uint8_t (*list)[NB], uint32_t* cnt) {
@@ -154,9 +161,10 @@ __device__ __forceinline__ void compact_rows(const SplatLds<NB>& L, int nb, floa
         const float u = (float)p.x, v = (float)p.y;
         const float hx = R.hx, hy = L.S[kk].w;
         const bool bx = valid && (u + hx >= x0) && (u - hx <= x1);
-        const double cut = (double)(logf(255.0f * R.o) + kCutMargin);
+        const float2 cs = L.T[kk];
+        const double cut = (double)cs.x;
         const bool convex = qd.x > 0.0;                      // A > 0 for every projected conic; else no row test
-        const double slope = convex ? -qd.y / (2.0 * qd.x) : 0.0;   // vertex offset per unit dy: -B / A
+        const double slope = (double)cs.y;                   // vertex offset per unit dy: -B / A (0 unless A > 0)
         const double dlo = p.x - (double)x1, dhi = p.x - (double)x0;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -200,16 +208,15 @@ __device__ __forceinline__ uint32_t dispatch_tile(const uint32_t* __restrict__ t
 // the target exactly as k_loss_l1 does, writes dL/dimg, and each tile leaves
 // its sum of |img - target| in loss_partial[tile] for k_loss_final.
 template <bool STATS, bool LOSS>
-__global__ void __launch_bounds__(GS_BLOCK, 7) k_raster_fwd(
+__global__ void __launch_bounds__(GS_BLOCK, STATS ? 5 : 7) k_raster_fwd(
     const uint32_t* __restrict__ tile_order, const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals,
-    const float2* __restrict__ mean2d,
-    const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
-    float bg1, float bg2, float* __restrict__ img, float* __restrict__ final_T, uint32_t* __restrict__ n_contrib,
+    const float2* __restrict__ mean2d, const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W,
+    int32_t H, int32_t TX, float bg0, float bg1, float bg2, float* __restrict__ img, float* __restrict__ final_T,
+    uint32_t* __restrict__ n_contrib,
     uint8_t* __restrict__ active, unsigned long long* __restrict__ pair_stats, const float* __restrict__ target,
     float inv_total, float* __restrict__ dL, float* __restrict__ loss_partial) {
     __shared__ SplatLds<GS_BLOCK> L;
-    __shared__ uint32_t s_id[GS_BLOCK];
-    __shared__ uint32_t s_hit[GS_BLOCK];
+    __shared__ uint32_t s_hit[GS_BLOCK / 32];       // entries some pixel included (active flags)
     __shared__ uint8_t s_list[4][4][GS_BLOCK];
     __shared__ uint32_t s_stat[4][4];
     const uint32_t tile = dispatch_tile(tile_order);
@@ -230,15 +237,15 @@ __global__ void __launch_bounds__(GS_BLOCK, 7) k_raster_fwd(
     float T = 1.0f, c0 = 0.0f, c1 = 0.0f, c2 = 0.0f;
     uint32_t last = 0, n_inc = 0, term_at = 0, w_iter = 0, w_hit = 0;
     bool done = !inside, terminated = false;
+    // the ids of the next batch load while this one is walked
+    uint32_t g = start + tid < end ? vals[start + tid] : 0u;
     for (uint32_t bs = start; bs < end; bs += GS_BLOCK) {
         if (__syncthreads_count(done) == GS_BLOCK) break;
         const uint32_t j = bs + tid;
-        if (j < end) {
-            const uint32_t g = vals[j];
-            stage_splat(L, tid, mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
-            s_id[tid] = g;
-        }
-        s_hit[tid] = 0;
+        const uint32_t gj = g;
+        if (j < end) stage_splat(L, tid, mean2d[gj], conic_op[gj], rgb + 3 * (size_t)gj);
+        if (j + GS_BLOCK < end) g = vals[j + GS_BLOCK];
+        if (tid < GS_BLOCK / 32) s_hit[tid] = 0u;
         __syncthreads();
         const int nb = (int)min((uint32_t)GS_BLOCK, end - bs);
         // rows whose 16 pixels are all finished take no entries
@@ -292,10 +299,10 @@ __global__ void __launch_bounds__(GS_BLOCK, 7) k_raster_fwd(
                     w_hit += ((om >> (16 * q)) & 0xFFFFull) ? 1u : 0u;
                 }
             }
-            if (active != nullptr && ok) s_hit[k] = 1u;
+            if (active != nullptr && ok) atomicOr(&s_hit[k >> 5], 1u << (k & 31));
         }
         __syncthreads();
-        if (active && j < end && s_hit[tid]) active[s_id[tid]] = 1;
+        if (active && j < end && ((s_hit[tid >> 5] >> (tid & 31)) & 1u)) active[gj] = 1;
     }
     if (STATS) {
         // entries the per-pixel definition examines: up to and including the
@@ -467,8 +474,8 @@ constexpr int kBwdBatch = GS_WAVE;
 // conic once per primitive.
 __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const uint32_t* __restrict__ tile_order, const uint32_t* __restrict__ ranges, const uint32_t* __restrict__ vals,
-    const float2* __restrict__ mean2d,
-    const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W, int32_t H, int32_t TX, float bg0,
+    const float2* __restrict__ mean2d, const float4* __restrict__ conic_op, const float* __restrict__ rgb, int32_t W,
+    int32_t H, int32_t TX, float bg0,
     float bg1, float bg2, const float* __restrict__ final_T, const uint32_t* __restrict__ n_contrib,
     const float* __restrict__ dL_dimg, const uint32_t* __restrict__ pair_emit, float* __restrict__ slots) {
     __shared__ SplatLds<kBwdBatch> L;
