@@ -849,17 +849,10 @@ __device__ __forceinline__ void geometry_bwd(const float* mu_f, const float* ls_
     out[9] = (float)((gz - z * along) * iq);
 }
 
-__device__ __forceinline__ void add_slot(float* g, const float* __restrict__ slots, uint32_t pos) {
-    const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)pos * kSlot);
-    const float4 v0 = sl[0], v1 = sl[1], v2 = sl[2];
-    g[0] += v0.x; g[1] += v0.y; g[2] += v0.z; g[3] += v0.w;
-    g[4] += v1.x; g[5] += v1.y; g[6] += v1.z; g[7] += v1.w; g[8] += v2.x;
-}
-
 // Lists of up to kSerialSlots slots are summed by their own thread; longer
-// ones (a primitive spanning many tiles) by the whole wave, 64 slots at a
-// time.  Either way the order is fixed, so the result is deterministic.
-constexpr uint32_t kSerialSlots = 32;
+// ones (a primitive spanning many tiles) by the whole wave, 256 slots a
+// round.  Either way the order is fixed, so the result is deterministic.
+constexpr uint32_t kSerialSlots = 8;
 
 template <int N>
 __device__ __forceinline__ void load_row(const float* __restrict__ src, float* dst) {
@@ -886,25 +879,19 @@ __device__ __forceinline__ uint32_t find_row(const uint32_t* __restrict__ u, uin
     return (lo < m && u[lo] == id) ? lo : m;
 }
 
-// Per visible row r: the primitive's 2D gradient (the sum of its pair slots,
-// emission positions pair_offset[id] .. + tiles[id], side by side; none if the
-// pair list overflowed its capacity), then the chain rule to the parameters;
-// writes the row's gradient record at grad_rows + r * ld.  ACCUM (a task unit
-// of several views): the record is added to row u instead, u the position of
-// id in the unit's ascending union list, and |dL/d(u,v)| is added to
-// grad_norm[id].
-template <int DEG, bool ACCUM>
-__global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
-    const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
-    const uint32_t* __restrict__ pair_offset, const float* __restrict__ slots, uint32_t capacity,
-    const float4* __restrict__ conic_op, const uint8_t* __restrict__ clampm, const float* __restrict__ mean, const float* __restrict__ log_scale,
-    const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, SceneLd pld,
-    CamArgs c, float* __restrict__ grad_rows, int32_t ld, float* __restrict__ grad2d, float* __restrict__ grad_norm,
-    const uint32_t* __restrict__ union_idx, const uint32_t* __restrict__ union_count) {
-    using L = RowLayout<DEG>;
-    constexpr int K = L::K;
+// Per visible row r: the sum of the primitive's pair slots (emission
+// positions pair_offset[id] .. + tiles[id], side by side; none if the pair
+// list overflowed its capacity), as one kSlot-float row at sums + kSlot r.
+// A kernel of its own: the chain rule's registers would leave the slot
+// stream too few waves to keep its loads in flight.
+__global__ void __launch_bounds__(GS_BLOCK) k_slot_sum(const uint32_t* __restrict__ vis_idx,
+                                                       const uint32_t* __restrict__ vis_count,
+                                                       const uint32_t* __restrict__ tiles,
+                                                       const uint32_t* __restrict__ pair_offset,
+                                                       const float* __restrict__ slots, uint32_t capacity,
+                                                       float* __restrict__ sums) {
     const uint32_t V = *vis_count;
-    // Rows in chunks of 16 consecutive ones (neighbouring rows' loads share
+    // Rows in chunks of 16 consecutive ones (neighbouring rows' slots share
     // cache lines); workgroup b takes chunks b, b + NB, b + 2 NB, ... (NB the
     // workgroups needed), so a wave's four chunks lie across the whole list.
     // In a spatially ordered pool the long slot lists of neighbours near the
@@ -916,38 +903,94 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
     const bool valid = r < V;
     const uint32_t id = valid ? vis_idx[r] : 0u;
     float g2[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-    {
-        const uint32_t first = valid ? pair_offset[id] : 0u;
-        const uint32_t nt = valid ? tiles[id] : 0u;
-        const bool fits = (uint64_t)first + nt <= capacity;
-        if (fits && nt <= kSerialSlots) {
-            uint32_t k = 0;
-            for (; k + 2 <= nt; k += 2) {
-                const float4* s0 = reinterpret_cast<const float4*>(slots + (size_t)(first + k) * kSlot);
-                const float4 a0 = s0[0], a1 = s0[1], a2 = s0[2], b0 = s0[3], b1 = s0[4], b2 = s0[5];
-                g2[0] += a0.x; g2[1] += a0.y; g2[2] += a0.z; g2[3] += a0.w;
-                g2[4] += a1.x; g2[5] += a1.y; g2[6] += a1.z; g2[7] += a1.w; g2[8] += a2.x;
-                g2[0] += b0.x; g2[1] += b0.y; g2[2] += b0.z; g2[3] += b0.w;
-                g2[4] += b1.x; g2[5] += b1.y; g2[6] += b1.z; g2[7] += b1.w; g2[8] += b2.x;
-            }
-            if (k < nt) add_slot(g2, slots, first + k);
-        }
-        uint64_t big = __ballot(fits && nt > kSerialSlots);
-        while (big) {
-            const int owner = __ffsll((unsigned long long)big) - 1;
-            big &= big - 1;
-            const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)first, owner);
-            const uint32_t nb = (uint32_t)__builtin_amdgcn_readlane((int)nt, owner);
-            float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-            for (uint32_t k = lane_id(); k < nb; k += GS_WAVE) add_slot(acc, slots, f + k);
+    const uint32_t first = valid ? pair_offset[id] : 0u;
+    const uint32_t nt = valid ? tiles[id] : 0u;
+    const bool fits = (uint64_t)first + nt <= capacity;
+    if (fits && nt <= kSerialSlots) {
+        // up to four slots per round, all loads in flight
+        for (uint32_t k = 0; k < nt; k += 4) {
+            float4 v[4][3];
 #pragma unroll
-            for (int q = 0; q < kG; ++q) {
-                const float v = wave_sum(acc[q]);
-                if (lane_id() == owner) g2[q] = v;
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t q = first + min(k + j, nt - 1u);     // past the list: the last slot again, unused
+                const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)q * kSlot);
+                v[j][0] = sl[0]; v[j][1] = sl[1]; v[j][2] = sl[2];
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (k + j < nt) {
+                    g2[0] += v[j][0].x; g2[1] += v[j][0].y; g2[2] += v[j][0].z; g2[3] += v[j][0].w;
+                    g2[4] += v[j][1].x; g2[5] += v[j][1].y; g2[6] += v[j][1].z; g2[7] += v[j][1].w;
+                    g2[8] += v[j][2].x;
+                }
             }
         }
     }
+    // longer lists: the whole wave, 4 x 64 slots per round with coalesced loads,
+    // the lanes' partial sums added in a fixed order
+    uint64_t big = __ballot(fits && nt > kSerialSlots);
+    while (big) {
+        const int owner = __ffsll((unsigned long long)big) - 1;
+        big &= big - 1;
+        const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)first, owner);
+        const uint32_t nb2 = (uint32_t)__builtin_amdgcn_readlane((int)nt, owner);
+        float acc[kG] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+        for (uint32_t k0 = 0; k0 < nb2; k0 += 4 * GS_WAVE) {
+            float4 v[4][3];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t k = min(k0 + j * GS_WAVE + lane_id(), nb2 - 1u);
+                const float4* sl = reinterpret_cast<const float4*>(slots + (size_t)(f + k) * kSlot);
+                v[j][0] = sl[0]; v[j][1] = sl[1]; v[j][2] = sl[2];
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (k0 + j * GS_WAVE + lane_id() < nb2) {
+                    acc[0] += v[j][0].x; acc[1] += v[j][0].y; acc[2] += v[j][0].z; acc[3] += v[j][0].w;
+                    acc[4] += v[j][1].x; acc[5] += v[j][1].y; acc[6] += v[j][1].z; acc[7] += v[j][1].w;
+                    acc[8] += v[j][2].x;
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kG; ++q) {
+            const float sv = wave_sum(acc[q]);
+            if (lane_id() == owner) g2[q] = sv;
+        }
+    }
     if (!valid) return;
+    float4* dst = reinterpret_cast<float4*>(sums + (size_t)r * kSlot);
+    dst[0] = make_float4(g2[0], g2[1], g2[2], g2[3]);
+    dst[1] = make_float4(g2[4], g2[5], g2[6], g2[7]);
+    dst[2] = make_float4(g2[8], 0.0f, 0.0f, 0.0f);
+}
+
+// Per visible row r: the primitive's 2D gradient (from its slot sums, row r
+// of k_slot_sum), then the chain rule to the parameters; writes the row's
+// gradient record at grad_rows + r * ld.  ACCUM (a task unit
+// of several views): the record is added to row u instead, u the position of
+// id in the unit's ascending union list, and |dL/d(u,v)| is added to
+// grad_norm[id].
+template <int DEG, bool ACCUM>
+__global__ void __launch_bounds__(GS_BLOCK) k_project_bwd(
+    const uint32_t* __restrict__ vis_idx, const uint32_t* __restrict__ vis_count, const float* __restrict__ sums,
+    const float4* __restrict__ conic_op, const uint8_t* __restrict__ clampm, const float* __restrict__ mean, const float* __restrict__ log_scale,
+    const float* __restrict__ quat, const float* __restrict__ opacity, const float* __restrict__ sh, SceneLd pld,
+    CamArgs c, float* __restrict__ grad_rows, int32_t ld, float* __restrict__ grad2d, float* __restrict__ grad_norm,
+    const uint32_t* __restrict__ union_idx, const uint32_t* __restrict__ union_count) {
+    using L = RowLayout<DEG>;
+    constexpr int K = L::K;
+    const uint32_t V = *vis_count;
+    const uint32_t r = blockIdx.x * GS_BLOCK + threadIdx.x;
+    if (r >= V) return;
+    const uint32_t id = vis_idx[r];
+    float g2[kG];
+    {
+        const float4* src = reinterpret_cast<const float4*>(sums + (size_t)r * kSlot);
+        const float4 a0 = src[0], a1 = src[1], a2 = src[2];
+        g2[0] = a0.x; g2[1] = a0.y; g2[2] = a0.z; g2[3] = a0.w;
+        g2[4] = a1.x; g2[5] = a1.y; g2[6] = a1.z; g2[7] = a1.w; g2[8] = a2.x;
+    }
     {
         // moments -> 2D gradient, with the conic the pixels used; fp64 because
         // A m_x and B m_y can nearly cancel for elongated footprints
@@ -1135,9 +1178,12 @@ hipError_t launch_loss_l1(const float* img, const float* target, int32_t width, 
     return hipGetLastError();
 }
 
-// Workspace: the pair slots (capacity x kSlot floats).
-size_t raster_bwd_ws_bytes(int32_t, uint32_t capacity) {
-    return align256(sizeof(float) * kSlot * (size_t)(capacity > 0 ? capacity : 1));
+// Workspace: the pair slots (capacity x kSlot floats), then the slot sums of
+// the visible rows (n x kSlot floats; the pixel half alone needs only the
+// slots, n = 0).
+size_t raster_bwd_ws_bytes(int32_t n, uint32_t capacity) {
+    return align256(sizeof(float) * kSlot * (size_t)(capacity > 0 ? capacity : 1)) +
+           (n > 0 ? align256(sizeof(float) * kSlot * (size_t)n) : 0);
 }
 
 hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs_proj& proj, const uint32_t* vals,
@@ -1156,6 +1202,9 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || scene.n == 0 || !(stages & 2)) return e;
     const dim3 grid(div_up(scene.n, GS_BLOCK));
+    float* sums = slots + align256(sizeof(float) * kSlot * (size_t)(capacity > 0 ? capacity : 1)) / sizeof(float);
+    hipLaunchKernelGGL(k_slot_sum, grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles, pair_offset, slots,
+                       capacity, sums);
     if (union_idx) {
         if (first) {
             uint32_t cb = div_up((uint64_t)scene.n * (uint64_t)(grad_ld / 4), GS_BLOCK);
@@ -1165,8 +1214,8 @@ hipError_t launch_raster_bwd(const gs_scene& scene, const CamArgs& cam, const gs
         }
     }
 #define GS_LAUNCH_PBWD(D, A)                                                                                     \
-    hipLaunchKernelGGL((k_project_bwd<D, A>), grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, proj.tiles,        \
-                       pair_offset, slots, capacity, reinterpret_cast<const float4*>(proj.conic_opacity),         \
+    hipLaunchKernelGGL((k_project_bwd<D, A>), grid, dim3(GS_BLOCK), 0, st, vis_idx, vis_count, sums,             \
+                       reinterpret_cast<const float4*>(proj.conic_opacity),                                       \
                        proj.clamp, scene.mean, scene.log_scale, scene.quat, scene.opacity, scene.sh,              \
                        scene_ld(scene), cam,                                                                      \
                        grad_rows, grad_ld, grad2d, grad_norm, union_idx, union_count)
