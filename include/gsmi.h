@@ -653,7 +653,14 @@ gs_status gs_rlg_build(int32_t n_items, int32_t n_tracks, const int64_t* item_pt
  * ascending order, each group taking at most ceil(n / K) views, and moves
  * each centre to its members' mean (summed in ascending view order).  It
  * stops when a round repeats the previous assignment or after max_iters
- * rounds.  The region-level coupling summary coupling[a*K + b] is the sum
+ * rounds.  The groups are then refined on the graph, so that strong coupling
+ * stays within groups (the goal Section 4.2 sets for a partition): in passes
+ * over the views in ascending order (at most 16, until one moves nothing), a
+ * view moves to the group its edges weigh most towards (weights summed by
+ * ascending neighbour; lowest group on ties) when that exceeds the weight
+ * towards its own group, keeping every group size within floor(n / K) - s ..
+ * ceil(n / K) + s, s = max(1, ceil(n / K) / 16).  The region-level coupling
+ * summary coupling[a*K + b] is the sum
  * of the retained edge weights between groups a and b (within group a for
  * a = b), summed by ascending view, then neighbour.
  *

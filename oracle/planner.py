@@ -19,8 +19,14 @@ What each function follows:
   * ``lp_partition``: logical partitioning (Section 4.2, LP) into K groups
     by balanced k-means over the camera centres (MacQueen / Lloyd
     iterations with a capacity of ceil(n / K) views per group), seeded by
-    farthest-point selection from view 0; the region-level coupling summary
-    is the sum of retained edge weights between (and within) groups.
+    farthest-point selection from view 0, then refined on the RLG so that
+    strong coupling stays within groups: in passes over the views in
+    ascending order, a view moves to the group its retained edges weigh most
+    towards when that weight exceeds the weight towards its own group, within
+    a balance band of the group sizes (floor(n / K) - s .. ceil(n / K) + s,
+    s = max(1, ceil(n / K) // 16)), until a pass moves nothing (at most
+    ``REFINE_PASSES``); the region-level coupling summary is the sum of
+    retained edge weights between (and within) groups.
   * ``sds_order``: static data scheduling (Section 4.2, SDS, Eq. 2): a cyclic
     traversal of the non-empty groups that starts at the first one and
     repeatedly moves to the least-coupled unvisited group; task units of
@@ -125,6 +131,46 @@ def _sqdist(p, c) -> float:
     return dx * dx + dy * dy + dz * dz
 
 
+REFINE_PASSES = 16
+
+
+def refine_groups(group: List[int], rlg: RLG, K: int) -> None:
+    """The LP refinement (module docstring), in place.  A view's weight
+    towards each group is the sum of its retained edge weights, neighbours in
+    ascending order; the move goes to the group of largest gain over the own
+    group (the lowest such group on ties), if the gain is positive, that group
+    is below the band's top and the own group above its bottom."""
+    n = len(group)
+    if n == 0 or K < 2:
+        return
+    base, top = n // K, -(-n // K)
+    slack = max(1, top // 16)
+    lo, hi = base - slack, top + slack
+    size = [0] * K
+    for g in group:
+        size[g] += 1
+    for _ in range(REFINE_PASSES):
+        moved = False
+        for u in range(n):
+            a = group[u]
+            W = [0.0] * K
+            for j, w in rlg.neighbours(u):
+                W[group[j]] += w
+            best, gain = -1, 0.0
+            for b in range(K):
+                if b != a and (size[b] < hi or _mut() == 28):      # planted (28): no top of the band
+                    d = W[b] - W[a]
+                    if d > gain:
+                        best, gain = b, d
+            if best >= 0 and size[a] > lo:
+                group[u] = best
+                size[a] -= 1
+                size[best] += 1
+                moved = True
+        if not moved:
+            break
+
+
 @dataclasses.dataclass
 class Partition:
     group: np.ndarray          # [n] int32
@@ -172,6 +218,8 @@ def lp_partition(position: np.ndarray, rlg: RLG, K: int, max_iters: int) -> Part
                     c += 1
             if c:
                 centres[g] = (sx / c, sy / c, sz / c)
+    if _mut() != 27:                                  # planted (27): no refinement
+        refine_groups(assign, rlg, K)
     C = [[0.0] * K for _ in range(K)]
     for i in range(n):
         for j, w in rlg.neighbours(i):

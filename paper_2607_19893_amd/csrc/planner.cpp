@@ -1,6 +1,7 @@
 // Ahead-of-time planner on the host: the relative locality graph (Section
-// 4.1.1, Eq. 1), logical partitioning (Section 4.2, LP) and static data
-// scheduling (Section 4.2, SDS, Eq. 2).
+// 4.1.1, Eq. 1), logical partitioning (Section 4.2, LP: balanced k-means over
+// the camera centres, refined on the graph so that strong coupling stays
+// within groups) and static data scheduling (Section 4.2, SDS, Eq. 2).
 //
 // Every floating-point value is produced by one fixed sequence of IEEE double
 // operations (this file is built without FMA contraction), so the results do
@@ -189,6 +190,9 @@ int check_graph(int32_t n, const int64_t* edge_ptr, const int32_t* edge_dst, con
     return GS_OK;
 }
 
+// Passes of the LP refinement at most.
+constexpr int kRefinePasses = 16;
+
 int lp_partition(int32_t n, const double* pos, const int64_t* edge_ptr, const int32_t* edge_dst,
                  const double* edge_w, int32_t K, int32_t max_iters, int32_t* group, double* coupling,
                  int32_t* iters_run, char* err, size_t errlen) {
@@ -253,6 +257,45 @@ int lp_partition(int32_t n, const double* pos, const int64_t* edge_ptr, const in
         for (int32_t g = 0; g < K; ++g)
             if (c[g])
                 for (int k = 0; k < 3; ++k) cen[3 * g + k] = sum[3 * g + k] / (double)c[g];
+    }
+    // Refinement on the graph, so that strong coupling stays within groups: in
+    // passes over the views in ascending order, a view moves to the group its
+    // retained edges weigh most towards (neighbours summed in ascending order;
+    // the lowest group on ties) when that beats the weight towards its own
+    // group, within the size band floor(n/K) - s .. ceil(n/K) + s, s =
+    // max(1, ceil(n/K) / 16); until a pass moves nothing.
+    if (K >= 2) {
+        const int32_t top = (n + K - 1) / K;
+        const int32_t slack = std::max(1, top / 16);
+        const int32_t lo = n / K - slack, hi = top + slack;
+        std::vector<int32_t> size((size_t)K, 0);
+        for (int32_t i = 0; i < n; ++i) ++size[cur[i]];
+        std::vector<double> W((size_t)K);
+        for (int pass = 0; pass < kRefinePasses; ++pass) {
+            bool moved = false;
+            for (int32_t u = 0; u < n; ++u) {
+                const int32_t a = cur[u];
+                std::fill(W.begin(), W.end(), 0.0);
+                for (int64_t e = edge_ptr[u]; e < edge_ptr[u + 1]; ++e) W[cur[edge_dst[e]]] += edge_w[e];
+                int32_t best = -1;
+                double gain = 0.0;
+                for (int32_t b = 0; b < K; ++b) {
+                    if (b == a || size[b] >= hi) continue;
+                    const double d = W[b] - W[a];
+                    if (d > gain) {
+                        best = b;
+                        gain = d;
+                    }
+                }
+                if (best >= 0 && size[a] > lo) {
+                    cur[u] = best;
+                    --size[a];
+                    ++size[best];
+                    moved = true;
+                }
+            }
+            if (!moved) break;
+        }
     }
     for (int32_t i = 0; i < n; ++i) group[i] = cur[i];
     // region-level coupling: retained edge weights summed per group pair, views ascending

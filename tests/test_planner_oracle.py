@@ -138,8 +138,70 @@ def check_lp_examples(o):
     assert P.coupling.tolist() == [[0.5, 0.25], [0.25, 0.5]]
 
 
+def check_lp_refinement(o):
+    # two clusters of four on a line, K = 2: k-means puts views 0-3 and 4-7 together; view 3's
+    # retained edges go mostly to views 4-6 (7/8 each) and weakly to view 0 (1/8), so the
+    # refinement moves it (band 4 +- 1: group sizes 3 and 5 allowed) and nothing else moves
+    edges = [(0, 1, 0.5), (1, 2, 0.5), (0, 2, 0.5), (0, 3, 0.125), (3, 4, 0.875), (3, 5, 0.875),
+             (3, 6, 0.875), (4, 5, 0.5), (5, 6, 0.5), (6, 7, 0.5)]
+    R = hand_graph(o, 8, edges)
+    pos = line([0, 0.1, 0.2, 0.3, 10, 10.1, 10.2, 10.3])
+    P = o.lp_partition(pos, R, 2, 10)
+    assert list(P.group) == [0, 0, 0, 1, 1, 1, 1, 1]
+    # within: {0,1,2} 3 x 1/2; {3..7} 3 x 7/8 + 3 x 1/2; across: the 0-3 edge
+    assert P.coupling.tolist() == [[1.5, 0.125], [0.125, 4.125]]
+    # three clusters of four at x = 0, 10, 20, K = 3 (k-means groups 0, 2, 1 by the seeding order):
+    # the first cluster's views tied to each other (1 each) and to every other view (3/4 each),
+    # so they gain nothing by moving; the others gain 3 by joining group 0, but only view 4 (the
+    # first in ascending order) may: group 0 is then at the band's top (4 + 1)
+    edges = [(i, j, 1.0) for i in range(4) for j in range(i + 1, 4)]
+    edges += [(i, j, 0.75) for i in range(4) for j in range(4, 12)]
+    pos3 = line([0, 0.1, 0.2, 0.3, 10, 10.1, 10.2, 10.3, 20, 20.1, 20.2, 20.3])
+    P = o.lp_partition(pos3, hand_graph(o, 12, edges), 3, 10)
+    assert [int(g) for g in P.group] == [0, 0, 0, 0, 0, 2, 2, 2, 1, 1, 1, 1], list(P.group)
+
+
+def cut_weight(R, group):
+    return sum(w for i in range(len(group)) for j, w in R.neighbours(i) if j > i and group[i] != group[j])
+
+
 def test_lp_worked_examples(orc):
     check_lp_examples(orc)
+    check_lp_refinement(orc)
+
+
+def test_lp_refinement_lowers_the_cut(orc):
+    """On random captures the refinement never raises the weight across
+    groups, keeps the sizes in the band, and leaves a partition in which no
+    single move within the band would lower the cut."""
+    for seed in range(4):
+        rng = np.random.default_rng(seed)
+        n = 60
+        pos = rng.normal(0, 1, (n, 3))
+        edges = [(i, j, float(rng.integers(1, 9)) / 8.0) for i in range(n) for j in range(i + 1, n)
+                 if rng.random() < 0.08]
+        R = hand_graph(orc, n, edges)
+        K = 3
+        orc.set_mutation(27)
+        try:
+            P0 = orc.lp_partition(pos, R, K, 20)
+        finally:
+            orc.set_mutation(0)
+        P = orc.lp_partition(pos, R, K, 20)
+        assert cut_weight(R, P.group) <= cut_weight(R, P0.group)
+        top = -(-n // K)
+        slack = max(1, top // 16)
+        sizes = np.bincount(P.group, minlength=K)
+        assert sizes.min() >= n // K - slack and sizes.max() <= top + slack
+        # local optimality within the band (when the passes ended by themselves)
+        g = list(P.group)
+        for u in range(n):
+            W = np.zeros(K)
+            for j, w in R.neighbours(u):
+                W[g[j]] += w
+            for b in range(K):
+                if b != g[u] and sizes[b] < top + slack and sizes[g[u]] > n // K - slack:
+                    assert W[b] <= W[g[u]], (seed, u, b)
 
 
 def test_lp_blobs_and_balance(orc):
@@ -256,7 +318,8 @@ def test_sds_rule_on_random_schedules(orc):
 # ---------------------------------------------------------------------------
 
 PLANNER_MUTATIONS = {16: check_rlg_example, 17: check_rlg_example, 18: check_rlg_brute_force,
-                     19: check_lp_examples, 20: check_sds_examples, 21: check_sds_examples}
+                     19: check_lp_examples, 20: check_sds_examples, 21: check_sds_examples,
+                     27: check_lp_refinement, 28: check_lp_refinement}
 
 
 @pytest.mark.parametrize("k", sorted(PLANNER_MUTATIONS))
