@@ -32,7 +32,10 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gs_oracle.c")
-_LIB = os.path.join(_HERE, "liborc.so")
+# GS_ORACLE_LIB names another build of gs_oracle.c to load (the sanitizer
+# test's instrumented one); it is used as it is, never rebuilt here.
+_LIB_OVERRIDE = os.environ.get("GS_ORACLE_LIB")
+_LIB = _LIB_OVERRIDE or os.path.join(_HERE, "liborc.so")
 TILE = 16
 
 
@@ -60,7 +63,7 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        if not _LIB_OVERRIDE and (not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC)):
             build(force=True)
         L = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p

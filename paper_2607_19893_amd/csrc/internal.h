@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include "../../include/gsmi.h"
+#include "planner.h"
 
 namespace gsmi {
 
@@ -120,17 +121,5 @@ hipError_t launch_publish_commit(const gs_ring& ring, uint32_t version, const gs
 hipError_t launch_delta_apply(const void* msg, size_t msg_capacity, const gs_group* dst, int32_t n_groups,
                               int32_t n_rows, int32_t max_rows, int32_t mode, uint32_t* prim_version,
                               gs_device_status* status, hipStream_t st);
-
-// planner.cpp (host): return GS_OK, GS_ERR_INVALID_ARG (message in err) or GS_ERR_WORKSPACE
-int rlg_build(int32_t n, int32_t n_tracks, const int64_t* item_ptr, const int32_t* item_tracks, int32_t track_cap,
-              int32_t top_k, int64_t* edge_ptr, int32_t* edge_dst, double* edge_w, int64_t edge_capacity,
-              int64_t* n_edges, char* err, size_t errlen);
-int lp_partition(int32_t n, const double* pos, const int64_t* edge_ptr, const int32_t* edge_dst,
-                 const double* edge_w, int32_t K, int32_t max_iters, int32_t* group, double* coupling,
-                 int32_t* iters_run, char* err, size_t errlen);
-int sds_order(int32_t n, const int32_t* group, int32_t K, const double* coupling, const int64_t* edge_ptr,
-              const int32_t* edge_dst, const double* edge_w, int32_t unit_size, int32_t* cycle, int32_t* n_cycle,
-              int32_t* order, int32_t* unit_group, double* transition, int32_t* n_units, char* err,
-              size_t errlen);
 
 }  // namespace gsmi

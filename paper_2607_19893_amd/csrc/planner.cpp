@@ -14,7 +14,7 @@
 #include <thread>
 #include <vector>
 
-#include "internal.h"
+#include "planner.h"
 
 namespace gsmi {
 
