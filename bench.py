@@ -239,6 +239,39 @@ OTHER_STEPS, OTHER_WARMUP = 24, 6
 DELTA_WORKLOADS = ("spiral", "aerial")
 
 
+_RENDERERS = {}
+
+
+def gpu_render(scene, cam):
+    """Target image of a workload whose targets are renders of its perturbed
+    copy: the copy rendered by the library's own projection, binning and
+    forward raster (made once per workload before any timing)."""
+    import torch
+    from paper_2607_19893_amd.pipeline import ViewTrainer
+    key = id(scene)
+    tr = _RENDERERS.get(key)
+    if tr is None:
+        _RENDERERS.clear()
+        tr = _RENDERERS[key] = ViewTrainer(scene, capacity=1, max_width=cam.width, max_height=cam.height)
+    if cam.width > tr.width or cam.height > tr.height:
+        tr._set_image(cam.width, cam.height)
+    tr.ensure_capacity([cam])
+    tr.project(cam)
+    tr.visible()
+    tr.bin_sort()
+    tr.raster_fwd(active=False)
+    torch.cuda.synchronize()
+    n = cam.width * cam.height
+    return tr.img.view(-1)[:3 * n].cpu().numpy().reshape(3, cam.height, cam.width).copy()
+
+
+def oracle_render(scene, cam):
+    """The same target image made by the CPU oracle (its timing legs only)."""
+    import oracle
+    pr = oracle.project(scene, cam, 0)
+    return oracle.render(oracle.visible(pr.tiles), pr, cam).img.astype(np.float32)
+
+
 def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False, id_order="spatial"):
     """Build the workload, store its primitives in `id_order` ("spatial": the
     pool's Morton order; "given": the generator's order), make its inputs
@@ -264,7 +297,8 @@ def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False
     need = tr.ensure_capacity(cams)
     log("pair capacity %d (max pairs over the views %d)" % (tr.capacity, need))
     t0 = time.time()
-    targets = [torch.from_numpy(w.target(i).reshape(-1)).to(tr.dev) for i in range(len(cams))]
+    targets = [torch.from_numpy(w.target(i, render=gpu_render).reshape(-1)).to(tr.dev) for i in range(len(cams))]
+    _RENDERERS.clear()
     log("targets resident (%.1fs)" % (time.time() - t0))
 
     # pair statistics per view (untimed): evaluated / included (pixel, pair) counts
@@ -481,7 +515,7 @@ def oracle_stage_times():
         tot = {}
         t0 = time.perf_counter()
         for k, i in enumerate(views):
-            r = oracle.train_view(w.scene, w.cameras[i], w.target(i), m, v, k + 1, lr=w.lr)
+            r = oracle.train_view(w.scene, w.cameras[i], w.target(i, render=oracle_render), m, v, k + 1, lr=w.lr)
             for st, t in r.times.items():
                 tot[st] = tot.get(st, 0.0) + t
         dt = time.perf_counter() - t0
@@ -654,7 +688,8 @@ def cpu_baseline(w, nviews):
     v = [np.zeros_like(a) for _, a in w.scene.groups()]
     for i in range(nviews):
         cam = w.cameras[i % len(w.cameras)]
-        oracle.train_view(w.scene, cam, w.target(i), m, v, i + 1, lr=w.lr, with_pairs=False)
+        oracle.train_view(w.scene, cam, w.target(i, render=oracle_render), m, v, i + 1, lr=w.lr,
+                          with_pairs=False)
         done += 1
     dt = time.perf_counter() - t0
     return {"value": round(done / dt, 4), "unit": "views/s", "cores": oracle.num_threads(), "kind": "oracle",

@@ -106,14 +106,32 @@ class Workload:
     scene: Scene
     cameras: List[Camera]
     seed: int
-    target_kind: str      # "uniform" or "smooth"
+    target_kind: str      # "uniform", "smooth" or "perturbed"
     lr: float = 1e-3
     beta1: float = 0.9
     beta2: float = 0.999
     eps: float = 1e-15
+    # storage order of the primitives: row i is row perm[i] of the generated
+    # scene (None: the generator's order)
+    perm: Optional[np.ndarray] = None
 
-    def target(self, view: int) -> np.ndarray:
+    def target_scene(self) -> "Scene":
+        """The perturbed copy of the scene whose renders are the "perturbed"
+        targets (the same physical scene whatever the storage order)."""
+        return perturbed_copy(self.scene, self.seed, self.perm)
+
+    def target(self, view: int, render=None) -> np.ndarray:
+        """Target image [3,H,W] fp32 of a view.  "perturbed" targets are renders
+        of target_scene() from the view's camera, made by the caller's
+        render(scene, camera) (this module draws inputs and renders nothing)."""
         cam = self.cameras[view % len(self.cameras)]
+        if self.target_kind == "perturbed":
+            if render is None:
+                raise ValueError("%s: targets are renders of the perturbed copy; pass render(scene, camera)"
+                                 % self.name)
+            if getattr(self, "_target_scene", None) is None:
+                self._target_scene = self.target_scene()
+            return np.ascontiguousarray(render(self._target_scene, cam), dtype=np.float32)
         return make_target(cam.width, cam.height, self.seed, view, self.target_kind)
 
 
@@ -187,6 +205,27 @@ def _finish(rng, mean, ls_mu, ls_sd, logit_sd, logit_mu, degree, dc_kind) -> Sce
                  opacity=opacity, sh=sh, sh_degree=degree)
 
 
+def perturbed_copy(scene: "Scene", seed: int, perm: Optional[np.ndarray] = None) -> "Scene":
+    """A seeded perturbation of a scene, the stand-in for the scene a set of
+    photographs shows: means moved by N(0, 0.02) per axis, log-scales by
+    N(0, 0.1), quaternion components by N(0, 0.05), opacity logits by N(0, 0.5)
+    and every SH coefficient by N(0, 0.05).  The noise is drawn in the
+    generator's order; perm (row i of `scene` is generated row perm[i]) picks
+    each stored row's own noise."""
+    rng = np.random.default_rng([seed, 4241])
+    n = scene.n
+    f32 = np.float32
+    pick = (lambda a: a) if perm is None else (lambda a: a[perm])
+    noise = [normals(rng, (n, 3)), normals(rng, (n, 3)), normals(rng, (n, 4)), normals(rng, scene.opacity.shape),
+             normals(rng, scene.sh.shape)]
+    return Scene(mean=(scene.mean + pick(noise[0]) * f32(0.02)).astype(f32),
+                 log_scale=(scene.log_scale + pick(noise[1]) * f32(0.1)).astype(f32),
+                 quat=(scene.quat + pick(noise[2]) * f32(0.05)).astype(f32),
+                 opacity=(scene.opacity + pick(noise[3]) * f32(0.5)).astype(f32),
+                 sh=(scene.sh + pick(noise[4]) * f32(0.05)).astype(f32),
+                 sh_degree=scene.sh_degree)
+
+
 def make_target(width: int, height: int, seed: int, view: int, kind: str) -> np.ndarray:
     """Target image [3,H,W] in [0,1].
 
@@ -250,7 +289,7 @@ def ring(seed: int = 1, n: int = 200_000, width: int = 1280, height: int = 720) 
         th = 2 * math.pi * i / 8
         eye = (6.0 * math.cos(th), 0.0, 6.0 * math.sin(th))
         cams.append(look_at(eye, (0.0, 0.0, 0.0), (0.0, -1.0, 0.0), width, height, 60.0))
-    return Workload("ring-200k-L3-720p", scene, cams, seed, "smooth")
+    return Workload("ring-200k-L3-720p", scene, cams, seed, "perturbed")
 
 
 def room(seed: int = 2, n: int = 1_000_000, width: int = 1920, height: int = 1080) -> Workload:
@@ -382,7 +421,8 @@ def spatial_order(mean: np.ndarray) -> np.ndarray:
 
 def spatially_ordered(w: Workload) -> Workload:
     """The workload with its primitives stored in spatial order (same cameras, targets and content)."""
-    return dataclasses.replace(w, scene=w.scene.permuted(spatial_order(w.scene.mean)))
+    p = spatial_order(w.scene.mean)
+    return dataclasses.replace(w, scene=w.scene.permuted(p), perm=p if w.perm is None else w.perm[p])
 
 
 def random_scene(seed: int, n: int, degree: int, extent: float = 1.0, ls_mu: float = -2.5,

@@ -100,3 +100,16 @@ def expected_tile_order(ranges):
     ranges = np.asarray(ranges, np.int64).reshape(-1, 2)
     codes = np.array([order_code(e - s) for s, e in ranges], np.int64)
     return np.lexsort((np.arange(codes.size), -codes)).astype(np.uint32)
+
+
+def oracle_render(scene, cam):
+    """The oracle's image of a scene from a camera (fp32), for targets that are
+    renders of a workload's perturbed copy."""
+    import oracle as orc
+    pr = orc.project(scene, cam, 0)
+    return orc.render(orc.visible(pr.tiles), pr, cam).img.astype(np.float32)
+
+
+def target_of(w, view):
+    """A workload's target image for a view, renders made by the oracle."""
+    return w.target(view, render=oracle_render)

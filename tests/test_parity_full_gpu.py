@@ -31,6 +31,7 @@ import numpy as np
 import pytest
 
 from parity_util import AMB_SHARE, GRAD_RTOL, assert_grads, assert_pixels, expected_tile_order, grad_floor
+from parity_util import target_of
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -62,7 +63,7 @@ def test_full_view(name, orc):
     _say(name, "generated n=%d in %.1fs" % (n, time.time() - t0))
     tr = ViewTrainer(w.scene, capacity=1, max_width=W, max_height=H, lr=w.lr, with_keys=True)
     tr.ensure_capacity(w.cameras[:1])
-    tgt = w.target(0)
+    tgt = target_of(w, 0)
     tr.set_target(tgt)
 
     # oracle: projection, visible set, pairs, render, and the ambiguous pixels

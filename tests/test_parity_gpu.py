@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 
 from parity_util import AMB_SHARE, assert_grads, assert_pixels, expected_tile_order
+from parity_util import target_of
 
 pytestmark = pytest.mark.gpu
 
@@ -161,7 +162,7 @@ def test_loss_l1(case, torch_gpu, orc):
     w = get_case(case)
     tr = trainer_for(w, torch_gpu)
     cam = w.cameras[0]
-    tgt = w.target(0)
+    tgt = target_of(w, 0)
     tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd()
     tr.set_target(tgt)
     tr.loss_l1()
@@ -182,7 +183,7 @@ def test_raster_fwd_l1_matches_separate_calls(case, torch_gpu, orc):
     w = get_case(case)
     tr = trainer_for(w, torch_gpu)
     cam = w.cameras[0]
-    tr.set_target(w.target(0))
+    tr.set_target(target_of(w, 0))
     tr.project(cam); tr.visible(); tr.bin_sort()
     tr.raster_fwd(active=True); tr.loss_l1()
     torch_gpu.cuda.synchronize()
@@ -607,7 +608,7 @@ def test_pair_overflow_leaves_state_untouched(torch_gpu, orc):
     torch = torch_gpu
     w = get_case("tiny-10k-256")
     tr = trainer_for(w, torch, capacity=1000)
-    tr.set_target(w.target(0))
+    tr.set_target(target_of(w, 0))
     tr.ws_bwd.view(torch.float32).fill_(1.0)        # stale slots of an earlier view
     tr.grad_rows.fill_(7.0)
     snap = lambda: [t.clone() for t in (*tr.params, tr.m, tr.v, *tr.msgs, *tr.replica, tr.version, tr.ring_state)]
@@ -670,7 +671,7 @@ def test_empty_and_degenerate(torch_gpu, orc):
     w = scenes.tiny(n=500)
     w.scene.mean[:, 2] = -10.0
     tr = trainer_for(w, torch_gpu, capacity=1024)
-    tr.set_target(w.target(0))
+    tr.set_target(target_of(w, 0))
     tr.step(w.cameras[0], step=1)
     torch_gpu.cuda.synchronize()
     assert int(u32(tr.counts[0:1])[0]) == 0 and int(u32(tr.counts[1:2])[0]) == 0
@@ -692,7 +693,7 @@ def test_dispatch_order_changes_no_result(case, torch_gpu, orc):
         tr = trainer_for(w, torch_gpu)
         tr.longest_first = longest_first
         cam = w.cameras[1]
-        tr.set_target(w.target(1))
+        tr.set_target(target_of(w, 1))
         tr.pair_stats.zero_()
         tr.project(cam); tr.visible(); tr.bin_sort()
         tr.raster_fwd(active=True, stats=True)
@@ -742,7 +743,7 @@ def test_backward_halves_match_combined(torch_gpu, orc):
     w = get_case("room-60k-392x216")
     tr = trainer_for(w, torch_gpu)
     cam = w.cameras[0]
-    tr.set_target(w.target(0))
+    tr.set_target(target_of(w, 0))
     tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd(); tr.loss_l1()
     tr.raster_bwd(grad2d=True)
     torch_gpu.cuda.synchronize()
@@ -765,7 +766,7 @@ def test_step_matches_phase_calls(torch_gpu, orc):
     for fast in (True, False):
         tr = trainer_for(w, torch_gpu)
         for s, cam in enumerate(w.cameras[:2], start=1):
-            tgt = torch_gpu.from_numpy(w.target(s - 1).reshape(-1)).cuda()
+            tgt = torch_gpu.from_numpy(target_of(w, s - 1).reshape(-1)).cuda()
             if fast:
                 tr.step(cam, step=s, version=s, target=tgt)
             else:
@@ -787,7 +788,7 @@ def test_overlapped_publication_matches_sequential(torch_gpu, orc):
     runs = []
     for overlap in (False, True):
         tr = trainer_for(w, torch_gpu)
-        tr.set_target(w.target(0))
+        tr.set_target(target_of(w, 0))
         for s in range(1, 6):
             tr.step(cam, step=s, version=s, overlap=overlap)
         tr.flush_apply()
@@ -822,7 +823,7 @@ def test_record_table_matches_dense_groups(case, torch_gpu, orc):
             assert tr.params[1].data_ptr() == tr.params[2].data_ptr() + 16
         for s in range(1, 4):
             k = (s - 1) % len(w.cameras)
-            tgt = torch_gpu.from_numpy(w.target(k).reshape(-1)).cuda()
+            tgt = torch_gpu.from_numpy(target_of(w, k).reshape(-1)).cuda()
             tr.step(w.cameras[k], step=s, version=s, target=tgt)
         tr.flush_apply()
         torch_gpu.cuda.synchronize()

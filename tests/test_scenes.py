@@ -2,6 +2,7 @@
 primitive pool is a permutation that follows the Z-order curve, and storing
 the pool in it changes no rendered result (CPU oracle)."""
 import numpy as np
+import pytest
 
 from paper_2607_19893_amd import scenes
 
@@ -60,3 +61,22 @@ def test_permuted_scene_renders_the_same(orc):
     r1 = orc.render(orc.visible(p1.tiles), p1, cam)
     np.testing.assert_allclose(r1.img, r0.img, rtol=1e-12, atol=1e-15)
     np.testing.assert_array_equal(r1.active[np.argsort(perm)], r0.active)
+
+
+def test_perturbed_copy_is_one_scene_in_any_storage_order():
+    """The ring workload's targets are renders of a perturbed copy: the copy
+    of the spatially ordered pool is the copy of the generated pool, rows
+    permuted the same way (each primitive keeps its own noise), and it differs
+    from the pool itself by the stated noise scales."""
+    w = scenes.ring(n=5000, width=64, height=48)
+    assert w.target_kind == "perturbed"
+    ws = scenes.spatially_ordered(w)
+    a, b = w.target_scene(), ws.target_scene()
+    for x, y in zip(a.groups(), b.groups()):
+        np.testing.assert_array_equal(x[1][ws.perm], y[1])
+    d = (a.mean - w.scene.mean).std(), (a.opacity - w.scene.opacity).std(), (a.sh - w.scene.sh).std()
+    assert abs(d[0] - 0.02) < 0.002 and abs(d[1] - 0.5) < 0.05 and abs(d[2] - 0.05) < 0.005
+    with pytest.raises(ValueError):
+        w.target(0)
+    img = w.target(0, render=lambda sc, cam: np.full((3, cam.height, cam.width), 0.25, np.float32))
+    assert img.shape == (3, 48, 64) and img.dtype == np.float32

@@ -7,6 +7,7 @@ import sys
 
 import numpy as np
 import pytest
+from parity_util import target_of
 
 pytestmark = pytest.mark.gpu
 
@@ -255,7 +256,7 @@ def test_scopes_of_consecutive_room_views(torch_gpu, gs, orc):
     vis, act = {}, {}
     for k, cam in zip("AB", cams):
         tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd(active=True)
-        tr.loss_l1(target=torch.from_numpy(w.target(0 if k == "A" else 1).reshape(-1)).cuda())
+        tr.loss_l1(target=torch.from_numpy(target_of(w, 0 if k == "A" else 1).reshape(-1)).cuda())
         gs.gs_scope_from_pred(gs.GS_PRED_U32_NONZERO, tr.tiles, n, 0, sc["R" + k])
         gs.gs_scope_from_pred(gs.GS_PRED_U8_NONZERO, tr.active, n, 0, sc["W" + k])
         torch.cuda.synchronize()

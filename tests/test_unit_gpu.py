@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 
 from parity_util import GRAD_RTOL, assert_grads, grad_floor
+from parity_util import target_of
 
 pytestmark = pytest.mark.gpu
 
@@ -131,7 +132,7 @@ def test_unit_step_end_to_end(orc):
     w = scenes.room(n=60000, width=392, height=216)
     tr = ViewTrainer(w.scene, capacity=1, max_width=392, max_height=216, lr=w.lr)
     tr.ensure_capacity(w.cameras[:6])
-    targets = [torch.from_numpy(w.target(i).reshape(-1)).cuda() for i in range(6)]
+    targets = [torch.from_numpy(target_of(w, i).reshape(-1)).cuda() for i in range(6)]
     for u in range(3):
         tr.step_unit(w.cameras[2 * u:2 * u + 2], step=u + 1, version=u + 1, targets=targets[2 * u:2 * u + 2])
     torch.cuda.synchronize()

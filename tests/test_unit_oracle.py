@@ -8,6 +8,7 @@ import pytest
 
 from paper_2607_19893_amd import scenes
 from test_oracle_pins import _forward_loss, _perturbed
+from parity_util import target_of
 
 
 def two_cameras(W=40, H=32):
@@ -65,7 +66,7 @@ def check_unit_fd(o, seed=6, n=8, deg=2, tol=1e-5):
 def check_unit_rows(o):
     w = scenes.tiny(n=400)
     cams = [w.cameras[0], scenes.look_at((1.5, 0.0, -3.5), (0.5, 0.0, 0.0), (0.0, -1.0, 0.0), 96, 64, 40.0)]
-    tg = [w.target(0)[:, :c.height, :c.width] for c in cams]
+    tg = [target_of(w, 0)[:, :c.height, :c.width] for c in cams]
     union, grads, gnorm, views = o.unit_gradients(w.scene, cams, targets=tg)
     v0, v1 = views[0][0], views[1][0]
     np.testing.assert_array_equal(union, np.union1d(v0, v1).astype(np.uint32))
@@ -93,8 +94,8 @@ def test_one_view_unit_is_the_training_view(orc):
     cam = w.cameras[0]
     m0 = [np.zeros_like(a).reshape(w.scene.n, -1) for _, a in w.scene.groups()]
     v0 = [np.zeros_like(a) for a in m0]
-    u = orc.train_unit(w.scene, [cam], [w.target(0)], m0, v0, 1)
-    t = orc.train_view(w.scene, cam, w.target(0), m0, v0, 1)
+    u = orc.train_unit(w.scene, [cam], [target_of(w, 0)], m0, v0, 1)
+    t = orc.train_view(w.scene, cam, target_of(w, 0), m0, v0, 1)
     np.testing.assert_array_equal(u.union, t.vis)
     for a, b in zip(u.grads, t.grads.groups()):
         np.testing.assert_array_equal(a, b)
