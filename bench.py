@@ -142,6 +142,9 @@ def main():
     ap.add_argument("--id-order", choices=("spatial", "given"), default="spatial",
                     help="storage order of the primitive pool: spatial (Morton order of the means, a load-time "
                          "layout step) or given (the generator's order); the scene's content is the same")
+    ap.add_argument("--delta-only", action="store_true",
+                    help="only time the publication kernels alone (cold) on --workload and print them; for "
+                         "profiling those kernels")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy (read + write of this many MiB, 4 times) and exit; "
                          "its HBM counters calibrate the traffic counters of the path's kernels")
@@ -161,6 +164,10 @@ def main():
     torch.cuda.set_device(0)
     if args.apply_after is not None:
         ViewTrainer.APPLY_AFTER = args.apply_after
+    if args.delta_only:
+        r = run_workload(args.workload, 2, 1, overlap=not args.no_overlap, id_order=args.id_order)
+        print(json.dumps({"delta": {r["w"].name: bench_delta(r["tr"], r["cams"])}}), flush=True)
+        return
     run = run_workload(args.workload, args.steps, args.warmup, overlap=not args.no_overlap,
                        packed=not args.dense_params, row_major=args.row_major_tiles, id_order=args.id_order)
     tr, cams, targets, w = run.pop("tr"), run.pop("cams"), run.pop("targets"), run.pop("w")
@@ -494,6 +501,16 @@ def bench_delta(tr, cams, reps=20):
     b = K * (4 + P4) + 2.0 * K * P4 + 8 * K
     out["commit"] = {"ms": round(ms, 4), "gbs": round(b / ms / 1e6, 1), "frac": round(b / ms / 1e6 / HBM_PEAK_GBS, 4)}
     assert to_u32(tr.status)[0] == 0, "device status flags set by the publication kernels"
+    # for comparison: a library row gather of the same rows (torch.index_select of K rows of a
+    # row_len-float table by the same ascending ids), the access pattern with no arithmetic
+    table = torch.zeros(tr.n, tr.row_len, device=tr.dev)
+    ids = tr.vis_idx[:K].to(torch.int64)
+    dst = torch.empty(K, tr.row_len, device=tr.dev)
+    ms = timed(lambda: torch.index_select(table, 0, ids, out=dst))
+    b = 2.0 * K * P4 + 8 * K
+    out["row_gather_probe"] = {"ms": round(ms, 4), "gbs": round(b / ms / 1e6, 1),
+                               "frac": round(b / ms / 1e6 / HBM_PEAK_GBS, 4)}
+    del table, ids, dst
     return out
 
 
