@@ -226,7 +226,7 @@ def main():
         "config": {"workload": w.name, "gaussians": w.scene.n, "sh_degree": w.scene.sh_degree,
                    "width": cams[0].width, "height": cams[0].height, "views": len(cams),
                    "mean_visible": run["mean_visible"], "mean_pairs": run["mean_pairs"],
-                   "step": "project+visible+bin_sort+fwd_l1+bwd+sparse_adam_publish+commit",
+                   "step": "project+visible+bin_sort+fwd_l1+active_set+bwd+sparse_adam_publish+commit",
                    "apply_overlapped": not args.no_overlap,
                    "param_layout": "dense" if args.dense_params else "head8",
                    "id_order": args.id_order,

@@ -216,7 +216,10 @@ __global__ void __launch_bounds__(GS_BLOCK, STATS ? 5 : 7) k_raster_fwd(
     uint8_t* __restrict__ active, unsigned long long* __restrict__ pair_stats, const float* __restrict__ target,
     float inv_total, float* __restrict__ dL, float* __restrict__ loss_partial) {
     __shared__ SplatLds<GS_BLOCK> L;
-    __shared__ uint32_t s_hit[GS_BLOCK / 32];       // entries some pixel included (active flags)
+    // entries some pixel included (active flags): every including lane stores 1 to
+    // the entry's byte, plain stores of one value (LDS atomics on one word from a
+    // whole row serialize)
+    __shared__ uint8_t s_hit[GS_BLOCK];
     __shared__ uint8_t s_list[4][4][GS_BLOCK];
     __shared__ uint32_t s_stat[4][4];
     const uint32_t tile = dispatch_tile(tile_order);
@@ -245,7 +248,7 @@ __global__ void __launch_bounds__(GS_BLOCK, STATS ? 5 : 7) k_raster_fwd(
         const uint32_t gj = g;
         if (j < end) stage_splat(L, tid, mean2d[gj], conic_op[gj], rgb + 3 * (size_t)gj);
         if (j + GS_BLOCK < end) g = vals[j + GS_BLOCK];
-        if (tid < GS_BLOCK / 32) s_hit[tid] = 0u;
+        s_hit[tid] = 0;
         __syncthreads();
         const int nb = (int)min((uint32_t)GS_BLOCK, end - bs);
         // rows whose 16 pixels are all finished take no entries
@@ -299,10 +302,10 @@ __global__ void __launch_bounds__(GS_BLOCK, STATS ? 5 : 7) k_raster_fwd(
                     w_hit += ((om >> (16 * q)) & 0xFFFFull) ? 1u : 0u;
                 }
             }
-            if (active != nullptr && ok) atomicOr(&s_hit[k >> 5], 1u << (k & 31));
+            if (active != nullptr && ok) s_hit[k] = 1;
         }
         __syncthreads();
-        if (active && j < end && ((s_hit[tid >> 5] >> (tid & 31)) & 1u)) active[gj] = 1;
+        if (active && j < end && s_hit[tid]) active[gj] = 1;
     }
     if (STATS) {
         // entries the per-pixel definition examines: up to and including the
@@ -466,8 +469,9 @@ constexpr int kBwdBatch = GS_WAVE;
 // line because ds = -dL/dalpha * o e^-sigma below the 0.99 cap, and both are 0
 // at it).  A pixel row shares dy, so a row needs only m, m_x and m_xx (plus
 // the three colour sums) over its lanes.  A row visits an entry at most once
-// per batch, so its leader stores the six sums with plain LDS writes into the
-// row's own record of that entry (no atomics); after the walk lane k of each
+// per batch, so two lanes of the row (one holding the moment sums, one the
+// colour sums) store the six sums with plain LDS writes into the row's own
+// record of that entry (no atomics); after the walk lane k of each
 // wave scales its four rows' records of entry k by their dy and adds them,
 // and the four waves' results are added in a fixed order.  A pair slot holds
 // (m_x, m_y, m_xx, m_xy, m_yy, m, colour); k_project_bwd expands it with the
@@ -511,6 +515,8 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     if (last > 0) atomicMax(&s_max, last);
     __syncthreads();
     const uint32_t maxlast = s_max;
+    const bool hi_half = (lane & 8) != 0;       // high half of the lane's 16-lane row
+    const int q_half = hi_half ? 3 : 0;         // the half's three sums in a row record
     // largest n_contrib of each pixel row of this wave (wave-uniform values)
     uint32_t rl = last;
 #pragma unroll
@@ -523,6 +529,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
         const uint32_t bs = (uint32_t)(be > kBwdBatch ? be - kBwdBatch : 0);
         const uint32_t cnt = (uint32_t)be - bs;
         const bool work = bs < maxlast;
+        const uint32_t last_b = last > bs ? last - bs : 0u;    // the pixel's entries in this batch: k < last_b
         if ((uint32_t)tid < cnt && work) {
             const uint32_t g = vals[start + bs + tid];
             stage_splat(L, tid, mean2d[g], conic_op[g], rgb + 3 * (size_t)g);
@@ -563,10 +570,10 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             const float e = exp_neg(sigma);
             const float gv = R.o * e;
             const float alpha = fminf(kAlphaMax, gv);
-            const bool ok = act && bs + (uint32_t)k < last && !(sigma < 0.0f) && !(alpha < kAlphaMin);
+            const bool ok = act && (uint32_t)k < last_b && !(sigma < 0.0f) && !(alpha < kAlphaMin);
             // the lanes of ok, as ballots of the comparisons themselves (a ballot of a
             // compare is its lane mask; a ballot of a combined flag costs two VALU ops)
-            const uint64_t mask = act_mask & __builtin_amdgcn_ballot_w64(bs + (uint32_t)k < last) &
+            const uint64_t mask = act_mask & __builtin_amdgcn_ballot_w64((uint32_t)k < last_b) &
                                   __builtin_amdgcn_ballot_w64(!(sigma < 0.0f)) &
                                   __builtin_amdgcn_ballot_w64(!(alpha < kAlphaMin));
             if (mask == 0ull) continue;
@@ -581,28 +588,39 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             const bool geo = ok && gv < kAlphaMax;      // the 0.99 cap stops d/d(opacity, sigma)
             const float ds = geo ? -dalpha * alpha : 0.0f;
             const float dsx = ds * (float)ddx;
-            float gr[kRowSums];
-            gr[0] = ds;
-            gr[1] = dsx;
-            gr[2] = dsx * (float)ddx;
-            gr[3] = gC0 * wgt;
-            gr[4] = gC1 * wgt;
-            gr[5] = gC2 * wgt;
-            // sum each 16-lane row (all its lanes hold the same entry) with DPP, then
-            // one lane per contributing row stores the sums in the row's record
+            // the six sums over each 16-lane row (all its lanes hold the same entry)
+            // in 18 DPP adds instead of 24: the first stage pairs lane i with lane
+            // 15 - i, the low half of the row keeping the three moment terms and the
+            // high half the three colour terms (each adds its partner's copy of the
+            // term it keeps); three butterfly stages within each half of eight lanes
+            // then leave the moment sums in every low lane and the colour sums in
+            // every high lane
+            const float mo[3] = {ds, dsx, dsx * (float)ddx};
+            const float co[3] = {gC0 * wgt, gC1 * wgt, gC2 * wgt};
+            float gr[3];
 #pragma unroll
-            for (int q = 0; q < kRowSums; ++q) {
-                gr[q] = dpp_row_sum(gr[q]);
+            for (int q = 0; q < 3; ++q) {
+                const float keep = hi_half ? co[q] : mo[q];
+                const float send = hi_half ? mo[q] : co[q];
+                gr[q] = keep + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(send), 0x140, 0xF, 0xF,
+                                                                          true));
+            }
+#pragma unroll
+            for (int q = 0; q < 3; ++q) {
+                gr[q] += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(gr[q]), 0xB1, 0xF, 0xF, true));
+                gr[q] += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(gr[q]), 0x4E, 0xF, 0xF, true));
+                gr[q] += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(gr[q]), 0x141, 0xF, 0xF, true));
                 // keep the last add in front of the branch (all lanes active), where
                 // it folds into the DPP instruction
                 asm volatile("" : "+v"(gr[q]));
             }
-            // the leader of every row that walks an entry stores: a row without a
-            // contributing pixel stores zero sums into its record, which holds zeros
-            // (records are cleared per batch and a row visits an entry once)
-            if ((lane & 15) == 0 && act) {
+            // lanes 0 and 8 of every row that walks an entry store (moments and colour
+            // sums): a row without a contributing pixel stores zero sums into its
+            // record, which holds zeros (records are cleared per batch and a row
+            // visits an entry once)
+            if ((lane & 7) == 0 && act) {
 #pragma unroll
-                for (int q = 0; q < kRowSums; ++q) s_row[w][row][q][k] = gr[q];
+                for (int q = 0; q < 3; ++q) s_row[w][row][q_half + q][k] = gr[q];
             }
         }
         // lane k adds this wave's four row records of entry k: only this wave

@@ -397,8 +397,16 @@ class ViewTrainer:
     PHASES = ("project", "visible", "bin_sort", "raster_fwd_l1", "raster_bwd_pixels", "raster_bwd_project",
               "adam_publish", "apply")
 
-    def step(self, cam, step, version=1, publish=True, active=False, target=None, events=None, overlap=False):
-        """Project, visible set, bin+sort, forward, L1, backward, Adam staged as the message of `version` in
+    def _fwd_step(self, target, active):
+        """The step's forward + L1; with active, also the realized active set (flags from the forward,
+        compacted into act_idx, its size in counts[2])."""
+        self.raster_fwd_l1(target, active=active)
+        if active:
+            self.active_set()
+
+    def step(self, cam, step, version=1, publish=True, active=True, target=None, events=None, overlap=False):
+        """Project, visible set, bin+sort, forward, L1 (and the realized active set: the primitives some
+        pixel included, when active), backward, Adam staged as the message of `version` in
         ring slot version & 1, and its commit to the replica (versions must follow each other by one).
         publish=False runs plain Adam (steps to delta_rows) and no commit.
         target: device tensor (3*H*W) or None for the set_target buffer.
@@ -414,7 +422,7 @@ class ViewTrainer:
             msg = self.msgs[k]
             main = torch.cuda.current_stream()
             calls = (lambda: self.project(cam), self.visible, self.bin_sort,
-                     lambda: self.raster_fwd_l1(target, active=active), self.raster_bwd_pixels,
+                     lambda: self._fwd_step(target, active), self.raster_bwd_pixels,
                      self.raster_bwd_project)
             if ev:
                 ev[0].record()
@@ -434,7 +442,7 @@ class ViewTrainer:
             self._pending = (version, ev)
             return
         calls = (lambda: self.project(cam), self.visible, self.bin_sort,
-                 lambda: self.raster_fwd_l1(target, active=active), self.raster_bwd_pixels, self.raster_bwd_project,
+                 lambda: self._fwd_step(target, active), self.raster_bwd_pixels, self.raster_bwd_project,
                  (lambda: self.adam_publish(step, version, self.msgs[version & 1])) if publish
                  else (lambda: self.adam(step)),
                  (lambda: self.commit(version)) if publish else (lambda: None))

@@ -11,7 +11,7 @@ Two passes over view 0 of each workload:
      its own upstream gradient);
   2. the benchmark's training step itself (ViewTrainer.step with the
      overlapped commit, exactly as bench.py times it): visible set, pairs and
-     ranges bit-exact, image, dL/dimg bit-exact against the sign of the GPU
+     ranges bit-exact, the realized active set equal to pass 1's, image, dL/dimg bit-exact against the sign of the GPU
      image's difference from the target, the step's gradient rows against the
      oracle's backward of that same dL/dimg on every visible primitive (the
      bound of each element widened by twice the magnitude that the ambiguous
@@ -127,6 +127,12 @@ def test_full_view(name, orc):
     np.testing.assert_array_equal(to_u32(tr.ranges)[:2 * T].reshape(T, 2), ranges_o)
     np.testing.assert_array_equal(to_u32(tr.tile_order)[:T], expected_tile_order(ranges_o))
     _say(name, "V=%d M=%d bit-exact" % (V, M))
+    # the realized active set: the same flags as the forward of pass 1, compacted in ascending order
+    act_step = tr.active.cpu().numpy()[:n]
+    np.testing.assert_array_equal(act_step, act)
+    A = int(to_u32(tr.counts[2:3])[0])
+    np.testing.assert_array_equal(to_u32(tr.act_idx)[:A], np.flatnonzero(act_step))
+    _say(name, "realized active set %d of %d visible" % (A, V))
     img = tr.img.view(-1)[:3 * H * W].cpu().numpy().reshape(3, H, W)
     assert_pixels(img, rn.img, np.broadcast_to(~amb, img.shape), "img")
     fT = tr.final_T.view(-1)[:H * W].cpu().numpy().reshape(H, W)

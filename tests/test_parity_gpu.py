@@ -675,6 +675,7 @@ def test_empty_and_degenerate(torch_gpu, orc):
     tr.step(w.cameras[0], step=1)
     torch_gpu.cuda.synchronize()
     assert int(u32(tr.counts[0:1])[0]) == 0 and int(u32(tr.counts[1:2])[0]) == 0
+    assert int(u32(tr.counts[2:3])[0]) == 0                 # no realized active primitive
     hw = w.cameras[0].width * w.cameras[0].height
     assert float(tr.img.view(-1)[:3 * hw].abs().max()) == 0.0
     assert float(tr.final_T.view(-1)[:hw].min()) == 1.0
@@ -760,7 +761,7 @@ def test_backward_halves_match_combined(torch_gpu, orc):
 def test_step_matches_phase_calls(torch_gpu, orc):
     """The training step's prepared-argument launches give the phase-by-phase
     calls' results bit for bit (parameters, moments, replica, versions, image,
-    gradients), over two views of two cameras."""
+    gradients, realized active flags and ids), over two views of two cameras."""
     w = get_case("room-60k-392x216")
     runs = []
     for fast in (True, False):
@@ -770,12 +771,15 @@ def test_step_matches_phase_calls(torch_gpu, orc):
             if fast:
                 tr.step(cam, step=s, version=s, target=tgt)
             else:
-                tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd_l1(tgt); tr.raster_bwd_pixels()
-                tr.raster_bwd_project(); tr.adam_publish(s, s, tr.msgs[s & 1]); tr.commit(s)
+                tr.project(cam); tr.visible(); tr.bin_sort(); tr.raster_fwd_l1(tgt, active=True); tr.active_set()
+                tr.raster_bwd_pixels(); tr.raster_bwd_project(); tr.adam_publish(s, s, tr.msgs[s & 1]); tr.commit(s)
         torch_gpu.cuda.synchronize()
         assert int(u32(tr.status)[0]) == 0
+        A = int(u32(tr.counts[2:3])[0])
+        assert A > 0
         runs.append([t.clone() for t in tr.params] + [tr.m.clone(), tr.v.clone()] +
-                    [t.clone() for t in tr.replica] + [tr.version.clone(), tr.img.clone(), tr.grad_rows.clone()])
+                    [t.clone() for t in tr.replica] + [tr.version.clone(), tr.img.clone(), tr.grad_rows.clone(),
+                                                       tr.active.clone(), tr.act_idx[:A].clone()])
     for a, b in zip(*runs):
         assert torch_gpu.equal(a, b)
 
