@@ -258,8 +258,11 @@ static_assert(kWaveSortMax == 512u, "kLongKey is the key of 512 pairs");
 // Exclusive scan over the 4 waves of a workgroup of GS_BLOCK threads is
 // block_excl_scan.
 
-// Tiles per workgroup of the finishing grid (4 per thread).
-constexpr uint32_t kFinishSeg = 4 * GS_BLOCK;
+// Tiles per workgroup of the finishing grid (2 per thread), and the totals
+// each thread loads per pass over all tiles (one pass up to 8192 tiles).
+constexpr uint32_t kFinishPer = 2;
+constexpr uint32_t kFinishSeg = kFinishPer * GS_BLOCK;
+constexpr int kFinishLoads = 32;
 
 // From the per-tile totals: the tile ranges (exclusive scan in tile order;
 // [0, 0) for a tile without pairs), the placement cursors (each range's
@@ -267,12 +270,14 @@ constexpr uint32_t kFinishSeg = 4 * GS_BLOCK;
 // by ascending id) with one record per dispatch position (tile, range start,
 // pair count), and the number of tiles with kWaveSortMax pairs or more, which
 // the order puts first.  Workgroup b owns the tiles [b*kFinishSeg, ..) of one
-// segment.  It reads every total: their sum before the segment starts its
-// ranges, and the key counts over all tiles and over the tiles before the
-// segment give each key's first position for the segment.  Inside the
-// segment, wave w owns a contiguous quarter: it counts its keys, the counts
-// give every (wave, key) its first position, and the wave then places its
-// tiles 64 at a time, each lane ranked among the earlier lanes with its key.
+// segment.  It reads every total (all loads of a pass in flight together):
+// their sum before the segment starts its ranges, and the key counts over all
+// tiles and over the tiles before the segment give each key's first position
+// for the segment; the segment's own totals and range starts stay in LDS.
+// Inside the segment, wave w owns a contiguous quarter: it counts its keys,
+// the counts give every (wave, key) its first position, and the wave then
+// places its tiles 64 at a time, each lane ranked among the earlier lanes
+// with its key.
 __global__ void __launch_bounds__(GS_BLOCK) k_tile_finish(const uint32_t* __restrict__ tcount, uint32_t T,
                                                           uint32_t* __restrict__ ranges,
                                                           uint32_t* __restrict__ cursor,
@@ -281,6 +286,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_finish(const uint32_t* __rest
     constexpr int kWaves = GS_BLOCK / GS_WAVE;
     __shared__ uint32_t s_all[256], s_before[256];
     __shared__ uint32_t s_wc[kWaves][256];
+    __shared__ uint32_t s_cnt[kFinishSeg], s_sta[kFinishSeg];
     __shared__ uint32_t scratch[4];
     const uint32_t tid = threadIdx.x;
     const uint32_t w = tid / GS_WAVE;
@@ -290,16 +296,17 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_finish(const uint32_t* __rest
     s_before[tid] = 0u;
     s_wc[0][tid] = 0u; s_wc[1][tid] = 0u; s_wc[2][tid] = 0u; s_wc[3][tid] = 0u;
     __syncthreads();
-    // every total: key counts over all tiles and before the segment, the pairs before it
+    // every total: key counts over all tiles and before the segment, the pairs
+    // before it; the segment's totals to LDS
     uint32_t before = 0;
-    for (uint32_t r0 = 0; r0 < T; r0 += GS_BLOCK * GS_ITEMS) {
-        uint32_t c[GS_ITEMS];
+    for (uint32_t r0 = 0; r0 < T; r0 += GS_BLOCK * kFinishLoads) {
+        uint32_t c[kFinishLoads];
 #pragma unroll
-        for (int k = 0; k < GS_ITEMS; ++k) c[k] = tcount[min(r0 + k * GS_BLOCK + tid, T - 1u)];
+        for (int k = 0; k < kFinishLoads; ++k) c[k] = tcount[min(r0 + k * GS_BLOCK + tid, T - 1u)];
 #pragma unroll
-        for (int k = 0; k < GS_ITEMS; ++k) loaded(c[k]);
+        for (int k = 0; k < kFinishLoads; ++k) loaded(c[k]);
 #pragma unroll
-        for (int k = 0; k < GS_ITEMS; ++k) {
+        for (int k = 0; k < kFinishLoads; ++k) {
             const uint32_t t = r0 + k * GS_BLOCK + tid;
             if (t < T) {
                 const uint32_t key = tile_order_key(c[k]);
@@ -307,24 +314,32 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_finish(const uint32_t* __rest
                 if (t < lo) {
                     atomicAdd(&s_before[key], 1u);
                     before += c[k];
+                } else if (t < hi) {
+                    s_cnt[t - lo] = c[k];
                 }
             }
         }
     }
-    // the segment: 4 consecutive tiles per thread
-    const uint32_t t0 = lo + tid * 4u;
-    uint32_t c[4];
+    __syncthreads();
+    // the segment: kFinishPer consecutive tiles per thread
+    const uint32_t l0 = tid * kFinishPer;
+    uint32_t c[kFinishPer], csum = 0;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) c[k] = t0 + k < hi ? tcount[t0 + k] : 0u;
+    for (uint32_t k = 0; k < kFinishPer; ++k) {
+        c[k] = lo + l0 + k < hi ? s_cnt[l0 + k] : 0u;
+        csum += c[k];
+    }
     uint32_t tot;
     const uint32_t pre = block_sum_u32(before, scratch);       // (the block's sum of `before`)
-    uint32_t run = block_excl_scan(c[0] + c[1] + c[2] + c[3], scratch, &tot) + pre;
+    uint32_t run = block_excl_scan(csum, scratch, &tot) + pre;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        if (t0 + k < hi) {
-            ranges[2 * (t0 + k)] = c[k] ? run : 0u;
-            ranges[2 * (t0 + k) + 1] = c[k] ? run + c[k] : 0u;
-            cursor[t0 + k] = run;
+    for (uint32_t k = 0; k < kFinishPer; ++k) {
+        const uint32_t t = lo + l0 + k;
+        if (t < hi) {
+            ranges[2 * t] = c[k] ? run : 0u;
+            ranges[2 * t + 1] = c[k] ? run + c[k] : 0u;
+            cursor[t] = run;
+            s_sta[l0 + k] = c[k] ? run : 0u;
         }
         run += c[k];
     }
@@ -336,11 +351,11 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_finish(const uint32_t* __rest
         s_all[tid] = kstart + s_before[tid];
     }
     // per wave: key counts of its quarter of the segment (its lanes' tiles, in order)
-    const uint32_t qlo = lo + w * (kFinishSeg / kWaves);
-    const uint32_t qhi = min(qlo + kFinishSeg / kWaves, hi);
+    const uint32_t qlo = w * (kFinishSeg / kWaves);                         // segment-relative
+    const uint32_t qhi = min(qlo + kFinishSeg / kWaves, hi - lo);
     uint32_t* wc = s_wc[w];
     __syncthreads();
-    for (uint32_t t = qlo + lane; t < qhi; t += GS_WAVE) atomicAdd(&wc[tile_order_key(tcount[t])], 1u);
+    for (uint32_t l = qlo + lane; l < qhi; l += GS_WAVE) atomicAdd(&wc[tile_order_key(s_cnt[l])], 1u);
     __syncthreads();
     {
         uint32_t b = s_all[tid];
@@ -351,21 +366,20 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_finish(const uint32_t* __rest
         s_wc[3][tid] = b + c0 + c1 + c2;
     }
     __syncthreads();
-    // placement: the quarter's tiles 64 at a time (each tile's range start as
-    // this workgroup wrote it above)
+    // placement: the quarter's tiles 64 at a time
     const uint64_t lt = lanemask_lt();
     for (uint32_t b0 = qlo; b0 < qhi; b0 += GS_WAVE) {
-        const uint32_t t = b0 + lane;
-        const bool valid = t < qhi;
-        const uint32_t cnt = valid ? tcount[t] : 0u;
-        const uint32_t sta = valid ? ranges[2 * t] : 0u;
+        const uint32_t l = b0 + lane;
+        const bool valid = l < qhi;
+        const uint32_t cnt = valid ? s_cnt[l] : 0u;
+        const uint32_t sta = valid ? s_sta[l] : 0u;
         const uint32_t key = tile_order_key(cnt);
         const uint64_t peers = match_digit(key, valid, 8);
         const uint32_t bw = valid ? wc[key] : 0u;
         if (valid) {
             const uint32_t pos = bw + (uint32_t)popc64(peers & lt);
-            order[pos] = t;
-            rec[pos] = make_uint4(t, cnt ? sta : 0u, cnt, 0u);
+            order[pos] = lo + l;
+            rec[pos] = make_uint4(lo + l, sta, cnt, 0u);
         }
         // all reads of this round precede the leaders' updates
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -728,12 +742,11 @@ constexpr int kLongK = (int)kWaveSortMax / GS_WAVE;     // keys per lane
 // Workgroups per compute unit of the persistent depth-sort grid.
 constexpr uint32_t kDepthSortBlocksPerCU = 8;
 
-// The exact network over the n (<= kLongCap) 64-bit keys of a tile by the
-// whole workgroup in LDS.
-__device__ void block_sort_tile64(uint32_t t, uint32_t start, uint32_t n, const unsigned long long* __restrict__ skey,
-                                  const uint32_t* __restrict__ sval, unsigned long long* sk, uint32_t* sv,
-                                  uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
-                                  uint64_t* __restrict__ keys64) {
+// The exact network over the n (<= kLongCap) 64-bit keys skey[start ..
+// start + n) by the whole workgroup in LDS: sorted keys in sk[0..n), their
+// primitives in sv.
+__device__ void block_sort_lds64(uint32_t start, uint32_t n, const unsigned long long* __restrict__ skey,
+                                 const uint32_t* __restrict__ sval, unsigned long long* sk, uint32_t* sv) {
     uint32_t np = 2;
     while (np < n) np <<= 1;
     for (uint32_t i = threadIdx.x; i < np; i += GS_BLOCK) {
@@ -759,14 +772,111 @@ __device__ void block_sort_tile64(uint32_t t, uint32_t start, uint32_t n, const 
             __syncthreads();
         }
     }
+}
+
+// The exact network over the n (<= kLongCap) 64-bit keys of a tile by the
+// whole workgroup in LDS, written out in order.
+__device__ void block_sort_tile64(uint32_t t, uint32_t start, uint32_t n, const unsigned long long* __restrict__ skey,
+                                  const uint32_t* __restrict__ sval, unsigned long long* sk, uint32_t* sv,
+                                  uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
+                                  uint64_t* __restrict__ keys64) {
+    block_sort_lds64(start, n, skey, sval, sk, sv);
     for (uint32_t i = threadIdx.x; i < n; i += GS_BLOCK) put_sorted(t, start + i, sk[i], sv[i], pair_emit, vals, keys64);
     __syncthreads();
 }
 
-// A tile by the whole workgroup, exactly, in place in global memory.
+// Number of keys below each of the thread's R keys in the ascending keys
+// sk[0..m) (keys are unique): a branch-free binary search, the R searches
+// stepping together.
+template <int R>
+__device__ __forceinline__ void rank_in(const unsigned long long* sk, uint32_t m, const unsigned long long (&key)[R],
+                                        uint32_t (&pos)[R]) {
+    uint32_t step = 1;
+    while (step <= m) step <<= 1;
+#pragma unroll
+    for (int k = 0; k < R; ++k) pos[k] = 0;
+    for (step >>= 1; step > 0; step >>= 1) {
+#pragma unroll
+        for (int k = 0; k < R; ++k)
+            if (pos[k] + step <= m && sk[pos[k] + step - 1] < key[k]) pos[k] += step;
+    }
+}
+
+// A tile of kLongCap < n <= 2 kLongCap pairs: its first kLongCap keys and the
+// rest are each sorted exactly in LDS, and every key goes to its index in
+// its own run plus its rank in the other run (the merged order; keys are
+// unique).  Each sorted run is kept in its own place in global memory (this
+// workgroup's segment) while the other one sits in LDS; the ranks are
+// searched kRankGroup keys at a time per thread.
+constexpr int kRankGroup = 4;
+
+// The keys of run [r0, r0 + m) of the segment, ranked in the ascending keys
+// sk[0..mo) in LDS; key i of the run goes to r_out + i + its rank.
+__device__ __forceinline__ void place_ranked(uint32_t t, uint32_t start, uint32_t r0, uint32_t m, uint32_t r_out,
+                                             const unsigned long long* __restrict__ skey,
+                                             const uint32_t* __restrict__ sval, const unsigned long long* sk,
+                                             uint32_t mo, uint32_t* __restrict__ pair_emit,
+                                             uint32_t* __restrict__ vals, uint64_t* __restrict__ keys64) {
+    constexpr uint32_t kGroupSpan = kRankGroup * GS_BLOCK;
+#pragma unroll 1
+    for (uint32_t g = 0; g < m; g += kGroupSpan) {
+        unsigned long long kk[kRankGroup];
+        uint32_t pk[kRankGroup], rk[kRankGroup];
+#pragma unroll
+        for (int k = 0; k < kRankGroup; ++k) {
+            const uint32_t i = min(g + threadIdx.x + k * GS_BLOCK, m - 1u);
+            kk[k] = skey[start + r0 + i];
+            pk[k] = sval[start + r0 + i];
+        }
+        rank_in<kRankGroup>(sk, mo, kk, rk);
+#pragma unroll
+        for (int k = 0; k < kRankGroup; ++k) {
+            const uint32_t i = g + threadIdx.x + k * GS_BLOCK;
+            if (i < m) put_sorted(t, start + r_out + i + rk[k], kk[k], pk[k], pair_emit, vals, keys64);
+        }
+    }
+}
+
+__device__ void sort_two_runs(uint32_t t, uint32_t start, uint32_t n, unsigned long long* __restrict__ skey,
+                              uint32_t* __restrict__ sval, unsigned long long* sk, uint32_t* sv,
+                              uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
+                              uint64_t* __restrict__ keys64) {
+    const uint32_t tid = threadIdx.x;
+    const uint32_t na = kLongCap, nb = n - kLongCap;
+    // the first run sorted, to its place
+    block_sort_lds64(start, na, skey, sval, sk, sv);
+    for (uint32_t i = tid; i < na; i += GS_BLOCK) {
+        skey[start + i] = sk[i];
+        sval[start + i] = sv[i];
+    }
+    __threadfence_block();
+    __syncthreads();
+    // the second run sorted (in LDS); the first run's keys placed by their ranks in it
+    block_sort_lds64(start + na, nb, skey, sval, sk, sv);
+    place_ranked(t, start, 0u, na, 0u, skey, sval, sk, nb, pair_emit, vals, keys64);
+    // the second run to its place, the first back to LDS; the second run's keys placed
+    for (uint32_t i = tid; i < nb; i += GS_BLOCK) {
+        skey[start + na + i] = sk[i];
+        sval[start + na + i] = sv[i];
+    }
+    __threadfence_block();
+    __syncthreads();
+    for (uint32_t i = tid; i < na; i += GS_BLOCK) sk[i] = skey[start + i];
+    __syncthreads();
+    place_ranked(t, start, na, nb, 0u, skey, sval, sk, na, pair_emit, vals, keys64);
+    __syncthreads();
+}
+
+// A tile by the whole workgroup, exactly: up to 2 kLongCap pairs as two runs
+// in LDS, longer ones in place in global memory.
 __device__ void sort_huge_tile(uint32_t t, uint32_t start, uint32_t n, unsigned long long* __restrict__ skey,
-                               uint32_t* __restrict__ sval, uint32_t* __restrict__ pair_emit,
-                               uint32_t* __restrict__ vals, uint64_t* __restrict__ keys64) {
+                               uint32_t* __restrict__ sval, unsigned long long* sk, uint32_t* sv,
+                               uint32_t* __restrict__ pair_emit, uint32_t* __restrict__ vals,
+                               uint64_t* __restrict__ keys64) {
+    if (n <= 2 * kLongCap) {
+        sort_two_runs(t, start, n, skey, sval, sk, sv, pair_emit, vals, keys64);
+        return;
+    }
     unsigned long long* key = skey + start;
     uint32_t* val = sval + start;
     bitonic_global(key, val, n);
@@ -896,7 +1006,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_depth_sort(const uint4* __res
         if (rl.z <= kLongCap)
             sort_long_tile(rl.x, rl.y, rl.z, skey, sval, s_kv, s_v, s_first, pair_emit, vals, keys64);
         else
-            sort_huge_tile(rl.x, rl.y, rl.z, skey, sval, pair_emit, vals, keys64);
+            sort_huge_tile(rl.x, rl.y, rl.z, skey, sval, s_kv, s_v, pair_emit, vals, keys64);
     }
     unsigned long long* sk = s_kv + w * kWaveSortMax;
     uint32_t* sv = s_v + w * kWaveSortMax;

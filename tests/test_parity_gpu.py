@@ -501,7 +501,8 @@ def test_long_tile_lists(torch_gpu, orc):
 
 # (tile x, tile y, primitives, short ties, long run): one cluster per tile
 # class of the per-tile depth sort, from one wave with one key per lane up to
-# tiles longer than a workgroup's register sort.  Short ties: an eighth of
+# tiles longer than a workgroup's register sort (two runs merged, 2049..4096
+# pairs) and longer than two runs (global memory).  Short ties: an eighth of
 # the primitives copy a neighbour's mean (runs of equal depth bits of a few
 # pairs); long run: that many primitives share one mean (a run longer than
 # the in-place placement takes).
@@ -509,14 +510,16 @@ DEPTH_SORT_CLUSTERS = [(1, 1, 40, True, 0), (3, 1, 40, False, 0), (5, 1, 100, Tr
                        (9, 1, 400, True, 0), (11, 1, 400, False, 0), (13, 1, 230, False, 0),
                        (1, 5, 1000, False, 0), (5, 5, 1000, True, 0), (9, 5, 1800, False, 0),
                        (13, 5, 3000, False, 0), (3, 9, 700, True, 0), (7, 9, 300, False, 80),
-                       (11, 9, 900, False, 100)]
+                       (11, 9, 900, False, 100), (1, 13, 2300, True, 0), (5, 13, 2600, False, 300),
+                       (9, 13, 4500, True, 0)]
 
 
 def test_depth_sort_paths(torch_gpu, orc):
     """Tiles of every size class of the per-tile sort (one wave with 1, 2, 4
-    or 8 keys per lane, a workgroup up to 2048 keys, global memory beyond),
-    with and without pairs of equal depth bits (copies of a primitive's
-    mean): the order is exactly (tile, depth bits, id) in every class."""
+    or 8 keys per lane, a workgroup up to 2048 keys, two merged runs up to
+    4096, global memory beyond), with and without pairs of equal depth bits
+    (copies of a primitive's mean): the order is exactly (tile, depth bits,
+    id) in every class."""
     from paper_2607_19893_amd import scenes
     rng = np.random.default_rng(33)
     n_bg = 1500
@@ -560,7 +563,8 @@ def test_depth_sort_paths(torch_gpu, orc):
         _say("cluster tile (%d,%d): %d pairs, longest run of equal depth bits %d" % (tx, ty, lengths[t], longest[t]))
     _say("tiles with equal depth bits:", tied)
     cl = [lengths[ty * cam.tiles_x + tx] for tx, ty, _, _, _ in DEPTH_SORT_CLUSTERS]
-    assert min(cl) <= 64 and max(cl) > 2048 and any(512 <= c <= 2048 for c in cl)
+    assert min(cl) <= 64 and max(cl) > 4096 and any(512 <= c <= 2048 for c in cl)
+    assert sum(2048 < c <= 4096 for c in cl) >= 3
     assert any(256 < c < 512 for c in cl) and tied >= 4
     runs = {(tx, ty): longest[ty * cam.tiles_x + tx] for tx, ty, _, _, _ in DEPTH_SORT_CLUSTERS}
     assert runs[(7, 9)] > 64 and runs[(11, 9)] > 64 and 2 <= runs[(9, 1)] <= 64 and 2 <= runs[(5, 5)] <= 64
