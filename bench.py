@@ -1,7 +1,8 @@
 """Throughput of the one-GPU 3DGS training-view hot path.
 
 A step is one training view through every phase: projection, visible-set
-extraction, tile binning + sort, forward raster fused with the L1 loss,
+extraction, tile binning + sort, forward raster fused with the L1 loss (and
+the realized active set: the primitives some pixel blended, as ascending ids),
 backward, sparse Adam over the visible rows with its steps staged as a
 publication message, and the commit of that message to a replica (the
 pending-update publication).  The workload is the 1M-Gaussian
