@@ -385,11 +385,11 @@ class ViewTrainer:
             self.apply_stream.wait_event(self.pub_ev[k])
             if after is not None:
                 self.apply_stream.wait_event(after)
-            if ev:
+            if ev and ev[-2] is not None:
                 ev[-2].record(self.apply_stream)
             self.commit(version, background=True)
             self.app_ev[k].record(self.apply_stream)
-            if ev:
+            if ev and ev[-1] is not None:
                 ev[-1].record(self.apply_stream)
 
     # -- whole view ----------------------------------------------------------
@@ -410,12 +410,18 @@ class ViewTrainer:
         ring slot version & 1, and its commit to the replica (versions must follow each other by one).
         publish=False runs plain Adam (steps to delta_rows) and no commit.
         target: device tensor (3*H*W) or None for the set_target buffer.
-        events: optional list of len(PHASES)+1 torch.cuda.Event recorded around the phases.
+        events: optional list of len(PHASES)+1 torch.cuda.Event recorded around the phases (None entries
+        are skipped: each recorded event is a marker the device processes between two kernels).
         overlap: apply on the second stream, deferred into the next step (enable_overlap; call
         flush_apply after the last step); events then holds len(PHASES)+2 events: the first
         len(PHASES) bracket the other phases on the current stream, the last two bracket the
         apply on the second stream."""
         ev = events
+
+        def mark(i):
+            if ev and ev[i] is not None:
+                ev[i].record()
+
         if overlap and publish:
             self.enable_overlap()
             k = version & 1
@@ -424,12 +430,10 @@ class ViewTrainer:
             calls = (lambda: self.project(cam), self.visible, self.bin_sort,
                      lambda: self._fwd_step(target, active), self.raster_bwd_pixels,
                      self.raster_bwd_project)
-            if ev:
-                ev[0].record()
+            mark(0)
             for i, fn in enumerate(calls):
                 fn()
-                if ev:
-                    ev[i + 1].record()
+                mark(i + 1)
                 if i == self.APPLY_AFTER:
                     # the previous view's apply, once this view reaches that phase on the device
                     self.front_ev.record(main)
@@ -437,8 +441,7 @@ class ViewTrainer:
             main.wait_event(self.app_ev[k])          # the commit that read this slot two versions ago
             self.adam_publish(step, version, msg)
             self.pub_ev[k].record(main)
-            if ev:
-                ev[len(calls) + 1].record()
+            mark(len(calls) + 1)
             self._pending = (version, ev)
             return
         calls = (lambda: self.project(cam), self.visible, self.bin_sort,
@@ -446,12 +449,10 @@ class ViewTrainer:
                  (lambda: self.adam_publish(step, version, self.msgs[version & 1])) if publish
                  else (lambda: self.adam(step)),
                  (lambda: self.commit(version)) if publish else (lambda: None))
-        if ev:
-            ev[0].record()
+        mark(0)
         for i, fn in enumerate(calls):
             fn()
-            if ev:
-                ev[i + 1].record()
+            mark(i + 1)
 
     def ensure_capacity(self, cams, margin=1.25):
         """Size the pair buffers for the given cameras (synchronizes)."""
