@@ -344,6 +344,8 @@ def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False
     # brackets only the phase whose rate the roofline reports
     pevs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(steps)]
     pviews = []
+    torch.cuda.synchronize()
+    no_collector()
     for k in range(steps):
         step += 1
         v = (warmup + k) % nviews
@@ -351,6 +353,7 @@ def run_workload(name, steps, warmup, overlap=True, packed=True, row_major=False
         tr.step(cams[v], step, version=step, target=targets[v], events=pevs[k], overlap=overlap)
     tr.flush_apply()
     torch.cuda.synchronize()
+    gc.enable()
     assert to_u32(tr.status)[0] == 0, "device status flags set during the per-phase pass"
     phase_ms = np.zeros(nph)
     for k in range(steps):

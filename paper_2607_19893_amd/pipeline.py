@@ -371,18 +371,25 @@ class ViewTrainer:
         self._pending = None
         self.front_ev = torch.cuda.Event()
 
-    def flush_apply(self, after=None):
+    def flush_apply(self, after=None, staged=False):
         """Issue the deferred apply of the last view, if any (overlap mode); it
         starts on the device once its message is staged and, if given, once the
-        event `after` has been reached."""
+        event `after` has been reached.  staged: `after` was recorded on the
+        current stream behind the view's staging, so waiting for it covers the
+        staging too (no event of its own: each one is a marker the device
+        processes between two kernels)."""
         pend = getattr(self, "_pending", None)
         if pend is None:
             return
         self._pending = None
         version, ev = pend
         k = version & 1
+        if not (staged and after is not None):
+            # the current stream has issued the view's staging: mark its position
+            self.pub_ev[k].record(torch.cuda.current_stream())
         with torch.cuda.stream(self.apply_stream):
-            self.apply_stream.wait_event(self.pub_ev[k])
+            if not (staged and after is not None):
+                self.apply_stream.wait_event(self.pub_ev[k])
             if after is not None:
                 self.apply_stream.wait_event(after)
             if ev and ev[-2] is not None:
@@ -437,10 +444,9 @@ class ViewTrainer:
                 if i == self.APPLY_AFTER:
                     # the previous view's apply, once this view reaches that phase on the device
                     self.front_ev.record(main)
-                    self.flush_apply(after=self.front_ev)
+                    self.flush_apply(after=self.front_ev, staged=True)
             main.wait_event(self.app_ev[k])          # the commit that read this slot two versions ago
             self.adam_publish(step, version, msg)
-            self.pub_ev[k].record(main)
             mark(len(calls) + 1)
             self._pending = (version, ev)
             return
