@@ -517,6 +517,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const uint32_t maxlast = s_max;
     const bool hi_half = (lane & 8) != 0;       // high half of the lane's 16-lane row
     const int q_half = hi_half ? 3 : 0;         // the half's three sums in a row record
+    // the colour sums of entry k sit at index k ^ 16: the row's two storing lanes
+    // (same entry, records 3 x 64 floats apart) then hit different banks
+    const int k_half = hi_half ? 16 : 0;
     // largest n_contrib of each pixel row of this wave (wave-uniform values)
     uint32_t rl = last;
 #pragma unroll
@@ -620,7 +623,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             // visits an entry once)
             if ((lane & 7) == 0 && act) {
 #pragma unroll
-                for (int q = 0; q < 3; ++q) s_row[w][row][q_half + q][k] = gr[q];
+                for (int q = 0; q < 3; ++q) s_row[w][row][q_half + q][k ^ k_half] = gr[q];
             }
         }
         // lane k adds this wave's four row records of entry k: only this wave
@@ -642,9 +645,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
                 acc[3] += dy * mx;
                 acc[4] += dy * my;
                 acc[5] += m;
-                acc[6] += s_row[w][q][3][lane];
-                acc[7] += s_row[w][q][4][lane];
-                acc[8] += s_row[w][q][5][lane];
+                acc[6] += s_row[w][q][3][lane ^ 16];
+                acc[7] += s_row[w][q][4][lane ^ 16];
+                acc[8] += s_row[w][q][5][lane ^ 16];
             }
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
             __builtin_amdgcn_wave_barrier();
