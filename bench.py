@@ -70,9 +70,9 @@ TRAFFIC = {
     "workload": "room-1M-L3-1080p",
     "id_order": "spatial",
     "sources": ["paper_2607_19893_amd/csrc/raster.hip", "paper_2607_19893_amd/csrc/binsort.hip"],
-    "code_sha256": "f390434199484ee194766c26630a36f721bd2465fb48e146a86d0de3a7b08614",
-    "fetch_kib": 112106.16, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 96733.56, "write_scale": 1048576.0 / 1048576.0,
+    "code_sha256": "d23421874611e8df05687391d502a73959b92296deaa95d664e54f58f86aeb98",
+    "fetch_kib": 109224.20, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 91878.41, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
