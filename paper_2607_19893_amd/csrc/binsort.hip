@@ -14,13 +14,14 @@
 //      per tile in LDS and claims one run of slots per distinct tile from the
 //      tile's cursor (a device atomic), so the order of a tile's pairs inside
 //      its range depends on scheduling;
-//   4. each tile's segment is sorted by (depth bits, emission position) in LDS
-//      by one workgroup (a bitonic network; segments longer than the LDS
-//      capacity are sorted in global memory by the same workgroup), tiles
-//      taken in the dispatch order.  The key is unique per pair, so the result
-//      does not depend on the order step 3 left; emission positions grow with
-//      the primitive id inside a tile, so this is exactly the (tile, depth
-//      bits, id) order.
+//   4. each tile's segment is sorted by (depth bits, emission position), tiles
+//      taken in the dispatch order by a persistent grid: a wave sorts a tile of
+//      fewer than 512 pairs in registers, a workgroup one of up to 2048 (each
+//      wave 512 in registers, merges across waves through LDS), two exact runs
+//      in LDS merged by rank up to 4096, and a network in global memory beyond.
+//      The key is unique per pair, so the result does not depend on the order
+//      step 3 left; emission positions grow with the primitive id inside a
+//      tile, so this is exactly the (tile, depth bits, id) order.
 // The per-tile kernels that follow (this sort, the forward and backward
 // raster) end when their longest tile ends; taking the longest first lets
 // the short ones fill in beside it instead of after it.

@@ -8,14 +8,15 @@
 //
 // Backward: same tile/pixel mapping, walking each tile's pairs back to front.
 // Each pixel recovers the transmittance in front of a pair by dividing by
-// (1 - alpha) and keeps the suffix colour sum; per pair, the 9 partial
-// derivatives are summed over each 16-lane pixel row with DPP, over the rows
-// of a wave with LDS atomics, and over the 4 waves in a fixed order, then
+// (1 - alpha) and keeps the projection of the suffix colour sum on its
+// upstream gradient; per pair, six moment and colour sums are taken over each
+// 16-lane pixel row with DPP, stored in the row's LDS record of the pair,
+// combined over the rows of a wave and over the 4 waves in a fixed order, and
 // written to the pair's slot at its emission position (a primitive's pairs
-// side by side).  Per visible primitive, k_project_bwd adds its slots in order
+// side by side).  Per visible primitive, k_slot_sum adds its slots in order
 // -- deterministic, no floating-point atomics in global memory -- and
-// applies the projection and colour chain rule
-// (geometry in fp64) and writes one compact gradient row.
+// k_project_bwd applies the projection and colour chain rule (geometry in
+// fp64) and writes one compact gradient row.
 #include "common.h"
 #include "internal.h"
 
