@@ -77,7 +77,7 @@ def lib():
         L.orc_render.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, P, P, P, P, P, P, P]
         L.orc_render.restype = None
         L.orc_render_backward.argtypes = [i64, P, P, P, P, P, P, P, i32, i32, P, P, i32, P, P, f64, f64, f64, P, f64,
-                                          P]
+                                          P, i32]
         L.orc_render_backward.restype = None
         L.orc_project_backward.argtypes = [i32, i32, P, P, P, P, P, ctypes.POINTER(_Cam), i64, P, P, P,
                                            P, P, P, P, P, P]
@@ -244,9 +244,13 @@ def ambiguous_pixels(rnd: "Render", loss_margin=None, amb_alpha=AMB_ALPHA, amb_T
 
 
 def render_backward(vis, proj: Projection, cam, dL_dimg, bg=(0.0, 0.0, 0.0), loss_margin=None,
-                    amb_alpha=AMB_ALPHA, amb_T=AMB_T, amb_cap=AMB_CAP, amb_loss=AMB_LOSS, want_abs=False):
+                    amb_alpha=AMB_ALPHA, amb_T=AMB_T, amb_cap=AMB_CAP, amb_loss=AMB_LOSS, want_abs=False,
+                    alternative=False):
     """d loss / d(u, v, A, B, C, opacity, rgb) per visible primitive, plus flags
-    (FLAG_AMB_PIXEL | FLAG_NEAR_CAP bits per primitive)."""
+    (FLAG_AMB_PIXEL | FLAG_NEAR_CAP bits per primitive).  alternative=True takes
+    the other outcome of every failed decision within the (amb_alpha, amb_T)
+    bands: such a pair is included and such a termination test does not stop
+    the pixel (what a computation in another precision may do instead)."""
     W, H = cam.width, cam.height
     n = proj.radius.size
     vis = np.ascontiguousarray(vis, np.uint32)
@@ -259,7 +263,8 @@ def render_backward(vis, proj: Projection, cam, dL_dimg, bg=(0.0, 0.0, 0.0), los
     lib().orc_render_backward(vis.size, _p(vis), _p(proj.rect), _p(proj.depth), _p(proj.mean2d), _p(proj.conic),
                               _p(proj.opacity), _p(proj.rgb), W, H, _p(bg), _p(g), n, _p(grad2d), _p(flag),
                               float(amb_alpha), float(amb_T), float(amb_cap),
-                              None if lm is None else _p(lm), float(amb_loss), None if gabs is None else _p(gabs))
+                              None if lm is None else _p(lm), float(amb_loss), None if gabs is None else _p(gabs),
+                              int(bool(alternative)))
     if want_abs:
         return grad2d, flag, gabs
     return grad2d, flag

@@ -564,8 +564,13 @@ typedef struct {
     uint32_t capped_sig;  /* sum of (list position + 1) over the included pairs at the 0.99 cap */
 } orc_pixres;
 
-/* Front-to-back pass of pixel (px, py) over candidates L[0..nl). */
-static orc_pixres composite_pixel(const orc_scene2d* s, const orc_cand* L, int nl, int px, int py, orc_hit* hits)
+/* Front-to-back pass of pixel (px, py) over candidates L[0..nl).  With alt
+ * set, every decision within its band (an alpha test within band_alpha of
+ * 1/255, a termination test within band_T of 1e-4) that fails is taken the
+ * other way: such a pair is included, and such a test does not stop the pass.
+ * That is the outcome a computation in another precision may reach instead. */
+static orc_pixres composite_pixel(const orc_scene2d* s, const orc_cand* L, int nl, int px, int py, orc_hit* hits,
+                                  int alt, double band_alpha, double band_T)
 {
     orc_pixres r;
     memset(&r, 0, sizeof r);
@@ -589,11 +594,11 @@ static orc_pixres composite_pixel(const orc_scene2d* s, const orc_cand* L, int n
         double mc = fabs(gval - amax) / amax;
         if (mc < r.margin_cap) r.margin_cap = mc;
         double alpha = gval < amax ? gval : amax;
-        if (alpha < ORC_ALPHA_MIN) continue;
+        if (alpha < ORC_ALPHA_MIN && !(alt && ma < band_alpha)) continue;
         double Tn = T * (1.0 - alpha);
         double mt = fabs(Tn - ORC_T_MIN) / ORC_T_MIN;
         if (mt < r.margin_T) r.margin_T = mt;
-        if (Tn < ORC_T_MIN) { ++k; break; }
+        if (Tn < ORC_T_MIN && !(alt && mt < band_T)) { ++k; break; }
         if (hits) {
             orc_hit* h = &hits[r.nhit];
             h->pos = k; h->alpha = alpha; h->T = T; h->g = gval; h->e = e; h->dx = dx; h->dy = dy;
@@ -642,7 +647,7 @@ void orc_render(int64_t nvis, const uint32_t* vis, const int32_t* rect, const fl
             int nl = tile_candidates(&s, tx, ty, L);
             for (int py = ty * ORC_TILE; py < (ty + 1) * ORC_TILE && py < H; ++py)
                 for (int px = tx * ORC_TILE; px < (tx + 1) * ORC_TILE && px < W; ++px) {
-                    orc_pixres r = composite_pixel(&s, L, nl, px, py, active ? hits : NULL);
+                    orc_pixres r = composite_pixel(&s, L, nl, px, py, active ? hits : NULL, 0, 0.0, 0.0);
                     size_t p = (size_t)py * W + px;
                     for (int ch = 0; ch < 3; ++ch) img[(size_t)ch * W * H + p] = r.C[ch];
                     if (T_final) T_final[p] = r.T;
@@ -676,17 +681,20 @@ void orc_render(int64_t nvis, const uint32_t* vis, const int32_t* rect, const fl
  * pixels in a fixed tile order (deterministic).  Rows of invisible primitives
  * are zeroed.  flag[j] (if not NULL) gets bit 0 when j was examined by a
  * pixel whose margins fall below (amb_alpha, amb_T), or whose loss sign is
- * close (|loss_margin| < amb_loss, if loss_margin != NULL), and bit 1 when one
+ * close (|loss_margin| < amb_loss, if loss_margin != NULL), bit 1 when one
  * of its included pairs sits within amb_cap of the 0.99 cap (where the
  * derivative w.r.t. opacity and sigma jumps).  grad2d_abs (if not NULL)
  * receives the per-component sums of |per-pixel term| (the magnitude an
- * fp32 summation's rounding error is proportional to).
+ * fp32 summation's rounding error is proportional to).  With alt set, every
+ * pixel takes the other outcome of each decision within the (amb_alpha, amb_T)
+ * bands that failed (see composite_pixel), so the terms, their magnitudes and
+ * the flags are those of that alternative pass.
  */
 void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect, const float* depth,
                          const double* mean2d, const double* conic, const double* opacity, const double* rgb,
                          int W, int H, const double* bg, const double* dL_dimg, int n,
                          double* grad2d, uint8_t* flag, double amb_alpha, double amb_T, double amb_cap,
-                         const double* loss_margin, double amb_loss, double* grad2d_abs)
+                         const double* loss_margin, double amb_loss, double* grad2d_abs, int alt)
 {
     orc_scene2d s = {nvis, vis, rect, depth, mean2d, conic, opacity, rgb, W, H,
                      (W + ORC_TILE - 1) / ORC_TILE, (H + ORC_TILE - 1) / ORC_TILE, {bg[0], bg[1], bg[2]}};
@@ -724,7 +732,7 @@ void orc_render_backward(int64_t nvis, const uint32_t* vis, const int32_t* rect,
             for (int k = 0; k < nl; ++k) accj[toff[t] + k] = L[k].j;
             for (int py = ty * ORC_TILE; py < (ty + 1) * ORC_TILE && py < H; ++py)
                 for (int px = tx * ORC_TILE; px < (tx + 1) * ORC_TILE && px < W; ++px) {
-                    orc_pixres r = composite_pixel(&s, L, nl, px, py, hits);
+                    orc_pixres r = composite_pixel(&s, L, nl, px, py, hits, alt, amb_alpha, amb_T);
                     size_t p = (size_t)py * W + px;
                     double gC[3] = {dL_dimg[p], dL_dimg[HW + p], dL_dimg[2 * HW + p]};
                     int amb = (r.margin_alpha < amb_alpha) || (r.margin_T < amb_T);

@@ -242,6 +242,64 @@ def test_capped_pair_backward_is_zero(orc):
     check_capped_backward(orc)
 
 
+def _stack_at_pixel(orc, opacities):
+    """Gaussians stacked on the centre of pixel (8, 8) of a 16 x 16 image (one
+    tile), front to back in the given order, each seen there with sigma = 0,
+    so that its alpha at that pixel is its opacity exactly."""
+    n = len(opacities)
+    pr = orc.Projection(radius=np.full(n, 8, np.int32), tiles=np.ones(n, np.uint32),
+                        rect=np.tile(np.array([0, 0, 1, 1], np.int32), (n, 1)),
+                        depth=np.arange(1, n + 1, dtype=np.float32),
+                        mean2d=np.tile([8.5, 8.5], (n, 1)), conic=np.tile([4.0, 0.0, 4.0], (n, 1)),
+                        mean2d_f32=np.tile(np.float32([8.5, 8.5]), (n, 1)),
+                        conic_f32=np.tile(np.float32([4.0, 0.0, 4.0]), (n, 1)),
+                        opacity=np.asarray(opacities, np.float64), rgb=np.full((n, 3), 0.5),
+                        clamp=np.zeros(n, np.uint8), clamp_margin=np.full(n, np.inf),
+                        jclamp_margin=np.full(n, np.inf))
+    cam = dataclasses.make_dataclass("Cam", ["width", "height"])(16, 16)
+    w = np.zeros((3, 16, 16))
+    w[0, 8, 8] = 1.0
+    return pr, cam, w, np.arange(n, dtype=np.uint32)
+
+
+def test_alternative_outcome_of_banded_decisions(orc):
+    """The backward's alternative pass takes the other outcome of each failed
+    decision within its band and no other.  d L / d r of a pair at the one
+    pixel with dL/dR = 1 is alpha T when it is included and 0 when not."""
+    a_min = 1.0 / 255.0
+    # an alpha test failing within the band: left out, included by the alternative
+    for rel, inside in ((0.5 * orc.AMB_ALPHA, True), (2.0 * orc.AMB_ALPHA, False)):
+        o = a_min * (1.0 - rel)
+        pr, cam, w, vis = _stack_at_pixel(orc, [o])
+        g0, _ = orc.render_backward(vis, pr, cam, w)
+        g1, _ = orc.render_backward(vis, pr, cam, w, alternative=True)
+        assert g0[0, 6] == 0.0
+        assert g1[0, 6] == (o if inside else 0.0)
+    # a termination test within the band: the fourth pair's T (1e-3 behind
+    # three pairs of alpha 0.9) would fall just under 1e-4, so the pixel stops
+    # there; the alternative includes it and stops at the fifth, whose test
+    # lies far outside the band.  The pairs in front gain the fourth's colour
+    # in their suffix: d L / d o_k there is T_k (c - S_k / (1 - alpha_k)).
+    T3 = 1.0
+    for _ in range(3):
+        T3 *= 1.0 - 0.9
+    for rel, inside in ((0.5 * orc.AMB_T, True), (2.0 * orc.AMB_T, False)):
+        a4 = 1.0 - 1e-4 * (1.0 - rel) / T3
+        pr, cam, w, vis = _stack_at_pixel(orc, [0.9, 0.9, 0.9, a4, 0.5])
+        g0, _ = orc.render_backward(vis, pr, cam, w)
+        g1, _ = orc.render_backward(vis, pr, cam, w, alternative=True)
+        assert g0[3, 6] == 0.0 and g0[4, 6] == 0.0
+        assert g1[4, 6] == 0.0
+        if not inside:
+            np.testing.assert_array_equal(g1, g0)
+            continue
+        assert math.isclose(g1[3, 6], a4 * T3, rel_tol=1e-12)
+        # the suffix behind the third pair gains the fourth's 0.5 a4 T3 in the
+        # alternative, so its d L / d o differs by -0.5 a4 T3 / (1 - 0.9)
+        diff = g1[2, 5] - g0[2, 5]
+        assert math.isclose(diff, -0.5 * a4 * T3 / (1.0 - 0.9), rel_tol=1e-9), diff
+
+
 def test_two_layer_composite(orc):
     cam = axis_camera(64, 64, 60.0)
     sc = make_scene([[0.0, 0.0, 3.0], [0.0, 0.0, 5.0]], [[0.04] * 3, [0.12] * 3], [1, 0, 0, 0],
