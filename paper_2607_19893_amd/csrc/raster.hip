@@ -132,7 +132,9 @@ __device__ __forceinline__ float exp_neg(float sigma) {
 // that row's pixel centres (and lie below the row's limit).  The four rows of
 // a wave then walk their lists in lockstep, so an entry costs a quarter of a
 // wave step for every pixel row it reaches instead of a whole step for every
-// 16x4 strip.  cnt[r] receives the length of row r's list.
+// 16x4 strip.  cnt[r] receives the length of row r's list.  With REV (one
+// ballot round, NB = 64) each list is stored back to front, so that a walk
+// from the last entry to the first reads positions 0, 1, 2, ...
 //
 // An entry reaches row y if sigma <= s somewhere on the row's segment of
 // pixel centres [x0, x1] (s = cut = ln(255 o) + kCutMargin as for hx, hy):
@@ -144,9 +146,10 @@ __device__ __forceinline__ float exp_neg(float sigma) {
 // axis ratio of the footprint: inside the 1e-3 margin up to ratios near 5e4,
 // where the fp32 conic itself has lost its accuracy.  Any pixel of a skipped
 // row stays below the 1/255 threshold.
-template <int NB>
+template <int NB, bool REV = false>
 __device__ __forceinline__ void compact_rows(const SplatLds<NB>& L, int nb, float x0, float x1, float y0,
                                              const uint32_t* lim, uint8_t (*list)[NB], uint32_t* cnt) {
+    static_assert(!REV || NB == GS_WAVE, "a list is reversed within its one ballot round");
     const int lane = lane_id();
     const uint64_t lt = lanemask_lt();
 #pragma unroll
@@ -175,7 +178,7 @@ __device__ __forceinline__ void compact_rows(const SplatLds<NB>& L, int nb, floa
             const double smin = dx * fma(qd.x, dx, qd.y * dy) + R.c2 * dy * dy;
             const bool t = bx && (uint32_t)k < lim[q] && (v + hy >= y) && (v - hy <= y) && (smin <= cut || !convex);
             const uint64_t m = __ballot(t);
-            if (t) list[q][cnt[q] + popc64(m & lt)] = (uint8_t)k;
+            if (t) list[q][REV ? popc64(m) - 1u - popc64(m & lt) : cnt[q] + popc64(m & lt)] = (uint8_t)k;
             cnt[q] += popc64(m);
         }
     }
@@ -512,6 +515,15 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
     const float gC2 = inside ? dL_dimg[2 * HW + pix] : 0.0f;
     float gS = T * (gC0 * bg0 + gC1 * bg1 + gC2 * bg2);
     if (tid == 0) s_max = 0;
+    {
+        // a walk reads list bytes past its row's count too (without a branch): every
+        // byte must name an entry of the batch arrays, and every entry must hold
+        // finite values, also before a batch has written them
+        static_assert(sizeof(s_list) == 4 * GS_BLOCK, "one word of the lists per thread");
+        reinterpret_cast<uint32_t*>(&s_list[0][0][0])[tid] = 0u;
+        float4* zs = reinterpret_cast<float4*>(&L);
+        for (int i = tid; i < (int)(sizeof(L) / 16); i += GS_BLOCK) zs[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    }
     __syncthreads();
     if (last > 0) atomicMax(&s_max, last);
     __syncthreads();
@@ -553,7 +565,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             lim[q] = row_last[q] > bs ? row_last[q] - bs : 0u;
             any = any || lim[q] > 0u;
         }
-        if (work && any) compact_rows(L, (int)cnt, wx0, wx1, wy0, lim, s_list[w], nl);
+        if (work && any) compact_rows<kBwdBatch, true>(L, (int)cnt, wx0, wx1, wy0, lim, s_list[w], nl);
         const uint32_t my_n = for_row(nl, row);
         // the counts come from ballots, so every lane holds the same values
         uint32_t nls[4];
@@ -566,15 +578,17 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
             uint64_t act_mask = 0ull;
 #pragma unroll
             for (int q = 0; q < 4; ++q) act_mask |= jj < nls[q] ? 0xFFFFull << (16 * q) : 0ull;
-            const int k = act ? s_list[w][row][my_n - 1u - jj] : 0;
+            // the lists are stored back to front; past the row's count the byte is stale
+            // (or cleared) but names an entry whose values are finite, and the lane is
+            // not ok
+            const int k = s_list[w][row][jj];
             const SplatR R = L.R[k];
-            const double2 Q = L.Q[k];
             double ddx, ddy, inner, cdy;
-            const float sigma = splat_sigma(L.P[k], Q, R.c2, fx, fy, ddx, ddy, inner, cdy);
+            const float sigma = splat_sigma(L.P[k], L.Q[k], R.c2, fx, fy, ddx, ddy, inner, cdy);
             const float e = exp_neg(sigma);
             const float gv = R.o * e;
             const float alpha = fminf(kAlphaMax, gv);
-            const bool ok = act && (uint32_t)k < last_b && !(sigma < 0.0f) && !(alpha < kAlphaMin);
+            const bool ok = act & ((uint32_t)k < last_b) & !(sigma < 0.0f) & !(alpha < kAlphaMin);
             // the lanes of ok, as ballots of the comparisons themselves (a ballot of a
             // compare is its lane mask; a ballot of a combined flag costs two VALU ops)
             const uint64_t mask = act_mask & __builtin_amdgcn_ballot_w64((uint32_t)k < last_b) &
@@ -582,15 +596,18 @@ __global__ void __launch_bounds__(GS_BLOCK) k_raster_bwd(
                                   __builtin_amdgcn_ballot_w64(!(alpha < kAlphaMin));
             if (mask == 0ull) continue;
             const float4 col = L.S[k];
-            const float inv_om = __builtin_amdgcn_rcpf(1.0f - alpha);
-            const float Tk = ok ? T * inv_om : T;
+            // a lane that is not ok takes alpha = 0: 1 / (1 - 0) = 1 leaves its T as it
+            // is, and its weight and d sigma are 0
+            const float a_ok = ok ? alpha : 0.0f;
+            const float inv_om = __builtin_amdgcn_rcpf(1.0f - a_ok);
+            const float Tk = T * inv_om;
             const float gcol = gC0 * col.x + gC1 * col.y + gC2 * col.z;
             const float dalpha = Tk * gcol - gS * inv_om;
-            const float wgt = ok ? alpha * Tk : 0.0f;
+            const float wgt = a_ok * Tk;
             gS = fmaf(wgt, gcol, gS);
             T = Tk;
-            const bool geo = ok && gv < kAlphaMax;      // the 0.99 cap stops d/d(opacity, sigma)
-            const float ds = geo ? -dalpha * alpha : 0.0f;
+            const float a_geo = gv < kAlphaMax ? a_ok : 0.0f;   // the 0.99 cap stops d/d(opacity, sigma)
+            const float ds = -dalpha * a_geo;
             const float dsx = ds * (float)ddx;
             // the six sums over each 16-lane row (all its lanes hold the same entry)
             // in 18 DPP adds instead of 24: the first stage pairs lane i with lane
