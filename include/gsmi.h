@@ -186,7 +186,8 @@ gs_status gs_project(const gs_scene* scene, const gs_camera* cam, const gs_proj*
  *     or GS_PRED_BITMAP (src is a scope bitmap, see gs_scope_from_ids)
  *   out_idx [n] uint32 (the first *out_count entries are written)
  *   out_count: one uint32 on the device
- *   ws: gs_workspace_bytes(GS_WS_VISIBLE_SET, n, 0, 0, 0) bytes
+ *   ws: gs_workspace_bytes(GS_WS_VISIBLE_SET, n, 0, 0, 0) bytes, 256-byte
+ *     aligned (else GS_ERR_INVALID_ARG)
  */
 enum { GS_PRED_U32_NONZERO = 0, GS_PRED_U8_NONZERO = 1, GS_PRED_BITMAP = 2 };
 gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count,
@@ -238,7 +239,8 @@ gs_status gs_visible_set_noalloc(int32_t kind, const void* src, int32_t n, uint3
  *                             (pair_offset[id] + tile number in id's rectangle)
  *   keys   [capacity] uint64 or NULL: (tile << 32) | bits(depth) per sorted pair
  *   num_pairs: one uint32 on the device (the pair count, also on overflow)
- *   ws: gs_workspace_bytes(GS_WS_BIN_SORT, n, capacity, width, height) bytes
+ *   ws: gs_workspace_bytes(GS_WS_BIN_SORT, n, capacity, width, height) bytes,
+ *     256-byte aligned (else GS_ERR_INVALID_ARG)
  */
 gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, const uint32_t* vis_count,
                       int32_t width, int32_t height, uint32_t capacity, uint32_t* vals, uint32_t* ranges,

@@ -163,6 +163,7 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
     GS_REQUIRE(out_count != nullptr, "gs_visible_set: null out_count");
     if (n > 0) {
         GS_REQUIRE(src && out_idx && ws, "gs_visible_set: null pointer");
+        GS_REQUIRE(aligned(ws, 256), "gs_visible_set: workspace must be 256-byte aligned");
         GS_REQUIRE(aligned(src, kind == GS_PRED_U32_NONZERO ? 16 : (kind == GS_PRED_BITMAP ? 4 : 8)),
                    "gs_visible_set: src misaligned");
     }
@@ -207,6 +208,7 @@ gs_status gs_bin_sort(const gs_proj* proj, int32_t n, const uint32_t* vis_idx, c
     GS_REQUIRE(vis_idx && vis_count && ranges && pair_offset && num_pairs && status && ws,
                "gs_bin_sort: null pointer");
     GS_REQUIRE(capacity == 0 || (vals && pair_emit), "gs_bin_sort: null vals / pair_emit");
+    GS_REQUIRE(aligned(ws, 256), "gs_bin_sort: workspace must be 256-byte aligned");
     if (ws_bytes < gsmi::binsort_ws_bytes(n, capacity, width, height))
         return fail(GS_ERR_WORKSPACE, "gs_bin_sort: workspace too small");
     return hip_status(gsmi::launch_binsort(*proj, n, vis_idx, vis_count, width, height, capacity, vals, ranges,

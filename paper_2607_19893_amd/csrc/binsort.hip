@@ -73,7 +73,9 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restri
 }
 
 // Exclusive offsets in visible-set order: pair_offset[id] and offs_r[rank],
-// with offs_r[V] = M as a sentinel.  Also publishes the pair count and the
+// with offs_r[V] = M as a sentinel.  Each block adds up the per-block sums of
+// k_tile_sums itself, those before it for its offset and all of them for M
+// (no separate scan pass).  Also publishes the pair count and the
 // overflow flag, and for every 2048-pair emission block m the rank that holds
 // its first pair (bstart[m], m < nbs): the rank whose pairs [off, off + t)
 // contain m * 2048 writes it, so each entry has one writer.  On overflow
@@ -81,13 +83,16 @@ __global__ void __launch_bounds__(GS_BLOCK) k_tile_sums(const uint32_t* __restri
 // per-primitive backward finds none of its slots in the buffer.
 __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
     const uint32_t* __restrict__ order, const uint32_t* __restrict__ vis_count, const uint32_t* __restrict__ tiles,
-    const uint32_t* __restrict__ bsum, const uint32_t* __restrict__ total, uint32_t capacity,
+    const uint32_t* __restrict__ bsum, uint32_t capacity,
     uint32_t* __restrict__ pair_offset, uint32_t* __restrict__ offs_r, uint32_t* __restrict__ sort_count,
     uint32_t* __restrict__ num_pairs, gs_device_status* __restrict__ status, uint32_t* __restrict__ bstart,
     uint32_t nbs) {
     __shared__ uint32_t scratch[4];
     const uint32_t V = *vis_count;
-    const uint32_t M = *total;
+    const uint32_t nbv = (V + GS_TILE_ITEMS - 1) / GS_TILE_ITEMS;     // blocks that hold visible ranks
+    if (blockIdx.x > 0 && blockIdx.x >= nbv) return;
+    uint32_t before;
+    const uint32_t M = block_sum_prefix2(bsum, min(blockIdx.x, nbv), nbv, scratch, &before);
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         *num_pairs = M;
         *sort_count = M <= capacity ? M : 0u;
@@ -108,7 +113,7 @@ __global__ void __launch_bounds__(GS_BLOCK) k_offsets(
         s += t[k];
     }
     uint32_t tot;
-    uint32_t off = block_excl_scan(s, scratch, &tot) + bsum[blockIdx.x];
+    uint32_t off = block_excl_scan(s, scratch, &tot) + before;
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) {
         if (base + k >= V) break;
@@ -1081,7 +1086,7 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     const int32_t TX = (width + GS_TILE - 1) / GS_TILE;
     const uint32_t T = tile_count(width, height);
     uint32_t* bsum = at<uint32_t>(ws, L.bsum);
-    uint32_t* ctr = at<uint32_t>(ws, L.counters);   // [0] M, [1] sort count, [2] long tiles
+    uint32_t* ctr = at<uint32_t>(ws, L.counters);   // [1] sort count, [2] long tiles
     uint32_t* tcount = at<uint32_t>(ws, L.tcount);
     uint32_t* cursor = at<uint32_t>(ws, L.cursor);
     uint32_t* order = tile_order ? tile_order : at<uint32_t>(ws, L.order);
@@ -1107,12 +1112,11 @@ hipError_t launch_binsort(const gs_proj& proj, int32_t n, const uint32_t* vis_id
     const uint32_t* vorder = vis_idx;
     const uint32_t nb = div_up(n, GS_TILE_ITEMS);
     hipLaunchKernelGGL(k_tile_sums, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum, tcount, T);
-    hipError_t e = launch_scan_blocks(bsum, nb, ctr + 0, nullptr, st);
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     uint32_t* offs_r = at<uint32_t>(ws, L.offs);
     const uint32_t nbs = div_up(capacity, GS_TILE_ITEMS) + 1u;
-    hipLaunchKernelGGL(k_offsets, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum, ctr + 0,
-                       capacity, pair_offset, offs_r, ctr + 1, num_pairs, status, at<uint32_t>(ws, L.bstart), nbs);
+    hipLaunchKernelGGL(k_offsets, dim3(nb), dim3(GS_BLOCK), 0, st, vorder, vis_count, proj.tiles, bsum, capacity, pair_offset, offs_r, ctr + 1, num_pairs, status, at<uint32_t>(ws, L.bstart), nbs);
     if (capacity == 0 || T == 0) return no_pairs();
     // 2. emission: one (tile, primitive) pair per touched tile, and the per-tile totals
     const uint32_t nbp = div_up(capacity, GS_TILE_ITEMS);

@@ -93,6 +93,52 @@ __device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* scratch)
     return t;
 }
 
+// Sum of c[0..m) by the whole workgroup, for a block's offset among the
+// per-block counts of a compaction (in place of a separate scan pass).  c is
+// 16-byte aligned; every thread keeps up to four 16-byte loads in flight.
+__device__ __forceinline__ uint32_t block_sum_prefix(const uint32_t* __restrict__ c, uint32_t m, uint32_t* scratch) {
+    const uint4* c4 = reinterpret_cast<const uint4*>(c);
+    const uint32_t m4 = m / 4;
+    uint32_t s = 0;
+    for (uint32_t i = threadIdx.x; i < m4; i += 4 * GS_BLOCK) {
+        uint4 v[4];
+#pragma unroll
+        for (uint32_t j = 0; j < 4; ++j) v[j] = i + j * GS_BLOCK < m4 ? c4[i + j * GS_BLOCK] : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s += (v[j].x + v[j].y) + (v[j].z + v[j].w);
+    }
+    if (threadIdx.x < m - 4 * m4) s += c[4 * m4 + threadIdx.x];
+    return block_sum_u32(s, scratch);
+}
+
+// The same over c[0..m_all), also returning in *before the sum of c[0..m_before)
+// (m_before <= m_all): a block's offset and the grand total in one pass.
+__device__ __forceinline__ uint32_t block_sum_prefix2(const uint32_t* __restrict__ c, uint32_t m_before,
+                                                      uint32_t m_all, uint32_t* scratch, uint32_t* before) {
+    const uint4* c4 = reinterpret_cast<const uint4*>(c);
+    const uint32_t m4 = m_all / 4;
+    uint32_t sa = 0, sb = 0;
+    for (uint32_t i = threadIdx.x; i < m4; i += 4 * GS_BLOCK) {
+        uint4 v[4];
+#pragma unroll
+        for (uint32_t j = 0; j < 4; ++j) v[j] = i + j * GS_BLOCK < m4 ? c4[i + j * GS_BLOCK] : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+        for (uint32_t j = 0; j < 4; ++j) {
+            const uint32_t e = 4 * (i + j * GS_BLOCK);
+            sa += (v[j].x + v[j].y) + (v[j].z + v[j].w);
+            sb += (e < m_before ? v[j].x : 0u) + (e + 1 < m_before ? v[j].y : 0u) +
+                  (e + 2 < m_before ? v[j].z : 0u) + (e + 3 < m_before ? v[j].w : 0u);
+        }
+    }
+    if (threadIdx.x < m_all - 4 * m4) {
+        const uint32_t e = 4 * m4 + threadIdx.x;
+        sa += c[e];
+        sb += e < m_before ? c[e] : 0u;
+    }
+    *before = block_sum_u32(sb, scratch);
+    return block_sum_u32(sa, scratch);
+}
+
 }  // namespace gsmi
 
 // ---------------------------------------------------------------------------

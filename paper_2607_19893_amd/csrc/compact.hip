@@ -1,9 +1,11 @@
 // Scope extraction: ordered (ascending) stream compaction of a per-primitive
 // predicate (a uint32 or uint8 array, or a scope bitmap), plus the small device-wide scan used by several passes.
 //
-// Three launches: per-block counts (blocked arrangement, 2048 items per
-// block), one single-workgroup exclusive scan of the block counts, and the
-// scatter that recomputes each item's rank within its block.
+// Two launches: per-block counts (blocked arrangement, 2048 items per block),
+// then the scatter, in which each block adds up the counts of the blocks
+// before it for its offset (a few 16-byte loads per thread: no separate scan
+// pass) and recomputes each item's rank within its block; the last block
+// writes the total.
 #include <mutex>
 
 #include "common.h"
@@ -69,9 +71,11 @@ __global__ void __launch_bounds__(GS_BLOCK) k_vis_count(const void* __restrict__
 
 template <int KIND>
 __global__ void __launch_bounds__(GS_BLOCK) k_vis_scatter(const void* __restrict__ src, int32_t n,
-                                                          const uint32_t* __restrict__ offsets,
-                                                          uint32_t* __restrict__ out_idx) {
+                                                          const uint32_t* __restrict__ counts,
+                                                          uint32_t* __restrict__ out_idx,
+                                                          uint32_t* __restrict__ out_count) {
     __shared__ uint32_t scratch[4];
+    const uint32_t before = block_sum_prefix(counts, blockIdx.x, scratch);
     const int32_t base = blockIdx.x * GS_TILE_ITEMS + threadIdx.x * GS_ITEMS;
     uint32_t on[GS_ITEMS];
     load_pred<KIND>(src, n, base, on);
@@ -79,36 +83,11 @@ __global__ void __launch_bounds__(GS_BLOCK) k_vis_scatter(const void* __restrict
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) c += on[k];
     uint32_t tot;
-    uint32_t pos = block_excl_scan(c, scratch, &tot) + offsets[blockIdx.x];
+    uint32_t pos = block_excl_scan(c, scratch, &tot) + before;
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k)
         if (on[k]) out_idx[pos++] = (uint32_t)(base + k);
-}
-
-// Exclusive scan of data[0..n) in place by one workgroup; total -> *total_out.
-__global__ void __launch_bounds__(GS_BLOCK) k_scan_single(uint32_t* __restrict__ data, uint32_t n,
-                                                          uint32_t* __restrict__ total_out) {
-    __shared__ uint32_t scratch[4];
-    uint32_t carry = 0;
-    for (uint32_t chunk = 0; chunk < n; chunk += GS_TILE_ITEMS) {
-        const uint32_t base = chunk + threadIdx.x * GS_ITEMS;
-        uint32_t v[GS_ITEMS];
-        uint32_t s = 0;
-#pragma unroll
-        for (int k = 0; k < GS_ITEMS; ++k) {
-            v[k] = (base + k < n) ? data[base + k] : 0u;
-            s += v[k];
-        }
-        uint32_t tot;
-        uint32_t run = block_excl_scan(s, scratch, &tot) + carry;
-#pragma unroll
-        for (int k = 0; k < GS_ITEMS; ++k) {
-            if (base + k < n) data[base + k] = run;
-            run += v[k];
-        }
-        carry += tot;
-    }
-    if (threadIdx.x == 0 && total_out) *total_out = carry;
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *out_count = before + tot;
 }
 
 __global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t value, size_t n) {
@@ -118,13 +97,6 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t value, size_t n) {
 }
 
 }  // namespace
-
-size_t scan_blocks_aux_words(uint32_t) { return 0; }
-
-hipError_t launch_scan_blocks(uint32_t* data, uint32_t n, uint32_t* total_out, uint32_t*, hipStream_t s) {
-    hipLaunchKernelGGL(k_scan_single, dim3(1), dim3(GS_BLOCK), 0, s, data, n, total_out);
-    return hipGetLastError();
-}
 
 hipError_t launch_fill_u32(uint32_t* p, uint32_t value, size_t n, hipStream_t st) {
     if (n == 0) return hipSuccess;
@@ -175,17 +147,15 @@ hipError_t launch_visible(int kind, const void* src, int32_t n, uint32_t* out_id
         hipLaunchKernelGGL(k_vis_count<GS_PRED_U8_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = launch_scan_blocks(counts, nb, out_count, nullptr, st);
-    if (e != hipSuccess) return e;
     if (kind == GS_PRED_U32_NONZERO)
         hipLaunchKernelGGL(k_vis_scatter<GS_PRED_U32_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,
-                           out_idx);
+                           out_idx, out_count);
     else if (kind == GS_PRED_BITMAP)
         hipLaunchKernelGGL(k_vis_scatter<GS_PRED_BITMAP>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,
-                           out_idx);
+                           out_idx, out_count);
     else
         hipLaunchKernelGGL(k_vis_scatter<GS_PRED_U8_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,
-                           out_idx);
+                           out_idx, out_count);
     return hipGetLastError();
 }
 

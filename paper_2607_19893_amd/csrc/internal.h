@@ -49,8 +49,6 @@ hipError_t launch_project(const gs_scene& s, const CamArgs& cam, const gs_proj& 
 size_t visible_ws_bytes(int32_t n);
 hipError_t launch_visible(int kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count, void* ws,
                           hipStream_t st);
-hipError_t launch_scan_blocks(uint32_t* data, uint32_t n, uint32_t* total_out, uint32_t* aux, hipStream_t s);
-size_t scan_blocks_aux_words(uint32_t n);
 hipError_t launch_fill_u32(uint32_t* p, uint32_t value, size_t n, hipStream_t st);
 // Device address of the fixed visible-set workspace on the current device
 // (GS_NOALLOC_SCRATCH_BYTES, 256-byte aligned); nullptr with *err set if the

@@ -60,7 +60,13 @@ def test_null_and_range_arguments_rejected(gs):
     cam.width = 40000
     assert L.gs_project(ctypes.byref(sc), ctypes.byref(cam), ctypes.byref(pr), None) == gs.GS_ERR_UNSUPPORTED
     assert L.gs_visible_set(7, None, 0, None, None, None, 0, None) == gs.GS_ERR_INVALID_ARG
-    assert L.gs_visible_set(0, 16, 100, 16, 16, 16, 0, None) == gs.GS_ERR_WORKSPACE
+    assert L.gs_visible_set(0, 16, 100, 16, 16, 256, 0, None) == gs.GS_ERR_WORKSPACE
+    # workspaces are 256-byte aligned (the per-block counts are read 16 bytes at a time)
+    assert L.gs_visible_set(0, 16, 100, 16, 16, 16, 1 << 20, None) == gs.GS_ERR_INVALID_ARG
+    assert "aligned" in gs.gs_last_error()
+    assert L.gs_bin_sort(ctypes.byref(pr), 10, 16, 16, 64, 64, 0, None, 16, None, 16, None, None, 16, 16, 16, 1 << 20,
+                         None) == gs.GS_ERR_INVALID_ARG
+    assert "aligned" in gs.gs_last_error()
     # the no-allocation variant: sizes beyond its fixed workspace are refused before any HIP call
     assert L.gs_visible_set_noalloc(0, 16, gs.GS_NOALLOC_MAX_N + 1, 16, 16, None) == gs.GS_ERR_UNSUPPORTED
     assert "GS_NOALLOC_MAX_N" in gs.gs_last_error()
