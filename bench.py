@@ -70,9 +70,9 @@ TRAFFIC = {
     "workload": "room-1M-L3-1080p",
     "id_order": "spatial",
     "sources": ["paper_2607_19893_amd/csrc/raster.hip", "paper_2607_19893_amd/csrc/binsort.hip"],
-    "code_sha256": "d23421874611e8df05687391d502a73959b92296deaa95d664e54f58f86aeb98",
-    "fetch_kib": 109224.20, "fetch_scale": 1048576.0 / 524294.5,
-    "write_kib": 91878.41, "write_scale": 1048576.0 / 1048576.0,
+    "code_sha256": "60c6eb1a4bc46d587fb4164bc2cc0fa91dee0deab096d3be3fda849634a6a28d",
+    "fetch_kib": 109111.74, "fetch_scale": 1048576.0 / 524294.5,
+    "write_kib": 91881.94, "write_scale": 1048576.0 / 1048576.0,
     "profile": "profiles/k_raster_bwd-room-1M-1080p_hbm_traffic.md",
 }
 
