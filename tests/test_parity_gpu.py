@@ -669,6 +669,46 @@ def test_zero_tile_ids_in_the_visible_list(torch_gpu, orc):
     np.testing.assert_array_equal(u32(tr.pair_offset)[vis], off)
 
 
+def test_offsets_over_many_rank_blocks(torch_gpu, orc):
+    """gs_bin_sort over a list of 9M ids of which one in a thousand has tiles:
+    the offsets pass then adds up more than 4096 per-block tile sums (two
+    rounds of 16-byte loads per thread) for every block's offset and for the
+    pair total, and must give the same pairs, order, ranges and emission map
+    as over the visible set alone."""
+    from paper_2607_19893_amd import scenes
+    torch = torch_gpu
+    n = 9_000_000
+    assert (n + 2047) // 2048 > 4096
+    w = scenes.tiny(n=n)
+    w.scene.mean[np.arange(n) % 1000 != 0, 2] = -10.0      # behind the camera
+    tr = trainer_for(w, torch, capacity=1 << 16)
+    cam = w.cameras[0]
+    T = cam.num_tiles
+    tr.status.zero_()
+    tr.project(cam); tr.visible(); tr.bin_sort()
+    torch.cuda.synchronize()
+    V = int(u32(tr.counts[0:1])[0])
+    M = int(u32(tr.counts[1:2])[0])
+    assert 8000 < V <= 9000 and 2048 < M <= 1 << 16
+    ref = [u32(t)[:k].copy() for t, k in ((tr.vals, M), (tr.pair_emit, M), (tr.ranges, 2 * T), (tr.tile_order, T))]
+    vis = u32(tr.vis_idx)[:V].copy()
+    off = u32(tr.pair_offset)[vis].copy()
+    tiles = u32(tr.tiles)[vis].astype(np.int64)
+    for t in (tr.vals, tr.pair_emit, tr.ranges, tr.tile_order, tr.pair_offset):
+        t.fill_(-1)
+    tr.vis_idx.copy_(torch.arange(n, dtype=torch.int32, device=tr.vis_idx.device))
+    tr.counts[0:1].fill_(n)
+    tr.bin_sort()
+    torch.cuda.synchronize()
+    assert u32(tr.status)[0] == 0 and int(u32(tr.counts[1:2])[0]) == M
+    got = [u32(t)[:k] for t, k in ((tr.vals, M), (tr.pair_emit, M), (tr.ranges, 2 * T), (tr.tile_order, T))]
+    for a, b in zip(ref, got):
+        np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(u32(tr.pair_offset)[vis], off)
+    # the offsets are the exclusive prefix of the visible ids' tile counts
+    np.testing.assert_array_equal(off, np.concatenate([[0], np.cumsum(tiles)[:-1]]).astype(np.uint32))
+
+
 def test_empty_and_degenerate(torch_gpu, orc):
     """All primitives behind the camera: empty visible set, empty image."""
     from paper_2607_19893_amd import scenes
