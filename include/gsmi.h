@@ -183,13 +183,17 @@ gs_status gs_project(const gs_scene* scene, const gs_camera* cam, const gs_proj*
  * set C_i of Section 2.1); with the active flags of gs_raster_fwd it is C_i
  * itself; any caller mask works the same way.
  *   kind: GS_PRED_U32_NONZERO (src is uint32[n]), GS_PRED_U8_NONZERO (uint8[n])
- *     or GS_PRED_BITMAP (src is a scope bitmap, see gs_scope_from_ids)
+ *     or GS_PRED_BITMAP (src is a scope bitmap, see gs_scope_from_ids);
+ *     GS_PRED_U8_NONZERO_CLEAR compacts uint8[n] flags as GS_PRED_U8_NONZERO
+ *     and also sets every flag it finds nonzero back to 0 (src is written):
+ *     flags that a forward marks afresh for each view then need no separate
+ *     clear before the next marking
  *   out_idx [n] uint32 (the first *out_count entries are written)
  *   out_count: one uint32 on the device
  *   ws: gs_workspace_bytes(GS_WS_VISIBLE_SET, n, 0, 0, 0) bytes, 256-byte
  *     aligned (else GS_ERR_INVALID_ARG)
  */
-enum { GS_PRED_U32_NONZERO = 0, GS_PRED_U8_NONZERO = 1, GS_PRED_BITMAP = 2 };
+enum { GS_PRED_U32_NONZERO = 0, GS_PRED_U8_NONZERO = 1, GS_PRED_BITMAP = 2, GS_PRED_U8_NONZERO_CLEAR = 3 };
 gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count,
                          void* ws, size_t ws_bytes, void* stream);
 

@@ -157,7 +157,8 @@ gs_status gs_project(const gs_scene* scene, const gs_camera* cam, const gs_proj*
 
 gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count, void* ws,
                          size_t ws_bytes, void* stream) {
-    GS_REQUIRE(kind == GS_PRED_U32_NONZERO || kind == GS_PRED_U8_NONZERO || kind == GS_PRED_BITMAP,
+    GS_REQUIRE(kind == GS_PRED_U32_NONZERO || kind == GS_PRED_U8_NONZERO || kind == GS_PRED_BITMAP ||
+                   kind == GS_PRED_U8_NONZERO_CLEAR,
                "gs_visible_set: bad kind %d", kind);
     GS_REQUIRE(n >= 0, "gs_visible_set: n < 0");
     GS_REQUIRE(out_count != nullptr, "gs_visible_set: null out_count");
@@ -174,7 +175,8 @@ gs_status gs_visible_set(int32_t kind, const void* src, int32_t n, uint32_t* out
 
 gs_status gs_visible_set_noalloc(int32_t kind, const void* src, int32_t n, uint32_t* out_idx, uint32_t* out_count,
                                  void* stream) {
-    GS_REQUIRE(kind == GS_PRED_U32_NONZERO || kind == GS_PRED_U8_NONZERO || kind == GS_PRED_BITMAP,
+    GS_REQUIRE(kind == GS_PRED_U32_NONZERO || kind == GS_PRED_U8_NONZERO || kind == GS_PRED_BITMAP ||
+                   kind == GS_PRED_U8_NONZERO_CLEAR,
                "gs_visible_set_noalloc: bad kind %d", kind);
     GS_REQUIRE(n >= 0, "gs_visible_set_noalloc: n < 0");
     if (n > GS_NOALLOC_MAX_N)

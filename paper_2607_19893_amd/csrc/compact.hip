@@ -82,6 +82,18 @@ __global__ void __launch_bounds__(GS_BLOCK) k_vis_scatter(const void* __restrict
     uint32_t c = 0;
 #pragma unroll
     for (int k = 0; k < GS_ITEMS; ++k) c += on[k];
+    if (KIND == GS_PRED_U8_NONZERO_CLEAR && c) {
+        // the flags this thread found set go back to 0 (it alone reads and writes
+        // them here; the count pass read them in an earlier launch)
+        uint8_t* s = static_cast<uint8_t*>(const_cast<void*>(src));
+        if (base + GS_ITEMS <= n) {
+            *reinterpret_cast<uint2*>(s + base) = make_uint2(0u, 0u);
+        } else {
+#pragma unroll
+            for (int k = 0; k < GS_ITEMS; ++k)
+                if (on[k]) s[base + k] = 0;
+        }
+    }
     uint32_t tot;
     uint32_t pos = block_excl_scan(c, scratch, &tot) + before;
 #pragma unroll
@@ -143,6 +155,8 @@ hipError_t launch_visible(int kind, const void* src, int32_t n, uint32_t* out_id
         hipLaunchKernelGGL(k_vis_count<GS_PRED_U32_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
     else if (kind == GS_PRED_BITMAP)
         hipLaunchKernelGGL(k_vis_count<GS_PRED_BITMAP>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
+    else if (kind == GS_PRED_U8_NONZERO_CLEAR)
+        hipLaunchKernelGGL(k_vis_count<GS_PRED_U8_NONZERO_CLEAR>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
     else
         hipLaunchKernelGGL(k_vis_count<GS_PRED_U8_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts);
     hipError_t e = hipGetLastError();
@@ -152,6 +166,9 @@ hipError_t launch_visible(int kind, const void* src, int32_t n, uint32_t* out_id
                            out_idx, out_count);
     else if (kind == GS_PRED_BITMAP)
         hipLaunchKernelGGL(k_vis_scatter<GS_PRED_BITMAP>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,
+                           out_idx, out_count);
+    else if (kind == GS_PRED_U8_NONZERO_CLEAR)
+        hipLaunchKernelGGL(k_vis_scatter<GS_PRED_U8_NONZERO_CLEAR>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,
                            out_idx, out_count);
     else
         hipLaunchKernelGGL(k_vis_scatter<GS_PRED_U8_NONZERO>, dim3(nb), dim3(GS_BLOCK), 0, st, src, n, counts,

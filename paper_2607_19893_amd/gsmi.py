@@ -24,7 +24,7 @@ i32, u32, i64, f32, sz = ctypes.c_int32, ctypes.c_uint32, ctypes.c_int64, ctypes
 
 GS_OK, GS_ERR_INVALID_ARG, GS_ERR_UNSUPPORTED, GS_ERR_WORKSPACE, GS_ERR_HIP = range(5)
 GS_WS_VISIBLE_SET, GS_WS_BIN_SORT, GS_WS_RASTER_BWD, GS_WS_LOSS, GS_WS_SCOPE, GS_WS_RASTER_FWD_L1 = 1, 2, 3, 4, 5, 6
-GS_PRED_U32_NONZERO, GS_PRED_U8_NONZERO, GS_PRED_BITMAP = 0, 1, 2
+GS_PRED_U32_NONZERO, GS_PRED_U8_NONZERO, GS_PRED_BITMAP, GS_PRED_U8_NONZERO_CLEAR = 0, 1, 2, 3
 (GS_GATE_NO_DELAY, GS_GATE_ADMIT, GS_GATE_WAIT_RHO, GS_GATE_WAIT_NO_ACTIVE, GS_GATE_WAIT_MISSING, GS_GATE_WAIT_SECOND,
  GS_GATE_WAIT_GRADIENT) = range(7)
 GS_APPLY_ADD, GS_APPLY_OVERWRITE = 0, 1

@@ -90,6 +90,9 @@ class ViewTrainer:
         self.rgb = torch.zeros(max(1, n), 3, device=self.dev)
         self.clamp = torch.zeros(max(1, n), dtype=torch.uint8, device=self.dev)
         self.active = torch.zeros(max(1, n), dtype=torch.uint8, device=self.dev)
+        # True while every active flag is 0: the step's compaction of the flags
+        # (active_set) clears them, so the next marking forward needs no fill
+        self._active_clean = True
         self.vis_idx = _u32(n, self.dev)
         self.act_idx = _u32(n, self.dev)
         self.counts = _u32(8, self.dev)          # [0] V, [1] M, [2] active count
@@ -193,7 +196,7 @@ class ViewTrainer:
     def raster_fwd(self, bg=(0.0, 0.0, 0.0), active=True, stats=False):
         img, fT, nc, _, _ = self._img_views()
         if active:
-            self.active.zero_()
+            self._mark_active()
         gsmi.gs_raster_fwd(self.proj_s, self.n, self.vals, self.ranges, self.cam.width, self.cam.height, bg, img, fT,
                            nc, self.active if active else None, self.pair_stats if stats else None,
                            tile_order=self._order())
@@ -203,7 +206,7 @@ class ViewTrainer:
         set_target buffer)."""
         img, fT, nc, dL, tgt = self._img_views()
         if active:
-            self.active.zero_()
+            self._mark_active()
         gsmi.gs_raster_fwd_l1(self.proj_s, self.n, self.vals, self.ranges, self.cam.width, self.cam.height, bg,
                               tgt if target is None else target, img, fT, nc, self.active if active else None,
                               self.loss, dL, self.ws_fwd_l1, tile_order=self._order())
@@ -243,8 +246,20 @@ class ViewTrainer:
                                    self.vis_idx, self.counts[0:1], self.capacity, self.grad_rows, self.ld,
                                    self.grad2d if grad2d else None, self.grad_norm, self.ws_bwd)
 
+    def _mark_active(self):
+        """Before a forward that marks active flags: zero them unless the last
+        compaction cleared them."""
+        if not self._active_clean:
+            self.active.zero_()
+        self._active_clean = False
+
     def active_set(self):
-        gsmi.gs_visible_set(gsmi.GS_PRED_U8_NONZERO, self.active, self.n, self.act_idx, self.counts[2:3], self.ws_vis)
+        """The realized active set C_i: ids of the flags the last forward set, in
+        ascending order (act_idx, count in counts[2]); the compaction also
+        clears the flags it reads."""
+        gsmi.gs_visible_set(gsmi.GS_PRED_U8_NONZERO_CLEAR, self.active, self.n, self.act_idx, self.counts[2:3],
+                            self.ws_vis)
+        self._active_clean = True
 
     def adam(self, step):
         """Sparse Adam over the visible rows; the steps go to delta_rows."""

@@ -60,6 +60,11 @@ def test_null_and_range_arguments_rejected(gs):
     cam.width = 40000
     assert L.gs_project(ctypes.byref(sc), ctypes.byref(cam), ctypes.byref(pr), None) == gs.GS_ERR_UNSUPPORTED
     assert L.gs_visible_set(7, None, 0, None, None, None, 0, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_visible_set(4, None, 0, None, None, None, 0, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_visible_set(gs.GS_PRED_U8_NONZERO_CLEAR, 12, 100, 16, 16, 256, 1 << 20,
+                            None) == gs.GS_ERR_INVALID_ARG                 # flags must be 8-byte aligned
+    assert "misaligned" in gs.gs_last_error()
+    assert L.gs_scope_from_pred(gs.GS_PRED_U8_NONZERO_CLEAR, 16, 100, 0, 16, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_visible_set(0, 16, 100, 16, 16, 256, 0, None) == gs.GS_ERR_WORKSPACE
     # workspaces are 256-byte aligned (the per-block counts are read 16 bytes at a time)
     assert L.gs_visible_set(0, 16, 100, 16, 16, 16, 1 << 20, None) == gs.GS_ERR_INVALID_ARG
@@ -70,7 +75,7 @@ def test_null_and_range_arguments_rejected(gs):
     # the no-allocation variant: sizes beyond its fixed workspace are refused before any HIP call
     assert L.gs_visible_set_noalloc(0, 16, gs.GS_NOALLOC_MAX_N + 1, 16, 16, None) == gs.GS_ERR_UNSUPPORTED
     assert "GS_NOALLOC_MAX_N" in gs.gs_last_error()
-    assert L.gs_visible_set_noalloc(3, 16, 100, 16, 16, None) == gs.GS_ERR_INVALID_ARG
+    assert L.gs_visible_set_noalloc(4, 16, 100, 16, 16, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_visible_set_noalloc(0, 16, -1, 16, 16, None) == gs.GS_ERR_INVALID_ARG
     assert L.gs_visible_set_noalloc(0, 16, 100, 16, None, None) == gs.GS_ERR_INVALID_ARG
     A = (16, 16, 10, 16, 64, 16, 16, 64)          # idx, count, max_rows, grad_rows, grad_ld, m, v, state_ld

@@ -709,6 +709,38 @@ def test_offsets_over_many_rank_blocks(torch_gpu, orc):
     np.testing.assert_array_equal(off, np.concatenate([[0], np.cumsum(tiles)[:-1]]).astype(np.uint32))
 
 
+def test_clearing_compaction(torch_gpu, orc):
+    """GS_PRED_U8_NONZERO_CLEAR gives the ascending ids of the nonzero flags (as
+    GS_PRED_U8_NONZERO does) and leaves every flag at 0, through gs_visible_set
+    and gs_visible_set_noalloc, on lengths with a ragged last block; a second
+    call then finds nothing."""
+    from paper_2607_19893_amd import gsmi as gs
+    torch = torch_gpu
+    rng = np.random.default_rng(7)
+    for n in (300_001, 5, 3 * 2048):
+        f = np.where(rng.random(n) < 0.3, rng.integers(1, 256, n), 0).astype(np.uint8)
+        want = np.flatnonzero(f).astype(np.uint32)
+        for noalloc in (False, True):
+            flags = torch.from_numpy(f.copy()).cuda()
+            out = torch.zeros(n, dtype=torch.int32, device="cuda")
+            cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+            ws = torch.zeros(gs.gs_workspace_bytes(gs.GS_WS_VISIBLE_SET, n, 0, 0, 0), dtype=torch.uint8,
+                             device="cuda")
+            for rep in range(2):
+                if noalloc:
+                    gs.gs_visible_set_noalloc(gs.GS_PRED_U8_NONZERO_CLEAR, flags, n, out, cnt)
+                else:
+                    gs.gs_visible_set(gs.GS_PRED_U8_NONZERO_CLEAR, flags, n, out, cnt, ws)
+                torch.cuda.synchronize()
+                c = int(u32(cnt)[0])
+                if rep == 0:
+                    assert c == want.size, (n, noalloc, c, want.size)
+                    np.testing.assert_array_equal(u32(out)[:c], want)
+                    assert int(flags.max()) == 0
+                else:
+                    assert c == 0
+
+
 def test_empty_and_degenerate(torch_gpu, orc):
     """All primitives behind the camera: empty visible set, empty image."""
     from paper_2607_19893_amd import scenes
@@ -805,7 +837,8 @@ def test_backward_halves_match_combined(torch_gpu, orc):
 def test_step_matches_phase_calls(torch_gpu, orc):
     """The training step's prepared-argument launches give the phase-by-phase
     calls' results bit for bit (parameters, moments, replica, versions, image,
-    gradients, realized active flags and ids), over two views of two cameras."""
+    gradients, realized active ids, and the flags, which both leave cleared),
+    over two views of two cameras."""
     w = get_case("room-60k-392x216")
     runs = []
     for fast in (True, False):
