@@ -72,9 +72,6 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
         tiles[i] = 0;
         return;
     }
-
-    // 3D covariance  Sigma = (Rq S)(Rq S)^T
-    const float4 q = *reinterpret_cast<const float4*>(quat + (size_t)i * ld.quat);
     float l0, l1, l2, logit;
     if (ld.head) {
         // the record's head: one 16-byte load for log_scale and the opacity logit
@@ -88,6 +85,35 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
     const float s0 = (float)exp((double)l0);
     const float s1 = (float)exp((double)l1);
     const float s2 = (float)exp((double)l2);
+    const float lx = 1.3f * c.tan_fovx, ly = 1.3f * c.tan_fovy;
+    const float u = c.fx * (p0 / p2) + c.cx;
+    const float v = c.fy * (p1 / p2) + c.cy;
+    const float fTX = (float)c.tiles_x, fTY = (float)c.tiles_y;
+    {
+        // Off-screen primitives leave before their rotation is read.  The 2D
+        // covariance's larger eigenvalue is at most |J|_F^2 smax^2 + 0.3 (J the
+        // clamped projection Jacobian, Sigma's spectral norm smax^2), and the
+        // radius rule below adds at most sqrt(0.1) to it, so 3 sqrt of that bound
+        // (with 0.1% and 2 pixels to spare for rounding) is at least the radius.
+        // The rectangle only grows with the radius: if it is empty at the bound,
+        // the full rule would find it empty too and write the same zeros.
+        const float smax = fmaxf(s0, fmaxf(s1, s2));
+        const float jx = c.fx / p2, jy = c.fy / p2;
+        const float jf2 = jx * jx * (1.0f + lx * lx) + jy * jy * (1.0f + ly * ly);
+        const float rb = 3.0f * sqrtf(jf2 * (smax * smax) + 0.62f) * 1.001f + 2.0f;
+        const int bx0 = (int)floorf(fminf(fmaxf((u - rb) / 16.0f, 0.0f), fTX));
+        const int bx1 = (int)floorf(fminf(fmaxf(((u + rb) + 15.0f) / 16.0f, 0.0f), fTX));
+        const int by0 = (int)floorf(fminf(fmaxf((v - rb) / 16.0f, 0.0f), fTY));
+        const int by1 = (int)floorf(fminf(fmaxf(((v + rb) + 15.0f) / 16.0f, 0.0f), fTY));
+        if ((bx1 - bx0) * (by1 - by0) <= 0) {
+            radius[i] = 0;
+            tiles[i] = 0;
+            return;
+        }
+    }
+
+    // 3D covariance  Sigma = (Rq S)(Rq S)^T
+    const float4 q = *reinterpret_cast<const float4*>(quat + (size_t)i * ld.quat);
     const float qn = sqrtf(((q.x * q.x + q.y * q.y) + q.z * q.z) + q.w * q.w);
     const float w = q.x / qn, x = q.y / qn, y = q.z / qn, z = q.w / qn;
     float Rq[3][3];
@@ -116,7 +142,6 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
         }
 
     // EWA: Sigma2D = (J Rcam) Sigma (J Rcam)^T + 0.3 I
-    const float lx = 1.3f * c.tan_fovx, ly = 1.3f * c.tan_fovy;
     const float rx = p0 / p2, ry = p1 / p2;
     const float xc = fminf(lx, fmaxf(-lx, rx)) * p2;
     const float yc = fminf(ly, fmaxf(-ly, ry)) * p2;
@@ -149,9 +174,6 @@ __global__ void __launch_bounds__(GS_BLOCK) k_project(
     const float mid = 0.5f * (a + cc);
     const float lam = mid + sqrtf(fmaxf(0.1f, mid * mid - det));
     const float rf = ceilf(3.0f * sqrtf(lam));
-    const float u = c.fx * (p0 / p2) + c.cx;
-    const float v = c.fy * (p1 / p2) + c.cy;
-    const float fTX = (float)c.tiles_x, fTY = (float)c.tiles_y;
     const int x0 = (int)floorf(fminf(fmaxf((u - rf) / 16.0f, 0.0f), fTX));
     const int x1 = (int)floorf(fminf(fmaxf(((u + rf) + 15.0f) / 16.0f, 0.0f), fTX));
     const int y0 = (int)floorf(fminf(fmaxf((v - rf) / 16.0f, 0.0f), fTY));
