@@ -709,6 +709,41 @@ def test_offsets_over_many_rank_blocks(torch_gpu, orc):
     np.testing.assert_array_equal(off, np.concatenate([[0], np.cumsum(tiles)[:-1]]).astype(np.uint32))
 
 
+def test_projection_near_the_image_border(torch_gpu, orc):
+    """Primitives centred up to 300 pixels past every border of the image,
+    with one long scale axis, random rotations and camera depths from 0.3 to
+    20: radius, tile counts and rectangles equal the oracle's bit for bit, so
+    the projection's early off-screen cull (a bound on the radius from the
+    largest scale) rejects exactly the primitives whose rectangle is empty."""
+    from paper_2607_19893_amd import scenes
+    rng = np.random.default_rng(41)
+    n = 200_000
+    w = scenes.tiny(n=n)
+    cam = w.cameras[0]
+    u = rng.uniform(-300.0, cam.width + 300.0, n)
+    v = rng.uniform(-300.0, cam.height + 300.0, n)
+    z = np.exp(rng.uniform(np.log(0.3), np.log(20.0), n))
+    pc = np.stack([(u - cam.cx) * z / cam.fx, (v - cam.cy) * z / cam.fy, z], 1)
+    R = np.asarray(cam.R, np.float64)
+    w.scene.mean[:] = ((pc - np.asarray(cam.t, np.float64)) @ R).astype(np.float32)   # R^T (p - t)
+    ls = rng.normal(-3.0, 1.0, (n, 3))
+    ls[:, 0] += rng.uniform(0.0, 3.0, n)
+    w.scene.log_scale[:] = ls.astype(np.float32)
+    tr = trainer_for(w, torch_gpu, capacity=1 << 20)
+    tr.project(cam)
+    torch_gpu.cuda.synchronize()
+    ref = orc.project(w.scene, cam, 0)
+    np.testing.assert_array_equal(tr.radius.cpu().numpy()[:n], ref.radius)
+    np.testing.assert_array_equal(u32(tr.tiles)[:n], ref.tiles)
+    vis = np.flatnonzero(ref.tiles)
+    rect = tr.rect.cpu().numpy().view(np.uint16)[:n]
+    np.testing.assert_array_equal(rect[vis].astype(np.int32), ref.rect[vis])
+    outside = (u < 0) | (u >= cam.width) | (v < 0) | (v >= cam.height)
+    reach = int((outside & (ref.tiles > 0)).sum())
+    _say("centres outside the image: %d, of which %d reach a tile" % (int(outside.sum()), reach))
+    assert reach > 1000 and int((outside & (ref.tiles == 0)).sum()) > 10000
+
+
 def test_clearing_compaction(torch_gpu, orc):
     """GS_PRED_U8_NONZERO_CLEAR gives the ascending ids of the nonzero flags (as
     GS_PRED_U8_NONZERO does) and leaves every flag at 0, through gs_visible_set
