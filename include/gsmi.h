@@ -185,9 +185,12 @@ gs_status gs_project(const gs_scene* scene, const gs_camera* cam, const gs_proj*
  *   kind: GS_PRED_U32_NONZERO (src is uint32[n]), GS_PRED_U8_NONZERO (uint8[n])
  *     or GS_PRED_BITMAP (src is a scope bitmap, see gs_scope_from_ids);
  *     GS_PRED_U8_NONZERO_CLEAR compacts uint8[n] flags as GS_PRED_U8_NONZERO
- *     and also sets every flag it finds nonzero back to 0 (src is written):
- *     flags that a forward marks afresh for each view then need no separate
- *     clear before the next marking
+ *     and also sets every flag it finds nonzero back to 0: flags that a
+ *     forward marks afresh for each view then need no separate clear before
+ *     the next marking.  src is then written, so it must be writable device
+ *     memory (it is declared const for the kinds that only read it).
+ *   src: 16-byte aligned for GS_PRED_U32_NONZERO, 8 for the uint8 kinds, 4
+ *     for the bitmap (else GS_ERR_INVALID_ARG)
  *   out_idx [n] uint32 (the first *out_count entries are written)
  *   out_count: one uint32 on the device
  *   ws: gs_workspace_bytes(GS_WS_VISIBLE_SET, n, 0, 0, 0) bytes, 256-byte
